@@ -1,0 +1,475 @@
+"""Model of the guarded specialization cache (test infrastructure only).
+
+What it models
+--------------
+* Ordered dispatch, Algorithm 1 of the paper (Sec. 3.2): versions are kept
+  in creation order; a call runs the first version whose guards hold; if
+  none holds the result is a distinguished MISS; an execution error of the
+  selected version is returned as an error and no other version is tried.
+* The three runtime paths of Sec. 3.5: a hit runs compiled code; a miss
+  returns to the caller, who installs a new version and calls again (the
+  paper recompiles here; this library selects among precompiled kernels);
+  an error never installs anything.
+* Guards are the ones a specialization of these ops depends on: dtype,
+  hidden / intermediate sizes, head_dim and head counts, a token-count
+  bucket, 16-byte alignment, contiguity, and the RoPE base (a captured
+  constant of the version, as source-visible constants are in Sec. 3.3).
+
+Guards are equality tests on a packed key, so two versions can never both
+match and "first match in creation order" is the unique match.
+
+This file is written from the policy contract (the table in the design
+notes) independently of the C++ library; the two must agree bit for bit on
+every selection record.
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+import struct
+from typing import Dict, List, Optional, Tuple
+
+# ---- enumerations (the ABI's numeric values) --------------------------------
+OP_RMSNORM, OP_RES_RMSNORM, OP_ROPE_QK, OP_SWIGLU, OP_CHAIN = 1, 2, 3, 4, 5
+DT_F32, DT_BF16 = 0, 1
+OK, MISS = 0, 1
+E_INVALID, E_UNSUPPORTED, E_FULL, E_NOMEM, E_LAUNCH, E_RUNTIME = -1, -2, -3, -4, -5, -6
+
+RN_SCALAR = 10
+RN_WAVE = {1: 11, 2: 12, 4: 13, 8: 14, 16: 15}
+RN_BLOCK = {8: 16, 16: 17}
+RN_LOOP = 18
+ROPE_SCALAR, ROPE_VEC_T1, ROPE_VEC_T4 = 20, 21, 22
+SW_SCALAR, SW_FLAT_U1, SW_FLAT_U4, SW_ROWS = 30, 31, 32, 33
+CH_FUSED, CH_SEQ = 50, 51
+
+BLOCK = 256
+GRID_CAP = 1 << 20
+T_MAX = 1 << 22
+H_LIMIT = 1 << 24          # H must be below this
+I_LIMIT = 1 << 31          # I must be below this
+HD_MAX = 512
+HEADS_MAX = 4096
+DEFAULT_CAPACITY = 256
+MAX_CAPACITY = 4096
+FLAG_AUTO_INSTALL = 1
+
+ALIGN, CONTIG = 1, 2       # per-op guard flag bits
+
+
+def elem_size(dtype: int) -> int:
+    return 4 if dtype == DT_F32 else 2
+
+
+def bucket(T: int) -> int:
+    """Smallest b >= 0 with 2^b >= T (T >= 1)."""
+    b = 0
+    while (1 << b) < T:
+        b += 1
+    return b
+
+
+def cdiv(a: int, b: int) -> int:
+    return -(-a // b)
+
+
+def next_pow2(n: int) -> int:
+    p = 1
+    while p < n:
+        p *= 2
+    return p
+
+
+def is_pow2(n: int) -> bool:
+    return n > 0 and (n & (n - 1)) == 0
+
+
+def f32_bits(x: float) -> int:
+    return struct.unpack("<I", struct.pack("<f", x))[0]
+
+
+def _finite(x: float) -> bool:
+    return math.isfinite(x)
+
+
+def _f32(x: float) -> float:
+    return struct.unpack("<f", struct.pack("<f", x))[0]
+
+
+def _aligned(es: int, ptrs, strides) -> bool:
+    return all(p % 16 == 0 for p in ptrs) and all((s * es) % 16 == 0 for s in strides)
+
+
+# ---- role policies -----------------------------------------------------------
+def rn_role(dtype: int, H: int, flags: int, T: int) -> Tuple[int, int]:
+    """(variant, grid) for RMSNorm / residual RMSNorm rows."""
+    v = 16 // elem_size(dtype)
+    if not (flags & ALIGN) or H % v:
+        return RN_SCALAR, T
+    nvec = H // v
+    nv = next_pow2(cdiv(nvec, 64))
+    if nv <= 16:
+        return RN_WAVE[nv], cdiv(T, 4)
+    nb = next_pow2(cdiv(nvec, 256))
+    if nb <= 16:
+        return RN_BLOCK[nb], T
+    return RN_LOOP, T
+
+
+def rope_role(dtype: int, hd: int, flags: int, b: int, T: int) -> Tuple[int, int]:
+    v = 16 // elem_size(dtype)
+    half = hd // 2
+    if not (flags & ALIGN) or half % v or not is_pow2(half // v):
+        return ROPE_SCALAR, T
+    if b <= 3:
+        return ROPE_VEC_T1, T
+    return ROPE_VEC_T4, cdiv(T, 4)
+
+
+def sw_role(dtype: int, I: int, flags: int, b: int, T: int) -> Tuple[int, int]:
+    v = 16 // elem_size(dtype)
+    if (flags & ALIGN) and (flags & CONTIG):
+        u = 1 if b <= 6 else 4
+        nvec = (T * I) // v
+        grid = max(1, min(cdiv(nvec, BLOCK * u), GRID_CAP))
+        return (SW_FLAT_U1 if u == 1 else SW_FLAT_U4), grid
+    if (flags & ALIGN) and I % v == 0:
+        cb = cdiv(I // v, BLOCK)
+        return SW_ROWS, min(T * cb, GRID_CAP)
+    return SW_SCALAR, min(cdiv(T * I, BLOCK), GRID_CAP)
+
+
+# ---- calls -------------------------------------------------------------------
+@dataclasses.dataclass
+class Call:
+    """One entry call: the op and every argument the guards can see."""
+    op: int
+    dtype: int
+    T: int
+    H: int = 0
+    I: int = 0
+    hd: int = 0
+    nq: int = 0
+    nk: int = 0
+    eps: float = 1e-6
+    base: float = 10000.0
+    # addresses (integers) and strides in elements; None = null pointer
+    ptr: Dict[str, Optional[int]] = dataclasses.field(default_factory=dict)
+    stride: Dict[str, int] = dataclasses.field(default_factory=dict)
+
+
+@dataclasses.dataclass
+class Record:
+    op: int = 0
+    status: int = 0
+    version: int = -1
+    variant: int = 0
+    n_launches: int = 0
+    roles: Tuple[int, int, int] = (0, 0, 0)
+    launch: Tuple[Tuple[int, int, int], ...] = ((0, 0, 0), (0, 0, 0), (0, 0, 0))
+    key: Tuple[int, int, int] = (0, 0, 0)
+
+    def as_tuple(self):
+        return (self.op, self.status, self.version, self.variant, self.n_launches,
+                tuple(self.roles), tuple(tuple(l) for l in self.launch), tuple(self.key))
+
+
+def _validate_common(c: Call) -> Optional[int]:
+    if c.dtype not in (DT_F32, DT_BF16):
+        return E_INVALID
+    if c.T < 0:
+        return E_INVALID
+    if c.T == 0:
+        return OK
+    if c.T > T_MAX:
+        return E_UNSUPPORTED
+    return None
+
+
+def _validate_rn(c: Call, names, strides) -> Optional[int]:
+    if c.H < 1:
+        return E_INVALID
+    if c.H >= H_LIMIT:
+        return E_UNSUPPORTED
+    if any(c.ptr.get(n) is None for n in names):
+        return E_INVALID
+    if any(c.stride[s] < c.H for s in strides):
+        return E_INVALID
+    eps = _f32(c.eps)
+    if not _finite(eps) or eps < 0:
+        return E_INVALID
+    return None
+
+
+def _validate_rope(c: Call) -> Optional[int]:
+    if c.hd < 2 or c.hd % 2:
+        return E_INVALID
+    if c.hd > HD_MAX:
+        return E_UNSUPPORTED
+    if c.nq < 1 or c.nk < 0:
+        return E_INVALID
+    if c.nq > HEADS_MAX or c.nk > HEADS_MAX:
+        return E_UNSUPPORTED
+    if c.ptr.get("q") is None or c.ptr.get("pos") is None:
+        return E_INVALID
+    if c.nk > 0 and c.ptr.get("k") is None:
+        return E_INVALID
+    if c.ptr["pos"] % 4:
+        return E_INVALID
+    if c.stride["q"] < c.nq * c.hd:
+        return E_INVALID
+    if c.nk > 0 and c.stride["k"] < c.nk * c.hd:
+        return E_INVALID
+    base = _f32(c.base)
+    if not _finite(base) or base <= 1.0:
+        return E_INVALID
+    return None
+
+
+def _validate_sw(c: Call) -> Optional[int]:
+    if c.I < 1:
+        return E_INVALID
+    if c.I >= I_LIMIT:
+        return E_UNSUPPORTED
+    if any(c.ptr.get(n) is None for n in ("gate", "up", "out")):
+        return E_INVALID
+    if any(c.stride[s] < c.I for s in ("gate", "up", "out")):
+        return E_INVALID
+    return None
+
+
+RN_PTRS = ("x", "w", "y")
+RN_STRIDES = ("x", "y")
+RES_PTRS = ("x", "res", "w", "y", "res_out")
+RES_STRIDES = ("x", "res", "y", "res_out")
+
+
+def validate(c: Call) -> Optional[int]:
+    """None if the call is valid and non-empty, else its status."""
+    st = _validate_common(c)
+    if st is not None:
+        return st
+    if c.op == OP_RMSNORM:
+        return _validate_rn(c, RN_PTRS, RN_STRIDES)
+    if c.op == OP_RES_RMSNORM:
+        return _validate_rn(c, RES_PTRS, RES_STRIDES)
+    if c.op == OP_ROPE_QK:
+        return _validate_rope(c)
+    if c.op == OP_SWIGLU:
+        return _validate_sw(c)
+    if c.op == OP_CHAIN:
+        for f in (lambda: _validate_rn(c, RES_PTRS, RES_STRIDES),
+                  lambda: _validate_rope(c), lambda: _validate_sw(c)):
+            st = f()
+            if st is not None:
+                return st
+        return None
+    return E_INVALID
+
+
+# ---- guard flags and key ------------------------------------------------------
+def rn_flags(c: Call, names, strides) -> int:
+    es = elem_size(c.dtype)
+    f = 0
+    if _aligned(es, [c.ptr[n] for n in names], [c.stride[s] for s in strides]):
+        f |= ALIGN
+    if all(c.stride[s] == c.H for s in strides):
+        f |= CONTIG
+    return f
+
+
+def rope_flags(c: Call) -> int:
+    es = elem_size(c.dtype)
+    ptrs, strides = [c.ptr["q"]], [c.stride["q"]]
+    contig = c.stride["q"] == c.nq * c.hd
+    if c.nk > 0:
+        ptrs.append(c.ptr["k"])
+        strides.append(c.stride["k"])
+        contig = contig and c.stride["k"] == c.nk * c.hd
+    f = ALIGN if _aligned(es, ptrs, strides) else 0
+    return f | (CONTIG if contig else 0)
+
+
+def sw_flags(c: Call) -> int:
+    es = elem_size(c.dtype)
+    names = ("gate", "up", "out")
+    f = ALIGN if _aligned(es, [c.ptr[n] for n in names], [c.stride[n] for n in names]) else 0
+    if all(c.stride[n] == c.I for n in names):
+        f |= CONTIG
+    return f
+
+
+def op_flags(c: Call) -> int:
+    if c.op == OP_RMSNORM:
+        return rn_flags(c, RN_PTRS, RN_STRIDES)
+    if c.op == OP_RES_RMSNORM:
+        return rn_flags(c, RES_PTRS, RES_STRIDES)
+    if c.op == OP_ROPE_QK:
+        return rope_flags(c)
+    if c.op == OP_SWIGLU:
+        return sw_flags(c)
+    return (rn_flags(c, RES_PTRS, RES_STRIDES) | (rope_flags(c) << 2)
+            | (sw_flags(c) << 4))
+
+
+def make_key(c: Call) -> Tuple[int, int, int]:
+    b = bucket(c.T)
+    flags = op_flags(c)
+    base_bits = f32_bits(c.base) if c.op in (OP_ROPE_QK, OP_CHAIN) else 0
+    H = c.H if c.op in (OP_RMSNORM, OP_RES_RMSNORM, OP_CHAIN) else 0
+    I = c.I if c.op in (OP_SWIGLU, OP_CHAIN) else 0
+    hd, nq, nk = (c.hd, c.nq, c.nk) if c.op in (OP_ROPE_QK, OP_CHAIN) else (0, 0, 0)
+    k0 = c.op | (c.dtype << 8) | (b << 16) | (flags << 24) | (base_bits << 32)
+    k1 = H | (I << 32)
+    k2 = hd | (nq << 16) | (nk << 32)
+    return (k0, k1, k2)
+
+
+def unpack_key(key):
+    k0, k1, k2 = key
+    return dict(op=k0 & 0xFF, dtype=(k0 >> 8) & 0xFF, bucket=(k0 >> 16) & 0xFF,
+                flags=(k0 >> 24) & 0xFF, base_bits=k0 >> 32,
+                H=k1 & 0xFFFFFFFF, I=k1 >> 32,
+                hd=k2 & 0xFFFF, nq=(k2 >> 16) & 0xFFFF, nk=(k2 >> 32) & 0xFFFF)
+
+
+# ---- install policy: key -> variants, and per-call launch geometry ---------------
+def plan(key, T: int):
+    """(variant, roles, launches) for a version with `key`, called with T tokens."""
+    f = unpack_key(key)
+    op, dt, b, fl = f["op"], f["dtype"], f["bucket"], f["flags"]
+    if op in (OP_RMSNORM, OP_RES_RMSNORM):
+        v, g = rn_role(dt, f["H"], fl, T)
+        return v, (0, 0, 0), [(v, g, BLOCK)]
+    if op == OP_ROPE_QK:
+        v, g = rope_role(dt, f["hd"], fl, b, T)
+        return v, (0, 0, 0), [(v, g, BLOCK)]
+    if op == OP_SWIGLU:
+        v, g = sw_role(dt, f["I"], fl, b, T)
+        return v, (0, 0, 0), [(v, g, BLOCK)]
+    rn = rn_role(dt, f["H"], fl & 3, T)
+    ro = rope_role(dt, f["hd"], (fl >> 2) & 3, b, T)
+    sw = sw_role(dt, f["I"], (fl >> 4) & 3, b, T)
+    roles = (rn[0], ro[0], sw[0])
+    fused = (fl == 0x3F and rn[0] in RN_WAVE.values()
+             and ro[0] in (ROPE_VEC_T1, ROPE_VEC_T4)
+             and sw[0] in (SW_FLAT_U1, SW_FLAT_U4))
+    if fused:
+        return CH_FUSED, roles, [(CH_FUSED, rn[1] + ro[1] + sw[1], BLOCK)]
+    return CH_SEQ, roles, [(rn[0], rn[1], BLOCK), (ro[0], ro[1], BLOCK),
+                           (sw[0], sw[1], BLOCK)]
+
+
+# ---- the cache -----------------------------------------------------------------
+@dataclasses.dataclass
+class Stats:
+    calls: int = 0
+    hits: int = 0
+    misses: int = 0
+    errors: int = 0
+    empty: int = 0
+    installs: int = 0
+
+
+class SpecCacheModel:
+    """Ordered versions, Algorithm 1 lookup, miss / install / error paths."""
+
+    def __init__(self, capacity: int = 0, flags: int = 0):
+        if capacity < 0 or capacity > MAX_CAPACITY or flags & ~FLAG_AUTO_INSTALL:
+            raise ValueError("invalid cache parameters")
+        self.capacity = capacity or DEFAULT_CAPACITY
+        self.flags = flags
+        self.versions: List[Tuple[int, int, int]] = []
+        self.version_hits: List[int] = []
+        self.last_miss: Optional[Tuple[Tuple[int, int, int], int]] = None
+        self.stats = Stats()
+        self.last = Record()
+        # launch_fails: set of global launch ordinals (0-based) that fail,
+        # mirroring fault injection in the host test double.
+        self.launch_fails = set()
+        self.launch_count = 0
+
+    def lookup(self, key) -> int:
+        """Algorithm 1's scan: index of the first version whose guards hold."""
+        for i, vkey in enumerate(self.versions):
+            if vkey == key:
+                return i
+        return -1
+
+    def _launch(self, launches) -> int:
+        for _ in launches:
+            n = self.launch_count
+            self.launch_count += 1
+            if n in self.launch_fails:
+                return E_LAUNCH
+        return OK
+
+    def call(self, c: Call) -> int:
+        self.stats.calls += 1
+        rec = Record(op=c.op)
+        st = validate(c)
+        if st is not None:
+            rec.status = st
+            self.last = rec
+            if st == OK:
+                self.stats.empty += 1
+            else:
+                self.stats.errors += 1
+            return st
+        key = make_key(c)
+        rec.key = key
+        i = self.lookup(key)
+        auto = False
+        if i < 0:
+            self.stats.misses += 1
+            self.last_miss = (key, c.T)
+            if not (self.flags & FLAG_AUTO_INSTALL):
+                rec.status = MISS
+                self.last = rec
+                return MISS
+            st = self._install(key)
+            if st < 0:
+                rec.status = st
+                self.last = rec
+                return st
+            i = self.lookup(key)
+            auto = True
+        variant, roles, launches = plan(key, c.T)
+        rec.version, rec.variant, rec.roles = i, variant, roles
+        rec.n_launches = len(launches)
+        rec.launch = tuple(launches) + ((0, 0, 0),) * (3 - len(launches))
+        st = self._launch(launches)
+        rec.status = st
+        self.last = rec
+        if st < 0:
+            if not auto:
+                self.stats.errors += 1
+            return st
+        if not auto:
+            self.stats.hits += 1
+            self.version_hits[i] += 1
+        return OK
+
+    def _install(self, key) -> int:
+        if self.lookup(key) >= 0:
+            return OK
+        if len(self.versions) >= self.capacity:
+            return E_FULL
+        self.versions.append(key)
+        self.version_hits.append(0)
+        self.stats.installs += 1
+        return OK
+
+    def install_last_miss(self) -> Tuple[int, Optional[Record]]:
+        if self.last_miss is None:
+            return E_INVALID, None
+        key, T = self.last_miss
+        st = self._install(key)
+        if st < 0:
+            return st, None
+        variant, roles, launches = plan(key, T)
+        rec = Record(op=key[0] & 0xFF, status=OK, version=self.lookup(key),
+                     variant=variant, n_launches=len(launches), roles=roles,
+                     launch=tuple(launches) + ((0, 0, 0),) * (3 - len(launches)),
+                     key=key)
+        return OK, rec

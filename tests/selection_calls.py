@@ -1,0 +1,65 @@
+"""Builders of oracle selection-model calls from plain dimensions.
+
+Shared by the CPU tests of the selection model and of the host library, so
+both see the same synthetic addresses and strides. Addresses are integers
+(no memory behind them): the selection depends only on their values.
+"""
+from oracle import selection as S
+
+BASE_ADDR = 0x7F0000000000
+
+
+def _addr(i):
+    return BASE_ADDR + i * (1 << 32)
+
+
+def rn_call(dtype, T, H, *, eps=1e-6, off=0, pad=0, null=()):
+    ptr = {n: (_addr(i) + off if n != "w" else _addr(i)) for i, n in enumerate(S.RN_PTRS)}
+    for n in null:
+        ptr[n] = None
+    return S.Call(S.OP_RMSNORM, dtype, T, H=H, eps=eps, ptr=ptr,
+                  stride={"x": H + pad, "y": H + pad})
+
+
+def res_call(dtype, T, H, *, eps=1e-6, off=0, pad=0, null=(), op=S.OP_RES_RMSNORM):
+    ptr = {n: (_addr(i) + off if n != "w" else _addr(i)) for i, n in enumerate(S.RES_PTRS)}
+    for n in null:
+        ptr[n] = None
+    return S.Call(op, dtype, T, H=H, eps=eps, ptr=ptr,
+                  stride={n: H + pad for n in S.RES_STRIDES})
+
+
+def rope_call(dtype, T, nq, nk, hd, *, base=10000.0, off=0, pad=0, pos_off=0, null=()):
+    ptr = {"q": _addr(10) + off, "k": _addr(11) + off, "pos": _addr(12) + pos_off}
+    for n in null:
+        ptr[n] = None
+    return S.Call(S.OP_ROPE_QK, dtype, T, hd=hd, nq=nq, nk=nk, base=base, ptr=ptr,
+                  stride={"q": nq * hd + pad, "k": nk * hd + pad})
+
+
+def sw_call(dtype, T, I, *, off=0, pad=0, null=()):
+    ptr = {"gate": _addr(20) + off, "up": _addr(21) + off, "out": _addr(22) + off}
+    for n in null:
+        ptr[n] = None
+    return S.Call(S.OP_SWIGLU, dtype, T, I=I, ptr=ptr,
+                  stride={"gate": I + pad, "up": I + pad, "out": I + pad})
+
+
+def chain_call(dtype, T, H, I, nq, nk, hd, *, base=10000.0, eps=1e-6,
+               res_off=0, res_pad=0, rope_off=0, rope_pad=0, sw_off=0, sw_pad=0):
+    r = res_call(dtype, T, H, eps=eps, off=res_off, pad=res_pad)
+    q = rope_call(dtype, T, nq, nk, hd, base=base, off=rope_off, pad=rope_pad)
+    s = sw_call(dtype, T, I, off=sw_off, pad=sw_pad)
+    ptr = dict(r.ptr)
+    ptr.update(q.ptr)
+    ptr.update(s.ptr)
+    stride = dict(r.stride)
+    stride.update(q.stride)
+    stride.update(s.stride)
+    return S.Call(S.OP_CHAIN, dtype, T, H=H, I=I, hd=hd, nq=nq, nk=nk, eps=eps,
+                  base=base, ptr=ptr, stride=stride)
+
+
+def elem_offset(dtype, n=1):
+    """Byte offset of n elements (used to build unaligned layouts)."""
+    return n * S.elem_size(dtype)

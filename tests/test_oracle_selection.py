@@ -1,0 +1,210 @@
+"""Pins for the selection model: ordered dispatch (Algorithm 1, Sec. 3.2),
+the miss / install / error paths (Sec. 3.5) and the install policy table,
+worked by hand for the decode shapes (CPU only)."""
+import pytest
+
+from oracle import selection as S
+from tests.selection_calls import (chain_call, elem_offset, res_call, rn_call,
+                                   rope_call, sw_call)
+
+BF, F = S.DT_BF16, S.DT_F32
+
+
+def test_bucket_closed_form():
+    # ceil(log2 T) for T >= 1, via the bit length of T - 1.
+    for T in range(1, 1 << 16):
+        assert S.bucket(T) == (T - 1).bit_length()
+    for T in (1 << 20, (1 << 20) + 1, S.T_MAX):
+        assert S.bucket(T) == (T - 1).bit_length()
+
+
+def test_key_round_trip():
+    c = chain_call(BF, 8, 4096, 14336, 32, 8, 128, base=500000.0)
+    f = S.unpack_key(S.make_key(c))
+    assert (f["op"], f["dtype"], f["bucket"], f["flags"]) == (S.OP_CHAIN, BF, 3, 0x3F)
+    assert (f["H"], f["I"], f["hd"], f["nq"], f["nk"]) == (4096, 14336, 128, 32, 8)
+    assert f["base_bits"] == 0x48F42400          # 500000.0f
+
+
+def test_unused_key_fields_are_zero():
+    f = S.unpack_key(S.make_key(rn_call(F, 3, 256)))
+    assert (f["I"], f["hd"], f["nq"], f["nk"], f["base_bits"]) == (0, 0, 0, 0, 0)
+    f = S.unpack_key(S.make_key(sw_call(F, 3, 688)))
+    assert (f["H"], f["hd"], f["base_bits"]) == (0, 0, 0)
+
+
+# ---- policy worked by hand --------------------------------------------------------
+def test_policy_llama7b_decode_chain():
+    # bf16: 8 elements per 16 B. H = 4096 -> 512 vectors -> 8 per lane -> RN_WAVE_8,
+    # 1 row -> 1 workgroup. T = 1 -> bucket 0 -> RoPE one token per block, SwiGLU
+    # one vector per thread: 11008 / 8 = 1376 vectors -> 6 workgroups.
+    v, roles, launches = S.plan(S.make_key(chain_call(BF, 1, 4096, 11008, 32, 32, 128)), 1)
+    assert v == S.CH_FUSED
+    assert roles == (14, 21, 31)
+    assert launches == [(50, 1 + 1 + 6, 256)]
+
+
+def test_policy_gqa_decode_chain():
+    # T = 8 -> bucket 3: RoPE still one token per block (8 blocks);
+    # SwiGLU 8 * 14336 / 8 = 14336 vectors -> 56 blocks; norm ceil(8/4) = 2.
+    v, roles, launches = S.plan(S.make_key(chain_call(BF, 8, 4096, 14336, 32, 8, 128,
+                                                      base=500000.0)), 8)
+    assert (v, roles, launches) == (S.CH_FUSED, (14, 21, 31), [(50, 2 + 8 + 56, 256)])
+
+
+def test_policy_prefill_chain():
+    # H = 8192 bf16 -> 1024 vectors -> 16 per lane -> RN_WAVE_16, 2048 blocks;
+    # T = 8192 -> bucket 13: RoPE 4 tokens per block (2048 blocks); SwiGLU
+    # 8192 * 28672 / 8 = 29360128 vectors at 4 per thread -> 28672 blocks.
+    v, roles, launches = S.plan(S.make_key(chain_call(BF, 8192, 8192, 28672, 64, 8, 128,
+                                                      base=500000.0)), 8192)
+    assert (v, roles) == (S.CH_FUSED, (15, 22, 32))
+    assert launches == [(50, 2048 + 2048 + 28672, 256)]
+
+
+def test_policy_tiny_f32_chain():
+    # f32: 4 per 16 B. H = 256 -> 64 vectors -> 1 per lane -> RN_WAVE_1.
+    # hd 64 -> 32 pairs -> 8 vectors per half (power of two) -> ROPE_VEC_T1.
+    # SwiGLU 4 * 688 / 4 = 688 vectors -> 3 blocks.
+    v, roles, launches = S.plan(S.make_key(chain_call(F, 4, 256, 688, 4, 4, 64)), 4)
+    assert (v, roles, launches) == (S.CH_FUSED, (11, 21, 31), [(50, 1 + 4 + 3, 256)])
+
+
+@pytest.mark.parametrize("H,dtype,want", [
+    (64, F, (11, 2)), (256, BF, (11, 2)), (520, BF, (12, 2)), (4096, F, (15, 2)),
+    (8192, F, (16, 5)), (16384, F, (17, 5)), (32768, BF, (17, 5)),
+    (65536, BF, (18, 5)), (100, BF, (10, 5)), (4097, F, (10, 5))])
+def test_rmsnorm_policy_by_row_size(H, dtype, want):
+    # 5 rows: one wave per row packs 4 rows per block (2 blocks); the other
+    # variants take one block per row.
+    v, g = S.rn_role(dtype, H, S.ALIGN | S.CONTIG, 5)
+    assert (v, g) == want
+
+
+def test_unaligned_and_strided_layouts():
+    off = elem_offset(BF)
+    assert S.plan(S.make_key(rn_call(BF, 2, 4096, off=off)), 2)[0] == S.RN_SCALAR
+    # a padded row stride that keeps 16 B alignment stays vectorised
+    assert S.plan(S.make_key(rn_call(BF, 2, 4096, pad=64)), 2)[0] == 14
+    assert S.plan(S.make_key(sw_call(BF, 2, 11008, pad=64)), 2)[0] == S.SW_ROWS
+    assert S.plan(S.make_key(sw_call(BF, 2, 11008, off=off)), 2)[0] == S.SW_SCALAR
+    assert S.plan(S.make_key(sw_call(BF, 2, 11003, pad=1)), 2)[0] == S.SW_SCALAR
+    assert S.plan(S.make_key(rope_call(BF, 2, 32, 32, 128, off=off)), 2)[0] == S.ROPE_SCALAR
+    # hd 96 bf16: 48 pairs = 6 vectors per half, not a power of two
+    assert S.plan(S.make_key(rope_call(BF, 2, 4, 4, 96)), 2)[0] == S.ROPE_SCALAR
+    c = chain_call(BF, 4, 4096, 11008, 32, 32, 128, sw_pad=64)
+    v, roles, launches = S.plan(S.make_key(c), 4)
+    assert v == S.CH_SEQ and roles == (14, 21, S.SW_ROWS) and len(launches) == 3
+
+
+def test_chain_key_keeps_per_role_flags():
+    a = chain_call(BF, 4, 4096, 11008, 32, 32, 128, sw_pad=64)
+    b = chain_call(BF, 4, 4096, 11008, 32, 32, 128, rope_pad=64)
+    assert S.make_key(a) != S.make_key(b)
+    assert S.plan(S.make_key(a), 4)[1] != S.plan(S.make_key(b), 4)[1]
+
+
+def test_swiglu_flat_grid_cap_and_tail():
+    # 3 * 5 = 15 f32 elements: 3 whole vectors + a 3-element tail -> 1 block
+    assert S.sw_role(F, 5, 3, 2, 3) == (S.SW_FLAT_U1, 1)
+    # 1 element: no whole vector, still one block for the tail
+    assert S.sw_role(F, 1, 3, 0, 1) == (S.SW_FLAT_U1, 1)
+    v, g = S.sw_role(BF, 1 << 30, 3, 10, 1024)
+    assert (v, g) == (S.SW_FLAT_U4, S.GRID_CAP)
+
+
+# ---- Algorithm 1 and the three paths ---------------------------------------------
+def test_miss_install_hit_and_order():
+    m = S.SpecCacheModel()
+    a = rn_call(BF, 1, 4096)
+    b = rn_call(BF, 3, 4096)          # bucket 2: a different specialization
+    assert m.call(a) == S.MISS and m.last.n_launches == 0 and m.launch_count == 0
+    assert m.install_last_miss()[0] == S.OK
+    assert m.call(a) == S.OK and m.last.version == 0
+    assert m.call(b) == S.MISS
+    st, rec = m.install_last_miss()
+    assert st == S.OK and rec.version == 1
+    assert m.call(b) == S.OK and m.last.version == 1
+    assert m.call(a) == S.OK and m.last.version == 0
+    assert m.versions[0] != m.versions[1]
+    s = m.stats
+    assert (s.calls, s.hits, s.misses, s.errors, s.installs) == (5, 3, 2, 0, 2)
+    assert m.version_hits == [2, 1]
+
+
+def test_install_is_idempotent_and_needs_a_miss():
+    m = S.SpecCacheModel()
+    assert m.install_last_miss()[0] == S.E_INVALID
+    c = sw_call(F, 4, 688)
+    m.call(c)
+    m.call(c)
+    assert m.install_last_miss()[0] == S.OK
+    assert m.install_last_miss()[0] == S.OK
+    assert len(m.versions) == 1 and m.stats.installs == 1
+
+
+def test_capacity_is_enforced():
+    m = S.SpecCacheModel(capacity=2)
+    for T in (1, 2, 4):
+        assert m.call(sw_call(BF, T, 128)) == S.MISS
+        st, _ = m.install_last_miss()
+    assert st == S.E_FULL and len(m.versions) == 2
+
+
+def test_errors_never_install_or_launch():
+    m = S.SpecCacheModel(flags=S.FLAG_AUTO_INSTALL)
+    bad = [rn_call(BF, 1, 4096, null=("x",)), rn_call(BF, -1, 4096), rn_call(BF, 1, 0),
+           rn_call(BF, 1, 4096, eps=float("nan")), rn_call(BF, 1, 4096, eps=-1.0),
+           rope_call(BF, 1, 4, 4, 63), rope_call(BF, 1, 4, 4, 64, base=1.0),
+           rope_call(BF, 1, 4, 4, 64, pos_off=2), rope_call(BF, 1, 0, 4, 64),
+           sw_call(BF, 1, 0), rn_call(7, 1, 4096)]
+    for c in bad:
+        assert m.call(c) == S.E_INVALID
+    assert m.call(rn_call(BF, S.T_MAX + 1, 64)) == S.E_UNSUPPORTED
+    assert m.call(rope_call(BF, 1, 4, 4, 1024)) == S.E_UNSUPPORTED
+    assert m.call(rn_call(BF, 1, S.H_LIMIT)) == S.E_UNSUPPORTED
+    assert m.versions == [] and m.launch_count == 0
+    assert m.stats.errors == len(bad) + 3
+
+
+def test_empty_call_is_ok_and_launches_nothing():
+    m = S.SpecCacheModel()
+    assert m.call(rn_call(BF, 0, 4096, null=("x", "y"))) == S.OK
+    assert m.last.n_launches == 0 and m.stats.empty == 1 and m.versions == []
+
+
+def test_launch_error_stops_dispatch():
+    m = S.SpecCacheModel()
+    c = chain_call(BF, 4, 4096, 11008, 32, 32, 128, sw_pad=64)     # three launches
+    m.call(c)
+    m.install_last_miss()
+    m.launch_fails = {1}
+    assert m.call(c) == S.E_LAUNCH
+    assert m.launch_count == 2                       # the third launch never issued
+    assert len(m.versions) == 1 and m.stats.errors == 1 and m.version_hits == [0]
+
+
+def test_auto_install_counts_one_miss():
+    m = S.SpecCacheModel(flags=S.FLAG_AUTO_INSTALL)
+    c = rn_call(BF, 1, 4096)
+    assert m.call(c) == S.OK and m.call(c) == S.OK
+    s = m.stats
+    assert (s.calls, s.hits, s.misses, s.installs) == (2, 1, 1, 1)
+
+
+def test_stats_invariant_over_mixed_stream():
+    import workloads as wl
+    m = S.SpecCacheModel()
+    for T, dt, layout in wl.mixed_stream(n=2000):
+        d = BF if dt == wl.BF16 else F
+        off = elem_offset(d) if layout == wl.LAYOUT_UNALIGNED else 0
+        pad = wl.MIXED_PAD if layout == wl.LAYOUT_STRIDED else 0
+        c = chain_call(d, T, 4096, 11008, 32, 32, 128, res_off=off, rope_off=off,
+                       sw_off=off, res_pad=pad, rope_pad=pad, sw_pad=pad)
+        if m.call(c) == S.MISS:
+            m.install_last_miss()
+            assert m.call(c) == S.OK
+    s = m.stats
+    assert s.calls == s.hits + s.misses + s.errors + s.empty
+    assert len(set(m.versions)) == len(m.versions) <= 9 * 2 * 3
+    assert s.misses == len(m.versions)
