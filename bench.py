@@ -1,0 +1,242 @@
+#!/usr/bin/env python3
+"""Benchmark of the guarded decode-op path on one MI355X.
+
+Headline (the JSON line's `value`): end-to-end microseconds per decode-chain
+call (host + device: entry call, then stream synchronisation) at 1 token on
+the Llama-7B decode shapes (hidden 4096, 32 + 32 heads of 128, intermediate
+11008, bf16), median over --steps synchronised calls timed in native code.
+Next to it: the same loop around an empty kernel launched through the same
+path, the host-only part, the Python-binding path and the pipelined issue
+rate; and HBM bandwidth of the fused chain and of each op at 8192 tokens
+(hidden 8192, 64 + 8 heads of 128, intermediate 28672, bf16), each launch
+timed with HIP events on its stream after a 1 GiB cache flush.
+
+The CPU oracle is timed on the host as a baseline only.
+"""
+import argparse
+import ctypes as C
+import json
+import os
+import platform
+import statistics
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "µs per decode-chain call (host+device) at 1 token; HBM GB/s at 8192 tokens"
+HBM_PEAK_GBS = 8000.0
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=10000)
+    p.add_argument("--warmup", type=int, default=200)
+    p.add_argument("--bw-reps", type=int, default=20)
+    p.add_argument("--cpu-seconds", type=float, default=10.0)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-bandwidth", action="store_true")
+    return p.parse_args()
+
+
+def summary(xs):
+    xs = sorted(xs)
+    n = len(xs)
+    q1, q3 = xs[n // 4], xs[(3 * n) // 4]
+    iqr = q3 - q1
+    kept = [x for x in xs if q1 - 1.5 * iqr <= x <= q3 + 1.5 * iqr]
+    return {"median": xs[n // 2], "p10": xs[n // 10], "p90": xs[(9 * n) // 10],
+            "mean_iqr": statistics.fmean(kept), "n": n}
+
+
+def algorithmic_bytes(cfg):
+    """Bytes each op must move once: inputs read once, outputs written once,
+    weights and tables counted once per call."""
+    es = 2 if cfg.dtype == "bf16" else 4
+    T, H, I, hd, nh = cfg.T, cfg.H, cfg.I, cfg.hd, cfg.nq + cfg.nk
+    rms = 2 * T * H * es + H * es
+    res = 4 * T * H * es + H * es
+    rope = 2 * T * nh * hd * es + 4 * T + 4 * (hd // 2)
+    sw = 3 * T * I * es
+    return {"rmsnorm": rms, "residual_rmsnorm": res, "rope_qk": rope, "swiglu": sw,
+            "chain": res + rope + sw}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(this path runs on one MI355X and has no multi-GPU leg)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2609_37241_amd as tri
+    import workloads as wl
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    bench = C.CDLL(os.path.join(ROOT, "paper_2609_37241_amd", "libtri_bench.so"))
+    bench.trib_latency.argtypes = [C.c_void_p, C.c_int, C.c_void_p, C.c_void_p, C.c_int, C.c_int,
+                                   C.POINTER(C.c_double), C.POINTER(C.c_double)]
+    bench.trib_issue.argtypes = [C.c_void_p, C.c_int, C.c_void_p, C.c_void_p, C.c_int,
+                                 C.POINTER(C.c_double)]
+    stream = torch.cuda.Stream(device=dev)
+    sptr = stream.cuda_stream
+
+    # ---- 1-token decode chain: per-call latency -----------------------------------
+    cfg = wl.LLAMA7B_DECODE
+    inp = wl.host_inputs(cfg)
+    d = {k: wl.to_torch(v, cfg.dtype, dev) for k, v in inp.items()}
+    cache = tri.SpecCache()
+    args_c, _outs = cache.chain_args(d["x"], d["residual"], d["w"], d["q"], d["k"], d["pos"],
+                                     d["gate"], d["up"], cfg.eps, cfg.base)
+    cache.decode_chain_args(args_c, stream)          # miss -> install -> hit
+    torch.cuda.synchronize()
+    sel = cache.last_selection()
+    K, W = args.steps, args.warmup
+    e2e = (C.c_double * max(K, 1))()
+    hst = (C.c_double * max(K, 1))()
+
+    def run(mode, n_warm, n):
+        st = bench.trib_latency(cache.handle, mode, C.byref(args_c), sptr, n_warm, n, e2e, hst)
+        if st != 0:
+            raise RuntimeError(f"latency loop failed: {st}")
+
+    run(1, W, 0)                                     # warm the empty-kernel path
+    torch.cuda.synchronize()
+    run(1, 0, K)
+    torch.cuda.synchronize()
+    empty_e2e, empty_host = list(e2e[:K]), list(hst[:K])
+
+    run(0, W, 0)                                     # W untimed warmup steps
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    run(0, 0, K)                                     # exactly K timed steps
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    chain_e2e, chain_host = list(e2e[:K]), list(hst[:K])
+
+    tot = C.c_double()
+    n_issue = min(K, 10000)
+    assert bench.trib_issue(cache.handle, 0, C.byref(args_c), sptr, n_issue, C.byref(tot)) == 0
+    issue_us = tot.value / n_issue
+
+    n_py = min(K, 2000)
+    py = []
+    for _ in range(n_py):
+        a = time.perf_counter()
+        cache.decode_chain_args(args_c, stream)
+        stream.synchronize()
+        py.append((time.perf_counter() - a) * 1e6)
+    stats = cache.stats()
+
+    ce, ee = summary(chain_e2e), summary(empty_e2e)
+    latency = {
+        "chain_e2e_us": ce, "chain_host_us": summary(chain_host),
+        "empty_e2e_us": ee, "empty_host_us": summary(empty_host),
+        "ratio_to_empty_median": ce["median"] / ee["median"],
+        "python_binding_e2e_us": summary(py),
+        "pipelined_issue_us_per_call": issue_us,
+        "selection": {"variant": sel.variant, "n_launches": sel.n_launches,
+                      "grid": sel.launch[0].grid_x, "roles": list(sel.roles)},
+        "cache_stats": stats,
+    }
+
+    # ---- 8192-token prefill: HBM bandwidth ------------------------------------------
+    bandwidth, roofline = None, None
+    if not args.no_bandwidth:
+        cfgb = wl.PREFILL_8K
+        nbytes = algorithmic_bytes(cfgb)
+        db = wl.device_inputs(cfgb, dev)
+        y = torch.empty_like(db["x"])
+        ro = torch.empty_like(db["x"])
+        out = torch.empty_like(db["gate"])
+        flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        cb = tri.SpecCache()
+        ab, _ = cb.chain_args(db["x"], db["residual"], db["w"], db["q"], db["k"], db["pos"],
+                              db["gate"], db["up"], cfgb.eps, cfgb.base, y=y, residual_out=ro,
+                              out=out)
+        copy_src = torch.empty(1 << 29, dtype=torch.bfloat16, device=dev)
+        copy_dst = torch.empty_like(copy_src)
+        ops = {
+            "chain": lambda: cb.decode_chain_args(ab, stream),
+            "residual_rmsnorm": lambda: cb.residual_rmsnorm(db["x"], db["residual"], db["w"],
+                                                            cfgb.eps, out=y, residual_out=ro,
+                                                            stream=stream),
+            "rmsnorm": lambda: cb.rmsnorm(db["x"], db["w"], cfgb.eps, out=y, stream=stream),
+            "rope_qk": lambda: cb.rope_qk(db["q"], db["k"], db["pos"], cfgb.base, stream=stream),
+            "swiglu": lambda: cb.swiglu(db["gate"], db["up"], out=out, stream=stream),
+            "copy_1GiB_torch": lambda: copy_dst.copy_(copy_src),
+        }
+        nbytes["copy_1GiB_torch"] = 2 * copy_src.numel() * 2
+        bandwidth = {}
+        for name, fn in ops.items():
+            with torch.cuda.stream(stream):
+                fn()                                 # install / warm
+            torch.cuda.synchronize()
+            times = []
+            for _ in range(args.bw_reps):
+                with torch.cuda.stream(stream):
+                    flush.zero_()
+                    s_ev = torch.cuda.Event(enable_timing=True)
+                    e_ev = torch.cuda.Event(enable_timing=True)
+                    s_ev.record(stream)
+                    fn()
+                    e_ev.record(stream)
+                e_ev.synchronize()
+                times.append(s_ev.elapsed_time(e_ev) * 1e3)   # µs
+            mean_us = statistics.fmean(times)
+            gbs = nbytes[name] / (mean_us * 1e-6) / 1e9
+            bandwidth[name] = {"bytes": nbytes[name], "mean_us": mean_us,
+                               "median_us": statistics.median(times), "GB/s": gbs,
+                               "frac_of_peak": gbs / HBM_PEAK_GBS}
+        ch = bandwidth["chain"]
+        roofline = {"bound": "hbm", "achieved": ch["GB/s"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": ch["GB/s"] / HBM_PEAK_GBS, "traffic": None,
+                    "kernel": "fused decode chain, 8192 tokens (k_chain<bf16, 16, 4, 4>)",
+                    "bytes_per_launch": ch["bytes"], "avg_launch_us": ch["mean_us"]}
+        del db, y, ro, out, flush, copy_src, copy_dst
+
+    # ---- CPU oracle baseline (after all GPU work) ----------------------------------------
+    cpu = None
+    if not args.no_cpu_baseline:
+        from oracle import ops as O
+        try:
+            os.sched_setaffinity(0, {sorted(os.sched_getaffinity(0))[0]})
+        except (AttributeError, OSError):
+            pass
+        times = []
+        t_end = time.perf_counter() + args.cpu_seconds
+        while time.perf_counter() < t_end or len(times) < 5:
+            a = time.perf_counter()
+            O.decode_chain(inp, cfg.eps, cfg.base, cfg.dtype)
+            times.append((time.perf_counter() - a) * 1e6)
+        cpu = {"value": statistics.median(times), "unit": "µs per decode-chain call",
+               "cores": len(os.sched_getaffinity(0)), "kind": "oracle",
+               "sample": f"{len(times)} calls of the float64 oracle decode chain on the "
+                         "1-token Llama-7B shapes, median; host "
+                         f"{platform.processor() or platform.machine()}, "
+                         f"{os.cpu_count()} logical CPUs visible"}
+
+    line = {
+        "metric": METRIC, "value": ce["median"], "unit": "µs", "n_gpus": 1, "steps": K,
+        "warmup": W, "ms_per_step": wall * 1e3 / K, "higher_is_better": False,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "llama7b_decode_bf16: decode chain (residual+RMSNorm, RoPE-QK, "
+                               "SwiGLU) at T=1, hidden 4096, 32+32 heads x 128, "
+                               "intermediate 11008, RoPE base 1e4",
+                   "accumulate": "f32",
+                   "bandwidth_workload": "prefill8k_bf16: T=8192, hidden 8192, 64+8 heads x "
+                                         "128, intermediate 28672, base 5e5, x50 outliers"},
+        "latency": latency, "bandwidth_8192": bandwidth, "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line))
+
+
+if __name__ == "__main__":
+    main()

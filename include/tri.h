@@ -1,0 +1,234 @@
+/*
+ * tri.h -- C ABI of libtri: guarded dispatch of short LLM decode kernels on
+ * AMD MI355X (gfx950).
+ *
+ * What the library is
+ * -------------------
+ * A native specialization cache in the sense of the paper's Specialization
+ * Cache Module (Sec. 3.1): one entry call per op invocation evaluates the
+ * guards of every installed version in C, selects the first version whose
+ * guards hold (ordered dispatch, Algorithm 1 in Sec. 3.2), prepares the
+ * kernel arguments and launches the version's precompiled gfx950 kernel on
+ * the caller's stream. No version matching is a MISS, reported with a status
+ * distinct from every error (Sec. 3.4 keeps miss and error in distinct
+ * result tags; Sec. 3.5 gives the three paths): nothing is launched and the
+ * caller installs a version (tri_spec_install_last_miss) and calls again.
+ * An error never installs anything and never tries another version.
+ *
+ * Guards (the key): op, dtype, hidden size H, intermediate size I, head_dim,
+ * Q and K head counts, token-count bucket ceil(log2 T), 16-byte alignment of
+ * every activation / weight pointer and row stride, contiguity of every row
+ * stride, and the RoPE base. They are equality tests on a packed key, so at
+ * most one version matches.
+ *
+ * Conventions (all entry points)
+ * ------------------------------
+ * - Pointers are DEVICE pointers of the cache's device, owned by the caller,
+ *   and must be aligned to their element size. Outputs are preallocated by
+ *   the caller; no entry point allocates on the hit path.
+ * - Strides are in ELEMENTS. `*_rs` is a row stride, `*_ts` a token stride;
+ *   the innermost stride is always 1. A stride must be at least the logical
+ *   width of its row.
+ * - `stream` is a hipStream_t passed as void* (NULL = the null stream). Work
+ *   is enqueued asynchronously; the call returns before it completes.
+ * - dtype: weights share the activations' dtype. Arithmetic is float32 with
+ *   one rounding to the output dtype.
+ * - T == 0 is a valid no-op: TRI_OK, nothing launched, no other argument
+ *   inspected.
+ * - Validation happens before any launch; a failed check returns a negative
+ *   status and leaves the cache unchanged except its counters.
+ * - One thread per cache. A cache is bound to the device current when it is
+ *   created.
+ */
+#ifndef TRI_H
+#define TRI_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct tri_cache tri_cache;
+
+typedef enum tri_dtype { TRI_F32 = 0, TRI_BF16 = 1 } tri_dtype;
+
+/* TRI_MISS is positive and distinct from the negative errors (Sec. 3.4). */
+typedef enum tri_status {
+  TRI_OK = 0,
+  TRI_MISS = 1,            /* no version matched; nothing launched         */
+  TRI_E_INVALID = -1,      /* bad argument                                  */
+  TRI_E_UNSUPPORTED = -2,  /* valid but beyond the library's limits         */
+  TRI_E_FULL = -3,         /* install: cache at capacity                    */
+  TRI_E_NOMEM = -4,        /* install: device or host allocation failed     */
+  TRI_E_LAUNCH = -5,       /* the selected version's launch failed          */
+  TRI_E_RUNTIME = -6       /* HIP runtime failure outside a launch          */
+} tri_status;
+
+typedef enum tri_op {
+  TRI_OP_RMSNORM = 1, TRI_OP_RES_RMSNORM = 2, TRI_OP_ROPE_QK = 3,
+  TRI_OP_SWIGLU = 4, TRI_OP_CHAIN = 5
+} tri_op;
+
+enum { TRI_CACHE_AUTO_INSTALL = 1u };   /* on a miss: install, then launch */
+
+/* One kernel launch of a selection. */
+typedef struct tri_launch_rec {
+  int32_t variant;     /* kernel variant id (the install policy table)       */
+  uint32_t grid_x;     /* workgroups                                          */
+  uint32_t block_x;    /* work-items per workgroup                            */
+} tri_launch_rec;
+
+/* The selection record of the last entry call (or of an install). */
+typedef struct tri_selection {
+  int32_t op;          /* tri_op                                              */
+  int32_t status;      /* tri_status the call returned                        */
+  int32_t version;     /* index in creation order, -1 when none ran           */
+  int32_t variant;     /* op variant (chain: 50 fused / 51 three launches)    */
+  int32_t n_launches;  /* launches issued (0 on miss / error / T == 0)        */
+  int32_t roles[3];    /* chain only: norm, RoPE, SwiGLU role variants        */
+  tri_launch_rec launch[3];
+  uint64_t key[3];     /* packed guard key, zero when not computed            */
+} tri_selection;
+
+typedef struct tri_stats {
+  uint64_t calls;      /* entry calls with a non-NULL cache                   */
+  uint64_t hits;       /* a version matched and its launches succeeded        */
+  uint64_t misses;     /* no version matched (auto-installed ones included)   */
+  uint64_t errors;     /* negative status (validation or launch)              */
+  uint64_t empty;      /* T == 0 no-ops                                       */
+  uint64_t installs;   /* versions created                                    */
+  uint32_t n_versions;
+  uint32_t capacity;
+} tri_stats;
+
+typedef struct tri_version_info {
+  uint64_t key[3];
+  int32_t variant;
+  int32_t roles[3];
+  uint64_t hits;
+} tri_version_info;
+
+/* Arguments of tri_decode_chain: the three ops on disjoint operands. */
+typedef struct tri_chain_args {
+  int32_t dtype;       /* tri_dtype for every tensor                          */
+  int32_t nq, nk, hd;  /* RoPE: Q heads, K heads, head_dim                    */
+  int64_t T, H, I;     /* tokens, hidden size, intermediate size              */
+  float eps;           /* RMSNorm epsilon                                      */
+  float base;          /* RoPE base                                            */
+  /* residual add + RMSNorm over [T, H] */
+  const void *x;   int64_t x_rs;
+  const void *res; int64_t res_rs;
+  const void *w;                       /* [H]                                 */
+  void *y;         int64_t y_rs;
+  void *res_out;   int64_t ro_rs;
+  /* RoPE, in place: q [T, nq, hd], k [T, nk, hd], head stride hd */
+  void *q;         int64_t q_ts;
+  void *k;         int64_t k_ts;
+  const int32_t *pos;                  /* [T]                                 */
+  /* SwiGLU over [T, I] */
+  const void *gate; int64_t g_rs;
+  const void *up;   int64_t u_rs;
+  void *out;        int64_t o_rs;
+} tri_chain_args;
+
+/* ---- cache ---------------------------------------------------------------- */
+
+/* Create an empty cache on the current device. capacity 0 selects 256
+ * (at most 4096); flags: 0 or TRI_CACHE_AUTO_INSTALL. The cache owns every
+ * version, its resolved kernel handles and its device constants; release it
+ * with tri_spec_cache_destroy. Errors: INVALID (NULL out, capacity or flags
+ * out of range), RUNTIME (no usable device), NOMEM. */
+tri_status tri_spec_cache_create(tri_cache **out, uint32_t capacity, uint32_t flags);
+void tri_spec_cache_destroy(tri_cache *cache);
+
+/* ---- ops (the hit path) ------------------------------------------------------ */
+
+/* RMSNorm of each row of x [T, H]: y = w * x / sqrt(mean(x^2) + eps).
+ * The paper's motivating kernel (`rms_norm`, Sec. 2.3 and Fig. 1); the
+ * formula is the standard Llama form, float32 accumulation. y may alias x
+ * exactly. Returns OK, MISS or an error. */
+tri_status tri_rmsnorm(tri_cache *cache, tri_dtype dtype,
+                       const void *x, int64_t x_rs, const void *w,
+                       void *y, int64_t y_rs,
+                       int64_t T, int64_t H, float eps, void *stream);
+
+/* Fused residual add + RMSNorm: h = RN_dtype(x + res), res_out = h,
+ * y = RMSNorm(h) (the norm of the rounded sum). `add` and `rms_norm` are in
+ * the paper's kernel suite (Sec. 4.1). res_out may alias res and y may alias
+ * x exactly. */
+tri_status tri_residual_rmsnorm(tri_cache *cache, tri_dtype dtype,
+                                const void *x, int64_t x_rs,
+                                const void *res, int64_t res_rs,
+                                const void *w,
+                                void *y, int64_t y_rs,
+                                void *res_out, int64_t ro_rs,
+                                int64_t T, int64_t H, float eps, void *stream);
+
+/* Rotary position embedding on Q [T, nq, hd] and K [T, nk, hd], in place,
+ * rotate-half pairs (i, i + hd/2): theta = float32(pos[t]) * inv_i with
+ * inv_i = RN_f32(base^(-2i/hd)); the same angles for every Q and K head of
+ * a token. Not defined in the paper (a standard Llama-family op). hd even,
+ * 2..512; nq 1..4096; nk 0..4096 (k may be NULL when nk == 0); pos int32 [T],
+ * 4-byte aligned; base finite and > 1. The per-version table of inv_i is
+ * computed and uploaded at install. */
+tri_status tri_rope_qk(tri_cache *cache, tri_dtype dtype,
+                       void *q, int64_t q_ts, void *k, int64_t k_ts,
+                       const int32_t *pos, int64_t T,
+                       int32_t nq, int32_t nk, int32_t hd, float base,
+                       void *stream);
+
+/* SwiGLU: out = g / (1 + exp(-g)) * u over [T, I] (`silu` is in the paper's
+ * kernel suite, Sec. 4.1). out may alias gate or up exactly. */
+tri_status tri_swiglu(tri_cache *cache, tri_dtype dtype,
+                      const void *gate, int64_t g_rs, const void *up, int64_t u_rs,
+                      void *out, int64_t o_rs, int64_t T, int64_t I, void *stream);
+
+/* The decode chain: residual+RMSNorm, RoPE-QK and SwiGLU of one decode step,
+ * on disjoint operands (overlap between the three ops is undefined). When
+ * every tensor is 16-byte aligned and contiguous this is ONE launch of a
+ * fused kernel whose workgroups take the three roles by blockIdx range;
+ * otherwise three launches. If a later launch of the three fails, earlier
+ * ones may already be enqueued; E_LAUNCH is returned and no other version is
+ * tried. */
+tri_status tri_decode_chain(tri_cache *cache, const tri_chain_args *args, void *stream);
+
+/* ---- miss handling, introspection -------------------------------------------- */
+
+/* Install a version for the key of the most recent MISS (Sec. 3.5: growth on
+ * a miss): the install policy picks the kernel variant(s) from the key, the
+ * kernel handles are resolved once, per-version constants (the RoPE inverse
+ * frequencies) are uploaded, and the version is appended. Idempotent: a key
+ * already installed adds nothing. `out` (nullable) receives the selection a
+ * call with the missed arguments will make. Errors: INVALID (no miss yet),
+ * FULL, NOMEM, RUNTIME. */
+tri_status tri_spec_install_last_miss(tri_cache *cache, tri_selection *out);
+
+/* Copy the selection record of the last entry call. */
+tri_status tri_spec_last_selection(const tri_cache *cache, tri_selection *out);
+
+/* Copy the counters. */
+tri_status tri_spec_stats(const tri_cache *cache, tri_stats *out);
+
+/* Describe version `index` (creation order). INVALID if out of range. */
+tri_status tri_spec_version_info(const tri_cache *cache, uint32_t index,
+                                 tri_version_info *out);
+
+/* Copy version `index`'s host copy of its constants (RoPE inverse
+ * frequencies, hd/2 floats; none for other ops) into out[0..cap); *n gets
+ * the count. */
+tri_status tri_spec_version_constants(const tri_cache *cache, uint32_t index,
+                                      float *out, uint32_t cap, uint32_t *n);
+
+/* Launch the empty kernel (1 workgroup of 64 work-items, no arguments)
+ * through the same launch path: the yardstick for per-call cost. */
+tri_status tri_launch_empty(tri_cache *cache, void *stream);
+
+/* Static name of a status value. */
+const char *tri_status_str(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TRI_H */

@@ -26,8 +26,9 @@ from __future__ import annotations
 
 import dataclasses
 import math
-import struct
 from typing import Dict, List, Optional, Tuple
+
+import numpy as np
 
 # ---- enumerations (the ABI's numeric values) --------------------------------
 OP_RMSNORM, OP_RES_RMSNORM, OP_ROPE_QK, OP_SWIGLU, OP_CHAIN = 1, 2, 3, 4, 5
@@ -85,7 +86,7 @@ def is_pow2(n: int) -> bool:
 
 
 def f32_bits(x: float) -> int:
-    return struct.unpack("<I", struct.pack("<f", x))[0]
+    return int(np.array([x], dtype=np.float64).astype(np.float32).view(np.uint32)[0])
 
 
 def _finite(x: float) -> bool:
@@ -93,7 +94,9 @@ def _finite(x: float) -> bool:
 
 
 def _f32(x: float) -> float:
-    return struct.unpack("<f", struct.pack("<f", x))[0]
+    """The float32 value a C caller passes for x (overflow -> inf)."""
+    with np.errstate(over="ignore"):
+        return float(np.array([x], dtype=np.float64).astype(np.float32)[0])
 
 
 def _aligned(es: int, ptrs, strides) -> bool:
@@ -193,6 +196,9 @@ def _validate_rn(c: Call, names, strides) -> Optional[int]:
         return E_UNSUPPORTED
     if any(c.ptr.get(n) is None for n in names):
         return E_INVALID
+    es = elem_size(c.dtype)
+    if any(c.ptr[n] % es for n in names):
+        return E_INVALID
     if any(c.stride[s] < c.H for s in strides):
         return E_INVALID
     eps = _f32(c.eps)
@@ -216,6 +222,9 @@ def _validate_rope(c: Call) -> Optional[int]:
         return E_INVALID
     if c.ptr["pos"] % 4:
         return E_INVALID
+    es = elem_size(c.dtype)
+    if c.ptr["q"] % es or (c.nk > 0 and c.ptr["k"] % es):
+        return E_INVALID
     if c.stride["q"] < c.nq * c.hd:
         return E_INVALID
     if c.nk > 0 and c.stride["k"] < c.nk * c.hd:
@@ -232,6 +241,9 @@ def _validate_sw(c: Call) -> Optional[int]:
     if c.I >= I_LIMIT:
         return E_UNSUPPORTED
     if any(c.ptr.get(n) is None for n in ("gate", "up", "out")):
+        return E_INVALID
+    es = elem_size(c.dtype)
+    if any(c.ptr[n] % es for n in ("gate", "up", "out")):
         return E_INVALID
     if any(c.stride[s] < c.I for s in ("gate", "up", "out")):
         return E_INVALID

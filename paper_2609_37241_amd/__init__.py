@@ -1,0 +1,227 @@
+"""tri: guarded dispatch of short LLM decode kernels on AMD MI355X (gfx950).
+
+A thin binding over libtri's C ABI (include/tri.h). Every call marshals
+torch tensors into pointers, element strides and the current HIP stream,
+and makes ONE native entry call; guard evaluation, version lookup, argument
+preparation, the launch and all arithmetic happen in libtri and its gfx950
+kernels. On TRI_MISS the binding asks the library to install a version for
+the missed key and calls again -- the paper's miss path (Sec. 3.5), with
+"compile" replaced by selecting a precompiled kernel variant.
+
+PyTorch is used for device memory and streams only. There is no fallback:
+if libtri.so is missing, importing this package raises.
+"""
+from __future__ import annotations
+
+import ctypes as C
+from typing import Optional, Tuple
+
+import torch
+
+from . import _lib as L
+from ._lib import (AUTO_INSTALL, BF16, E_FULL, E_INVALID, E_LAUNCH, E_NOMEM, E_RUNTIME,
+                   E_UNSUPPORTED, F32, MISS, OK, ChainArgs, Selection, Stats, VersionInfo)
+
+__all__ = ["SpecCache", "TriError", "dtype_code", "Selection", "Stats", "ChainArgs",
+           "OK", "MISS", "E_INVALID", "E_UNSUPPORTED", "E_FULL", "E_NOMEM", "E_LAUNCH",
+           "E_RUNTIME", "F32", "BF16", "AUTO_INSTALL"]
+
+_dll = L.load()
+
+
+class TriError(RuntimeError):
+    def __init__(self, status: int, what: str = ""):
+        self.status = status
+        name = _dll.tri_status_str(status).decode()
+        super().__init__(f"{what}: {name} ({status})" if what else f"{name} ({status})")
+
+
+def dtype_code(dt: torch.dtype) -> int:
+    if dt == torch.float32:
+        return F32
+    if dt == torch.bfloat16:
+        return BF16
+    raise TypeError(f"unsupported dtype {dt} (float32 or bfloat16)")
+
+
+def _stream_ptr(stream) -> Optional[int]:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream or None
+
+
+def _rows(t: torch.Tensor, name: str) -> int:
+    """Row stride (elements) of a [T, W] tensor with unit inner stride."""
+    if t.dim() != 2:
+        raise ValueError(f"{name}: expected 2 dims, got {tuple(t.shape)}")
+    if t.shape[1] > 1 and t.stride(1) != 1:
+        raise ValueError(f"{name}: inner stride must be 1")
+    return t.stride(0) if t.shape[0] > 1 else max(t.stride(0), t.shape[1])
+
+
+def _tokens(t: torch.Tensor, name: str) -> int:
+    """Token stride (elements) of a [T, heads, hd] tensor with heads packed."""
+    if t.dim() != 3:
+        raise ValueError(f"{name}: expected 3 dims, got {tuple(t.shape)}")
+    _, nh, hd = t.shape
+    if (hd > 1 and t.stride(2) != 1) or (nh > 1 and t.stride(1) != hd):
+        raise ValueError(f"{name}: heads must be packed (stride {hd}) with unit inner stride")
+    return t.stride(0) if t.shape[0] > 1 else max(t.stride(0), nh * hd)
+
+
+class SpecCache:
+    """One native specialization cache (bound to the current device)."""
+
+    def __init__(self, capacity: int = 0, auto_install: bool = False):
+        h = C.c_void_p()
+        st = _dll.tri_spec_cache_create(C.byref(h), capacity,
+                                        AUTO_INSTALL if auto_install else 0)
+        if st != OK:
+            raise TriError(st, "tri_spec_cache_create")
+        self._h = h
+        self.misses_handled = 0
+
+    def close(self):
+        if self._h:
+            _dll.tri_spec_cache_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    @property
+    def handle(self) -> C.c_void_p:
+        return self._h
+
+    # ---- miss path ---------------------------------------------------------
+    def _call(self, what: str, fn, *args) -> None:
+        st = fn(self._h, *args)
+        if st == MISS:
+            self.install_last_miss()
+            self.misses_handled += 1
+            st = fn(self._h, *args)
+        if st != OK:
+            raise TriError(st, what)
+
+    def install_last_miss(self) -> Selection:
+        sel = Selection()
+        st = _dll.tri_spec_install_last_miss(self._h, C.byref(sel))
+        if st != OK:
+            raise TriError(st, "tri_spec_install_last_miss")
+        return sel
+
+    # ---- ops ---------------------------------------------------------------
+    def rmsnorm(self, x: torch.Tensor, w: torch.Tensor, eps: float = 1e-6,
+                out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+        y = torch.empty_like(x) if out is None else out
+        T, H = x.shape
+        self._call("tri_rmsnorm", _dll.tri_rmsnorm, dtype_code(x.dtype), x.data_ptr(),
+                   _rows(x, "x"), w.data_ptr(), y.data_ptr(), _rows(y, "y"), T, H, eps,
+                   _stream_ptr(stream))
+        return y
+
+    def residual_rmsnorm(self, x, residual, w, eps: float = 1e-6, out=None, residual_out=None,
+                         stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+        y = torch.empty_like(x) if out is None else out
+        ro = torch.empty_like(residual) if residual_out is None else residual_out
+        T, H = x.shape
+        self._call("tri_residual_rmsnorm", _dll.tri_residual_rmsnorm, dtype_code(x.dtype),
+                   x.data_ptr(), _rows(x, "x"), residual.data_ptr(), _rows(residual, "residual"),
+                   w.data_ptr(), y.data_ptr(), _rows(y, "out"), ro.data_ptr(),
+                   _rows(ro, "residual_out"), T, H, eps, _stream_ptr(stream))
+        return y, ro
+
+    def rope_qk(self, q, k, pos, base: float = 10000.0, stream=None):
+        """In-place RoPE of q [T, nq, hd] and k [T, nk, hd] (k may be None)."""
+        T, nq, hd = q.shape
+        nk = 0 if k is None else k.shape[1]
+        kp = 0 if k is None or nk == 0 else k.data_ptr()
+        kts = 0 if k is None or nk == 0 else _tokens(k, "k")
+        if pos.dtype != torch.int32:
+            raise TypeError("pos must be int32")
+        self._call("tri_rope_qk", _dll.tri_rope_qk, dtype_code(q.dtype), q.data_ptr(),
+                   _tokens(q, "q"), kp, kts, pos.data_ptr(), T, nq, nk, hd, base,
+                   _stream_ptr(stream))
+        return q, k
+
+    def swiglu(self, gate, up, out=None, stream=None) -> torch.Tensor:
+        o = torch.empty_like(gate) if out is None else out
+        T, I = gate.shape
+        self._call("tri_swiglu", _dll.tri_swiglu, dtype_code(gate.dtype), gate.data_ptr(),
+                   _rows(gate, "gate"), up.data_ptr(), _rows(up, "up"), o.data_ptr(),
+                   _rows(o, "out"), T, I, _stream_ptr(stream))
+        return o
+
+    def chain_args(self, x, residual, w, q, k, pos, gate, up, eps=1e-6, base=10000.0,
+                   y=None, residual_out=None, out=None) -> Tuple[ChainArgs, tuple]:
+        """Build the tri_chain_args struct once (outputs allocated if absent)."""
+        y = torch.empty_like(x) if y is None else y
+        ro = torch.empty_like(residual) if residual_out is None else residual_out
+        o = torch.empty_like(gate) if out is None else out
+        T, H = x.shape
+        a = ChainArgs()
+        a.dtype = dtype_code(x.dtype)
+        a.nq, a.hd = q.shape[1], q.shape[2]
+        a.nk = 0 if k is None else k.shape[1]
+        a.T, a.H, a.I = T, H, gate.shape[1]
+        a.eps, a.base = eps, base
+        a.x, a.x_rs = x.data_ptr(), _rows(x, "x")
+        a.res, a.res_rs = residual.data_ptr(), _rows(residual, "residual")
+        a.w = w.data_ptr()
+        a.y, a.y_rs = y.data_ptr(), _rows(y, "y")
+        a.res_out, a.ro_rs = ro.data_ptr(), _rows(ro, "residual_out")
+        a.q, a.q_ts = q.data_ptr(), _tokens(q, "q")
+        if a.nk:
+            a.k, a.k_ts = k.data_ptr(), _tokens(k, "k")
+        a.pos = pos.data_ptr()
+        a.gate, a.g_rs = gate.data_ptr(), _rows(gate, "gate")
+        a.up, a.u_rs = up.data_ptr(), _rows(up, "up")
+        a.out, a.o_rs = o.data_ptr(), _rows(o, "out")
+        return a, (y, ro, o)
+
+    def decode_chain_args(self, args: ChainArgs, stream=None) -> None:
+        self._call("tri_decode_chain", _dll.tri_decode_chain, C.byref(args),
+                   _stream_ptr(stream))
+
+    def decode_chain(self, x, residual, w, q, k, pos, gate, up, eps=1e-6, base=10000.0,
+                     y=None, residual_out=None, out=None, stream=None):
+        """Residual+RMSNorm, in-place RoPE of q/k and SwiGLU in one entry call.
+        Returns (y, residual_out, out)."""
+        a, outs = self.chain_args(x, residual, w, q, k, pos, gate, up, eps, base, y,
+                                  residual_out, out)
+        self.decode_chain_args(a, stream)
+        return outs
+
+    def launch_empty(self, stream=None) -> None:
+        st = _dll.tri_launch_empty(self._h, _stream_ptr(stream))
+        if st != OK:
+            raise TriError(st, "tri_launch_empty")
+
+    # ---- introspection -------------------------------------------------------
+    def last_selection(self) -> Selection:
+        s = Selection()
+        _dll.tri_spec_last_selection(self._h, C.byref(s))
+        return s
+
+    def stats(self) -> dict:
+        s = Stats()
+        _dll.tri_spec_stats(self._h, C.byref(s))
+        return s.as_dict()
+
+    def version_info(self, i: int) -> VersionInfo:
+        v = VersionInfo()
+        st = _dll.tri_spec_version_info(self._h, i, C.byref(v))
+        if st != OK:
+            raise TriError(st, "tri_spec_version_info")
+        return v
+
+    def version_constants(self, i: int):
+        n = C.c_uint32()
+        buf = (C.c_float * 256)()
+        st = _dll.tri_spec_version_constants(self._h, i, buf, 256, C.byref(n))
+        if st != OK:
+            raise TriError(st, "tri_spec_version_constants")
+        return list(buf[: n.value])

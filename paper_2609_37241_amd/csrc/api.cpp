@@ -1,0 +1,390 @@
+// The op entry points: the cache-hit path.
+//
+// One call = validate arguments -> pack the guard key -> ordered lookup
+// (Algorithm 1, Sec. 3.2) -> fill the kernel's argument block -> launch the
+// version's resolved kernel on the caller's stream (Sec. 3.3: the launch
+// preconditions are checked right before submission). Nothing on this path
+// allocates, logs, or queries the runtime. A miss returns TRI_MISS with
+// nothing launched; an error returns a negative status, tries no other
+// version and installs nothing (Sec. 3.5).
+#include <math.h>
+#include <string.h>
+
+#include "internal.h"
+#include "kernargs.h"
+
+using namespace tri;
+
+namespace {
+
+enum { kGo = 2 };   // validation passed, continue (distinct from every status)
+
+inline uint64_t es_of(uint32_t dtype) { return dtype == TRI_F32 ? 4u : 2u; }
+inline uint64_t addr(const void *p) { return uint64_t(uintptr_t(p)); }
+
+// Status of a call that ended before lookup: T == 0 (OK) or an error.
+tri_status finish_early(tri_cache *c, uint32_t op, int st) {
+  if (st == TRI_OK)
+    c->stats.empty++;
+  else
+    c->stats.errors++;
+  tri_selection &r = c->last;
+  memset(&r, 0, sizeof r);
+  r.op = int32_t(op);
+  r.status = st;
+  r.version = -1;
+  return tri_status(st);
+}
+
+inline int check_common(int32_t dtype, int64_t T) {
+  if (dtype != TRI_F32 && dtype != TRI_BF16) return TRI_E_INVALID;
+  if (T < 0) return TRI_E_INVALID;
+  if (T == 0) return TRI_OK;
+  if (T > kTMax) return TRI_E_UNSUPPORTED;
+  return kGo;
+}
+
+// Norm rows: H range, non-null and element-aligned pointers, strides >= H,
+// finite non-negative eps.
+inline int check_norm(uint64_t es, int64_t H, const void *const *ptrs, int np,
+                      const int64_t *strides, int ns, float eps) {
+  if (H < 1) return TRI_E_INVALID;
+  if (H >= kHLimit) return TRI_E_UNSUPPORTED;
+  for (int i = 0; i < np; ++i)
+    if (!ptrs[i]) return TRI_E_INVALID;
+  for (int i = 0; i < np; ++i)
+    if (addr(ptrs[i]) % es) return TRI_E_INVALID;
+  for (int i = 0; i < ns; ++i)
+    if (strides[i] < H) return TRI_E_INVALID;
+  if (!isfinite(eps) || eps < 0.0f) return TRI_E_INVALID;
+  return kGo;
+}
+
+inline int check_rope(uint64_t es, const void *q, int64_t q_ts, const void *k, int64_t k_ts,
+                      const int32_t *pos, int32_t nq, int32_t nk, int32_t hd, float base) {
+  if (hd < 2 || (hd & 1)) return TRI_E_INVALID;
+  if (hd > kHdMax) return TRI_E_UNSUPPORTED;
+  if (nq < 1 || nk < 0) return TRI_E_INVALID;
+  if (nq > kHeadsMax || nk > kHeadsMax) return TRI_E_UNSUPPORTED;
+  if (!q || !pos || (nk > 0 && !k)) return TRI_E_INVALID;
+  if (addr(pos) % 4) return TRI_E_INVALID;
+  if (addr(q) % es || (nk > 0 && addr(k) % es)) return TRI_E_INVALID;
+  if (q_ts < int64_t(nq) * hd) return TRI_E_INVALID;
+  if (nk > 0 && k_ts < int64_t(nk) * hd) return TRI_E_INVALID;
+  if (!isfinite(base) || base <= 1.0f) return TRI_E_INVALID;
+  return kGo;
+}
+
+inline int check_sw(uint64_t es, int64_t I, const void *g, int64_t g_rs, const void *u,
+                    int64_t u_rs, const void *o, int64_t o_rs) {
+  if (I < 1) return TRI_E_INVALID;
+  if (I >= kILimit) return TRI_E_UNSUPPORTED;
+  if (!g || !u || !o) return TRI_E_INVALID;
+  if ((addr(g) | addr(u) | addr(o)) % es) return TRI_E_INVALID;
+  if (g_rs < I || u_rs < I || o_rs < I) return TRI_E_INVALID;
+  return kGo;
+}
+
+// ---- guard flags --------------------------------------------------------------
+inline unsigned flags_of(uint64_t or_bits, bool contig) {
+  return ((or_bits & 15u) == 0 ? kAlign : 0u) | (contig ? kContig : 0u);
+}
+
+inline unsigned rn_flags(uint64_t es, const void *x, int64_t x_rs, const void *w, const void *y,
+                         int64_t y_rs, int64_t H) {
+  const uint64_t o = addr(x) | addr(w) | addr(y) | uint64_t(x_rs) * es | uint64_t(y_rs) * es;
+  return flags_of(o, x_rs == H && y_rs == H);
+}
+
+inline unsigned res_flags(uint64_t es, const void *x, int64_t x_rs, const void *r, int64_t r_rs,
+                          const void *w, const void *y, int64_t y_rs, const void *ro,
+                          int64_t ro_rs, int64_t H) {
+  const uint64_t o = addr(x) | addr(r) | addr(w) | addr(y) | addr(ro) | uint64_t(x_rs) * es |
+                     uint64_t(r_rs) * es | uint64_t(y_rs) * es | uint64_t(ro_rs) * es;
+  return flags_of(o, x_rs == H && r_rs == H && y_rs == H && ro_rs == H);
+}
+
+inline unsigned rope_flags(uint64_t es, const void *q, int64_t q_ts, const void *k, int64_t k_ts,
+                           int32_t nq, int32_t nk, int32_t hd) {
+  uint64_t o = addr(q) | uint64_t(q_ts) * es;
+  bool contig = q_ts == int64_t(nq) * hd;
+  if (nk > 0) {
+    o |= addr(k) | uint64_t(k_ts) * es;
+    contig = contig && k_ts == int64_t(nk) * hd;
+  }
+  return flags_of(o, contig);
+}
+
+inline unsigned sw_flags(uint64_t es, const void *g, int64_t g_rs, const void *u, int64_t u_rs,
+                         const void *o, int64_t o_rs, int64_t I) {
+  const uint64_t b = addr(g) | addr(u) | addr(o) | uint64_t(g_rs) * es | uint64_t(u_rs) * es |
+                     uint64_t(o_rs) * es;
+  return flags_of(b, g_rs == I && u_rs == I && o_rs == I);
+}
+
+inline uint32_t f32_bits(float f) {
+  uint32_t b;
+  memcpy(&b, &f, sizeof b);
+  return b;
+}
+
+inline Key make_key(uint32_t op, uint32_t dtype, int64_t T, unsigned flags, uint32_t base_bits,
+                    uint64_t H, uint64_t I, uint64_t hd, uint64_t nq, uint64_t nk) {
+  Key k;
+  k.k0 = uint64_t(op) | (uint64_t(dtype) << 8) | (uint64_t(token_bucket(T)) << 16) |
+         (uint64_t(flags) << 24) | (uint64_t(base_bits) << 32);
+  k.k1 = H | (I << 32);
+  k.k2 = hd | (nq << 16) | (nk << 32);
+  return k;
+}
+
+// ---- lookup and launch bookkeeping -----------------------------------------------------
+// Finds the version for `k`. On a miss records it and, with auto-install,
+// installs and returns the new version (*auto_inst = true).
+inline int lookup(tri_cache *c, uint32_t op, const Key &k, int64_t T, int32_t *vi,
+                  bool *auto_inst) {
+  int32_t i = find_version(c, op, k);
+  if (i >= 0) {
+    *vi = i;
+    return TRI_OK;
+  }
+  c->stats.misses++;
+  c->has_miss = true;
+  c->miss_key = k;
+  c->miss_T = T;
+  tri_selection &r = c->last;
+  memset(&r, 0, sizeof r);
+  r.op = int32_t(op);
+  r.version = -1;
+  r.key[0] = k.k0;
+  r.key[1] = k.k1;
+  r.key[2] = k.k2;
+  if (!(c->flags & TRI_CACHE_AUTO_INSTALL)) {
+    r.status = TRI_MISS;
+    return TRI_MISS;
+  }
+  const tri_status st = install_key(c, k);
+  if (st != TRI_OK) {
+    r.status = st;
+    return st;
+  }
+  *vi = find_version(c, op, k);
+  *auto_inst = true;
+  return TRI_OK;
+}
+
+inline void record(tri_cache *c, uint32_t op, const Version &v, int32_t vi, const Key &k,
+                   int n, const tri_launch_rec *l, int st) {
+  tri_selection &r = c->last;
+  r.op = int32_t(op);
+  r.status = st;
+  r.version = vi;
+  r.variant = v.plan.variant;
+  r.n_launches = n;
+  r.roles[0] = v.plan.roles[0];
+  r.roles[1] = v.plan.roles[1];
+  r.roles[2] = v.plan.roles[2];
+  for (int i = 0; i < 3; ++i) r.launch[i] = i < n ? l[i] : tri_launch_rec{0, 0, 0};
+  r.key[0] = k.k0;
+  r.key[1] = k.k1;
+  r.key[2] = k.k2;
+}
+
+inline tri_status finish(tri_cache *c, Version &v, bool auto_inst, int rc) {
+  if (rc != 0) {
+    if (!auto_inst) c->stats.errors++;
+    return TRI_E_LAUNCH;
+  }
+  if (!auto_inst) {
+    c->stats.hits++;
+    v.hits++;
+  }
+  return TRI_OK;
+}
+
+inline int64_t vec_elems(uint32_t dtype) { return dtype == TRI_F32 ? 4 : 8; }
+
+}  // namespace
+
+extern "C" {
+
+tri_status tri_rmsnorm(tri_cache *c, tri_dtype dtype, const void *x, int64_t x_rs,
+                       const void *w, void *y, int64_t y_rs, int64_t T, int64_t H, float eps,
+                       void *stream) {
+  if (!c) return TRI_E_INVALID;
+  const uint32_t op = TRI_OP_RMSNORM;
+  c->stats.calls++;
+  int st = check_common(dtype, T);
+  if (st != kGo) return finish_early(c, op, st);
+  const uint64_t es = es_of(dtype);
+  const void *ptrs[3] = {x, w, y};
+  const int64_t strides[2] = {x_rs, y_rs};
+  st = check_norm(es, H, ptrs, 3, strides, 2, eps);
+  if (st != kGo) return finish_early(c, op, st);
+
+  const Key k = make_key(op, dtype, T, rn_flags(es, x, x_rs, w, y, y_rs, H), 0, uint64_t(H), 0,
+                         0, 0, 0);
+  int32_t vi;
+  bool auto_inst = false;
+  st = lookup(c, op, k, T, &vi, &auto_inst);
+  if (st != TRI_OK) return tri_status(st);
+  Version &v = c->versions[vi];
+
+  RnArgs a{x, nullptr, w, y, nullptr, x_rs, 0, y_rs, 0, T, int32_t(H), eps};
+  const tri_launch_rec l{v.plan.kvariant[0], role_grid(v.plan.kvariant[0], dtype, T, 0), kBlock};
+  const int rc = be_launch(v.fn[0], l.grid_x, kBlock, &a, stream);
+  record(c, op, v, vi, k, 1, &l, rc ? TRI_E_LAUNCH : TRI_OK);
+  return finish(c, v, auto_inst, rc);
+}
+
+tri_status tri_residual_rmsnorm(tri_cache *c, tri_dtype dtype, const void *x, int64_t x_rs,
+                                const void *res, int64_t res_rs, const void *w, void *y,
+                                int64_t y_rs, void *res_out, int64_t ro_rs, int64_t T, int64_t H,
+                                float eps, void *stream) {
+  if (!c) return TRI_E_INVALID;
+  const uint32_t op = TRI_OP_RES_RMSNORM;
+  c->stats.calls++;
+  int st = check_common(dtype, T);
+  if (st != kGo) return finish_early(c, op, st);
+  const uint64_t es = es_of(dtype);
+  const void *ptrs[5] = {x, res, w, y, res_out};
+  const int64_t strides[4] = {x_rs, res_rs, y_rs, ro_rs};
+  st = check_norm(es, H, ptrs, 5, strides, 4, eps);
+  if (st != kGo) return finish_early(c, op, st);
+
+  const Key k = make_key(op, dtype, T,
+                         res_flags(es, x, x_rs, res, res_rs, w, y, y_rs, res_out, ro_rs, H), 0,
+                         uint64_t(H), 0, 0, 0, 0);
+  int32_t vi;
+  bool auto_inst = false;
+  st = lookup(c, op, k, T, &vi, &auto_inst);
+  if (st != TRI_OK) return tri_status(st);
+  Version &v = c->versions[vi];
+
+  RnArgs a{x, res, w, y, res_out, x_rs, res_rs, y_rs, ro_rs, T, int32_t(H), eps};
+  const tri_launch_rec l{v.plan.kvariant[0], role_grid(v.plan.kvariant[0], dtype, T, 0), kBlock};
+  const int rc = be_launch(v.fn[0], l.grid_x, kBlock, &a, stream);
+  record(c, op, v, vi, k, 1, &l, rc ? TRI_E_LAUNCH : TRI_OK);
+  return finish(c, v, auto_inst, rc);
+}
+
+tri_status tri_rope_qk(tri_cache *c, tri_dtype dtype, void *q, int64_t q_ts, void *kp,
+                       int64_t k_ts, const int32_t *pos, int64_t T, int32_t nq, int32_t nk,
+                       int32_t hd, float base, void *stream) {
+  if (!c) return TRI_E_INVALID;
+  const uint32_t op = TRI_OP_ROPE_QK;
+  c->stats.calls++;
+  int st = check_common(dtype, T);
+  if (st != kGo) return finish_early(c, op, st);
+  const uint64_t es = es_of(dtype);
+  st = check_rope(es, q, q_ts, kp, k_ts, pos, nq, nk, hd, base);
+  if (st != kGo) return finish_early(c, op, st);
+
+  const Key k = make_key(op, dtype, T, rope_flags(es, q, q_ts, kp, k_ts, nq, nk, hd),
+                         f32_bits(base), 0, 0, uint64_t(hd), uint64_t(nq), uint64_t(nk));
+  int32_t vi;
+  bool auto_inst = false;
+  st = lookup(c, op, k, T, &vi, &auto_inst);
+  if (st != TRI_OK) return tri_status(st);
+  Version &v = c->versions[vi];
+
+  RopeArgs a{q, nk > 0 ? kp : nullptr, pos, v.d_consts, q_ts, k_ts, T, nq, nk, hd, 0};
+  const tri_launch_rec l{v.plan.kvariant[0], role_grid(v.plan.kvariant[0], dtype, T, 0), kBlock};
+  const int rc = be_launch(v.fn[0], l.grid_x, kBlock, &a, stream);
+  record(c, op, v, vi, k, 1, &l, rc ? TRI_E_LAUNCH : TRI_OK);
+  return finish(c, v, auto_inst, rc);
+}
+
+tri_status tri_swiglu(tri_cache *c, tri_dtype dtype, const void *gate, int64_t g_rs,
+                      const void *up, int64_t u_rs, void *out, int64_t o_rs, int64_t T, int64_t I,
+                      void *stream) {
+  if (!c) return TRI_E_INVALID;
+  const uint32_t op = TRI_OP_SWIGLU;
+  c->stats.calls++;
+  int st = check_common(dtype, T);
+  if (st != kGo) return finish_early(c, op, st);
+  const uint64_t es = es_of(dtype);
+  st = check_sw(es, I, gate, g_rs, up, u_rs, out, o_rs);
+  if (st != kGo) return finish_early(c, op, st);
+
+  const Key k = make_key(op, dtype, T, sw_flags(es, gate, g_rs, up, u_rs, out, o_rs, I), 0, 0,
+                         uint64_t(I), 0, 0, 0);
+  int32_t vi;
+  bool auto_inst = false;
+  st = lookup(c, op, k, T, &vi, &auto_inst);
+  if (st != TRI_OK) return tri_status(st);
+  Version &v = c->versions[vi];
+
+  SwArgs a{gate, up, out, g_rs, u_rs, o_rs, T, I, (T * I) / vec_elems(dtype), T * I};
+  const tri_launch_rec l{v.plan.kvariant[0], role_grid(v.plan.kvariant[0], dtype, T, I), kBlock};
+  const int rc = be_launch(v.fn[0], l.grid_x, kBlock, &a, stream);
+  record(c, op, v, vi, k, 1, &l, rc ? TRI_E_LAUNCH : TRI_OK);
+  return finish(c, v, auto_inst, rc);
+}
+
+tri_status tri_decode_chain(tri_cache *c, const tri_chain_args *p, void *stream) {
+  if (!c) return TRI_E_INVALID;
+  const uint32_t op = TRI_OP_CHAIN;
+  c->stats.calls++;
+  if (!p) return finish_early(c, op, TRI_E_INVALID);
+  const int32_t dtype = p->dtype;
+  const int64_t T = p->T, H = p->H, I = p->I;
+  int st = check_common(dtype, T);
+  if (st != kGo) return finish_early(c, op, st);
+  const uint64_t es = es_of(uint32_t(dtype));
+  {
+    const void *ptrs[5] = {p->x, p->res, p->w, p->y, p->res_out};
+    const int64_t strides[4] = {p->x_rs, p->res_rs, p->y_rs, p->ro_rs};
+    st = check_norm(es, H, ptrs, 5, strides, 4, p->eps);
+    if (st != kGo) return finish_early(c, op, st);
+  }
+  st = check_rope(es, p->q, p->q_ts, p->k, p->k_ts, p->pos, p->nq, p->nk, p->hd, p->base);
+  if (st != kGo) return finish_early(c, op, st);
+  st = check_sw(es, I, p->gate, p->g_rs, p->up, p->u_rs, p->out, p->o_rs);
+  if (st != kGo) return finish_early(c, op, st);
+
+  const unsigned fl =
+      res_flags(es, p->x, p->x_rs, p->res, p->res_rs, p->w, p->y, p->y_rs, p->res_out, p->ro_rs,
+                H) |
+      (rope_flags(es, p->q, p->q_ts, p->k, p->k_ts, p->nq, p->nk, p->hd) << 2) |
+      (sw_flags(es, p->gate, p->g_rs, p->up, p->u_rs, p->out, p->o_rs, I) << 4);
+  const Key k = make_key(op, uint32_t(dtype), T, fl, f32_bits(p->base), uint64_t(H), uint64_t(I),
+                         uint64_t(p->hd), uint64_t(p->nq), uint64_t(p->nk));
+  int32_t vi;
+  bool auto_inst = false;
+  st = lookup(c, op, k, T, &vi, &auto_inst);
+  if (st != TRI_OK) return tri_status(st);
+  Version &v = c->versions[vi];
+
+  const RnArgs rn{p->x, p->res, p->w, p->y, p->res_out, p->x_rs, p->res_rs, p->y_rs, p->ro_rs,
+                  T, int32_t(H), p->eps};
+  const RopeArgs ro{p->q, p->nk > 0 ? p->k : nullptr, p->pos, v.d_consts, p->q_ts, p->k_ts, T,
+                    p->nq, p->nk, p->hd, 0};
+  const SwArgs sw{p->gate, p->up, p->out, p->g_rs, p->u_rs, p->o_rs, T, I,
+                  (T * I) / vec_elems(uint32_t(dtype)), T * I};
+  const uint32_t g0 = role_grid(v.plan.roles[0], uint32_t(dtype), T, I);
+  const uint32_t g1 = role_grid(v.plan.roles[1], uint32_t(dtype), T, I);
+  const uint32_t g2 = role_grid(v.plan.roles[2], uint32_t(dtype), T, I);
+
+  if (v.plan.variant == CH_FUSED) {
+    ChainArgs a{rn, ro, sw, g0, g1};
+    const tri_launch_rec l{CH_FUSED, g0 + g1 + g2, kBlock};
+    const int rc = be_launch(v.fn[0], l.grid_x, kBlock, &a, stream);
+    record(c, op, v, vi, k, 1, &l, rc ? TRI_E_LAUNCH : TRI_OK);
+    return finish(c, v, auto_inst, rc);
+  }
+  // Three launches: the residual norm, RoPE and SwiGLU role kernels.
+  RnArgs a0 = rn;
+  RopeArgs a1 = ro;
+  SwArgs a2 = sw;
+  void *args[3] = {&a0, &a1, &a2};
+  const tri_launch_rec l[3] = {{v.plan.kvariant[0], g0, kBlock},
+                               {v.plan.kvariant[1], g1, kBlock},
+                               {v.plan.kvariant[2], g2, kBlock}};
+  int rc = 0;
+  for (int i = 0; i < 3 && rc == 0; ++i) rc = be_launch(v.fn[i], l[i].grid_x, kBlock, args[i], stream);
+  record(c, op, v, vi, k, 3, l, rc ? TRI_E_LAUNCH : TRI_OK);
+  return finish(c, v, auto_inst, rc);
+}
+
+}  // extern "C"

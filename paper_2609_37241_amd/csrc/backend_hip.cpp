@@ -1,0 +1,68 @@
+// HIP launch backend.
+//
+// Kernels are compiled into this library for gfx950. At install a version's
+// kernels are resolved once to hipFunction_t handles (hipGetFuncBySymbol);
+// each hit is a single hipModuleLaunchKernel of that handle with a pointer to
+// the argument block on the caller's stream -- no symbol lookup, no
+// per-argument marshalling, no device query on the hit path.
+#include <hip/hip_runtime.h>
+
+#include "internal.h"
+
+namespace tri {
+
+const void *rn_kernel(int32_t variant, uint32_t dtype, int32_t res);
+const void *rope_kernel(int32_t variant, uint32_t dtype);
+const void *sw_kernel(int32_t variant, uint32_t dtype);
+const void *chain_kernel_f32(int32_t sub);
+const void *chain_kernel_bf16(int32_t sub);
+const void *empty_kernel();
+
+int be_init(int *device) {
+  int n = 0;
+  if (hipGetDeviceCount(&n) != hipSuccess || n < 1) return TRI_E_RUNTIME;
+  if (hipGetDevice(device) != hipSuccess) return TRI_E_RUNTIME;
+  return 0;
+}
+
+int be_resolve(int32_t kvariant, uint32_t dtype, int32_t ksub, void **fn) {
+  const void *sym = nullptr;
+  if (kvariant >= RN_SCALAR && kvariant <= RN_LOOP)
+    sym = rn_kernel(kvariant, dtype, ksub);
+  else if (kvariant >= ROPE_SCALAR && kvariant <= ROPE_VEC_T4)
+    sym = rope_kernel(kvariant, dtype);
+  else if (kvariant >= SW_SCALAR && kvariant <= SW_ROWS)
+    sym = sw_kernel(kvariant, dtype);
+  else if (kvariant == CH_FUSED)
+    sym = dtype == TRI_F32 ? chain_kernel_f32(ksub) : chain_kernel_bf16(ksub);
+  else if (kvariant == EMPTY)
+    sym = empty_kernel();
+  if (!sym) return TRI_E_RUNTIME;
+  hipFunction_t f = nullptr;
+  if (hipGetFuncBySymbol(&f, sym) != hipSuccess || !f) return TRI_E_RUNTIME;
+  *fn = reinterpret_cast<void *>(f);
+  return 0;
+}
+
+int be_launch(void *fn, uint32_t grid, uint32_t block, void *args, void *stream) {
+  void *params[1] = {args};
+  const hipError_t e =
+      hipModuleLaunchKernel(reinterpret_cast<hipFunction_t>(fn), grid, 1, 1, block, 1, 1, 0,
+                            reinterpret_cast<hipStream_t>(stream), args ? params : nullptr, nullptr);
+  return e == hipSuccess ? 0 : -1;
+}
+
+int be_upload(const void *host, uint64_t bytes, void **dev) {
+  void *p = nullptr;
+  if (hipMalloc(&p, bytes) != hipSuccess) return TRI_E_NOMEM;
+  if (hipMemcpy(p, host, bytes, hipMemcpyHostToDevice) != hipSuccess) {
+    (void)hipFree(p);
+    return TRI_E_RUNTIME;
+  }
+  *dev = p;
+  return 0;
+}
+
+void be_free(void *dev) { (void)hipFree(dev); }
+
+}  // namespace tri

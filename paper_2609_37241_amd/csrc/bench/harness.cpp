@@ -1,0 +1,68 @@
+// Native timing loops for the benchmark: per-call latency with no Python
+// between the clock reads and the entry call.
+//
+// E2E latency of one call = steady_clock around {entry call; stream sync};
+// host latency = the clock read right after the entry call returns. The
+// empty-kernel yardstick runs the identical loop around tri_launch_empty.
+#include <hip/hip_runtime.h>
+
+#include <chrono>
+
+#include "tri.h"
+
+namespace {
+
+using Clock = std::chrono::steady_clock;
+
+inline double us_between(Clock::time_point a, Clock::time_point b) {
+  return std::chrono::duration<double, std::micro>(b - a).count();
+}
+
+// mode 0: tri_decode_chain(args); mode 1: tri_launch_empty.
+inline int one_call(tri_cache *c, int mode, const tri_chain_args *args, void *stream) {
+  return mode == 0 ? int(tri_decode_chain(c, args, stream)) : int(tri_launch_empty(c, stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+// n_warm untimed calls, then n timed calls, each synchronised. Writes n
+// samples to e2e_us and host_us. Returns 0, or the first failing status.
+int trib_latency(tri_cache *c, int mode, const tri_chain_args *args, void *stream, int n_warm,
+                 int n, double *e2e_us, double *host_us) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  for (int i = 0; i < n_warm; ++i) {
+    const int st = one_call(c, mode, args, stream);
+    if (st != 0) return st;
+    if (hipStreamSynchronize(s) != hipSuccess) return TRI_E_RUNTIME;
+  }
+  for (int i = 0; i < n; ++i) {
+    const Clock::time_point t0 = Clock::now();
+    const int st = one_call(c, mode, args, stream);
+    const Clock::time_point t1 = Clock::now();
+    if (hipStreamSynchronize(s) != hipSuccess) return TRI_E_RUNTIME;
+    const Clock::time_point t2 = Clock::now();
+    if (st != 0) return st;
+    e2e_us[i] = us_between(t0, t2);
+    host_us[i] = us_between(t0, t1);
+  }
+  return 0;
+}
+
+// n back-to-back calls and one synchronisation: the pipelined issue rate.
+int trib_issue(tri_cache *c, int mode, const tri_chain_args *args, void *stream, int n,
+               double *total_us) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (hipStreamSynchronize(s) != hipSuccess) return TRI_E_RUNTIME;
+  const Clock::time_point t0 = Clock::now();
+  for (int i = 0; i < n; ++i) {
+    const int st = one_call(c, mode, args, stream);
+    if (st != 0) return st;
+  }
+  if (hipStreamSynchronize(s) != hipSuccess) return TRI_E_RUNTIME;
+  *total_us = us_between(t0, Clock::now());
+  return 0;
+}
+
+}  // extern "C"

@@ -1,0 +1,221 @@
+// The specialization cache: ordered versions, lookup, install on miss,
+// counters and introspection.
+//
+// Versions are kept in creation order and looked up with the first-match
+// rule of the paper's ordered dispatch (Algorithm 1, Sec. 3.2). Guards are
+// equality tests on a packed key and install is idempotent, so at most one
+// version matches a key; checking the op's last hit before the ordered scan
+// therefore returns exactly the version the scan would.
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include "internal.h"
+
+namespace tri {
+
+int32_t find_version(tri_cache *c, uint32_t op, const Key &k) {
+  const int32_t h = c->last_hit[op];
+  if (h >= 0 && c->versions[h].key == k) return h;
+  const uint32_t n = c->n_versions;
+  for (uint32_t i = 0; i < n; ++i) {
+    if (c->versions[i].key == k) {
+      c->last_hit[op] = int32_t(i);
+      return int32_t(i);
+    }
+  }
+  return -1;
+}
+
+namespace {
+
+// inv_i = the float32 nearest to base^(-2i/hd). The power is taken in x87
+// extended precision (64-bit significand) and rounded once to float32.
+void rope_inverse_frequencies(float base, uint32_t hd, float *out) {
+  const long double b = (long double)base;
+  for (uint32_t i = 0; i < hd / 2; ++i) {
+    const long double e = -2.0L * (long double)i / (long double)hd;
+    out[i] = (float)powl(b, e);
+  }
+}
+
+}  // namespace
+
+tri_status install_key(tri_cache *c, const Key &k) {
+  for (uint32_t i = 0; i < c->n_versions; ++i)
+    if (c->versions[i].key == k) return TRI_OK;          // idempotent
+  if (c->n_versions >= c->capacity) return TRI_E_FULL;
+
+  Version v;
+  memset(&v, 0, sizeof v);
+  v.key = k;
+  v.plan = plan_for_key(k);
+  const uint32_t dt = key_dtype(k);
+  for (int i = 0; i < v.plan.n_launches; ++i) {
+    const int st = be_resolve(v.plan.kvariant[i], dt, v.plan.ksub[i], &v.fn[i]);
+    if (st != 0) return tri_status(st);
+  }
+  const uint32_t op = key_op(k);
+  if (op == TRI_OP_ROPE_QK || op == TRI_OP_CHAIN) {
+    const uint32_t hd = key_hd(k);
+    float base;
+    const uint32_t bits = key_base_bits(k);
+    memcpy(&base, &bits, sizeof base);
+    v.n_consts = hd / 2;
+    v.h_consts = static_cast<float *>(malloc(sizeof(float) * v.n_consts));
+    if (!v.h_consts) return TRI_E_NOMEM;
+    rope_inverse_frequencies(base, hd, v.h_consts);
+    void *dev = nullptr;
+    const int st = be_upload(v.h_consts, sizeof(float) * v.n_consts, &dev);
+    if (st != 0) {
+      free(v.h_consts);
+      return tri_status(st);
+    }
+    v.d_consts = static_cast<float *>(dev);
+  }
+  c->versions[c->n_versions++] = v;
+  c->stats.installs++;
+  c->stats.n_versions = c->n_versions;
+  return TRI_OK;
+}
+
+void fill_selection(const Version &v, int32_t index, int64_t T, tri_selection *out) {
+  const Key &k = v.key;
+  const uint32_t dt = key_dtype(k);
+  const int64_t I = key_I(k);
+  memset(out, 0, sizeof *out);
+  out->op = int32_t(key_op(k));
+  out->status = TRI_OK;
+  out->version = index;
+  out->variant = v.plan.variant;
+  out->n_launches = v.plan.n_launches;
+  for (int i = 0; i < 3; ++i) out->roles[i] = v.plan.roles[i];
+  if (v.plan.variant == CH_FUSED) {
+    const uint32_t g = role_grid(v.plan.roles[0], dt, T, I) + role_grid(v.plan.roles[1], dt, T, I) +
+                       role_grid(v.plan.roles[2], dt, T, I);
+    out->launch[0] = {CH_FUSED, g, kBlock};
+  } else {
+    for (int i = 0; i < v.plan.n_launches; ++i)
+      out->launch[i] = {v.plan.kvariant[i], role_grid(v.plan.kvariant[i], dt, T, I), kBlock};
+  }
+  out->key[0] = k.k0;
+  out->key[1] = k.k1;
+  out->key[2] = k.k2;
+}
+
+}  // namespace tri
+
+using namespace tri;
+
+extern "C" {
+
+tri_status tri_spec_cache_create(tri_cache **out, uint32_t capacity, uint32_t flags) {
+  if (!out) return TRI_E_INVALID;
+  *out = nullptr;
+  if (capacity > kMaxCapacity || (flags & ~uint32_t(TRI_CACHE_AUTO_INSTALL)))
+    return TRI_E_INVALID;
+  if (capacity == 0) capacity = kDefaultCapacity;
+  int device = 0;
+  int st = be_init(&device);
+  if (st != 0) return tri_status(st);
+  tri_cache *c = static_cast<tri_cache *>(calloc(1, sizeof(tri_cache)));
+  if (!c) return TRI_E_NOMEM;
+  c->versions = static_cast<Version *>(calloc(capacity, sizeof(Version)));
+  if (!c->versions) {
+    free(c);
+    return TRI_E_NOMEM;
+  }
+  st = be_resolve(EMPTY, 0, 0, &c->empty_fn);
+  if (st != 0) {
+    free(c->versions);
+    free(c);
+    return tri_status(st);
+  }
+  c->capacity = capacity;
+  c->flags = flags;
+  c->device = device;
+  for (int i = 0; i < kOps; ++i) c->last_hit[i] = -1;
+  c->stats.capacity = capacity;
+  c->last.version = -1;
+  *out = c;
+  return TRI_OK;
+}
+
+void tri_spec_cache_destroy(tri_cache *c) {
+  if (!c) return;
+  for (uint32_t i = 0; i < c->n_versions; ++i) {
+    if (c->versions[i].d_consts) be_free(c->versions[i].d_consts);
+    free(c->versions[i].h_consts);
+  }
+  free(c->versions);
+  free(c);
+}
+
+tri_status tri_spec_install_last_miss(tri_cache *c, tri_selection *out) {
+  if (!c || !c->has_miss) return TRI_E_INVALID;
+  const tri_status st = install_key(c, c->miss_key);
+  if (st != TRI_OK) return st;
+  if (out) {
+    for (uint32_t i = 0; i < c->n_versions; ++i)
+      if (c->versions[i].key == c->miss_key) {
+        fill_selection(c->versions[i], int32_t(i), c->miss_T, out);
+        break;
+      }
+  }
+  return TRI_OK;
+}
+
+tri_status tri_spec_last_selection(const tri_cache *c, tri_selection *out) {
+  if (!c || !out) return TRI_E_INVALID;
+  *out = c->last;
+  return TRI_OK;
+}
+
+tri_status tri_spec_stats(const tri_cache *c, tri_stats *out) {
+  if (!c || !out) return TRI_E_INVALID;
+  *out = c->stats;
+  return TRI_OK;
+}
+
+tri_status tri_spec_version_info(const tri_cache *c, uint32_t index, tri_version_info *out) {
+  if (!c || !out || index >= c->n_versions) return TRI_E_INVALID;
+  const Version &v = c->versions[index];
+  out->key[0] = v.key.k0;
+  out->key[1] = v.key.k1;
+  out->key[2] = v.key.k2;
+  out->variant = v.plan.variant;
+  for (int i = 0; i < 3; ++i) out->roles[i] = v.plan.roles[i];
+  out->hits = v.hits;
+  return TRI_OK;
+}
+
+tri_status tri_spec_version_constants(const tri_cache *c, uint32_t index, float *out,
+                                      uint32_t cap, uint32_t *n) {
+  if (!c || !n || index >= c->n_versions) return TRI_E_INVALID;
+  const Version &v = c->versions[index];
+  *n = v.n_consts;
+  if (v.n_consts && !out) return TRI_E_INVALID;
+  for (uint32_t i = 0; i < v.n_consts && i < cap; ++i) out[i] = v.h_consts[i];
+  return TRI_OK;
+}
+
+tri_status tri_launch_empty(tri_cache *c, void *stream) {
+  if (!c) return TRI_E_INVALID;
+  return be_launch(c->empty_fn, 1, 64, nullptr, stream) == 0 ? TRI_OK : TRI_E_LAUNCH;
+}
+
+const char *tri_status_str(int status) {
+  switch (status) {
+    case TRI_OK: return "TRI_OK";
+    case TRI_MISS: return "TRI_MISS";
+    case TRI_E_INVALID: return "TRI_E_INVALID";
+    case TRI_E_UNSUPPORTED: return "TRI_E_UNSUPPORTED";
+    case TRI_E_FULL: return "TRI_E_FULL";
+    case TRI_E_NOMEM: return "TRI_E_NOMEM";
+    case TRI_E_LAUNCH: return "TRI_E_LAUNCH";
+    case TRI_E_RUNTIME: return "TRI_E_RUNTIME";
+    default: return "TRI_UNKNOWN";
+  }
+}
+
+}  // extern "C"

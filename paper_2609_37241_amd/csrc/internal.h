@@ -1,0 +1,122 @@
+// Internals of the specialization cache: key, versions, the install policy
+// and the launch backend interface. Host-only C++; no HIP headers, so the
+// cache core also builds with a plain host compiler against a recording
+// backend for CPU tests.
+#pragma once
+#include <stdint.h>
+
+#include "tri.h"
+
+namespace tri {
+
+// ---- variant ids (the install policy table) ------------------------------------
+enum Variant : int32_t {
+  RN_SCALAR = 10, RN_WAVE_1 = 11, RN_WAVE_2 = 12, RN_WAVE_4 = 13, RN_WAVE_8 = 14,
+  RN_WAVE_16 = 15, RN_BLOCK_8 = 16, RN_BLOCK_16 = 17, RN_LOOP = 18,
+  ROPE_SCALAR = 20, ROPE_VEC_T1 = 21, ROPE_VEC_T4 = 22,
+  SW_SCALAR = 30, SW_FLAT_U1 = 31, SW_FLAT_U4 = 32, SW_ROWS = 33,
+  CH_FUSED = 50, CH_SEQ = 51,
+  EMPTY = 99,
+};
+
+constexpr uint32_t kBlock = 256;
+constexpr uint32_t kGridCap = 1u << 20;
+constexpr int64_t kTMax = int64_t(1) << 22;
+constexpr int64_t kHLimit = int64_t(1) << 24;
+constexpr int64_t kILimit = int64_t(1) << 31;
+constexpr int32_t kHdMax = 512;
+constexpr int32_t kHeadsMax = 4096;
+constexpr uint32_t kDefaultCapacity = 256;
+constexpr uint32_t kMaxCapacity = 4096;
+constexpr unsigned kAlign = 1, kContig = 2;   // per-role guard flag bits
+
+// ---- key --------------------------------------------------------------------------
+struct Key {
+  uint64_t k0, k1, k2;
+};
+inline bool operator==(const Key &a, const Key &b) {
+  return a.k0 == b.k0 && a.k1 == b.k1 && a.k2 == b.k2;
+}
+inline uint32_t key_op(const Key &k) { return uint32_t(k.k0 & 0xFF); }
+inline uint32_t key_dtype(const Key &k) { return uint32_t((k.k0 >> 8) & 0xFF); }
+inline uint32_t key_bucket(const Key &k) { return uint32_t((k.k0 >> 16) & 0xFF); }
+inline uint32_t key_flags(const Key &k) { return uint32_t((k.k0 >> 24) & 0xFF); }
+inline uint32_t key_base_bits(const Key &k) { return uint32_t(k.k0 >> 32); }
+inline uint32_t key_H(const Key &k) { return uint32_t(k.k1 & 0xFFFFFFFFu); }
+inline uint32_t key_I(const Key &k) { return uint32_t(k.k1 >> 32); }
+inline uint32_t key_hd(const Key &k) { return uint32_t(k.k2 & 0xFFFF); }
+inline uint32_t key_nq(const Key &k) { return uint32_t((k.k2 >> 16) & 0xFFFF); }
+inline uint32_t key_nk(const Key &k) { return uint32_t((k.k2 >> 32) & 0xFFFF); }
+
+// ceil(log2 T) for 1 <= T <= 2^22.
+inline uint32_t token_bucket(int64_t T) {
+  return T <= 1 ? 0u : uint32_t(64 - __builtin_clzll(uint64_t(T - 1)));
+}
+
+// ---- policy -------------------------------------------------------------------------
+// Role choice: variant + workgroups for T tokens. Pure functions of the key
+// fields they take; the per-call grid only depends on T and the sizes.
+struct Role {
+  int32_t variant;
+  uint32_t grid;
+};
+Role rn_role(uint32_t dtype, int64_t H, unsigned flags, int64_t T);
+Role rope_role(uint32_t dtype, int32_t hd, unsigned flags, uint32_t bucket, int64_t T);
+Role sw_role(uint32_t dtype, int64_t I, unsigned flags, uint32_t bucket, int64_t T);
+uint32_t role_grid(int32_t variant, uint32_t dtype, int64_t T, int64_t I);
+
+// A version's plan: which kernels it launches, fixed at install.
+struct Plan {
+  int32_t variant;        // op variant or CH_FUSED / CH_SEQ
+  int32_t roles[3];       // chain only
+  int32_t n_launches;
+  int32_t kvariant[3];    // kernel variant per launch
+  int32_t ksub[3];        // kernel sub-selector (residual flag / fused template index)
+};
+Plan plan_for_key(const Key &k);
+
+// ---- backend --------------------------------------------------------------------------
+// The launch backend. The HIP build resolves kernel handles with the runtime
+// and launches with hipModuleLaunchKernel; the CPU test build records calls.
+int be_init(int *device);                                         // 0 or tri_status
+int be_resolve(int32_t kvariant, uint32_t dtype, int32_t ksub, void **fn);
+int be_launch(void *fn, uint32_t grid, uint32_t block, void *args, void *stream);
+int be_upload(const void *host, uint64_t bytes, void **dev);      // per-version constants
+void be_free(void *dev);
+
+// ---- versions and the cache ------------------------------------------------------------
+struct Version {
+  Key key;
+  Plan plan;
+  void *fn[3];
+  float *d_consts;        // device copy of the RoPE inverse frequencies, or null
+  float *h_consts;        // host copy (hd/2 floats), or null
+  uint32_t n_consts;
+  uint64_t hits;
+};
+
+constexpr int kOps = 6;   // op ids 1..5
+
+}  // namespace tri
+
+struct tri_cache {
+  uint32_t capacity;
+  uint32_t flags;
+  int device;
+  uint32_t n_versions;
+  tri::Version *versions;
+  int32_t last_hit[tri::kOps];   // per op: version index of the last hit, -1 none
+  bool has_miss;
+  tri::Key miss_key;
+  int64_t miss_T;
+  tri_stats stats;
+  tri_selection last;
+  void *empty_fn;
+};
+
+namespace tri {
+// Cache core (cache.cpp).
+int32_t find_version(tri_cache *c, uint32_t op, const Key &k);
+tri_status install_key(tri_cache *c, const Key &k);
+void fill_selection(const Version &v, int32_t index, int64_t T, tri_selection *out);
+}  // namespace tri

@@ -1,0 +1,65 @@
+// Kernel argument blocks: one struct per kernel family, passed by value as
+// the kernel's only parameter. Host code fills them on the hit path and hands
+// a pointer to the launch; device code reads them from the kernarg segment.
+// Plain fixed-width fields only, so host (x86-64) and device (amdgcn) lay
+// them out identically; the static_asserts below pin the layout on both.
+#pragma once
+#include <stddef.h>
+#include <stdint.h>
+
+namespace tri {
+
+// Residual add + RMSNorm and plain RMSNorm ([T, H] rows, element strides).
+struct RnArgs {
+  const void *x;
+  const void *res;       // residual input (residual variants only)
+  const void *w;         // [H]
+  void *y;
+  void *res_out;         // residual output (residual variants only)
+  int64_t x_rs, res_rs, y_rs, ro_rs;
+  int64_t T;
+  int32_t H;
+  float eps;
+};
+
+// RoPE on Q [T, nq, hd] and K [T, nk, hd], in place.
+struct RopeArgs {
+  void *q;
+  void *k;
+  const int32_t *pos;
+  const float *inv_freq;  // [hd/2], the version's table
+  int64_t q_ts, k_ts;
+  int64_t T;
+  int32_t nq, nk, hd;
+  int32_t pad_;
+};
+
+// SwiGLU over [T, I].
+struct SwArgs {
+  const void *gate;
+  const void *up;
+  void *out;
+  int64_t g_rs, u_rs, o_rs;
+  int64_t T, I;
+  int64_t nvec;           // flat variants: whole 16-byte vectors in T*I
+  int64_t n;              // flat variants: T*I elements
+};
+
+// The fused decode chain: workgroups [0, rn_blocks) run residual RMSNorm rows,
+// [rn_blocks, rn_blocks + rope_blocks) RoPE tokens, the rest SwiGLU.
+struct ChainArgs {
+  RnArgs rn;
+  RopeArgs rope;
+  SwArgs sw;
+  uint32_t rn_blocks;
+  uint32_t rope_blocks;
+};
+
+static_assert(sizeof(RnArgs) == 88 && offsetof(RnArgs, T) == 72 && offsetof(RnArgs, eps) == 84,
+              "RnArgs layout");
+static_assert(sizeof(RopeArgs) == 72 && offsetof(RopeArgs, nq) == 56, "RopeArgs layout");
+static_assert(sizeof(SwArgs) == 80 && offsetof(SwArgs, n) == 72, "SwArgs layout");
+static_assert(sizeof(ChainArgs) == 248 && offsetof(ChainArgs, rn_blocks) == 240,
+              "ChainArgs layout");
+
+}  // namespace tri

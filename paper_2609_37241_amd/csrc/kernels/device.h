@@ -1,0 +1,452 @@
+// Device-side building blocks shared by the standalone kernels and the fused
+// decode-chain kernel: 16-byte packed element access, wavefront / workgroup
+// reductions, and the per-role bodies. A role body is the same inlined code
+// in both places, so the fused chain computes exactly what the three
+// separate launches compute.
+//
+// Layout conventions: every workgroup has 256 work-items (4 wavefronts of
+// 64). A "vector" is 16 bytes: 4 float32 or 8 bfloat16 elements, loaded and
+// stored with one global_load/store_dwordx4 per lane.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../kernargs.h"
+
+namespace tri {
+namespace dev {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kF32 = 0, kBF16 = 1;
+constexpr int kThreads = 256;
+
+template <int DT>
+struct Elt;
+
+template <>
+struct Elt<kF32> {
+  static constexpr int V = 4;
+  static constexpr int ES = 4;
+  __device__ static inline void unpack(const u32x4 &p, float *f) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) f[i] = __uint_as_float(p[i]);
+  }
+  __device__ static inline u32x4 pack(const float *f) {
+    u32x4 p;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) p[i] = __float_as_uint(f[i]);
+    return p;
+  }
+  __device__ static inline float ld(const void *b, int64_t i) {
+    return static_cast<const float *>(b)[i];
+  }
+  __device__ static inline void st(void *b, int64_t i, float v) { static_cast<float *>(b)[i] = v; }
+  __device__ static inline float round(float v) { return v; }
+};
+
+template <>
+struct Elt<kBF16> {
+  static constexpr int V = 8;
+  static constexpr int ES = 2;
+  // bf16 -> f32 is exact: the bf16 bits are the upper half of the f32 bits.
+  __device__ static inline void unpack(const u32x4 &p, float *f) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      f[2 * j] = __uint_as_float(p[j] << 16);
+      f[2 * j + 1] = __uint_as_float(p[j] & 0xFFFF0000u);
+    }
+  }
+  // f32 -> bf16 round-to-nearest-even, two at a time (v_cvt_pk_bf16_f32).
+  __device__ static inline uint32_t pack2(float a, float b) {
+    const f32x2 v = {a, b};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+  }
+  __device__ static inline u32x4 pack(const float *f) {
+    u32x4 p;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) p[j] = pack2(f[2 * j], f[2 * j + 1]);
+    return p;
+  }
+  __device__ static inline float ld(const void *b, int64_t i) {
+    return __uint_as_float(uint32_t(static_cast<const uint16_t *>(b)[i]) << 16);
+  }
+  __device__ static inline void st(void *b, int64_t i, float v) {
+    static_cast<uint16_t *>(b)[i] = uint16_t(pack2(v, 0.0f) & 0xFFFFu);
+  }
+  __device__ static inline float round(float v) {
+    return __uint_as_float(pack2(v, 0.0f) << 16);
+  }
+};
+
+// ---- reductions ----------------------------------------------------------------
+// Butterfly over the 64 lanes: every lane ends with the same, bitwise equal
+// total (each exchange adds the same two operands on both partners).
+template <typename T>
+__device__ inline T wave_sum(T v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// Sum over the 256 work-items of a workgroup; `red` is 4 words of LDS.
+template <typename T>
+__device__ inline T block_sum(T v, T *red) {
+  v = wave_sum(v);
+  const int wid = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) red[wid] = v;
+  __syncthreads();
+  const T s = (red[0] + red[1]) + (red[2] + red[3]);
+  __syncthreads();
+  return s;
+}
+
+// ---- RMSNorm / residual RMSNorm --------------------------------------------------
+// One row held in registers: lane `lane` of LANES owns vectors lane + LANES*k,
+// k < NV. With RES, h = RN(x + r) is written to res_out and normalised.
+// LANES = 64: one wavefront per row, no barrier. LANES = 256: one workgroup.
+template <int DT, int NV, bool RES, int LANES>
+__device__ __forceinline__ void rn_row_regs(const RnArgs &a, int64_t row, int lane, float *red) {
+  using E = Elt<DT>;
+  constexpr int V = E::V;
+  const int nvec = a.H / V;
+  const u32x4 *xr = reinterpret_cast<const u32x4 *>(static_cast<const char *>(a.x) +
+                                                     row * a.x_rs * E::ES);
+  u32x4 xv[NV];
+#pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    const int vi = lane + LANES * k;
+    xv[k] = vi < nvec ? xr[vi] : u32x4{0, 0, 0, 0};
+  }
+  if constexpr (RES) {
+    const u32x4 *rr = reinterpret_cast<const u32x4 *>(static_cast<const char *>(a.res) +
+                                                       row * a.res_rs * E::ES);
+    u32x4 rv[NV];
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+      const int vi = lane + LANES * k;
+      rv[k] = vi < nvec ? rr[vi] : u32x4{0, 0, 0, 0};
+    }
+    u32x4 *orow = reinterpret_cast<u32x4 *>(static_cast<char *>(a.res_out) + row * a.ro_rs * E::ES);
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+      float f[V], g[V];
+      E::unpack(xv[k], f);
+      E::unpack(rv[k], g);
+#pragma unroll
+      for (int e = 0; e < V; ++e) f[e] += g[e];
+      xv[k] = E::pack(f);
+      const int vi = lane + LANES * k;
+      if (vi < nvec) orow[vi] = xv[k];
+    }
+  }
+  float ss = 0.0f;
+#pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    float f[V];
+    E::unpack(xv[k], f);
+#pragma unroll
+    for (int e = 0; e < V; ++e) ss += f[e] * f[e];
+  }
+  if constexpr (LANES == 64)
+    ss = wave_sum(ss);
+  else
+    ss = block_sum(ss, red);
+  const float inv = rsqrtf(ss / float(a.H) + a.eps);
+  const u32x4 *wr = static_cast<const u32x4 *>(a.w);
+  u32x4 *yr = reinterpret_cast<u32x4 *>(static_cast<char *>(a.y) + row * a.y_rs * E::ES);
+#pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    const int vi = lane + LANES * k;
+    if (vi < nvec) {
+      float f[V], w[V];
+      E::unpack(xv[k], f);
+      E::unpack(wr[vi], w);
+#pragma unroll
+      for (int e = 0; e < V; ++e) f[e] = (f[e] * inv) * w[e];
+      yr[vi] = E::pack(f);
+    }
+  }
+}
+
+// Workgroup `blk` of the one-wavefront-per-row layout: rows 4*blk .. 4*blk+3.
+template <int DT, int NV, bool RES>
+__device__ __forceinline__ void rn_wave_block(const RnArgs &a, int64_t blk) {
+  const int64_t row = blk * 4 + (threadIdx.x >> 6);
+  if (row >= a.T) return;
+  rn_row_regs<DT, NV, RES, 64>(a, row, threadIdx.x & 63, nullptr);
+}
+
+// Long rows: two passes over global memory with float64 accumulation (each
+// thread sums up to H/256 elements, so a float32 running sum would lose
+// accuracy at the largest H). Vector form (16-byte aligned rows).
+template <int DT, bool RES>
+__device__ __forceinline__ void rn_loop_row(const RnArgs &a, int64_t row, double *red) {
+  using E = Elt<DT>;
+  constexpr int V = E::V;
+  const int nvec = a.H / V;
+  const u32x4 *xr = reinterpret_cast<const u32x4 *>(static_cast<const char *>(a.x) +
+                                                     row * a.x_rs * E::ES);
+  const u32x4 *src = xr;
+  double ss = 0.0;
+  if constexpr (RES) {
+    const u32x4 *rr = reinterpret_cast<const u32x4 *>(static_cast<const char *>(a.res) +
+                                                       row * a.res_rs * E::ES);
+    u32x4 *orow = reinterpret_cast<u32x4 *>(static_cast<char *>(a.res_out) + row * a.ro_rs * E::ES);
+    for (int vi = threadIdx.x; vi < nvec; vi += kThreads) {
+      float f[V], g[V];
+      E::unpack(xr[vi], f);
+      E::unpack(rr[vi], g);
+#pragma unroll
+      for (int e = 0; e < V; ++e) f[e] += g[e];
+      const u32x4 h = E::pack(f);
+      orow[vi] = h;
+      E::unpack(h, f);
+#pragma unroll
+      for (int e = 0; e < V; ++e) ss += double(f[e]) * double(f[e]);
+    }
+    src = orow;   // pass 2 re-reads h (this thread's own writes)
+  } else {
+    for (int vi = threadIdx.x; vi < nvec; vi += kThreads) {
+      float f[V];
+      E::unpack(xr[vi], f);
+#pragma unroll
+      for (int e = 0; e < V; ++e) ss += double(f[e]) * double(f[e]);
+    }
+  }
+  ss = block_sum(ss, red);
+  const float inv = float(1.0 / sqrt(ss / double(a.H) + double(a.eps)));
+  const u32x4 *wr = static_cast<const u32x4 *>(a.w);
+  u32x4 *yr = reinterpret_cast<u32x4 *>(static_cast<char *>(a.y) + row * a.y_rs * E::ES);
+  for (int vi = threadIdx.x; vi < nvec; vi += kThreads) {
+    float f[V], w[V];
+    E::unpack(src[vi], f);
+    E::unpack(wr[vi], w);
+#pragma unroll
+    for (int e = 0; e < V; ++e) f[e] = (f[e] * inv) * w[e];
+    yr[vi] = E::pack(f);
+  }
+}
+
+// Any alignment: element-wise two-pass row, float64 accumulation.
+template <int DT, bool RES>
+__device__ __forceinline__ void rn_scalar_row(const RnArgs &a, int64_t row, double *red) {
+  using E = Elt<DT>;
+  const int H = a.H;
+  const char *xr = static_cast<const char *>(a.x) + row * a.x_rs * E::ES;
+  const char *src = xr;
+  double ss = 0.0;
+  if constexpr (RES) {
+    const char *rr = static_cast<const char *>(a.res) + row * a.res_rs * E::ES;
+    char *orow = static_cast<char *>(a.res_out) + row * a.ro_rs * E::ES;
+    for (int j = threadIdx.x; j < H; j += kThreads) {
+      const float h = E::round(E::ld(xr, j) + E::ld(rr, j));
+      E::st(orow, j, h);
+      ss += double(h) * double(h);
+    }
+    src = orow;
+  } else {
+    for (int j = threadIdx.x; j < H; j += kThreads) {
+      const float v = E::ld(xr, j);
+      ss += double(v) * double(v);
+    }
+  }
+  ss = block_sum(ss, red);
+  const float inv = float(1.0 / sqrt(ss / double(H) + double(a.eps)));
+  char *yr = static_cast<char *>(a.y) + row * a.y_rs * E::ES;
+  for (int j = threadIdx.x; j < H; j += kThreads)
+    E::st(yr, j, (E::ld(src, j) * inv) * E::ld(a.w, j));
+}
+
+// ---- RoPE ---------------------------------------------------------------------
+// Angles theta = float(pos) * inv_i (one float32 product) and their cos/sin
+// are computed once per (token, pair) into LDS; every head of the token
+// reuses them.
+__device__ __forceinline__ void rope_angles(const RopeArgs &a, int64_t t, int tt, int half,
+                                            float *cs, float *sn) {
+  for (int i = threadIdx.x; i < half; i += kThreads) {
+    float c = 1.0f, s = 0.0f;
+    if (t < a.T) {
+      const float th = float(a.pos[t]) * a.inv_freq[i];
+      sincosf(th, &s, &c);
+    }
+    cs[tt * half + i] = c;
+    sn[tt * half + i] = s;
+  }
+}
+
+__device__ __forceinline__ char *rope_head(const RopeArgs &a, int64_t t, int h, int es) {
+  return h < a.nq ? static_cast<char *>(a.q) + (t * a.q_ts + int64_t(h) * a.hd) * es
+                  : static_cast<char *>(a.k) + (t * a.k_ts + int64_t(h - a.nq) * a.hd) * es;
+}
+
+// TPB tokens per workgroup. Each half-head is cpb = (hd/2)/V 16-byte
+// vectors (a power of two); work-item `tid` owns chunk tid % cpb of heads
+// tid / cpb, tid / cpb + 256 / cpb, ... and reads its V angles once per token.
+template <int DT, int TPB>
+__device__ __forceinline__ void rope_vec_block(const RopeArgs &a, int64_t blk, float *lds) {
+  using E = Elt<DT>;
+  constexpr int V = E::V;
+  const int half = a.hd >> 1;
+  float *cs = lds;
+  float *sn = lds + TPB * 256;
+  const int64_t t0 = blk * TPB;
+  // half = cpb * V is a power of two here: (token, pair) = (e >> lh, e & (half - 1)).
+  const int lh = __builtin_ctz(unsigned(half));
+  for (int e = threadIdx.x; e < TPB * half; e += kThreads) {
+    const int64_t t = t0 + (e >> lh);
+    const int i = e & (half - 1);
+    float c = 1.0f, s = 0.0f;
+    if (t < a.T) {
+      const float th = float(a.pos[t]) * a.inv_freq[i];
+      sincosf(th, &s, &c);
+    }
+    cs[e] = c;
+    sn[e] = s;
+  }
+  __syncthreads();
+  const int cpb = half / V;
+  const int shift = __builtin_ctz(unsigned(cpb));
+  const int chunk = threadIdx.x & (cpb - 1);
+  const int hg = threadIdx.x >> shift;
+  const int hstep = kThreads >> shift;
+  const int nh = a.nq + a.nk;
+  for (int tt = 0; tt < TPB; ++tt) {
+    const int64_t t = t0 + tt;
+    if (t >= a.T) break;
+    float c[V], s[V];
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+      c[j] = cs[tt * half + chunk * V + j];
+      s[j] = sn[tt * half + chunk * V + j];
+    }
+    for (int h = hg; h < nh; h += hstep) {
+      char *base = rope_head(a, t, h, E::ES);
+      u32x4 *p1 = reinterpret_cast<u32x4 *>(base) + chunk;
+      u32x4 *p2 = reinterpret_cast<u32x4 *>(base + half * E::ES) + chunk;
+      float f1[V], f2[V], o1[V], o2[V];
+      E::unpack(*p1, f1);
+      E::unpack(*p2, f2);
+#pragma unroll
+      for (int j = 0; j < V; ++j) {
+        o1[j] = f1[j] * c[j] - f2[j] * s[j];
+        o2[j] = f2[j] * c[j] + f1[j] * s[j];
+      }
+      *p1 = E::pack(o1);
+      *p2 = E::pack(o2);
+    }
+  }
+}
+
+// Any alignment / head size: one token per workgroup, element pairs.
+template <int DT>
+__device__ __forceinline__ void rope_scalar_block(const RopeArgs &a, int64_t t, float *lds) {
+  using E = Elt<DT>;
+  const int half = a.hd >> 1;
+  float *cs = lds;
+  float *sn = lds + 256;
+  rope_angles(a, t, 0, half, cs, sn);
+  __syncthreads();
+  const int nh = a.nq + a.nk;
+  const int total = nh * half;
+  for (int e = threadIdx.x; e < total; e += kThreads) {
+    const int h = e / half;
+    const int i = e - h * half;
+    char *base = rope_head(a, t, h, E::ES);
+    const float v1 = E::ld(base, i), v2 = E::ld(base, i + half);
+    E::st(base, i, v1 * cs[i] - v2 * sn[i]);
+    E::st(base, i + half, v2 * cs[i] + v1 * sn[i]);
+  }
+}
+
+// ---- SwiGLU ----------------------------------------------------------------------
+// silu(g) * u = g / (1 + exp(-g)) * u; for g << 0 exp overflows to +inf and
+// the quotient is a signed zero.
+__device__ __forceinline__ float silu_mul(float g, float u) {
+  return g / (1.0f + expf(-g)) * u;
+}
+
+// Flat contiguous [T*I]: workgroup `blk` of `nblk` handles U vectors per
+// work-item per step; workgroup 0 also does the < V element tail.
+template <int DT, int U>
+__device__ __forceinline__ void sw_flat_part(const SwArgs &a, int64_t blk, int64_t nblk) {
+  using E = Elt<DT>;
+  constexpr int V = E::V;
+  const u32x4 *g = static_cast<const u32x4 *>(a.gate);
+  const u32x4 *u = static_cast<const u32x4 *>(a.up);
+  u32x4 *o = static_cast<u32x4 *>(a.out);
+  const int64_t nvec = a.nvec;
+  const int64_t step = nblk * kThreads * U;
+  for (int64_t base = blk * kThreads * U + threadIdx.x; base < nvec; base += step) {
+    u32x4 gv[U], uv[U];
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      const int64_t idx = base + int64_t(k) * kThreads;
+      if (idx < nvec) {
+        gv[k] = g[idx];
+        uv[k] = u[idx];
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      const int64_t idx = base + int64_t(k) * kThreads;
+      if (idx < nvec) {
+        float fg[V], fu[V];
+        E::unpack(gv[k], fg);
+        E::unpack(uv[k], fu);
+#pragma unroll
+        for (int e = 0; e < V; ++e) fg[e] = silu_mul(fg[e], fu[e]);
+        o[idx] = E::pack(fg);
+      }
+    }
+  }
+  if (blk == 0) {
+    const int64_t i = nvec * V + threadIdx.x;
+    if (i < a.n) E::st(a.out, i, silu_mul(E::ld(a.gate, i), E::ld(a.up, i)));
+  }
+}
+
+// Aligned rows with padded strides: (row, 256-vector chunk) items.
+template <int DT>
+__device__ __forceinline__ void sw_rows_part(const SwArgs &a, int64_t blk, int64_t nblk) {
+  using E = Elt<DT>;
+  constexpr int V = E::V;
+  const int64_t nvr = a.I / V;
+  const int64_t cb = (nvr + kThreads - 1) / kThreads;
+  const int64_t total = a.T * cb;
+  for (int64_t it = blk; it < total; it += nblk) {
+    const int64_t row = it / cb;
+    const int64_t vi = (it - row * cb) * kThreads + threadIdx.x;
+    if (vi < nvr) {
+      const u32x4 gv = reinterpret_cast<const u32x4 *>(static_cast<const char *>(a.gate) +
+                                                        row * a.g_rs * E::ES)[vi];
+      const u32x4 uv = reinterpret_cast<const u32x4 *>(static_cast<const char *>(a.up) +
+                                                        row * a.u_rs * E::ES)[vi];
+      float fg[V], fu[V];
+      E::unpack(gv, fg);
+      E::unpack(uv, fu);
+#pragma unroll
+      for (int e = 0; e < V; ++e) fg[e] = silu_mul(fg[e], fu[e]);
+      reinterpret_cast<u32x4 *>(static_cast<char *>(a.out) + row * a.o_rs * E::ES)[vi] =
+          E::pack(fg);
+    }
+  }
+}
+
+// Any alignment: element-wise over T*I.
+template <int DT>
+__device__ __forceinline__ void sw_scalar_part(const SwArgs &a, int64_t blk, int64_t nblk) {
+  using E = Elt<DT>;
+  const int64_t n = a.T * a.I;
+  for (int64_t e = blk * kThreads + threadIdx.x; e < n; e += nblk * kThreads) {
+    const int64_t row = e / a.I;
+    const int64_t j = e - row * a.I;
+    const float r = silu_mul(E::ld(a.gate, row * a.g_rs + j), E::ld(a.up, row * a.u_rs + j));
+    E::st(a.out, row * a.o_rs + j, r);
+  }
+}
+
+}  // namespace dev
+}  // namespace tri

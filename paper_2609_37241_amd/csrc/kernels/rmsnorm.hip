@@ -1,0 +1,57 @@
+// RMSNorm and residual-add + RMSNorm kernels, one per install-policy variant
+// and dtype. Row bodies live in device.h (shared with the fused chain).
+#include "../internal.h"
+#include "device.h"
+
+namespace tri {
+using namespace dev;
+
+template <int DT, int NV, bool RES>
+__global__ __launch_bounds__(256) void k_rn_wave(RnArgs a) {
+  rn_wave_block<DT, NV, RES>(a, blockIdx.x);
+}
+
+template <int DT, int NB, bool RES>
+__global__ __launch_bounds__(256) void k_rn_block(RnArgs a) {
+  __shared__ float red[4];
+  rn_row_regs<DT, NB, RES, 256>(a, blockIdx.x, threadIdx.x, red);
+}
+
+template <int DT, bool RES>
+__global__ __launch_bounds__(256) void k_rn_loop(RnArgs a) {
+  __shared__ double red[4];
+  rn_loop_row<DT, RES>(a, blockIdx.x, red);
+}
+
+template <int DT, bool RES>
+__global__ __launch_bounds__(256) void k_rn_scalar(RnArgs a) {
+  __shared__ double red[4];
+  rn_scalar_row<DT, RES>(a, blockIdx.x, red);
+}
+
+namespace {
+template <int DT, bool RES>
+const void *rn_pick(int32_t variant) {
+  switch (variant) {
+    case RN_SCALAR: return reinterpret_cast<const void *>(&k_rn_scalar<DT, RES>);
+    case RN_WAVE_1: return reinterpret_cast<const void *>(&k_rn_wave<DT, 1, RES>);
+    case RN_WAVE_2: return reinterpret_cast<const void *>(&k_rn_wave<DT, 2, RES>);
+    case RN_WAVE_4: return reinterpret_cast<const void *>(&k_rn_wave<DT, 4, RES>);
+    case RN_WAVE_8: return reinterpret_cast<const void *>(&k_rn_wave<DT, 8, RES>);
+    case RN_WAVE_16: return reinterpret_cast<const void *>(&k_rn_wave<DT, 16, RES>);
+    case RN_BLOCK_8: return reinterpret_cast<const void *>(&k_rn_block<DT, 8, RES>);
+    case RN_BLOCK_16: return reinterpret_cast<const void *>(&k_rn_block<DT, 16, RES>);
+    case RN_LOOP: return reinterpret_cast<const void *>(&k_rn_loop<DT, RES>);
+    default: return nullptr;
+  }
+}
+}  // namespace
+
+// Host stub of the kernel for (variant, dtype, residual flavour).
+const void *rn_kernel(int32_t variant, uint32_t dtype, int32_t res) {
+  if (dtype == TRI_F32) return res ? rn_pick<kF32, true>(variant) : rn_pick<kF32, false>(variant);
+  if (dtype == TRI_BF16) return res ? rn_pick<kBF16, true>(variant) : rn_pick<kBF16, false>(variant);
+  return nullptr;
+}
+
+}  // namespace tri

@@ -1,0 +1,38 @@
+// RoPE-on-Q-and-K kernels (in place), one per install-policy variant and dtype.
+#include "../internal.h"
+#include "device.h"
+
+namespace tri {
+using namespace dev;
+
+template <int DT, int TPB>
+__global__ __launch_bounds__(256) void k_rope_vec(RopeArgs a) {
+  __shared__ float lds[2 * TPB * 256];
+  rope_vec_block<DT, TPB>(a, blockIdx.x, lds);
+}
+
+template <int DT>
+__global__ __launch_bounds__(256) void k_rope_scalar(RopeArgs a) {
+  __shared__ float lds[2 * 256];
+  rope_scalar_block<DT>(a, blockIdx.x, lds);
+}
+
+namespace {
+template <int DT>
+const void *rope_pick(int32_t variant) {
+  switch (variant) {
+    case ROPE_SCALAR: return reinterpret_cast<const void *>(&k_rope_scalar<DT>);
+    case ROPE_VEC_T1: return reinterpret_cast<const void *>(&k_rope_vec<DT, 1>);
+    case ROPE_VEC_T4: return reinterpret_cast<const void *>(&k_rope_vec<DT, 4>);
+    default: return nullptr;
+  }
+}
+}  // namespace
+
+const void *rope_kernel(int32_t variant, uint32_t dtype) {
+  if (dtype == TRI_F32) return rope_pick<kF32>(variant);
+  if (dtype == TRI_BF16) return rope_pick<kBF16>(variant);
+  return nullptr;
+}
+
+}  // namespace tri

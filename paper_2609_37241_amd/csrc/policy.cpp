@@ -1,0 +1,175 @@
+// Install policy: which precompiled kernel variant serves a specialization
+// key, and how many workgroups a call with T tokens launches.
+//
+// In the paper a miss captures and compiles a new specialization (Sec. 3.5);
+// here every specialization a key can need is already compiled for gfx950,
+// and installing a version means choosing among them. The choice is a pure
+// function of the key (dtype, sizes, token bucket, alignment and contiguity
+// flags), so the same key always selects the same kernels.
+#include "internal.h"
+
+namespace tri {
+
+namespace {
+
+inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+inline int64_t next_pow2(int64_t n) {
+  int64_t p = 1;
+  while (p < n) p <<= 1;
+  return p;
+}
+
+inline int64_t vec_elems(uint32_t dtype) { return dtype == TRI_F32 ? 4 : 8; }
+
+inline uint32_t clamp_grid(int64_t g) {
+  if (g < 1) return 1;
+  return g > int64_t(kGridCap) ? kGridCap : uint32_t(g);
+}
+
+int32_t rn_wave_id(int64_t nv) {
+  switch (nv) {
+    case 1: return RN_WAVE_1;
+    case 2: return RN_WAVE_2;
+    case 4: return RN_WAVE_4;
+    case 8: return RN_WAVE_8;
+    default: return RN_WAVE_16;
+  }
+}
+
+}  // namespace
+
+// One wavefront per row while a row fits in at most 16 16-byte vectors per
+// lane, then one workgroup per row up to 16 vectors per thread, then two
+// passes over global memory. Unaligned or ragged rows take the scalar kernel.
+Role rn_role(uint32_t dtype, int64_t H, unsigned flags, int64_t T) {
+  const int64_t v = vec_elems(dtype);
+  if (!(flags & kAlign) || H % v) return {RN_SCALAR, uint32_t(T)};
+  const int64_t nvec = H / v;
+  const int64_t nv = next_pow2(cdiv(nvec, 64));
+  if (nv <= 16) return {rn_wave_id(nv), uint32_t(cdiv(T, 4))};
+  const int64_t nb = next_pow2(cdiv(nvec, 256));
+  if (nb <= 16) return {nb == 8 ? RN_BLOCK_8 : RN_BLOCK_16, uint32_t(T)};
+  return {RN_LOOP, uint32_t(T)};
+}
+
+// Vector RoPE needs each half-head to be a power-of-two number of 16-byte
+// vectors, so a thread keeps one chunk of angles for every head it visits.
+Role rope_role(uint32_t dtype, int32_t hd, unsigned flags, uint32_t bucket, int64_t T) {
+  const int64_t v = vec_elems(dtype);
+  const int64_t half = hd / 2;
+  const int64_t cpb = half / v;
+  if (!(flags & kAlign) || half % v || (cpb & (cpb - 1)) != 0)
+    return {ROPE_SCALAR, uint32_t(T)};
+  if (bucket <= 3) return {ROPE_VEC_T1, uint32_t(T)};
+  return {ROPE_VEC_T4, uint32_t(cdiv(T, 4))};
+}
+
+Role sw_role(uint32_t dtype, int64_t I, unsigned flags, uint32_t bucket, int64_t T) {
+  const int64_t v = vec_elems(dtype);
+  if ((flags & kAlign) && (flags & kContig)) {
+    const int64_t u = bucket <= 6 ? 1 : 4;
+    const int64_t nvec = (T * I) / v;
+    return {u == 1 ? SW_FLAT_U1 : SW_FLAT_U4, clamp_grid(cdiv(nvec, int64_t(kBlock) * u))};
+  }
+  if ((flags & kAlign) && I % v == 0) {
+    const int64_t cb = cdiv(I / v, kBlock);
+    const int64_t g = T * cb;
+    return {SW_ROWS, g > int64_t(kGridCap) ? kGridCap : uint32_t(g)};
+  }
+  const int64_t g = cdiv(T * I, kBlock);
+  return {SW_SCALAR, g > int64_t(kGridCap) ? kGridCap : uint32_t(g)};
+}
+
+// Workgroups of a role variant for T tokens (I is the SwiGLU width).
+uint32_t role_grid(int32_t variant, uint32_t dtype, int64_t T, int64_t I) {
+  switch (variant) {
+    case RN_WAVE_1: case RN_WAVE_2: case RN_WAVE_4: case RN_WAVE_8: case RN_WAVE_16:
+    case ROPE_VEC_T4:
+      return uint32_t(cdiv(T, 4));
+    case RN_SCALAR: case RN_BLOCK_8: case RN_BLOCK_16: case RN_LOOP:
+    case ROPE_SCALAR: case ROPE_VEC_T1:
+      return uint32_t(T);
+    case SW_FLAT_U1:
+      return clamp_grid(cdiv((T * I) / vec_elems(dtype), kBlock));
+    case SW_FLAT_U4:
+      return clamp_grid(cdiv((T * I) / vec_elems(dtype), 4 * int64_t(kBlock)));
+    case SW_ROWS: {
+      const int64_t g = T * cdiv(I / vec_elems(dtype), kBlock);
+      return g > int64_t(kGridCap) ? kGridCap : uint32_t(g);
+    }
+    case SW_SCALAR: {
+      const int64_t g = cdiv(T * I, kBlock);
+      return g > int64_t(kGridCap) ? kGridCap : uint32_t(g);
+    }
+    default:
+      return 0;
+  }
+}
+
+namespace {
+
+// Template index of the fused chain kernel: (NV index) * 4 + (T4) * 2 + (U4).
+int32_t fused_sub(int32_t rn, int32_t rope, int32_t sw) {
+  return (rn - RN_WAVE_1) * 4 + (rope == ROPE_VEC_T4 ? 2 : 0) + (sw == SW_FLAT_U4 ? 1 : 0);
+}
+
+}  // namespace
+
+Plan plan_for_key(const Key &k) {
+  const uint32_t op = key_op(k), dt = key_dtype(k), b = key_bucket(k), fl = key_flags(k);
+  Plan p{};
+  // The grid does not affect the choice of variant; T = 1 stands in here.
+  switch (op) {
+    case TRI_OP_RMSNORM:
+    case TRI_OP_RES_RMSNORM: {
+      const Role r = rn_role(dt, key_H(k), fl, 1);
+      p.variant = r.variant;
+      p.n_launches = 1;
+      p.kvariant[0] = r.variant;
+      p.ksub[0] = op == TRI_OP_RES_RMSNORM ? 1 : 0;
+      return p;
+    }
+    case TRI_OP_ROPE_QK: {
+      const Role r = rope_role(dt, int32_t(key_hd(k)), fl, b, 1);
+      p.variant = r.variant;
+      p.n_launches = 1;
+      p.kvariant[0] = r.variant;
+      return p;
+    }
+    case TRI_OP_SWIGLU: {
+      const Role r = sw_role(dt, key_I(k), fl, b, 1);
+      p.variant = r.variant;
+      p.n_launches = 1;
+      p.kvariant[0] = r.variant;
+      return p;
+    }
+    default:
+      break;
+  }
+  const Role rn = rn_role(dt, key_H(k), fl & 3u, 1);
+  const Role ro = rope_role(dt, int32_t(key_hd(k)), (fl >> 2) & 3u, b, 1);
+  const Role sw = sw_role(dt, key_I(k), (fl >> 4) & 3u, b, 1);
+  p.roles[0] = rn.variant;
+  p.roles[1] = ro.variant;
+  p.roles[2] = sw.variant;
+  const bool rn_wave = rn.variant >= RN_WAVE_1 && rn.variant <= RN_WAVE_16;
+  const bool ro_vec = ro.variant == ROPE_VEC_T1 || ro.variant == ROPE_VEC_T4;
+  const bool sw_flat = sw.variant == SW_FLAT_U1 || sw.variant == SW_FLAT_U4;
+  if (fl == 0x3Fu && rn_wave && ro_vec && sw_flat) {
+    p.variant = CH_FUSED;
+    p.n_launches = 1;
+    p.kvariant[0] = CH_FUSED;
+    p.ksub[0] = fused_sub(rn.variant, ro.variant, sw.variant);
+    return p;
+  }
+  p.variant = CH_SEQ;
+  p.n_launches = 3;
+  p.kvariant[0] = rn.variant;
+  p.ksub[0] = 1;   // residual flavour
+  p.kvariant[1] = ro.variant;
+  p.kvariant[2] = sw.variant;
+  return p;
+}
+
+}  // namespace tri

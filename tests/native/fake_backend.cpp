@@ -1,0 +1,105 @@
+// Recording launch backend for CPU tests of the cache core (test double).
+//
+// Links with the library's host sources in place of the HIP backend. It
+// computes nothing: "kernel handles" encode (variant, dtype, sub), launches
+// are appended to a log with their grid, block and a copy of the argument
+// block, and a launch can be made to fail on purpose (fault injection).
+#include <stdlib.h>
+#include <string.h>
+
+#include <vector>
+
+#include "internal.h"
+
+namespace {
+
+struct Rec {
+  int32_t kvariant, dtype, ksub;
+  uint32_t grid, block;
+  unsigned char args[256];
+  void *stream;
+};
+
+std::vector<Rec> g_log;
+int64_t g_fail_at = -1;        // launch ordinal that fails, -1 none
+int g_init_status = 0;
+int64_t g_uploads = 0;
+
+uintptr_t encode(int32_t v, uint32_t dt, int32_t sub) {
+  return (uintptr_t(uint32_t(v)) << 20) | (uintptr_t(dt) << 16) | uintptr_t(uint32_t(sub) & 0xFFFF) |
+         (uintptr_t(1) << 40);
+}
+
+}  // namespace
+
+namespace tri {
+
+int be_init(int *device) {
+  *device = 0;
+  return g_init_status;
+}
+
+int be_resolve(int32_t kvariant, uint32_t dtype, int32_t ksub, void **fn) {
+  *fn = reinterpret_cast<void *>(encode(kvariant, dtype, ksub));
+  return 0;
+}
+
+int be_launch(void *fn, uint32_t grid, uint32_t block, void *args, void *stream) {
+  const int64_t n = int64_t(g_log.size());
+  Rec r;
+  memset(&r, 0, sizeof r);
+  const uintptr_t h = reinterpret_cast<uintptr_t>(fn);
+  r.kvariant = int32_t((h >> 20) & 0xFFFFF);
+  r.dtype = int32_t((h >> 16) & 0xF);
+  r.ksub = int32_t(h & 0xFFFF);
+  r.grid = grid;
+  r.block = block;
+  r.stream = stream;
+  if (args) memcpy(r.args, args, sizeof r.args);
+  g_log.push_back(r);
+  return n == g_fail_at ? -1 : 0;
+}
+
+int be_upload(const void *host, uint64_t bytes, void **dev) {
+  void *p = malloc(bytes);
+  if (!p) return TRI_E_NOMEM;
+  memcpy(p, host, bytes);
+  *dev = p;
+  g_uploads++;
+  return 0;
+}
+
+void be_free(void *dev) { free(dev); }
+
+}  // namespace tri
+
+extern "C" {
+
+void trifake_reset() {
+  g_log.clear();
+  g_fail_at = -1;
+  g_init_status = 0;
+  g_uploads = 0;
+}
+int64_t trifake_launch_count() { return int64_t(g_log.size()); }
+int64_t trifake_upload_count() { return g_uploads; }
+void trifake_fail_at(int64_t n) { g_fail_at = n; }
+void trifake_init_status(int st) { g_init_status = st; }
+
+// Launch i: kernel (variant, dtype, sub), grid, block, stream and the first
+// `nbytes` bytes of its argument block.
+int trifake_get(int64_t i, int32_t *kv, int32_t *dt, int32_t *sub, uint32_t *grid,
+                uint32_t *block, void **stream, unsigned char *args, int nbytes) {
+  if (i < 0 || i >= int64_t(g_log.size())) return -1;
+  const Rec &r = g_log[size_t(i)];
+  *kv = r.kvariant;
+  *dt = r.dtype;
+  *sub = r.ksub;
+  *grid = r.grid;
+  *block = r.block;
+  *stream = r.stream;
+  if (args) memcpy(args, r.args, nbytes > 256 ? 256 : nbytes);
+  return 0;
+}
+
+}  // extern "C"

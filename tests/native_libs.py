@@ -1,0 +1,55 @@
+"""Locate / build the native libraries the tests load.
+
+libtri.so (the product) is built by __graft_entry__.build(); the tests only
+build it here when it is missing. libtri_fake.so is the cache core linked
+with the recording backend in tests/native (CPU tests only).
+"""
+import ctypes as C
+import importlib.util
+import os
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+PKG = os.path.join(ROOT, "paper_2609_37241_amd")
+LIBTRI = os.path.join(PKG, "libtri.so")
+FAKE_SRC = os.path.join(ROOT, "tests", "native", "fake_backend.cpp")
+FAKE_LIB = os.path.join(ROOT, "tests", "native", "libtri_fake.so")
+
+
+def _build_module():
+    spec = importlib.util.spec_from_file_location("_tri_build", os.path.join(PKG, "build.py"))
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    return mod
+
+
+def ensure_libtri() -> str:
+    if not os.path.exists(LIBTRI):
+        _build_module().build()
+    return LIBTRI
+
+
+def ensure_fake() -> str:
+    srcs = [FAKE_SRC] + [os.path.join(PKG, "csrc", n)
+                         for n in ("api.cpp", "cache.cpp", "policy.cpp", "internal.h",
+                                   "kernargs.h")]
+    stale = (not os.path.exists(FAKE_LIB)
+             or any(os.path.getmtime(s) > os.path.getmtime(FAKE_LIB) for s in srcs))
+    if stale:
+        _build_module().build_host_core(FAKE_SRC, FAKE_LIB)
+    return FAKE_LIB
+
+
+def load_fake():
+    """The cache core + recording backend, with the ABI's signatures."""
+    ensure_libtri()
+    from paper_2609_37241_amd import _lib as L
+    lib = L.declare(C.CDLL(ensure_fake()))
+    lib.trifake_launch_count.restype = C.c_int64
+    lib.trifake_upload_count.restype = C.c_int64
+    lib.trifake_fail_at.argtypes = [C.c_int64]
+    lib.trifake_init_status.argtypes = [C.c_int]
+    lib.trifake_get.argtypes = [C.c_int64, C.POINTER(C.c_int32), C.POINTER(C.c_int32),
+                                C.POINTER(C.c_int32), C.POINTER(C.c_uint32),
+                                C.POINTER(C.c_uint32), C.POINTER(C.c_void_p),
+                                C.c_char_p, C.c_int]
+    return lib

@@ -1,0 +1,77 @@
+"""Tolerance checks and oracle-model calls built from real device tensors.
+
+Tolerances (the design's reading of the stated bar): float32 outputs pass
+when |g - o| <= 1e-5 |o| + 1e-6; bfloat16 outputs pass when |g - o| <= 2e-2
+or g is within one bf16 ulp of the oracle's correctly rounded value.
+"""
+import numpy as np
+
+from oracle import numerics as nm
+from oracle import selection as S
+import workloads as wl
+
+
+def check(name, got, want, dtype, exact=False):
+    """Compare a GPU result (host repr) with the oracle's (host repr)."""
+    got = np.asarray(got)
+    want = np.asarray(want)
+    assert got.shape == want.shape, (name, got.shape, want.shape)
+    if exact:
+        bad = got.view(np.uint16 if dtype == nm.BF16 else np.uint32) != \
+            want.view(np.uint16 if dtype == nm.BF16 else np.uint32)
+        assert not bad.any(), f"{name}: {int(bad.sum())} of {bad.size} differ (bit-exact)"
+        return
+    g = nm.values(got, dtype)
+    o = nm.values(want, dtype)
+    if dtype == nm.F32:
+        bad = ~(np.abs(g - o) <= 1e-5 * np.abs(o) + 1e-6)
+    else:
+        ulps = nm.bf16_ulp_distance(got, want)
+        bad = ~((np.abs(g - o) <= 2e-2) | (ulps <= 1))
+    if bad.any():
+        i = np.argwhere(bad)[0]
+        raise AssertionError(f"{name}: {int(bad.sum())} of {bad.size} outside tolerance; "
+                             f"first at {tuple(i)}: got {g[tuple(i)]!r} want {o[tuple(i)]!r}")
+
+
+def dt_code(dtype):
+    return S.DT_F32 if dtype == nm.F32 else S.DT_BF16
+
+
+def rows_stride(t):
+    return t.stride(0) if t.shape[0] > 1 else max(t.stride(0), t.shape[1])
+
+
+def tok_stride(t):
+    return t.stride(0) if t.shape[0] > 1 else max(t.stride(0), t.shape[1] * t.shape[2])
+
+
+def model_chain_call(d, eps, base):
+    """An oracle-model Call for a decode chain over device tensors `d`."""
+    dt = nm.BF16 if str(d["x"].dtype).endswith("bfloat16") else nm.F32
+    T, H = d["x"].shape
+    _, nq, hd = d["q"].shape
+    nk = d["k"].shape[1]
+    ptr = dict(x=d["x"].data_ptr(), res=d["residual"].data_ptr(), w=d["w"].data_ptr(),
+               y=d["y"].data_ptr(), res_out=d["res_out"].data_ptr(), q=d["q"].data_ptr(),
+               k=d["k"].data_ptr(), pos=d["pos"].data_ptr(), gate=d["gate"].data_ptr(),
+               up=d["up"].data_ptr(), out=d["out"].data_ptr())
+    stride = dict(x=rows_stride(d["x"]), res=rows_stride(d["residual"]),
+                  y=rows_stride(d["y"]), res_out=rows_stride(d["res_out"]),
+                  q=tok_stride(d["q"]), k=tok_stride(d["k"]), gate=rows_stride(d["gate"]),
+                  up=rows_stride(d["up"]), out=rows_stride(d["out"]))
+    return S.Call(S.OP_CHAIN, dt_code(dt), T, H=H, I=d["gate"].shape[1], hd=hd, nq=nq, nk=nk,
+                  eps=eps, base=base, ptr=ptr, stride=stride)
+
+
+def expected_record(call: S.Call, version: int):
+    """The oracle model's selection record for a hit on `version`."""
+    key = S.make_key(call)
+    variant, roles, launches = S.plan(key, call.T)
+    rec = S.Record(op=call.op, status=S.OK, version=version, variant=variant,
+                   n_launches=len(launches), roles=roles,
+                   launch=tuple(launches) + ((0, 0, 0),) * (3 - len(launches)), key=key)
+    return rec.as_tuple()
+
+
+__all__ = ["check", "model_chain_call", "expected_record", "wl"]

@@ -1,0 +1,389 @@
+"""GPU parity: the HIP path through the C ABI vs the CPU oracle.
+
+Every case prints its name (pytest -v) before touching the GPU. Inputs come
+from the seeded generators in `workloads`; expected values only from
+`oracle`. Selection records are compared with the oracle's selection model.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import numerics as nm
+from oracle import ops as O
+from oracle import selection as S
+from tests.parity import check, expected_record, model_chain_call
+import workloads as wl
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+@pytest.fixture(scope="module")
+def tri():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2609_37241_amd as tri
+    return tri
+
+
+@pytest.fixture
+def cache(tri):
+    c = tri.SpecCache()
+    yield c
+    torch.cuda.synchronize()
+    c.close()
+
+
+def rng(seed):
+    return np.random.Generator(np.random.PCG64(seed))
+
+
+def place(a: np.ndarray, dtype: str, layout: str = "plain", pad: int = 64):
+    """Host array [T, W] or [T, nh, hd] -> device tensor with the given layout."""
+    src = wl.to_torch(a, dtype, DEV)
+    shape = src.shape
+    T = shape[0]
+    W = int(np.prod(shape[1:]))
+    td = src.dtype
+    if layout == "plain":
+        return src.contiguous()
+    if layout == "strided":
+        buf = torch.zeros((T, W + pad), dtype=td, device=DEV)
+        rs = W + pad
+    elif layout == "unaligned":
+        buf = torch.zeros(T * W + 1, dtype=td, device=DEV)
+        rs = W
+    else:
+        raise ValueError(layout)
+    strides = (rs,) + tuple(int(np.prod(shape[i + 1:])) for i in range(1, len(shape)))
+    off = 1 if layout == "unaligned" else 0
+    view = torch.as_strided(buf, size=shape, stride=strides, storage_offset=off)
+    view.copy_(src)
+    return view
+
+
+def empty_like_layout(t):
+    """Output tensor with the same layout (strides, 16-byte phase) as t."""
+    buf = torch.zeros(t.untyped_storage().nbytes() // t.element_size(), dtype=t.dtype,
+                      device=DEV)
+    return torch.as_strided(buf, size=t.shape, stride=t.stride(),
+                            storage_offset=t.storage_offset())
+
+
+def host(t):
+    return wl.from_torch(t)
+
+
+# ---- the configured chains ---------------------------------------------------------
+@pytest.mark.parametrize("cfg", [wl.TINY_F32, wl.LLAMA7B_DECODE, wl.GQA_DECODE],
+                         ids=lambda c: c.name)
+def test_chain_config(tri, cache, cfg):
+    inp = wl.host_inputs(cfg)
+    d = {k: wl.to_torch(v, cfg.dtype, DEV) for k, v in inp.items()}
+    d["y"] = torch.empty_like(d["x"])
+    d["res_out"] = torch.empty_like(d["x"])
+    d["out"] = torch.empty_like(d["gate"])
+    cache.decode_chain(d["x"], d["residual"], d["w"], d["q"], d["k"], d["pos"], d["gate"],
+                       d["up"], cfg.eps, cfg.base, y=d["y"], residual_out=d["res_out"],
+                       out=d["out"])
+    torch.cuda.synchronize()
+    want = O.decode_chain(inp, cfg.eps, cfg.base, cfg.dtype)
+    check("y", host(d["y"]), want["y"], cfg.dtype)
+    check("res_out", host(d["res_out"]), want["res_out"], cfg.dtype, exact=True)
+    check("q", host(d["q"]), want["q"], cfg.dtype)
+    check("k", host(d["k"]), want["k"], cfg.dtype)
+    check("out", host(d["out"]), want["out"], cfg.dtype)
+    rec = cache.last_selection().as_tuple()
+    assert rec == expected_record(model_chain_call(d, cfg.eps, cfg.base), 0)
+    assert rec[3] == S.CH_FUSED
+
+
+@pytest.mark.parametrize("cfg", [wl.TINY_F32, wl.LLAMA7B_DECODE, wl.GQA_DECODE],
+                         ids=lambda c: c.name)
+def test_fused_chain_equals_separate_ops_bitwise(tri, cache, cfg):
+    inp = wl.host_inputs(cfg)
+    a = {k: wl.to_torch(v, cfg.dtype, DEV) for k, v in inp.items()}
+    b = {k: v.clone() for k, v in a.items()}
+    y, ro, out = cache.decode_chain(a["x"], a["residual"], a["w"], a["q"], a["k"], a["pos"],
+                                    a["gate"], a["up"], cfg.eps, cfg.base)
+    y2, ro2 = cache.residual_rmsnorm(b["x"], b["residual"], b["w"], cfg.eps)
+    cache.rope_qk(b["q"], b["k"], b["pos"], cfg.base)
+    out2 = cache.swiglu(b["gate"], b["up"])
+    torch.cuda.synchronize()
+    for n, g, h in (("y", y, y2), ("res_out", ro, ro2), ("q", a["q"], b["q"]),
+                    ("k", a["k"], b["k"]), ("out", out, out2)):
+        check(n, host(g), host(h), cfg.dtype, exact=True)
+
+
+# ---- RMSNorm / residual RMSNorm: every variant ------------------------------------------
+RN_CASES = [
+    # dtype, T, H, layout -> variant (by the policy table)
+    (nm.F32, 5, 64, "plain"), (nm.F32, 5, 100, "plain"), (nm.F32, 37, 520, "plain"),
+    (nm.F32, 6, 4096, "plain"), (nm.F32, 3, 8192, "plain"), (nm.F32, 3, 16384, "plain"),
+    (nm.F32, 2, 65536, "plain"), (nm.F32, 5, 4097, "plain"), (nm.F32, 7, 4096, "unaligned"),
+    (nm.F32, 7, 4096, "strided"),
+    (nm.BF16, 1, 4096, "plain"), (nm.BF16, 9, 256, "plain"), (nm.BF16, 9, 520, "plain"),
+    (nm.BF16, 6, 4096, "plain"), (nm.BF16, 5, 8192, "plain"), (nm.BF16, 3, 32768, "plain"),
+    (nm.BF16, 2, 65536, "plain"), (nm.BF16, 4, 100, "plain"), (nm.BF16, 7, 4096, "unaligned"),
+    (nm.BF16, 7, 4096, "strided"), (nm.BF16, 3, 1, "plain"),
+]
+
+
+@pytest.mark.parametrize("res", [False, True], ids=["rmsnorm", "residual"])
+@pytest.mark.parametrize("dtype,T,H,layout", RN_CASES)
+def test_rmsnorm_variants(tri, cache, dtype, T, H, layout, res):
+    r = rng(T * 131 + H)
+    x = wl.host_array(r, (T, H), dtype)
+    rr = wl.host_array(r, (T, H), dtype)
+    w = wl.host_weight(r, H, dtype)
+    xd = place(x, dtype, layout)
+    wd = wl.to_torch(w, dtype, DEV)
+    yd = empty_like_layout(xd)
+    if res:
+        rd = place(rr, dtype, layout)
+        rod = empty_like_layout(xd)
+        cache.residual_rmsnorm(xd, rd, wd, 1e-6, out=yd, residual_out=rod)
+        want_y, want_h = O.residual_rmsnorm(x, rr, w, 1e-6, dtype)
+    else:
+        cache.rmsnorm(xd, wd, 1e-6, out=yd)
+        want_y = O.rmsnorm(x, w, 1e-6, dtype)
+    torch.cuda.synchronize()
+    check("y", host(yd), want_y, dtype)
+    if res:
+        check("res_out", host(rod), want_h, dtype, exact=True)
+    sel = cache.last_selection()
+    es = 4 if dtype == nm.F32 else 2
+    flags = S.ALIGN if (xd.data_ptr() % 16 == 0 and (xd.stride(0) * es) % 16 == 0) else 0
+    assert sel.variant == S.rn_role(S.DT_F32 if dtype == nm.F32 else S.DT_BF16, H, flags, T)[0]
+
+
+def test_rmsnorm_in_place(tri, cache):
+    r = rng(3)
+    x = wl.host_array(r, (6, 4096), nm.BF16)
+    w = wl.host_weight(r, 4096, nm.BF16)
+    xd = wl.to_torch(x, nm.BF16, DEV)
+    cache.rmsnorm(xd, wl.to_torch(w, nm.BF16, DEV), 1e-6, out=xd)
+    torch.cuda.synchronize()
+    check("y", host(xd), O.rmsnorm(x, w, 1e-6, nm.BF16), nm.BF16)
+
+
+# ---- RoPE: every variant ---------------------------------------------------------------
+ROPE_CASES = [
+    # dtype, T, nq, nk, hd, base, layout
+    (nm.BF16, 1, 32, 32, 128, 1e4, "plain"), (nm.BF16, 8, 32, 8, 128, 5e5, "plain"),
+    (nm.BF16, 37, 32, 8, 128, 5e5, "plain"), (nm.F32, 4, 4, 4, 64, 1e4, "plain"),
+    (nm.F32, 19, 4, 4, 64, 1e4, "plain"), (nm.BF16, 5, 2, 2, 96, 1e4, "plain"),
+    (nm.F32, 3, 3, 0, 128, 1e4, "plain"), (nm.BF16, 6, 4, 4, 512, 1e4, "plain"),
+    (nm.F32, 6, 2, 3, 512, 1e4, "plain"), (nm.F32, 2, 2, 2, 2, 1e4, "plain"),
+    (nm.BF16, 9, 8, 2, 128, 5e5, "unaligned"), (nm.F32, 9, 8, 2, 128, 5e5, "strided"),
+    (nm.BF16, 17, 64, 8, 128, 5e5, "plain"),
+]
+
+
+@pytest.mark.parametrize("dtype,T,nq,nk,hd,base,layout", ROPE_CASES)
+def test_rope_variants(tri, cache, dtype, T, nq, nk, hd, base, layout):
+    r = rng(T * 7 + nq * 13 + hd)
+    q = wl.host_array(r, (T, nq, hd), dtype)
+    k = wl.host_array(r, (T, nk, hd), dtype)
+    pos = r.integers(0, 8192, size=T).astype(np.int32)
+    qd = place(q, dtype, layout)
+    kd = place(k, dtype, layout) if nk else None
+    cache.rope_qk(qd, kd, wl.to_torch(pos, dtype, DEV), base)
+    torch.cuda.synchronize()
+    wq, wk = O.rope_qk(q, k, pos, base, dtype)
+    check("q", host(qd), wq, dtype)
+    if nk:
+        check("k", host(kd), wk, dtype)
+
+
+@pytest.mark.parametrize("dtype", [nm.F32, nm.BF16])
+def test_rope_position_zero_is_exact_identity(tri, cache, dtype):
+    r = rng(11)
+    q = wl.host_array(r, (12, 8, 128), dtype)
+    k = wl.host_array(r, (12, 2, 128), dtype)
+    qd, kd = wl.to_torch(q, dtype, DEV), wl.to_torch(k, dtype, DEV)
+    cache.rope_qk(qd, kd, torch.zeros(12, dtype=torch.int32, device=DEV), 5e5)
+    torch.cuda.synchronize()
+    check("q", host(qd), q, dtype, exact=True)
+    check("k", host(kd), k, dtype, exact=True)
+
+
+# ---- SwiGLU: every variant ---------------------------------------------------------------
+SW_CASES = [
+    # dtype, T, I, layout
+    (nm.BF16, 1, 11008, "plain"), (nm.BF16, 8, 14336, "plain"), (nm.BF16, 300, 688, "plain"),
+    (nm.F32, 4, 688, "plain"), (nm.F32, 130, 1000, "plain"), (nm.F32, 3, 11003, "plain"),
+    (nm.BF16, 3, 11003, "plain"), (nm.BF16, 1, 5, "plain"), (nm.F32, 1, 1, "plain"),
+    (nm.BF16, 5, 11008, "strided"), (nm.F32, 5, 11008, "strided"),
+    (nm.BF16, 5, 11008, "unaligned"), (nm.F32, 5, 1001, "unaligned"),
+]
+
+
+@pytest.mark.parametrize("dtype,T,I,layout", SW_CASES)
+def test_swiglu_variants(tri, cache, dtype, T, I, layout):
+    r = rng(T * 3 + I)
+    g = wl.host_array(r, (T, I), dtype)
+    u = wl.host_array(r, (T, I), dtype)
+    gd, ud = place(g, dtype, layout), place(u, dtype, layout)
+    od = empty_like_layout(gd)
+    cache.swiglu(gd, ud, out=od)
+    torch.cuda.synchronize()
+    check("out", host(od), O.swiglu(g, u, dtype), dtype)
+
+
+@pytest.mark.parametrize("dtype", [nm.F32, nm.BF16])
+def test_swiglu_extremes(tri, cache, dtype):
+    g = np.array([[0.0, 1.0, -1.0, 88.0, -88.0, 200.0, -200.0, 3.0] * 4], np.float32)
+    u = np.array([[5.0, 1.0, 1.0, 1.0, 1.0, 1.0, 1.0, 0.0] * 4], np.float32)
+    if dtype == nm.BF16:
+        g, u = nm.round_to(g, nm.BF16), nm.round_to(u, nm.BF16)
+    gd, ud = wl.to_torch(g, dtype, DEV), wl.to_torch(u, dtype, DEV)
+    od = cache.swiglu(gd, ud)
+    torch.cuda.synchronize()
+    got = host(od)
+    check("out", got, O.swiglu(g, u, dtype), dtype)
+    v = nm.values(got, dtype)
+    assert not np.isnan(v).any()
+    assert v[0, 6] == 0.0 and np.signbit(v[0, 6])
+
+
+def test_swiglu_in_place(tri, cache):
+    r = rng(5)
+    g = wl.host_array(r, (4, 11008), nm.BF16)
+    u = wl.host_array(r, (4, 11008), nm.BF16)
+    gd, ud = wl.to_torch(g, nm.BF16, DEV), wl.to_torch(u, nm.BF16, DEV)
+    cache.swiglu(gd, ud, out=gd)
+    torch.cuda.synchronize()
+    check("out", host(gd), O.swiglu(g, u, nm.BF16), nm.BF16)
+
+
+# ---- chain layouts, degenerate calls, miss path ----------------------------------------------
+@pytest.mark.parametrize("layout", ["strided", "unaligned"])
+def test_chain_three_launch_variant(tri, cache, layout):
+    cfg = wl.GQA_DECODE
+    inp = wl.host_inputs(cfg)
+    d = {k: place(v, cfg.dtype, layout) if k not in ("w", "pos") else
+         wl.to_torch(v, cfg.dtype, DEV) for k, v in inp.items()}
+    d["y"], d["res_out"], d["out"] = (empty_like_layout(d["x"]), empty_like_layout(d["x"]),
+                                      empty_like_layout(d["gate"]))
+    cache.decode_chain(d["x"], d["residual"], d["w"], d["q"], d["k"], d["pos"], d["gate"],
+                       d["up"], cfg.eps, cfg.base, y=d["y"], residual_out=d["res_out"],
+                       out=d["out"])
+    torch.cuda.synchronize()
+    want = O.decode_chain(inp, cfg.eps, cfg.base, cfg.dtype)
+    for n in ("y", "q", "k", "out"):
+        check(n, host(d[n]), want[n], cfg.dtype)
+    check("res_out", host(d["res_out"]), want["res_out"], cfg.dtype, exact=True)
+    rec = cache.last_selection().as_tuple()
+    assert rec == expected_record(model_chain_call(d, cfg.eps, cfg.base), 0)
+    assert rec[3] == S.CH_SEQ and rec[4] == 3
+
+
+def test_empty_calls_launch_nothing(tri, cache):
+    x = torch.zeros((0, 4096), dtype=torch.bfloat16, device=DEV)
+    w = torch.ones(4096, dtype=torch.bfloat16, device=DEV)
+    cache.rmsnorm(x, w)
+    g = torch.zeros((0, 128), dtype=torch.float32, device=DEV)
+    cache.swiglu(g, g)
+    s = cache.stats()
+    assert s["empty"] == 2 and s["n_versions"] == 0 and s["errors"] == 0
+
+
+def test_miss_then_hit_and_stats(tri, cache):
+    r = rng(1)
+    x = wl.to_torch(wl.host_array(r, (2, 4096), nm.BF16), nm.BF16, DEV)
+    w = wl.to_torch(wl.host_weight(r, 4096, nm.BF16), nm.BF16, DEV)
+    for _ in range(5):
+        cache.rmsnorm(x, w)
+    torch.cuda.synchronize()
+    s = cache.stats()
+    assert (s["calls"], s["hits"], s["misses"], s["installs"]) == (6, 5, 1, 1)
+    assert cache.version_info(0).hits == 5
+
+
+def test_empty_kernel_launch(tri, cache):
+    for _ in range(10):
+        cache.launch_empty()
+    torch.cuda.synchronize()
+
+
+def test_invalid_arguments_raise_and_launch_nothing(tri, cache):
+    x = torch.zeros((2, 64), dtype=torch.float32, device=DEV)
+    w = torch.ones(64, dtype=torch.float32, device=DEV)
+    with pytest.raises(tri.TriError) as e:
+        cache.rmsnorm(x, w, eps=float("nan"))
+    assert e.value.status == tri.E_INVALID
+    assert cache.stats()["n_versions"] == 0
+
+
+# ---- full-size prefill chain, sampled ------------------------------------------------------
+def test_prefill_chain_full_size_sampled(tri, cache):
+    cfg = wl.PREFILL_8K
+    d = wl.device_inputs(cfg, DEV)
+    src = {k: v.clone() for k, v in d.items() if k in ("q", "k")}
+    y, ro, out = cache.decode_chain(d["x"], d["residual"], d["w"], d["q"], d["k"], d["pos"],
+                                    d["gate"], d["up"], cfg.eps, cfg.base)
+    torch.cuda.synchronize()
+    rec = cache.last_selection()
+    assert rec.variant == S.CH_FUSED and rec.launch[0].grid_x == 2048 + 2048 + 28672
+    rows = np.sort(rng(99).choice(cfg.T, size=40, replace=False))
+    rows = np.concatenate([[0, 1, 2, 3, cfg.T - 1], rows])
+    ri = torch.from_numpy(rows).to(DEV)
+    x, r, w = host(d["x"][ri]), host(d["residual"][ri]), host(d["w"])
+    wy, wh = O.residual_rmsnorm(x, r, w, cfg.eps, cfg.dtype)
+    check("y", host(y[ri]), wy, cfg.dtype)
+    check("res_out", host(ro[ri]), wh, cfg.dtype, exact=True)
+    pos = host(d["pos"][ri])
+    wq, wk = O.rope_qk(host(src["q"][ri]), host(src["k"][ri]), pos, cfg.base, cfg.dtype)
+    check("q", host(d["q"][ri]), wq, cfg.dtype)
+    check("k", host(d["k"][ri]), wk, cfg.dtype)
+    check("out", host(out[ri]), O.swiglu(host(d["gate"][ri]), host(d["up"][ri]), cfg.dtype),
+          cfg.dtype)
+
+
+# ---- mixed-shape stream -----------------------------------------------------------------------
+def test_mixed_stream_selection_and_outputs(tri, cache):
+    """The first 400 calls of the mixed stream on real buffers: every selection
+    record against the oracle's model, outputs against the oracle every 20th."""
+    Tmax = max(wl.MIXED_T_CHOICES)
+    H, I, nq, nk, hd = wl.MIXED_H, wl.MIXED_I, wl.MIXED_NQ, wl.MIXED_NK, wl.MIXED_HD
+    bufs = {}
+    model = S.SpecCacheModel()
+    for n, (T, dt, layout) in enumerate(wl.mixed_stream(n=400)):
+        key = (dt, layout)
+        if key not in bufs:
+            r = rng(len(bufs) + 1)
+            h = dict(x=wl.host_array(r, (Tmax, H), dt), residual=wl.host_array(r, (Tmax, H), dt),
+                     q=wl.host_array(r, (Tmax, nq, hd), dt), k=wl.host_array(r, (Tmax, nk, hd), dt),
+                     gate=wl.host_array(r, (Tmax, I), dt), up=wl.host_array(r, (Tmax, I), dt))
+            dd = {k: place(v, dt, layout, pad=wl.MIXED_PAD) for k, v in h.items()}
+            dd["w"] = wl.to_torch(wl.host_weight(r, H, dt), dt, DEV)
+            dd["pos"] = torch.from_numpy(
+                r.integers(0, wl.MIXED_POS_MAX + 1, Tmax).astype(np.int32)).to(DEV)
+            for o, s in (("y", "x"), ("res_out", "x"), ("out", "gate")):
+                dd[o] = empty_like_layout(dd[s])
+            bufs[key] = (h, dd)
+        h, dd = bufs[key]
+        d = {k: v[:T] for k, v in dd.items() if k != "w"}
+        d["w"] = dd["w"]
+        check_out = n % 20 == 0
+        if check_out:
+            q0, k0 = host(d["q"]), host(d["k"])
+        cache.decode_chain(d["x"], d["residual"], d["w"], d["q"], d["k"], d["pos"], d["gate"],
+                           d["up"], 1e-6, wl.MIXED_BASE, y=d["y"], residual_out=d["res_out"],
+                           out=d["out"])
+        call = model_chain_call(d, 1e-6, wl.MIXED_BASE)
+        if model.call(call) == S.MISS:
+            model.install_last_miss()
+            model.call(call)
+        assert cache.last_selection().as_tuple() == model.last.as_tuple(), (n, T, dt, layout)
+        if check_out:
+            torch.cuda.synchronize()
+            inp = dict(x=host(d["x"]), residual=host(d["residual"]), w=host(d["w"]), q=q0, k=k0,
+                       pos=host(d["pos"]), gate=host(d["gate"]), up=host(d["up"]))
+            want = O.decode_chain(inp, 1e-6, wl.MIXED_BASE, dt)
+            for nme in ("y", "q", "k", "out"):
+                check(f"{n}:{nme}", host(d[nme]), want[nme], dt)
+            check(f"{n}:res_out", host(d["res_out"]), want["res_out"], dt, exact=True)
+    torch.cuda.synchronize()
+    s = cache.stats()
+    assert s["misses"] == model.stats.misses and s["n_versions"] == len(model.versions)

@@ -1,0 +1,340 @@
+"""The native cache core on the CPU, against the recording launch backend.
+
+Checks the library's guards, ordered dispatch (Algorithm 1, Sec. 3.2), the
+miss / install / error paths (Sec. 3.5), argument preparation and the
+selection records -- bit for bit against the oracle's selection model.
+"""
+import ctypes as C
+import math
+import struct
+
+import numpy as np
+import pytest
+
+from oracle import ops as O
+from oracle import selection as S
+from tests.native_libs import load_fake
+from tests.selection_calls import (chain_call, elem_offset, res_call, rn_call, rope_call,
+                                   sw_call)
+import workloads as wl
+
+BF, F = S.DT_BF16, S.DT_F32
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return load_fake()
+
+
+@pytest.fixture
+def fresh(lib):
+    caches = []
+
+    def make(capacity=0, flags=0):
+        lib.trifake_reset()
+        h = C.c_void_p()
+        assert lib.tri_spec_cache_create(C.byref(h), capacity, flags) == 0
+        caches.append(h)
+        return h
+    yield make
+    for h in caches:
+        lib.tri_spec_cache_destroy(h)
+
+
+def c_call(lib, cache, c: S.Call, stream=None):
+    from paper_2609_37241_amd._lib import ChainArgs
+    p, s = c.ptr, c.stride
+    if c.op == S.OP_RMSNORM:
+        return lib.tri_rmsnorm(cache, c.dtype, p.get("x"), s["x"], p.get("w"), p.get("y"),
+                               s["y"], c.T, c.H, c.eps, stream)
+    if c.op == S.OP_RES_RMSNORM:
+        return lib.tri_residual_rmsnorm(cache, c.dtype, p.get("x"), s["x"], p.get("res"),
+                                        s["res"], p.get("w"), p.get("y"), s["y"],
+                                        p.get("res_out"), s["res_out"], c.T, c.H, c.eps, stream)
+    if c.op == S.OP_ROPE_QK:
+        return lib.tri_rope_qk(cache, c.dtype, p.get("q"), s["q"], p.get("k"), s["k"],
+                               p.get("pos"), c.T, c.nq, c.nk, c.hd, c.base, stream)
+    if c.op == S.OP_SWIGLU:
+        return lib.tri_swiglu(cache, c.dtype, p.get("gate"), s["gate"], p.get("up"), s["up"],
+                              p.get("out"), s["out"], c.T, c.I, stream)
+    a = ChainArgs()
+    a.dtype, a.nq, a.nk, a.hd = c.dtype, c.nq, c.nk, c.hd
+    a.T, a.H, a.I, a.eps, a.base = c.T, c.H, c.I, c.eps, c.base
+    a.x, a.x_rs = p.get("x"), s["x"]
+    a.res, a.res_rs = p.get("res"), s["res"]
+    a.w = p.get("w")
+    a.y, a.y_rs = p.get("y"), s["y"]
+    a.res_out, a.ro_rs = p.get("res_out"), s["res_out"]
+    a.q, a.q_ts = p.get("q"), s["q"]
+    a.k, a.k_ts = p.get("k"), s["k"]
+    a.pos = p.get("pos")
+    a.gate, a.g_rs = p.get("gate"), s["gate"]
+    a.up, a.u_rs = p.get("up"), s["up"]
+    a.out, a.o_rs = p.get("out"), s["out"]
+    return lib.tri_decode_chain(cache, C.byref(a), stream)
+
+
+def c_record(lib, cache):
+    from paper_2609_37241_amd._lib import Selection
+    sel = Selection()
+    assert lib.tri_spec_last_selection(cache, C.byref(sel)) == 0
+    return sel.as_tuple()
+
+
+def c_stats(lib, cache):
+    from paper_2609_37241_amd._lib import Stats
+    st = Stats()
+    lib.tri_spec_stats(cache, C.byref(st))
+    return (st.calls, st.hits, st.misses, st.errors, st.empty, st.installs, st.n_versions)
+
+
+def m_stats(m):
+    s = m.stats
+    return (s.calls, s.hits, s.misses, s.errors, s.empty, s.installs, len(m.versions))
+
+
+def c_install(lib, cache):
+    from paper_2609_37241_amd._lib import Selection
+    sel = Selection()
+    st = lib.tri_spec_install_last_miss(cache, C.byref(sel))
+    return st, (sel.as_tuple() if st == 0 else None)
+
+
+def run_both(lib, cache, m, c, install=True):
+    """Call both sides (installing on a miss) and compare every observable."""
+    st_c = c_call(lib, cache, c)
+    st_m = m.call(c)
+    assert st_c == st_m, (c, st_c, st_m)
+    assert c_record(lib, cache) == m.last.as_tuple(), c
+    if st_c == S.MISS and install:
+        ic, rc = c_install(lib, cache)
+        im, rm = m.install_last_miss()
+        assert ic == im
+        if ic == 0:
+            assert rc == rm.as_tuple()
+            st_c = c_call(lib, cache, c)
+            st_m = m.call(c)
+            assert st_c == st_m == S.OK
+            assert c_record(lib, cache) == m.last.as_tuple()
+    assert c_stats(lib, cache) == m_stats(m)
+    assert lib.trifake_launch_count() == m.launch_count
+    return st_c
+
+
+def call_zoo():
+    """Calls over every op, dtype, size class, layout and error kind."""
+    calls = []
+    for d in (F, BF):
+        off = elem_offset(d)
+        for T in (0, 1, 2, 3, 4, 5, 8, 9, 64, 65, 512, 8192):
+            for H in (64, 256, 520, 4096, 8192, 16384, 40000, 100):
+                calls.append(rn_call(d, T, H))
+                calls.append(res_call(d, T, H))
+            calls.append(rn_call(d, T, 4096, off=off))
+            calls.append(res_call(d, T, 4096, pad=64))
+            for nq, nk, hd in ((4, 4, 64), (32, 32, 128), (32, 8, 128), (64, 8, 128),
+                               (4, 0, 64), (2, 2, 96), (1, 1, 2), (8, 8, 512)):
+                calls.append(rope_call(d, T, nq, nk, hd))
+            calls.append(rope_call(d, T, 32, 8, 128, base=500000.0, off=off))
+            calls.append(rope_call(d, T, 32, 8, 128, pad=64))
+            for I in (688, 11008, 14336, 28672, 11003, 1):
+                calls.append(sw_call(d, T, I))
+            calls.append(sw_call(d, T, 11008, off=off))
+            calls.append(sw_call(d, T, 11008, pad=64))
+            calls.append(sw_call(d, T, 11003, pad=1))
+            calls.append(chain_call(d, T, 4096, 11008, 32, 32, 128))
+            calls.append(chain_call(d, T, 8192, 28672, 64, 8, 128, base=500000.0))
+            calls.append(chain_call(d, T, 256, 688, 4, 4, 64))
+            calls.append(chain_call(d, T, 4096, 14336, 32, 8, 128, sw_pad=64))
+            calls.append(chain_call(d, T, 4096, 14336, 32, 8, 128, rope_off=off))
+            calls.append(chain_call(d, T, 40000, 11008, 32, 32, 128))
+    # errors
+    calls += [rn_call(BF, 1, 4096, null=("x",)), rn_call(BF, -1, 4096), rn_call(BF, 1, 0),
+              rn_call(BF, 1, 4096, eps=float("nan")), rn_call(BF, 1, 4096, eps=-1.0),
+              rn_call(BF, 1, 4096, eps=float("inf")), rn_call(BF, 1, 4096, eps=1e39),
+              rn_call(BF, 1, 4096, off=1), rn_call(7, 1, 4096), rn_call(BF, S.T_MAX + 1, 64),
+              rn_call(BF, S.T_MAX, 64), rn_call(BF, 1, S.H_LIMIT), rn_call(BF, 1, S.H_LIMIT - 1),
+              res_call(BF, 2, 4096, null=("res_out",)), res_call(F, 2, 64, pad=-1),
+              rope_call(BF, 1, 4, 4, 63), rope_call(BF, 1, 4, 4, 0), rope_call(BF, 1, 4, 4, 1024),
+              rope_call(BF, 1, 4, 4, 64, base=1.0), rope_call(BF, 1, 4, 4, 64, base=float("nan")),
+              rope_call(BF, 1, 4, 4, 64, pos_off=2), rope_call(BF, 1, 0, 4, 64),
+              rope_call(BF, 1, 4, -1, 64), rope_call(BF, 1, 5000, 4, 64),
+              rope_call(BF, 1, 4, 4, 64, null=("k",)), rope_call(BF, 1, 4, 0, 64, null=("k",)),
+              rope_call(BF, 1, 4, 4, 64, null=("pos",)), rope_call(BF, 1, 4, 4, 64, off=1),
+              rope_call(BF, 1, 4, 4, 64, pad=-1),
+              sw_call(BF, 1, 0), sw_call(BF, 1, S.I_LIMIT), sw_call(BF, 1, 64, null=("up",)),
+              sw_call(BF, 1, 64, off=1), sw_call(BF, 3, 64, pad=-1)]
+    return calls
+
+
+def test_selection_parity_over_call_zoo(lib, fresh):
+    cache = fresh(capacity=4096)
+    m = S.SpecCacheModel(capacity=4096)
+    for c in call_zoo():
+        run_both(lib, cache, m, c)
+    # second pass: everything installed now hits (or errors) identically
+    for c in call_zoo():
+        st = run_both(lib, cache, m, c)
+        assert st != S.MISS
+
+
+def test_selection_parity_mixed_stream(lib, fresh):
+    # The full mixed-shape stream: 10,000 chain calls with token counts from
+    # 1..512, 90 % bf16, 5 % unaligned or padded layouts.
+    cache = fresh()
+    m = S.SpecCacheModel()
+    for T, dt, layout in wl.mixed_stream():
+        d = BF if dt == wl.BF16 else F
+        off = elem_offset(d) if layout == wl.LAYOUT_UNALIGNED else 0
+        pad = wl.MIXED_PAD if layout == wl.LAYOUT_STRIDED else 0
+        c = chain_call(d, T, wl.MIXED_H, wl.MIXED_I, wl.MIXED_NQ, wl.MIXED_NK, wl.MIXED_HD,
+                       res_off=off, rope_off=off, sw_off=off, res_pad=pad, rope_pad=pad,
+                       sw_pad=pad)
+        run_both(lib, cache, m, c)
+    # one miss per distinct key: 9 token buckets x 2 dtypes x 3 layouts at most
+    assert m.stats.misses == len(m.versions) <= 54
+    assert m.stats.hits == wl.MIXED_CALLS
+
+
+def test_auto_install_parity(lib, fresh):
+    cache = fresh(flags=1)
+    m = S.SpecCacheModel(flags=S.FLAG_AUTO_INSTALL)
+    for c in call_zoo()[:400]:
+        run_both(lib, cache, m, c, install=False)
+
+
+def test_capacity_full(lib, fresh):
+    cache = fresh(capacity=2)
+    m = S.SpecCacheModel(capacity=2)
+    for T in (1, 2, 4, 8):
+        run_both(lib, cache, m, sw_call(BF, T, 128))
+    assert c_install(lib, cache)[0] == S.E_FULL
+    cache2 = fresh(capacity=1, flags=1)
+    m2 = S.SpecCacheModel(capacity=1, flags=S.FLAG_AUTO_INSTALL)
+    for T in (1, 2):
+        run_both(lib, cache2, m2, sw_call(BF, T, 128), install=False)
+    assert c_record(lib, cache2)[1] == S.E_FULL
+
+
+@pytest.mark.parametrize("fail_at", [0, 1, 2])
+def test_launch_failure_stops_dispatch(lib, fresh, fail_at):
+    cache = fresh()
+    m = S.SpecCacheModel()
+    c = chain_call(BF, 4, 4096, 11008, 32, 32, 128, sw_pad=64)    # three launches
+    run_both(lib, cache, m, c)
+    base = lib.trifake_launch_count()
+    lib.trifake_fail_at(base + fail_at)
+    m.launch_fails = {base + fail_at}
+    assert run_both(lib, cache, m, c) == S.E_LAUNCH
+    assert lib.trifake_launch_count() == base + fail_at + 1
+    # the version is kept and the next call hits
+    lib.trifake_fail_at(-1)
+    m.launch_fails = set()
+    assert run_both(lib, cache, m, c) == S.OK
+
+
+def test_install_needs_a_miss_and_is_idempotent(lib, fresh):
+    cache = fresh()
+    assert c_install(lib, cache)[0] == S.E_INVALID
+    c = rope_call(BF, 1, 32, 32, 128)
+    assert c_call(lib, cache, c) == S.MISS
+    assert c_call(lib, cache, c) == S.MISS
+    assert c_install(lib, cache)[0] == 0
+    assert c_install(lib, cache)[0] == 0
+    assert c_stats(lib, cache)[-1] == 1
+    assert lib.trifake_upload_count() == 1
+
+
+def test_create_errors(lib):
+    h = C.c_void_p()
+    assert lib.tri_spec_cache_create(C.byref(h), 4097, 0) == S.E_INVALID
+    assert lib.tri_spec_cache_create(C.byref(h), 0, 2) == S.E_INVALID
+    assert lib.tri_spec_cache_create(None, 0, 0) == S.E_INVALID
+    lib.trifake_init_status(S.E_RUNTIME)
+    assert lib.tri_spec_cache_create(C.byref(h), 0, 0) == S.E_RUNTIME
+    lib.trifake_reset()
+    assert lib.tri_rmsnorm(None, 1, 1, 1, 1, 1, 1, 1, 1, 1e-6, None) == S.E_INVALID
+    assert lib.tri_decode_chain(None, None, None) == S.E_INVALID
+
+
+def test_chain_null_args(lib, fresh):
+    cache = fresh()
+    assert lib.tri_decode_chain(cache, None, None) == S.E_INVALID
+    assert c_stats(lib, cache)[3] == 1
+
+
+def test_status_strings(lib):
+    assert lib.tri_status_str(1) == b"TRI_MISS"
+    assert lib.tri_status_str(-5) == b"TRI_E_LAUNCH"
+    assert lib.tri_status_str(42) == b"TRI_UNKNOWN"
+
+
+# ---- argument preparation ----------------------------------------------------------
+def _last_launch(lib, nbytes=256):
+    i = lib.trifake_launch_count() - 1
+    kv, dt, sub = C.c_int32(), C.c_int32(), C.c_int32()
+    grid, block = C.c_uint32(), C.c_uint32()
+    stream = C.c_void_p()
+    buf = C.create_string_buffer(256)
+    assert lib.trifake_get(i, C.byref(kv), C.byref(dt), C.byref(sub), C.byref(grid),
+                           C.byref(block), C.byref(stream), buf, nbytes) == 0
+    return kv.value, dt.value, sub.value, grid.value, block.value, stream.value, buf.raw
+
+
+def test_rmsnorm_argument_block_and_stream(lib, fresh):
+    cache = fresh(flags=1)
+    c = res_call(BF, 5, 4096, pad=64)
+    assert c_call(lib, cache, c, stream=0xABC0) == 0
+    kv, dt, sub, grid, block, stream, raw = _last_launch(lib)
+    assert (kv, dt, sub, grid, block, stream) == (14, BF, 1, 2, 256, 0xABC0)
+    f = struct.unpack_from("<5Q4qqif", raw)
+    p = c.ptr
+    assert f[:5] == (p["x"], p["res"], p["w"], p["y"], p["res_out"])
+    assert f[5:9] == (4160,) * 4 and f[9:11] == (5, 4096)
+    assert f[11] == np.float32(1e-6)
+
+
+def test_chain_argument_block(lib, fresh):
+    cache = fresh(flags=1)
+    c = chain_call(BF, 8, 4096, 14336, 32, 8, 128, base=500000.0)
+    assert c_call(lib, cache, c) == 0
+    kv, dt, sub, grid, block, _, raw = _last_launch(lib)
+    # fused kernel: RN_WAVE_8 (NV index 3), one RoPE token per block, U = 1
+    assert (kv, dt, sub, grid, block) == (50, BF, 3 * 4, 2 + 8 + 56, 256)
+    rope = struct.unpack_from("<4Q3q4i", raw, 88)
+    assert rope[0] == c.ptr["q"] and rope[1] == c.ptr["k"] and rope[2] == c.ptr["pos"]
+    assert rope[4:7] == (32 * 128, 8 * 128, 8) and rope[7:10] == (32, 8, 128)
+    sw = struct.unpack_from("<3Q7q", raw, 160)
+    assert sw[:3] == (c.ptr["gate"], c.ptr["up"], c.ptr["out"])
+    assert sw[3:] == (14336, 14336, 14336, 8, 14336, 8 * 14336 // 8, 8 * 14336)
+    assert struct.unpack_from("<2I", raw, 240) == (2, 8)
+    # the RoPE table pointer is this version's uploaded constants
+    assert rope[3] != 0
+
+
+@pytest.mark.parametrize("base,hd", [(10000.0, 64), (10000.0, 128), (500000.0, 128),
+                                     (10000.0, 96), (10000.0, 512), (1234.5, 2),
+                                     (1e6, 256), (2.0, 128)])
+def test_rope_table_matches_oracle_exactly(lib, fresh, base, hd):
+    cache = fresh(flags=1)
+    assert c_call(lib, cache, rope_call(BF, 3, 4, 2, hd, base=base)) == 0
+    n = C.c_uint32()
+    buf = (C.c_float * 256)()
+    assert lib.tri_spec_version_constants(cache, 0, buf, 256, C.byref(n)) == 0
+    got = np.array(buf[: n.value], dtype=np.float32)
+    want = O.rope_inv_freq(base, hd)
+    assert n.value == hd // 2
+    assert np.array_equal(got.view(np.uint32), want.view(np.uint32))
+
+
+def test_version_info(lib, fresh):
+    from paper_2609_37241_amd._lib import VersionInfo
+    cache = fresh(flags=1)
+    c = chain_call(F, 4, 256, 688, 4, 4, 64)
+    for _ in range(3):
+        c_call(lib, cache, c)
+    v = VersionInfo()
+    assert lib.tri_spec_version_info(cache, 0, C.byref(v)) == 0
+    assert (v.variant, tuple(v.roles), v.hits) == (50, (11, 21, 31), 2)
+    assert tuple(v.key) == S.make_key(c)
+    assert lib.tri_spec_version_info(cache, 1, C.byref(v)) == S.E_INVALID
