@@ -200,7 +200,8 @@ def main():
         ch = bandwidth["chain"]
         roofline = {"bound": "hbm", "achieved": ch["GB/s"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                     "frac": ch["GB/s"] / HBM_PEAK_GBS, "traffic": None,
-                    "kernel": "fused decode chain, 8192 tokens (k_chain<bf16, 16, 4, 4>)",
+                    "kernel": "fused decode chain, 8192 tokens (k_chain: block-per-row norm, "
+                              "4-token RoPE blocks, streaming 4-vector SwiGLU)",
                     "bytes_per_launch": ch["bytes"], "avg_launch_us": ch["mean_us"]}
         del db, y, ro, out, flush, copy_src, copy_dst
 
@@ -233,6 +234,8 @@ def main():
                                "SwiGLU) at T=1, hidden 4096, 32+32 heads x 128, "
                                "intermediate 11008, RoPE base 1e4",
                    "accumulate": "f32",
+                   "hip_force_dev_kernarg": os.environ.get("HIP_FORCE_DEV_KERNARG",
+                                                           "unset (runtime default)"),
                    "bandwidth_workload": "prefill8k_bf16: T=8192, hidden 8192, 64+8 heads x "
                                          "128, intermediate 28672, base 5e5, x50 outliers"},
         "latency": latency, "bandwidth_8192": bandwidth, "roofline": roofline,

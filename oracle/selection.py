@@ -38,11 +38,12 @@ E_INVALID, E_UNSUPPORTED, E_FULL, E_NOMEM, E_LAUNCH, E_RUNTIME = -1, -2, -3, -4,
 
 RN_SCALAR = 10
 RN_WAVE = {1: 11, 2: 12, 4: 13, 8: 14, 16: 15}
-RN_BLOCK = {8: 16, 16: 17}
-RN_LOOP = 18
-ROPE_SCALAR, ROPE_VEC_T1, ROPE_VEC_T4 = 20, 21, 22
-SW_SCALAR, SW_FLAT_U1, SW_FLAT_U4, SW_ROWS = 30, 31, 32, 33
+RN_BLOCK = {1: 16, 2: 17, 4: 18, 8: 19, 16: 20}
+RN_LOOP = 21
+ROPE_SCALAR, ROPE_VEC_T1, ROPE_VEC_T4 = 30, 31, 32
+SW_SCALAR, SW_FLAT, SW_FLAT_NT, SW_ROWS, SW_FLAT_U4_NT = 40, 41, 42, 43, 44
 CH_FUSED, CH_SEQ = 50, 51
+DECODE_BUCKET_MAX = 6       # buckets up to here are decode sized
 
 BLOCK = 256
 GRID_CAP = 1 << 20
@@ -104,15 +105,16 @@ def _aligned(es: int, ptrs, strides) -> bool:
 
 
 # ---- role policies -----------------------------------------------------------
-def rn_role(dtype: int, H: int, flags: int, T: int) -> Tuple[int, int]:
+def rn_role(dtype: int, H: int, flags: int, b: int, T: int) -> Tuple[int, int]:
     """(variant, grid) for RMSNorm / residual RMSNorm rows."""
     v = 16 // elem_size(dtype)
     if not (flags & ALIGN) or H % v:
         return RN_SCALAR, T
     nvec = H // v
-    nv = next_pow2(cdiv(nvec, 64))
-    if nv <= 16:
-        return RN_WAVE[nv], cdiv(T, 4)
+    if b <= DECODE_BUCKET_MAX:
+        nv = next_pow2(cdiv(nvec, 64))
+        if nv <= 16:
+            return RN_WAVE[nv], cdiv(T, 4)
     nb = next_pow2(cdiv(nvec, 256))
     if nb <= 16:
         return RN_BLOCK[nb], T
@@ -129,13 +131,16 @@ def rope_role(dtype: int, hd: int, flags: int, b: int, T: int) -> Tuple[int, int
     return ROPE_VEC_T4, cdiv(T, 4)
 
 
-def sw_role(dtype: int, I: int, flags: int, b: int, T: int) -> Tuple[int, int]:
+def sw_role(dtype: int, I: int, flags: int, b: int, T: int,
+            in_chain: bool = False) -> Tuple[int, int]:
     v = 16 // elem_size(dtype)
     if (flags & ALIGN) and (flags & CONTIG):
-        u = 1 if b <= 6 else 4
         nvec = (T * I) // v
-        grid = max(1, min(cdiv(nvec, BLOCK * u), GRID_CAP))
-        return (SW_FLAT_U1 if u == 1 else SW_FLAT_U4), grid
+        if b <= DECODE_BUCKET_MAX:
+            return SW_FLAT, max(1, min(cdiv(nvec, BLOCK), GRID_CAP))
+        if in_chain:
+            return SW_FLAT_U4_NT, max(1, min(cdiv(nvec, 4 * BLOCK), GRID_CAP))
+        return SW_FLAT_NT, max(1, min(cdiv(nvec, BLOCK), GRID_CAP))
     if (flags & ALIGN) and I % v == 0:
         cb = cdiv(I // v, BLOCK)
         return SW_ROWS, min(T * cb, GRID_CAP)
@@ -351,7 +356,7 @@ def plan(key, T: int):
     f = unpack_key(key)
     op, dt, b, fl = f["op"], f["dtype"], f["bucket"], f["flags"]
     if op in (OP_RMSNORM, OP_RES_RMSNORM):
-        v, g = rn_role(dt, f["H"], fl, T)
+        v, g = rn_role(dt, f["H"], fl, b, T)
         return v, (0, 0, 0), [(v, g, BLOCK)]
     if op == OP_ROPE_QK:
         v, g = rope_role(dt, f["hd"], fl, b, T)
@@ -359,13 +364,14 @@ def plan(key, T: int):
     if op == OP_SWIGLU:
         v, g = sw_role(dt, f["I"], fl, b, T)
         return v, (0, 0, 0), [(v, g, BLOCK)]
-    rn = rn_role(dt, f["H"], fl & 3, T)
+    rn = rn_role(dt, f["H"], fl & 3, b, T)
     ro = rope_role(dt, f["hd"], (fl >> 2) & 3, b, T)
-    sw = sw_role(dt, f["I"], (fl >> 4) & 3, b, T)
+    sw = sw_role(dt, f["I"], (fl >> 4) & 3, b, T, in_chain=True)
     roles = (rn[0], ro[0], sw[0])
-    fused = (fl == 0x3F and rn[0] in RN_WAVE.values()
+    fused = (fl == 0x3F
+             and (rn[0] in RN_WAVE.values() or rn[0] in RN_BLOCK.values())
              and ro[0] in (ROPE_VEC_T1, ROPE_VEC_T4)
-             and sw[0] in (SW_FLAT_U1, SW_FLAT_U4))
+             and sw[0] in (SW_FLAT, SW_FLAT_U4_NT))
     if fused:
         return CH_FUSED, roles, [(CH_FUSED, rn[1] + ro[1] + sw[1], BLOCK)]
     return CH_SEQ, roles, [(rn[0], rn[1], BLOCK), (ro[0], ro[1], BLOCK),

@@ -1,6 +1,6 @@
 // The fused decode-chain kernel (bf16): one launch whose workgroups take the
 // residual-RMSNorm, RoPE-QK and SwiGLU roles by blockIdx range. Instantiated
-// for every (rows per lane, RoPE tokens per workgroup, SwiGLU unroll) the
+// for every (norm role variant, RoPE tokens per workgroup, SwiGLU role) the
 // install policy can pick.
 #include "../internal.h"
 #include "device.h"
@@ -8,41 +8,58 @@
 namespace tri {
 using namespace dev;
 
-template <int DT, int NV, int TPB, int U>
+// RNV: RN_WAVE_1..16 (one wavefront per row) or RN_BLOCK_1..16 (one
+// workgroup per row); TPB: RoPE tokens per workgroup; SWV: SW_FLAT (one
+// vector per work-item, cached) or SW_FLAT_U4_NT (four, streaming).
+template <int DT, int RNV, int TPB, int SWV>
 __global__ __launch_bounds__(256) void k_chain(ChainArgs a) {
   __shared__ float lds[2 * TPB * 256];
   const uint32_t b = blockIdx.x;
   if (b < a.rn_blocks) {
-    rn_wave_block<DT, NV, true>(a.rn, b);
+    if constexpr (RNV <= RN_WAVE_16) {
+      rn_wave_block<DT, 1 << (RNV - RN_WAVE_1), true, false>(a.rn, b);
+    } else {
+      __shared__ float red[4];
+      rn_row_regs<DT, 1 << (RNV - RN_BLOCK_1), true, 256, false>(a.rn, b, threadIdx.x, red);
+    }
     return;
   }
   const uint32_t b1 = b - a.rn_blocks;
   if (b1 < a.rope_blocks) {
-    rope_vec_block<DT, TPB>(a.rope, b1, lds);
+    rope_vec_block<DT, TPB, false>(a.rope, b1, lds);
     return;
   }
-  sw_flat_part<DT, U>(a.sw, b1 - a.rope_blocks, gridDim.x - a.rn_blocks - a.rope_blocks);
+  const uint32_t nsw = gridDim.x - a.rn_blocks - a.rope_blocks;
+  if constexpr (SWV == SW_FLAT_U4_NT)
+    sw_flat_part<DT, 4, true>(a.sw, b1 - a.rope_blocks, nsw);
+  else
+    sw_flat_part<DT, 1, false>(a.sw, b1 - a.rope_blocks, nsw);
 }
 
 namespace {
-template <int DT, int NV>
-const void *chain_pick_nv(bool t4, bool u4) {
-  if (t4) return u4 ? reinterpret_cast<const void *>(&k_chain<DT, NV, 4, 4>)
-                    : reinterpret_cast<const void *>(&k_chain<DT, NV, 4, 1>);
-  return u4 ? reinterpret_cast<const void *>(&k_chain<DT, NV, 1, 4>)
-            : reinterpret_cast<const void *>(&k_chain<DT, NV, 1, 1>);
+template <int RNV>
+const void *chain_pick_rn(bool t4, bool u4) {
+  if (t4) return u4 ? reinterpret_cast<const void *>(&k_chain<kBF16, RNV, 4, SW_FLAT_U4_NT>)
+                    : reinterpret_cast<const void *>(&k_chain<kBF16, RNV, 4, SW_FLAT>);
+  return u4 ? reinterpret_cast<const void *>(&k_chain<kBF16, RNV, 1, SW_FLAT_U4_NT>)
+            : reinterpret_cast<const void *>(&k_chain<kBF16, RNV, 1, SW_FLAT>);
 }
 }  // namespace
 
-// sub = (index of NV in 1,2,4,8,16) * 4 + (4 RoPE tokens per block) * 2 + (SwiGLU unroll 4).
+// sub = (norm role - RN_WAVE_1) * 4 + (4 RoPE tokens per block) * 2 + (SwiGLU U4 streaming).
 const void *chain_kernel_bf16(int32_t sub) {
   const bool t4 = (sub >> 1) & 1, u4 = sub & 1;
-  switch (sub >> 2) {
-    case 0: return chain_pick_nv<kBF16, 1>(t4, u4);
-    case 1: return chain_pick_nv<kBF16, 2>(t4, u4);
-    case 2: return chain_pick_nv<kBF16, 4>(t4, u4);
-    case 3: return chain_pick_nv<kBF16, 8>(t4, u4);
-    case 4: return chain_pick_nv<kBF16, 16>(t4, u4);
+  switch (RN_WAVE_1 + (sub >> 2)) {
+    case RN_WAVE_1: return chain_pick_rn<RN_WAVE_1>(t4, u4);
+    case RN_WAVE_2: return chain_pick_rn<RN_WAVE_2>(t4, u4);
+    case RN_WAVE_4: return chain_pick_rn<RN_WAVE_4>(t4, u4);
+    case RN_WAVE_8: return chain_pick_rn<RN_WAVE_8>(t4, u4);
+    case RN_WAVE_16: return chain_pick_rn<RN_WAVE_16>(t4, u4);
+    case RN_BLOCK_1: return chain_pick_rn<RN_BLOCK_1>(t4, u4);
+    case RN_BLOCK_2: return chain_pick_rn<RN_BLOCK_2>(t4, u4);
+    case RN_BLOCK_4: return chain_pick_rn<RN_BLOCK_4>(t4, u4);
+    case RN_BLOCK_8: return chain_pick_rn<RN_BLOCK_8>(t4, u4);
+    case RN_BLOCK_16: return chain_pick_rn<RN_BLOCK_16>(t4, u4);
     default: return nullptr;
   }
 }

@@ -81,6 +81,25 @@ struct Elt<kBF16> {
   }
 };
 
+// 16-byte global access; NT marks streaming data (nontemporal: the line is
+// not kept in the caches for reuse), used where the working set is far larger
+// than the caches.
+template <bool NT>
+__device__ inline u32x4 ld16(const u32x4 *p) {
+  if constexpr (NT)
+    return __builtin_nontemporal_load(p);
+  else
+    return *p;
+}
+
+template <bool NT>
+__device__ inline void st16(u32x4 *p, const u32x4 &v) {
+  if constexpr (NT)
+    __builtin_nontemporal_store(v, p);
+  else
+    *p = v;
+}
+
 // ---- reductions ----------------------------------------------------------------
 // Butterfly over the 64 lanes: every lane ends with the same, bitwise equal
 // total (each exchange adds the same two operands on both partners).
@@ -107,28 +126,42 @@ __device__ inline T block_sum(T v, T *red) {
 // One row held in registers: lane `lane` of LANES owns vectors lane + LANES*k,
 // k < NV. With RES, h = RN(x + r) is written to res_out and normalised.
 // LANES = 64: one wavefront per row, no barrier. LANES = 256: one workgroup.
-template <int DT, int NV, bool RES, int LANES>
+// Without NT (decode sizes) the weight vectors are requested together with the
+// row, so the row costs one memory round trip; with NT (streaming sizes) they
+// are loaded after the reduction to keep fewer registers live.
+template <int DT, int NV, bool RES, int LANES, bool NT>
 __device__ __forceinline__ void rn_row_regs(const RnArgs &a, int64_t row, int lane, float *red) {
   using E = Elt<DT>;
   constexpr int V = E::V;
   const int nvec = a.H / V;
   const u32x4 *xr = reinterpret_cast<const u32x4 *>(static_cast<const char *>(a.x) +
                                                      row * a.x_rs * E::ES);
+  const u32x4 *wr = static_cast<const u32x4 *>(a.w);
   u32x4 xv[NV];
 #pragma unroll
   for (int k = 0; k < NV; ++k) {
     const int vi = lane + LANES * k;
-    xv[k] = vi < nvec ? xr[vi] : u32x4{0, 0, 0, 0};
+    xv[k] = vi < nvec ? ld16<NT>(xr + vi) : u32x4{0, 0, 0, 0};
   }
+  u32x4 rv[RES ? NV : 1];
   if constexpr (RES) {
     const u32x4 *rr = reinterpret_cast<const u32x4 *>(static_cast<const char *>(a.res) +
                                                        row * a.res_rs * E::ES);
-    u32x4 rv[NV];
 #pragma unroll
     for (int k = 0; k < NV; ++k) {
       const int vi = lane + LANES * k;
-      rv[k] = vi < nvec ? rr[vi] : u32x4{0, 0, 0, 0};
+      rv[k] = vi < nvec ? ld16<NT>(rr + vi) : u32x4{0, 0, 0, 0};
     }
+  }
+  u32x4 wv[NT ? 1 : NV];
+  if constexpr (!NT) {
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+      const int vi = lane + LANES * k;
+      wv[k] = vi < nvec ? wr[vi] : u32x4{0, 0, 0, 0};
+    }
+  }
+  if constexpr (RES) {
     u32x4 *orow = reinterpret_cast<u32x4 *>(static_cast<char *>(a.res_out) + row * a.ro_rs * E::ES);
 #pragma unroll
     for (int k = 0; k < NV; ++k) {
@@ -139,7 +172,7 @@ __device__ __forceinline__ void rn_row_regs(const RnArgs &a, int64_t row, int la
       for (int e = 0; e < V; ++e) f[e] += g[e];
       xv[k] = E::pack(f);
       const int vi = lane + LANES * k;
-      if (vi < nvec) orow[vi] = xv[k];
+      if (vi < nvec) st16<NT>(orow + vi, xv[k]);
     }
   }
   float ss = 0.0f;
@@ -155,7 +188,6 @@ __device__ __forceinline__ void rn_row_regs(const RnArgs &a, int64_t row, int la
   else
     ss = block_sum(ss, red);
   const float inv = rsqrtf(ss / float(a.H) + a.eps);
-  const u32x4 *wr = static_cast<const u32x4 *>(a.w);
   u32x4 *yr = reinterpret_cast<u32x4 *>(static_cast<char *>(a.y) + row * a.y_rs * E::ES);
 #pragma unroll
   for (int k = 0; k < NV; ++k) {
@@ -163,20 +195,23 @@ __device__ __forceinline__ void rn_row_regs(const RnArgs &a, int64_t row, int la
     if (vi < nvec) {
       float f[V], w[V];
       E::unpack(xv[k], f);
-      E::unpack(wr[vi], w);
+      if constexpr (NT)
+        E::unpack(wr[vi], w);
+      else
+        E::unpack(wv[k], w);
 #pragma unroll
       for (int e = 0; e < V; ++e) f[e] = (f[e] * inv) * w[e];
-      yr[vi] = E::pack(f);
+      st16<NT>(yr + vi, E::pack(f));
     }
   }
 }
 
 // Workgroup `blk` of the one-wavefront-per-row layout: rows 4*blk .. 4*blk+3.
-template <int DT, int NV, bool RES>
+template <int DT, int NV, bool RES, bool NT>
 __device__ __forceinline__ void rn_wave_block(const RnArgs &a, int64_t blk) {
   const int64_t row = blk * 4 + (threadIdx.x >> 6);
   if (row >= a.T) return;
-  rn_row_regs<DT, NV, RES, 64>(a, row, threadIdx.x & 63, nullptr);
+  rn_row_regs<DT, NV, RES, 64, NT>(a, row, threadIdx.x & 63, nullptr);
 }
 
 // Long rows: two passes over global memory with float64 accumulation (each
@@ -284,59 +319,100 @@ __device__ __forceinline__ char *rope_head(const RopeArgs &a, int64_t t, int h, 
 
 // TPB tokens per workgroup. Each half-head is cpb = (hd/2)/V 16-byte
 // vectors (a power of two); work-item `tid` owns chunk tid % cpb of heads
-// tid / cpb, tid / cpb + 256 / cpb, ... and reads its V angles once per token.
-template <int DT, int TPB>
+// tid / cpb, tid / cpb + 256 / cpb, ... of every token of the block. Its
+// (token, head) items are processed PF at a time with all loads issued before
+// any use, and the first batch is requested before the angle math and the
+// barrier, so at decode sizes the block costs one memory round trip.
+template <int DT, int TPB, bool NT>
 __device__ __forceinline__ void rope_vec_block(const RopeArgs &a, int64_t blk, float *lds) {
   using E = Elt<DT>;
   constexpr int V = E::V;
+  constexpr int PF = 4;
   const int half = a.hd >> 1;
-  float *cs = lds;
-  float *sn = lds + TPB * 256;
-  const int64_t t0 = blk * TPB;
-  // half = cpb * V is a power of two here: (token, pair) = (e >> lh, e & (half - 1)).
   const int lh = __builtin_ctz(unsigned(half));
-  for (int e = threadIdx.x; e < TPB * half; e += kThreads) {
-    const int64_t t = t0 + (e >> lh);
-    const int i = e & (half - 1);
-    float c = 1.0f, s = 0.0f;
-    if (t < a.T) {
-      const float th = float(a.pos[t]) * a.inv_freq[i];
-      sincosf(th, &s, &c);
-    }
-    cs[e] = c;
-    sn[e] = s;
-  }
-  __syncthreads();
   const int cpb = half / V;
   const int shift = __builtin_ctz(unsigned(cpb));
   const int chunk = threadIdx.x & (cpb - 1);
   const int hg = threadIdx.x >> shift;
   const int hstep = kThreads >> shift;
   const int nh = a.nq + a.nk;
-  for (int tt = 0; tt < TPB; ++tt) {
-    const int64_t t = t0 + tt;
-    if (t >= a.T) break;
-    float c[V], s[V];
+  const int64_t t0 = blk * TPB;
+  const int64_t tlast = a.T - 1;
+  float *cs = lds;
+  float *sn = lds + TPB * 256;
+  const int na = TPB * half;
+
+  // Operands of this work-item's angle slot (token t0 + tid / half, pair
+  // tid % half); indices are clamped so the loads are always in bounds.
+  const int ia = threadIdx.x & (half - 1);
+  const int64_t ta = t0 + (threadIdx.x >> lh);
+  const int32_t pa = a.pos[ta <= tlast ? ta : tlast];
+  const float ina = a.inv_freq[ia];
+
+  int tt = 0, h = hg;
+  const int hfirst = hg < nh ? hg : nh - 1;
+  u32x4 x1[PF], x2[PF];
+  int it[PF], ih[PF];
+  bool ok[PF];
+  auto gather = [&]() {
 #pragma unroll
-    for (int j = 0; j < V; ++j) {
-      c[j] = cs[tt * half + chunk * V + j];
-      s[j] = sn[tt * half + chunk * V + j];
-    }
-    for (int h = hg; h < nh; h += hstep) {
-      char *base = rope_head(a, t, h, E::ES);
-      u32x4 *p1 = reinterpret_cast<u32x4 *>(base) + chunk;
-      u32x4 *p2 = reinterpret_cast<u32x4 *>(base + half * E::ES) + chunk;
-      float f1[V], f2[V], o1[V], o2[V];
-      E::unpack(*p1, f1);
-      E::unpack(*p2, f2);
-#pragma unroll
-      for (int j = 0; j < V; ++j) {
-        o1[j] = f1[j] * c[j] - f2[j] * s[j];
-        o2[j] = f2[j] * c[j] + f1[j] * s[j];
+    for (int j = 0; j < PF; ++j) {
+      ok[j] = tt < TPB && t0 + tt <= tlast && h < nh;
+      it[j] = ok[j] ? tt : 0;
+      ih[j] = ok[j] ? h : hfirst;
+      const char *b = rope_head(a, t0 + it[j], ih[j], E::ES);
+      x1[j] = ld16<NT>(reinterpret_cast<const u32x4 *>(b) + chunk);
+      x2[j] = ld16<NT>(reinterpret_cast<const u32x4 *>(b + half * E::ES) + chunk);
+      if (ok[j]) {
+        h += hstep;
+        if (h >= nh) {
+          h = hg;
+          ++tt;
+        }
       }
-      *p1 = E::pack(o1);
-      *p2 = E::pack(o2);
     }
+  };
+  gather();
+
+  if (na <= kThreads) {
+    if (threadIdx.x < na) {
+      float c = 1.0f, s = 0.0f;
+      if (ta <= tlast) sincosf(float(pa) * ina, &s, &c);
+      cs[threadIdx.x] = c;
+      sn[threadIdx.x] = s;
+    }
+  } else {
+    for (int e = threadIdx.x; e < na; e += kThreads) {
+      const int64_t t = t0 + (e >> lh);
+      const int i = e & (half - 1);
+      float c = 1.0f, s = 0.0f;
+      if (t <= tlast) sincosf(float(a.pos[t]) * a.inv_freq[i], &s, &c);
+      cs[e] = c;
+      sn[e] = s;
+    }
+  }
+  __syncthreads();
+
+  for (;;) {
+#pragma unroll
+    for (int j = 0; j < PF; ++j) {
+      if (!ok[j]) continue;
+      const int base = it[j] * half + chunk * V;
+      float f1[V], f2[V], o1[V], o2[V];
+      E::unpack(x1[j], f1);
+      E::unpack(x2[j], f2);
+#pragma unroll
+      for (int e = 0; e < V; ++e) {
+        const float c = cs[base + e], s = sn[base + e];
+        o1[e] = f1[e] * c - f2[e] * s;
+        o2[e] = f2[e] * c + f1[e] * s;
+      }
+      char *b = rope_head(a, t0 + it[j], ih[j], E::ES);
+      st16<NT>(reinterpret_cast<u32x4 *>(b) + chunk, E::pack(o1));
+      st16<NT>(reinterpret_cast<u32x4 *>(b + half * E::ES) + chunk, E::pack(o2));
+    }
+    if (!(tt < TPB && t0 + tt <= tlast && hg < nh)) break;
+    gather();
   }
 }
 
@@ -370,7 +446,7 @@ __device__ __forceinline__ float silu_mul(float g, float u) {
 
 // Flat contiguous [T*I]: workgroup `blk` of `nblk` handles U vectors per
 // work-item per step; workgroup 0 also does the < V element tail.
-template <int DT, int U>
+template <int DT, int U, bool NT>
 __device__ __forceinline__ void sw_flat_part(const SwArgs &a, int64_t blk, int64_t nblk) {
   using E = Elt<DT>;
   constexpr int V = E::V;
@@ -385,8 +461,8 @@ __device__ __forceinline__ void sw_flat_part(const SwArgs &a, int64_t blk, int64
     for (int k = 0; k < U; ++k) {
       const int64_t idx = base + int64_t(k) * kThreads;
       if (idx < nvec) {
-        gv[k] = g[idx];
-        uv[k] = u[idx];
+        gv[k] = ld16<NT>(g + idx);
+        uv[k] = ld16<NT>(u + idx);
       }
     }
 #pragma unroll
@@ -398,7 +474,7 @@ __device__ __forceinline__ void sw_flat_part(const SwArgs &a, int64_t blk, int64
         E::unpack(uv[k], fu);
 #pragma unroll
         for (int e = 0; e < V; ++e) fg[e] = silu_mul(fg[e], fu[e]);
-        o[idx] = E::pack(fg);
+        st16<NT>(o + idx, E::pack(fg));
       }
     }
   }

@@ -8,13 +8,13 @@ using namespace dev;
 
 template <int DT, int NV, bool RES>
 __global__ __launch_bounds__(256) void k_rn_wave(RnArgs a) {
-  rn_wave_block<DT, NV, RES>(a, blockIdx.x);
+  rn_wave_block<DT, NV, RES, false>(a, blockIdx.x);
 }
 
 template <int DT, int NB, bool RES>
 __global__ __launch_bounds__(256) void k_rn_block(RnArgs a) {
   __shared__ float red[4];
-  rn_row_regs<DT, NB, RES, 256>(a, blockIdx.x, threadIdx.x, red);
+  rn_row_regs<DT, NB, RES, 256, false>(a, blockIdx.x, threadIdx.x, red);
 }
 
 template <int DT, bool RES>
@@ -39,6 +39,9 @@ const void *rn_pick(int32_t variant) {
     case RN_WAVE_4: return reinterpret_cast<const void *>(&k_rn_wave<DT, 4, RES>);
     case RN_WAVE_8: return reinterpret_cast<const void *>(&k_rn_wave<DT, 8, RES>);
     case RN_WAVE_16: return reinterpret_cast<const void *>(&k_rn_wave<DT, 16, RES>);
+    case RN_BLOCK_1: return reinterpret_cast<const void *>(&k_rn_block<DT, 1, RES>);
+    case RN_BLOCK_2: return reinterpret_cast<const void *>(&k_rn_block<DT, 2, RES>);
+    case RN_BLOCK_4: return reinterpret_cast<const void *>(&k_rn_block<DT, 4, RES>);
     case RN_BLOCK_8: return reinterpret_cast<const void *>(&k_rn_block<DT, 8, RES>);
     case RN_BLOCK_16: return reinterpret_cast<const void *>(&k_rn_block<DT, 16, RES>);
     case RN_LOOP: return reinterpret_cast<const void *>(&k_rn_loop<DT, RES>);

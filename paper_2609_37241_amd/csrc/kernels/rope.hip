@@ -8,7 +8,7 @@ using namespace dev;
 template <int DT, int TPB>
 __global__ __launch_bounds__(256) void k_rope_vec(RopeArgs a) {
   __shared__ float lds[2 * TPB * 256];
-  rope_vec_block<DT, TPB>(a, blockIdx.x, lds);
+  rope_vec_block<DT, TPB, false>(a, blockIdx.x, lds);
 }
 
 template <int DT>

@@ -5,9 +5,9 @@
 namespace tri {
 using namespace dev;
 
-template <int DT, int U>
+template <int DT, int U, bool NT>
 __global__ __launch_bounds__(256) void k_sw_flat(SwArgs a) {
-  sw_flat_part<DT, U>(a, blockIdx.x, gridDim.x);
+  sw_flat_part<DT, U, NT>(a, blockIdx.x, gridDim.x);
 }
 
 template <int DT>
@@ -25,8 +25,9 @@ template <int DT>
 const void *sw_pick(int32_t variant) {
   switch (variant) {
     case SW_SCALAR: return reinterpret_cast<const void *>(&k_sw_scalar<DT>);
-    case SW_FLAT_U1: return reinterpret_cast<const void *>(&k_sw_flat<DT, 1>);
-    case SW_FLAT_U4: return reinterpret_cast<const void *>(&k_sw_flat<DT, 4>);
+    case SW_FLAT: return reinterpret_cast<const void *>(&k_sw_flat<DT, 1, false>);
+    case SW_FLAT_NT: return reinterpret_cast<const void *>(&k_sw_flat<DT, 1, true>);
+    case SW_FLAT_U4_NT: return reinterpret_cast<const void *>(&k_sw_flat<DT, 4, true>);
     case SW_ROWS: return reinterpret_cast<const void *>(&k_sw_rows<DT>);
     default: return nullptr;
   }

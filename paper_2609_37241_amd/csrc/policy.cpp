@@ -27,29 +27,30 @@ inline uint32_t clamp_grid(int64_t g) {
   return g > int64_t(kGridCap) ? kGridCap : uint32_t(g);
 }
 
-int32_t rn_wave_id(int64_t nv) {
-  switch (nv) {
-    case 1: return RN_WAVE_1;
-    case 2: return RN_WAVE_2;
-    case 4: return RN_WAVE_4;
-    case 8: return RN_WAVE_8;
-    default: return RN_WAVE_16;
-  }
+int32_t pow2_index(int64_t n) {   // n in {1, 2, 4, 8, 16}
+  int32_t i = 0;
+  while ((int64_t(1) << i) < n) ++i;
+  return i;
 }
 
 }  // namespace
 
-// One wavefront per row while a row fits in at most 16 16-byte vectors per
-// lane, then one workgroup per row up to 16 vectors per thread, then two
-// passes over global memory. Unaligned or ragged rows take the scalar kernel.
-Role rn_role(uint32_t dtype, int64_t H, unsigned flags, int64_t T) {
+// Decode-sized buckets keep a row in one wavefront's registers (no barrier)
+// while it fits in 16 16-byte vectors per lane; larger token counts, and rows
+// too long for one wavefront, take one workgroup per row (fewer registers per
+// lane, more wavefronts resident), up to 16 vectors per work-item; longer
+// rows make two passes over global memory. Unaligned or ragged rows take the
+// scalar kernel.
+Role rn_role(uint32_t dtype, int64_t H, unsigned flags, uint32_t bucket, int64_t T) {
   const int64_t v = vec_elems(dtype);
   if (!(flags & kAlign) || H % v) return {RN_SCALAR, uint32_t(T)};
   const int64_t nvec = H / v;
-  const int64_t nv = next_pow2(cdiv(nvec, 64));
-  if (nv <= 16) return {rn_wave_id(nv), uint32_t(cdiv(T, 4))};
+  if (bucket <= kDecodeBucketMax) {
+    const int64_t nv = next_pow2(cdiv(nvec, 64));
+    if (nv <= 16) return {RN_WAVE_1 + pow2_index(nv), uint32_t(cdiv(T, 4))};
+  }
   const int64_t nb = next_pow2(cdiv(nvec, 256));
-  if (nb <= 16) return {nb == 8 ? RN_BLOCK_8 : RN_BLOCK_16, uint32_t(T)};
+  if (nb <= 16) return {RN_BLOCK_1 + pow2_index(nb), uint32_t(T)};
   return {RN_LOOP, uint32_t(T)};
 }
 
@@ -65,12 +66,17 @@ Role rope_role(uint32_t dtype, int32_t hd, unsigned flags, uint32_t bucket, int6
   return {ROPE_VEC_T4, uint32_t(cdiv(T, 4))};
 }
 
-Role sw_role(uint32_t dtype, int64_t I, unsigned flags, uint32_t bucket, int64_t T) {
+// Flat SwiGLU streams nontemporally beyond decode sizes: one vector per
+// work-item as a standalone kernel, four per work-item as a role of the fused
+// chain (where the norm and RoPE roles share the workgroup budget).
+Role sw_role(uint32_t dtype, int64_t I, unsigned flags, uint32_t bucket, int64_t T,
+             bool in_chain) {
   const int64_t v = vec_elems(dtype);
   if ((flags & kAlign) && (flags & kContig)) {
-    const int64_t u = bucket <= 6 ? 1 : 4;
     const int64_t nvec = (T * I) / v;
-    return {u == 1 ? SW_FLAT_U1 : SW_FLAT_U4, clamp_grid(cdiv(nvec, int64_t(kBlock) * u))};
+    if (bucket <= kDecodeBucketMax) return {SW_FLAT, clamp_grid(cdiv(nvec, kBlock))};
+    if (in_chain) return {SW_FLAT_U4_NT, clamp_grid(cdiv(nvec, 4 * int64_t(kBlock)))};
+    return {SW_FLAT_NT, clamp_grid(cdiv(nvec, kBlock))};
   }
   if ((flags & kAlign) && I % v == 0) {
     const int64_t cb = cdiv(I / v, kBlock);
@@ -83,16 +89,16 @@ Role sw_role(uint32_t dtype, int64_t I, unsigned flags, uint32_t bucket, int64_t
 
 // Workgroups of a role variant for T tokens (I is the SwiGLU width).
 uint32_t role_grid(int32_t variant, uint32_t dtype, int64_t T, int64_t I) {
+  if (variant >= RN_WAVE_1 && variant <= RN_WAVE_16) return uint32_t(cdiv(T, 4));
   switch (variant) {
-    case RN_WAVE_1: case RN_WAVE_2: case RN_WAVE_4: case RN_WAVE_8: case RN_WAVE_16:
     case ROPE_VEC_T4:
       return uint32_t(cdiv(T, 4));
-    case RN_SCALAR: case RN_BLOCK_8: case RN_BLOCK_16: case RN_LOOP:
-    case ROPE_SCALAR: case ROPE_VEC_T1:
+    case RN_SCALAR: case RN_BLOCK_1: case RN_BLOCK_2: case RN_BLOCK_4: case RN_BLOCK_8:
+    case RN_BLOCK_16: case RN_LOOP: case ROPE_SCALAR: case ROPE_VEC_T1:
       return uint32_t(T);
-    case SW_FLAT_U1:
+    case SW_FLAT: case SW_FLAT_NT:
       return clamp_grid(cdiv((T * I) / vec_elems(dtype), kBlock));
-    case SW_FLAT_U4:
+    case SW_FLAT_U4_NT:
       return clamp_grid(cdiv((T * I) / vec_elems(dtype), 4 * int64_t(kBlock)));
     case SW_ROWS: {
       const int64_t g = T * cdiv(I / vec_elems(dtype), kBlock);
@@ -109,9 +115,9 @@ uint32_t role_grid(int32_t variant, uint32_t dtype, int64_t T, int64_t I) {
 
 namespace {
 
-// Template index of the fused chain kernel: (NV index) * 4 + (T4) * 2 + (U4).
+// Template index of the fused chain kernel (see Plan::ksub).
 int32_t fused_sub(int32_t rn, int32_t rope, int32_t sw) {
-  return (rn - RN_WAVE_1) * 4 + (rope == ROPE_VEC_T4 ? 2 : 0) + (sw == SW_FLAT_U4 ? 1 : 0);
+  return (rn - RN_WAVE_1) * 4 + (rope == ROPE_VEC_T4 ? 2 : 0) + (sw == SW_FLAT_U4_NT ? 1 : 0);
 }
 
 }  // namespace
@@ -123,7 +129,7 @@ Plan plan_for_key(const Key &k) {
   switch (op) {
     case TRI_OP_RMSNORM:
     case TRI_OP_RES_RMSNORM: {
-      const Role r = rn_role(dt, key_H(k), fl, 1);
+      const Role r = rn_role(dt, key_H(k), fl, b, 1);
       p.variant = r.variant;
       p.n_launches = 1;
       p.kvariant[0] = r.variant;
@@ -138,7 +144,7 @@ Plan plan_for_key(const Key &k) {
       return p;
     }
     case TRI_OP_SWIGLU: {
-      const Role r = sw_role(dt, key_I(k), fl, b, 1);
+      const Role r = sw_role(dt, key_I(k), fl, b, 1, false);
       p.variant = r.variant;
       p.n_launches = 1;
       p.kvariant[0] = r.variant;
@@ -147,16 +153,16 @@ Plan plan_for_key(const Key &k) {
     default:
       break;
   }
-  const Role rn = rn_role(dt, key_H(k), fl & 3u, 1);
+  const Role rn = rn_role(dt, key_H(k), fl & 3u, b, 1);
   const Role ro = rope_role(dt, int32_t(key_hd(k)), (fl >> 2) & 3u, b, 1);
-  const Role sw = sw_role(dt, key_I(k), (fl >> 4) & 3u, b, 1);
+  const Role sw = sw_role(dt, key_I(k), (fl >> 4) & 3u, b, 1, true);
   p.roles[0] = rn.variant;
   p.roles[1] = ro.variant;
   p.roles[2] = sw.variant;
-  const bool rn_wave = rn.variant >= RN_WAVE_1 && rn.variant <= RN_WAVE_16;
+  const bool rn_regs = rn.variant >= RN_WAVE_1 && rn.variant <= RN_BLOCK_16;
   const bool ro_vec = ro.variant == ROPE_VEC_T1 || ro.variant == ROPE_VEC_T4;
-  const bool sw_flat = sw.variant == SW_FLAT_U1 || sw.variant == SW_FLAT_U4;
-  if (fl == 0x3Fu && rn_wave && ro_vec && sw_flat) {
+  const bool sw_flat = sw.variant == SW_FLAT || sw.variant == SW_FLAT_U4_NT;
+  if (fl == 0x3Fu && rn_regs && ro_vec && sw_flat) {
     p.variant = CH_FUSED;
     p.n_launches = 1;
     p.kvariant[0] = CH_FUSED;

@@ -335,6 +335,6 @@ def test_version_info(lib, fresh):
         c_call(lib, cache, c)
     v = VersionInfo()
     assert lib.tri_spec_version_info(cache, 0, C.byref(v)) == 0
-    assert (v.variant, tuple(v.roles), v.hits) == (50, (11, 21, 31), 2)
+    assert (v.variant, tuple(v.roles), v.hits) == (50, (11, 31, 41), 2)
     assert tuple(v.key) == S.make_key(c)
     assert lib.tri_spec_version_info(cache, 1, C.byref(v)) == S.E_INVALID

@@ -40,7 +40,7 @@ def test_policy_llama7b_decode_chain():
     # one vector per thread: 11008 / 8 = 1376 vectors -> 6 workgroups.
     v, roles, launches = S.plan(S.make_key(chain_call(BF, 1, 4096, 11008, 32, 32, 128)), 1)
     assert v == S.CH_FUSED
-    assert roles == (14, 21, 31)
+    assert roles == (14, 31, 41)
     assert launches == [(50, 1 + 1 + 6, 256)]
 
 
@@ -49,17 +49,18 @@ def test_policy_gqa_decode_chain():
     # SwiGLU 8 * 14336 / 8 = 14336 vectors -> 56 blocks; norm ceil(8/4) = 2.
     v, roles, launches = S.plan(S.make_key(chain_call(BF, 8, 4096, 14336, 32, 8, 128,
                                                       base=500000.0)), 8)
-    assert (v, roles, launches) == (S.CH_FUSED, (14, 21, 31), [(50, 2 + 8 + 56, 256)])
+    assert (v, roles, launches) == (S.CH_FUSED, (14, 31, 41), [(50, 2 + 8 + 56, 256)])
 
 
 def test_policy_prefill_chain():
-    # H = 8192 bf16 -> 1024 vectors -> 16 per lane -> RN_WAVE_16, 2048 blocks;
-    # T = 8192 -> bucket 13: RoPE 4 tokens per block (2048 blocks); SwiGLU
-    # 8192 * 28672 / 8 = 29360128 vectors at 4 per thread -> 28672 blocks.
+    # T = 8192 -> bucket 13, beyond decode sizes: H = 8192 bf16 -> 1024 vectors
+    # -> 4 per work-item -> RN_BLOCK_4, one block per row (8192); RoPE 4 tokens
+    # per block (2048 blocks); SwiGLU role 8192 * 28672 / 8 = 29360128 vectors
+    # at 4 per work-item, streaming -> 28672 blocks.
     v, roles, launches = S.plan(S.make_key(chain_call(BF, 8192, 8192, 28672, 64, 8, 128,
                                                       base=500000.0)), 8192)
-    assert (v, roles) == (S.CH_FUSED, (15, 22, 32))
-    assert launches == [(50, 2048 + 2048 + 28672, 256)]
+    assert (v, roles) == (S.CH_FUSED, (18, 32, 44))
+    assert launches == [(50, 8192 + 2048 + 28672, 256)]
 
 
 def test_policy_tiny_f32_chain():
@@ -67,18 +68,26 @@ def test_policy_tiny_f32_chain():
     # hd 64 -> 32 pairs -> 8 vectors per half (power of two) -> ROPE_VEC_T1.
     # SwiGLU 4 * 688 / 4 = 688 vectors -> 3 blocks.
     v, roles, launches = S.plan(S.make_key(chain_call(F, 4, 256, 688, 4, 4, 64)), 4)
-    assert (v, roles, launches) == (S.CH_FUSED, (11, 21, 31), [(50, 1 + 4 + 3, 256)])
+    assert (v, roles, launches) == (S.CH_FUSED, (11, 31, 41), [(50, 1 + 4 + 3, 256)])
 
 
 @pytest.mark.parametrize("H,dtype,want", [
     (64, F, (11, 2)), (256, BF, (11, 2)), (520, BF, (12, 2)), (4096, F, (15, 2)),
-    (8192, F, (16, 5)), (16384, F, (17, 5)), (32768, BF, (17, 5)),
-    (65536, BF, (18, 5)), (100, BF, (10, 5)), (4097, F, (10, 5))])
+    (8192, F, (19, 5)), (16384, F, (20, 5)), (32768, BF, (20, 5)),
+    (65536, BF, (21, 5)), (100, BF, (10, 5)), (4097, F, (10, 5))])
 def test_rmsnorm_policy_by_row_size(H, dtype, want):
-    # 5 rows: one wave per row packs 4 rows per block (2 blocks); the other
-    # variants take one block per row.
-    v, g = S.rn_role(dtype, H, S.ALIGN | S.CONTIG, 5)
+    # 5 rows (bucket 3, decode sized): one wave per row packs 4 rows per block
+    # (2 blocks); rows beyond 16 vectors per lane take one block per row.
+    v, g = S.rn_role(dtype, H, S.ALIGN | S.CONTIG, S.bucket(5), 5)
     assert (v, g) == want
+
+
+@pytest.mark.parametrize("H,dtype,T,want", [
+    (4096, BF, 65, (17, 65)), (8192, BF, 8192, (18, 8192)), (256, F, 100, (16, 100)),
+    (4096, BF, 64, (14, 16)), (65536, F, 128, (21, 128))])
+def test_rmsnorm_policy_beyond_decode_sizes(H, dtype, T, want):
+    # more than 64 tokens: one workgroup per row, NB = next_pow2(H/v / 256)
+    assert S.rn_role(dtype, H, S.ALIGN | S.CONTIG, S.bucket(T), T) == want
 
 
 def test_unaligned_and_strided_layouts():
@@ -94,7 +103,7 @@ def test_unaligned_and_strided_layouts():
     assert S.plan(S.make_key(rope_call(BF, 2, 4, 4, 96)), 2)[0] == S.ROPE_SCALAR
     c = chain_call(BF, 4, 4096, 11008, 32, 32, 128, sw_pad=64)
     v, roles, launches = S.plan(S.make_key(c), 4)
-    assert v == S.CH_SEQ and roles == (14, 21, S.SW_ROWS) and len(launches) == 3
+    assert v == S.CH_SEQ and roles == (14, 31, S.SW_ROWS) and len(launches) == 3
 
 
 def test_chain_key_keeps_per_role_flags():
@@ -106,11 +115,14 @@ def test_chain_key_keeps_per_role_flags():
 
 def test_swiglu_flat_grid_cap_and_tail():
     # 3 * 5 = 15 f32 elements: 3 whole vectors + a 3-element tail -> 1 block
-    assert S.sw_role(F, 5, 3, 2, 3) == (S.SW_FLAT_U1, 1)
+    assert S.sw_role(F, 5, 3, 2, 3) == (S.SW_FLAT, 1)
     # 1 element: no whole vector, still one block for the tail
-    assert S.sw_role(F, 1, 3, 0, 1) == (S.SW_FLAT_U1, 1)
-    v, g = S.sw_role(BF, 1 << 30, 3, 10, 1024)
-    assert (v, g) == (S.SW_FLAT_U4, S.GRID_CAP)
+    assert S.sw_role(F, 1, 3, 0, 1) == (S.SW_FLAT, 1)
+    assert S.sw_role(BF, 1 << 30, 3, 10, 1024) == (S.SW_FLAT_NT, S.GRID_CAP)
+    assert S.sw_role(BF, 1 << 30, 3, 10, 1024, in_chain=True) == (S.SW_FLAT_U4_NT, S.GRID_CAP)
+    # 65 tokens x 1024 bf16: 8320 vectors -> 33 blocks standalone, 9 in the chain
+    assert S.sw_role(BF, 1024, 3, 7, 65) == (S.SW_FLAT_NT, 33)
+    assert S.sw_role(BF, 1024, 3, 7, 65, in_chain=True) == (S.SW_FLAT_U4_NT, 9)
 
 
 # ---- Algorithm 1 and the three paths ---------------------------------------------
