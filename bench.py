@@ -40,6 +40,7 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=10.0)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-bandwidth", action="store_true")
+    p.add_argument("--no-stream", action="store_true", help="skip the mixed-shape stream")
     return p.parse_args()
 
 
@@ -66,6 +67,92 @@ def algorithmic_bytes(cfg):
             "chain": res + rope + sw}
 
 
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "chain_prefill8k_hbm_traffic.md")
+TRAFFIC_SOURCES = ("paper_2609_37241_amd/csrc/kernargs.h",
+                   "paper_2609_37241_amd/csrc/kernels/device.h",
+                   "paper_2609_37241_amd/csrc/kernels/chain_bf16.hip")
+
+
+def measured_traffic():
+    """HBM bytes per launch of the 8192-token fused chain from the committed
+    rocprofv3 FETCH_SIZE / WRITE_SIZE summary, or None when the kernel sources
+    changed since those counters were taken."""
+    import hashlib
+    try:
+        text = open(TRAFFIC_FILE).read()
+    except OSError:
+        return None
+    fields = dict(l.strip().split(": ", 1) for l in text.splitlines()
+                  if l.strip().startswith(("chain_traffic_bytes:", "kernel_source_sha256:")))
+    h = hashlib.sha256()
+    for rel in TRAFFIC_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    if fields.get("kernel_source_sha256") != h.hexdigest():
+        return None
+    return float(fields["chain_traffic_bytes"])
+
+
+def run_mixed_stream(tri, wl, bench, dev, stream, torch):
+    """The 10,000-call mixed stream: token counts 1..512, 90 % bf16, 5 % unaligned
+    or padded layouts, through a fresh cache; every call synchronised."""
+    Tmax = max(wl.MIXED_T_CHOICES)
+    H, I, nq, nk, hd = wl.MIXED_H, wl.MIXED_I, wl.MIXED_NQ, wl.MIXED_NK, wl.MIXED_HD
+    calls = wl.mixed_stream()
+    bufs = {}
+
+    def tensor(shape, td, layout):
+        n = int(np.prod(shape[1:]))
+        inner = tuple(int(np.prod(shape[i + 1:])) for i in range(1, len(shape)))
+        if layout == wl.LAYOUT_STRIDED:        # row stride = width + pad
+            base = torch.randn((shape[0], n + wl.MIXED_PAD), device=dev).to(td)
+            return torch.as_strided(base, shape, (n + wl.MIXED_PAD,) + inner)
+        if layout == wl.LAYOUT_UNALIGNED:      # every pointer one element off
+            base = torch.randn(shape[0] * n + 1, device=dev).to(td)
+            return torch.as_strided(base, shape, (n,) + inner, 1)
+        return torch.randn(shape, device=dev).to(td)
+
+    arr = (tri.ChainArgs * len(calls))()
+    cache = tri.SpecCache()
+    for i, (T, dt, layout) in enumerate(calls):
+        if (dt, layout) not in bufs:
+            td = torch.bfloat16 if dt == wl.BF16 else torch.float32
+            b = {n: tensor(sh, td, layout) for n, sh in (
+                ("x", (Tmax, H)), ("residual", (Tmax, H)), ("y", (Tmax, H)),
+                ("res_out", (Tmax, H)), ("q", (Tmax, nq, hd)), ("k", (Tmax, nk, hd)),
+                ("gate", (Tmax, I)), ("up", (Tmax, I)), ("out", (Tmax, I)))}
+            b["w"] = (torch.rand(H, device=dev) + 0.5).to(td)
+            b["pos"] = torch.randint(0, wl.MIXED_POS_MAX + 1, (Tmax,), device=dev,
+                                     dtype=torch.int32)
+            bufs[(dt, layout)] = b
+        b = bufs[(dt, layout)]
+        a, _ = cache.chain_args(b["x"][:T], b["residual"][:T], b["w"], b["q"][:T], b["k"][:T],
+                                b["pos"][:T], b["gate"][:T], b["up"][:T], 1e-6, wl.MIXED_BASE,
+                                y=b["y"][:T], residual_out=b["res_out"][:T], out=b["out"][:T])
+        arr[i] = a
+    torch.cuda.synchronize()
+    n = len(calls)
+    e2e = (C.c_double * n)()
+    missed = (C.c_int * n)()
+    st = bench.trib_stream(cache.handle, arr, n, stream.cuda_stream, e2e, missed)
+    assert st == 0, st
+    stats = cache.stats()
+    per_bucket = {}
+    for (T, _, _), t, m in zip(calls, e2e, missed):
+        if not m:
+            per_bucket.setdefault(T, []).append(t)
+    miss_t = [t for t, m in zip(e2e, missed) if m]
+    return {
+        "calls": n, "misses": sum(missed), "versions": stats["n_versions"],
+        "user_level_hit_rate": 1.0 - sum(missed) / n,
+        "hit_e2e_us_by_tokens": {str(T): {"median": summary(v)["median"],
+                                           "p90": summary(v)["p90"], "n": len(v)}
+                                  for T, v in sorted(per_bucket.items())},
+        "miss_handling_e2e_us": summary(miss_t) if miss_t else None,
+        "cache_stats": stats,
+    }
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -84,6 +171,8 @@ def main():
                                    C.POINTER(C.c_double), C.POINTER(C.c_double)]
     bench.trib_issue.argtypes = [C.c_void_p, C.c_int, C.c_void_p, C.c_void_p, C.c_int,
                                  C.POINTER(C.c_double)]
+    bench.trib_stream.argtypes = [C.c_void_p, C.c_void_p, C.c_int, C.c_void_p,
+                                  C.POINTER(C.c_double), C.POINTER(C.c_int)]
     stream = torch.cuda.Stream(device=dev)
     sptr = stream.cuda_stream
 
@@ -146,6 +235,23 @@ def main():
         "cache_stats": stats,
     }
 
+    # ---- GQA decode (8 tokens, 32 Q / 8 K heads, base 5e5): same loop -------------------
+    cfg2 = wl.GQA_DECODE
+    inp2 = wl.host_inputs(cfg2)
+    d2 = {k: wl.to_torch(v, cfg2.dtype, dev) for k, v in inp2.items()}
+    args2, _outs2 = cache.chain_args(d2["x"], d2["residual"], d2["w"], d2["q"], d2["k"],
+                                     d2["pos"], d2["gate"], d2["up"], cfg2.eps, cfg2.base)
+    cache.decode_chain_args(args2, stream)
+    torch.cuda.synchronize()
+    n2 = min(K, 5000)
+    st = bench.trib_latency(cache.handle, 0, C.byref(args2), sptr, W, n2, e2e, hst)
+    assert st == 0, st
+    latency["gqa_decode_chain_e2e_us"] = summary(list(e2e[:n2]))
+    latency["gqa_decode_chain_host_us"] = summary(list(hst[:n2]))
+
+    # ---- mixed-shape stream: guard hits, misses, latency per token bucket ---------------
+    mixed = None if args.no_stream else run_mixed_stream(tri, wl, bench, dev, stream, torch)
+
     # ---- 8192-token prefill: HBM bandwidth ------------------------------------------
     bandwidth, roofline = None, None
     if not args.no_bandwidth:
@@ -199,7 +305,7 @@ def main():
                                "frac_of_peak": gbs / HBM_PEAK_GBS}
         ch = bandwidth["chain"]
         roofline = {"bound": "hbm", "achieved": ch["GB/s"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                    "frac": ch["GB/s"] / HBM_PEAK_GBS, "traffic": None,
+                    "frac": ch["GB/s"] / HBM_PEAK_GBS, "traffic": measured_traffic(),
                     "kernel": "fused decode chain, 8192 tokens (k_chain: block-per-row norm, "
                               "4-token RoPE blocks, streaming 4-vector SwiGLU)",
                     "bytes_per_launch": ch["bytes"], "avg_launch_us": ch["mean_us"]}
@@ -226,6 +332,7 @@ def main():
                          f"{platform.processor() or platform.machine()}, "
                          f"{os.cpu_count()} logical CPUs visible"}
 
+    latency["mixed_stream"] = mixed
     line = {
         "metric": METRIC, "value": ce["median"], "unit": "µs", "n_gpus": 1, "steps": K,
         "warmup": W, "ms_per_step": wall * 1e3 / K, "higher_is_better": False,

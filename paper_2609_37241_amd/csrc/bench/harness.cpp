@@ -65,4 +65,27 @@ int trib_issue(tri_cache *c, int mode, const tri_chain_args *args, void *stream,
   return 0;
 }
 
+// The mixed-shape stream: calls[i] in order, each synchronised. A MISS is
+// handled the way a caller of the library handles it (install the missed key,
+// call again); missed[i] = 1 marks those calls, whose e2e_us then covers
+// miss + install + retry. Returns 0 or the first failing status.
+int trib_stream(tri_cache *c, const tri_chain_args *calls, int n, void *stream,
+                double *e2e_us, int *missed) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  for (int i = 0; i < n; ++i) {
+    const Clock::time_point t0 = Clock::now();
+    int st = tri_decode_chain(c, calls + i, stream);
+    missed[i] = 0;
+    if (st == TRI_MISS) {
+      missed[i] = 1;
+      st = tri_spec_install_last_miss(c, nullptr);
+      if (st == TRI_OK) st = tri_decode_chain(c, calls + i, stream);
+    }
+    if (hipStreamSynchronize(s) != hipSuccess) return TRI_E_RUNTIME;
+    e2e_us[i] = us_between(t0, Clock::now());
+    if (st != TRI_OK) return st;
+  }
+  return 0;
+}
+
 }  // extern "C"
