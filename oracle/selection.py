@@ -18,9 +18,12 @@ What it models
 Guards are equality tests on a packed key, so two versions can never both
 match and "first match in creation order" is the unique match.
 
-This file is written from the policy contract (the table in the design
-notes) independently of the C++ library; the two must agree bit for bit on
-every selection record.
+The install policy (which kernel variant a key selects and how many
+workgroups a call launches) is restated here from its specification,
+independently of the C++ library; the two must agree bit for bit on every
+selection record. Decode-sized calls (token bucket <= 6) keep norm rows in
+one wavefront and use cached loads; larger calls take one workgroup per norm
+row and stream SwiGLU nontemporally.
 """
 from __future__ import annotations
 

@@ -1,8 +1,10 @@
 """Tolerance checks and oracle-model calls built from real device tensors.
 
-Tolerances (the design's reading of the stated bar): float32 outputs pass
-when |g - o| <= 1e-5 |o| + 1e-6; bfloat16 outputs pass when |g - o| <= 2e-2
-or g is within one bf16 ulp of the oracle's correctly rounded value.
+Tolerances: float32 outputs pass when |g - o| <= 1e-5 |o| + 1e-6 (the
+absolute floor covers cancellation near zero in RoPE); bfloat16 outputs pass
+when |g - o| <= 2e-2 or g is within one bf16 ulp of the oracle's correctly
+rounded value (2e-2 alone is less than one ulp once |o| >= 4, and the
+prefill inputs carry x50 outliers).
 """
 import numpy as np
 
