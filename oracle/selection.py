@@ -21,9 +21,9 @@ match and "first match in creation order" is the unique match.
 The install policy (which kernel variant a key selects and how many
 workgroups a call launches) is restated here from its specification,
 independently of the C++ library; the two must agree bit for bit on every
-selection record. Decode-sized calls (token bucket <= 6) keep norm rows in
-one wavefront and use cached loads; larger calls take one workgroup per norm
-row and stream SwiGLU nontemporally.
+selection record. Norm rows of up to 128 16-byte vectors take one wavefront
+each, longer rows one workgroup each; decode-sized calls (token bucket <= 6)
+use cached SwiGLU loads, larger calls stream SwiGLU nontemporally.
 """
 from __future__ import annotations
 
@@ -40,10 +40,10 @@ OK, MISS = 0, 1
 E_INVALID, E_UNSUPPORTED, E_FULL, E_NOMEM, E_LAUNCH, E_RUNTIME = -1, -2, -3, -4, -5, -6
 
 RN_SCALAR = 10
-RN_WAVE = {1: 11, 2: 12, 4: 13, 8: 14, 16: 15}
-RN_BLOCK = {1: 16, 2: 17, 4: 18, 8: 19, 16: 20}
-RN_LOOP = 21
-ROPE_SCALAR, ROPE_VEC_T1, ROPE_VEC_T4 = 30, 31, 32
+RN_WAVE = {1: 11, 2: 12}
+RN_BLOCK = {1: 13, 2: 14, 4: 15, 8: 16, 16: 17}
+RN_LOOP = 18
+ROPE_SCALAR, ROPE_VEC = 30, 31
 SW_SCALAR, SW_FLAT, SW_FLAT_NT, SW_ROWS, SW_FLAT_U4_NT = 40, 41, 42, 43, 44
 CH_FUSED, CH_SEQ = 50, 51
 DECODE_BUCKET_MAX = 6       # buckets up to here are decode sized
@@ -108,30 +108,26 @@ def _aligned(es: int, ptrs, strides) -> bool:
 
 
 # ---- role policies -----------------------------------------------------------
-def rn_role(dtype: int, H: int, flags: int, b: int, T: int) -> Tuple[int, int]:
+def rn_role(dtype: int, H: int, flags: int, T: int) -> Tuple[int, int]:
     """(variant, grid) for RMSNorm / residual RMSNorm rows."""
     v = 16 // elem_size(dtype)
     if not (flags & ALIGN) or H % v:
         return RN_SCALAR, T
     nvec = H // v
-    if b <= DECODE_BUCKET_MAX:
-        nv = next_pow2(cdiv(nvec, 64))
-        if nv <= 16:
-            return RN_WAVE[nv], cdiv(T, 4)
-    nb = next_pow2(cdiv(nvec, 256))
+    if nvec <= 128:                       # short rows: a wavefront each, 4 per block
+        return RN_WAVE[next_pow2(cdiv(nvec, 64))], cdiv(T, 4)
+    nb = next_pow2(cdiv(nvec, 256))       # a workgroup per row
     if nb <= 16:
         return RN_BLOCK[nb], T
     return RN_LOOP, T
 
 
-def rope_role(dtype: int, hd: int, flags: int, b: int, T: int) -> Tuple[int, int]:
+def rope_role(dtype: int, hd: int, flags: int, T: int) -> Tuple[int, int]:
     v = 16 // elem_size(dtype)
     half = hd // 2
     if not (flags & ALIGN) or half % v or not is_pow2(half // v):
         return ROPE_SCALAR, T
-    if b <= 3:
-        return ROPE_VEC_T1, T
-    return ROPE_VEC_T4, cdiv(T, 4)
+    return ROPE_VEC, T
 
 
 def sw_role(dtype: int, I: int, flags: int, b: int, T: int,
@@ -359,21 +355,21 @@ def plan(key, T: int):
     f = unpack_key(key)
     op, dt, b, fl = f["op"], f["dtype"], f["bucket"], f["flags"]
     if op in (OP_RMSNORM, OP_RES_RMSNORM):
-        v, g = rn_role(dt, f["H"], fl, b, T)
+        v, g = rn_role(dt, f["H"], fl, T)
         return v, (0, 0, 0), [(v, g, BLOCK)]
     if op == OP_ROPE_QK:
-        v, g = rope_role(dt, f["hd"], fl, b, T)
+        v, g = rope_role(dt, f["hd"], fl, T)
         return v, (0, 0, 0), [(v, g, BLOCK)]
     if op == OP_SWIGLU:
         v, g = sw_role(dt, f["I"], fl, b, T)
         return v, (0, 0, 0), [(v, g, BLOCK)]
-    rn = rn_role(dt, f["H"], fl & 3, b, T)
-    ro = rope_role(dt, f["hd"], (fl >> 2) & 3, b, T)
+    rn = rn_role(dt, f["H"], fl & 3, T)
+    ro = rope_role(dt, f["hd"], (fl >> 2) & 3, T)
     sw = sw_role(dt, f["I"], (fl >> 4) & 3, b, T, in_chain=True)
     roles = (rn[0], ro[0], sw[0])
     fused = (fl == 0x3F
              and (rn[0] in RN_WAVE.values() or rn[0] in RN_BLOCK.values())
-             and ro[0] in (ROPE_VEC_T1, ROPE_VEC_T4)
+             and ro[0] == ROPE_VEC
              and sw[0] in (SW_FLAT, SW_FLAT_U4_NT))
     if fused:
         return CH_FUSED, roles, [(CH_FUSED, rn[1] + ro[1] + sw[1], BLOCK)]

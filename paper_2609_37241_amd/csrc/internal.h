@@ -12,17 +12,17 @@ namespace tri {
 // ---- variant ids (the install policy table) ------------------------------------
 enum Variant : int32_t {
   RN_SCALAR = 10,
-  RN_WAVE_1 = 11, RN_WAVE_2 = 12, RN_WAVE_4 = 13, RN_WAVE_8 = 14, RN_WAVE_16 = 15,
-  RN_BLOCK_1 = 16, RN_BLOCK_2 = 17, RN_BLOCK_4 = 18, RN_BLOCK_8 = 19, RN_BLOCK_16 = 20,
-  RN_LOOP = 21,
-  ROPE_SCALAR = 30, ROPE_VEC_T1 = 31, ROPE_VEC_T4 = 32,
+  RN_WAVE_1 = 11, RN_WAVE_2 = 12,
+  RN_BLOCK_1 = 13, RN_BLOCK_2 = 14, RN_BLOCK_4 = 15, RN_BLOCK_8 = 16, RN_BLOCK_16 = 17,
+  RN_LOOP = 18,
+  ROPE_SCALAR = 30, ROPE_VEC = 31,
   SW_SCALAR = 40, SW_FLAT = 41, SW_FLAT_NT = 42, SW_ROWS = 43, SW_FLAT_U4_NT = 44,
   CH_FUSED = 50, CH_SEQ = 51,
   EMPTY = 99,
 };
 
-// Token buckets up to this one are "decode sized": register-resident norm rows
-// one wavefront each, cached loads. Larger buckets stream.
+// Token buckets up to this one are "decode sized" (cached loads); larger
+// buckets stream SwiGLU nontemporally.
 constexpr uint32_t kDecodeBucketMax = 6;
 
 constexpr uint32_t kBlock = 256;
@@ -66,8 +66,8 @@ struct Role {
   int32_t variant;
   uint32_t grid;
 };
-Role rn_role(uint32_t dtype, int64_t H, unsigned flags, uint32_t bucket, int64_t T);
-Role rope_role(uint32_t dtype, int32_t hd, unsigned flags, uint32_t bucket, int64_t T);
+Role rn_role(uint32_t dtype, int64_t H, unsigned flags, int64_t T);
+Role rope_role(uint32_t dtype, int32_t hd, unsigned flags, int64_t T);
 Role sw_role(uint32_t dtype, int64_t I, unsigned flags, uint32_t bucket, int64_t T, bool in_chain);
 uint32_t role_grid(int32_t variant, uint32_t dtype, int64_t T, int64_t I);
 
@@ -78,7 +78,7 @@ struct Plan {
   int32_t n_launches;
   int32_t kvariant[3];    // kernel variant per launch
   int32_t ksub[3];        // kernel sub-selector (residual flag / fused template index)
-                          // fused: (role norm variant - RN_WAVE_1) * 4 + (4 RoPE tokens) * 2
+                          // fused: (role norm variant - RN_WAVE_1) * 2
                           //        + (SwiGLU role is SW_FLAT_U4_NT)
 };
 Plan plan_for_key(const Key &k);

@@ -1,22 +1,22 @@
 // The fused decode-chain kernel (bf16): one launch whose workgroups take the
 // residual-RMSNorm, RoPE-QK and SwiGLU roles by blockIdx range. Instantiated
-// for every (norm role variant, RoPE tokens per workgroup, SwiGLU role) the
-// install policy can pick.
+// for every (norm role variant, SwiGLU role) the install policy can pick.
 #include "../internal.h"
 #include "device.h"
 
 namespace tri {
 using namespace dev;
 
-// RNV: RN_WAVE_1..16 (one wavefront per row) or RN_BLOCK_1..16 (one
-// workgroup per row); TPB: RoPE tokens per workgroup; SWV: SW_FLAT (one
-// vector per work-item, cached) or SW_FLAT_U4_NT (four, streaming).
-template <int DT, int RNV, int TPB, int SWV>
+// RNV: RN_WAVE_1/2 (one wavefront per row) or RN_BLOCK_1..16 (one
+// workgroup per row); the RoPE role takes one token per workgroup; SWV:
+// SW_FLAT (one vector per work-item, cached) or SW_FLAT_U4_NT (four,
+// streaming).
+template <int DT, int RNV, int SWV>
 __global__ __launch_bounds__(256) void k_chain(ChainArgs a) {
-  __shared__ float lds[2 * TPB * 256];
+  __shared__ float lds[2 * 256];
   const uint32_t b = blockIdx.x;
   if (b < a.rn_blocks) {
-    if constexpr (RNV <= RN_WAVE_16) {
+    if constexpr (RNV <= RN_WAVE_2) {
       rn_wave_block<DT, 1 << (RNV - RN_WAVE_1), true, false>(a.rn, b);
     } else {
       __shared__ float red[4];
@@ -26,7 +26,7 @@ __global__ __launch_bounds__(256) void k_chain(ChainArgs a) {
   }
   const uint32_t b1 = b - a.rn_blocks;
   if (b1 < a.rope_blocks) {
-    rope_vec_block<DT, TPB, false>(a.rope, b1, lds);
+    rope_vec_block<DT, 1, false>(a.rope, b1, lds);
     return;
   }
   const uint32_t nsw = gridDim.x - a.rn_blocks - a.rope_blocks;
@@ -38,28 +38,23 @@ __global__ __launch_bounds__(256) void k_chain(ChainArgs a) {
 
 namespace {
 template <int RNV>
-const void *chain_pick_rn(bool t4, bool u4) {
-  if (t4) return u4 ? reinterpret_cast<const void *>(&k_chain<kBF16, RNV, 4, SW_FLAT_U4_NT>)
-                    : reinterpret_cast<const void *>(&k_chain<kBF16, RNV, 4, SW_FLAT>);
-  return u4 ? reinterpret_cast<const void *>(&k_chain<kBF16, RNV, 1, SW_FLAT_U4_NT>)
-            : reinterpret_cast<const void *>(&k_chain<kBF16, RNV, 1, SW_FLAT>);
+const void *chain_pick_rn(bool u4) {
+  return u4 ? reinterpret_cast<const void *>(&k_chain<kBF16, RNV, SW_FLAT_U4_NT>)
+            : reinterpret_cast<const void *>(&k_chain<kBF16, RNV, SW_FLAT>);
 }
 }  // namespace
 
-// sub = (norm role - RN_WAVE_1) * 4 + (4 RoPE tokens per block) * 2 + (SwiGLU U4 streaming).
+// sub = (norm role - RN_WAVE_1) * 2 + (SwiGLU role streams four vectors per work-item).
 const void *chain_kernel_bf16(int32_t sub) {
-  const bool t4 = (sub >> 1) & 1, u4 = sub & 1;
-  switch (RN_WAVE_1 + (sub >> 2)) {
-    case RN_WAVE_1: return chain_pick_rn<RN_WAVE_1>(t4, u4);
-    case RN_WAVE_2: return chain_pick_rn<RN_WAVE_2>(t4, u4);
-    case RN_WAVE_4: return chain_pick_rn<RN_WAVE_4>(t4, u4);
-    case RN_WAVE_8: return chain_pick_rn<RN_WAVE_8>(t4, u4);
-    case RN_WAVE_16: return chain_pick_rn<RN_WAVE_16>(t4, u4);
-    case RN_BLOCK_1: return chain_pick_rn<RN_BLOCK_1>(t4, u4);
-    case RN_BLOCK_2: return chain_pick_rn<RN_BLOCK_2>(t4, u4);
-    case RN_BLOCK_4: return chain_pick_rn<RN_BLOCK_4>(t4, u4);
-    case RN_BLOCK_8: return chain_pick_rn<RN_BLOCK_8>(t4, u4);
-    case RN_BLOCK_16: return chain_pick_rn<RN_BLOCK_16>(t4, u4);
+  const bool u4 = sub & 1;
+  switch (RN_WAVE_1 + (sub >> 1)) {
+    case RN_WAVE_1: return chain_pick_rn<RN_WAVE_1>(u4);
+    case RN_WAVE_2: return chain_pick_rn<RN_WAVE_2>(u4);
+    case RN_BLOCK_1: return chain_pick_rn<RN_BLOCK_1>(u4);
+    case RN_BLOCK_2: return chain_pick_rn<RN_BLOCK_2>(u4);
+    case RN_BLOCK_4: return chain_pick_rn<RN_BLOCK_4>(u4);
+    case RN_BLOCK_8: return chain_pick_rn<RN_BLOCK_8>(u4);
+    case RN_BLOCK_16: return chain_pick_rn<RN_BLOCK_16>(u4);
     default: return nullptr;
   }
 }

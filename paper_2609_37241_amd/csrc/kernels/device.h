@@ -101,10 +101,33 @@ __device__ inline void st16(u32x4 *p, const u32x4 &v) {
 }
 
 // ---- reductions ----------------------------------------------------------------
-// Butterfly over the 64 lanes: every lane ends with the same, bitwise equal
-// total (each exchange adds the same two operands on both partners).
-template <typename T>
-__device__ inline T wave_sum(T v) {
+// DPP move within a row of 16 lanes (every source lane is in range for the
+// controls used here, so no lane reads an out-of-row value).
+template <int CTRL>
+__device__ inline float dpp_mov(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+
+// Sum over the 64 lanes of a wavefront (all lanes active). Within each row of
+// 16 lanes: exchange with lane^1 and lane^2 (quad permutes), then with the
+// mirrored lane in each half row and in the row, so every lane holds its
+// row's sum; the four row sums are read from lanes 0, 16, 32, 48 and added in
+// a fixed order. Every lane returns the same, bitwise equal total.
+__device__ inline float wave_sum(float v) {
+  v += dpp_mov<0xB1>(v);    // quad_perm [1,0,3,2]
+  v += dpp_mov<0x4E>(v);    // quad_perm [2,3,0,1]
+  v += dpp_mov<0x141>(v);   // row_half_mirror
+  v += dpp_mov<0x140>(v);   // row_mirror
+  const int b = __float_as_int(v);
+  const float r0 = __int_as_float(__builtin_amdgcn_readlane(b, 0));
+  const float r1 = __int_as_float(__builtin_amdgcn_readlane(b, 16));
+  const float r2 = __int_as_float(__builtin_amdgcn_readlane(b, 32));
+  const float r3 = __int_as_float(__builtin_amdgcn_readlane(b, 48));
+  return (r0 + r1) + (r2 + r3);
+}
+
+// float64 butterfly over the 64 lanes (long-row and scalar norm paths).
+__device__ inline double wave_sum(double v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
   return v;
@@ -323,11 +346,10 @@ __device__ __forceinline__ char *rope_head(const RopeArgs &a, int64_t t, int h, 
 // (token, head) items are processed PF at a time with all loads issued before
 // any use, and the first batch is requested before the angle math and the
 // barrier, so at decode sizes the block costs one memory round trip.
-template <int DT, int TPB, bool NT>
+template <int DT, int TPB, bool NT, int PF = 4>
 __device__ __forceinline__ void rope_vec_block(const RopeArgs &a, int64_t blk, float *lds) {
   using E = Elt<DT>;
   constexpr int V = E::V;
-  constexpr int PF = 4;
   const int half = a.hd >> 1;
   const int lh = __builtin_ctz(unsigned(half));
   const int cpb = half / V;

@@ -36,9 +36,6 @@ const void *rn_pick(int32_t variant) {
     case RN_SCALAR: return reinterpret_cast<const void *>(&k_rn_scalar<DT, RES>);
     case RN_WAVE_1: return reinterpret_cast<const void *>(&k_rn_wave<DT, 1, RES>);
     case RN_WAVE_2: return reinterpret_cast<const void *>(&k_rn_wave<DT, 2, RES>);
-    case RN_WAVE_4: return reinterpret_cast<const void *>(&k_rn_wave<DT, 4, RES>);
-    case RN_WAVE_8: return reinterpret_cast<const void *>(&k_rn_wave<DT, 8, RES>);
-    case RN_WAVE_16: return reinterpret_cast<const void *>(&k_rn_wave<DT, 16, RES>);
     case RN_BLOCK_1: return reinterpret_cast<const void *>(&k_rn_block<DT, 1, RES>);
     case RN_BLOCK_2: return reinterpret_cast<const void *>(&k_rn_block<DT, 2, RES>);
     case RN_BLOCK_4: return reinterpret_cast<const void *>(&k_rn_block<DT, 4, RES>);

@@ -5,10 +5,10 @@
 namespace tri {
 using namespace dev;
 
-template <int DT, int TPB>
+template <int DT>
 __global__ __launch_bounds__(256) void k_rope_vec(RopeArgs a) {
-  __shared__ float lds[2 * TPB * 256];
-  rope_vec_block<DT, TPB, false>(a, blockIdx.x, lds);
+  __shared__ float lds[2 * 256];
+  rope_vec_block<DT, 1, false>(a, blockIdx.x, lds);
 }
 
 template <int DT>
@@ -22,8 +22,7 @@ template <int DT>
 const void *rope_pick(int32_t variant) {
   switch (variant) {
     case ROPE_SCALAR: return reinterpret_cast<const void *>(&k_rope_scalar<DT>);
-    case ROPE_VEC_T1: return reinterpret_cast<const void *>(&k_rope_vec<DT, 1>);
-    case ROPE_VEC_T4: return reinterpret_cast<const void *>(&k_rope_vec<DT, 4>);
+    case ROPE_VEC: return reinterpret_cast<const void *>(&k_rope_vec<DT>);
     default: return nullptr;
   }
 }

@@ -125,9 +125,10 @@ RN_CASES = [
     (nm.BF16, 6, 4096, "plain"), (nm.BF16, 5, 8192, "plain"), (nm.BF16, 3, 32768, "plain"),
     (nm.BF16, 2, 65536, "plain"), (nm.BF16, 4, 100, "plain"), (nm.BF16, 7, 4096, "unaligned"),
     (nm.BF16, 7, 4096, "strided"), (nm.BF16, 3, 1, "plain"),
-    # beyond decode sizes (> 64 tokens): one workgroup per row
+    # more rows and short rows (a wavefront per row, 4 rows per block)
     (nm.BF16, 130, 4096, "plain"), (nm.F32, 100, 256, "plain"), (nm.BF16, 70, 8192, "plain"),
     (nm.F32, 65, 4096, "unaligned"), (nm.BF16, 66, 4096, "strided"), (nm.F32, 67, 16384, "plain"),
+    (nm.BF16, 13, 1024, "plain"), (nm.BF16, 13, 1032, "plain"), (nm.F32, 7, 512, "plain"),
 ]
 
 
@@ -156,8 +157,7 @@ def test_rmsnorm_variants(tri, cache, dtype, T, H, layout, res):
     sel = cache.last_selection()
     es = 4 if dtype == nm.F32 else 2
     flags = S.ALIGN if (xd.data_ptr() % 16 == 0 and (xd.stride(0) * es) % 16 == 0) else 0
-    assert sel.variant == S.rn_role(S.DT_F32 if dtype == nm.F32 else S.DT_BF16, H, flags,
-                                    S.bucket(T), T)[0]
+    assert sel.variant == S.rn_role(S.DT_F32 if dtype == nm.F32 else S.DT_BF16, H, flags, T)[0]
 
 
 def test_rmsnorm_in_place(tri, cache):
@@ -270,8 +270,8 @@ MEDIUM = [wl.ChainConfig("medium_bf16", wl.BF16, T=100, H=4096, nq=32, nk=8, hd=
 
 @pytest.mark.parametrize("cfg", MEDIUM, ids=lambda c: c.name)
 def test_chain_beyond_decode_sizes(tri, cache, cfg):
-    """Fused chain with the workgroup-per-row norm role, 4-token RoPE blocks
-    and the streaming 4-vector SwiGLU role (ragged tails included)."""
+    """Fused chain with the workgroup-per-row norm role and the streaming
+    4-vector SwiGLU role (ragged tails included)."""
     inp = wl.host_inputs(cfg)
     d = {k: wl.to_torch(v, cfg.dtype, DEV) for k, v in inp.items()}
     d["y"], d["res_out"], d["out"] = (torch.empty_like(d["x"]), torch.empty_like(d["x"]),
@@ -356,7 +356,7 @@ def test_prefill_chain_full_size_sampled(tri, cache):
                                     d["gate"], d["up"], cfg.eps, cfg.base)
     torch.cuda.synchronize()
     rec = cache.last_selection()
-    assert rec.variant == S.CH_FUSED and rec.launch[0].grid_x == 8192 + 2048 + 28672
+    assert rec.variant == S.CH_FUSED and rec.launch[0].grid_x == 8192 + 8192 + 28672
     rows = np.sort(rng(99).choice(cfg.T, size=40, replace=False))
     rows = np.concatenate([[0, 1, 2, 3, cfg.T - 1], rows])
     ri = torch.from_numpy(rows).to(DEV)

@@ -286,7 +286,7 @@ def test_rmsnorm_argument_block_and_stream(lib, fresh):
     c = res_call(BF, 5, 4096, pad=64)
     assert c_call(lib, cache, c, stream=0xABC0) == 0
     kv, dt, sub, grid, block, stream, raw = _last_launch(lib)
-    assert (kv, dt, sub, grid, block, stream) == (14, BF, 1, 2, 256, 0xABC0)
+    assert (kv, dt, sub, grid, block, stream) == (S.RN_BLOCK[2], BF, 1, 5, 256, 0xABC0)
     f = struct.unpack_from("<5Q4qqif", raw)
     p = c.ptr
     assert f[:5] == (p["x"], p["res"], p["w"], p["y"], p["res_out"])
@@ -299,15 +299,15 @@ def test_chain_argument_block(lib, fresh):
     c = chain_call(BF, 8, 4096, 14336, 32, 8, 128, base=500000.0)
     assert c_call(lib, cache, c) == 0
     kv, dt, sub, grid, block, _, raw = _last_launch(lib)
-    # fused kernel: RN_WAVE_8 (NV index 3), one RoPE token per block, U = 1
-    assert (kv, dt, sub, grid, block) == (50, BF, 3 * 4, 2 + 8 + 56, 256)
+    # fused kernel: RN_BLOCK_2 (norm role index 3), cached one-vector SwiGLU
+    assert (kv, dt, sub, grid, block) == (50, BF, 3 * 2, 8 + 8 + 56, 256)
     rope = struct.unpack_from("<4Q3q4i", raw, 88)
     assert rope[0] == c.ptr["q"] and rope[1] == c.ptr["k"] and rope[2] == c.ptr["pos"]
     assert rope[4:7] == (32 * 128, 8 * 128, 8) and rope[7:10] == (32, 8, 128)
     sw = struct.unpack_from("<3Q7q", raw, 160)
     assert sw[:3] == (c.ptr["gate"], c.ptr["up"], c.ptr["out"])
     assert sw[3:] == (14336, 14336, 14336, 8, 14336, 8 * 14336 // 8, 8 * 14336)
-    assert struct.unpack_from("<2I", raw, 240) == (2, 8)
+    assert struct.unpack_from("<2I", raw, 240) == (8, 8)
     # the RoPE table pointer is this version's uploaded constants
     assert rope[3] != 0
 

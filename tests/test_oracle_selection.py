@@ -35,9 +35,9 @@ def test_unused_key_fields_are_zero():
 
 # ---- policy worked by hand --------------------------------------------------------
 def test_policy_llama7b_decode_chain():
-    # bf16: 8 elements per 16 B. H = 4096 -> 512 vectors -> 8 per lane -> RN_WAVE_8,
-    # 1 row -> 1 workgroup. T = 1 -> bucket 0 -> RoPE one token per block, SwiGLU
-    # one vector per thread: 11008 / 8 = 1376 vectors -> 6 workgroups.
+    # bf16: 8 elements per 16 B. H = 4096 -> 512 vectors -> 2 per work-item ->
+    # RN_BLOCK_2, one workgroup per row. RoPE one token per block; T = 1 ->
+    # bucket 0 -> SwiGLU one vector per thread: 11008 / 8 = 1376 vectors -> 6 blocks.
     v, roles, launches = S.plan(S.make_key(chain_call(BF, 1, 4096, 11008, 32, 32, 128)), 1)
     assert v == S.CH_FUSED
     assert roles == (14, 31, 41)
@@ -45,49 +45,47 @@ def test_policy_llama7b_decode_chain():
 
 
 def test_policy_gqa_decode_chain():
-    # T = 8 -> bucket 3: RoPE still one token per block (8 blocks);
-    # SwiGLU 8 * 14336 / 8 = 14336 vectors -> 56 blocks; norm ceil(8/4) = 2.
+    # T = 8 -> bucket 3: norm and RoPE one block per row / token (8 + 8);
+    # SwiGLU 8 * 14336 / 8 = 14336 vectors -> 56 blocks.
     v, roles, launches = S.plan(S.make_key(chain_call(BF, 8, 4096, 14336, 32, 8, 128,
                                                       base=500000.0)), 8)
-    assert (v, roles, launches) == (S.CH_FUSED, (14, 31, 41), [(50, 2 + 8 + 56, 256)])
+    assert (v, roles, launches) == (S.CH_FUSED, (14, 31, 41), [(50, 8 + 8 + 56, 256)])
 
 
 def test_policy_prefill_chain():
     # T = 8192 -> bucket 13, beyond decode sizes: H = 8192 bf16 -> 1024 vectors
-    # -> 4 per work-item -> RN_BLOCK_4, one block per row (8192); RoPE 4 tokens
-    # per block (2048 blocks); SwiGLU role 8192 * 28672 / 8 = 29360128 vectors
+    # -> 4 per work-item -> RN_BLOCK_4, one block per row (8192); RoPE one token
+    # per block (8192 blocks); SwiGLU role 8192 * 28672 / 8 = 29360128 vectors
     # at 4 per work-item, streaming -> 28672 blocks.
     v, roles, launches = S.plan(S.make_key(chain_call(BF, 8192, 8192, 28672, 64, 8, 128,
                                                       base=500000.0)), 8192)
-    assert (v, roles) == (S.CH_FUSED, (18, 32, 44))
-    assert launches == [(50, 8192 + 2048 + 28672, 256)]
+    assert (v, roles) == (S.CH_FUSED, (15, 31, 44))
+    assert launches == [(50, 8192 + 8192 + 28672, 256)]
 
 
 def test_policy_tiny_f32_chain():
     # f32: 4 per 16 B. H = 256 -> 64 vectors -> 1 per lane -> RN_WAVE_1.
-    # hd 64 -> 32 pairs -> 8 vectors per half (power of two) -> ROPE_VEC_T1.
+    # hd 64 -> 32 pairs -> 8 vectors per half (power of two) -> ROPE_VEC.
     # SwiGLU 4 * 688 / 4 = 688 vectors -> 3 blocks.
     v, roles, launches = S.plan(S.make_key(chain_call(F, 4, 256, 688, 4, 4, 64)), 4)
     assert (v, roles, launches) == (S.CH_FUSED, (11, 31, 41), [(50, 1 + 4 + 3, 256)])
 
 
 @pytest.mark.parametrize("H,dtype,want", [
-    (64, F, (11, 2)), (256, BF, (11, 2)), (520, BF, (12, 2)), (4096, F, (15, 2)),
-    (8192, F, (19, 5)), (16384, F, (20, 5)), (32768, BF, (20, 5)),
-    (65536, BF, (21, 5)), (100, BF, (10, 5)), (4097, F, (10, 5))])
+    (64, F, (11, 2)), (256, BF, (11, 2)), (520, BF, (12, 2)), (1024, BF, (12, 2)),
+    (1032, BF, (13, 5)), (4096, F, (15, 5)), (8192, F, (16, 5)), (16384, F, (17, 5)),
+    (32768, BF, (17, 5)), (65536, BF, (18, 5)), (100, BF, (10, 5)), (4097, F, (10, 5))])
 def test_rmsnorm_policy_by_row_size(H, dtype, want):
-    # 5 rows (bucket 3, decode sized): one wave per row packs 4 rows per block
-    # (2 blocks); rows beyond 16 vectors per lane take one block per row.
-    v, g = S.rn_role(dtype, H, S.ALIGN | S.CONTIG, S.bucket(5), 5)
+    # 5 rows: rows of <= 128 vectors take a wavefront each, 4 per block
+    # (2 blocks); longer rows one block per row (5 blocks).
+    v, g = S.rn_role(dtype, H, S.ALIGN | S.CONTIG, 5)
     assert (v, g) == want
 
 
-@pytest.mark.parametrize("H,dtype,T,want", [
-    (4096, BF, 65, (17, 65)), (8192, BF, 8192, (18, 8192)), (256, F, 100, (16, 100)),
-    (4096, BF, 64, (14, 16)), (65536, F, 128, (21, 128))])
-def test_rmsnorm_policy_beyond_decode_sizes(H, dtype, T, want):
-    # more than 64 tokens: one workgroup per row, NB = next_pow2(H/v / 256)
-    assert S.rn_role(dtype, H, S.ALIGN | S.CONTIG, S.bucket(T), T) == want
+@pytest.mark.parametrize("T", [1, 8, 64, 65, 8192])
+def test_rmsnorm_policy_does_not_depend_on_tokens(T):
+    assert S.rn_role(BF, 4096, S.ALIGN | S.CONTIG, T) == (S.RN_BLOCK[2], T)
+    assert S.rn_role(F, 256, S.ALIGN | S.CONTIG, T) == (S.RN_WAVE[1], -(-T // 4))
 
 
 def test_unaligned_and_strided_layouts():
