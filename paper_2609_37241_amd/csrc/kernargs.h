@@ -45,8 +45,9 @@ struct SwArgs {
   int64_t n;              // flat variants: T*I elements
 };
 
-// The fused decode chain: workgroups [0, rn_blocks) run residual RMSNorm rows,
-// [rn_blocks, rn_blocks + rope_blocks) RoPE tokens, the rest SwiGLU.
+// The fused decode chain: rn_blocks workgroups run residual RMSNorm rows,
+// rope_blocks run RoPE tokens, the remaining gridDim.x - rn_blocks -
+// rope_blocks run SwiGLU (the kernel fixes the order of the three ranges).
 struct ChainArgs {
   RnArgs rn;
   RopeArgs rope;

@@ -11,29 +11,44 @@ using namespace dev;
 // workgroup per row); the RoPE role takes one token per workgroup; SWV:
 // SW_FLAT (one vector per work-item, cached) or SW_FLAT_U4_NT (four,
 // streaming).
+template <int DT, int RNV>
+__device__ __forceinline__ void chain_norm_role(const ChainArgs &a, uint32_t blk) {
+  if constexpr (RNV <= RN_WAVE_2) {
+    rn_wave_block<DT, 1 << (RNV - RN_WAVE_1), true, false>(a.rn, blk);
+  } else {
+    __shared__ float red[4];
+    rn_row_regs<DT, 1 << (RNV - RN_BLOCK_1), true, 256, false>(a.rn, blk, threadIdx.x, red);
+  }
+}
+
+// Role order by blockIdx. Decode sizes (SW_FLAT): norm rows, RoPE tokens,
+// then SwiGLU -- the norm and RoPE roles take about as long as SwiGLU but
+// have far fewer workgroups, so dispatching them first shortens the critical
+// path (2.75 vs 3.1 µs device time at 1 token). Streaming sizes
+// (SW_FLAT_U4_NT): SwiGLU first, then norm, then RoPE (about 1 % faster at
+// 8192 tokens than norm first).
 template <int DT, int RNV, int SWV>
 __global__ __launch_bounds__(256) void k_chain(ChainArgs a) {
   __shared__ float lds[2 * 256];
   const uint32_t b = blockIdx.x;
-  if (b < a.rn_blocks) {
-    if constexpr (RNV <= RN_WAVE_2) {
-      rn_wave_block<DT, 1 << (RNV - RN_WAVE_1), true, false>(a.rn, b);
+  const uint32_t R = a.rn_blocks, P = a.rope_blocks, S = gridDim.x - R - P;
+  if constexpr (SWV == SW_FLAT_U4_NT) {
+    if (b < S) {
+      sw_flat_part<DT, 4, true>(a.sw, b, S);
+    } else if (b < S + R) {
+      chain_norm_role<DT, RNV>(a, b - S);
     } else {
-      __shared__ float red[4];
-      rn_row_regs<DT, 1 << (RNV - RN_BLOCK_1), true, 256, false>(a.rn, b, threadIdx.x, red);
+      rope_vec_block<DT, 1, false>(a.rope, b - S - R, lds);
     }
-    return;
+  } else {
+    if (b < R) {
+      chain_norm_role<DT, RNV>(a, b);
+    } else if (b < R + P) {
+      rope_vec_block<DT, 1, false>(a.rope, b - R, lds);
+    } else {
+      sw_flat_part<DT, 1, false>(a.sw, b - R - P, S);
+    }
   }
-  const uint32_t b1 = b - a.rn_blocks;
-  if (b1 < a.rope_blocks) {
-    rope_vec_block<DT, 1, false>(a.rope, b1, lds);
-    return;
-  }
-  const uint32_t nsw = gridDim.x - a.rn_blocks - a.rope_blocks;
-  if constexpr (SWV == SW_FLAT_U4_NT)
-    sw_flat_part<DT, 4, true>(a.sw, b1 - a.rope_blocks, nsw);
-  else
-    sw_flat_part<DT, 1, false>(a.sw, b1 - a.rope_blocks, nsw);
 }
 
 namespace {
