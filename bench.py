@@ -67,6 +67,25 @@ def algorithmic_bytes(cfg):
             "chain": res + rope + sw}
 
 
+def torch_eager_chain(d, eps, base, out):
+    """The same decode chain written as PyTorch eager ops: the comparison the
+    paper measures against (its eager wrapper). Context only; not part of the
+    library. Angles as float32 products, rotate-half pairs."""
+    import torch
+    import torch.nn.functional as F
+    h = d["x"] + d["residual"]
+    out["res_out"].copy_(h)
+    out["y"].copy_(F.rms_norm(h, (h.shape[-1],), d["w"], eps))
+    hd = d["q"].shape[-1]
+    inv = out["inv_freq"]
+    th = d["pos"].to(torch.float32)[:, None] * inv[None, :]
+    c, s = torch.cos(th)[:, None, :], torch.sin(th)[:, None, :]
+    for t in (d["q"], d["k"]):
+        v1, v2 = t[..., : hd // 2].float(), t[..., hd // 2:].float()
+        t.copy_(torch.cat([v1 * c - v2 * s, v2 * c + v1 * s], dim=-1))
+    out["out"].copy_(F.silu(d["gate"]) * d["up"])
+
+
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "chain_prefill8k_hbm_traffic.md")
 TRAFFIC_SOURCES = ("paper_2609_37241_amd/csrc/kernargs.h",
                    "paper_2609_37241_amd/csrc/kernels/device.h",
@@ -234,6 +253,37 @@ def main():
                       "grid": sel.launch[0].grid_x, "roles": list(sel.roles)},
         "cache_stats": stats,
     }
+
+    # ---- context: the same chain as PyTorch eager ops, and HIP-graph replay ---------------
+    import torch.nn.functional as F  # noqa: F401
+    eager_out = {k: torch.empty_like(v) for k, v in (("res_out", d["x"]), ("y", d["x"]),
+                                                      ("out", d["gate"]))}
+    eager_out["inv_freq"] = torch.tensor(cache.version_constants(0), device=dev)
+    with torch.cuda.stream(stream):
+        for _ in range(20):
+            torch_eager_chain(d, cfg.eps, cfg.base, eager_out)
+    stream.synchronize()
+    eager = []
+    for _ in range(min(K, 2000)):
+        a = time.perf_counter()
+        with torch.cuda.stream(stream):
+            torch_eager_chain(d, cfg.eps, cfg.base, eager_out)
+        stream.synchronize()
+        eager.append((time.perf_counter() - a) * 1e6)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=stream):
+        cache.decode_chain_args(args_c, stream=torch.cuda.current_stream())
+    graph.replay()
+    stream.synchronize()
+    replay = []
+    for _ in range(min(K, 2000)):
+        a = time.perf_counter()
+        graph.replay()
+        stream.synchronize()
+        replay.append((time.perf_counter() - a) * 1e6)
+    latency["torch_eager_chain_e2e_us"] = summary(eager)
+    latency["hip_graph_replay_e2e_us"] = summary(replay)
+    latency["speedup_vs_torch_eager"] = summary(eager)["median"] / ce["median"]
 
     # ---- GQA decode (8 tokens, 32 Q / 8 K heads, base 5e5): same loop -------------------
     cfg2 = wl.GQA_DECODE

@@ -419,3 +419,43 @@ def test_mixed_stream_selection_and_outputs(tri, cache):
     torch.cuda.synchronize()
     s = cache.stats()
     assert s["misses"] == model.stats.misses and s["n_versions"] == len(model.versions)
+
+
+# ---- HIP graph capture of the hit path ------------------------------------------------------
+def test_chain_call_replays_from_a_hip_graph(tri, cache):
+    """A hit is one plain kernel launch, so it can be captured in a graph and
+    replayed. Replays run with eager work and synchronisations in between and
+    each must equal a direct call on a twin set of buffers, bit for bit."""
+    cfg = wl.LLAMA7B_DECODE
+    inp = wl.host_inputs(cfg)
+    A = {k: wl.to_torch(v, cfg.dtype, DEV) for k, v in inp.items()}
+    B = {k: v.clone() for k, v in A.items()}
+    for d in (A, B):
+        d["y"], d["res_out"], d["out"] = (torch.empty_like(d["x"]), torch.empty_like(d["x"]),
+                                          torch.empty_like(d["gate"]))
+    args_a, _ = cache.chain_args(A["x"], A["residual"], A["w"], A["q"], A["k"], A["pos"],
+                                 A["gate"], A["up"], cfg.eps, cfg.base, y=A["y"],
+                                 residual_out=A["res_out"], out=A["out"])
+    args_b, _ = cache.chain_args(B["x"], B["residual"], B["w"], B["q"], B["k"], B["pos"],
+                                 B["gate"], B["up"], cfg.eps, cfg.base, y=B["y"],
+                                 residual_out=B["res_out"], out=B["out"])
+    cache.decode_chain_args(args_b)            # installs the version (no allocation later)
+    torch.cuda.synchronize()
+    B["q"].copy_(A["q"])                       # undo B's rotation: both start equal
+    B["k"].copy_(A["k"])
+    s = torch.cuda.Stream()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        cache.decode_chain_args(args_a, stream=torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    # capture does not run the kernel: A is still untouched
+    check("q before replay", host(A["q"]), host(B["q"]), cfg.dtype, exact=True)
+    for step in range(4):
+        for d in (A, B):                       # the program's own eager work in between
+            d["x"].mul_(0.5).add_(0.25)
+        torch.cuda.synchronize()
+        g.replay()
+        cache.decode_chain_args(args_b)
+        torch.cuda.synchronize()
+        for n in ("y", "res_out", "q", "k", "out"):
+            check(f"replay {step}: {n}", host(A[n]), host(B[n]), cfg.dtype, exact=True)
