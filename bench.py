@@ -299,6 +299,22 @@ def main():
     latency["gqa_decode_chain_e2e_us"] = summary(list(e2e[:n2]))
     latency["gqa_decode_chain_host_us"] = summary(list(hst[:n2]))
 
+    # ---- Qwen3-8B-shaped decode (1 token, per-head QK-RMSNorm before RoPE) -------------
+    cfg3 = wl.QWEN3_8B_DECODE
+    inp3 = wl.host_inputs(cfg3)
+    d3 = {k: wl.to_torch(v, cfg3.dtype, dev) for k, v in inp3.items()}
+    args3, _outs3 = cache.chain_args(d3["x"], d3["residual"], d3["w"], d3["q"], d3["k"],
+                                     d3["pos"], d3["gate"], d3["up"], cfg3.eps, cfg3.base,
+                                     q_norm_w=d3["q_norm_w"], k_norm_w=d3["k_norm_w"])
+    cache.decode_chain_args(args3, stream)
+    torch.cuda.synchronize()
+    sel3 = cache.last_selection()
+    st = bench.trib_latency(cache.handle, 0, C.byref(args3), sptr, W, n2, e2e, hst)
+    assert st == 0, st
+    latency["qk_norm_decode_chain_e2e_us"] = summary(list(e2e[:n2]))
+    latency["qk_norm_decode_chain_host_us"] = summary(list(hst[:n2]))
+    latency["qk_norm_decode_selection"] = {"variant": sel3.variant, "roles": list(sel3.roles)}
+
     # ---- mixed-shape stream: guard hits, misses, latency per token bucket ---------------
     mixed = None if args.no_stream else run_mixed_stream(tri, wl, bench, dev, stream, torch)
 

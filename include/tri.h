@@ -67,7 +67,7 @@ typedef enum tri_status {
 
 typedef enum tri_op {
   TRI_OP_RMSNORM = 1, TRI_OP_RES_RMSNORM = 2, TRI_OP_ROPE_QK = 3,
-  TRI_OP_SWIGLU = 4, TRI_OP_CHAIN = 5
+  TRI_OP_SWIGLU = 4, TRI_OP_CHAIN = 5, TRI_OP_QK_NORM_ROPE = 6
 } tri_op;
 
 enum { TRI_CACHE_AUTO_INSTALL = 1u };   /* on a miss: install, then launch */
@@ -130,6 +130,13 @@ typedef struct tri_chain_args {
   const void *gate; int64_t g_rs;
   const void *up;   int64_t u_rs;
   void *out;        int64_t o_rs;
+  /* optional per-head RMSNorm of Q and K before RoPE (Qwen3-style): NULL
+   * q_norm_w disables it; otherwise q_norm_w [hd] and (when nk > 0)
+   * k_norm_w [hd] are the head-norm weights and qk_eps their epsilon. */
+  const void *q_norm_w;
+  const void *k_norm_w;
+  float qk_eps;
+  int32_t reserved;    /* padding; ignored */
 } tri_chain_args;
 
 /* ---- cache ---------------------------------------------------------------- */
@@ -178,14 +185,29 @@ tri_status tri_rope_qk(tri_cache *cache, tri_dtype dtype,
                        int32_t nq, int32_t nk, int32_t hd, float base,
                        void *stream);
 
+/* Per-head RMSNorm of Q and K followed by RoPE, in place (the head layout of
+ * Qwen3, one of the two model families the paper evaluates, Sec. 4.1): each
+ * head vector v is normalised to n = q_w * v / sqrt(mean(v^2) + eps) (k_w
+ * for K heads; mean over the hd elements, float32 on the device), n is
+ * rotated with the angles of tri_rope_qk, and the result is rounded to the
+ * dtype once (n is not rounded). q_w [hd] is required, k_w [hd] when
+ * nk > 0; both element-aligned; eps finite and >= 0. Other arguments and
+ * errors as tri_rope_qk. */
+tri_status tri_qk_norm_rope(tri_cache *cache, tri_dtype dtype,
+                            void *q, int64_t q_ts, void *k, int64_t k_ts,
+                            const int32_t *pos, int64_t T,
+                            int32_t nq, int32_t nk, int32_t hd, float base,
+                            const void *q_w, const void *k_w, float eps, void *stream);
+
 /* SwiGLU: out = g / (1 + exp(-g)) * u over [T, I] (`silu` is in the paper's
  * kernel suite, Sec. 4.1). out may alias gate or up exactly. */
 tri_status tri_swiglu(tri_cache *cache, tri_dtype dtype,
                       const void *gate, int64_t g_rs, const void *up, int64_t u_rs,
                       void *out, int64_t o_rs, int64_t T, int64_t I, void *stream);
 
-/* The decode chain: residual+RMSNorm, RoPE-QK and SwiGLU of one decode step,
- * on disjoint operands (overlap between the three ops is undefined). When
+/* The decode chain: residual+RMSNorm, RoPE-QK (or QK-RMSNorm + RoPE when
+ * q_norm_w is set) and SwiGLU of one decode step, on disjoint operands
+ * (overlap between the three ops is undefined). When
  * every tensor is 16-byte aligned and contiguous this is ONE launch of a
  * fused kernel whose workgroups take the three roles by blockIdx range;
  * otherwise three launches. If a later launch of the three fails, earlier

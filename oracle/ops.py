@@ -21,7 +21,12 @@ are:
 * SwiGLU: out = g / (1 + exp(-g)) * u with the gate as the first operand;
   for very negative g the exponential overflows and the result is a signed
   zero, never NaN.
-* Decode chain: the three ops above on disjoint operands, in one call.
+* QK-RMSNorm before RoPE (Qwen3-style heads): every Q and K head vector is
+  RMS-normalised over its hd elements with a per-dimension weight (one
+  weight vector for Q, one for K) and then rotated; the normalised head is
+  not rounded in between, so the fused op rounds once, like every op here.
+* Decode chain: the three ops above on disjoint operands, in one call; with
+  head-norm weights given, RoPE becomes QK-RMSNorm + RoPE.
 """
 from __future__ import annotations
 
@@ -33,14 +38,16 @@ import numpy as np
 from .numerics import BF16, F32, round_to, values
 
 
-def rmsnorm(x: np.ndarray, w: np.ndarray, eps: float, dtype: str) -> np.ndarray:
-    """RMSNorm over the last axis. x: [..., H], w: [H]."""
-    xv = values(x, dtype)
-    wv = values(w, dtype)
+def _rmsnorm64(xv: np.ndarray, wv: np.ndarray, eps: float) -> np.ndarray:
+    """w * x / sqrt(mean(x^2) + eps) over the last axis, float64 in and out."""
     eps64 = float(np.float32(eps))          # the caller passes eps as float32
     ms = np.mean(xv * xv, axis=-1, keepdims=True)
-    y = wv * xv / np.sqrt(ms + eps64)
-    return round_to(y, dtype)
+    return wv * xv / np.sqrt(ms + eps64)
+
+
+def rmsnorm(x: np.ndarray, w: np.ndarray, eps: float, dtype: str) -> np.ndarray:
+    """RMSNorm over the last axis. x: [..., H], w: [H]."""
+    return round_to(_rmsnorm64(values(x, dtype), values(w, dtype), eps), dtype)
 
 
 def residual_add(x: np.ndarray, r: np.ndarray, dtype: str) -> np.ndarray:
@@ -94,16 +101,19 @@ def rope_angles(pos: np.ndarray, inv: np.ndarray) -> np.ndarray:
     return th.astype(np.float64)
 
 
-def rope_apply(v: np.ndarray, theta: np.ndarray, dtype: str) -> np.ndarray:
-    """Rotate-half RoPE of v: [T, nh, hd] by angles theta: [T, hd/2]."""
-    vv = values(v, dtype)
+def _rotate64(vv: np.ndarray, theta: np.ndarray) -> np.ndarray:
+    """Rotate-half of float64 heads vv: [T, nh, hd] by theta: [T, hd/2]."""
     half = vv.shape[-1] // 2
     c = np.cos(theta)[:, None, :]
     s = np.sin(theta)[:, None, :]
     v1 = vv[..., :half]
     v2 = vv[..., half:]
-    out = np.concatenate([v1 * c - v2 * s, v2 * c + v1 * s], axis=-1)
-    return round_to(out, dtype)
+    return np.concatenate([v1 * c - v2 * s, v2 * c + v1 * s], axis=-1)
+
+
+def rope_apply(v: np.ndarray, theta: np.ndarray, dtype: str) -> np.ndarray:
+    """Rotate-half RoPE of v: [T, nh, hd] by angles theta: [T, hd/2]."""
+    return round_to(_rotate64(values(v, dtype), theta), dtype)
 
 
 def rope_qk(q, k, pos, base, dtype):
@@ -112,6 +122,20 @@ def rope_qk(q, k, pos, base, dtype):
     theta = rope_angles(pos, rope_inv_freq(base, hd))
     qo = rope_apply(q, theta, dtype)
     ko = rope_apply(k, theta, dtype) if k is not None and k.size else k
+    return qo, ko
+
+
+def qk_norm_rope(q, k, pos, base, q_w, k_w, eps, dtype):
+    """Per-head RMSNorm of Q [T, nq, hd] and K [T, nk, hd] (weights [hd]),
+    then rotate-half RoPE of the normalised heads; one rounding at the end."""
+    hd = q.shape[-1]
+    theta = rope_angles(pos, rope_inv_freq(base, hd))
+
+    def one(v, w):
+        n = _rmsnorm64(values(v, dtype), values(w, dtype), eps)
+        return round_to(_rotate64(n, theta), dtype)
+    qo = one(q, q_w)
+    ko = one(k, k_w) if k is not None and k.size else k
     return qo, ko
 
 
@@ -128,11 +152,15 @@ def decode_chain(inp: Dict[str, np.ndarray], eps: float, base: float,
                  dtype: str) -> Dict[str, np.ndarray]:
     """Residual add + RMSNorm, RoPE on Q/K and SwiGLU on disjoint operands."""
     y, h = residual_rmsnorm(inp["x"], inp["residual"], inp["w"], eps, dtype)
-    qo, ko = rope_qk(inp["q"], inp["k"], inp["pos"], base, dtype)
+    if inp.get("q_norm_w") is not None:
+        qo, ko = qk_norm_rope(inp["q"], inp["k"], inp["pos"], base, inp["q_norm_w"],
+                              inp["k_norm_w"], inp.get("qk_eps", eps), dtype)
+    else:
+        qo, ko = rope_qk(inp["q"], inp["k"], inp["pos"], base, dtype)
     out = swiglu(inp["gate"], inp["up"], dtype)
     return dict(y=y, res_out=h, q=qo, k=ko, out=out)
 
 
 __all__ = ["rmsnorm", "residual_add", "residual_rmsnorm", "rope_inv_freq",
-           "rope_angles", "rope_apply", "rope_qk", "swiglu", "decode_chain",
+           "rope_angles", "rope_apply", "rope_qk", "qk_norm_rope", "swiglu", "decode_chain",
            "F32", "BF16"]

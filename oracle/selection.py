@@ -12,8 +12,9 @@ What it models
   an error never installs anything.
 * Guards are the ones a specialization of these ops depends on: dtype,
   hidden / intermediate sizes, head_dim and head counts, a token-count
-  bucket, 16-byte alignment, contiguity, and the RoPE base (a captured
-  constant of the version, as source-visible constants are in Sec. 3.3).
+  bucket, 16-byte alignment, contiguity, whether the RoPE step carries the
+  per-head QK RMSNorm, and the RoPE base (a captured constant of the
+  version, as source-visible constants are in Sec. 3.3).
 
 Guards are equality tests on a packed key, so two versions can never both
 match and "first match in creation order" is the unique match.
@@ -34,7 +35,8 @@ from typing import Dict, List, Optional, Tuple
 import numpy as np
 
 # ---- enumerations (the ABI's numeric values) --------------------------------
-OP_RMSNORM, OP_RES_RMSNORM, OP_ROPE_QK, OP_SWIGLU, OP_CHAIN = 1, 2, 3, 4, 5
+OP_RMSNORM, OP_RES_RMSNORM, OP_ROPE_QK, OP_SWIGLU, OP_CHAIN, OP_QK_NORM_ROPE = 1, 2, 3, 4, 5, 6
+ROPE_OPS = (OP_ROPE_QK, OP_QK_NORM_ROPE, OP_CHAIN)
 DT_F32, DT_BF16 = 0, 1
 OK, MISS = 0, 1
 E_INVALID, E_UNSUPPORTED, E_FULL, E_NOMEM, E_LAUNCH, E_RUNTIME = -1, -2, -3, -4, -5, -6
@@ -43,7 +45,7 @@ RN_SCALAR = 10
 RN_WAVE = {1: 11, 2: 12}
 RN_BLOCK = {1: 13, 2: 14, 4: 15, 8: 16, 16: 17}
 RN_LOOP = 18
-ROPE_SCALAR, ROPE_VEC = 30, 31
+ROPE_SCALAR, ROPE_VEC, ROPE_QKN_SCALAR, ROPE_QKN_VEC = 30, 31, 33, 34
 SW_SCALAR, SW_FLAT, SW_FLAT_NT, SW_ROWS, SW_FLAT_U4_NT = 40, 41, 42, 43, 44
 CH_FUSED, CH_SEQ = 50, 51
 DECODE_BUCKET_MAX = 6       # buckets up to here are decode sized
@@ -60,6 +62,7 @@ MAX_CAPACITY = 4096
 FLAG_AUTO_INSTALL = 1
 
 ALIGN, CONTIG = 1, 2       # per-op guard flag bits
+CHAIN_QK_NORM = 0x40       # chain key flag: the RoPE step has the QK RMSNorm
 
 
 def elem_size(dtype: int) -> int:
@@ -122,12 +125,15 @@ def rn_role(dtype: int, H: int, flags: int, T: int) -> Tuple[int, int]:
     return RN_LOOP, T
 
 
-def rope_role(dtype: int, hd: int, flags: int, T: int) -> Tuple[int, int]:
+def rope_role(dtype: int, hd: int, flags: int, T: int,
+              qk_norm: bool = False) -> Tuple[int, int]:
+    """Vector path when 16-byte aligned and each half-head is a power-of-two
+    number of 16-byte vectors; the QK-norm variants follow the same rule."""
     v = 16 // elem_size(dtype)
     half = hd // 2
     if not (flags & ALIGN) or half % v or not is_pow2(half // v):
-        return ROPE_SCALAR, T
-    return ROPE_VEC, T
+        return (ROPE_QKN_SCALAR if qk_norm else ROPE_SCALAR), T
+    return (ROPE_QKN_VEC if qk_norm else ROPE_VEC), T
 
 
 def sw_role(dtype: int, I: int, flags: int, b: int, T: int,
@@ -160,6 +166,7 @@ class Call:
     nk: int = 0
     eps: float = 1e-6
     base: float = 10000.0
+    qk_eps: float = 1e-6     # chain only: epsilon of the QK RMSNorm
     # addresses (integers) and strides in elements; None = null pointer
     ptr: Dict[str, Optional[int]] = dataclasses.field(default_factory=dict)
     stride: Dict[str, int] = dataclasses.field(default_factory=dict)
@@ -239,6 +246,23 @@ def _validate_rope(c: Call) -> Optional[int]:
     return None
 
 
+def _validate_qkn(c: Call, eps: float) -> Optional[int]:
+    """Head-norm weights: q_w always, k_w when nk > 0; element-aligned."""
+    if c.ptr.get("q_w") is None or (c.nk > 0 and c.ptr.get("k_w") is None):
+        return E_INVALID
+    es = elem_size(c.dtype)
+    if c.ptr["q_w"] % es or (c.nk > 0 and c.ptr["k_w"] % es):
+        return E_INVALID
+    eps = _f32(eps)
+    if not _finite(eps) or eps < 0:
+        return E_INVALID
+    return None
+
+
+def chain_has_qk_norm(c: Call) -> bool:
+    return c.ptr.get("q_w") is not None
+
+
 def _validate_sw(c: Call) -> Optional[int]:
     if c.I < 1:
         return E_INVALID
@@ -271,11 +295,17 @@ def validate(c: Call) -> Optional[int]:
         return _validate_rn(c, RES_PTRS, RES_STRIDES)
     if c.op == OP_ROPE_QK:
         return _validate_rope(c)
+    if c.op == OP_QK_NORM_ROPE:
+        st = _validate_rope(c)
+        return st if st is not None else _validate_qkn(c, c.eps)
     if c.op == OP_SWIGLU:
         return _validate_sw(c)
     if c.op == OP_CHAIN:
-        for f in (lambda: _validate_rn(c, RES_PTRS, RES_STRIDES),
-                  lambda: _validate_rope(c), lambda: _validate_sw(c)):
+        checks = [lambda: _validate_rn(c, RES_PTRS, RES_STRIDES), lambda: _validate_rope(c)]
+        if chain_has_qk_norm(c):
+            checks.append(lambda: _validate_qkn(c, c.qk_eps))
+        checks.append(lambda: _validate_sw(c))
+        for f in checks:
             st = f()
             if st is not None:
                 return st
@@ -294,13 +324,18 @@ def rn_flags(c: Call, names, strides) -> int:
     return f
 
 
-def rope_flags(c: Call) -> int:
+def rope_flags(c: Call, qk_norm: bool = False) -> int:
+    """With the QK norm the head-norm weights join the alignment test."""
     es = elem_size(c.dtype)
     ptrs, strides = [c.ptr["q"]], [c.stride["q"]]
+    if qk_norm:
+        ptrs.append(c.ptr["q_w"])
     contig = c.stride["q"] == c.nq * c.hd
     if c.nk > 0:
         ptrs.append(c.ptr["k"])
         strides.append(c.stride["k"])
+        if qk_norm:
+            ptrs.append(c.ptr["k_w"])
         contig = contig and c.stride["k"] == c.nk * c.hd
     f = ALIGN if _aligned(es, ptrs, strides) else 0
     return f | (CONTIG if contig else 0)
@@ -322,19 +357,22 @@ def op_flags(c: Call) -> int:
         return rn_flags(c, RES_PTRS, RES_STRIDES)
     if c.op == OP_ROPE_QK:
         return rope_flags(c)
+    if c.op == OP_QK_NORM_ROPE:
+        return rope_flags(c, True)
     if c.op == OP_SWIGLU:
         return sw_flags(c)
-    return (rn_flags(c, RES_PTRS, RES_STRIDES) | (rope_flags(c) << 2)
-            | (sw_flags(c) << 4))
+    qkn = chain_has_qk_norm(c)
+    return (rn_flags(c, RES_PTRS, RES_STRIDES) | (rope_flags(c, qkn) << 2)
+            | (sw_flags(c) << 4) | (CHAIN_QK_NORM if qkn else 0))
 
 
 def make_key(c: Call) -> Tuple[int, int, int]:
     b = bucket(c.T)
     flags = op_flags(c)
-    base_bits = f32_bits(c.base) if c.op in (OP_ROPE_QK, OP_CHAIN) else 0
+    base_bits = f32_bits(c.base) if c.op in ROPE_OPS else 0
     H = c.H if c.op in (OP_RMSNORM, OP_RES_RMSNORM, OP_CHAIN) else 0
     I = c.I if c.op in (OP_SWIGLU, OP_CHAIN) else 0
-    hd, nq, nk = (c.hd, c.nq, c.nk) if c.op in (OP_ROPE_QK, OP_CHAIN) else (0, 0, 0)
+    hd, nq, nk = (c.hd, c.nq, c.nk) if c.op in ROPE_OPS else (0, 0, 0)
     k0 = c.op | (c.dtype << 8) | (b << 16) | (flags << 24) | (base_bits << 32)
     k1 = H | (I << 32)
     k2 = hd | (nq << 16) | (nk << 32)
@@ -357,19 +395,19 @@ def plan(key, T: int):
     if op in (OP_RMSNORM, OP_RES_RMSNORM):
         v, g = rn_role(dt, f["H"], fl, T)
         return v, (0, 0, 0), [(v, g, BLOCK)]
-    if op == OP_ROPE_QK:
-        v, g = rope_role(dt, f["hd"], fl, T)
+    if op in (OP_ROPE_QK, OP_QK_NORM_ROPE):
+        v, g = rope_role(dt, f["hd"], fl, T, op == OP_QK_NORM_ROPE)
         return v, (0, 0, 0), [(v, g, BLOCK)]
     if op == OP_SWIGLU:
         v, g = sw_role(dt, f["I"], fl, b, T)
         return v, (0, 0, 0), [(v, g, BLOCK)]
     rn = rn_role(dt, f["H"], fl & 3, T)
-    ro = rope_role(dt, f["hd"], (fl >> 2) & 3, T)
+    ro = rope_role(dt, f["hd"], (fl >> 2) & 3, T, bool(fl & CHAIN_QK_NORM))
     sw = sw_role(dt, f["I"], (fl >> 4) & 3, b, T, in_chain=True)
     roles = (rn[0], ro[0], sw[0])
-    fused = (fl == 0x3F
+    fused = ((fl & 0x3F) == 0x3F
              and (rn[0] in RN_WAVE.values() or rn[0] in RN_BLOCK.values())
-             and ro[0] == ROPE_VEC
+             and ro[0] in (ROPE_VEC, ROPE_QKN_VEC)
              and sw[0] in (SW_FLAT, SW_FLAT_U4_NT))
     if fused:
         return CH_FUSED, roles, [(CH_FUSED, rn[1] + ro[1] + sw[1], BLOCK)]

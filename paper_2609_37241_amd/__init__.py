@@ -147,6 +147,22 @@ class SpecCache:
                    _stream_ptr(stream))
         return q, k
 
+    def qk_norm_rope(self, q, k, pos, q_w, k_w=None, base: float = 10000.0, eps: float = 1e-6,
+                     stream=None):
+        """In-place per-head RMSNorm (weights q_w / k_w [hd]) then RoPE of
+        q [T, nq, hd] and k [T, nk, hd] (k may be None)."""
+        T, nq, hd = q.shape
+        nk = 0 if k is None else k.shape[1]
+        kp = 0 if k is None or nk == 0 else k.data_ptr()
+        kts = 0 if k is None or nk == 0 else _tokens(k, "k")
+        if pos.dtype != torch.int32:
+            raise TypeError("pos must be int32")
+        kw = 0 if k_w is None else k_w.data_ptr()
+        self._call("tri_qk_norm_rope", _dll.tri_qk_norm_rope, dtype_code(q.dtype), q.data_ptr(),
+                   _tokens(q, "q"), kp, kts, pos.data_ptr(), T, nq, nk, hd, base,
+                   q_w.data_ptr(), kw, eps, _stream_ptr(stream))
+        return q, k
+
     def swiglu(self, gate, up, out=None, stream=None) -> torch.Tensor:
         o = torch.empty_like(gate) if out is None else out
         T, I = gate.shape
@@ -156,8 +172,11 @@ class SpecCache:
         return o
 
     def chain_args(self, x, residual, w, q, k, pos, gate, up, eps=1e-6, base=10000.0,
-                   y=None, residual_out=None, out=None) -> Tuple[ChainArgs, tuple]:
-        """Build the tri_chain_args struct once (outputs allocated if absent)."""
+                   y=None, residual_out=None, out=None, q_norm_w=None, k_norm_w=None,
+                   qk_eps=None) -> Tuple[ChainArgs, tuple]:
+        """Build the tri_chain_args struct once (outputs allocated if absent).
+        With q_norm_w (and k_norm_w) the RoPE step is QK-RMSNorm + RoPE with
+        epsilon qk_eps (default: eps)."""
         y = torch.empty_like(x) if y is None else y
         ro = torch.empty_like(residual) if residual_out is None else residual_out
         o = torch.empty_like(gate) if out is None else out
@@ -180,6 +199,10 @@ class SpecCache:
         a.gate, a.g_rs = gate.data_ptr(), _rows(gate, "gate")
         a.up, a.u_rs = up.data_ptr(), _rows(up, "up")
         a.out, a.o_rs = o.data_ptr(), _rows(o, "out")
+        if q_norm_w is not None:
+            a.q_norm_w = q_norm_w.data_ptr()
+            a.k_norm_w = 0 if k_norm_w is None else k_norm_w.data_ptr()
+            a.qk_eps = eps if qk_eps is None else qk_eps
         return a, (y, ro, o)
 
     def decode_chain_args(self, args: ChainArgs, stream=None) -> None:
@@ -187,11 +210,12 @@ class SpecCache:
                    _stream_ptr(stream))
 
     def decode_chain(self, x, residual, w, q, k, pos, gate, up, eps=1e-6, base=10000.0,
-                     y=None, residual_out=None, out=None, stream=None):
-        """Residual+RMSNorm, in-place RoPE of q/k and SwiGLU in one entry call.
-        Returns (y, residual_out, out)."""
+                     y=None, residual_out=None, out=None, stream=None, q_norm_w=None,
+                     k_norm_w=None, qk_eps=None):
+        """Residual+RMSNorm, in-place (QK-RMSNorm +) RoPE of q/k and SwiGLU in
+        one entry call. Returns (y, residual_out, out)."""
         a, outs = self.chain_args(x, residual, w, q, k, pos, gate, up, eps, base, y,
-                                  residual_out, out)
+                                  residual_out, out, q_norm_w, k_norm_w, qk_eps)
         self.decode_chain_args(a, stream)
         return outs
 

@@ -65,10 +65,12 @@ class ChainArgs(C.Structure):
                 ("pos", C.c_void_p),
                 ("gate", C.c_void_p), ("g_rs", C.c_int64),
                 ("up", C.c_void_p), ("u_rs", C.c_int64),
-                ("out", C.c_void_p), ("o_rs", C.c_int64)]
+                ("out", C.c_void_p), ("o_rs", C.c_int64),
+                ("q_norm_w", C.c_void_p), ("k_norm_w", C.c_void_p),
+                ("qk_eps", C.c_float), ("reserved", C.c_int32)]
 
 
-assert C.sizeof(Selection) == 96 and C.sizeof(ChainArgs) == 208
+assert C.sizeof(Selection) == 96 and C.sizeof(ChainArgs) == 232
 
 _P, _I64, _I32, _F, _U32 = C.c_void_p, C.c_int64, C.c_int32, C.c_float, C.c_uint32
 
@@ -80,6 +82,8 @@ SIGNATURES = {
                                        _I64, _I64, _F, _P]),
     "tri_rope_qk": (C.c_int, [_P, C.c_int, _P, _I64, _P, _I64, _P, _I64, _I32, _I32, _I32, _F,
                               _P]),
+    "tri_qk_norm_rope": (C.c_int, [_P, C.c_int, _P, _I64, _P, _I64, _P, _I64, _I32, _I32, _I32,
+                                   _F, _P, _P, _F, _P]),
     "tri_swiglu": (C.c_int, [_P, C.c_int, _P, _I64, _P, _I64, _P, _I64, _I64, _I64, _P]),
     "tri_decode_chain": (C.c_int, [_P, C.POINTER(ChainArgs), _P]),
     "tri_spec_install_last_miss": (C.c_int, [_P, C.POINTER(Selection)]),

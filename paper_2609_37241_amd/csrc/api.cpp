@@ -75,6 +75,15 @@ inline int check_rope(uint64_t es, const void *q, int64_t q_ts, const void *k, i
   return kGo;
 }
 
+// Head-norm weights of QK-RMSNorm: q_w always, k_w when there are K heads;
+// element-aligned; finite non-negative eps.
+inline int check_qkn(uint64_t es, const void *q_w, const void *k_w, int32_t nk, float eps) {
+  if (!q_w || (nk > 0 && !k_w)) return TRI_E_INVALID;
+  if (addr(q_w) % es || (nk > 0 && addr(k_w) % es)) return TRI_E_INVALID;
+  if (!isfinite(eps) || eps < 0.0f) return TRI_E_INVALID;
+  return kGo;
+}
+
 inline int check_sw(uint64_t es, int64_t I, const void *g, int64_t g_rs, const void *u,
                     int64_t u_rs, const void *o, int64_t o_rs) {
   if (I < 1) return TRI_E_INVALID;
@@ -104,12 +113,15 @@ inline unsigned res_flags(uint64_t es, const void *x, int64_t x_rs, const void *
   return flags_of(o, x_rs == H && r_rs == H && y_rs == H && ro_rs == H);
 }
 
+// With QK-RMSNorm (q_w non-null) the head-norm weights join the alignment test.
 inline unsigned rope_flags(uint64_t es, const void *q, int64_t q_ts, const void *k, int64_t k_ts,
-                           int32_t nq, int32_t nk, int32_t hd) {
-  uint64_t o = addr(q) | uint64_t(q_ts) * es;
+                           int32_t nq, int32_t nk, int32_t hd, const void *q_w = nullptr,
+                           const void *k_w = nullptr) {
+  uint64_t o = addr(q) | uint64_t(q_ts) * es | addr(q_w);
   bool contig = q_ts == int64_t(nq) * hd;
   if (nk > 0) {
     o |= addr(k) | uint64_t(k_ts) * es;
+    if (q_w) o |= addr(k_w);
     contig = contig && k_ts == int64_t(nk) * hd;
   }
   return flags_of(o, contig);
@@ -232,7 +244,7 @@ tri_status tri_rmsnorm(tri_cache *c, tri_dtype dtype, const void *x, int64_t x_r
 
   RnArgs a{x, nullptr, w, y, nullptr, x_rs, 0, y_rs, 0, T, int32_t(H), eps};
   const tri_launch_rec l{v.plan.kvariant[0], role_grid(v.plan.kvariant[0], dtype, T, 0), kBlock};
-  const int rc = be_launch(v.fn[0], l.grid_x, kBlock, &a, stream);
+  const int rc = be_launch(v.fn[0], l.grid_x, kBlock, &a, sizeof a, stream);
   record(c, op, v, vi, k, 1, &l, rc ? TRI_E_LAUNCH : TRI_OK);
   return finish(c, v, auto_inst, rc);
 }
@@ -263,7 +275,7 @@ tri_status tri_residual_rmsnorm(tri_cache *c, tri_dtype dtype, const void *x, in
 
   RnArgs a{x, res, w, y, res_out, x_rs, res_rs, y_rs, ro_rs, T, int32_t(H), eps};
   const tri_launch_rec l{v.plan.kvariant[0], role_grid(v.plan.kvariant[0], dtype, T, 0), kBlock};
-  const int rc = be_launch(v.fn[0], l.grid_x, kBlock, &a, stream);
+  const int rc = be_launch(v.fn[0], l.grid_x, kBlock, &a, sizeof a, stream);
   record(c, op, v, vi, k, 1, &l, rc ? TRI_E_LAUNCH : TRI_OK);
   return finish(c, v, auto_inst, rc);
 }
@@ -288,9 +300,41 @@ tri_status tri_rope_qk(tri_cache *c, tri_dtype dtype, void *q, int64_t q_ts, voi
   if (st != TRI_OK) return tri_status(st);
   Version &v = c->versions[vi];
 
-  RopeArgs a{q, nk > 0 ? kp : nullptr, pos, v.d_consts, q_ts, k_ts, T, nq, nk, hd, 0};
+  RopeArgs a{q, nk > 0 ? kp : nullptr, pos, v.d_consts, nullptr, nullptr, q_ts, k_ts, T,
+             nq, nk, hd, 0.0f};
   const tri_launch_rec l{v.plan.kvariant[0], role_grid(v.plan.kvariant[0], dtype, T, 0), kBlock};
-  const int rc = be_launch(v.fn[0], l.grid_x, kBlock, &a, stream);
+  const int rc = be_launch(v.fn[0], l.grid_x, kBlock, &a, sizeof a, stream);
+  record(c, op, v, vi, k, 1, &l, rc ? TRI_E_LAUNCH : TRI_OK);
+  return finish(c, v, auto_inst, rc);
+}
+
+tri_status tri_qk_norm_rope(tri_cache *c, tri_dtype dtype, void *q, int64_t q_ts, void *kp,
+                            int64_t k_ts, const int32_t *pos, int64_t T, int32_t nq, int32_t nk,
+                            int32_t hd, float base, const void *q_w, const void *k_w, float eps,
+                            void *stream) {
+  if (!c) return TRI_E_INVALID;
+  const uint32_t op = TRI_OP_QK_NORM_ROPE;
+  c->stats.calls++;
+  int st = check_common(dtype, T);
+  if (st != kGo) return finish_early(c, op, st);
+  const uint64_t es = es_of(dtype);
+  st = check_rope(es, q, q_ts, kp, k_ts, pos, nq, nk, hd, base);
+  if (st != kGo) return finish_early(c, op, st);
+  st = check_qkn(es, q_w, k_w, nk, eps);
+  if (st != kGo) return finish_early(c, op, st);
+
+  const Key k = make_key(op, dtype, T, rope_flags(es, q, q_ts, kp, k_ts, nq, nk, hd, q_w, k_w),
+                         f32_bits(base), 0, 0, uint64_t(hd), uint64_t(nq), uint64_t(nk));
+  int32_t vi;
+  bool auto_inst = false;
+  st = lookup(c, op, k, T, &vi, &auto_inst);
+  if (st != TRI_OK) return tri_status(st);
+  Version &v = c->versions[vi];
+
+  RopeArgs a{q, nk > 0 ? kp : nullptr, pos, v.d_consts, q_w, nk > 0 ? k_w : nullptr, q_ts, k_ts,
+             T, nq, nk, hd, eps};
+  const tri_launch_rec l{v.plan.kvariant[0], role_grid(v.plan.kvariant[0], dtype, T, 0), kBlock};
+  const int rc = be_launch(v.fn[0], l.grid_x, kBlock, &a, sizeof a, stream);
   record(c, op, v, vi, k, 1, &l, rc ? TRI_E_LAUNCH : TRI_OK);
   return finish(c, v, auto_inst, rc);
 }
@@ -317,7 +361,7 @@ tri_status tri_swiglu(tri_cache *c, tri_dtype dtype, const void *gate, int64_t g
 
   SwArgs a{gate, up, out, g_rs, u_rs, o_rs, T, I, (T * I) / vec_elems(dtype), T * I};
   const tri_launch_rec l{v.plan.kvariant[0], role_grid(v.plan.kvariant[0], dtype, T, I), kBlock};
-  const int rc = be_launch(v.fn[0], l.grid_x, kBlock, &a, stream);
+  const int rc = be_launch(v.fn[0], l.grid_x, kBlock, &a, sizeof a, stream);
   record(c, op, v, vi, k, 1, &l, rc ? TRI_E_LAUNCH : TRI_OK);
   return finish(c, v, auto_inst, rc);
 }
@@ -340,14 +384,21 @@ tri_status tri_decode_chain(tri_cache *c, const tri_chain_args *p, void *stream)
   }
   st = check_rope(es, p->q, p->q_ts, p->k, p->k_ts, p->pos, p->nq, p->nk, p->hd, p->base);
   if (st != kGo) return finish_early(c, op, st);
+  const bool qkn = p->q_norm_w != nullptr;
+  if (qkn) {
+    st = check_qkn(es, p->q_norm_w, p->k_norm_w, p->nk, p->qk_eps);
+    if (st != kGo) return finish_early(c, op, st);
+  }
   st = check_sw(es, I, p->gate, p->g_rs, p->up, p->u_rs, p->out, p->o_rs);
   if (st != kGo) return finish_early(c, op, st);
 
   const unsigned fl =
       res_flags(es, p->x, p->x_rs, p->res, p->res_rs, p->w, p->y, p->y_rs, p->res_out, p->ro_rs,
                 H) |
-      (rope_flags(es, p->q, p->q_ts, p->k, p->k_ts, p->nq, p->nk, p->hd) << 2) |
-      (sw_flags(es, p->gate, p->g_rs, p->up, p->u_rs, p->out, p->o_rs, I) << 4);
+      (rope_flags(es, p->q, p->q_ts, p->k, p->k_ts, p->nq, p->nk, p->hd,
+                  qkn ? p->q_norm_w : nullptr, qkn ? p->k_norm_w : nullptr) << 2) |
+      (sw_flags(es, p->gate, p->g_rs, p->up, p->u_rs, p->out, p->o_rs, I) << 4) |
+      (qkn ? kChainQkNorm : 0u);
   const Key k = make_key(op, uint32_t(dtype), T, fl, f32_bits(p->base), uint64_t(H), uint64_t(I),
                          uint64_t(p->hd), uint64_t(p->nq), uint64_t(p->nk));
   int32_t vi;
@@ -358,8 +409,9 @@ tri_status tri_decode_chain(tri_cache *c, const tri_chain_args *p, void *stream)
 
   const RnArgs rn{p->x, p->res, p->w, p->y, p->res_out, p->x_rs, p->res_rs, p->y_rs, p->ro_rs,
                   T, int32_t(H), p->eps};
-  const RopeArgs ro{p->q, p->nk > 0 ? p->k : nullptr, p->pos, v.d_consts, p->q_ts, p->k_ts, T,
-                    p->nq, p->nk, p->hd, 0};
+  const RopeArgs ro{p->q, p->nk > 0 ? p->k : nullptr, p->pos, v.d_consts,
+                    qkn ? p->q_norm_w : nullptr, qkn && p->nk > 0 ? p->k_norm_w : nullptr,
+                    p->q_ts, p->k_ts, T, p->nq, p->nk, p->hd, qkn ? p->qk_eps : 0.0f};
   const SwArgs sw{p->gate, p->up, p->out, p->g_rs, p->u_rs, p->o_rs, T, I,
                   (T * I) / vec_elems(uint32_t(dtype)), T * I};
   const uint32_t g0 = role_grid(v.plan.roles[0], uint32_t(dtype), T, I);
@@ -369,7 +421,7 @@ tri_status tri_decode_chain(tri_cache *c, const tri_chain_args *p, void *stream)
   if (v.plan.variant == CH_FUSED) {
     ChainArgs a{rn, ro, sw, g0, g1};
     const tri_launch_rec l{CH_FUSED, g0 + g1 + g2, kBlock};
-    const int rc = be_launch(v.fn[0], l.grid_x, kBlock, &a, stream);
+    const int rc = be_launch(v.fn[0], l.grid_x, kBlock, &a, sizeof a, stream);
     record(c, op, v, vi, k, 1, &l, rc ? TRI_E_LAUNCH : TRI_OK);
     return finish(c, v, auto_inst, rc);
   }
@@ -377,12 +429,13 @@ tri_status tri_decode_chain(tri_cache *c, const tri_chain_args *p, void *stream)
   RnArgs a0 = rn;
   RopeArgs a1 = ro;
   SwArgs a2 = sw;
-  void *args[3] = {&a0, &a1, &a2};
+  const void *args[3] = {&a0, &a1, &a2};
+  const uint32_t sizes[3] = {sizeof a0, sizeof a1, sizeof a2};
   const tri_launch_rec l[3] = {{v.plan.kvariant[0], g0, kBlock},
                                {v.plan.kvariant[1], g1, kBlock},
                                {v.plan.kvariant[2], g2, kBlock}};
   int rc = 0;
-  for (int i = 0; i < 3 && rc == 0; ++i) rc = be_launch(v.fn[i], l[i].grid_x, kBlock, args[i], stream);
+  for (int i = 0; i < 3 && rc == 0; ++i) rc = be_launch(v.fn[i], l[i].grid_x, kBlock, args[i], sizes[i], stream);
   record(c, op, v, vi, k, 3, l, rc ? TRI_E_LAUNCH : TRI_OK);
   return finish(c, v, auto_inst, rc);
 }

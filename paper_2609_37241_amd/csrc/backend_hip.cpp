@@ -29,7 +29,7 @@ int be_resolve(int32_t kvariant, uint32_t dtype, int32_t ksub, void **fn) {
   const void *sym = nullptr;
   if (kvariant >= RN_SCALAR && kvariant <= RN_LOOP)
     sym = rn_kernel(kvariant, dtype, ksub);
-  else if (kvariant >= ROPE_SCALAR && kvariant <= ROPE_VEC)
+  else if (kvariant >= ROPE_SCALAR && kvariant <= ROPE_QKN_VEC)
     sym = rope_kernel(kvariant, dtype);
   else if (kvariant >= SW_SCALAR && kvariant <= SW_FLAT_U4_NT)
     sym = sw_kernel(kvariant, dtype);
@@ -44,8 +44,12 @@ int be_resolve(int32_t kvariant, uint32_t dtype, int32_t ksub, void **fn) {
   return 0;
 }
 
-int be_launch(void *fn, uint32_t grid, uint32_t block, void *args, void *stream) {
-  void *params[1] = {args};
+int be_launch(void *fn, uint32_t grid, uint32_t block, const void *args, uint32_t,
+              void *stream) {
+  // The kernels take one by-value struct: the single parameter pointer
+  // points at it (the runtime copies args_size bytes from the kernel's
+  // parameter metadata).
+  void *params[1] = {const_cast<void *>(args)};
   const hipError_t e =
       hipModuleLaunchKernel(reinterpret_cast<hipFunction_t>(fn), grid, 1, 1, block, 1, 1, 0,
                             reinterpret_cast<hipStream_t>(stream), args ? params : nullptr, nullptr);

@@ -56,7 +56,7 @@ tri_status install_key(tri_cache *c, const Key &k) {
     if (st != 0) return tri_status(st);
   }
   const uint32_t op = key_op(k);
-  if (op == TRI_OP_ROPE_QK || op == TRI_OP_CHAIN) {
+  if (op == TRI_OP_ROPE_QK || op == TRI_OP_QK_NORM_ROPE || op == TRI_OP_CHAIN) {
     const uint32_t hd = key_hd(k);
     float base;
     const uint32_t bits = key_base_bits(k);
@@ -201,7 +201,7 @@ tri_status tri_spec_version_constants(const tri_cache *c, uint32_t index, float 
 
 tri_status tri_launch_empty(tri_cache *c, void *stream) {
   if (!c) return TRI_E_INVALID;
-  return be_launch(c->empty_fn, 1, 64, nullptr, stream) == 0 ? TRI_OK : TRI_E_LAUNCH;
+  return be_launch(c->empty_fn, 1, 64, nullptr, 0, stream) == 0 ? TRI_OK : TRI_E_LAUNCH;
 }
 
 const char *tri_status_str(int status) {

@@ -15,7 +15,7 @@ enum Variant : int32_t {
   RN_WAVE_1 = 11, RN_WAVE_2 = 12,
   RN_BLOCK_1 = 13, RN_BLOCK_2 = 14, RN_BLOCK_4 = 15, RN_BLOCK_8 = 16, RN_BLOCK_16 = 17,
   RN_LOOP = 18,
-  ROPE_SCALAR = 30, ROPE_VEC = 31,
+  ROPE_SCALAR = 30, ROPE_VEC = 31, ROPE_QKN_SCALAR = 33, ROPE_QKN_VEC = 34,
   SW_SCALAR = 40, SW_FLAT = 41, SW_FLAT_NT = 42, SW_ROWS = 43, SW_FLAT_U4_NT = 44,
   CH_FUSED = 50, CH_SEQ = 51,
   EMPTY = 99,
@@ -35,6 +35,7 @@ constexpr int32_t kHeadsMax = 4096;
 constexpr uint32_t kDefaultCapacity = 256;
 constexpr uint32_t kMaxCapacity = 4096;
 constexpr unsigned kAlign = 1, kContig = 2;   // per-role guard flag bits
+constexpr unsigned kChainQkNorm = 0x40;        // chain key flag: QK-RMSNorm before RoPE
 
 // ---- key --------------------------------------------------------------------------
 struct Key {
@@ -67,7 +68,7 @@ struct Role {
   uint32_t grid;
 };
 Role rn_role(uint32_t dtype, int64_t H, unsigned flags, int64_t T);
-Role rope_role(uint32_t dtype, int32_t hd, unsigned flags, int64_t T);
+Role rope_role(uint32_t dtype, int32_t hd, unsigned flags, int64_t T, bool qk_norm);
 Role sw_role(uint32_t dtype, int64_t I, unsigned flags, uint32_t bucket, int64_t T, bool in_chain);
 uint32_t role_grid(int32_t variant, uint32_t dtype, int64_t T, int64_t I);
 
@@ -78,7 +79,8 @@ struct Plan {
   int32_t n_launches;
   int32_t kvariant[3];    // kernel variant per launch
   int32_t ksub[3];        // kernel sub-selector (residual flag / fused template index)
-                          // fused: (role norm variant - RN_WAVE_1) * 2
+                          // fused: (role norm variant - RN_WAVE_1) * 4
+                          //        + (QK-RMSNorm before RoPE) * 2
                           //        + (SwiGLU role is SW_FLAT_U4_NT)
 };
 Plan plan_for_key(const Key &k);
@@ -88,7 +90,9 @@ Plan plan_for_key(const Key &k);
 // and launches with hipModuleLaunchKernel; the CPU test build records calls.
 int be_init(int *device);                                         // 0 or tri_status
 int be_resolve(int32_t kvariant, uint32_t dtype, int32_t ksub, void **fn);
-int be_launch(void *fn, uint32_t grid, uint32_t block, void *args, void *stream);
+// `args` is the kernel's single argument struct of `args_size` bytes (or null).
+int be_launch(void *fn, uint32_t grid, uint32_t block, const void *args, uint32_t args_size,
+              void *stream);
 int be_upload(const void *host, uint64_t bytes, void **dev);      // per-version constants
 void be_free(void *dev);
 
@@ -103,7 +107,7 @@ struct Version {
   uint64_t hits;
 };
 
-constexpr int kOps = 6;   // op ids 1..5
+constexpr int kOps = 7;   // op ids 1..6
 
 }  // namespace tri
 

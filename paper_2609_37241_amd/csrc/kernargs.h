@@ -22,16 +22,19 @@ struct RnArgs {
   float eps;
 };
 
-// RoPE on Q [T, nq, hd] and K [T, nk, hd], in place.
+// RoPE on Q [T, nq, hd] and K [T, nk, hd], in place; with QK-RMSNorm the
+// heads are normalised first (qw, kw: [hd] head-norm weights).
 struct RopeArgs {
   void *q;
   void *k;
   const int32_t *pos;
   const float *inv_freq;  // [hd/2], the version's table
+  const void *qw;
+  const void *kw;
   int64_t q_ts, k_ts;
   int64_t T;
   int32_t nq, nk, hd;
-  int32_t pad_;
+  float eps;
 };
 
 // SwiGLU over [T, I].
@@ -58,9 +61,9 @@ struct ChainArgs {
 
 static_assert(sizeof(RnArgs) == 88 && offsetof(RnArgs, T) == 72 && offsetof(RnArgs, eps) == 84,
               "RnArgs layout");
-static_assert(sizeof(RopeArgs) == 72 && offsetof(RopeArgs, nq) == 56, "RopeArgs layout");
+static_assert(sizeof(RopeArgs) == 88 && offsetof(RopeArgs, nq) == 72, "RopeArgs layout");
 static_assert(sizeof(SwArgs) == 80 && offsetof(SwArgs, n) == 72, "SwArgs layout");
-static_assert(sizeof(ChainArgs) == 248 && offsetof(ChainArgs, rn_blocks) == 240,
+static_assert(sizeof(ChainArgs) == 264 && offsetof(ChainArgs, rn_blocks) == 256,
               "ChainArgs layout");
 
 }  // namespace tri

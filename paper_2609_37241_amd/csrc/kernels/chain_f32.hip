@@ -8,9 +8,9 @@ namespace tri {
 using namespace dev;
 
 // RNV: RN_WAVE_1/2 (one wavefront per row) or RN_BLOCK_1..16 (one
-// workgroup per row); the RoPE role takes one token per workgroup; SWV:
-// SW_FLAT (one vector per work-item, cached) or SW_FLAT_U4_NT (four,
-// streaming).
+// workgroup per row); the RoPE role takes one token per workgroup, with the
+// per-head QK RMSNorm first when QKN; SWV: SW_FLAT (one vector per
+// work-item, cached) or SW_FLAT_U4_NT (four, streaming).
 template <int DT, int RNV>
 __device__ __forceinline__ void chain_norm_role(const ChainArgs &a, uint32_t blk) {
   if constexpr (RNV <= RN_WAVE_2) {
@@ -27,7 +27,7 @@ __device__ __forceinline__ void chain_norm_role(const ChainArgs &a, uint32_t blk
 // path (2.75 vs 3.1 µs device time at 1 token). Streaming sizes
 // (SW_FLAT_U4_NT): SwiGLU first, then norm, then RoPE (about 1 % faster at
 // 8192 tokens than norm first).
-template <int DT, int RNV, int SWV>
+template <int DT, int RNV, int SWV, bool QKN>
 __global__ __launch_bounds__(256) void k_chain(ChainArgs a) {
   __shared__ float lds[2 * 256];
   const uint32_t b = blockIdx.x;
@@ -38,13 +38,13 @@ __global__ __launch_bounds__(256) void k_chain(ChainArgs a) {
     } else if (b < S + R) {
       chain_norm_role<DT, RNV>(a, b - S);
     } else {
-      rope_vec_block<DT, 1, false>(a.rope, b - S - R, lds);
+      rope_vec_block<DT, 1, false, 4, QKN>(a.rope, b - S - R, lds);
     }
   } else {
     if (b < R) {
       chain_norm_role<DT, RNV>(a, b);
     } else if (b < R + P) {
-      rope_vec_block<DT, 1, false>(a.rope, b - R, lds);
+      rope_vec_block<DT, 1, false, 4, QKN>(a.rope, b - R, lds);
     } else {
       sw_flat_part<DT, 1, false>(a.sw, b - R - P, S);
     }
@@ -53,23 +53,27 @@ __global__ __launch_bounds__(256) void k_chain(ChainArgs a) {
 
 namespace {
 template <int RNV>
-const void *chain_pick_rn(bool u4) {
-  return u4 ? reinterpret_cast<const void *>(&k_chain<kF32, RNV, SW_FLAT_U4_NT>)
-            : reinterpret_cast<const void *>(&k_chain<kF32, RNV, SW_FLAT>);
+const void *chain_pick_rn(bool qkn, bool u4) {
+  if (qkn)
+    return u4 ? reinterpret_cast<const void *>(&k_chain<kF32, RNV, SW_FLAT_U4_NT, true>)
+              : reinterpret_cast<const void *>(&k_chain<kF32, RNV, SW_FLAT, true>);
+  return u4 ? reinterpret_cast<const void *>(&k_chain<kF32, RNV, SW_FLAT_U4_NT, false>)
+            : reinterpret_cast<const void *>(&k_chain<kF32, RNV, SW_FLAT, false>);
 }
 }  // namespace
 
-// sub = (norm role - RN_WAVE_1) * 2 + (SwiGLU role streams four vectors per work-item).
+// sub = (norm role - RN_WAVE_1) * 4 + 2 * (RoPE role has the QK norm)
+//       + (SwiGLU role streams four vectors per work-item).
 const void *chain_kernel_f32(int32_t sub) {
-  const bool u4 = sub & 1;
-  switch (RN_WAVE_1 + (sub >> 1)) {
-    case RN_WAVE_1: return chain_pick_rn<RN_WAVE_1>(u4);
-    case RN_WAVE_2: return chain_pick_rn<RN_WAVE_2>(u4);
-    case RN_BLOCK_1: return chain_pick_rn<RN_BLOCK_1>(u4);
-    case RN_BLOCK_2: return chain_pick_rn<RN_BLOCK_2>(u4);
-    case RN_BLOCK_4: return chain_pick_rn<RN_BLOCK_4>(u4);
-    case RN_BLOCK_8: return chain_pick_rn<RN_BLOCK_8>(u4);
-    case RN_BLOCK_16: return chain_pick_rn<RN_BLOCK_16>(u4);
+  const bool u4 = sub & 1, qkn = sub & 2;
+  switch (RN_WAVE_1 + (sub >> 2)) {
+    case RN_WAVE_1: return chain_pick_rn<RN_WAVE_1>(qkn, u4);
+    case RN_WAVE_2: return chain_pick_rn<RN_WAVE_2>(qkn, u4);
+    case RN_BLOCK_1: return chain_pick_rn<RN_BLOCK_1>(qkn, u4);
+    case RN_BLOCK_2: return chain_pick_rn<RN_BLOCK_2>(qkn, u4);
+    case RN_BLOCK_4: return chain_pick_rn<RN_BLOCK_4>(qkn, u4);
+    case RN_BLOCK_8: return chain_pick_rn<RN_BLOCK_8>(qkn, u4);
+    case RN_BLOCK_16: return chain_pick_rn<RN_BLOCK_16>(qkn, u4);
     default: return nullptr;
   }
 }

@@ -133,6 +133,19 @@ __device__ inline double wave_sum(double v) {
   return v;
 }
 
+// Sum over aligned groups of n consecutive lanes (n a power of two, at most
+// 64, the same for the whole wavefront); every lane of a group returns the
+// same, bitwise equal sum. Lanes of one group must be active together.
+__device__ inline float group_sum(float v, int n) {
+  if (n >= 2) v += dpp_mov<0xB1>(v);    // lane ^ 1
+  if (n >= 4) v += dpp_mov<0x4E>(v);    // lane ^ 2
+  if (n >= 8) v += dpp_mov<0x141>(v);   // the other quad of the half row
+  if (n >= 16) v += dpp_mov<0x140>(v);  // the other half row
+  if (n >= 32) v += __shfl_xor(v, 16, 64);
+  if (n >= 64) v += __shfl_xor(v, 32, 64);
+  return v;
+}
+
 // Sum over the 256 work-items of a workgroup; `red` is 4 words of LDS.
 template <typename T>
 __device__ inline T block_sum(T v, T *red) {
@@ -346,7 +359,15 @@ __device__ __forceinline__ char *rope_head(const RopeArgs &a, int64_t t, int h, 
 // (token, head) items are processed PF at a time with all loads issued before
 // any use, and the first batch is requested before the angle math and the
 // barrier, so at decode sizes the block costs one memory round trip.
-template <int DT, int TPB, bool NT, int PF = 4>
+//
+// QKN: each head is first RMS-normalised over its hd elements with the Q or
+// K head-norm weight. The cpb work-items of a head hold the whole head in
+// registers (chunk c of both halves), so the sum of squares is a reduction
+// over cpb adjacent lanes and the head is read and written once. Every item
+// of a batch is then computed (clamped items on valid data) so that all
+// lanes of a group take part in the reduction; only stores are guarded.
+// cpb <= 64 since hd <= 512.
+template <int DT, int TPB, bool NT, int PF = 4, bool QKN = false>
 __device__ __forceinline__ void rope_vec_block(const RopeArgs &a, int64_t blk, float *lds) {
   using E = Elt<DT>;
   constexpr int V = E::V;
@@ -363,6 +384,17 @@ __device__ __forceinline__ void rope_vec_block(const RopeArgs &a, int64_t blk, f
   float *cs = lds;
   float *sn = lds + TPB * 256;
   const int na = TPB * half;
+
+  // Head-norm weight chunks of this work-item (both halves, Q and K).
+  u32x4 wq1, wq2, wk1, wk2;
+  if constexpr (QKN) {
+    const char *qw = static_cast<const char *>(a.qw);
+    const char *kw = a.kw ? static_cast<const char *>(a.kw) : qw;
+    wq1 = reinterpret_cast<const u32x4 *>(qw)[chunk];
+    wq2 = reinterpret_cast<const u32x4 *>(qw + half * E::ES)[chunk];
+    wk1 = reinterpret_cast<const u32x4 *>(kw)[chunk];
+    wk2 = reinterpret_cast<const u32x4 *>(kw + half * E::ES)[chunk];
+  }
 
   // Operands of this work-item's angle slot (token t0 + tid / half, pair
   // tid % half); indices are clamped so the loads are always in bounds.
@@ -418,17 +450,38 @@ __device__ __forceinline__ void rope_vec_block(const RopeArgs &a, int64_t blk, f
   for (;;) {
 #pragma unroll
     for (int j = 0; j < PF; ++j) {
-      if (!ok[j]) continue;
+      if constexpr (!QKN) {
+        if (!ok[j]) continue;
+      }
       const int base = it[j] * half + chunk * V;
       float f1[V], f2[V], o1[V], o2[V];
       E::unpack(x1[j], f1);
       E::unpack(x2[j], f2);
+      if constexpr (QKN) {
+        float ss = 0.0f;
+#pragma unroll
+        for (int e = 0; e < V; ++e) ss += f1[e] * f1[e];
+#pragma unroll
+        for (int e = 0; e < V; ++e) ss += f2[e] * f2[e];
+        ss = group_sum(ss, cpb);
+        const float inv = rsqrtf(ss / float(a.hd) + a.eps);
+        const bool isq = ih[j] < a.nq;
+        float w1[V], w2[V];
+        E::unpack(isq ? wq1 : wk1, w1);
+        E::unpack(isq ? wq2 : wk2, w2);
+#pragma unroll
+        for (int e = 0; e < V; ++e) {
+          f1[e] = (f1[e] * inv) * w1[e];
+          f2[e] = (f2[e] * inv) * w2[e];
+        }
+      }
 #pragma unroll
       for (int e = 0; e < V; ++e) {
         const float c = cs[base + e], s = sn[base + e];
         o1[e] = f1[e] * c - f2[e] * s;
         o2[e] = f2[e] * c + f1[e] * s;
       }
+      if (QKN && !ok[j]) continue;
       char *b = rope_head(a, t0 + it[j], ih[j], E::ES);
       st16<NT>(reinterpret_cast<u32x4 *>(b) + chunk, E::pack(o1));
       st16<NT>(reinterpret_cast<u32x4 *>(b + half * E::ES) + chunk, E::pack(o2));
@@ -438,8 +491,13 @@ __device__ __forceinline__ void rope_vec_block(const RopeArgs &a, int64_t blk, f
   }
 }
 
-// Any alignment / head size: one token per workgroup, element pairs.
-template <int DT>
+// Any alignment / head size: one token per workgroup, element pairs. `lds`
+// holds 2 * 256 floats (cos, sin), and 256 more for QKN.
+//
+// QKN: heads are taken 256 at a time; wavefront w reduces the squares of
+// heads w, w + 4, ... of the slice (element-wise loads, any alignment) and
+// leaves 1/rms in LDS, then all work-items normalise and rotate the slice.
+template <int DT, bool QKN = false>
 __device__ __forceinline__ void rope_scalar_block(const RopeArgs &a, int64_t t, float *lds) {
   using E = Elt<DT>;
   const int half = a.hd >> 1;
@@ -448,14 +506,48 @@ __device__ __forceinline__ void rope_scalar_block(const RopeArgs &a, int64_t t, 
   rope_angles(a, t, 0, half, cs, sn);
   __syncthreads();
   const int nh = a.nq + a.nk;
-  const int total = nh * half;
-  for (int e = threadIdx.x; e < total; e += kThreads) {
-    const int h = e / half;
-    const int i = e - h * half;
-    char *base = rope_head(a, t, h, E::ES);
-    const float v1 = E::ld(base, i), v2 = E::ld(base, i + half);
-    E::st(base, i, v1 * cs[i] - v2 * sn[i]);
-    E::st(base, i + half, v2 * cs[i] + v1 * sn[i]);
+  if constexpr (!QKN) {
+    const int total = nh * half;
+    for (int e = threadIdx.x; e < total; e += kThreads) {
+      const int h = e / half;
+      const int i = e - h * half;
+      char *base = rope_head(a, t, h, E::ES);
+      const float v1 = E::ld(base, i), v2 = E::ld(base, i + half);
+      E::st(base, i, v1 * cs[i] - v2 * sn[i]);
+      E::st(base, i + half, v2 * cs[i] + v1 * sn[i]);
+    }
+  } else {
+    float *rinv = lds + 512;
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+    const void *kw = a.kw ? a.kw : a.qw;
+    for (int h0 = 0; h0 < nh; h0 += kThreads) {
+      const int hn = nh - h0 < kThreads ? nh - h0 : kThreads;
+      for (int hl = wid; hl < hn; hl += kThreads / 64) {
+        const char *base = rope_head(a, t, h0 + hl, E::ES);
+        float ss = 0.0f;
+        for (int i = lane; i < a.hd; i += 64) {
+          const float v = E::ld(base, i);
+          ss += v * v;
+        }
+        ss = wave_sum(ss);
+        if (lane == 0) rinv[hl] = rsqrtf(ss / float(a.hd) + a.eps);
+      }
+      __syncthreads();
+      const int total = hn * half;
+      for (int e = threadIdx.x; e < total; e += kThreads) {
+        const int hl = e / half;
+        const int i = e - hl * half;
+        const int h = h0 + hl;
+        const void *w = h < a.nq ? a.qw : kw;
+        char *base = rope_head(a, t, h, E::ES);
+        const float r = rinv[hl];
+        const float n1 = (E::ld(base, i) * r) * E::ld(w, i);
+        const float n2 = (E::ld(base, i + half) * r) * E::ld(w, i + half);
+        E::st(base, i, n1 * cs[i] - n2 * sn[i]);
+        E::st(base, i + half, n2 * cs[i] + n1 * sn[i]);
+      }
+      __syncthreads();
+    }
   }
 }
 

@@ -1,28 +1,32 @@
-// RoPE-on-Q-and-K kernels (in place), one per install-policy variant and dtype.
+// RoPE-on-Q-and-K kernels (in place), with and without the per-head QK
+// RMSNorm, one per install-policy variant and dtype.
 #include "../internal.h"
 #include "device.h"
 
 namespace tri {
 using namespace dev;
 
-template <int DT>
+// QKN: per-head RMSNorm of Q and K before the rotation.
+template <int DT, bool QKN>
 __global__ __launch_bounds__(256) void k_rope_vec(RopeArgs a) {
   __shared__ float lds[2 * 256];
-  rope_vec_block<DT, 1, false>(a, blockIdx.x, lds);
+  rope_vec_block<DT, 1, false, 4, QKN>(a, blockIdx.x, lds);
 }
 
-template <int DT>
+template <int DT, bool QKN>
 __global__ __launch_bounds__(256) void k_rope_scalar(RopeArgs a) {
-  __shared__ float lds[2 * 256];
-  rope_scalar_block<DT>(a, blockIdx.x, lds);
+  __shared__ float lds[(QKN ? 3 : 2) * 256];
+  rope_scalar_block<DT, QKN>(a, blockIdx.x, lds);
 }
 
 namespace {
 template <int DT>
 const void *rope_pick(int32_t variant) {
   switch (variant) {
-    case ROPE_SCALAR: return reinterpret_cast<const void *>(&k_rope_scalar<DT>);
-    case ROPE_VEC: return reinterpret_cast<const void *>(&k_rope_vec<DT>);
+    case ROPE_SCALAR: return reinterpret_cast<const void *>(&k_rope_scalar<DT, false>);
+    case ROPE_VEC: return reinterpret_cast<const void *>(&k_rope_vec<DT, false>);
+    case ROPE_QKN_SCALAR: return reinterpret_cast<const void *>(&k_rope_scalar<DT, true>);
+    case ROPE_QKN_VEC: return reinterpret_cast<const void *>(&k_rope_vec<DT, true>);
     default: return nullptr;
   }
 }

@@ -56,13 +56,15 @@ Role rn_role(uint32_t dtype, int64_t H, unsigned flags, int64_t T) {
 // vectors, so a thread keeps one chunk of angles for every head it visits.
 // One token per workgroup at every size (it also streamed best at 8192
 // tokens: more workgroups, one angle table each).
-Role rope_role(uint32_t dtype, int32_t hd, unsigned flags, int64_t T) {
+// With QK-RMSNorm the same two layouts apply; the norm's per-head reduction
+// runs over the lanes (vector form) or wavefronts (scalar form) of a head.
+Role rope_role(uint32_t dtype, int32_t hd, unsigned flags, int64_t T, bool qk_norm) {
   const int64_t v = vec_elems(dtype);
   const int64_t half = hd / 2;
   const int64_t cpb = half / v;
   if (!(flags & kAlign) || half % v || (cpb & (cpb - 1)) != 0)
-    return {ROPE_SCALAR, uint32_t(T)};
-  return {ROPE_VEC, uint32_t(T)};
+    return {qk_norm ? ROPE_QKN_SCALAR : ROPE_SCALAR, uint32_t(T)};
+  return {qk_norm ? ROPE_QKN_VEC : ROPE_VEC, uint32_t(T)};
 }
 
 // Flat SwiGLU streams nontemporally beyond decode sizes: one vector per
@@ -91,7 +93,8 @@ uint32_t role_grid(int32_t variant, uint32_t dtype, int64_t T, int64_t I) {
   if (variant == RN_WAVE_1 || variant == RN_WAVE_2) return uint32_t(cdiv(T, 4));
   switch (variant) {
     case RN_SCALAR: case RN_BLOCK_1: case RN_BLOCK_2: case RN_BLOCK_4: case RN_BLOCK_8:
-    case RN_BLOCK_16: case RN_LOOP: case ROPE_SCALAR: case ROPE_VEC:
+    case RN_BLOCK_16: case RN_LOOP: case ROPE_SCALAR: case ROPE_VEC: case ROPE_QKN_SCALAR:
+    case ROPE_QKN_VEC:
       return uint32_t(T);
     case SW_FLAT: case SW_FLAT_NT:
       return clamp_grid(cdiv((T * I) / vec_elems(dtype), kBlock));
@@ -113,8 +116,8 @@ uint32_t role_grid(int32_t variant, uint32_t dtype, int64_t T, int64_t I) {
 namespace {
 
 // Template index of the fused chain kernel (see Plan::ksub).
-int32_t fused_sub(int32_t rn, int32_t sw) {
-  return (rn - RN_WAVE_1) * 2 + (sw == SW_FLAT_U4_NT ? 1 : 0);
+int32_t fused_sub(int32_t rn, int32_t rope, int32_t sw) {
+  return (rn - RN_WAVE_1) * 4 + (rope == ROPE_QKN_VEC ? 2 : 0) + (sw == SW_FLAT_U4_NT ? 1 : 0);
 }
 
 }  // namespace
@@ -133,8 +136,9 @@ Plan plan_for_key(const Key &k) {
       p.ksub[0] = op == TRI_OP_RES_RMSNORM ? 1 : 0;
       return p;
     }
-    case TRI_OP_ROPE_QK: {
-      const Role r = rope_role(dt, int32_t(key_hd(k)), fl, 1);
+    case TRI_OP_ROPE_QK:
+    case TRI_OP_QK_NORM_ROPE: {
+      const Role r = rope_role(dt, int32_t(key_hd(k)), fl, 1, op == TRI_OP_QK_NORM_ROPE);
       p.variant = r.variant;
       p.n_launches = 1;
       p.kvariant[0] = r.variant;
@@ -151,19 +155,19 @@ Plan plan_for_key(const Key &k) {
       break;
   }
   const Role rn = rn_role(dt, key_H(k), fl & 3u, 1);
-  const Role ro = rope_role(dt, int32_t(key_hd(k)), (fl >> 2) & 3u, 1);
+  const Role ro = rope_role(dt, int32_t(key_hd(k)), (fl >> 2) & 3u, 1, (fl & kChainQkNorm) != 0);
   const Role sw = sw_role(dt, key_I(k), (fl >> 4) & 3u, b, 1, true);
   p.roles[0] = rn.variant;
   p.roles[1] = ro.variant;
   p.roles[2] = sw.variant;
   const bool rn_regs = rn.variant >= RN_WAVE_1 && rn.variant <= RN_BLOCK_16;
-  const bool ro_vec = ro.variant == ROPE_VEC;
+  const bool ro_vec = ro.variant == ROPE_VEC || ro.variant == ROPE_QKN_VEC;
   const bool sw_flat = sw.variant == SW_FLAT || sw.variant == SW_FLAT_U4_NT;
-  if (fl == 0x3Fu && rn_regs && ro_vec && sw_flat) {
+  if ((fl & 0x3Fu) == 0x3Fu && rn_regs && ro_vec && sw_flat) {
     p.variant = CH_FUSED;
     p.n_launches = 1;
     p.kvariant[0] = CH_FUSED;
-    p.ksub[0] = fused_sub(rn.variant, sw.variant);
+    p.ksub[0] = fused_sub(rn.variant, ro.variant, sw.variant);
     return p;
   }
   p.variant = CH_SEQ;

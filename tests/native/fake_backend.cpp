@@ -16,7 +16,8 @@ namespace {
 struct Rec {
   int32_t kvariant, dtype, ksub;
   uint32_t grid, block;
-  unsigned char args[256];
+  unsigned char args[512];
+  uint32_t nargs;
   void *stream;
 };
 
@@ -44,7 +45,8 @@ int be_resolve(int32_t kvariant, uint32_t dtype, int32_t ksub, void **fn) {
   return 0;
 }
 
-int be_launch(void *fn, uint32_t grid, uint32_t block, void *args, void *stream) {
+int be_launch(void *fn, uint32_t grid, uint32_t block, const void *args, uint32_t args_size,
+              void *stream) {
   const int64_t n = int64_t(g_log.size());
   Rec r;
   memset(&r, 0, sizeof r);
@@ -55,7 +57,8 @@ int be_launch(void *fn, uint32_t grid, uint32_t block, void *args, void *stream)
   r.grid = grid;
   r.block = block;
   r.stream = stream;
-  if (args) memcpy(r.args, args, sizeof r.args);
+  r.nargs = args && args_size <= sizeof r.args ? args_size : 0;
+  if (r.nargs) memcpy(r.args, args, r.nargs);
   g_log.push_back(r);
   return n == g_fail_at ? -1 : 0;
 }
@@ -87,7 +90,8 @@ void trifake_fail_at(int64_t n) { g_fail_at = n; }
 void trifake_init_status(int st) { g_init_status = st; }
 
 // Launch i: kernel (variant, dtype, sub), grid, block, stream and the first
-// `nbytes` bytes of its argument block.
+// `nbytes` bytes of its argument block (zero beyond its size). Returns the
+// argument block's size, or -1 if there is no launch i.
 int trifake_get(int64_t i, int32_t *kv, int32_t *dt, int32_t *sub, uint32_t *grid,
                 uint32_t *block, void **stream, unsigned char *args, int nbytes) {
   if (i < 0 || i >= int64_t(g_log.size())) return -1;
@@ -98,8 +102,11 @@ int trifake_get(int64_t i, int32_t *kv, int32_t *dt, int32_t *sub, uint32_t *gri
   *grid = r.grid;
   *block = r.block;
   *stream = r.stream;
-  if (args) memcpy(args, r.args, nbytes > 256 ? 256 : nbytes);
-  return 0;
+  if (args && nbytes > 0) {
+    const int n = nbytes > int(sizeof r.args) ? int(sizeof r.args) : nbytes;
+    memcpy(args, r.args, size_t(n));
+  }
+  return int(r.nargs);
 }
 
 }  // extern "C"

@@ -48,8 +48,9 @@ def tok_stride(t):
     return t.stride(0) if t.shape[0] > 1 else max(t.stride(0), t.shape[1] * t.shape[2])
 
 
-def model_chain_call(d, eps, base):
-    """An oracle-model Call for a decode chain over device tensors `d`."""
+def model_chain_call(d, eps, base, qk_eps=None):
+    """An oracle-model Call for a decode chain over device tensors `d` (with
+    head-norm weights when `d` holds q_norm_w / k_norm_w)."""
     dt = nm.BF16 if str(d["x"].dtype).endswith("bfloat16") else nm.F32
     T, H = d["x"].shape
     _, nq, hd = d["q"].shape
@@ -62,8 +63,12 @@ def model_chain_call(d, eps, base):
                   y=rows_stride(d["y"]), res_out=rows_stride(d["res_out"]),
                   q=tok_stride(d["q"]), k=tok_stride(d["k"]), gate=rows_stride(d["gate"]),
                   up=rows_stride(d["up"]), out=rows_stride(d["out"]))
+    if d.get("q_norm_w") is not None:
+        ptr["q_w"] = d["q_norm_w"].data_ptr()
+        ptr["k_w"] = d["k_norm_w"].data_ptr()
     return S.Call(S.OP_CHAIN, dt_code(dt), T, H=H, I=d["gate"].shape[1], hd=hd, nq=nq, nk=nk,
-                  eps=eps, base=base, ptr=ptr, stride=stride)
+                  eps=eps, base=base, qk_eps=eps if qk_eps is None else qk_eps, ptr=ptr,
+                  stride=stride)
 
 
 def expected_record(call: S.Call, version: int):

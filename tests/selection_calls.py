@@ -37,6 +37,17 @@ def rope_call(dtype, T, nq, nk, hd, *, base=10000.0, off=0, pad=0, pos_off=0, nu
                   stride={"q": nq * hd + pad, "k": nk * hd + pad})
 
 
+def qkn_call(dtype, T, nq, nk, hd, *, base=10000.0, eps=1e-6, off=0, pad=0, w_off=0,
+             pos_off=0, null=()):
+    """QK-RMSNorm + RoPE; w_off displaces both head-norm weights."""
+    ptr = {"q": _addr(10) + off, "k": _addr(11) + off, "pos": _addr(12) + pos_off,
+           "q_w": _addr(13) + w_off, "k_w": _addr(14) + w_off}
+    for n in null:
+        ptr[n] = None
+    return S.Call(S.OP_QK_NORM_ROPE, dtype, T, hd=hd, nq=nq, nk=nk, base=base, eps=eps,
+                  ptr=ptr, stride={"q": nq * hd + pad, "k": nk * hd + pad})
+
+
 def sw_call(dtype, T, I, *, off=0, pad=0, null=()):
     ptr = {"gate": _addr(20) + off, "up": _addr(21) + off, "out": _addr(22) + off}
     for n in null:
@@ -46,9 +57,13 @@ def sw_call(dtype, T, I, *, off=0, pad=0, null=()):
 
 
 def chain_call(dtype, T, H, I, nq, nk, hd, *, base=10000.0, eps=1e-6,
-               res_off=0, res_pad=0, rope_off=0, rope_pad=0, sw_off=0, sw_pad=0):
+               res_off=0, res_pad=0, rope_off=0, rope_pad=0, sw_off=0, sw_pad=0,
+               qk_norm=False, qk_eps=1e-6, w_off=0, null=()):
     r = res_call(dtype, T, H, eps=eps, off=res_off, pad=res_pad)
-    q = rope_call(dtype, T, nq, nk, hd, base=base, off=rope_off, pad=rope_pad)
+    if qk_norm:
+        q = qkn_call(dtype, T, nq, nk, hd, base=base, off=rope_off, pad=rope_pad, w_off=w_off)
+    else:
+        q = rope_call(dtype, T, nq, nk, hd, base=base, off=rope_off, pad=rope_pad)
     s = sw_call(dtype, T, I, off=sw_off, pad=sw_pad)
     ptr = dict(r.ptr)
     ptr.update(q.ptr)
@@ -56,8 +71,10 @@ def chain_call(dtype, T, H, I, nq, nk, hd, *, base=10000.0, eps=1e-6,
     stride = dict(r.stride)
     stride.update(q.stride)
     stride.update(s.stride)
+    for n in null:
+        ptr[n] = None
     return S.Call(S.OP_CHAIN, dtype, T, H=H, I=I, hd=hd, nq=nq, nk=nk, eps=eps,
-                  base=base, ptr=ptr, stride=stride)
+                  base=base, qk_eps=qk_eps, ptr=ptr, stride=stride)
 
 
 def elem_offset(dtype, n=1):

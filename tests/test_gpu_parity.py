@@ -74,17 +74,26 @@ def host(t):
 
 
 # ---- the configured chains ---------------------------------------------------------
-@pytest.mark.parametrize("cfg", [wl.TINY_F32, wl.LLAMA7B_DECODE, wl.GQA_DECODE],
-                         ids=lambda c: c.name)
+TINY_QKN_F32 = wl.ChainConfig("tiny_qkn_f32", wl.F32, T=3, H=256, nq=4, nk=2, hd=64, I=688,
+                              base=1e6, pos_mode="uniform", pos_max=4095, qk_norm=True)
+CHAIN_CFGS = [wl.TINY_F32, wl.LLAMA7B_DECODE, wl.GQA_DECODE, wl.QWEN3_8B_DECODE, TINY_QKN_F32]
+
+
+def run_chain(cache, cfg, d):
+    """decode_chain over device tensors d (head-norm weights when present)."""
+    cache.decode_chain(d["x"], d["residual"], d["w"], d["q"], d["k"], d["pos"], d["gate"],
+                       d["up"], cfg.eps, cfg.base, y=d["y"], residual_out=d["res_out"],
+                       out=d["out"], q_norm_w=d.get("q_norm_w"), k_norm_w=d.get("k_norm_w"))
+
+
+@pytest.mark.parametrize("cfg", CHAIN_CFGS, ids=lambda c: c.name)
 def test_chain_config(tri, cache, cfg):
     inp = wl.host_inputs(cfg)
     d = {k: wl.to_torch(v, cfg.dtype, DEV) for k, v in inp.items()}
     d["y"] = torch.empty_like(d["x"])
     d["res_out"] = torch.empty_like(d["x"])
     d["out"] = torch.empty_like(d["gate"])
-    cache.decode_chain(d["x"], d["residual"], d["w"], d["q"], d["k"], d["pos"], d["gate"],
-                       d["up"], cfg.eps, cfg.base, y=d["y"], residual_out=d["res_out"],
-                       out=d["out"])
+    run_chain(cache, cfg, d)
     torch.cuda.synchronize()
     want = O.decode_chain(inp, cfg.eps, cfg.base, cfg.dtype)
     check("y", host(d["y"]), want["y"], cfg.dtype)
@@ -97,16 +106,21 @@ def test_chain_config(tri, cache, cfg):
     assert rec[3] == S.CH_FUSED
 
 
-@pytest.mark.parametrize("cfg", [wl.TINY_F32, wl.LLAMA7B_DECODE, wl.GQA_DECODE],
-                         ids=lambda c: c.name)
+@pytest.mark.parametrize("cfg", CHAIN_CFGS, ids=lambda c: c.name)
 def test_fused_chain_equals_separate_ops_bitwise(tri, cache, cfg):
     inp = wl.host_inputs(cfg)
     a = {k: wl.to_torch(v, cfg.dtype, DEV) for k, v in inp.items()}
     b = {k: v.clone() for k, v in a.items()}
     y, ro, out = cache.decode_chain(a["x"], a["residual"], a["w"], a["q"], a["k"], a["pos"],
-                                    a["gate"], a["up"], cfg.eps, cfg.base)
+                                    a["gate"], a["up"], cfg.eps, cfg.base,
+                                    q_norm_w=a.get("q_norm_w"), k_norm_w=a.get("k_norm_w"))
+    assert cache.last_selection().variant == S.CH_FUSED
     y2, ro2 = cache.residual_rmsnorm(b["x"], b["residual"], b["w"], cfg.eps)
-    cache.rope_qk(b["q"], b["k"], b["pos"], cfg.base)
+    if cfg.qk_norm:
+        cache.qk_norm_rope(b["q"], b["k"], b["pos"], b["q_norm_w"], b["k_norm_w"], cfg.base,
+                           cfg.eps)
+    else:
+        cache.rope_qk(b["q"], b["k"], b["pos"], cfg.base)
     out2 = cache.swiglu(b["gate"], b["up"])
     torch.cuda.synchronize()
     for n, g, h in (("y", y, y2), ("res_out", ro, ro2), ("q", a["q"], b["q"]),
@@ -211,6 +225,82 @@ def test_rope_position_zero_is_exact_identity(tri, cache, dtype):
     check("k", host(kd), k, dtype, exact=True)
 
 
+# ---- QK-RMSNorm + RoPE: every variant ------------------------------------------------
+QKN_CASES = [
+    # dtype, T, nq, nk, hd, layout, weight offset (elements); vector cases cover
+    # every lane-group width of the head reduction (hd/2 / V = 1 .. 64 lanes)
+    (nm.BF16, 1, 32, 8, 128, "plain", 0), (nm.BF16, 8, 32, 8, 128, "plain", 0),
+    (nm.BF16, 37, 64, 8, 128, "plain", 0), (nm.BF16, 5, 8, 8, 16, "plain", 0),
+    (nm.BF16, 5, 8, 4, 32, "plain", 0), (nm.BF16, 5, 8, 4, 64, "plain", 0),
+    (nm.BF16, 5, 8, 4, 256, "plain", 0), (nm.BF16, 3, 4, 4, 512, "plain", 0),
+    (nm.F32, 5, 8, 8, 8, "plain", 0), (nm.F32, 5, 8, 4, 16, "plain", 0),
+    (nm.F32, 5, 8, 4, 32, "plain", 0), (nm.F32, 5, 8, 4, 64, "plain", 0),
+    (nm.F32, 19, 64, 8, 128, "plain", 0), (nm.F32, 5, 8, 4, 256, "plain", 0),
+    (nm.F32, 3, 2, 3, 512, "plain", 0), (nm.F32, 4, 3, 0, 128, "plain", 0),
+    (nm.BF16, 9, 8, 2, 128, "strided", 0),
+    # scalar role: unaligned operands or weights, half-heads not a power of two
+    # of vectors, head counts beyond one 256-head slice
+    (nm.BF16, 9, 8, 2, 128, "unaligned", 0), (nm.F32, 9, 8, 2, 128, "plain", 1),
+    (nm.BF16, 5, 2, 2, 96, "plain", 0), (nm.F32, 2, 2, 2, 2, "plain", 0),
+    (nm.BF16, 3, 300, 20, 64, "unaligned", 0), (nm.F32, 3, 5, 0, 64, "unaligned", 0),
+]
+
+
+def place_weight(w: np.ndarray, dtype: str, off: int):
+    """A head-norm weight [hd] on the device, `off` elements past 16 B."""
+    src = wl.to_torch(w, dtype, DEV)
+    buf = torch.zeros(w.shape[0] + 8, dtype=src.dtype, device=DEV)
+    view = buf[off:off + w.shape[0]]
+    view.copy_(src)
+    return view
+
+
+@pytest.mark.parametrize("dtype,T,nq,nk,hd,layout,w_off", QKN_CASES)
+def test_qk_norm_rope_variants(tri, cache, dtype, T, nq, nk, hd, layout, w_off):
+    r = rng(T * 5 + nq * 11 + hd + w_off)
+    q = wl.host_array(r, (T, nq, hd), dtype)
+    k = wl.host_array(r, (T, nk, hd), dtype)
+    qw, kw = wl.host_weight(r, hd, dtype), wl.host_weight(r, hd, dtype)
+    pos = r.integers(0, 8192, size=T).astype(np.int32)
+    qd = place(q, dtype, layout)
+    kd = place(k, dtype, layout) if nk else None
+    qwd, kwd = place_weight(qw, dtype, w_off), place_weight(kw, dtype, w_off)
+    cache.qk_norm_rope(qd, kd, wl.to_torch(pos, dtype, DEV), qwd, kwd if nk else None, 1e6,
+                       1e-6)
+    torch.cuda.synchronize()
+    wq, wk = O.qk_norm_rope(q, k, pos, 1e6, qw, kw, 1e-6, dtype)
+    check("q", host(qd), wq, dtype)
+    if nk:
+        check("k", host(kd), wk, dtype)
+    c = S.Call(S.OP_QK_NORM_ROPE, S.DT_F32 if dtype == nm.F32 else S.DT_BF16, T, hd=hd,
+               nq=nq, nk=nk, base=1e6, eps=1e-6,
+               ptr=dict(q=qd.data_ptr(), k=kd.data_ptr() if nk else None, pos=0,
+                        q_w=qwd.data_ptr(), k_w=kwd.data_ptr() if nk else None),
+               stride=dict(q=qd.stride(0) if T > 1 else nq * hd,
+                           k=(kd.stride(0) if T > 1 else nk * hd) if nk else 0))
+    assert cache.last_selection().variant == S.plan(S.make_key(c), T)[0]
+
+
+@pytest.mark.parametrize("dtype", [nm.F32, nm.BF16])
+def test_qk_norm_rope_zero_heads_and_position_zero(tri, cache, dtype):
+    # A zero head normalises to zero (eps > 0); at position 0 the rotation is
+    # the identity, so the op is exactly a per-head RMSNorm.
+    r = rng(23)
+    q = wl.host_array(r, (6, 8, 128), dtype)
+    k = wl.host_array(r, (6, 2, 128), dtype)
+    q[2, 3] = 0
+    k[4, 1] = 0
+    qw, kw = wl.host_weight(r, 128, dtype), wl.host_weight(r, 128, dtype)
+    qd, kd = wl.to_torch(q, dtype, DEV), wl.to_torch(k, dtype, DEV)
+    cache.qk_norm_rope(qd, kd, torch.zeros(6, dtype=torch.int32, device=DEV),
+                       wl.to_torch(qw, dtype, DEV), wl.to_torch(kw, dtype, DEV), 1e4, 1e-6)
+    torch.cuda.synchronize()
+    gq, gk = host(qd), host(kd)
+    assert not nm.values(gq[2, 3], dtype).any() and not nm.values(gk[4, 1], dtype).any()
+    check("q", gq, O.rmsnorm(q, qw, 1e-6, dtype), dtype)
+    check("k", gk, O.rmsnorm(k, kw, 1e-6, dtype), dtype)
+
+
 # ---- SwiGLU: every variant ---------------------------------------------------------------
 SW_CASES = [
     # dtype, T, I, layout
@@ -265,7 +355,11 @@ MEDIUM = [wl.ChainConfig("medium_bf16", wl.BF16, T=100, H=4096, nq=32, nk=8, hd=
           wl.ChainConfig("medium_f32", wl.F32, T=70, H=256, nq=4, nk=4, hd=64, I=690,
                          pos_mode="uniform", pos_max=4095),
           wl.ChainConfig("ragged_bf16", wl.BF16, T=65, H=2048, nq=7, nk=3, hd=64, I=1001,
-                         pos_mode="uniform", pos_max=100000)]
+                         pos_mode="uniform", pos_max=100000),
+          wl.ChainConfig("medium_qkn_bf16", wl.BF16, T=100, H=4096, nq=32, nk=8, hd=128,
+                         I=12288, base=1e6, pos_mode="uniform", pos_max=8191, qk_norm=True),
+          wl.ChainConfig("ragged_qkn_f32", wl.F32, T=67, H=512, nq=5, nk=3, hd=128, I=1001,
+                         base=1e6, pos_mode="uniform", pos_max=100000, qk_norm=True)]
 
 
 @pytest.mark.parametrize("cfg", MEDIUM, ids=lambda c: c.name)
@@ -276,9 +370,7 @@ def test_chain_beyond_decode_sizes(tri, cache, cfg):
     d = {k: wl.to_torch(v, cfg.dtype, DEV) for k, v in inp.items()}
     d["y"], d["res_out"], d["out"] = (torch.empty_like(d["x"]), torch.empty_like(d["x"]),
                                       torch.empty_like(d["gate"]))
-    cache.decode_chain(d["x"], d["residual"], d["w"], d["q"], d["k"], d["pos"], d["gate"],
-                       d["up"], cfg.eps, cfg.base, y=d["y"], residual_out=d["res_out"],
-                       out=d["out"])
+    run_chain(cache, cfg, d)
     torch.cuda.synchronize()
     want = O.decode_chain(inp, cfg.eps, cfg.base, cfg.dtype)
     for n in ("y", "q", "k", "out"):

@@ -14,8 +14,8 @@ import pytest
 from oracle import ops as O
 from oracle import selection as S
 from tests.native_libs import load_fake
-from tests.selection_calls import (chain_call, elem_offset, res_call, rn_call, rope_call,
-                                   sw_call)
+from tests.selection_calls import (chain_call, elem_offset, qkn_call, res_call, rn_call,
+                                   rope_call, sw_call)
 import workloads as wl
 
 BF, F = S.DT_BF16, S.DT_F32
@@ -54,6 +54,10 @@ def c_call(lib, cache, c: S.Call, stream=None):
     if c.op == S.OP_ROPE_QK:
         return lib.tri_rope_qk(cache, c.dtype, p.get("q"), s["q"], p.get("k"), s["k"],
                                p.get("pos"), c.T, c.nq, c.nk, c.hd, c.base, stream)
+    if c.op == S.OP_QK_NORM_ROPE:
+        return lib.tri_qk_norm_rope(cache, c.dtype, p.get("q"), s["q"], p.get("k"), s["k"],
+                                    p.get("pos"), c.T, c.nq, c.nk, c.hd, c.base, p.get("q_w"),
+                                    p.get("k_w"), c.eps, stream)
     if c.op == S.OP_SWIGLU:
         return lib.tri_swiglu(cache, c.dtype, p.get("gate"), s["gate"], p.get("up"), s["up"],
                               p.get("out"), s["out"], c.T, c.I, stream)
@@ -71,6 +75,7 @@ def c_call(lib, cache, c: S.Call, stream=None):
     a.gate, a.g_rs = p.get("gate"), s["gate"]
     a.up, a.u_rs = p.get("up"), s["up"]
     a.out, a.o_rs = p.get("out"), s["out"]
+    a.q_norm_w, a.k_norm_w, a.qk_eps = p.get("q_w"), p.get("k_w"), c.qk_eps
     return lib.tri_decode_chain(cache, C.byref(a), stream)
 
 
@@ -137,6 +142,11 @@ def call_zoo():
                 calls.append(rope_call(d, T, nq, nk, hd))
             calls.append(rope_call(d, T, 32, 8, 128, base=500000.0, off=off))
             calls.append(rope_call(d, T, 32, 8, 128, pad=64))
+            for nq, nk, hd in ((32, 8, 128), (4, 0, 64), (2, 2, 96), (8, 8, 512), (1, 1, 2)):
+                calls.append(qkn_call(d, T, nq, nk, hd, base=1e6))
+            calls.append(qkn_call(d, T, 32, 8, 128, w_off=off))
+            calls.append(qkn_call(d, T, 32, 8, 128, off=off))
+            calls.append(qkn_call(d, T, 32, 8, 128, pad=64))
             for I in (688, 11008, 14336, 28672, 11003, 1):
                 calls.append(sw_call(d, T, I))
             calls.append(sw_call(d, T, 11008, off=off))
@@ -148,6 +158,10 @@ def call_zoo():
             calls.append(chain_call(d, T, 4096, 14336, 32, 8, 128, sw_pad=64))
             calls.append(chain_call(d, T, 4096, 14336, 32, 8, 128, rope_off=off))
             calls.append(chain_call(d, T, 40000, 11008, 32, 32, 128))
+            calls.append(chain_call(d, T, 4096, 12288, 32, 8, 128, base=1e6, qk_norm=True))
+            calls.append(chain_call(d, T, 4096, 12288, 32, 8, 128, base=1e6, qk_norm=True,
+                                    w_off=off))
+            calls.append(chain_call(d, T, 256, 688, 4, 0, 64, qk_norm=True))
     # errors
     calls += [rn_call(BF, 1, 4096, null=("x",)), rn_call(BF, -1, 4096), rn_call(BF, 1, 0),
               rn_call(BF, 1, 4096, eps=float("nan")), rn_call(BF, 1, 4096, eps=-1.0),
@@ -162,6 +176,14 @@ def call_zoo():
               rope_call(BF, 1, 4, 4, 64, null=("k",)), rope_call(BF, 1, 4, 0, 64, null=("k",)),
               rope_call(BF, 1, 4, 4, 64, null=("pos",)), rope_call(BF, 1, 4, 4, 64, off=1),
               rope_call(BF, 1, 4, 4, 64, pad=-1),
+              qkn_call(BF, 1, 4, 4, 64, null=("q_w",)), qkn_call(BF, 1, 4, 4, 64, null=("k_w",)),
+              qkn_call(BF, 1, 4, 0, 64, null=("k_w", "k")), qkn_call(BF, 1, 4, 4, 64, w_off=1),
+              qkn_call(BF, 1, 4, 4, 64, eps=float("nan")), qkn_call(BF, 1, 4, 4, 64, eps=-1.0),
+              qkn_call(BF, 1, 4, 4, 63, null=("q_w",)), qkn_call(BF, 1, 4, 4, 64, base=0.5),
+              chain_call(BF, 1, 4096, 12288, 32, 8, 128, qk_norm=True, null=("k_w",)),
+              chain_call(BF, 1, 4096, 12288, 32, 8, 128, qk_norm=True, qk_eps=float("inf")),
+              chain_call(BF, 1, 4096, 12288, 32, 8, 128, qk_norm=True, w_off=1),
+              chain_call(BF, 1, 4096, 12288, 32, 8, 128, qk_eps=float("nan")),
               sw_call(BF, 1, 0), sw_call(BF, 1, S.I_LIMIT), sw_call(BF, 1, 64, null=("up",)),
               sw_call(BF, 1, 64, off=1), sw_call(BF, 3, 64, pad=-1)]
     return calls
@@ -270,14 +292,21 @@ def test_status_strings(lib):
 
 
 # ---- argument preparation ----------------------------------------------------------
-def _last_launch(lib, nbytes=256):
+# Argument struct sizes the kernels take (RnArgs, RopeArgs, SwArgs, ChainArgs).
+ARG_SIZES = {"rn": 88, "rope": 88, "sw": 80, "chain": 264}
+
+
+def _last_launch(lib, nbytes=512, size=None):
     i = lib.trifake_launch_count() - 1
     kv, dt, sub = C.c_int32(), C.c_int32(), C.c_int32()
     grid, block = C.c_uint32(), C.c_uint32()
     stream = C.c_void_p()
-    buf = C.create_string_buffer(256)
-    assert lib.trifake_get(i, C.byref(kv), C.byref(dt), C.byref(sub), C.byref(grid),
-                           C.byref(block), C.byref(stream), buf, nbytes) == 0
+    buf = C.create_string_buffer(nbytes)
+    n = lib.trifake_get(i, C.byref(kv), C.byref(dt), C.byref(sub), C.byref(grid),
+                        C.byref(block), C.byref(stream), buf, nbytes)
+    assert n >= 0
+    if size is not None:
+        assert n == ARG_SIZES[size]
     return kv.value, dt.value, sub.value, grid.value, block.value, stream.value, buf.raw
 
 
@@ -285,7 +314,7 @@ def test_rmsnorm_argument_block_and_stream(lib, fresh):
     cache = fresh(flags=1)
     c = res_call(BF, 5, 4096, pad=64)
     assert c_call(lib, cache, c, stream=0xABC0) == 0
-    kv, dt, sub, grid, block, stream, raw = _last_launch(lib)
+    kv, dt, sub, grid, block, stream, raw = _last_launch(lib, size="rn")
     assert (kv, dt, sub, grid, block, stream) == (S.RN_BLOCK[2], BF, 1, 5, 256, 0xABC0)
     f = struct.unpack_from("<5Q4qqif", raw)
     p = c.ptr
@@ -298,18 +327,46 @@ def test_chain_argument_block(lib, fresh):
     cache = fresh(flags=1)
     c = chain_call(BF, 8, 4096, 14336, 32, 8, 128, base=500000.0)
     assert c_call(lib, cache, c) == 0
-    kv, dt, sub, grid, block, _, raw = _last_launch(lib)
-    # fused kernel: RN_BLOCK_2 (norm role index 3), cached one-vector SwiGLU
-    assert (kv, dt, sub, grid, block) == (50, BF, 3 * 2, 8 + 8 + 56, 256)
-    rope = struct.unpack_from("<4Q3q4i", raw, 88)
+    kv, dt, sub, grid, block, _, raw = _last_launch(lib, size="chain")
+    # fused kernel: RN_BLOCK_2 (norm role index 3), plain RoPE, cached one-vector SwiGLU
+    assert (kv, dt, sub, grid, block) == (50, BF, 3 * 4, 8 + 8 + 56, 256)
+    rope = struct.unpack_from("<6Q3q3if", raw, 88)
     assert rope[0] == c.ptr["q"] and rope[1] == c.ptr["k"] and rope[2] == c.ptr["pos"]
-    assert rope[4:7] == (32 * 128, 8 * 128, 8) and rope[7:10] == (32, 8, 128)
-    sw = struct.unpack_from("<3Q7q", raw, 160)
+    assert rope[4:6] == (0, 0) and rope[12] == 0.0
+    assert rope[6:9] == (32 * 128, 8 * 128, 8) and rope[9:12] == (32, 8, 128)
+    sw = struct.unpack_from("<3Q7q", raw, 176)
     assert sw[:3] == (c.ptr["gate"], c.ptr["up"], c.ptr["out"])
     assert sw[3:] == (14336, 14336, 14336, 8, 14336, 8 * 14336 // 8, 8 * 14336)
-    assert struct.unpack_from("<2I", raw, 240) == (8, 8)
+    assert struct.unpack_from("<2I", raw, 256) == (8, 8)
     # the RoPE table pointer is this version's uploaded constants
     assert rope[3] != 0
+
+
+def test_qk_norm_chain_argument_block(lib, fresh):
+    cache = fresh(flags=1)
+    c = chain_call(BF, 1, 4096, 12288, 32, 8, 128, base=1e6, qk_norm=True, qk_eps=1e-5)
+    assert c_call(lib, cache, c) == 0
+    kv, dt, sub, grid, block, _, raw = _last_launch(lib, size="chain")
+    # RN_BLOCK_2 with the QK-norm RoPE role and cached SwiGLU
+    assert (kv, dt, sub, grid, block) == (50, BF, 3 * 4 + 2, 1 + 1 + 6, 256)
+    rope = struct.unpack_from("<6Q3q3if", raw, 88)
+    assert rope[4:6] == (c.ptr["q_w"], c.ptr["k_w"])
+    assert rope[12] == np.float32(1e-5)
+    assert S.unpack_key(S.make_key(c))["flags"] == 0x7F
+    # the standalone op launches the same role body with the same block
+    c2 = qkn_call(BF, 1, 32, 8, 128, base=1e6, eps=1e-5)
+    assert c_call(lib, cache, c2) == 0
+    kv2, _, _, grid2, _, _, raw2 = _last_launch(lib, size="rope")
+    assert (kv2, grid2) == (S.ROPE_QKN_VEC, 1)
+    assert struct.unpack_from("<6Q3q3if", raw2, 0)[4:] == rope[4:]
+
+
+def test_qk_norm_without_k_heads_passes_no_k_weight(lib, fresh):
+    cache = fresh(flags=1)
+    c = qkn_call(F, 2, 4, 0, 64)
+    assert c_call(lib, cache, c) == 0
+    rope = struct.unpack_from("<6Q3q3if", _last_launch(lib, size="rope")[6], 0)
+    assert rope[1] == 0 and rope[4] == c.ptr["q_w"] and rope[5] == 0
 
 
 @pytest.mark.parametrize("base,hd", [(10000.0, 64), (10000.0, 128), (500000.0, 128),

@@ -277,3 +277,77 @@ def test_chain_is_the_three_ops():
     assert np.array_equal(out["y"], y) and np.array_equal(out["res_out"], h)
     assert np.array_equal(out["q"], q) and np.array_equal(out["k"], k)
     assert np.array_equal(out["out"], ops.swiglu(inp["gate"], inp["up"], nm.F32))
+
+
+# ---- QK-RMSNorm + RoPE ---------------------------------------------------------------
+def test_qk_norm_rope_constant_heads_at_position_zero():
+    # A head of constant value c with unit weights and eps 0 normalises to
+    # sign(c) everywhere; position 0 rotates by nothing.
+    q = np.full((2, 3, 64), -2.5, np.float32)
+    k = np.full((2, 1, 64), 0.125, np.float32)
+    ones = np.ones(64, np.float32)
+    qo, ko = ops.qk_norm_rope(q, k, np.zeros(2, np.int32), 1e4, ones, ones, 0.0, nm.F32)
+    assert np.all(qo == -1.0) and np.all(ko == 1.0)
+
+
+@pytest.mark.parametrize("dtype", [nm.F32, nm.BF16])
+def test_qk_norm_rope_matches_library_norm_and_complex_rotation(dtype):
+    cfg = wl.QWEN3_8B_DECODE
+    inp = wl.host_inputs(cfg, T=5)
+    if dtype == nm.F32:
+        inp = {k: (nm.values(v, nm.BF16).astype(np.float32) if v.dtype == np.uint16 else v)
+               for k, v in inp.items()}
+    q, qw, pos = inp["q"], inp["q_norm_w"], inp["pos"]
+    qo, _ = ops.qk_norm_rope(q, None, pos, cfg.base, qw, None, 1e-6, dtype)
+    # torch's RMSNorm over the head dimension in float64 (not rounded) ...
+    qt = torch.from_numpy(nm.values(q, dtype))
+    n = F.rms_norm(qt, (cfg.hd,), torch.from_numpy(nm.values(qw, dtype)),
+                   float(np.float32(1e-6))).numpy()
+    # ... then the rotation as a complex product, rounded once
+    half = cfg.hd // 2
+    inv = np.array([math.pow(cfg.base, -2.0 * i / cfg.hd) for i in range(half)])
+    theta = (pos.astype(np.float32)[:, None] * inv.astype(np.float32)[None, :]).astype(np.float64)
+    z = (n[..., :half] + 1j * n[..., half:]) * np.exp(1j * theta)[:, None, :]
+    want = nm.round_to(np.concatenate([z.real, z.imag], axis=-1), dtype)
+    if dtype == nm.F32:
+        assert within_ulps_f32(qo, want, 2).all()
+    else:
+        assert (nm.bf16_ulp_distance(qo, want) <= 1).all()
+
+
+def test_qk_norm_rope_rounds_once():
+    # Rounding the normalised head to bf16 before the rotation would be a
+    # second rounding; the op keeps it in full precision.
+    cfg = wl.QWEN3_8B_DECODE
+    inp = wl.host_inputs(cfg, T=3)
+    qo, _ = ops.qk_norm_rope(inp["q"], None, inp["pos"], cfg.base, inp["q_norm_w"], None,
+                             1e-6, nm.BF16)
+    twice, _ = ops.rope_qk(ops.rmsnorm(inp["q"], inp["q_norm_w"], 1e-6, nm.BF16), None,
+                           inp["pos"], cfg.base, nm.BF16)
+    a = nm.values(qo, nm.BF16)
+    b = nm.values(twice, nm.BF16)
+    # the two differ only by the intermediate rounding: at most 2^-8 of the
+    # head's largest normalised magnitude per element, plus the final roundings
+    scale = np.abs(a).max(axis=-1, keepdims=True)
+    assert (np.abs(a - b) <= scale * 2.0 ** -7).all()
+    assert not np.array_equal(qo, twice)
+
+
+def test_qk_norm_rope_preserves_head_rms_with_unit_weights():
+    rng = np.random.Generator(np.random.PCG64(21))
+    q = rng.standard_normal((4, 6, 128)).astype(np.float32) * np.float32(7.0)
+    ones = np.ones(128, np.float32)
+    qo, _ = ops.qk_norm_rope(q, None, np.array([0, 5, 500, 8000], np.int32), 5e5, ones, None,
+                             0.0, nm.F32)
+    ms = np.mean(qo.astype(np.float64) ** 2, axis=-1)     # rotation keeps the unit RMS
+    assert np.allclose(ms, 1.0, rtol=1e-5)
+
+
+def test_chain_with_qk_norm_is_norm_then_rope():
+    inp = wl.host_inputs(wl.QWEN3_8B_DECODE)
+    out = ops.decode_chain(inp, 1e-6, 1e6, nm.BF16)
+    q, k = ops.qk_norm_rope(inp["q"], inp["k"], inp["pos"], 1e6, inp["q_norm_w"],
+                            inp["k_norm_w"], 1e-6, nm.BF16)
+    assert np.array_equal(out["q"], q) and np.array_equal(out["k"], k)
+    plain = ops.rope_qk(inp["q"], inp["k"], inp["pos"], 1e6, nm.BF16)
+    assert not np.array_equal(out["q"], plain[0])

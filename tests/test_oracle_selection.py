@@ -4,7 +4,7 @@ worked by hand for the decode shapes (CPU only)."""
 import pytest
 
 from oracle import selection as S
-from tests.selection_calls import (chain_call, elem_offset, res_call, rn_call,
+from tests.selection_calls import (chain_call, elem_offset, qkn_call, res_call, rn_call,
                                    rope_call, sw_call)
 
 BF, F = S.DT_BF16, S.DT_F32
@@ -61,6 +61,51 @@ def test_policy_prefill_chain():
                                                       base=500000.0)), 8192)
     assert (v, roles) == (S.CH_FUSED, (15, 31, 44))
     assert launches == [(50, 8192 + 8192 + 28672, 256)]
+
+
+def test_policy_qwen3_decode_chain_with_qk_norm():
+    # As the Llama-7B decode, but the RoPE role is the QK-norm vector role (34)
+    # and the key carries flag 0x40; SwiGLU 12288 / 8 = 1536 vectors -> 6 blocks.
+    c = chain_call(BF, 1, 4096, 12288, 32, 8, 128, base=1e6, qk_norm=True)
+    assert S.unpack_key(S.make_key(c))["flags"] == 0x7F
+    v, roles, launches = S.plan(S.make_key(c), 1)
+    assert (v, roles, launches) == (S.CH_FUSED, (14, 34, 41), [(50, 1 + 1 + 6, 256)])
+
+
+def test_qk_norm_is_a_guard():
+    # Same shapes with and without the head norm are different versions.
+    plain = chain_call(BF, 1, 4096, 12288, 32, 8, 128, base=1e6)
+    qkn = chain_call(BF, 1, 4096, 12288, 32, 8, 128, base=1e6, qk_norm=True)
+    assert S.make_key(plain) != S.make_key(qkn)
+    m = S.SpecCacheModel(flags=S.FLAG_AUTO_INSTALL)
+    assert m.call(plain) == S.OK and m.call(qkn) == S.OK
+    assert len(m.versions) == 2 and m.last.roles[1] == S.ROPE_QKN_VEC
+
+
+def test_qk_norm_weight_alignment_selects_scalar_role():
+    # A head-norm weight one element off 16 B drops the vector path; the
+    # chain then runs as three launches with the scalar QK-norm role.
+    c = qkn_call(BF, 4, 32, 8, 128, w_off=elem_offset(BF))
+    assert S.plan(S.make_key(c), 4)[2] == [(S.ROPE_QKN_SCALAR, 4, 256)]
+    c = qkn_call(BF, 4, 32, 8, 128)
+    assert S.plan(S.make_key(c), 4)[2] == [(S.ROPE_QKN_VEC, 4, 256)]
+    ch = chain_call(BF, 4, 4096, 12288, 32, 8, 128, qk_norm=True, w_off=elem_offset(BF))
+    v, roles, launches = S.plan(S.make_key(ch), 4)
+    assert v == S.CH_SEQ and roles[1] == S.ROPE_QKN_SCALAR and len(launches) == 3
+
+
+def test_qk_norm_without_k_heads_needs_no_k_weight():
+    c = qkn_call(F, 2, 4, 0, 64, null=("k", "k_w"))
+    assert S.validate(c) is None
+    c = qkn_call(F, 2, 4, 4, 64, null=("k_w",))
+    assert S.validate(c) == S.E_INVALID
+
+
+def test_qk_eps_is_checked_only_with_the_head_norm():
+    bad = float("nan")
+    assert S.validate(chain_call(BF, 1, 256, 688, 4, 4, 64, qk_eps=bad)) is None
+    assert S.validate(chain_call(BF, 1, 256, 688, 4, 4, 64, qk_norm=True,
+                                 qk_eps=bad)) == S.E_INVALID
 
 
 def test_policy_tiny_f32_chain():

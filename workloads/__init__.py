@@ -6,8 +6,9 @@ parity tests and the benchmark, so that both sides see identical inputs.
 
 Shapes are those of Llama-family decode and prefill steps (hidden 4096/8192,
 32 or 64 query heads of width 128, 8-head GQA keys, SwiGLU intermediates of
-11008/14336/28672). Draw order per config is fixed:
-x, residual, w, q, k, positions, gate, up.
+11008/14336/28672) and a Qwen3-8B-shaped decode step with per-head QK norm.
+Draw order per config is fixed: x, residual, w, q, k, positions, gate, up,
+then (QK-norm configs) the Q and K head-norm weights.
 
 * activations ~ N(0, 1) drawn in float32, then rounded to bfloat16 (RNE, via
   torch's cast) when the config is bf16;
@@ -44,6 +45,7 @@ class ChainConfig:
     pos_mode: str = "arange"       # "arange" or "uniform"
     pos_max: int = 0               # inclusive upper bound for "uniform"
     outliers: bool = False         # element-wise Bernoulli(1e-3) x 50
+    qk_norm: bool = False          # per-head RMSNorm of Q and K before RoPE
     seed: int = 0
 
 
@@ -58,7 +60,14 @@ GQA_DECODE = ChainConfig("gqa_decode_bf16", BF16, T=8, H=4096, nq=32, nk=8, hd=1
 PREFILL_8K = ChainConfig("prefill8k_bf16", BF16, T=8192, H=8192, nq=64, nk=8, hd=128,
                          I=28672, base=500000.0, pos_mode="arange", outliers=True)
 
-CONFIGS = {c.name: c for c in (TINY_F32, LLAMA7B_DECODE, GQA_DECODE, PREFILL_8K)}
+# Qwen3-8B-shaped decode step (hidden 4096, 32 Q / 8 K heads of 128 with
+# per-head QK-RMSNorm, intermediate 12288, RoPE base 1e6).
+QWEN3_8B_DECODE = ChainConfig("qwen3_8b_decode_bf16", BF16, T=1, H=4096, nq=32, nk=8, hd=128,
+                              I=12288, base=1000000.0, pos_mode="uniform", pos_max=8191,
+                              qk_norm=True)
+
+CONFIGS = {c.name: c for c in (TINY_F32, LLAMA7B_DECODE, GQA_DECODE, PREFILL_8K,
+                               QWEN3_8B_DECODE)}
 
 # Mixed-shape stream: token counts, dtype mix and layout anomalies.
 MIXED_T_CHOICES = (1, 2, 4, 8, 16, 32, 64, 128, 512)
@@ -140,7 +149,11 @@ def host_inputs(cfg: ChainConfig, T: Optional[int] = None,
     pos = _positions(rng, cfg, T)
     gate = _act(rng, (T, cfg.I), d, o)
     up = _act(rng, (T, cfg.I), d, o)
-    return dict(x=x, residual=residual, w=w, q=q, k=k, pos=pos, gate=gate, up=up)
+    out = dict(x=x, residual=residual, w=w, q=q, k=k, pos=pos, gate=gate, up=up)
+    if cfg.qk_norm:
+        out["q_norm_w"] = _weight(rng, cfg.hd, d)
+        out["k_norm_w"] = _weight(rng, cfg.hd, d)
+    return out
 
 
 def host_array(rng, shape, dtype, outliers=False):
@@ -209,4 +222,8 @@ def device_inputs(cfg: ChainConfig, device="cuda", seed: Optional[int] = None):
                             dtype=torch.int32)
     gate = act((T, cfg.I))
     up = act((T, cfg.I))
-    return dict(x=x, residual=residual, w=w, q=q, k=k, pos=pos, gate=gate, up=up)
+    out = dict(x=x, residual=residual, w=w, q=q, k=k, pos=pos, gate=gate, up=up)
+    if cfg.qk_norm:
+        for n in ("q_norm_w", "k_norm_w"):
+            out[n] = (torch.rand((cfg.hd,), generator=g, device=device) + 0.5).to(td)
+    return out
