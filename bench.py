@@ -63,8 +63,9 @@ def algorithmic_bytes(cfg):
     res = 4 * T * H * es + H * es
     rope = 2 * T * nh * hd * es + 4 * T + 4 * (hd // 2)
     sw = 3 * T * I * es
+    qkn = rope + 2 * hd * es                     # + the two head-norm weights
     return {"rmsnorm": rms, "residual_rmsnorm": res, "rope_qk": rope, "swiglu": sw,
-            "chain": res + rope + sw}
+            "chain": res + rope + sw, "qk_norm_rope": qkn, "chain_qk_norm": res + qkn + sw}
 
 
 def torch_eager_chain(d, eps, base, out):
@@ -335,6 +336,12 @@ def main():
         ab, _ = cb.chain_args(db["x"], db["residual"], db["w"], db["q"], db["k"], db["pos"],
                               db["gate"], db["up"], cfgb.eps, cfgb.base, y=y, residual_out=ro,
                               out=out)
+        # the same shapes with per-head QK-RMSNorm (weights U(0.5, 1.5))
+        qw = (torch.rand(cfgb.hd, device=dev) + 0.5).to(db["q"].dtype)
+        kw = (torch.rand(cfgb.hd, device=dev) + 0.5).to(db["q"].dtype)
+        abq, _ = cb.chain_args(db["x"], db["residual"], db["w"], db["q"], db["k"], db["pos"],
+                               db["gate"], db["up"], cfgb.eps, cfgb.base, y=y,
+                               residual_out=ro, out=out, q_norm_w=qw, k_norm_w=kw)
         copy_src = torch.empty(1 << 29, dtype=torch.bfloat16, device=dev)
         copy_dst = torch.empty_like(copy_src)
         ops = {
@@ -345,6 +352,9 @@ def main():
             "rmsnorm": lambda: cb.rmsnorm(db["x"], db["w"], cfgb.eps, out=y, stream=stream),
             "rope_qk": lambda: cb.rope_qk(db["q"], db["k"], db["pos"], cfgb.base, stream=stream),
             "swiglu": lambda: cb.swiglu(db["gate"], db["up"], out=out, stream=stream),
+            "qk_norm_rope": lambda: cb.qk_norm_rope(db["q"], db["k"], db["pos"], qw, kw,
+                                                    cfgb.base, cfgb.eps, stream=stream),
+            "chain_qk_norm": lambda: cb.decode_chain_args(abq, stream),
             "copy_1GiB_torch": lambda: copy_dst.copy_(copy_src),
         }
         nbytes["copy_1GiB_torch"] = 2 * copy_src.numel() * 2
