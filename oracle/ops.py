@@ -27,6 +27,18 @@ are:
   not rounded in between, so the fused op rounds once, like every op here.
 * Decode chain: the three ops above on disjoint operands, in one call; with
   head-norm weights given, RoPE becomes QK-RMSNorm + RoPE.
+* RoPE variants (`rope_ext`): GPT-J pairs (2i, 2i + 1) instead of
+  rotate-half; partial rotary over the first rd <= hd elements of each head
+  with inv_i = RN_f32(base^(-2i/rd)) and the rest passed through (or only
+  normalised, with the QK norm); int64 positions, converted to float32 with
+  one round-to-nearest-even step; Llama-3 frequency scaling of the inverse
+  frequencies (the published piecewise rule: wavelengths below
+  L / high_freq_factor keep their frequency, those above L / low_freq_factor
+  are divided by `factor`, and those in between interpolate linearly in
+  L / wavelength, L the original context length), evaluated exactly and
+  rounded to float32 once; or cos / sin read from a caller's float32 cache
+  with rows [cos_0 .. cos_{rd/2-1}, sin_0 .. sin_{rd/2-1}] per position,
+  positions clamped to the cache's rows.
 """
 from __future__ import annotations
 
@@ -75,27 +87,76 @@ def _decimal_to_f32(d: Decimal) -> np.float32:
     return np.float32(best[1])
 
 
+_PREC = 60
+
+
+def _inv_freq_exact(base: float, hd: int):
+    """base^(-2i/hd) for i in [0, hd/2) as 60-digit Decimals (exp of a log);
+    `base` is the float32 value the caller passes."""
+    b = Decimal(float(np.float32(base)))
+    with localcontext() as ctx:
+        ctx.prec = _PREC
+        lnb = b.ln()
+        return [(lnb * (Decimal(-2 * i) / Decimal(hd))).exp() for i in range(hd // 2)]
+
+
 def rope_inv_freq(base: float, hd: int) -> np.ndarray:
     """inv_i = RN_f32(base^(-2i/hd)) for i in [0, hd/2), exactly rounded.
 
     The power is evaluated with 60 significant decimal digits
     (exp(ln(base) * -2i/hd)) and then rounded to the nearest float32.
-    `base` is the float32 value the caller passes.
     """
-    b = Decimal(float(np.float32(base)))
-    out = np.empty(hd // 2, dtype=np.float32)
+    return np.array([_decimal_to_f32(v) for v in _inv_freq_exact(base, hd)], dtype=np.float32)
+
+
+def _decimal_pi() -> Decimal:
+    """pi to the working precision (Machin: 16 atan(1/5) - 4 atan(1/239))."""
+    def atan_inv(n: int) -> Decimal:
+        x = Decimal(1) / n
+        x2 = x * x
+        term, total, k = x, x, 1
+        while True:
+            term = -term * x2
+            k += 2
+            t = term / k
+            if t == 0 or abs(t) < Decimal(10) ** (-(_PREC + 5)):
+                break
+            total += t
+        return total
     with localcontext() as ctx:
-        ctx.prec = 60
-        lnb = b.ln()
-        for i in range(hd // 2):
-            ex = Decimal(-2 * i) / Decimal(hd)
-            out[i] = _decimal_to_f32((lnb * ex).exp())
-    return out
+        ctx.prec = _PREC + 10
+        return 16 * atan_inv(5) - 4 * atan_inv(239)
+
+
+def llama3_scale(inv: Decimal, factor: float, low: float, high: float, orig: int) -> Decimal:
+    """The Llama-3 rule applied to one exact inverse frequency (Decimal)."""
+    f, lo, hi = (Decimal(float(np.float32(v))) for v in (factor, low, high))
+    L = Decimal(int(orig))
+    with localcontext() as ctx:
+        ctx.prec = _PREC
+        wavelen = 2 * _decimal_pi() / inv
+        if wavelen < L / hi:
+            return inv
+        if wavelen > L / lo:
+            return inv / f
+        smooth = (L / wavelen - lo) / (hi - lo)
+        return (1 - smooth) * inv / f + smooth * inv
+
+
+def rope_inv_freq_llama3(base: float, hd: int, factor: float, low: float, high: float,
+                         orig: int) -> np.ndarray:
+    """Llama-3-scaled inverse frequencies, evaluated exactly, rounded once."""
+    return np.array([_decimal_to_f32(llama3_scale(v, factor, low, high, orig))
+                     for v in _inv_freq_exact(base, hd)], dtype=np.float32)
 
 
 def rope_angles(pos: np.ndarray, inv: np.ndarray) -> np.ndarray:
-    """theta[t, i] = RN_f32(float32(pos_t) * inv_i), returned as float64."""
-    p32 = np.asarray(pos, dtype=np.int32).astype(np.float32)
+    """theta[t, i] = RN_f32(float32(pos_t) * inv_i), returned as float64.
+    Positions are int32 or int64; the conversion to float32 rounds to
+    nearest, ties to even."""
+    p = np.asarray(pos)
+    assert p.dtype in (np.int32, np.int64)
+    p32 = p.astype(np.float32)
     th = p32[:, None] * np.asarray(inv, dtype=np.float32)[None, :]   # float32 product
     assert th.dtype == np.float32
     return th.astype(np.float64)
@@ -139,6 +200,62 @@ def qk_norm_rope(q, k, pos, base, q_w, k_w, eps, dtype):
     return qo, ko
 
 
+def _rotate_pairs64(vv: np.ndarray, c: np.ndarray, s: np.ndarray, rd: int,
+                    interleaved: bool) -> np.ndarray:
+    """Rotate the first rd elements of float64 heads vv [T, nh, hd] by cos c /
+    sin s [T, rd/2]: pairs (i, i + rd/2), or (2i, 2i + 1) when interleaved.
+    Elements past rd are returned unchanged."""
+    out = vv.copy()
+    c = c[:, None, :]
+    s = s[:, None, :]
+    if interleaved:
+        x, y = vv[..., 0:rd:2], vv[..., 1:rd:2]
+        out[..., 0:rd:2] = x * c - y * s
+        out[..., 1:rd:2] = y * c + x * s
+    else:
+        h = rd // 2
+        x, y = vv[..., :h], vv[..., h:rd]
+        out[..., :h] = x * c - y * s
+        out[..., h:rd] = y * c + x * s
+    return out
+
+
+def rope_ext(q, k, pos, base, dtype, *, rotary_dim=None, interleaved=False, scaling=None,
+             cos_sin=None, q_w=None, k_w=None, eps=1e-6):
+    """RoPE on Q [T, nq, hd] and K [T, nk, hd] with the variants above.
+
+    rotary_dim: rd (default hd). scaling: None or a dict with factor,
+    low_freq_factor, high_freq_factor, original_max_pos (Llama-3 rule).
+    cos_sin: float32 [n, rd] cache (base and scaling unused). q_w / k_w:
+    QK-RMSNorm over the whole head first. One rounding at the end.
+    """
+    hd = q.shape[-1]
+    rd = hd if rotary_dim is None else rotary_dim
+    if cos_sin is not None:
+        cache = np.asarray(cos_sin, dtype=np.float32)
+        p = np.clip(np.asarray(pos).astype(np.int64), 0, cache.shape[0] - 1)
+        c = cache[p, : rd // 2].astype(np.float64)
+        s = cache[p, rd // 2: rd].astype(np.float64)
+    else:
+        if scaling is None:
+            inv = rope_inv_freq(base, rd)
+        else:
+            inv = rope_inv_freq_llama3(base, rd, scaling["factor"], scaling["low_freq_factor"],
+                                       scaling["high_freq_factor"],
+                                       scaling["original_max_pos"])
+        theta = rope_angles(pos, inv)
+        c, s = np.cos(theta), np.sin(theta)
+
+    def one(v, w):
+        vv = values(v, dtype)
+        if w is not None:
+            vv = _rmsnorm64(vv, values(w, dtype), eps)
+        return round_to(_rotate_pairs64(vv, c, s, rd, interleaved), dtype)
+    qo = one(q, q_w)
+    ko = one(k, k_w) if k is not None and k.size else k
+    return qo, ko
+
+
 def swiglu(gate, up, dtype):
     """out = silu(gate) * up with silu(g) = g / (1 + exp(-g))."""
     g = values(gate, dtype)
@@ -150,9 +267,14 @@ def swiglu(gate, up, dtype):
 
 def decode_chain(inp: Dict[str, np.ndarray], eps: float, base: float,
                  dtype: str) -> Dict[str, np.ndarray]:
-    """Residual add + RMSNorm, RoPE on Q/K and SwiGLU on disjoint operands."""
+    """Residual add + RMSNorm, RoPE on Q/K and SwiGLU on disjoint operands.
+    inp["rope_ext"] (keyword arguments of rope_ext) selects a RoPE variant."""
     y, h = residual_rmsnorm(inp["x"], inp["residual"], inp["w"], eps, dtype)
-    if inp.get("q_norm_w") is not None:
+    if inp.get("rope_ext") is not None:
+        qo, ko = rope_ext(inp["q"], inp["k"], inp["pos"], base, dtype, q_w=inp.get("q_norm_w"),
+                          k_w=inp.get("k_norm_w"), eps=inp.get("qk_eps", eps),
+                          **inp["rope_ext"])
+    elif inp.get("q_norm_w") is not None:
         qo, ko = qk_norm_rope(inp["q"], inp["k"], inp["pos"], base, inp["q_norm_w"],
                               inp["k_norm_w"], inp.get("qk_eps", eps), dtype)
     else:
@@ -162,5 +284,5 @@ def decode_chain(inp: Dict[str, np.ndarray], eps: float, base: float,
 
 
 __all__ = ["rmsnorm", "residual_add", "residual_rmsnorm", "rope_inv_freq",
-           "rope_angles", "rope_apply", "rope_qk", "qk_norm_rope", "swiglu", "decode_chain",
-           "F32", "BF16"]
+           "rope_inv_freq_llama3", "llama3_scale", "rope_angles", "rope_apply", "rope_qk",
+           "qk_norm_rope", "rope_ext", "swiglu", "decode_chain", "F32", "BF16"]
