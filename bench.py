@@ -316,6 +316,22 @@ def main():
     latency["qk_norm_decode_chain_host_us"] = summary(list(hst[:n2]))
     latency["qk_norm_decode_selection"] = {"variant": sel3.variant, "roles": list(sel3.roles)}
 
+    # ---- Llama-3.1-8B-shaped decode (1 token, Llama-3 frequency scaling) ---------------
+    cfg4 = wl.LLAMA31_8B_DECODE
+    inp4 = wl.host_inputs(cfg4)
+    d4 = {k: wl.to_torch(v, cfg4.dtype, dev) for k, v in inp4.items()}
+    x4 = cfg4.rope_ext
+    rope4 = tri.rope_ext(scaling={n: x4[n] for n in ("factor", "low_freq_factor",
+                                                     "high_freq_factor", "original_max_pos")})
+    args4, _outs4 = cache.chain_args(d4["x"], d4["residual"], d4["w"], d4["q"], d4["k"],
+                                     d4["pos"], d4["gate"], d4["up"], cfg4.eps, cfg4.base,
+                                     rope=rope4)
+    cache.decode_chain_args(args4, stream)
+    torch.cuda.synchronize()
+    st = bench.trib_latency(cache.handle, 0, C.byref(args4), sptr, W, n2, e2e, hst)
+    assert st == 0, st
+    latency["llama3_scaled_decode_chain_e2e_us"] = summary(list(e2e[:n2]))
+
     # ---- mixed-shape stream: guard hits, misses, latency per token bucket ---------------
     mixed = None if args.no_stream else run_mixed_stream(tri, wl, bench, dev, stream, torch)
 

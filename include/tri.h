@@ -18,8 +18,9 @@
  * Guards (the key): op, dtype, hidden size H, intermediate size I, head_dim,
  * Q and K head counts, token-count bucket ceil(log2 T), 16-byte alignment of
  * every activation / weight pointer and row stride, contiguity of every row
- * stride, and the RoPE base. They are equality tests on a packed key, so at
- * most one version matches.
+ * stride, the RoPE base and the RoPE variant (rotary dim, pairing, position
+ * width, angle source, frequency scaling and its parameters). They are
+ * equality tests on a packed key, so at most one version matches.
  *
  * Conventions (all entry points)
  * ------------------------------
@@ -79,6 +80,9 @@ typedef struct tri_launch_rec {
   uint32_t block_x;    /* work-items per workgroup                            */
 } tri_launch_rec;
 
+/* Words of the packed guard key. */
+enum { TRI_KEY_WORDS = 6 };
+
 /* The selection record of the last entry call (or of an install). */
 typedef struct tri_selection {
   int32_t op;          /* tri_op                                              */
@@ -88,7 +92,7 @@ typedef struct tri_selection {
   int32_t n_launches;  /* launches issued (0 on miss / error / T == 0)        */
   int32_t roles[3];    /* chain only: norm, RoPE, SwiGLU role variants        */
   tri_launch_rec launch[3];
-  uint64_t key[3];     /* packed guard key, zero when not computed            */
+  uint64_t key[TRI_KEY_WORDS];  /* packed guard key, zero when not computed   */
 } tri_selection;
 
 typedef struct tri_stats {
@@ -103,11 +107,55 @@ typedef struct tri_stats {
 } tri_stats;
 
 typedef struct tri_version_info {
-  uint64_t key[3];
+  uint64_t key[TRI_KEY_WORDS];
   int32_t variant;
   int32_t roles[3];
   uint64_t hits;
 } tri_version_info;
+
+/* RoPE variants. A zeroed struct (or a NULL pointer where one is taken) is
+ * the plain rotation of tri_rope_qk. None of these is defined in the paper;
+ * they are the common forms of the op in Llama-family and GPT-J / NeoX
+ * models, each a guard field of the key (a new shape of the op grows the
+ * cache, Sec. 3.5).
+ *  rotary_dim   rd: rotate the first rd elements of each head, pass the rest
+ *               through (0 means hd); even, 2..hd. inv_i = RN_f32(base^(-2i/rd)).
+ *  interleaved  0: pairs (i, i + rd/2) (rotate-half); 1: pairs (2i, 2i + 1)
+ *               (GPT-J).
+ *  pos_int64    0: pos is int32 [T] (4-byte aligned); 1: int64 [T] (8-byte
+ *               aligned). A position becomes float32 by round-to-nearest-even.
+ *  scaling      TRI_ROPE_SCALING_LLAMA3: the inverse frequencies are
+ *               rescaled at install by the Llama-3 rule with factor,
+ *               low_freq_factor, high_freq_factor and original_max_pos
+ *               (wavelength 2 pi / inv_i below original_max_pos /
+ *               high_freq_factor: kept; above original_max_pos /
+ *               low_freq_factor: divided by factor; in between: linear in
+ *               original_max_pos / wavelength), evaluated in extended
+ *               precision and rounded once. factor, low_freq_factor finite
+ *               and > 0, high_freq_factor finite and > low_freq_factor,
+ *               original_max_pos >= 1.
+ *  cos_sin      optional float32 cache [cos_sin_len, rd] (4-byte aligned):
+ *               row p holds cos_0 .. cos_{rd/2-1} then sin_0 .. sin_{rd/2-1}
+ *               for position p; positions are clamped to [0, cos_sin_len -
+ *               1]. With a cache, base is not used (nor checked) and scaling
+ *               must be NONE; cos_sin_len >= 1. */
+typedef enum tri_rope_scaling {
+  TRI_ROPE_SCALING_NONE = 0,
+  TRI_ROPE_SCALING_LLAMA3 = 1
+} tri_rope_scaling;
+
+typedef struct tri_rope_ext {
+  int32_t rotary_dim;
+  int32_t interleaved;
+  int32_t pos_int64;
+  int32_t scaling;               /* tri_rope_scaling */
+  float factor;
+  float low_freq_factor;
+  float high_freq_factor;
+  int32_t original_max_pos;
+  const float *cos_sin;
+  int64_t cos_sin_len;
+} tri_rope_ext;
 
 /* Arguments of tri_decode_chain: the three ops on disjoint operands. */
 typedef struct tri_chain_args {
@@ -125,7 +173,7 @@ typedef struct tri_chain_args {
   /* RoPE, in place: q [T, nq, hd], k [T, nk, hd], head stride hd */
   void *q;         int64_t q_ts;
   void *k;         int64_t k_ts;
-  const int32_t *pos;                  /* [T]                                 */
+  const void *pos;                     /* [T] int32 (int64 if rope_ext says)  */
   /* SwiGLU over [T, I] */
   const void *gate; int64_t g_rs;
   const void *up;   int64_t u_rs;
@@ -137,6 +185,8 @@ typedef struct tri_chain_args {
   const void *k_norm_w;
   float qk_eps;
   int32_t reserved;    /* padding; ignored */
+  /* optional RoPE variant (NULL: plain rotate-half over hd, int32 positions) */
+  const tri_rope_ext *rope_ext;
 } tri_chain_args;
 
 /* ---- cache ---------------------------------------------------------------- */
@@ -199,6 +249,22 @@ tri_status tri_qk_norm_rope(tri_cache *cache, tri_dtype dtype,
                             int32_t nq, int32_t nk, int32_t hd, float base,
                             const void *q_w, const void *k_w, float eps, void *stream);
 
+/* RoPE with the variants of tri_rope_ext (ext may be NULL), optionally
+ * after the per-head QK-RMSNorm of tri_qk_norm_rope (q_w non-NULL; the norm
+ * covers all hd elements of a head, including those past rotary_dim). With
+ * ext == NULL and q_w == NULL this is tri_rope_qk; with ext == NULL and q_w
+ * set it is tri_qk_norm_rope (same keys, same versions). pos points to int32
+ * or int64 positions as ext->pos_int64 says. Validation order: head_dim and
+ * head counts; the ext fields; pointers and their alignment; strides; the
+ * angle source (cache, or base and scaling parameters); the head-norm
+ * weights and eps. */
+tri_status tri_rope_qk_ext(tri_cache *cache, tri_dtype dtype,
+                           void *q, int64_t q_ts, void *k, int64_t k_ts,
+                           const void *pos, int64_t T,
+                           int32_t nq, int32_t nk, int32_t hd, float base,
+                           const tri_rope_ext *ext,
+                           const void *q_w, const void *k_w, float eps, void *stream);
+
 /* SwiGLU: out = g / (1 + exp(-g)) * u over [T, I] (`silu` is in the paper's
  * kernel suite, Sec. 4.1). out may alias gate or up exactly. */
 tri_status tri_swiglu(tri_cache *cache, tri_dtype dtype,
@@ -206,7 +272,8 @@ tri_status tri_swiglu(tri_cache *cache, tri_dtype dtype,
                       void *out, int64_t o_rs, int64_t T, int64_t I, void *stream);
 
 /* The decode chain: residual+RMSNorm, RoPE-QK (or QK-RMSNorm + RoPE when
- * q_norm_w is set) and SwiGLU of one decode step, on disjoint operands
+ * q_norm_w is set; with the variant of rope_ext when set) and SwiGLU of one
+ * decode step, on disjoint operands
  * (overlap between the three ops is undefined). When
  * every tensor is 16-byte aligned and contiguous this is ONE launch of a
  * fused kernel whose workgroups take the three roles by blockIdx range;
@@ -237,8 +304,8 @@ tri_status tri_spec_version_info(const tri_cache *cache, uint32_t index,
                                  tri_version_info *out);
 
 /* Copy version `index`'s host copy of its constants (RoPE inverse
- * frequencies, hd/2 floats; none for other ops) into out[0..cap); *n gets
- * the count. */
+ * frequencies, rotary_dim/2 floats; none for other ops or with a cos/sin
+ * cache) into out[0..cap); *n gets the count. */
 tri_status tri_spec_version_constants(const tri_cache *cache, uint32_t index,
                                       float *out, uint32_t cap, uint32_t *n);
 

@@ -13,8 +13,10 @@ What it models
 * Guards are the ones a specialization of these ops depends on: dtype,
   hidden / intermediate sizes, head_dim and head counts, a token-count
   bucket, 16-byte alignment, contiguity, whether the RoPE step carries the
-  per-head QK RMSNorm, and the RoPE base (a captured constant of the
-  version, as source-visible constants are in Sec. 3.3).
+  per-head QK RMSNorm, the RoPE variant (rotary dim, pairing, position
+  width, angle source, frequency scaling and its parameters) and the RoPE
+  base (captured constants of the version, as source-visible constants are
+  in Sec. 3.3).
 
 Guards are equality tests on a packed key, so two versions can never both
 match and "first match in creation order" is the unique match.
@@ -45,7 +47,9 @@ RN_SCALAR = 10
 RN_WAVE = {1: 11, 2: 12}
 RN_BLOCK = {1: 13, 2: 14, 4: 15, 8: 16, 16: 17}
 RN_LOOP = 18
-ROPE_SCALAR, ROPE_VEC, ROPE_QKN_SCALAR, ROPE_QKN_VEC = 30, 31, 33, 34
+ROPE_SCALAR, ROPE_VEC, ROPE_VEC_I, ROPE_QKN_SCALAR, ROPE_QKN_VEC, ROPE_QKN_VEC_I = \
+    30, 31, 32, 33, 34, 35
+ROPE_VEC_ROLES = (ROPE_VEC, ROPE_VEC_I, ROPE_QKN_VEC, ROPE_QKN_VEC_I)
 SW_SCALAR, SW_FLAT, SW_FLAT_NT, SW_ROWS, SW_FLAT_U4_NT = 40, 41, 42, 43, 44
 CH_FUSED, CH_SEQ = 50, 51
 DECODE_BUCKET_MAX = 6       # buckets up to here are decode sized
@@ -63,6 +67,12 @@ FLAG_AUTO_INSTALL = 1
 
 ALIGN, CONTIG = 1, 2       # per-op guard flag bits
 CHAIN_QK_NORM = 0x40       # chain key flag: the RoPE step has the QK RMSNorm
+# RoPE variant bits (key word 3, above the 16-bit rotary dim)
+ROPE_INTERLEAVED, ROPE_POS64, ROPE_CACHE = 1, 2, 4
+SCALING_NONE, SCALING_LLAMA3 = 0, 1
+PLAIN_EXT = dict(rotary_dim=0, interleaved=0, pos_int64=0, scaling=SCALING_NONE, factor=0.0,
+                 low_freq_factor=0.0, high_freq_factor=0.0, original_max_pos=0, cos_sin=None,
+                 cos_sin_len=0)
 
 
 def elem_size(dtype: int) -> int:
@@ -125,14 +135,22 @@ def rn_role(dtype: int, H: int, flags: int, T: int) -> Tuple[int, int]:
     return RN_LOOP, T
 
 
-def rope_role(dtype: int, hd: int, flags: int, T: int,
-              qk_norm: bool = False) -> Tuple[int, int]:
-    """Vector path when 16-byte aligned and each half-head is a power-of-two
-    number of 16-byte vectors; the QK-norm variants follow the same rule."""
+def rope_role(dtype: int, hd: int, flags: int, T: int, qk_norm: bool = False,
+              rd: Optional[int] = None, interleaved: bool = False) -> Tuple[int, int]:
+    """Vector path when 16-byte aligned and the rotated span of a head (rd/2
+    elements per half for rotate-half pairs, rd for GPT-J pairs) is a
+    power-of-two number of 16-byte vectors; with the QK norm the vector path
+    also needs rd == hd and at most 64 vectors in that span."""
+    rd = hd if rd is None else rd
     v = 16 // elem_size(dtype)
-    half = hd // 2
-    if not (flags & ALIGN) or half % v or not is_pow2(half // v):
+    span = rd if interleaved else rd // 2
+    vec = bool(flags & ALIGN) and span % v == 0 and is_pow2(span // v)
+    if qk_norm:
+        vec = vec and rd == hd and span // v <= 64
+    if not vec:
         return (ROPE_QKN_SCALAR if qk_norm else ROPE_SCALAR), T
+    if interleaved:
+        return (ROPE_QKN_VEC_I if qk_norm else ROPE_VEC_I), T
     return (ROPE_QKN_VEC if qk_norm else ROPE_VEC), T
 
 
@@ -167,6 +185,7 @@ class Call:
     eps: float = 1e-6
     base: float = 10000.0
     qk_eps: float = 1e-6     # chain only: epsilon of the QK RMSNorm
+    ext: Optional[dict] = None   # RoPE variant (keys of PLAIN_EXT); None = plain
     # addresses (integers) and strides in elements; None = null pointer
     ptr: Dict[str, Optional[int]] = dataclasses.field(default_factory=dict)
     stride: Dict[str, int] = dataclasses.field(default_factory=dict)
@@ -181,7 +200,7 @@ class Record:
     n_launches: int = 0
     roles: Tuple[int, int, int] = (0, 0, 0)
     launch: Tuple[Tuple[int, int, int], ...] = ((0, 0, 0), (0, 0, 0), (0, 0, 0))
-    key: Tuple[int, int, int] = (0, 0, 0)
+    key: Tuple[int, ...] = (0, 0, 0, 0, 0, 0)
 
     def as_tuple(self):
         return (self.op, self.status, self.version, self.variant, self.n_launches,
@@ -218,7 +237,17 @@ def _validate_rn(c: Call, names, strides) -> Optional[int]:
     return None
 
 
+def rope_ext_of(c: Call) -> dict:
+    x = dict(PLAIN_EXT)
+    if c.ext:
+        x.update(c.ext)
+    return x
+
+
 def _validate_rope(c: Call) -> Optional[int]:
+    """Head dim and head counts; the variant fields; pointers and their
+    alignment; strides; the angle source."""
+    x = rope_ext_of(c)
     if c.hd < 2 or c.hd % 2:
         return E_INVALID
     if c.hd > HD_MAX:
@@ -227,11 +256,18 @@ def _validate_rope(c: Call) -> Optional[int]:
         return E_INVALID
     if c.nq > HEADS_MAX or c.nk > HEADS_MAX:
         return E_UNSUPPORTED
+    rd = x["rotary_dim"]
+    if rd != 0 and (rd < 2 or rd % 2 or rd > c.hd):
+        return E_INVALID
+    if x["interleaved"] not in (0, 1) or x["pos_int64"] not in (0, 1):
+        return E_INVALID
+    if x["scaling"] not in (SCALING_NONE, SCALING_LLAMA3):
+        return E_INVALID
     if c.ptr.get("q") is None or c.ptr.get("pos") is None:
         return E_INVALID
     if c.nk > 0 and c.ptr.get("k") is None:
         return E_INVALID
-    if c.ptr["pos"] % 4:
+    if c.ptr["pos"] % (8 if x["pos_int64"] else 4):
         return E_INVALID
     es = elem_size(c.dtype)
     if c.ptr["q"] % es or (c.nk > 0 and c.ptr["k"] % es):
@@ -240,9 +276,21 @@ def _validate_rope(c: Call) -> Optional[int]:
         return E_INVALID
     if c.nk > 0 and c.stride["k"] < c.nk * c.hd:
         return E_INVALID
+    if x["cos_sin"] is not None:
+        if x["cos_sin"] % 4 or x["cos_sin_len"] < 1 or x["scaling"] != SCALING_NONE:
+            return E_INVALID
+        return None
     base = _f32(c.base)
     if not _finite(base) or base <= 1.0:
         return E_INVALID
+    if x["scaling"] == SCALING_LLAMA3:
+        f, lo, hi = _f32(x["factor"]), _f32(x["low_freq_factor"]), _f32(x["high_freq_factor"])
+        if not _finite(f) or f <= 0 or not _finite(lo) or lo <= 0:
+            return E_INVALID
+        if not _finite(hi) or hi <= lo:
+            return E_INVALID
+        if x["original_max_pos"] < 1:
+            return E_INVALID
     return None
 
 
@@ -366,25 +414,48 @@ def op_flags(c: Call) -> int:
             | (sw_flags(c) << 4) | (CHAIN_QK_NORM if qkn else 0))
 
 
-def make_key(c: Call) -> Tuple[int, int, int]:
+def make_key(c: Call) -> Tuple[int, ...]:
+    """Six 64-bit words:
+    k0 op | dtype << 8 | bucket << 16 | flags << 24 | base bits << 32;
+    k1 H | I << 32;  k2 hd | nq << 16 | nk << 32;
+    k3 rotary dim | variant bits << 16 | scaling << 24 | original_max_pos << 32;
+    k4 factor bits | low_freq_factor bits << 32;  k5 high_freq_factor bits.
+    Unused fields are zero; with a cos/sin cache the base and scaling fields
+    are unused."""
     b = bucket(c.T)
     flags = op_flags(c)
-    base_bits = f32_bits(c.base) if c.op in ROPE_OPS else 0
     H = c.H if c.op in (OP_RMSNORM, OP_RES_RMSNORM, OP_CHAIN) else 0
     I = c.I if c.op in (OP_SWIGLU, OP_CHAIN) else 0
     hd, nq, nk = (c.hd, c.nq, c.nk) if c.op in ROPE_OPS else (0, 0, 0)
+    base_bits, k3, k4, k5 = 0, 0, 0, 0
+    if c.op in ROPE_OPS:
+        x = rope_ext_of(c)
+        rd = x["rotary_dim"] or c.hd
+        bits = ((ROPE_INTERLEAVED if x["interleaved"] else 0)
+                | (ROPE_POS64 if x["pos_int64"] else 0)
+                | (ROPE_CACHE if x["cos_sin"] is not None else 0))
+        k3 = rd | (bits << 16)
+        if x["cos_sin"] is None:
+            base_bits = f32_bits(c.base)
+            if x["scaling"] == SCALING_LLAMA3:
+                k3 |= (SCALING_LLAMA3 << 24) | ((x["original_max_pos"] & 0xFFFFFFFF) << 32)
+                k4 = f32_bits(x["factor"]) | (f32_bits(x["low_freq_factor"]) << 32)
+                k5 = f32_bits(x["high_freq_factor"])
     k0 = c.op | (c.dtype << 8) | (b << 16) | (flags << 24) | (base_bits << 32)
     k1 = H | (I << 32)
     k2 = hd | (nq << 16) | (nk << 32)
-    return (k0, k1, k2)
+    return (k0, k1, k2, k3, k4, k5)
 
 
 def unpack_key(key):
-    k0, k1, k2 = key
+    k0, k1, k2, k3, k4, k5 = key
     return dict(op=k0 & 0xFF, dtype=(k0 >> 8) & 0xFF, bucket=(k0 >> 16) & 0xFF,
                 flags=(k0 >> 24) & 0xFF, base_bits=k0 >> 32,
                 H=k1 & 0xFFFFFFFF, I=k1 >> 32,
-                hd=k2 & 0xFFFF, nq=(k2 >> 16) & 0xFFFF, nk=(k2 >> 32) & 0xFFFF)
+                hd=k2 & 0xFFFF, nq=(k2 >> 16) & 0xFFFF, nk=(k2 >> 32) & 0xFFFF,
+                rd=k3 & 0xFFFF, rope_bits=(k3 >> 16) & 0xFF, scaling=(k3 >> 24) & 0xFF,
+                orig_max=k3 >> 32, factor_bits=k4 & 0xFFFFFFFF, low_bits=k4 >> 32,
+                high_bits=k5 & 0xFFFFFFFF)
 
 
 # ---- install policy: key -> variants, and per-call launch geometry ---------------
@@ -395,19 +466,20 @@ def plan(key, T: int):
     if op in (OP_RMSNORM, OP_RES_RMSNORM):
         v, g = rn_role(dt, f["H"], fl, T)
         return v, (0, 0, 0), [(v, g, BLOCK)]
+    inter = bool(f["rope_bits"] & ROPE_INTERLEAVED)
     if op in (OP_ROPE_QK, OP_QK_NORM_ROPE):
-        v, g = rope_role(dt, f["hd"], fl, T, op == OP_QK_NORM_ROPE)
+        v, g = rope_role(dt, f["hd"], fl, T, op == OP_QK_NORM_ROPE, f["rd"], inter)
         return v, (0, 0, 0), [(v, g, BLOCK)]
     if op == OP_SWIGLU:
         v, g = sw_role(dt, f["I"], fl, b, T)
         return v, (0, 0, 0), [(v, g, BLOCK)]
     rn = rn_role(dt, f["H"], fl & 3, T)
-    ro = rope_role(dt, f["hd"], (fl >> 2) & 3, T, bool(fl & CHAIN_QK_NORM))
+    ro = rope_role(dt, f["hd"], (fl >> 2) & 3, T, bool(fl & CHAIN_QK_NORM), f["rd"], inter)
     sw = sw_role(dt, f["I"], (fl >> 4) & 3, b, T, in_chain=True)
     roles = (rn[0], ro[0], sw[0])
     fused = ((fl & 0x3F) == 0x3F
              and (rn[0] in RN_WAVE.values() or rn[0] in RN_BLOCK.values())
-             and ro[0] in (ROPE_VEC, ROPE_QKN_VEC)
+             and ro[0] in ROPE_VEC_ROLES
              and sw[0] in (SW_FLAT, SW_FLAT_U4_NT))
     if fused:
         return CH_FUSED, roles, [(CH_FUSED, rn[1] + ro[1] + sw[1], BLOCK)]
@@ -434,9 +506,9 @@ class SpecCacheModel:
             raise ValueError("invalid cache parameters")
         self.capacity = capacity or DEFAULT_CAPACITY
         self.flags = flags
-        self.versions: List[Tuple[int, int, int]] = []
+        self.versions: List[Tuple[int, ...]] = []
         self.version_hits: List[int] = []
-        self.last_miss: Optional[Tuple[Tuple[int, int, int], int]] = None
+        self.last_miss: Optional[Tuple[Tuple[int, ...], int]] = None
         self.stats = Stats()
         self.last = Record()
         # launch_fails: set of global launch ordinals (0-based) that fail,

@@ -20,11 +20,12 @@ import torch
 
 from . import _lib as L
 from ._lib import (AUTO_INSTALL, BF16, E_FULL, E_INVALID, E_LAUNCH, E_NOMEM, E_RUNTIME,
-                   E_UNSUPPORTED, F32, MISS, OK, ChainArgs, Selection, Stats, VersionInfo)
+                   E_UNSUPPORTED, F32, MISS, OK, ROPE_SCALING_LLAMA3, ROPE_SCALING_NONE,
+                   ChainArgs, RopeExt, Selection, Stats, VersionInfo)
 
-__all__ = ["SpecCache", "TriError", "dtype_code", "Selection", "Stats", "ChainArgs",
-           "OK", "MISS", "E_INVALID", "E_UNSUPPORTED", "E_FULL", "E_NOMEM", "E_LAUNCH",
-           "E_RUNTIME", "F32", "BF16", "AUTO_INSTALL"]
+__all__ = ["SpecCache", "TriError", "dtype_code", "rope_ext", "Selection", "Stats",
+           "ChainArgs", "RopeExt", "OK", "MISS", "E_INVALID", "E_UNSUPPORTED", "E_FULL",
+           "E_NOMEM", "E_LAUNCH", "E_RUNTIME", "F32", "BF16", "AUTO_INSTALL"]
 
 _dll = L.load()
 
@@ -42,6 +43,35 @@ def dtype_code(dt: torch.dtype) -> int:
     if dt == torch.bfloat16:
         return BF16
     raise TypeError(f"unsupported dtype {dt} (float32 or bfloat16)")
+
+
+def rope_ext(rotary_dim: int = 0, interleaved: bool = False, pos_int64: bool = False,
+             scaling: Optional[dict] = None, cos_sin: Optional[torch.Tensor] = None) -> RopeExt:
+    """A tri_rope_ext: rotary_dim (0 = head_dim), GPT-J pairs, int64 positions,
+    Llama-3 scaling (dict with factor, low_freq_factor, high_freq_factor,
+    original_max_pos) or a float32 cos/sin cache [n, rotary_dim]."""
+    x = RopeExt()
+    x.rotary_dim = rotary_dim
+    x.interleaved = int(interleaved)
+    x.pos_int64 = int(pos_int64)
+    if scaling is not None:
+        x.scaling = ROPE_SCALING_LLAMA3
+        x.factor = scaling["factor"]
+        x.low_freq_factor = scaling["low_freq_factor"]
+        x.high_freq_factor = scaling["high_freq_factor"]
+        x.original_max_pos = scaling["original_max_pos"]
+    if cos_sin is not None:
+        if cos_sin.dtype != torch.float32 or cos_sin.dim() != 2 or not cos_sin.is_contiguous():
+            raise ValueError("cos_sin: contiguous float32 [n, rotary_dim] expected")
+        x.cos_sin = cos_sin.data_ptr()
+        x.cos_sin_len = cos_sin.shape[0]
+    return x
+
+
+def _pos_check(pos: torch.Tensor, ext: Optional[RopeExt]) -> None:
+    want = torch.int64 if ext is not None and ext.pos_int64 else torch.int32
+    if pos.dtype != want:
+        raise TypeError(f"pos must be {want}")
 
 
 def _stream_ptr(stream) -> Optional[int]:
@@ -163,6 +193,23 @@ class SpecCache:
                    q_w.data_ptr(), kw, eps, _stream_ptr(stream))
         return q, k
 
+    def rope(self, q, k, pos, base: float = 10000.0, ext: Optional[RopeExt] = None, q_w=None,
+             k_w=None, eps: float = 1e-6, stream=None):
+        """In-place RoPE of q [T, nq, hd] and k [T, nk, hd] (k may be None)
+        with an optional variant (`rope_ext(...)`) and, with q_w, the per-head
+        QK RMSNorm first (tri_rope_qk_ext)."""
+        T, nq, hd = q.shape
+        nk = 0 if k is None else k.shape[1]
+        kp = 0 if k is None or nk == 0 else k.data_ptr()
+        kts = 0 if k is None or nk == 0 else _tokens(k, "k")
+        _pos_check(pos, ext)
+        self._call("tri_rope_qk_ext", _dll.tri_rope_qk_ext, dtype_code(q.dtype), q.data_ptr(),
+                   _tokens(q, "q"), kp, kts, pos.data_ptr(), T, nq, nk, hd, base,
+                   C.byref(ext) if ext is not None else None,
+                   0 if q_w is None else q_w.data_ptr(), 0 if k_w is None else k_w.data_ptr(),
+                   eps, _stream_ptr(stream))
+        return q, k
+
     def swiglu(self, gate, up, out=None, stream=None) -> torch.Tensor:
         o = torch.empty_like(gate) if out is None else out
         T, I = gate.shape
@@ -173,10 +220,11 @@ class SpecCache:
 
     def chain_args(self, x, residual, w, q, k, pos, gate, up, eps=1e-6, base=10000.0,
                    y=None, residual_out=None, out=None, q_norm_w=None, k_norm_w=None,
-                   qk_eps=None) -> Tuple[ChainArgs, tuple]:
+                   qk_eps=None, rope: Optional[RopeExt] = None) -> Tuple[ChainArgs, tuple]:
         """Build the tri_chain_args struct once (outputs allocated if absent).
         With q_norm_w (and k_norm_w) the RoPE step is QK-RMSNorm + RoPE with
-        epsilon qk_eps (default: eps)."""
+        epsilon qk_eps (default: eps); `rope` selects a RoPE variant."""
+        _pos_check(pos, rope)
         y = torch.empty_like(x) if y is None else y
         ro = torch.empty_like(residual) if residual_out is None else residual_out
         o = torch.empty_like(gate) if out is None else out
@@ -203,6 +251,9 @@ class SpecCache:
             a.q_norm_w = q_norm_w.data_ptr()
             a.k_norm_w = 0 if k_norm_w is None else k_norm_w.data_ptr()
             a.qk_eps = eps if qk_eps is None else qk_eps
+        if rope is not None:
+            a.rope_ext = C.pointer(rope)
+            a._rope = rope          # keeps the variant alive as long as the args
         return a, (y, ro, o)
 
     def decode_chain_args(self, args: ChainArgs, stream=None) -> None:
@@ -211,11 +262,11 @@ class SpecCache:
 
     def decode_chain(self, x, residual, w, q, k, pos, gate, up, eps=1e-6, base=10000.0,
                      y=None, residual_out=None, out=None, stream=None, q_norm_w=None,
-                     k_norm_w=None, qk_eps=None):
+                     k_norm_w=None, qk_eps=None, rope: Optional[RopeExt] = None):
         """Residual+RMSNorm, in-place (QK-RMSNorm +) RoPE of q/k and SwiGLU in
         one entry call. Returns (y, residual_out, out)."""
         a, outs = self.chain_args(x, residual, w, q, k, pos, gate, up, eps, base, y,
-                                  residual_out, out, q_norm_w, k_norm_w, qk_eps)
+                                  residual_out, out, q_norm_w, k_norm_w, qk_eps, rope)
         self.decode_chain_args(a, stream)
         return outs
 

@@ -16,8 +16,10 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtri.so")
 OK, MISS = 0, 1
 E_INVALID, E_UNSUPPORTED, E_FULL, E_NOMEM, E_LAUNCH, E_RUNTIME = -1, -2, -3, -4, -5, -6
 F32, BF16 = 0, 1
-OP_RMSNORM, OP_RES_RMSNORM, OP_ROPE_QK, OP_SWIGLU, OP_CHAIN = 1, 2, 3, 4, 5
+OP_RMSNORM, OP_RES_RMSNORM, OP_ROPE_QK, OP_SWIGLU, OP_CHAIN, OP_QK_NORM_ROPE = 1, 2, 3, 4, 5, 6
 AUTO_INSTALL = 1
+KEY_WORDS = 6
+ROPE_SCALING_NONE, ROPE_SCALING_LLAMA3 = 0, 1
 
 
 class LaunchRec(C.Structure):
@@ -28,7 +30,7 @@ class Selection(C.Structure):
     _fields_ = [("op", C.c_int32), ("status", C.c_int32), ("version", C.c_int32),
                 ("variant", C.c_int32), ("n_launches", C.c_int32),
                 ("roles", C.c_int32 * 3), ("launch", LaunchRec * 3),
-                ("key", C.c_uint64 * 3)]
+                ("key", C.c_uint64 * KEY_WORDS)]
 
     def as_tuple(self):
         return (self.op, self.status, self.version, self.variant, self.n_launches,
@@ -47,8 +49,16 @@ class Stats(C.Structure):
 
 
 class VersionInfo(C.Structure):
-    _fields_ = [("key", C.c_uint64 * 3), ("variant", C.c_int32), ("roles", C.c_int32 * 3),
+    _fields_ = [("key", C.c_uint64 * KEY_WORDS), ("variant", C.c_int32), ("roles", C.c_int32 * 3),
                 ("hits", C.c_uint64)]
+
+
+class RopeExt(C.Structure):
+    _fields_ = [("rotary_dim", C.c_int32), ("interleaved", C.c_int32),
+                ("pos_int64", C.c_int32), ("scaling", C.c_int32),
+                ("factor", C.c_float), ("low_freq_factor", C.c_float),
+                ("high_freq_factor", C.c_float), ("original_max_pos", C.c_int32),
+                ("cos_sin", C.c_void_p), ("cos_sin_len", C.c_int64)]
 
 
 class ChainArgs(C.Structure):
@@ -67,10 +77,11 @@ class ChainArgs(C.Structure):
                 ("up", C.c_void_p), ("u_rs", C.c_int64),
                 ("out", C.c_void_p), ("o_rs", C.c_int64),
                 ("q_norm_w", C.c_void_p), ("k_norm_w", C.c_void_p),
-                ("qk_eps", C.c_float), ("reserved", C.c_int32)]
+                ("qk_eps", C.c_float), ("reserved", C.c_int32),
+                ("rope_ext", C.POINTER(RopeExt))]
 
 
-assert C.sizeof(Selection) == 96 and C.sizeof(ChainArgs) == 232
+assert C.sizeof(Selection) == 120 and C.sizeof(ChainArgs) == 240 and C.sizeof(RopeExt) == 48
 
 _P, _I64, _I32, _F, _U32 = C.c_void_p, C.c_int64, C.c_int32, C.c_float, C.c_uint32
 
@@ -82,6 +93,8 @@ SIGNATURES = {
                                        _I64, _I64, _F, _P]),
     "tri_rope_qk": (C.c_int, [_P, C.c_int, _P, _I64, _P, _I64, _P, _I64, _I32, _I32, _I32, _F,
                               _P]),
+    "tri_rope_qk_ext": (C.c_int, [_P, C.c_int, _P, _I64, _P, _I64, _P, _I64, _I32, _I32, _I32,
+                                  _F, C.POINTER(RopeExt), _P, _P, _F, _P]),
     "tri_qk_norm_rope": (C.c_int, [_P, C.c_int, _P, _I64, _P, _I64, _P, _I64, _I32, _I32, _I32,
                                    _F, _P, _P, _F, _P]),
     "tri_swiglu": (C.c_int, [_P, C.c_int, _P, _I64, _P, _I64, _P, _I64, _I64, _I64, _P]),

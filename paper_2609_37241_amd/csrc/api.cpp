@@ -60,18 +60,42 @@ inline int check_norm(uint64_t es, int64_t H, const void *const *ptrs, int np,
   return kGo;
 }
 
+// The plain rotation: rotate-half over the whole head, int32 positions,
+// computed angles without scaling.
+const tri_rope_ext kRopePlain = {0, 0, 0, TRI_ROPE_SCALING_NONE, 0.0f, 0.0f, 0.0f, 0, nullptr, 0};
+
+// RoPE arguments in the documented order: head_dim and head counts; the
+// variant fields; pointers and their alignment; strides; the angle source.
 inline int check_rope(uint64_t es, const void *q, int64_t q_ts, const void *k, int64_t k_ts,
-                      const int32_t *pos, int32_t nq, int32_t nk, int32_t hd, float base) {
+                      const void *pos, int32_t nq, int32_t nk, int32_t hd, float base,
+                      const tri_rope_ext &x) {
   if (hd < 2 || (hd & 1)) return TRI_E_INVALID;
   if (hd > kHdMax) return TRI_E_UNSUPPORTED;
   if (nq < 1 || nk < 0) return TRI_E_INVALID;
   if (nq > kHeadsMax || nk > kHeadsMax) return TRI_E_UNSUPPORTED;
+  if (x.rotary_dim != 0 && (x.rotary_dim < 2 || (x.rotary_dim & 1) || x.rotary_dim > hd))
+    return TRI_E_INVALID;
+  if ((x.interleaved | 1) != 1 || (x.pos_int64 | 1) != 1) return TRI_E_INVALID;
+  if (x.scaling != TRI_ROPE_SCALING_NONE && x.scaling != TRI_ROPE_SCALING_LLAMA3)
+    return TRI_E_INVALID;
   if (!q || !pos || (nk > 0 && !k)) return TRI_E_INVALID;
-  if (addr(pos) % 4) return TRI_E_INVALID;
+  if (addr(pos) % (x.pos_int64 ? 8 : 4)) return TRI_E_INVALID;
   if (addr(q) % es || (nk > 0 && addr(k) % es)) return TRI_E_INVALID;
   if (q_ts < int64_t(nq) * hd) return TRI_E_INVALID;
   if (nk > 0 && k_ts < int64_t(nk) * hd) return TRI_E_INVALID;
+  if (x.cos_sin) {
+    if (addr(x.cos_sin) % 4 || x.cos_sin_len < 1 || x.scaling != TRI_ROPE_SCALING_NONE)
+      return TRI_E_INVALID;
+    return kGo;
+  }
   if (!isfinite(base) || base <= 1.0f) return TRI_E_INVALID;
+  if (x.scaling == TRI_ROPE_SCALING_LLAMA3) {
+    if (!isfinite(x.factor) || x.factor <= 0.0f) return TRI_E_INVALID;
+    if (!isfinite(x.low_freq_factor) || x.low_freq_factor <= 0.0f) return TRI_E_INVALID;
+    if (!isfinite(x.high_freq_factor) || x.high_freq_factor <= x.low_freq_factor)
+      return TRI_E_INVALID;
+    if (x.original_max_pos < 1) return TRI_E_INVALID;
+  }
   return kGo;
 }
 
@@ -147,7 +171,35 @@ inline Key make_key(uint32_t op, uint32_t dtype, int64_t T, unsigned flags, uint
          (uint64_t(flags) << 24) | (uint64_t(base_bits) << 32);
   k.k1 = H | (I << 32);
   k.k2 = hd | (nq << 16) | (nk << 32);
+  k.k3 = k.k4 = k.k5 = 0;
   return k;
+}
+
+// The RoPE variant words of a key (k3..k5) and the base bits of k0. With a
+// cos/sin cache the base and scaling fields are unused and stay zero.
+inline void rope_key_words(Key &k, int32_t hd, float base, const tri_rope_ext &x) {
+  const uint64_t rd = uint64_t(x.rotary_dim ? x.rotary_dim : hd);
+  const uint64_t bits = (x.interleaved ? kRopeInterleaved : 0u) | (x.pos_int64 ? kRopePos64 : 0u) |
+                        (x.cos_sin ? kRopeCache : 0u);
+  k.k3 = rd | (bits << 16);
+  if (x.cos_sin) return;
+  k.k0 |= uint64_t(f32_bits(base)) << 32;
+  if (x.scaling == TRI_ROPE_SCALING_LLAMA3) {
+    k.k3 |= (uint64_t(TRI_ROPE_SCALING_LLAMA3) << 24) | (uint64_t(uint32_t(x.original_max_pos)) << 32);
+    k.k4 = uint64_t(f32_bits(x.factor)) | (uint64_t(f32_bits(x.low_freq_factor)) << 32);
+    k.k5 = uint64_t(f32_bits(x.high_freq_factor));
+  }
+}
+
+// Kernel arguments of the RoPE role (q_w null: no head norm).
+inline RopeArgs rope_args(const Version &v, void *q, int64_t q_ts, void *kp, int64_t k_ts,
+                          const void *pos, int64_t T, int32_t nq, int32_t nk, int32_t hd,
+                          const tri_rope_ext &x, const void *q_w, const void *k_w, float eps) {
+  const uint32_t mode = (x.interleaved ? kRopeInterleaved : 0u) |
+                        (x.pos_int64 ? kRopePos64 : 0u) | (x.cos_sin ? kRopeCache : 0u);
+  return RopeArgs{q, nk > 0 ? kp : nullptr, pos, v.d_consts, q_w, (q_w && nk > 0) ? k_w : nullptr,
+                  x.cos_sin, q_ts, k_ts, T, x.cos_sin ? x.cos_sin_len : 0, nq, nk, hd,
+                  x.rotary_dim ? x.rotary_dim : hd, q_w ? eps : 0.0f, mode};
 }
 
 // ---- lookup and launch bookkeeping -----------------------------------------------------
@@ -168,9 +220,7 @@ inline int lookup(tri_cache *c, uint32_t op, const Key &k, int64_t T, int32_t *v
   memset(&r, 0, sizeof r);
   r.op = int32_t(op);
   r.version = -1;
-  r.key[0] = k.k0;
-  r.key[1] = k.k1;
-  r.key[2] = k.k2;
+  key_words(k, r.key);
   if (!(c->flags & TRI_CACHE_AUTO_INSTALL)) {
     r.status = TRI_MISS;
     return TRI_MISS;
@@ -197,9 +247,7 @@ inline void record(tri_cache *c, uint32_t op, const Version &v, int32_t vi, cons
   r.roles[1] = v.plan.roles[1];
   r.roles[2] = v.plan.roles[2];
   for (int i = 0; i < 3; ++i) r.launch[i] = i < n ? l[i] : tri_launch_rec{0, 0, 0};
-  r.key[0] = k.k0;
-  r.key[1] = k.k1;
-  r.key[2] = k.k2;
+  key_words(k, r.key);
 }
 
 inline tri_status finish(tri_cache *c, Version &v, bool auto_inst, int rc) {
@@ -215,6 +263,45 @@ inline tri_status finish(tri_cache *c, Version &v, bool auto_inst, int rc) {
 }
 
 inline int64_t vec_elems(uint32_t dtype) { return dtype == TRI_F32 ? 4 : 8; }
+
+// RoPE (op 3) or QK-RMSNorm + RoPE (op 6; the head-norm weights are then
+// required) with an optional variant.
+tri_status rope_entry(tri_cache *c, uint32_t op, int32_t dtype, void *q, int64_t q_ts, void *kp,
+                      int64_t k_ts, const void *pos, int64_t T, int32_t nq, int32_t nk,
+                      int32_t hd, float base, const tri_rope_ext *ext, const void *q_w,
+                      const void *k_w, float eps, void *stream) {
+  if (!c) return TRI_E_INVALID;
+  c->stats.calls++;
+  int st = check_common(dtype, T);
+  if (st != kGo) return finish_early(c, op, st);
+  const uint64_t es = es_of(uint32_t(dtype));
+  const tri_rope_ext &x = ext ? *ext : kRopePlain;
+  st = check_rope(es, q, q_ts, kp, k_ts, pos, nq, nk, hd, base, x);
+  if (st != kGo) return finish_early(c, op, st);
+  const bool qkn = op == TRI_OP_QK_NORM_ROPE;
+  if (qkn) {
+    st = check_qkn(es, q_w, k_w, nk, eps);
+    if (st != kGo) return finish_early(c, op, st);
+  }
+
+  Key k = make_key(op, uint32_t(dtype), T,
+                   rope_flags(es, q, q_ts, kp, k_ts, nq, nk, hd, qkn ? q_w : nullptr, k_w), 0, 0,
+                   0, uint64_t(hd), uint64_t(nq), uint64_t(nk));
+  rope_key_words(k, hd, base, x);
+  int32_t vi;
+  bool auto_inst = false;
+  st = lookup(c, op, k, T, &vi, &auto_inst);
+  if (st != TRI_OK) return tri_status(st);
+  Version &v = c->versions[vi];
+
+  const RopeArgs a =
+      rope_args(v, q, q_ts, kp, k_ts, pos, T, nq, nk, hd, x, qkn ? q_w : nullptr, k_w, eps);
+  const tri_launch_rec l{v.plan.kvariant[0], role_grid(v.plan.kvariant[0], uint32_t(dtype), T, 0),
+                         kBlock};
+  const int rc = be_launch(v.fn[0], l.grid_x, kBlock, &a, sizeof a, stream);
+  record(c, op, v, vi, k, 1, &l, rc ? TRI_E_LAUNCH : TRI_OK);
+  return finish(c, v, auto_inst, rc);
+}
 
 }  // namespace
 
@@ -280,63 +367,27 @@ tri_status tri_residual_rmsnorm(tri_cache *c, tri_dtype dtype, const void *x, in
   return finish(c, v, auto_inst, rc);
 }
 
+tri_status tri_rope_qk_ext(tri_cache *c, tri_dtype dtype, void *q, int64_t q_ts, void *kp,
+                           int64_t k_ts, const void *pos, int64_t T, int32_t nq, int32_t nk,
+                           int32_t hd, float base, const tri_rope_ext *ext, const void *q_w,
+                           const void *k_w, float eps, void *stream) {
+  return rope_entry(c, q_w ? TRI_OP_QK_NORM_ROPE : TRI_OP_ROPE_QK, dtype, q, q_ts, kp, k_ts, pos,
+                    T, nq, nk, hd, base, ext, q_w, k_w, eps, stream);
+}
+
 tri_status tri_rope_qk(tri_cache *c, tri_dtype dtype, void *q, int64_t q_ts, void *kp,
                        int64_t k_ts, const int32_t *pos, int64_t T, int32_t nq, int32_t nk,
                        int32_t hd, float base, void *stream) {
-  if (!c) return TRI_E_INVALID;
-  const uint32_t op = TRI_OP_ROPE_QK;
-  c->stats.calls++;
-  int st = check_common(dtype, T);
-  if (st != kGo) return finish_early(c, op, st);
-  const uint64_t es = es_of(dtype);
-  st = check_rope(es, q, q_ts, kp, k_ts, pos, nq, nk, hd, base);
-  if (st != kGo) return finish_early(c, op, st);
-
-  const Key k = make_key(op, dtype, T, rope_flags(es, q, q_ts, kp, k_ts, nq, nk, hd),
-                         f32_bits(base), 0, 0, uint64_t(hd), uint64_t(nq), uint64_t(nk));
-  int32_t vi;
-  bool auto_inst = false;
-  st = lookup(c, op, k, T, &vi, &auto_inst);
-  if (st != TRI_OK) return tri_status(st);
-  Version &v = c->versions[vi];
-
-  RopeArgs a{q, nk > 0 ? kp : nullptr, pos, v.d_consts, nullptr, nullptr, q_ts, k_ts, T,
-             nq, nk, hd, 0.0f};
-  const tri_launch_rec l{v.plan.kvariant[0], role_grid(v.plan.kvariant[0], dtype, T, 0), kBlock};
-  const int rc = be_launch(v.fn[0], l.grid_x, kBlock, &a, sizeof a, stream);
-  record(c, op, v, vi, k, 1, &l, rc ? TRI_E_LAUNCH : TRI_OK);
-  return finish(c, v, auto_inst, rc);
+  return rope_entry(c, TRI_OP_ROPE_QK, dtype, q, q_ts, kp, k_ts, pos, T, nq, nk, hd, base,
+                    nullptr, nullptr, nullptr, 0.0f, stream);
 }
 
 tri_status tri_qk_norm_rope(tri_cache *c, tri_dtype dtype, void *q, int64_t q_ts, void *kp,
                             int64_t k_ts, const int32_t *pos, int64_t T, int32_t nq, int32_t nk,
                             int32_t hd, float base, const void *q_w, const void *k_w, float eps,
                             void *stream) {
-  if (!c) return TRI_E_INVALID;
-  const uint32_t op = TRI_OP_QK_NORM_ROPE;
-  c->stats.calls++;
-  int st = check_common(dtype, T);
-  if (st != kGo) return finish_early(c, op, st);
-  const uint64_t es = es_of(dtype);
-  st = check_rope(es, q, q_ts, kp, k_ts, pos, nq, nk, hd, base);
-  if (st != kGo) return finish_early(c, op, st);
-  st = check_qkn(es, q_w, k_w, nk, eps);
-  if (st != kGo) return finish_early(c, op, st);
-
-  const Key k = make_key(op, dtype, T, rope_flags(es, q, q_ts, kp, k_ts, nq, nk, hd, q_w, k_w),
-                         f32_bits(base), 0, 0, uint64_t(hd), uint64_t(nq), uint64_t(nk));
-  int32_t vi;
-  bool auto_inst = false;
-  st = lookup(c, op, k, T, &vi, &auto_inst);
-  if (st != TRI_OK) return tri_status(st);
-  Version &v = c->versions[vi];
-
-  RopeArgs a{q, nk > 0 ? kp : nullptr, pos, v.d_consts, q_w, nk > 0 ? k_w : nullptr, q_ts, k_ts,
-             T, nq, nk, hd, eps};
-  const tri_launch_rec l{v.plan.kvariant[0], role_grid(v.plan.kvariant[0], dtype, T, 0), kBlock};
-  const int rc = be_launch(v.fn[0], l.grid_x, kBlock, &a, sizeof a, stream);
-  record(c, op, v, vi, k, 1, &l, rc ? TRI_E_LAUNCH : TRI_OK);
-  return finish(c, v, auto_inst, rc);
+  return rope_entry(c, TRI_OP_QK_NORM_ROPE, dtype, q, q_ts, kp, k_ts, pos, T, nq, nk, hd, base,
+                    nullptr, q_w, k_w, eps, stream);
 }
 
 tri_status tri_swiglu(tri_cache *c, tri_dtype dtype, const void *gate, int64_t g_rs,
@@ -382,7 +433,8 @@ tri_status tri_decode_chain(tri_cache *c, const tri_chain_args *p, void *stream)
     st = check_norm(es, H, ptrs, 5, strides, 4, p->eps);
     if (st != kGo) return finish_early(c, op, st);
   }
-  st = check_rope(es, p->q, p->q_ts, p->k, p->k_ts, p->pos, p->nq, p->nk, p->hd, p->base);
+  const tri_rope_ext &x = p->rope_ext ? *p->rope_ext : kRopePlain;
+  st = check_rope(es, p->q, p->q_ts, p->k, p->k_ts, p->pos, p->nq, p->nk, p->hd, p->base, x);
   if (st != kGo) return finish_early(c, op, st);
   const bool qkn = p->q_norm_w != nullptr;
   if (qkn) {
@@ -399,8 +451,9 @@ tri_status tri_decode_chain(tri_cache *c, const tri_chain_args *p, void *stream)
                   qkn ? p->q_norm_w : nullptr, qkn ? p->k_norm_w : nullptr) << 2) |
       (sw_flags(es, p->gate, p->g_rs, p->up, p->u_rs, p->out, p->o_rs, I) << 4) |
       (qkn ? kChainQkNorm : 0u);
-  const Key k = make_key(op, uint32_t(dtype), T, fl, f32_bits(p->base), uint64_t(H), uint64_t(I),
-                         uint64_t(p->hd), uint64_t(p->nq), uint64_t(p->nk));
+  Key k = make_key(op, uint32_t(dtype), T, fl, 0, uint64_t(H), uint64_t(I), uint64_t(p->hd),
+                   uint64_t(p->nq), uint64_t(p->nk));
+  rope_key_words(k, p->hd, p->base, x);
   int32_t vi;
   bool auto_inst = false;
   st = lookup(c, op, k, T, &vi, &auto_inst);
@@ -409,9 +462,8 @@ tri_status tri_decode_chain(tri_cache *c, const tri_chain_args *p, void *stream)
 
   const RnArgs rn{p->x, p->res, p->w, p->y, p->res_out, p->x_rs, p->res_rs, p->y_rs, p->ro_rs,
                   T, int32_t(H), p->eps};
-  const RopeArgs ro{p->q, p->nk > 0 ? p->k : nullptr, p->pos, v.d_consts,
-                    qkn ? p->q_norm_w : nullptr, qkn && p->nk > 0 ? p->k_norm_w : nullptr,
-                    p->q_ts, p->k_ts, T, p->nq, p->nk, p->hd, qkn ? p->qk_eps : 0.0f};
+  const RopeArgs ro = rope_args(v, p->q, p->q_ts, p->k, p->k_ts, p->pos, T, p->nq, p->nk, p->hd,
+                                x, qkn ? p->q_norm_w : nullptr, p->k_norm_w, p->qk_eps);
   const SwArgs sw{p->gate, p->up, p->out, p->g_rs, p->u_rs, p->o_rs, T, I,
                   (T * I) / vec_elems(uint32_t(dtype)), T * I};
   const uint32_t g0 = role_grid(v.plan.roles[0], uint32_t(dtype), T, I);

@@ -29,7 +29,7 @@ int be_resolve(int32_t kvariant, uint32_t dtype, int32_t ksub, void **fn) {
   const void *sym = nullptr;
   if (kvariant >= RN_SCALAR && kvariant <= RN_LOOP)
     sym = rn_kernel(kvariant, dtype, ksub);
-  else if (kvariant >= ROPE_SCALAR && kvariant <= ROPE_QKN_VEC)
+  else if (kvariant >= ROPE_SCALAR && kvariant <= ROPE_QKN_VEC_I)
     sym = rope_kernel(kvariant, dtype);
   else if (kvariant >= SW_SCALAR && kvariant <= SW_FLAT_U4_NT)
     sym = sw_kernel(kvariant, dtype);

@@ -29,13 +29,41 @@ int32_t find_version(tri_cache *c, uint32_t op, const Key &k) {
 
 namespace {
 
-// inv_i = the float32 nearest to base^(-2i/hd). The power is taken in x87
-// extended precision (64-bit significand) and rounded once to float32.
-void rope_inverse_frequencies(float base, uint32_t hd, float *out) {
-  const long double b = (long double)base;
-  for (uint32_t i = 0; i < hd / 2; ++i) {
-    const long double e = -2.0L * (long double)i / (long double)hd;
-    out[i] = (float)powl(b, e);
+float f32_of_bits(uint32_t bits) {
+  float f;
+  memcpy(&f, &bits, sizeof f);
+  return f;
+}
+
+// inv_i = the float32 nearest to base^(-2i/rd), i < rd/2. The power is taken
+// in x87 extended precision (64-bit significand) and rounded once to
+// float32. With Llama-3 scaling the rule is applied to the extended value
+// before that one rounding: wavelength w = 2 pi / inv; w < L / high keeps
+// inv, w > L / low divides it by factor, and in between
+// s = (L / w - low) / (high - low) blends inv / factor and inv as
+// (1 - s) inv / factor + s inv (L = original context length).
+void rope_inverse_frequencies(const Key &k, float *out) {
+  const long double b = (long double)f32_of_bits(key_base_bits(k));
+  const uint32_t rd = key_rd(k);
+  const bool llama3 = key_scaling(k) == TRI_ROPE_SCALING_LLAMA3;
+  const long double factor = f32_of_bits(uint32_t(k.k4 & 0xFFFFFFFFu));
+  const long double low = f32_of_bits(uint32_t(k.k4 >> 32));
+  const long double high = f32_of_bits(uint32_t(k.k5 & 0xFFFFFFFFu));
+  const long double L = (long double)key_orig_max(k);
+  const long double two_pi = 6.283185307179586476925286766559005768L;
+  for (uint32_t i = 0; i < rd / 2; ++i) {
+    const long double e = -2.0L * (long double)i / (long double)rd;
+    long double inv = powl(b, e);
+    if (llama3) {
+      const long double w = two_pi / inv;
+      if (w > L / low) {
+        inv = inv / factor;
+      } else if (w >= L / high) {
+        const long double sm = (L / w - low) / (high - low);
+        inv = (1.0L - sm) * inv / factor + sm * inv;
+      }
+    }
+    out[i] = (float)inv;
   }
 }
 
@@ -56,15 +84,12 @@ tri_status install_key(tri_cache *c, const Key &k) {
     if (st != 0) return tri_status(st);
   }
   const uint32_t op = key_op(k);
-  if (op == TRI_OP_ROPE_QK || op == TRI_OP_QK_NORM_ROPE || op == TRI_OP_CHAIN) {
-    const uint32_t hd = key_hd(k);
-    float base;
-    const uint32_t bits = key_base_bits(k);
-    memcpy(&base, &bits, sizeof base);
-    v.n_consts = hd / 2;
+  const bool rope = op == TRI_OP_ROPE_QK || op == TRI_OP_QK_NORM_ROPE || op == TRI_OP_CHAIN;
+  if (rope && !(key_rope_bits(k) & kRopeCache)) {
+    v.n_consts = key_rd(k) / 2;
     v.h_consts = static_cast<float *>(malloc(sizeof(float) * v.n_consts));
     if (!v.h_consts) return TRI_E_NOMEM;
-    rope_inverse_frequencies(base, hd, v.h_consts);
+    rope_inverse_frequencies(k, v.h_consts);
     void *dev = nullptr;
     const int st = be_upload(v.h_consts, sizeof(float) * v.n_consts, &dev);
     if (st != 0) {
@@ -98,9 +123,7 @@ void fill_selection(const Version &v, int32_t index, int64_t T, tri_selection *o
     for (int i = 0; i < v.plan.n_launches; ++i)
       out->launch[i] = {v.plan.kvariant[i], role_grid(v.plan.kvariant[i], dt, T, I), kBlock};
   }
-  out->key[0] = k.k0;
-  out->key[1] = k.k1;
-  out->key[2] = k.k2;
+  key_words(k, out->key);
 }
 
 }  // namespace tri
@@ -180,9 +203,7 @@ tri_status tri_spec_stats(const tri_cache *c, tri_stats *out) {
 tri_status tri_spec_version_info(const tri_cache *c, uint32_t index, tri_version_info *out) {
   if (!c || !out || index >= c->n_versions) return TRI_E_INVALID;
   const Version &v = c->versions[index];
-  out->key[0] = v.key.k0;
-  out->key[1] = v.key.k1;
-  out->key[2] = v.key.k2;
+  key_words(v.key, out->key);
   out->variant = v.plan.variant;
   for (int i = 0; i < 3; ++i) out->roles[i] = v.plan.roles[i];
   out->hits = v.hits;

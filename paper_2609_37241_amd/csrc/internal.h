@@ -5,6 +5,7 @@
 #pragma once
 #include <stdint.h>
 
+#include "kernargs.h"
 #include "tri.h"
 
 namespace tri {
@@ -15,7 +16,8 @@ enum Variant : int32_t {
   RN_WAVE_1 = 11, RN_WAVE_2 = 12,
   RN_BLOCK_1 = 13, RN_BLOCK_2 = 14, RN_BLOCK_4 = 15, RN_BLOCK_8 = 16, RN_BLOCK_16 = 17,
   RN_LOOP = 18,
-  ROPE_SCALAR = 30, ROPE_VEC = 31, ROPE_QKN_SCALAR = 33, ROPE_QKN_VEC = 34,
+  ROPE_SCALAR = 30, ROPE_VEC = 31, ROPE_VEC_I = 32, ROPE_QKN_SCALAR = 33, ROPE_QKN_VEC = 34,
+  ROPE_QKN_VEC_I = 35,
   SW_SCALAR = 40, SW_FLAT = 41, SW_FLAT_NT = 42, SW_ROWS = 43, SW_FLAT_U4_NT = 44,
   CH_FUSED = 50, CH_SEQ = 51,
   EMPTY = 99,
@@ -38,11 +40,18 @@ constexpr unsigned kAlign = 1, kContig = 2;   // per-role guard flag bits
 constexpr unsigned kChainQkNorm = 0x40;        // chain key flag: QK-RMSNorm before RoPE
 
 // ---- key --------------------------------------------------------------------------
+// k0: op | dtype << 8 | bucket << 16 | flags << 24 | RoPE base bits << 32
+// k1: H | I << 32
+// k2: hd | nq << 16 | nk << 32
+// k3: rotary dim | variant bits << 16 | scaling << 24 | original_max_pos << 32
+// k4: factor bits | low_freq_factor bits << 32;  k5: high_freq_factor bits
+// Fields an op does not use are zero.
 struct Key {
-  uint64_t k0, k1, k2;
+  uint64_t k0, k1, k2, k3, k4, k5;
 };
 inline bool operator==(const Key &a, const Key &b) {
-  return a.k0 == b.k0 && a.k1 == b.k1 && a.k2 == b.k2;
+  return a.k0 == b.k0 && a.k1 == b.k1 && a.k2 == b.k2 && a.k3 == b.k3 && a.k4 == b.k4 &&
+         a.k5 == b.k5;
 }
 inline uint32_t key_op(const Key &k) { return uint32_t(k.k0 & 0xFF); }
 inline uint32_t key_dtype(const Key &k) { return uint32_t((k.k0 >> 8) & 0xFF); }
@@ -54,6 +63,18 @@ inline uint32_t key_I(const Key &k) { return uint32_t(k.k1 >> 32); }
 inline uint32_t key_hd(const Key &k) { return uint32_t(k.k2 & 0xFFFF); }
 inline uint32_t key_nq(const Key &k) { return uint32_t((k.k2 >> 16) & 0xFFFF); }
 inline uint32_t key_nk(const Key &k) { return uint32_t((k.k2 >> 32) & 0xFFFF); }
+inline uint32_t key_rd(const Key &k) { return uint32_t(k.k3 & 0xFFFF); }
+inline uint32_t key_rope_bits(const Key &k) { return uint32_t((k.k3 >> 16) & 0xFF); }
+inline uint32_t key_scaling(const Key &k) { return uint32_t((k.k3 >> 24) & 0xFF); }
+inline uint32_t key_orig_max(const Key &k) { return uint32_t(k.k3 >> 32); }
+inline void key_words(const Key &k, uint64_t *w) {
+  w[0] = k.k0;
+  w[1] = k.k1;
+  w[2] = k.k2;
+  w[3] = k.k3;
+  w[4] = k.k4;
+  w[5] = k.k5;
+}
 
 // ceil(log2 T) for 1 <= T <= 2^22.
 inline uint32_t token_bucket(int64_t T) {
@@ -68,7 +89,8 @@ struct Role {
   uint32_t grid;
 };
 Role rn_role(uint32_t dtype, int64_t H, unsigned flags, int64_t T);
-Role rope_role(uint32_t dtype, int32_t hd, unsigned flags, int64_t T, bool qk_norm);
+Role rope_role(uint32_t dtype, int32_t hd, int32_t rd, bool interleaved, unsigned flags, int64_t T,
+               bool qk_norm);
 Role sw_role(uint32_t dtype, int64_t I, unsigned flags, uint32_t bucket, int64_t T, bool in_chain);
 uint32_t role_grid(int32_t variant, uint32_t dtype, int64_t T, int64_t I);
 
@@ -79,7 +101,8 @@ struct Plan {
   int32_t n_launches;
   int32_t kvariant[3];    // kernel variant per launch
   int32_t ksub[3];        // kernel sub-selector (residual flag / fused template index)
-                          // fused: (role norm variant - RN_WAVE_1) * 4
+                          // fused: (role norm variant - RN_WAVE_1) * 8
+                          //        + (GPT-J pairs) * 4
                           //        + (QK-RMSNorm before RoPE) * 2
                           //        + (SwiGLU role is SW_FLAT_U4_NT)
 };
@@ -102,7 +125,7 @@ struct Version {
   Plan plan;
   void *fn[3];
   float *d_consts;        // device copy of the RoPE inverse frequencies, or null
-  float *h_consts;        // host copy (hd/2 floats), or null
+  float *h_consts;        // host copy (rotary_dim/2 floats), or null
   uint32_t n_consts;
   uint64_t hits;
 };

@@ -9,6 +9,10 @@
 
 namespace tri {
 
+// RoPE variant bits: RopeArgs::mode, and key word 3 above the 16-bit rotary
+// dim.
+constexpr uint32_t kRopeInterleaved = 1, kRopePos64 = 2, kRopeCache = 4;
+
 // Residual add + RMSNorm and plain RMSNorm ([T, H] rows, element strides).
 struct RnArgs {
   const void *x;
@@ -22,19 +26,24 @@ struct RnArgs {
   float eps;
 };
 
-// RoPE on Q [T, nq, hd] and K [T, nk, hd], in place; with QK-RMSNorm the
-// heads are normalised first (qw, kw: [hd] head-norm weights).
+// RoPE on Q [T, nq, hd] and K [T, nk, hd], in place, over the first rd
+// elements of each head; with QK-RMSNorm the whole heads are normalised first
+// (qw, kw: [hd] head-norm weights). Angles come from pos and inv_freq, or
+// from the cos_sin cache [cs_len, rd] (mode bit kRopeCache).
 struct RopeArgs {
   void *q;
   void *k;
-  const int32_t *pos;
-  const float *inv_freq;  // [hd/2], the version's table
+  const void *pos;        // int32 [T], or int64 [T] with mode bit kRopePos64
+  const float *inv_freq;  // [rd/2], the version's table (null with a cache)
   const void *qw;
   const void *kw;
+  const float *cos_sin;
   int64_t q_ts, k_ts;
   int64_t T;
-  int32_t nq, nk, hd;
+  int64_t cs_len;
+  int32_t nq, nk, hd, rd;
   float eps;
+  uint32_t mode;          // kRopeInterleaved | kRopePos64 | kRopeCache
 };
 
 // SwiGLU over [T, I].
@@ -61,9 +70,11 @@ struct ChainArgs {
 
 static_assert(sizeof(RnArgs) == 88 && offsetof(RnArgs, T) == 72 && offsetof(RnArgs, eps) == 84,
               "RnArgs layout");
-static_assert(sizeof(RopeArgs) == 88 && offsetof(RopeArgs, nq) == 72, "RopeArgs layout");
+static_assert(sizeof(RopeArgs) == 112 && offsetof(RopeArgs, nq) == 88 &&
+                  offsetof(RopeArgs, mode) == 108,
+              "RopeArgs layout");
 static_assert(sizeof(SwArgs) == 80 && offsetof(SwArgs, n) == 72, "SwArgs layout");
-static_assert(sizeof(ChainArgs) == 264 && offsetof(ChainArgs, rn_blocks) == 256,
+static_assert(sizeof(ChainArgs) == 288 && offsetof(ChainArgs, rn_blocks) == 280,
               "ChainArgs layout");
 
 }  // namespace tri

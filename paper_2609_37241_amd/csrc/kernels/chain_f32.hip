@@ -9,8 +9,8 @@ using namespace dev;
 
 // RNV: RN_WAVE_1/2 (one wavefront per row) or RN_BLOCK_1..16 (one
 // workgroup per row); the RoPE role takes one token per workgroup, with the
-// per-head QK RMSNorm first when QKN; SWV: SW_FLAT (one vector per
-// work-item, cached) or SW_FLAT_U4_NT (four, streaming).
+// per-head QK RMSNorm first when QKN and GPT-J pairs when INTER; SWV: SW_FLAT
+// (one vector per work-item, cached) or SW_FLAT_U4_NT (four, streaming).
 template <int DT, int RNV>
 __device__ __forceinline__ void chain_norm_role(const ChainArgs &a, uint32_t blk) {
   if constexpr (RNV <= RN_WAVE_2) {
@@ -27,7 +27,7 @@ __device__ __forceinline__ void chain_norm_role(const ChainArgs &a, uint32_t blk
 // path (2.75 vs 3.1 µs device time at 1 token). Streaming sizes
 // (SW_FLAT_U4_NT): SwiGLU first, then norm, then RoPE (about 1 % faster at
 // 8192 tokens than norm first).
-template <int DT, int RNV, int SWV, bool QKN>
+template <int DT, int RNV, int SWV, bool QKN, bool INTER>
 __global__ __launch_bounds__(256) void k_chain(ChainArgs a) {
   __shared__ float lds[2 * 256];
   const uint32_t b = blockIdx.x;
@@ -38,13 +38,13 @@ __global__ __launch_bounds__(256) void k_chain(ChainArgs a) {
     } else if (b < S + R) {
       chain_norm_role<DT, RNV>(a, b - S);
     } else {
-      rope_vec_block<DT, 1, false, 4, QKN>(a.rope, b - S - R, lds);
+      rope_vec_block<DT, 1, false, 4, QKN, INTER>(a.rope, b - S - R, lds);
     }
   } else {
     if (b < R) {
       chain_norm_role<DT, RNV>(a, b);
     } else if (b < R + P) {
-      rope_vec_block<DT, 1, false, 4, QKN>(a.rope, b - R, lds);
+      rope_vec_block<DT, 1, false, 4, QKN, INTER>(a.rope, b - R, lds);
     } else {
       sw_flat_part<DT, 1, false>(a.sw, b - R - P, S);
     }
@@ -52,28 +52,36 @@ __global__ __launch_bounds__(256) void k_chain(ChainArgs a) {
 }
 
 namespace {
+template <int RNV, bool QKN, bool INTER>
+const void *chain_pick_sw(bool u4) {
+  return u4 ? reinterpret_cast<const void *>(&k_chain<kF32, RNV, SW_FLAT_U4_NT, QKN, INTER>)
+            : reinterpret_cast<const void *>(&k_chain<kF32, RNV, SW_FLAT, QKN, INTER>);
+}
+
 template <int RNV>
-const void *chain_pick_rn(bool qkn, bool u4) {
-  if (qkn)
-    return u4 ? reinterpret_cast<const void *>(&k_chain<kF32, RNV, SW_FLAT_U4_NT, true>)
-              : reinterpret_cast<const void *>(&k_chain<kF32, RNV, SW_FLAT, true>);
-  return u4 ? reinterpret_cast<const void *>(&k_chain<kF32, RNV, SW_FLAT_U4_NT, false>)
-            : reinterpret_cast<const void *>(&k_chain<kF32, RNV, SW_FLAT, false>);
+const void *chain_pick_rn(int32_t rope_bits, bool u4) {
+  switch (rope_bits) {
+    case 0: return chain_pick_sw<RNV, false, false>(u4);
+    case 1: return chain_pick_sw<RNV, true, false>(u4);
+    case 2: return chain_pick_sw<RNV, false, true>(u4);
+    default: return chain_pick_sw<RNV, true, true>(u4);
+  }
 }
 }  // namespace
 
-// sub = (norm role - RN_WAVE_1) * 4 + 2 * (RoPE role has the QK norm)
+// sub = (norm role - RN_WAVE_1) * 8 + 4 * (GPT-J pairs) + 2 * (QK norm)
 //       + (SwiGLU role streams four vectors per work-item).
 const void *chain_kernel_f32(int32_t sub) {
-  const bool u4 = sub & 1, qkn = sub & 2;
-  switch (RN_WAVE_1 + (sub >> 2)) {
-    case RN_WAVE_1: return chain_pick_rn<RN_WAVE_1>(qkn, u4);
-    case RN_WAVE_2: return chain_pick_rn<RN_WAVE_2>(qkn, u4);
-    case RN_BLOCK_1: return chain_pick_rn<RN_BLOCK_1>(qkn, u4);
-    case RN_BLOCK_2: return chain_pick_rn<RN_BLOCK_2>(qkn, u4);
-    case RN_BLOCK_4: return chain_pick_rn<RN_BLOCK_4>(qkn, u4);
-    case RN_BLOCK_8: return chain_pick_rn<RN_BLOCK_8>(qkn, u4);
-    case RN_BLOCK_16: return chain_pick_rn<RN_BLOCK_16>(qkn, u4);
+  const bool u4 = sub & 1;
+  const int32_t rb = (sub >> 1) & 3;   // bit 0: QK norm, bit 1: GPT-J pairs
+  switch (RN_WAVE_1 + (sub >> 3)) {
+    case RN_WAVE_1: return chain_pick_rn<RN_WAVE_1>(rb, u4);
+    case RN_WAVE_2: return chain_pick_rn<RN_WAVE_2>(rb, u4);
+    case RN_BLOCK_1: return chain_pick_rn<RN_BLOCK_1>(rb, u4);
+    case RN_BLOCK_2: return chain_pick_rn<RN_BLOCK_2>(rb, u4);
+    case RN_BLOCK_4: return chain_pick_rn<RN_BLOCK_4>(rb, u4);
+    case RN_BLOCK_8: return chain_pick_rn<RN_BLOCK_8>(rb, u4);
+    case RN_BLOCK_16: return chain_pick_rn<RN_BLOCK_16>(rb, u4);
     default: return nullptr;
   }
 }

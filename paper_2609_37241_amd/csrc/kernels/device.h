@@ -332,19 +332,25 @@ __device__ __forceinline__ void rn_scalar_row(const RnArgs &a, int64_t row, doub
 }
 
 // ---- RoPE ---------------------------------------------------------------------
-// Angles theta = float(pos) * inv_i (one float32 product) and their cos/sin
-// are computed once per (token, pair) into LDS; every head of the token
-// reuses them.
-__device__ __forceinline__ void rope_angles(const RopeArgs &a, int64_t t, int tt, int half,
-                                            float *cs, float *sn) {
-  for (int i = threadIdx.x; i < half; i += kThreads) {
-    float c = 1.0f, s = 0.0f;
-    if (t < a.T) {
-      const float th = float(a.pos[t]) * a.inv_freq[i];
-      sincosf(th, &s, &c);
-    }
-    cs[tt * half + i] = c;
-    sn[tt * half + i] = s;
+// Angles: theta = float(pos) * inv_i (one float32 product; int64 positions
+// convert with one rounding) and cos / sin of it, or cos / sin read from the
+// caller's cache row min(max(pos, 0), cs_len - 1). They are computed once per
+// (token, pair) into LDS; every head of the token reuses them.
+__device__ __forceinline__ int64_t rope_pos(const RopeArgs &a, int64_t t) {
+  return (a.mode & kRopePos64) ? static_cast<const int64_t *>(a.pos)[t]
+                               : int64_t(static_cast<const int32_t *>(a.pos)[t]);
+}
+
+__device__ __forceinline__ void rope_cos_sin(const RopeArgs &a, int64_t t, int i, float &c,
+                                             float &s) {
+  const int64_t p = rope_pos(a, t);
+  if (a.mode & kRopeCache) {
+    const int64_t r = p < 0 ? 0 : (p >= a.cs_len ? a.cs_len - 1 : p);
+    const float *row = a.cos_sin + r * a.rd;
+    c = row[i];
+    s = row[(a.rd >> 1) + i];
+  } else {
+    sincosf(float(p) * a.inv_freq[i], &s, &c);
   }
 }
 
@@ -353,27 +359,31 @@ __device__ __forceinline__ char *rope_head(const RopeArgs &a, int64_t t, int h, 
                   : static_cast<char *>(a.k) + (t * a.k_ts + int64_t(h - a.nq) * a.hd) * es;
 }
 
-// TPB tokens per workgroup. Each half-head is cpb = (hd/2)/V 16-byte
-// vectors (a power of two); work-item `tid` owns chunk tid % cpb of heads
-// tid / cpb, tid / cpb + 256 / cpb, ... of every token of the block. Its
-// (token, head) items are processed PF at a time with all loads issued before
-// any use, and the first batch is requested before the angle math and the
-// barrier, so at decode sizes the block costs one memory round trip.
+// TPB tokens per workgroup; P2 = rd/2 angle pairs per token (a power of
+// two). Rotate-half (INTER false): each half of the rotated span is
+// cpb = P2/V 16-byte vectors and a work-item holds chunk c of both halves;
+// GPT-J pairs (INTER true): the span is cpb = rd/V vectors of V/2 adjacent
+// pairs each and a work-item holds one. Work-item `tid` owns chunk tid % cpb
+// of heads tid / cpb, tid / cpb + 256 / cpb, ... of every token of the
+// block. Its (token, head) items are processed PF at a time with all loads
+// issued before any use, and the first batch is requested before the angle
+// math and the barrier, so at decode sizes the block costs one memory round
+// trip. Elements past rd are not touched.
 //
-// QKN: each head is first RMS-normalised over its hd elements with the Q or
-// K head-norm weight. The cpb work-items of a head hold the whole head in
-// registers (chunk c of both halves), so the sum of squares is a reduction
+// QKN (requires rd == hd): each head is first RMS-normalised over its hd
+// elements with the Q or K head-norm weight. The cpb work-items of a head
+// hold the whole head in registers, so the sum of squares is a reduction
 // over cpb adjacent lanes and the head is read and written once. Every item
 // of a batch is then computed (clamped items on valid data) so that all
 // lanes of a group take part in the reduction; only stores are guarded.
-// cpb <= 64 since hd <= 512.
-template <int DT, int TPB, bool NT, int PF = 4, bool QKN = false>
+// cpb <= 64 (the policy guarantees it).
+template <int DT, int TPB, bool NT, int PF = 4, bool QKN = false, bool INTER = false>
 __device__ __forceinline__ void rope_vec_block(const RopeArgs &a, int64_t blk, float *lds) {
   using E = Elt<DT>;
   constexpr int V = E::V;
-  const int half = a.hd >> 1;
-  const int lh = __builtin_ctz(unsigned(half));
-  const int cpb = half / V;
+  const int P2 = a.rd >> 1;
+  const int lp = __builtin_ctz(unsigned(P2));
+  const int cpb = (INTER ? a.rd : P2) / V;
   const int shift = __builtin_ctz(unsigned(cpb));
   const int chunk = threadIdx.x & (cpb - 1);
   const int hg = threadIdx.x >> shift;
@@ -383,25 +393,36 @@ __device__ __forceinline__ void rope_vec_block(const RopeArgs &a, int64_t blk, f
   const int64_t tlast = a.T - 1;
   float *cs = lds;
   float *sn = lds + TPB * 256;
-  const int na = TPB * half;
+  const int na = TPB * P2;
+  // byte offset of the second vector of an item (rotate-half: the other half)
+  const int off2 = P2 * E::ES;
 
-  // Head-norm weight chunks of this work-item (both halves, Q and K).
+  // Head-norm weight chunks of this work-item (Q and K; both halves).
   u32x4 wq1, wq2, wk1, wk2;
   if constexpr (QKN) {
     const char *qw = static_cast<const char *>(a.qw);
     const char *kw = a.kw ? static_cast<const char *>(a.kw) : qw;
     wq1 = reinterpret_cast<const u32x4 *>(qw)[chunk];
-    wq2 = reinterpret_cast<const u32x4 *>(qw + half * E::ES)[chunk];
     wk1 = reinterpret_cast<const u32x4 *>(kw)[chunk];
-    wk2 = reinterpret_cast<const u32x4 *>(kw + half * E::ES)[chunk];
+    if constexpr (!INTER) {
+      wq2 = reinterpret_cast<const u32x4 *>(qw + off2)[chunk];
+      wk2 = reinterpret_cast<const u32x4 *>(kw + off2)[chunk];
+    }
   }
 
-  // Operands of this work-item's angle slot (token t0 + tid / half, pair
-  // tid % half); indices are clamped so the loads are always in bounds.
-  const int ia = threadIdx.x & (half - 1);
-  const int64_t ta = t0 + (threadIdx.x >> lh);
-  const int32_t pa = a.pos[ta <= tlast ? ta : tlast];
-  const float ina = a.inv_freq[ia];
+  // Operands of this work-item's angle slot (token t0 + tid / P2, pair
+  // tid % P2); indices are clamped so the loads are always in bounds. The
+  // plain mode (int32 positions, computed angles) requests them before the
+  // gather.
+  const int ia = threadIdx.x & (P2 - 1);
+  const int64_t ta = t0 + (threadIdx.x >> lp);
+  const bool plain = a.mode == 0 || a.mode == kRopeInterleaved;
+  int32_t pa = 0;
+  float ina = 0.0f;
+  if (plain) {
+    pa = static_cast<const int32_t *>(a.pos)[ta <= tlast ? ta : tlast];
+    ina = a.inv_freq[ia];
+  }
 
   int tt = 0, h = hg;
   const int hfirst = hg < nh ? hg : nh - 1;
@@ -416,7 +437,7 @@ __device__ __forceinline__ void rope_vec_block(const RopeArgs &a, int64_t blk, f
       ih[j] = ok[j] ? h : hfirst;
       const char *b = rope_head(a, t0 + it[j], ih[j], E::ES);
       x1[j] = ld16<NT>(reinterpret_cast<const u32x4 *>(b) + chunk);
-      x2[j] = ld16<NT>(reinterpret_cast<const u32x4 *>(b + half * E::ES) + chunk);
+      if constexpr (!INTER) x2[j] = ld16<NT>(reinterpret_cast<const u32x4 *>(b + off2) + chunk);
       if (ok[j]) {
         h += hstep;
         if (h >= nh) {
@@ -431,16 +452,20 @@ __device__ __forceinline__ void rope_vec_block(const RopeArgs &a, int64_t blk, f
   if (na <= kThreads) {
     if (threadIdx.x < na) {
       float c = 1.0f, s = 0.0f;
-      if (ta <= tlast) sincosf(float(pa) * ina, &s, &c);
+      if (ta <= tlast) {
+        if (plain)
+          sincosf(float(pa) * ina, &s, &c);
+        else
+          rope_cos_sin(a, ta, ia, c, s);
+      }
       cs[threadIdx.x] = c;
       sn[threadIdx.x] = s;
     }
   } else {
     for (int e = threadIdx.x; e < na; e += kThreads) {
-      const int64_t t = t0 + (e >> lh);
-      const int i = e & (half - 1);
+      const int64_t t = t0 + (e >> lp);
       float c = 1.0f, s = 0.0f;
-      if (t <= tlast) sincosf(float(a.pos[t]) * a.inv_freq[i], &s, &c);
+      if (t <= tlast) rope_cos_sin(a, t, e & (P2 - 1), c, s);
       cs[e] = c;
       sn[e] = s;
     }
@@ -453,73 +478,101 @@ __device__ __forceinline__ void rope_vec_block(const RopeArgs &a, int64_t blk, f
       if constexpr (!QKN) {
         if (!ok[j]) continue;
       }
-      const int base = it[j] * half + chunk * V;
-      float f1[V], f2[V], o1[V], o2[V];
+      float f1[V], f2[V];
       E::unpack(x1[j], f1);
-      E::unpack(x2[j], f2);
+      if constexpr (!INTER) E::unpack(x2[j], f2);
       if constexpr (QKN) {
         float ss = 0.0f;
 #pragma unroll
         for (int e = 0; e < V; ++e) ss += f1[e] * f1[e];
+        if constexpr (!INTER) {
 #pragma unroll
-        for (int e = 0; e < V; ++e) ss += f2[e] * f2[e];
+          for (int e = 0; e < V; ++e) ss += f2[e] * f2[e];
+        }
         ss = group_sum(ss, cpb);
         const float inv = rsqrtf(ss / float(a.hd) + a.eps);
         const bool isq = ih[j] < a.nq;
-        float w1[V], w2[V];
+        float w1[V];
         E::unpack(isq ? wq1 : wk1, w1);
-        E::unpack(isq ? wq2 : wk2, w2);
 #pragma unroll
-        for (int e = 0; e < V; ++e) {
-          f1[e] = (f1[e] * inv) * w1[e];
-          f2[e] = (f2[e] * inv) * w2[e];
+        for (int e = 0; e < V; ++e) f1[e] = (f1[e] * inv) * w1[e];
+        if constexpr (!INTER) {
+          float w2[V];
+          E::unpack(isq ? wq2 : wk2, w2);
+#pragma unroll
+          for (int e = 0; e < V; ++e) f2[e] = (f2[e] * inv) * w2[e];
         }
       }
-#pragma unroll
-      for (int e = 0; e < V; ++e) {
-        const float c = cs[base + e], s = sn[base + e];
-        o1[e] = f1[e] * c - f2[e] * s;
-        o2[e] = f2[e] * c + f1[e] * s;
-      }
-      if (QKN && !ok[j]) continue;
       char *b = rope_head(a, t0 + it[j], ih[j], E::ES);
-      st16<NT>(reinterpret_cast<u32x4 *>(b) + chunk, E::pack(o1));
-      st16<NT>(reinterpret_cast<u32x4 *>(b + half * E::ES) + chunk, E::pack(o2));
+      if constexpr (INTER) {
+        const int base = it[j] * P2 + ((chunk * V) >> 1);
+        float o[V];
+#pragma unroll
+        for (int e = 0; e < V; e += 2) {
+          const float c = cs[base + (e >> 1)], s = sn[base + (e >> 1)];
+          o[e] = f1[e] * c - f1[e + 1] * s;
+          o[e + 1] = f1[e + 1] * c + f1[e] * s;
+        }
+        if (QKN && !ok[j]) continue;
+        st16<NT>(reinterpret_cast<u32x4 *>(b) + chunk, E::pack(o));
+      } else {
+        const int base = it[j] * P2 + chunk * V;
+        float o1[V], o2[V];
+#pragma unroll
+        for (int e = 0; e < V; ++e) {
+          const float c = cs[base + e], s = sn[base + e];
+          o1[e] = f1[e] * c - f2[e] * s;
+          o2[e] = f2[e] * c + f1[e] * s;
+        }
+        if (QKN && !ok[j]) continue;
+        st16<NT>(reinterpret_cast<u32x4 *>(b) + chunk, E::pack(o1));
+        st16<NT>(reinterpret_cast<u32x4 *>(b + off2) + chunk, E::pack(o2));
+      }
     }
     if (!(tt < TPB && t0 + tt <= tlast && hg < nh)) break;
     gather();
   }
 }
 
-// Any alignment / head size: one token per workgroup, element pairs. `lds`
-// holds 2 * 256 floats (cos, sin), and 256 more for QKN.
+// Any alignment / head size / variant: one token per workgroup, element
+// pairs. `lds` holds 2 * 256 floats (cos, sin), and 256 more for QKN. Pairs
+// are (i, i + rd/2), or (2i, 2i + 1) with kRopeInterleaved.
 //
 // QKN: heads are taken 256 at a time; wavefront w reduces the squares of
 // heads w, w + 4, ... of the slice (element-wise loads, any alignment) and
-// leaves 1/rms in LDS, then all work-items normalise and rotate the slice.
+// leaves 1/rms in LDS, then all work-items normalise and rotate the slice,
+// and normalise the elements past rd.
 template <int DT, bool QKN = false>
 __device__ __forceinline__ void rope_scalar_block(const RopeArgs &a, int64_t t, float *lds) {
   using E = Elt<DT>;
-  const int half = a.hd >> 1;
+  const int P2 = a.rd >> 1;
+  const bool inter = a.mode & kRopeInterleaved;
   float *cs = lds;
   float *sn = lds + 256;
-  rope_angles(a, t, 0, half, cs, sn);
+  for (int i = threadIdx.x; i < P2; i += kThreads) {
+    float c, s;
+    rope_cos_sin(a, t, i, c, s);
+    cs[i] = c;
+    sn[i] = s;
+  }
   __syncthreads();
   const int nh = a.nq + a.nk;
   if constexpr (!QKN) {
-    const int total = nh * half;
+    const int total = nh * P2;
     for (int e = threadIdx.x; e < total; e += kThreads) {
-      const int h = e / half;
-      const int i = e - h * half;
+      const int h = e / P2;
+      const int i = e - h * P2;
+      const int i0 = inter ? 2 * i : i, i1 = inter ? 2 * i + 1 : i + P2;
       char *base = rope_head(a, t, h, E::ES);
-      const float v1 = E::ld(base, i), v2 = E::ld(base, i + half);
-      E::st(base, i, v1 * cs[i] - v2 * sn[i]);
-      E::st(base, i + half, v2 * cs[i] + v1 * sn[i]);
+      const float v1 = E::ld(base, i0), v2 = E::ld(base, i1);
+      E::st(base, i0, v1 * cs[i] - v2 * sn[i]);
+      E::st(base, i1, v2 * cs[i] + v1 * sn[i]);
     }
   } else {
     float *rinv = lds + 512;
     const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
     const void *kw = a.kw ? a.kw : a.qw;
+    const int pass = a.hd - a.rd;
     for (int h0 = 0; h0 < nh; h0 += kThreads) {
       const int hn = nh - h0 < kThreads ? nh - h0 : kThreads;
       for (int hl = wid; hl < hn; hl += kThreads / 64) {
@@ -533,18 +586,28 @@ __device__ __forceinline__ void rope_scalar_block(const RopeArgs &a, int64_t t, 
         if (lane == 0) rinv[hl] = rsqrtf(ss / float(a.hd) + a.eps);
       }
       __syncthreads();
-      const int total = hn * half;
+      const int total = hn * P2;
       for (int e = threadIdx.x; e < total; e += kThreads) {
-        const int hl = e / half;
-        const int i = e - hl * half;
+        const int hl = e / P2;
+        const int i = e - hl * P2;
+        const int i0 = inter ? 2 * i : i, i1 = inter ? 2 * i + 1 : i + P2;
         const int h = h0 + hl;
         const void *w = h < a.nq ? a.qw : kw;
         char *base = rope_head(a, t, h, E::ES);
         const float r = rinv[hl];
-        const float n1 = (E::ld(base, i) * r) * E::ld(w, i);
-        const float n2 = (E::ld(base, i + half) * r) * E::ld(w, i + half);
-        E::st(base, i, n1 * cs[i] - n2 * sn[i]);
-        E::st(base, i + half, n2 * cs[i] + n1 * sn[i]);
+        const float n1 = (E::ld(base, i0) * r) * E::ld(w, i0);
+        const float n2 = (E::ld(base, i1) * r) * E::ld(w, i1);
+        E::st(base, i0, n1 * cs[i] - n2 * sn[i]);
+        E::st(base, i1, n2 * cs[i] + n1 * sn[i]);
+      }
+      const int tp = hn * pass;
+      for (int e = threadIdx.x; e < tp; e += kThreads) {
+        const int hl = e / pass;
+        const int j = a.rd + (e - hl * pass);
+        const int h = h0 + hl;
+        const void *w = h < a.nq ? a.qw : kw;
+        char *base = rope_head(a, t, h, E::ES);
+        E::st(base, j, (E::ld(base, j) * rinv[hl]) * E::ld(w, j));
       }
       __syncthreads();
     }

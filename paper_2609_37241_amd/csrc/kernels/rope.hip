@@ -1,16 +1,18 @@
 // RoPE-on-Q-and-K kernels (in place), with and without the per-head QK
-// RMSNorm, one per install-policy variant and dtype.
+// RMSNorm, rotate-half or GPT-J pairs, one per install-policy variant and
+// dtype (the scalar kernels take the pairing, position width and angle
+// source at run time).
 #include "../internal.h"
 #include "device.h"
 
 namespace tri {
 using namespace dev;
 
-// QKN: per-head RMSNorm of Q and K before the rotation.
-template <int DT, bool QKN>
+// QKN: per-head RMSNorm of Q and K before the rotation; INTER: GPT-J pairs.
+template <int DT, bool QKN, bool INTER>
 __global__ __launch_bounds__(256) void k_rope_vec(RopeArgs a) {
   __shared__ float lds[2 * 256];
-  rope_vec_block<DT, 1, false, 4, QKN>(a, blockIdx.x, lds);
+  rope_vec_block<DT, 1, false, 4, QKN, INTER>(a, blockIdx.x, lds);
 }
 
 template <int DT, bool QKN>
@@ -24,9 +26,11 @@ template <int DT>
 const void *rope_pick(int32_t variant) {
   switch (variant) {
     case ROPE_SCALAR: return reinterpret_cast<const void *>(&k_rope_scalar<DT, false>);
-    case ROPE_VEC: return reinterpret_cast<const void *>(&k_rope_vec<DT, false>);
+    case ROPE_VEC: return reinterpret_cast<const void *>(&k_rope_vec<DT, false, false>);
+    case ROPE_VEC_I: return reinterpret_cast<const void *>(&k_rope_vec<DT, false, true>);
     case ROPE_QKN_SCALAR: return reinterpret_cast<const void *>(&k_rope_scalar<DT, true>);
-    case ROPE_QKN_VEC: return reinterpret_cast<const void *>(&k_rope_vec<DT, true>);
+    case ROPE_QKN_VEC: return reinterpret_cast<const void *>(&k_rope_vec<DT, true, false>);
+    case ROPE_QKN_VEC_I: return reinterpret_cast<const void *>(&k_rope_vec<DT, true, true>);
     default: return nullptr;
   }
 }

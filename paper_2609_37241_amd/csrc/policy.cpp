@@ -5,7 +5,7 @@
 // here every specialization a key can need is already compiled for gfx950,
 // and installing a version means choosing among them. The choice is a pure
 // function of the key (dtype, sizes, token bucket, alignment and contiguity
-// flags), so the same key always selects the same kernels.
+// flags, RoPE variant), so the same key always selects the same kernels.
 #include "internal.h"
 
 namespace tri {
@@ -52,18 +52,24 @@ Role rn_role(uint32_t dtype, int64_t H, unsigned flags, int64_t T) {
   return {RN_LOOP, uint32_t(T)};
 }
 
-// Vector RoPE needs each half-head to be a power-of-two number of 16-byte
-// vectors, so a thread keeps one chunk of angles for every head it visits.
-// One token per workgroup at every size (it also streamed best at 8192
-// tokens: more workgroups, one angle table each).
-// With QK-RMSNorm the same two layouts apply; the norm's per-head reduction
-// runs over the lanes (vector form) or wavefronts (scalar form) of a head.
-Role rope_role(uint32_t dtype, int32_t hd, unsigned flags, int64_t T, bool qk_norm) {
+// Vector RoPE needs the rotated span of a head to split into a power-of-two
+// number of 16-byte vectors per work-item group: rd/2 elements per half for
+// rotate-half pairs (a work-item holds chunk c of both halves), rd elements
+// for GPT-J pairs (a work-item holds one vector of whole pairs). One token per
+// workgroup at every size (it also streamed best at 8192 tokens: more
+// workgroups, one angle table each). With QK-RMSNorm the vector form needs
+// the group to hold the whole head (rd == hd) in at most 64 lanes, since the
+// norm's per-head reduction runs over the group's lanes; otherwise the scalar
+// form reduces each head with a wavefront.
+Role rope_role(uint32_t dtype, int32_t hd, int32_t rd, bool interleaved, unsigned flags, int64_t T,
+               bool qk_norm) {
   const int64_t v = vec_elems(dtype);
-  const int64_t half = hd / 2;
-  const int64_t cpb = half / v;
-  if (!(flags & kAlign) || half % v || (cpb & (cpb - 1)) != 0)
-    return {qk_norm ? ROPE_QKN_SCALAR : ROPE_SCALAR, uint32_t(T)};
+  const int64_t span = interleaved ? rd : rd / 2;   // elements one group covers per half
+  const int64_t cpb = span / v;
+  bool vec = (flags & kAlign) && span % v == 0 && cpb > 0 && (cpb & (cpb - 1)) == 0;
+  if (qk_norm) vec = vec && rd == hd && cpb <= 64;
+  if (!vec) return {qk_norm ? ROPE_QKN_SCALAR : ROPE_SCALAR, uint32_t(T)};
+  if (interleaved) return {qk_norm ? ROPE_QKN_VEC_I : ROPE_VEC_I, uint32_t(T)};
   return {qk_norm ? ROPE_QKN_VEC : ROPE_VEC, uint32_t(T)};
 }
 
@@ -93,8 +99,8 @@ uint32_t role_grid(int32_t variant, uint32_t dtype, int64_t T, int64_t I) {
   if (variant == RN_WAVE_1 || variant == RN_WAVE_2) return uint32_t(cdiv(T, 4));
   switch (variant) {
     case RN_SCALAR: case RN_BLOCK_1: case RN_BLOCK_2: case RN_BLOCK_4: case RN_BLOCK_8:
-    case RN_BLOCK_16: case RN_LOOP: case ROPE_SCALAR: case ROPE_VEC: case ROPE_QKN_SCALAR:
-    case ROPE_QKN_VEC:
+    case RN_BLOCK_16: case RN_LOOP: case ROPE_SCALAR: case ROPE_VEC: case ROPE_VEC_I:
+    case ROPE_QKN_SCALAR: case ROPE_QKN_VEC: case ROPE_QKN_VEC_I:
       return uint32_t(T);
     case SW_FLAT: case SW_FLAT_NT:
       return clamp_grid(cdiv((T * I) / vec_elems(dtype), kBlock));
@@ -117,7 +123,13 @@ namespace {
 
 // Template index of the fused chain kernel (see Plan::ksub).
 int32_t fused_sub(int32_t rn, int32_t rope, int32_t sw) {
-  return (rn - RN_WAVE_1) * 4 + (rope == ROPE_QKN_VEC ? 2 : 0) + (sw == SW_FLAT_U4_NT ? 1 : 0);
+  const bool inter = rope == ROPE_VEC_I || rope == ROPE_QKN_VEC_I;
+  const bool qkn = rope == ROPE_QKN_VEC || rope == ROPE_QKN_VEC_I;
+  return (rn - RN_WAVE_1) * 8 + (inter ? 4 : 0) + (qkn ? 2 : 0) + (sw == SW_FLAT_U4_NT ? 1 : 0);
+}
+
+bool rope_vec_role(int32_t v) {
+  return v == ROPE_VEC || v == ROPE_VEC_I || v == ROPE_QKN_VEC || v == ROPE_QKN_VEC_I;
 }
 
 }  // namespace
@@ -138,7 +150,9 @@ Plan plan_for_key(const Key &k) {
     }
     case TRI_OP_ROPE_QK:
     case TRI_OP_QK_NORM_ROPE: {
-      const Role r = rope_role(dt, int32_t(key_hd(k)), fl, 1, op == TRI_OP_QK_NORM_ROPE);
+      const Role r = rope_role(dt, int32_t(key_hd(k)), int32_t(key_rd(k)),
+                               (key_rope_bits(k) & kRopeInterleaved) != 0, fl, 1,
+                               op == TRI_OP_QK_NORM_ROPE);
       p.variant = r.variant;
       p.n_launches = 1;
       p.kvariant[0] = r.variant;
@@ -155,13 +169,15 @@ Plan plan_for_key(const Key &k) {
       break;
   }
   const Role rn = rn_role(dt, key_H(k), fl & 3u, 1);
-  const Role ro = rope_role(dt, int32_t(key_hd(k)), (fl >> 2) & 3u, 1, (fl & kChainQkNorm) != 0);
+  const Role ro = rope_role(dt, int32_t(key_hd(k)), int32_t(key_rd(k)),
+                            (key_rope_bits(k) & kRopeInterleaved) != 0, (fl >> 2) & 3u, 1,
+                            (fl & kChainQkNorm) != 0);
   const Role sw = sw_role(dt, key_I(k), (fl >> 4) & 3u, b, 1, true);
   p.roles[0] = rn.variant;
   p.roles[1] = ro.variant;
   p.roles[2] = sw.variant;
   const bool rn_regs = rn.variant >= RN_WAVE_1 && rn.variant <= RN_BLOCK_16;
-  const bool ro_vec = ro.variant == ROPE_VEC || ro.variant == ROPE_QKN_VEC;
+  const bool ro_vec = rope_vec_role(ro.variant);
   const bool sw_flat = sw.variant == SW_FLAT || sw.variant == SW_FLAT_U4_NT;
   if ((fl & 0x3Fu) == 0x3Fu && rn_regs && ro_vec && sw_flat) {
     p.variant = CH_FUSED;

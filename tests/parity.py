@@ -48,7 +48,34 @@ def tok_stride(t):
     return t.stride(0) if t.shape[0] > 1 else max(t.stride(0), t.shape[1] * t.shape[2])
 
 
-def model_chain_call(d, eps, base, qk_eps=None):
+def oracle_rope_kw(ext, cos_sin=None):
+    """Keyword arguments of oracle.ops.rope_ext for an ABI-style variant dict
+    (keys of the selection model's PLAIN_EXT); cos_sin: the host table."""
+    ext = ext or {}
+    kw = dict(rotary_dim=ext.get("rotary_dim") or None,
+              interleaved=bool(ext.get("interleaved", 0)))
+    if ext.get("scaling", 0) == S.SCALING_LLAMA3:
+        kw["scaling"] = {n: ext[n] for n in ("factor", "low_freq_factor", "high_freq_factor",
+                                             "original_max_pos")}
+    if cos_sin is not None:
+        kw["cos_sin"] = cos_sin
+    return kw
+
+
+def binding_rope_ext(tri, ext, cos_sin=None):
+    """The binding's RopeExt for an ABI-style variant dict (cos_sin: device table)."""
+    ext = ext or {}
+    scaling = None
+    if ext.get("scaling", 0) == S.SCALING_LLAMA3:
+        scaling = {n: ext[n] for n in ("factor", "low_freq_factor", "high_freq_factor",
+                                       "original_max_pos")}
+    return tri.rope_ext(rotary_dim=ext.get("rotary_dim", 0),
+                        interleaved=bool(ext.get("interleaved", 0)),
+                        pos_int64=bool(ext.get("pos_int64", 0)), scaling=scaling,
+                        cos_sin=cos_sin)
+
+
+def model_chain_call(d, eps, base, qk_eps=None, ext=None):
     """An oracle-model Call for a decode chain over device tensors `d` (with
     head-norm weights when `d` holds q_norm_w / k_norm_w)."""
     dt = nm.BF16 if str(d["x"].dtype).endswith("bfloat16") else nm.F32
@@ -68,7 +95,7 @@ def model_chain_call(d, eps, base, qk_eps=None):
         ptr["k_w"] = d["k_norm_w"].data_ptr()
     return S.Call(S.OP_CHAIN, dt_code(dt), T, H=H, I=d["gate"].shape[1], hd=hd, nq=nq, nk=nk,
                   eps=eps, base=base, qk_eps=eps if qk_eps is None else qk_eps, ptr=ptr,
-                  stride=stride)
+                  stride=stride, ext=ext)
 
 
 def expected_record(call: S.Call, version: int):
@@ -81,4 +108,5 @@ def expected_record(call: S.Call, version: int):
     return rec.as_tuple()
 
 
-__all__ = ["check", "model_chain_call", "expected_record", "wl"]
+__all__ = ["check", "model_chain_call", "expected_record", "oracle_rope_kw", "binding_rope_ext",
+           "wl"]

@@ -29,23 +29,29 @@ def res_call(dtype, T, H, *, eps=1e-6, off=0, pad=0, null=(), op=S.OP_RES_RMSNOR
                   stride={n: H + pad for n in S.RES_STRIDES})
 
 
-def rope_call(dtype, T, nq, nk, hd, *, base=10000.0, off=0, pad=0, pos_off=0, null=()):
+CACHE_ADDR = _addr(15)
+
+
+def rope_call(dtype, T, nq, nk, hd, *, base=10000.0, off=0, pad=0, pos_off=0, null=(),
+              ext=None):
+    """RoPE call; `ext` (keys of the selection model's PLAIN_EXT, cos_sin as
+    an address) selects a variant."""
     ptr = {"q": _addr(10) + off, "k": _addr(11) + off, "pos": _addr(12) + pos_off}
     for n in null:
         ptr[n] = None
     return S.Call(S.OP_ROPE_QK, dtype, T, hd=hd, nq=nq, nk=nk, base=base, ptr=ptr,
-                  stride={"q": nq * hd + pad, "k": nk * hd + pad})
+                  stride={"q": nq * hd + pad, "k": nk * hd + pad}, ext=ext)
 
 
 def qkn_call(dtype, T, nq, nk, hd, *, base=10000.0, eps=1e-6, off=0, pad=0, w_off=0,
-             pos_off=0, null=()):
+             pos_off=0, null=(), ext=None):
     """QK-RMSNorm + RoPE; w_off displaces both head-norm weights."""
     ptr = {"q": _addr(10) + off, "k": _addr(11) + off, "pos": _addr(12) + pos_off,
            "q_w": _addr(13) + w_off, "k_w": _addr(14) + w_off}
     for n in null:
         ptr[n] = None
     return S.Call(S.OP_QK_NORM_ROPE, dtype, T, hd=hd, nq=nq, nk=nk, base=base, eps=eps,
-                  ptr=ptr, stride={"q": nq * hd + pad, "k": nk * hd + pad})
+                  ptr=ptr, stride={"q": nq * hd + pad, "k": nk * hd + pad}, ext=ext)
 
 
 def sw_call(dtype, T, I, *, off=0, pad=0, null=()):
@@ -58,7 +64,7 @@ def sw_call(dtype, T, I, *, off=0, pad=0, null=()):
 
 def chain_call(dtype, T, H, I, nq, nk, hd, *, base=10000.0, eps=1e-6,
                res_off=0, res_pad=0, rope_off=0, rope_pad=0, sw_off=0, sw_pad=0,
-               qk_norm=False, qk_eps=1e-6, w_off=0, null=()):
+               qk_norm=False, qk_eps=1e-6, w_off=0, null=(), ext=None):
     r = res_call(dtype, T, H, eps=eps, off=res_off, pad=res_pad)
     if qk_norm:
         q = qkn_call(dtype, T, nq, nk, hd, base=base, off=rope_off, pad=rope_pad, w_off=w_off)
@@ -74,7 +80,7 @@ def chain_call(dtype, T, H, I, nq, nk, hd, *, base=10000.0, eps=1e-6,
     for n in null:
         ptr[n] = None
     return S.Call(S.OP_CHAIN, dtype, T, H=H, I=I, hd=hd, nq=nq, nk=nk, eps=eps,
-                  base=base, qk_eps=qk_eps, ptr=ptr, stride=stride)
+                  base=base, qk_eps=qk_eps, ptr=ptr, stride=stride, ext=ext)
 
 
 def elem_offset(dtype, n=1):

@@ -11,7 +11,8 @@ import torch
 from oracle import numerics as nm
 from oracle import ops as O
 from oracle import selection as S
-from tests.parity import check, expected_record, model_chain_call
+from tests.parity import (binding_rope_ext, check, expected_record, model_chain_call,
+                          oracle_rope_kw)
 import workloads as wl
 
 pytestmark = pytest.mark.gpu
@@ -76,14 +77,24 @@ def host(t):
 # ---- the configured chains ---------------------------------------------------------
 TINY_QKN_F32 = wl.ChainConfig("tiny_qkn_f32", wl.F32, T=3, H=256, nq=4, nk=2, hd=64, I=688,
                               base=1e6, pos_mode="uniform", pos_max=4095, qk_norm=True)
-CHAIN_CFGS = [wl.TINY_F32, wl.LLAMA7B_DECODE, wl.GQA_DECODE, wl.QWEN3_8B_DECODE, TINY_QKN_F32]
+CHAIN_CFGS = [wl.TINY_F32, wl.LLAMA7B_DECODE, wl.GQA_DECODE, wl.QWEN3_8B_DECODE, TINY_QKN_F32,
+              wl.LLAMA31_8B_DECODE, wl.GPTJ_DECODE]
 
 
 def run_chain(cache, cfg, d):
     """decode_chain over device tensors d (head-norm weights when present)."""
+    import paper_2609_37241_amd as tri
+    rope = binding_rope_ext(tri, cfg.rope_ext) if cfg.rope_ext else None
     cache.decode_chain(d["x"], d["residual"], d["w"], d["q"], d["k"], d["pos"], d["gate"],
                        d["up"], cfg.eps, cfg.base, y=d["y"], residual_out=d["res_out"],
-                       out=d["out"], q_norm_w=d.get("q_norm_w"), k_norm_w=d.get("k_norm_w"))
+                       out=d["out"], q_norm_w=d.get("q_norm_w"), k_norm_w=d.get("k_norm_w"),
+                       rope=rope)
+
+
+def chain_oracle(inp, cfg):
+    if cfg.rope_ext:
+        inp = dict(inp, rope_ext=oracle_rope_kw(cfg.rope_ext))
+    return O.decode_chain(inp, cfg.eps, cfg.base, cfg.dtype)
 
 
 @pytest.mark.parametrize("cfg", CHAIN_CFGS, ids=lambda c: c.name)
@@ -95,14 +106,14 @@ def test_chain_config(tri, cache, cfg):
     d["out"] = torch.empty_like(d["gate"])
     run_chain(cache, cfg, d)
     torch.cuda.synchronize()
-    want = O.decode_chain(inp, cfg.eps, cfg.base, cfg.dtype)
+    want = chain_oracle(inp, cfg)
     check("y", host(d["y"]), want["y"], cfg.dtype)
     check("res_out", host(d["res_out"]), want["res_out"], cfg.dtype, exact=True)
     check("q", host(d["q"]), want["q"], cfg.dtype)
     check("k", host(d["k"]), want["k"], cfg.dtype)
     check("out", host(d["out"]), want["out"], cfg.dtype)
     rec = cache.last_selection().as_tuple()
-    assert rec == expected_record(model_chain_call(d, cfg.eps, cfg.base), 0)
+    assert rec == expected_record(model_chain_call(d, cfg.eps, cfg.base, ext=cfg.rope_ext), 0)
     assert rec[3] == S.CH_FUSED
 
 
@@ -111,12 +122,17 @@ def test_fused_chain_equals_separate_ops_bitwise(tri, cache, cfg):
     inp = wl.host_inputs(cfg)
     a = {k: wl.to_torch(v, cfg.dtype, DEV) for k, v in inp.items()}
     b = {k: v.clone() for k, v in a.items()}
+    rope = binding_rope_ext(tri, cfg.rope_ext) if cfg.rope_ext else None
     y, ro, out = cache.decode_chain(a["x"], a["residual"], a["w"], a["q"], a["k"], a["pos"],
                                     a["gate"], a["up"], cfg.eps, cfg.base,
-                                    q_norm_w=a.get("q_norm_w"), k_norm_w=a.get("k_norm_w"))
+                                    q_norm_w=a.get("q_norm_w"), k_norm_w=a.get("k_norm_w"),
+                                    rope=rope)
     assert cache.last_selection().variant == S.CH_FUSED
     y2, ro2 = cache.residual_rmsnorm(b["x"], b["residual"], b["w"], cfg.eps)
-    if cfg.qk_norm:
+    if cfg.rope_ext:
+        cache.rope(b["q"], b["k"], b["pos"], cfg.base, rope, q_w=b.get("q_norm_w"),
+                   k_w=b.get("k_norm_w"), eps=cfg.eps)
+    elif cfg.qk_norm:
         cache.qk_norm_rope(b["q"], b["k"], b["pos"], b["q_norm_w"], b["k_norm_w"], cfg.base,
                            cfg.eps)
     else:
@@ -301,6 +317,75 @@ def test_qk_norm_rope_zero_heads_and_position_zero(tri, cache, dtype):
     check("k", gk, O.rmsnorm(k, kw, 1e-6, dtype), dtype)
 
 
+# ---- RoPE variants ----------------------------------------------------------------------
+LLAMA3 = dict(scaling=S.SCALING_LLAMA3, factor=8.0, low_freq_factor=1.0, high_freq_factor=4.0,
+              original_max_pos=8192)
+EXT_CASES = [
+    # dtype, T, nq, nk, hd, variant, QK norm, layout
+    (nm.BF16, 5, 8, 2, 128, dict(rotary_dim=64), False, "plain"),
+    (nm.BF16, 5, 8, 2, 128, dict(rotary_dim=96), False, "plain"),
+    (nm.F32, 5, 8, 2, 128, dict(rotary_dim=32), False, "plain"),
+    (nm.BF16, 5, 8, 2, 128, dict(interleaved=1), False, "plain"),
+    (nm.F32, 9, 8, 2, 64, dict(interleaved=1), False, "plain"),
+    (nm.F32, 3, 2, 2, 512, dict(interleaved=1), False, "plain"),
+    (nm.BF16, 3, 2, 2, 512, dict(interleaved=1), True, "plain"),
+    (nm.F32, 3, 2, 2, 512, dict(interleaved=1), True, "plain"),
+    (nm.BF16, 7, 8, 2, 128, dict(interleaved=1, rotary_dim=64), False, "plain"),
+    (nm.BF16, 7, 8, 2, 96, dict(interleaved=1), False, "plain"),
+    (nm.BF16, 6, 8, 2, 128, dict(pos_int64=1), False, "plain"),
+    (nm.F32, 6, 8, 2, 128, LLAMA3, False, "plain"),
+    (nm.BF16, 6, 32, 8, 128, dict(LLAMA3, rotary_dim=64, interleaved=1, pos_int64=1), False,
+     "plain"),
+    (nm.BF16, 6, 8, 2, 128, dict(cache=1), False, "plain"),
+    (nm.F32, 6, 8, 2, 64, dict(cache=1, interleaved=1, pos_int64=1), False, "plain"),
+    (nm.BF16, 5, 8, 2, 128, dict(rotary_dim=64), True, "plain"),
+    (nm.BF16, 5, 8, 2, 128, dict(interleaved=1), True, "plain"),
+    (nm.F32, 5, 8, 2, 128, dict(interleaved=1, cache=1), True, "plain"),
+    (nm.BF16, 5, 8, 2, 128, dict(interleaved=1), False, "unaligned"),
+    (nm.F32, 4, 300, 20, 64, dict(interleaved=1, rotary_dim=48), True, "unaligned"),
+]
+
+
+@pytest.mark.parametrize("dtype,T,nq,nk,hd,ext,qkn,layout", EXT_CASES)
+def test_rope_variant_cases(tri, cache, dtype, T, nq, nk, hd, ext, qkn, layout):
+    r = rng(T * 3 + nq * 7 + hd + 5 * len(ext) + qkn)
+    q = wl.host_array(r, (T, nq, hd), dtype)
+    k = wl.host_array(r, (T, nk, hd), dtype)
+    qw, kw = wl.host_weight(r, hd, dtype), wl.host_weight(r, hd, dtype)
+    ext = dict(ext)
+    rd = ext.get("rotary_dim") or hd
+    table = None
+    if ext.pop("cache", 0):
+        table = wl.cos_sin_table(r, 300, rd)
+        pos = r.integers(-20, 320, size=T)              # some clamp at either end
+    elif ext.get("pos_int64"):
+        pos = r.integers(0, 1 << 40, size=T)
+    else:
+        pos = r.integers(0, 131072, size=T)
+    pos = pos.astype(np.int64 if ext.get("pos_int64") else np.int32)
+    qd = place(q, dtype, layout)
+    kd = place(k, dtype, layout)
+    td = torch.from_numpy(table).to(DEV) if table is not None else None
+    x = binding_rope_ext(tri, ext, td)
+    cache.rope(qd, kd, torch.from_numpy(pos).to(DEV), 5e5, x,
+               q_w=wl.to_torch(qw, dtype, DEV) if qkn else None,
+               k_w=wl.to_torch(kw, dtype, DEV) if qkn else None, eps=1e-6)
+    torch.cuda.synchronize()
+    wq, wk = O.rope_ext(q, k, pos, 5e5, dtype, q_w=qw if qkn else None, k_w=kw if qkn else None,
+                        eps=1e-6, **oracle_rope_kw(ext, table))
+    check("q", host(qd), wq, dtype)
+    check("k", host(kd), wk, dtype)
+    mext = dict(ext, cos_sin=td.data_ptr() if td is not None else None,
+                cos_sin_len=300 if td is not None else 0)
+    c = S.Call(S.OP_QK_NORM_ROPE if qkn else S.OP_ROPE_QK,
+               S.DT_F32 if dtype == nm.F32 else S.DT_BF16, T, hd=hd, nq=nq, nk=nk, base=5e5,
+               ptr=dict(q=qd.data_ptr(), k=kd.data_ptr(), pos=0, q_w=0, k_w=0),
+               stride=dict(q=qd.stride(0), k=kd.stride(0)), ext=mext)
+    assert cache.last_selection().variant == S.plan(S.make_key(c), T)[0]
+    if not qkn and rd < hd:          # elements past the rotary span are untouched
+        check("q tail", host(qd)[..., rd:], q[..., rd:], dtype, exact=True)
+
+
 # ---- SwiGLU: every variant ---------------------------------------------------------------
 SW_CASES = [
     # dtype, T, I, layout
@@ -359,7 +444,13 @@ MEDIUM = [wl.ChainConfig("medium_bf16", wl.BF16, T=100, H=4096, nq=32, nk=8, hd=
           wl.ChainConfig("medium_qkn_bf16", wl.BF16, T=100, H=4096, nq=32, nk=8, hd=128,
                          I=12288, base=1e6, pos_mode="uniform", pos_max=8191, qk_norm=True),
           wl.ChainConfig("ragged_qkn_f32", wl.F32, T=67, H=512, nq=5, nk=3, hd=128, I=1001,
-                         base=1e6, pos_mode="uniform", pos_max=100000, qk_norm=True)]
+                         base=1e6, pos_mode="uniform", pos_max=100000, qk_norm=True),
+          wl.ChainConfig("medium_gptj_bf16", wl.BF16, T=100, H=4096, nq=16, nk=16, hd=256,
+                         I=16384, pos_mode="uniform", pos_max=2047,
+                         rope=(("rotary_dim", 64), ("interleaved", 1))),
+          wl.ChainConfig("medium_llama31_qkn_bf16", wl.BF16, T=90, H=4096, nq=32, nk=8, hd=128,
+                         I=14336, base=5e5, pos_mode="uniform", pos_max=131071, qk_norm=True,
+                         rope=wl.LLAMA3_SCALING + (("interleaved", 1),))]
 
 
 @pytest.mark.parametrize("cfg", MEDIUM, ids=lambda c: c.name)
@@ -372,12 +463,12 @@ def test_chain_beyond_decode_sizes(tri, cache, cfg):
                                       torch.empty_like(d["gate"]))
     run_chain(cache, cfg, d)
     torch.cuda.synchronize()
-    want = O.decode_chain(inp, cfg.eps, cfg.base, cfg.dtype)
+    want = chain_oracle(inp, cfg)
     for n in ("y", "q", "k", "out"):
         check(n, host(d[n]), want[n], cfg.dtype)
     check("res_out", host(d["res_out"]), want["res_out"], cfg.dtype, exact=True)
     rec = cache.last_selection().as_tuple()
-    assert rec == expected_record(model_chain_call(d, cfg.eps, cfg.base), 0)
+    assert rec == expected_record(model_chain_call(d, cfg.eps, cfg.base, ext=cfg.rope_ext), 0)
 
 
 # ---- chain layouts, degenerate calls, miss path ----------------------------------------------

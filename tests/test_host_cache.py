@@ -4,6 +4,7 @@ Checks the library's guards, ordered dispatch (Algorithm 1, Sec. 3.2), the
 miss / install / error paths (Sec. 3.5), argument preparation and the
 selection records -- bit for bit against the oracle's selection model.
 """
+import collections
 import ctypes as C
 import math
 import struct
@@ -14,8 +15,8 @@ import pytest
 from oracle import ops as O
 from oracle import selection as S
 from tests.native_libs import load_fake
-from tests.selection_calls import (chain_call, elem_offset, qkn_call, res_call, rn_call,
-                                   rope_call, sw_call)
+from tests.selection_calls import (CACHE_ADDR, chain_call, elem_offset, qkn_call, res_call,
+                                   rn_call, rope_call, sw_call)
 import workloads as wl
 
 BF, F = S.DT_BF16, S.DT_F32
@@ -51,6 +52,11 @@ def c_call(lib, cache, c: S.Call, stream=None):
         return lib.tri_residual_rmsnorm(cache, c.dtype, p.get("x"), s["x"], p.get("res"),
                                         s["res"], p.get("w"), p.get("y"), s["y"],
                                         p.get("res_out"), s["res_out"], c.T, c.H, c.eps, stream)
+    if c.op in (S.OP_ROPE_QK, S.OP_QK_NORM_ROPE) and c.ext is not None:
+        return lib.tri_rope_qk_ext(cache, c.dtype, p.get("q"), s["q"], p.get("k"), s["k"],
+                                   p.get("pos"), c.T, c.nq, c.nk, c.hd, c.base,
+                                   C.byref(c_ext(c.ext)), p.get("q_w") if c.op == 6 else None,
+                                   p.get("k_w"), c.eps, stream)
     if c.op == S.OP_ROPE_QK:
         return lib.tri_rope_qk(cache, c.dtype, p.get("q"), s["q"], p.get("k"), s["k"],
                                p.get("pos"), c.T, c.nq, c.nk, c.hd, c.base, stream)
@@ -76,7 +82,20 @@ def c_call(lib, cache, c: S.Call, stream=None):
     a.up, a.u_rs = p.get("up"), s["up"]
     a.out, a.o_rs = p.get("out"), s["out"]
     a.q_norm_w, a.k_norm_w, a.qk_eps = p.get("q_w"), p.get("k_w"), c.qk_eps
+    if c.ext is not None:
+        x = c_ext(c.ext)
+        a.rope_ext = C.pointer(x)
     return lib.tri_decode_chain(cache, C.byref(a), stream)
+
+
+def c_ext(ext):
+    from paper_2609_37241_amd._lib import RopeExt
+    x = RopeExt()
+    full = dict(S.PLAIN_EXT)
+    full.update(ext)
+    for n, _ in RopeExt._fields_:
+        setattr(x, n, full[n] if full[n] is not None else 0)
+    return x
 
 
 def c_record(lib, cache):
@@ -126,6 +145,16 @@ def run_both(lib, cache, m, c, install=True):
     return st_c
 
 
+LLAMA3 = dict(scaling=S.SCALING_LLAMA3, factor=8.0, low_freq_factor=1.0, high_freq_factor=4.0,
+              original_max_pos=8192)
+ROPE_EXTS = [dict(rotary_dim=64), dict(rotary_dim=32), dict(rotary_dim=96), dict(interleaved=1),
+             dict(interleaved=1, rotary_dim=64), dict(pos_int64=1), LLAMA3,
+             dict(LLAMA3, rotary_dim=64, interleaved=1, pos_int64=1),
+             dict(cos_sin=CACHE_ADDR, cos_sin_len=4096),
+             dict(cos_sin=CACHE_ADDR, cos_sin_len=1, interleaved=1, pos_int64=1),
+             dict(rotary_dim=0, interleaved=0, pos_int64=0, scaling=0)]
+
+
 def call_zoo():
     """Calls over every op, dtype, size class, layout and error kind."""
     calls = []
@@ -147,6 +176,14 @@ def call_zoo():
             calls.append(qkn_call(d, T, 32, 8, 128, w_off=off))
             calls.append(qkn_call(d, T, 32, 8, 128, off=off))
             calls.append(qkn_call(d, T, 32, 8, 128, pad=64))
+            for ext in ROPE_EXTS:
+                calls.append(rope_call(d, T, 32, 8, 128, base=5e5, ext=ext))
+                calls.append(qkn_call(d, T, 8, 2, 64, base=5e5, ext=ext))
+            calls.append(rope_call(d, T, 4, 4, 64, off=off, ext=dict(interleaved=1)))
+            calls.append(rope_call(d, T, 4, 4, 96, ext=dict(rotary_dim=32, interleaved=1)))
+            calls.append(rope_call(d, T, 4, 4, 2, ext=dict(interleaved=1)))
+            calls.append(rope_call(d, T, 2, 2, 512, ext=dict(interleaved=1)))
+            calls.append(qkn_call(d, T, 2, 2, 512, ext=dict(interleaved=1)))
             for I in (688, 11008, 14336, 28672, 11003, 1):
                 calls.append(sw_call(d, T, I))
             calls.append(sw_call(d, T, 11008, off=off))
@@ -162,6 +199,10 @@ def call_zoo():
             calls.append(chain_call(d, T, 4096, 12288, 32, 8, 128, base=1e6, qk_norm=True,
                                     w_off=off))
             calls.append(chain_call(d, T, 256, 688, 4, 0, 64, qk_norm=True))
+            for ext in ROPE_EXTS[::2]:
+                calls.append(chain_call(d, T, 4096, 14336, 32, 8, 128, base=5e5, ext=ext))
+                calls.append(chain_call(d, T, 4096, 12288, 32, 8, 128, base=1e6, ext=ext,
+                                        qk_norm=True))
     # errors
     calls += [rn_call(BF, 1, 4096, null=("x",)), rn_call(BF, -1, 4096), rn_call(BF, 1, 0),
               rn_call(BF, 1, 4096, eps=float("nan")), rn_call(BF, 1, 4096, eps=-1.0),
@@ -184,6 +225,33 @@ def call_zoo():
               chain_call(BF, 1, 4096, 12288, 32, 8, 128, qk_norm=True, qk_eps=float("inf")),
               chain_call(BF, 1, 4096, 12288, 32, 8, 128, qk_norm=True, w_off=1),
               chain_call(BF, 1, 4096, 12288, 32, 8, 128, qk_eps=float("nan")),
+              rope_call(BF, 1, 4, 4, 64, ext=dict(rotary_dim=3)),
+              rope_call(BF, 1, 4, 4, 64, ext=dict(rotary_dim=66)),
+              rope_call(BF, 1, 4, 4, 64, ext=dict(rotary_dim=-2)),
+              rope_call(BF, 1, 4, 4, 1024, ext=dict(rotary_dim=3)),
+              rope_call(BF, 1, 4, 4, 64, ext=dict(interleaved=2)),
+              rope_call(BF, 1, 4, 4, 64, ext=dict(pos_int64=3)),
+              rope_call(BF, 1, 4, 4, 64, ext=dict(scaling=2)),
+              rope_call(BF, 1, 4, 4, 64, pos_off=4, ext=dict(pos_int64=1)),
+              rope_call(BF, 1, 4, 4, 64, pos_off=4),
+              rope_call(BF, 1, 4, 4, 64, ext=dict(cos_sin=CACHE_ADDR + 2, cos_sin_len=8)),
+              rope_call(BF, 1, 4, 4, 64, ext=dict(cos_sin=CACHE_ADDR, cos_sin_len=0)),
+              rope_call(BF, 1, 4, 4, 64, ext=dict(cos_sin=CACHE_ADDR, cos_sin_len=8,
+                                                  **LLAMA3)),
+              rope_call(BF, 1, 4, 4, 64, base=1.0, ext=dict(cos_sin=CACHE_ADDR, cos_sin_len=8)),
+              rope_call(BF, 1, 4, 4, 64, base=float("nan"),
+                        ext=dict(cos_sin=CACHE_ADDR, cos_sin_len=8)),
+              rope_call(BF, 1, 4, 4, 64, base=1.0, ext=LLAMA3),
+              rope_call(BF, 1, 4, 4, 64, ext=dict(LLAMA3, factor=0.0)),
+              rope_call(BF, 1, 4, 4, 64, ext=dict(LLAMA3, factor=float("inf"))),
+              rope_call(BF, 1, 4, 4, 64, ext=dict(LLAMA3, low_freq_factor=-1.0)),
+              rope_call(BF, 1, 4, 4, 64, ext=dict(LLAMA3, high_freq_factor=1.0)),
+              rope_call(BF, 1, 4, 4, 64, ext=dict(LLAMA3, high_freq_factor=float("nan"))),
+              rope_call(BF, 1, 4, 4, 64, ext=dict(LLAMA3, original_max_pos=0)),
+              qkn_call(BF, 1, 4, 4, 64, ext=dict(rotary_dim=80)),
+              qkn_call(BF, 1, 4, 4, 64, null=("k_w",), ext=dict(interleaved=1)),
+              chain_call(BF, 1, 4096, 11008, 32, 32, 128, ext=dict(rotary_dim=130)),
+              chain_call(BF, 1, 4096, 11008, 32, 32, 128, ext=dict(LLAMA3, factor=-8.0)),
               sw_call(BF, 1, 0), sw_call(BF, 1, S.I_LIMIT), sw_call(BF, 1, 64, null=("up",)),
               sw_call(BF, 1, 64, off=1), sw_call(BF, 3, 64, pad=-1)]
     return calls
@@ -293,7 +361,13 @@ def test_status_strings(lib):
 
 # ---- argument preparation ----------------------------------------------------------
 # Argument struct sizes the kernels take (RnArgs, RopeArgs, SwArgs, ChainArgs).
-ARG_SIZES = {"rn": 88, "rope": 88, "sw": 80, "chain": 264}
+ARG_SIZES = {"rn": 88, "rope": 112, "sw": 80, "chain": 288}
+RopeBlock = collections.namedtuple(
+    "RopeBlock", "q k pos inv qw kw cos_sin q_ts k_ts T cs_len nq nk hd rd eps mode")
+
+
+def rope_block(raw, off=0):
+    return RopeBlock(*struct.unpack_from("<7Q4q4ifI", raw, off))
 
 
 def _last_launch(lib, nbytes=512, size=None):
@@ -329,17 +403,18 @@ def test_chain_argument_block(lib, fresh):
     assert c_call(lib, cache, c) == 0
     kv, dt, sub, grid, block, _, raw = _last_launch(lib, size="chain")
     # fused kernel: RN_BLOCK_2 (norm role index 3), plain RoPE, cached one-vector SwiGLU
-    assert (kv, dt, sub, grid, block) == (50, BF, 3 * 4, 8 + 8 + 56, 256)
-    rope = struct.unpack_from("<6Q3q3if", raw, 88)
-    assert rope[0] == c.ptr["q"] and rope[1] == c.ptr["k"] and rope[2] == c.ptr["pos"]
-    assert rope[4:6] == (0, 0) and rope[12] == 0.0
-    assert rope[6:9] == (32 * 128, 8 * 128, 8) and rope[9:12] == (32, 8, 128)
-    sw = struct.unpack_from("<3Q7q", raw, 176)
+    assert (kv, dt, sub, grid, block) == (50, BF, 3 * 8, 8 + 8 + 56, 256)
+    rope = rope_block(raw, 88)
+    assert (rope.q, rope.k, rope.pos) == (c.ptr["q"], c.ptr["k"], c.ptr["pos"])
+    assert (rope.qw, rope.kw, rope.cos_sin, rope.eps, rope.mode) == (0, 0, 0, 0.0, 0)
+    assert (rope.q_ts, rope.k_ts, rope.T, rope.cs_len) == (32 * 128, 8 * 128, 8, 0)
+    assert (rope.nq, rope.nk, rope.hd, rope.rd) == (32, 8, 128, 128)
+    sw = struct.unpack_from("<3Q7q", raw, 200)
     assert sw[:3] == (c.ptr["gate"], c.ptr["up"], c.ptr["out"])
     assert sw[3:] == (14336, 14336, 14336, 8, 14336, 8 * 14336 // 8, 8 * 14336)
-    assert struct.unpack_from("<2I", raw, 256) == (8, 8)
+    assert struct.unpack_from("<2I", raw, 280) == (8, 8)
     # the RoPE table pointer is this version's uploaded constants
-    assert rope[3] != 0
+    assert rope.inv != 0
 
 
 def test_qk_norm_chain_argument_block(lib, fresh):
@@ -348,25 +423,25 @@ def test_qk_norm_chain_argument_block(lib, fresh):
     assert c_call(lib, cache, c) == 0
     kv, dt, sub, grid, block, _, raw = _last_launch(lib, size="chain")
     # RN_BLOCK_2 with the QK-norm RoPE role and cached SwiGLU
-    assert (kv, dt, sub, grid, block) == (50, BF, 3 * 4 + 2, 1 + 1 + 6, 256)
-    rope = struct.unpack_from("<6Q3q3if", raw, 88)
-    assert rope[4:6] == (c.ptr["q_w"], c.ptr["k_w"])
-    assert rope[12] == np.float32(1e-5)
+    assert (kv, dt, sub, grid, block) == (50, BF, 3 * 8 + 2, 1 + 1 + 6, 256)
+    rope = rope_block(raw, 88)
+    assert (rope.qw, rope.kw) == (c.ptr["q_w"], c.ptr["k_w"])
+    assert rope.eps == np.float32(1e-5)
     assert S.unpack_key(S.make_key(c))["flags"] == 0x7F
     # the standalone op launches the same role body with the same block
     c2 = qkn_call(BF, 1, 32, 8, 128, base=1e6, eps=1e-5)
     assert c_call(lib, cache, c2) == 0
     kv2, _, _, grid2, _, _, raw2 = _last_launch(lib, size="rope")
     assert (kv2, grid2) == (S.ROPE_QKN_VEC, 1)
-    assert struct.unpack_from("<6Q3q3if", raw2, 0)[4:] == rope[4:]
+    assert rope_block(raw2)[4:] == rope[4:]   # all but the per-version table
 
 
 def test_qk_norm_without_k_heads_passes_no_k_weight(lib, fresh):
     cache = fresh(flags=1)
     c = qkn_call(F, 2, 4, 0, 64)
     assert c_call(lib, cache, c) == 0
-    rope = struct.unpack_from("<6Q3q3if", _last_launch(lib, size="rope")[6], 0)
-    assert rope[1] == 0 and rope[4] == c.ptr["q_w"] and rope[5] == 0
+    rope = rope_block(_last_launch(lib, size="rope")[6])
+    assert rope.k == 0 and rope.qw == c.ptr["q_w"] and rope.kw == 0
 
 
 @pytest.mark.parametrize("base,hd", [(10000.0, 64), (10000.0, 128), (500000.0, 128),
@@ -382,6 +457,56 @@ def test_rope_table_matches_oracle_exactly(lib, fresh, base, hd):
     want = O.rope_inv_freq(base, hd)
     assert n.value == hd // 2
     assert np.array_equal(got.view(np.uint32), want.view(np.uint32))
+
+
+@pytest.mark.parametrize("base,hd,rd", [(5e5, 128, 128), (5e5, 128, 64), (1e4, 64, 32),
+                                        (5e5, 256, 256), (1e6, 128, 96)])
+def test_llama3_table_matches_oracle_exactly(lib, fresh, base, hd, rd):
+    cache = fresh(flags=1)
+    assert c_call(lib, cache, rope_call(BF, 3, 4, 2, hd, base=base,
+                                        ext=dict(LLAMA3, rotary_dim=rd))) == 0
+    n = C.c_uint32()
+    buf = (C.c_float * 256)()
+    assert lib.tri_spec_version_constants(cache, 0, buf, 256, C.byref(n)) == 0
+    got = np.array(buf[: n.value], dtype=np.float32)
+    want = O.rope_inv_freq_llama3(base, rd, 8.0, 1.0, 4.0, 8192)
+    assert n.value == rd // 2
+    assert np.array_equal(got.view(np.uint32), want.view(np.uint32))
+
+
+def test_partial_rotary_table_and_cache_mode_constants(lib, fresh):
+    cache = fresh(flags=1)
+    assert c_call(lib, cache, rope_call(F, 2, 4, 2, 128, ext=dict(rotary_dim=32))) == 0
+    assert c_call(lib, cache, rope_call(F, 2, 4, 2, 128,
+                                        ext=dict(cos_sin=CACHE_ADDR, cos_sin_len=9))) == 0
+    n = C.c_uint32()
+    buf = (C.c_float * 256)()
+    assert lib.tri_spec_version_constants(cache, 0, buf, 256, C.byref(n)) == 0
+    assert np.array_equal(np.array(buf[:n.value], dtype=np.float32), O.rope_inv_freq(1e4, 32))
+    assert lib.tri_spec_version_constants(cache, 1, buf, 256, C.byref(n)) == 0
+    assert n.value == 0
+    rope = rope_block(_last_launch(lib, size="rope")[6])
+    assert (rope.inv, rope.cos_sin, rope.cs_len, rope.mode) == (0, CACHE_ADDR, 9, 4)
+
+
+def test_rope_ext_argument_block(lib, fresh):
+    cache = fresh(flags=1)
+    c = rope_call(BF, 3, 8, 2, 128, ext=dict(rotary_dim=64, interleaved=1, pos_int64=1))
+    assert c_call(lib, cache, c) == 0
+    kv, _, _, grid, _, _, raw = _last_launch(lib, size="rope")
+    assert (kv, grid) == (S.ROPE_VEC_I, 3)
+    rope = rope_block(raw)
+    assert (rope.hd, rope.rd, rope.mode, rope.pos) == (128, 64, 1 | 2, c.ptr["pos"])
+
+
+def test_plain_ext_shares_versions_with_the_plain_entry(lib, fresh):
+    # A zeroed variant struct and the plain entry point make the same key.
+    cache = fresh()
+    m = S.SpecCacheModel()
+    run_both(lib, cache, m, rope_call(BF, 1, 32, 8, 128))
+    run_both(lib, cache, m, rope_call(BF, 1, 32, 8, 128, ext={}))
+    run_both(lib, cache, m, rope_call(BF, 1, 32, 8, 128, ext=dict(rotary_dim=128)))
+    assert m.stats.installs == 1 and m.stats.hits == 3
 
 
 def test_version_info(lib, fresh):

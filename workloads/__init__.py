@@ -46,7 +46,12 @@ class ChainConfig:
     pos_max: int = 0               # inclusive upper bound for "uniform"
     outliers: bool = False         # element-wise Bernoulli(1e-3) x 50
     qk_norm: bool = False          # per-head RMSNorm of Q and K before RoPE
+    rope: Tuple = ()               # RoPE variant as (name, value) pairs; () = plain
     seed: int = 0
+
+    @property
+    def rope_ext(self) -> Optional[dict]:
+        return dict(self.rope) if self.rope else None
 
 
 # The five workloads. Unstated parameters: eps 1e-6 everywhere; RoPE base
@@ -66,8 +71,22 @@ QWEN3_8B_DECODE = ChainConfig("qwen3_8b_decode_bf16", BF16, T=1, H=4096, nq=32, 
                               I=12288, base=1000000.0, pos_mode="uniform", pos_max=8191,
                               qk_norm=True)
 
+# Llama-3.1-8B-shaped decode step: Llama-3 frequency scaling (factor 8,
+# low / high frequency factors 1 / 4, original context 8192), base 5e5.
+LLAMA3_SCALING = (("scaling", 1), ("factor", 8.0), ("low_freq_factor", 1.0),
+                  ("high_freq_factor", 4.0), ("original_max_pos", 8192))
+LLAMA31_8B_DECODE = ChainConfig("llama31_8b_decode_bf16", BF16, T=1, H=4096, nq=32, nk=8, hd=128,
+                                I=14336, base=500000.0, pos_mode="uniform", pos_max=131071,
+                                rope=LLAMA3_SCALING)
+
+# GPT-J-6B-shaped step: 16 heads of 256 with GPT-J pairs over the first 64
+# elements of each head (hidden 4096, intermediate 16384).
+GPTJ_DECODE = ChainConfig("gptj_decode_bf16", BF16, T=4, H=4096, nq=16, nk=16, hd=256, I=16384,
+                          pos_mode="uniform", pos_max=2047,
+                          rope=(("rotary_dim", 64), ("interleaved", 1)))
+
 CONFIGS = {c.name: c for c in (TINY_F32, LLAMA7B_DECODE, GQA_DECODE, PREFILL_8K,
-                               QWEN3_8B_DECODE)}
+                               QWEN3_8B_DECODE, LLAMA31_8B_DECODE, GPTJ_DECODE)}
 
 # Mixed-shape stream: token counts, dtype mix and layout anomalies.
 MIXED_T_CHOICES = (1, 2, 4, 8, 16, 32, 64, 128, 512)
@@ -154,6 +173,13 @@ def host_inputs(cfg: ChainConfig, T: Optional[int] = None,
         out["q_norm_w"] = _weight(rng, cfg.hd, d)
         out["k_norm_w"] = _weight(rng, cfg.hd, d)
     return out
+
+
+def cos_sin_table(rng, n: int, rd: int) -> np.ndarray:
+    """A float32 [n, rd] table of (cos, sin) pairs of random angles
+    U(-pi, pi): cos in the first rd/2 columns, sin in the rest."""
+    th = rng.uniform(-np.pi, np.pi, size=(n, rd // 2))
+    return np.concatenate([np.cos(th), np.sin(th)], axis=1).astype(np.float32)
 
 
 def host_array(rng, shape, dtype, outliers=False):
