@@ -332,6 +332,40 @@ def main():
     assert st == 0, st
     latency["llama3_scaled_decode_chain_e2e_us"] = summary(list(e2e[:n2]))
 
+    # ---- one decode step of 32 layers: one entry call vs 32 calls ------------------------
+    bench.trib_layers.argtypes = [C.c_void_p, C.c_int, C.c_void_p, C.c_int, C.c_void_p, C.c_int,
+                                  C.c_int, C.POINTER(C.c_double)]
+    n_layers = 32
+    lay_bufs = []
+    lay_args = (tri.ChainArgs * n_layers)()
+    for l in range(n_layers):
+        dl = {k: v.clone() for k, v in d.items()}
+        al, outs_l = cache.chain_args(dl["x"], dl["residual"], dl["w"], dl["q"], dl["k"],
+                                      dl["pos"], dl["gate"], dl["up"], cfg.eps, cfg.base)
+        lay_bufs.append((dl, outs_l))
+        lay_args[l] = al
+    n3 = min(K, 2000)
+    steps = {}
+    for mode, name in ((0, "one_call"), (1, "per_layer_calls")):
+        st = bench.trib_layers(cache.handle, mode, lay_args, n_layers, sptr, 20, n3, e2e)
+        assert st == 0, st
+        steps[name] = summary(list(e2e[:n3]))
+    layer_list = [lay_args[l] for l in range(n_layers)]
+    g32 = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g32, stream=stream):
+        cache.decode_chain_layers(layer_list, stream=torch.cuda.current_stream())
+    g32.replay()
+    stream.synchronize()
+    rep = []
+    for _ in range(n3):
+        a = time.perf_counter()
+        g32.replay()
+        stream.synchronize()
+        rep.append((time.perf_counter() - a) * 1e6)
+    steps["hip_graph_replay"] = summary(rep)
+    latency["decode_step_32_layers_e2e_us"] = steps
+    del lay_bufs, g32
+
     # ---- mixed-shape stream: guard hits, misses, latency per token bucket ---------------
     mixed = None if args.no_stream else run_mixed_stream(tri, wl, bench, dev, stream, torch)
 

@@ -68,8 +68,11 @@ typedef enum tri_status {
 
 typedef enum tri_op {
   TRI_OP_RMSNORM = 1, TRI_OP_RES_RMSNORM = 2, TRI_OP_ROPE_QK = 3,
-  TRI_OP_SWIGLU = 4, TRI_OP_CHAIN = 5, TRI_OP_QK_NORM_ROPE = 6
+  TRI_OP_SWIGLU = 4, TRI_OP_CHAIN = 5, TRI_OP_QK_NORM_ROPE = 6,
+  TRI_OP_CHAIN_LAYERS = 7   /* selection records of tri_decode_chain_layers */
 } tri_op;
+
+enum { TRI_MAX_LAYERS = 1024 };   /* layers per tri_decode_chain_layers call */
 
 enum { TRI_CACHE_AUTO_INSTALL = 1u };   /* on a miss: install, then launch */
 
@@ -281,6 +284,25 @@ tri_status tri_swiglu(tri_cache *cache, tri_dtype dtype,
  * ones may already be enqueued; E_LAUNCH is returned and no other version is
  * tried. */
 tri_status tri_decode_chain(tri_cache *cache, const tri_chain_args *args, void *stream);
+
+/* Several decode chains in one entry call, e.g. the chains of every layer of
+ * one decode step: layers[0 .. n_layers) run in array order on `stream`, so
+ * a layer may consume an earlier layer's outputs. Pass 1 validates each
+ * layer, packs its key and looks its version up (installing it under
+ * TRI_CACHE_AUTO_INSTALL), in layer order; the first layer that fails
+ * validation returns its error, and without auto-install the first layer
+ * that misses returns MISS with its key recorded for
+ * tri_spec_install_last_miss. In both cases NOTHING is launched. Pass 2
+ * launches every layer (layers with T == 0 are skipped); a launch failure
+ * returns E_LAUNCH with the earlier launches already enqueued.
+ * n_layers 0..TRI_MAX_LAYERS (0, or all layers empty: OK, an empty call).
+ * One entry call counts once in the statistics; a hit counts one hit on
+ * each layer's version. The selection record has op TRI_OP_CHAIN_LAYERS,
+ * the version, variant, roles, launches and key of the last launched layer,
+ * and n_launches = the launches of all layers. Not in the paper: it
+ * amortises the single native entry over a whole decode step. */
+tri_status tri_decode_chain_layers(tri_cache *cache, const tri_chain_args *layers,
+                                   uint32_t n_layers, void *stream);
 
 /* ---- miss handling, introspection -------------------------------------------- */
 

@@ -39,6 +39,8 @@ import numpy as np
 # ---- enumerations (the ABI's numeric values) --------------------------------
 OP_RMSNORM, OP_RES_RMSNORM, OP_ROPE_QK, OP_SWIGLU, OP_CHAIN, OP_QK_NORM_ROPE = 1, 2, 3, 4, 5, 6
 ROPE_OPS = (OP_ROPE_QK, OP_QK_NORM_ROPE, OP_CHAIN)
+OP_CHAIN_LAYERS = 7        # records of the several-chains entry point
+MAX_LAYERS = 1024
 DT_F32, DT_BF16 = 0, 1
 OK, MISS = 0, 1
 E_INVALID, E_UNSUPPORTED, E_FULL, E_NOMEM, E_LAUNCH, E_RUNTIME = -1, -2, -3, -4, -5, -6
@@ -575,6 +577,78 @@ class SpecCacheModel:
         if not auto:
             self.stats.hits += 1
             self.version_hits[i] += 1
+        return OK
+
+    def call_layers(self, calls: List[Call]) -> int:
+        """Several decode chains in one entry call: validate and look up every
+        layer first (nothing installed or launched if one fails or, without
+        auto-install, misses), then launch them in order. One call in the
+        statistics; a hit counts a hit on every layer's version."""
+        self.stats.calls += 1
+        rec = Record(op=OP_CHAIN_LAYERS)
+
+        def done(st):
+            rec.status = st
+            self.last = rec
+            return st
+        if len(calls) > MAX_LAYERS:
+            self.stats.errors += 1
+            return done(E_INVALID)
+        keys, vis = [], []
+        first_miss, last = None, None
+        for i, c in enumerate(calls):
+            st = validate(c)
+            if st == OK:
+                keys.append(None)
+                vis.append(None)
+                continue
+            if st is not None:
+                self.stats.errors += 1
+                return done(st)
+            k = make_key(c)
+            keys.append(k)
+            vis.append(self.lookup(k))
+            if vis[-1] < 0 and first_miss is None:
+                first_miss = i
+            last = i
+        if last is None:
+            self.stats.empty += 1
+            return done(OK)
+        missed = first_miss is not None
+        if missed:
+            self.stats.misses += 1
+            self.last_miss = (keys[first_miss], calls[first_miss].T)
+            rec.key = keys[first_miss]
+            if not (self.flags & FLAG_AUTO_INSTALL):
+                return done(MISS)
+            for i in range(first_miss, last + 1):
+                if vis[i] is not None and vis[i] < 0:
+                    st = self._install(keys[i])
+                    if st < 0:
+                        return done(st)
+                    vis[i] = self.lookup(keys[i])
+        total = 0
+        for i, c in enumerate(calls):
+            if vis[i] is None:
+                continue
+            variant, roles, launches = plan(keys[i], c.T)
+            st = self._launch(launches)
+            total += len(launches)
+            if st < 0 or i == last:
+                rec = Record(op=OP_CHAIN_LAYERS, status=st, version=vis[i], variant=variant,
+                             n_launches=total, roles=roles,
+                             launch=tuple(launches) + ((0, 0, 0),) * (3 - len(launches)),
+                             key=keys[i])
+                self.last = rec
+            if st < 0:
+                if not missed:
+                    self.stats.errors += 1
+                return st
+        if not missed:
+            self.stats.hits += 1
+            for v in vis:
+                if v is not None:
+                    self.version_hits[v] += 1
         return OK
 
     def _install(self, key) -> int:

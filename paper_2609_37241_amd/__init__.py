@@ -127,9 +127,13 @@ class SpecCache:
         return self._h
 
     # ---- miss path ---------------------------------------------------------
-    def _call(self, what: str, fn, *args) -> None:
+    def _call(self, what: str, fn, *args, max_misses: int = 1) -> None:
+        """One entry call; on MISS install the recorded key and call again
+        (a call over several layers can miss once per distinct version)."""
         st = fn(self._h, *args)
-        if st == MISS:
+        for _ in range(max_misses):
+            if st != MISS:
+                break
             self.install_last_miss()
             self.misses_handled += 1
             st = fn(self._h, *args)
@@ -259,6 +263,13 @@ class SpecCache:
     def decode_chain_args(self, args: ChainArgs, stream=None) -> None:
         self._call("tri_decode_chain", _dll.tri_decode_chain, C.byref(args),
                    _stream_ptr(stream))
+
+    def decode_chain_layers(self, layers, stream=None) -> None:
+        """Several chains (a list of ChainArgs from chain_args) in one entry
+        call, launched in list order (tri_decode_chain_layers)."""
+        arr = (ChainArgs * max(1, len(layers)))(*layers)
+        self._call("tri_decode_chain_layers", _dll.tri_decode_chain_layers, arr, len(layers),
+                   _stream_ptr(stream), max_misses=len(layers))
 
     def decode_chain(self, x, residual, w, q, k, pos, gate, up, eps=1e-6, base=10000.0,
                      y=None, residual_out=None, out=None, stream=None, q_norm_w=None,

@@ -17,6 +17,8 @@ OK, MISS = 0, 1
 E_INVALID, E_UNSUPPORTED, E_FULL, E_NOMEM, E_LAUNCH, E_RUNTIME = -1, -2, -3, -4, -5, -6
 F32, BF16 = 0, 1
 OP_RMSNORM, OP_RES_RMSNORM, OP_ROPE_QK, OP_SWIGLU, OP_CHAIN, OP_QK_NORM_ROPE = 1, 2, 3, 4, 5, 6
+OP_CHAIN_LAYERS = 7
+MAX_LAYERS = 1024
 AUTO_INSTALL = 1
 KEY_WORDS = 6
 ROPE_SCALING_NONE, ROPE_SCALING_LLAMA3 = 0, 1
@@ -99,6 +101,7 @@ SIGNATURES = {
                                    _F, _P, _P, _F, _P]),
     "tri_swiglu": (C.c_int, [_P, C.c_int, _P, _I64, _P, _I64, _P, _I64, _I64, _I64, _P]),
     "tri_decode_chain": (C.c_int, [_P, C.POINTER(ChainArgs), _P]),
+    "tri_decode_chain_layers": (C.c_int, [_P, C.POINTER(ChainArgs), _U32, _P]),
     "tri_spec_install_last_miss": (C.c_int, [_P, C.POINTER(Selection)]),
     "tri_spec_last_selection": (C.c_int, [_P, C.POINTER(Selection)]),
     "tri_spec_stats": (C.c_int, [_P, C.POINTER(Stats)]),

@@ -264,6 +264,83 @@ inline tri_status finish(tri_cache *c, Version &v, bool auto_inst, int rc) {
 
 inline int64_t vec_elems(uint32_t dtype) { return dtype == TRI_F32 ? 4 : 8; }
 
+// Validation and key of one decode-chain call: kGo with *out set, TRI_OK
+// for T == 0, or an error. Order: common, norm, RoPE, QK norm, SwiGLU.
+int chain_check(const tri_chain_args *p, Key *out) {
+  if (!p) return TRI_E_INVALID;
+  const int32_t dtype = p->dtype;
+  const int64_t T = p->T, H = p->H, I = p->I;
+  int st = check_common(dtype, T);
+  if (st != kGo) return st;
+  const uint64_t es = es_of(uint32_t(dtype));
+  {
+    const void *ptrs[5] = {p->x, p->res, p->w, p->y, p->res_out};
+    const int64_t strides[4] = {p->x_rs, p->res_rs, p->y_rs, p->ro_rs};
+    st = check_norm(es, H, ptrs, 5, strides, 4, p->eps);
+    if (st != kGo) return st;
+  }
+  const tri_rope_ext &x = p->rope_ext ? *p->rope_ext : kRopePlain;
+  st = check_rope(es, p->q, p->q_ts, p->k, p->k_ts, p->pos, p->nq, p->nk, p->hd, p->base, x);
+  if (st != kGo) return st;
+  const bool qkn = p->q_norm_w != nullptr;
+  if (qkn) {
+    st = check_qkn(es, p->q_norm_w, p->k_norm_w, p->nk, p->qk_eps);
+    if (st != kGo) return st;
+  }
+  st = check_sw(es, I, p->gate, p->g_rs, p->up, p->u_rs, p->out, p->o_rs);
+  if (st != kGo) return st;
+
+  const unsigned fl =
+      res_flags(es, p->x, p->x_rs, p->res, p->res_rs, p->w, p->y, p->y_rs, p->res_out, p->ro_rs,
+                H) |
+      (rope_flags(es, p->q, p->q_ts, p->k, p->k_ts, p->nq, p->nk, p->hd,
+                  qkn ? p->q_norm_w : nullptr, qkn ? p->k_norm_w : nullptr) << 2) |
+      (sw_flags(es, p->gate, p->g_rs, p->up, p->u_rs, p->out, p->o_rs, I) << 4) |
+      (qkn ? kChainQkNorm : 0u);
+  *out = make_key(TRI_OP_CHAIN, uint32_t(dtype), T, fl, 0, uint64_t(H), uint64_t(I),
+                  uint64_t(p->hd), uint64_t(p->nq), uint64_t(p->nk));
+  rope_key_words(*out, p->hd, p->base, x);
+  return kGo;
+}
+
+// The launches of one chain call on version v: one fused launch, or the
+// three role kernels in order (stopping at the first failure). l receives
+// the launch records, *n their count. Returns 0 or the failing launch's code.
+int chain_launch(const Version &v, const tri_chain_args &p, void *stream, tri_launch_rec *l,
+                 int *n) {
+  const uint32_t dtype = uint32_t(p.dtype);
+  const int64_t T = p.T, I = p.I;
+  const tri_rope_ext &x = p.rope_ext ? *p.rope_ext : kRopePlain;
+  const bool qkn = p.q_norm_w != nullptr;
+  const RnArgs rn{p.x, p.res, p.w, p.y, p.res_out, p.x_rs, p.res_rs, p.y_rs, p.ro_rs,
+                  T, int32_t(p.H), p.eps};
+  const RopeArgs ro = rope_args(v, p.q, p.q_ts, p.k, p.k_ts, p.pos, T, p.nq, p.nk, p.hd, x,
+                                qkn ? p.q_norm_w : nullptr, p.k_norm_w, p.qk_eps);
+  const SwArgs sw{p.gate, p.up, p.out, p.g_rs, p.u_rs, p.o_rs, T, I,
+                  (T * I) / vec_elems(dtype), T * I};
+  const uint32_t g0 = role_grid(v.plan.roles[0], dtype, T, I);
+  const uint32_t g1 = role_grid(v.plan.roles[1], dtype, T, I);
+  const uint32_t g2 = role_grid(v.plan.roles[2], dtype, T, I);
+
+  if (v.plan.variant == CH_FUSED) {
+    const ChainArgs a{rn, ro, sw, g0, g1};
+    l[0] = {CH_FUSED, g0 + g1 + g2, kBlock};
+    *n = 1;
+    return be_launch(v.fn[0], l[0].grid_x, kBlock, &a, sizeof a, stream);
+  }
+  // Three launches: the residual norm, RoPE and SwiGLU role kernels.
+  const void *args[3] = {&rn, &ro, &sw};
+  const uint32_t sizes[3] = {sizeof rn, sizeof ro, sizeof sw};
+  const uint32_t grids[3] = {g0, g1, g2};
+  *n = 3;
+  int rc = 0;
+  for (int i = 0; i < 3; ++i) {
+    l[i] = {v.plan.kvariant[i], grids[i], kBlock};
+    if (rc == 0) rc = be_launch(v.fn[i], grids[i], kBlock, args[i], sizes[i], stream);
+  }
+  return rc;
+}
+
 // RoPE (op 3) or QK-RMSNorm + RoPE (op 6; the head-norm weights are then
 // required) with an optional variant.
 tri_status rope_entry(tri_cache *c, uint32_t op, int32_t dtype, void *q, int64_t q_ts, void *kp,
@@ -421,75 +498,101 @@ tri_status tri_decode_chain(tri_cache *c, const tri_chain_args *p, void *stream)
   if (!c) return TRI_E_INVALID;
   const uint32_t op = TRI_OP_CHAIN;
   c->stats.calls++;
-  if (!p) return finish_early(c, op, TRI_E_INVALID);
-  const int32_t dtype = p->dtype;
-  const int64_t T = p->T, H = p->H, I = p->I;
-  int st = check_common(dtype, T);
+  Key k;
+  int st = chain_check(p, &k);
   if (st != kGo) return finish_early(c, op, st);
-  const uint64_t es = es_of(uint32_t(dtype));
-  {
-    const void *ptrs[5] = {p->x, p->res, p->w, p->y, p->res_out};
-    const int64_t strides[4] = {p->x_rs, p->res_rs, p->y_rs, p->ro_rs};
-    st = check_norm(es, H, ptrs, 5, strides, 4, p->eps);
-    if (st != kGo) return finish_early(c, op, st);
-  }
-  const tri_rope_ext &x = p->rope_ext ? *p->rope_ext : kRopePlain;
-  st = check_rope(es, p->q, p->q_ts, p->k, p->k_ts, p->pos, p->nq, p->nk, p->hd, p->base, x);
-  if (st != kGo) return finish_early(c, op, st);
-  const bool qkn = p->q_norm_w != nullptr;
-  if (qkn) {
-    st = check_qkn(es, p->q_norm_w, p->k_norm_w, p->nk, p->qk_eps);
-    if (st != kGo) return finish_early(c, op, st);
-  }
-  st = check_sw(es, I, p->gate, p->g_rs, p->up, p->u_rs, p->out, p->o_rs);
-  if (st != kGo) return finish_early(c, op, st);
-
-  const unsigned fl =
-      res_flags(es, p->x, p->x_rs, p->res, p->res_rs, p->w, p->y, p->y_rs, p->res_out, p->ro_rs,
-                H) |
-      (rope_flags(es, p->q, p->q_ts, p->k, p->k_ts, p->nq, p->nk, p->hd,
-                  qkn ? p->q_norm_w : nullptr, qkn ? p->k_norm_w : nullptr) << 2) |
-      (sw_flags(es, p->gate, p->g_rs, p->up, p->u_rs, p->out, p->o_rs, I) << 4) |
-      (qkn ? kChainQkNorm : 0u);
-  Key k = make_key(op, uint32_t(dtype), T, fl, 0, uint64_t(H), uint64_t(I), uint64_t(p->hd),
-                   uint64_t(p->nq), uint64_t(p->nk));
-  rope_key_words(k, p->hd, p->base, x);
   int32_t vi;
   bool auto_inst = false;
-  st = lookup(c, op, k, T, &vi, &auto_inst);
+  st = lookup(c, op, k, p->T, &vi, &auto_inst);
   if (st != TRI_OK) return tri_status(st);
   Version &v = c->versions[vi];
-
-  const RnArgs rn{p->x, p->res, p->w, p->y, p->res_out, p->x_rs, p->res_rs, p->y_rs, p->ro_rs,
-                  T, int32_t(H), p->eps};
-  const RopeArgs ro = rope_args(v, p->q, p->q_ts, p->k, p->k_ts, p->pos, T, p->nq, p->nk, p->hd,
-                                x, qkn ? p->q_norm_w : nullptr, p->k_norm_w, p->qk_eps);
-  const SwArgs sw{p->gate, p->up, p->out, p->g_rs, p->u_rs, p->o_rs, T, I,
-                  (T * I) / vec_elems(uint32_t(dtype)), T * I};
-  const uint32_t g0 = role_grid(v.plan.roles[0], uint32_t(dtype), T, I);
-  const uint32_t g1 = role_grid(v.plan.roles[1], uint32_t(dtype), T, I);
-  const uint32_t g2 = role_grid(v.plan.roles[2], uint32_t(dtype), T, I);
-
-  if (v.plan.variant == CH_FUSED) {
-    ChainArgs a{rn, ro, sw, g0, g1};
-    const tri_launch_rec l{CH_FUSED, g0 + g1 + g2, kBlock};
-    const int rc = be_launch(v.fn[0], l.grid_x, kBlock, &a, sizeof a, stream);
-    record(c, op, v, vi, k, 1, &l, rc ? TRI_E_LAUNCH : TRI_OK);
-    return finish(c, v, auto_inst, rc);
-  }
-  // Three launches: the residual norm, RoPE and SwiGLU role kernels.
-  RnArgs a0 = rn;
-  RopeArgs a1 = ro;
-  SwArgs a2 = sw;
-  const void *args[3] = {&a0, &a1, &a2};
-  const uint32_t sizes[3] = {sizeof a0, sizeof a1, sizeof a2};
-  const tri_launch_rec l[3] = {{v.plan.kvariant[0], g0, kBlock},
-                               {v.plan.kvariant[1], g1, kBlock},
-                               {v.plan.kvariant[2], g2, kBlock}};
-  int rc = 0;
-  for (int i = 0; i < 3 && rc == 0; ++i) rc = be_launch(v.fn[i], l[i].grid_x, kBlock, args[i], sizes[i], stream);
-  record(c, op, v, vi, k, 3, l, rc ? TRI_E_LAUNCH : TRI_OK);
+  tri_launch_rec l[3];
+  int n = 0;
+  const int rc = chain_launch(v, *p, stream, l, &n);
+  record(c, op, v, vi, k, n, l, rc ? TRI_E_LAUNCH : TRI_OK);
   return finish(c, v, auto_inst, rc);
+}
+
+tri_status tri_decode_chain_layers(tri_cache *c, const tri_chain_args *layers, uint32_t n_layers,
+                                   void *stream) {
+  if (!c) return TRI_E_INVALID;
+  const uint32_t op = TRI_OP_CHAIN_LAYERS;
+  c->stats.calls++;
+  if (n_layers > uint32_t(TRI_MAX_LAYERS) || (n_layers > 0 && !layers))
+    return finish_early(c, op, TRI_E_INVALID);
+  // Pass 1, in layer order: validate, pack the key, look the version up.
+  // Nothing is installed or launched before every layer has passed.
+  int32_t vis[TRI_MAX_LAYERS];
+  int32_t first_miss = -1, last = -1;
+  for (uint32_t i = 0; i < n_layers; ++i) {
+    Key k;
+    const int st = chain_check(&layers[i], &k);
+    if (st == TRI_OK) {            // T == 0: this layer is a no-op
+      vis[i] = -1;
+      continue;
+    }
+    if (st != kGo) return finish_early(c, op, st);
+    vis[i] = find_version(c, TRI_OP_CHAIN, k);
+    if (vis[i] < 0 && first_miss < 0) first_miss = int32_t(i);
+    last = int32_t(i);
+  }
+  if (last < 0) return finish_early(c, op, TRI_OK);
+  // Misses: one per entry call; the first missed layer's key is recorded.
+  // With auto-install every missing version is installed, in layer order.
+  const bool missed = first_miss >= 0;
+  if (missed) {
+    c->stats.misses++;
+    Key k;
+    chain_check(&layers[first_miss], &k);
+    c->has_miss = true;
+    c->miss_key = k;
+    c->miss_T = layers[first_miss].T;
+    tri_selection &r = c->last;
+    memset(&r, 0, sizeof r);
+    r.op = int32_t(op);
+    r.version = -1;
+    key_words(k, r.key);
+    if (!(c->flags & TRI_CACHE_AUTO_INSTALL)) {
+      r.status = TRI_MISS;
+      return TRI_MISS;
+    }
+    for (uint32_t i = uint32_t(first_miss); i <= uint32_t(last); ++i) {
+      if (vis[i] >= 0 || layers[i].T == 0) continue;
+      chain_check(&layers[i], &k);
+      const tri_status ist = install_key(c, k);
+      if (ist != TRI_OK) {
+        r.status = ist;
+        return ist;
+      }
+      vis[i] = find_version(c, TRI_OP_CHAIN, k);
+    }
+  }
+  // Pass 2: the launches, in layer order on the caller's stream.
+  int total = 0;
+  for (uint32_t i = 0; i < n_layers; ++i) {
+    if (vis[i] < 0) continue;
+    Version &v = c->versions[vis[i]];
+    tri_launch_rec l[3];
+    int n = 0;
+    const int rc = chain_launch(v, layers[i], stream, l, &n);
+    total += n;
+    if (rc != 0 || int32_t(i) == last) {
+      Key k;
+      chain_check(&layers[i], &k);
+      record(c, op, v, vis[i], k, n, l, rc ? TRI_E_LAUNCH : TRI_OK);
+      c->last.n_launches = total;
+    }
+    if (rc != 0) {
+      if (!missed) c->stats.errors++;
+      return TRI_E_LAUNCH;
+    }
+  }
+  if (!missed) {
+    c->stats.hits++;
+    for (uint32_t i = 0; i < n_layers; ++i)
+      if (vis[i] >= 0) c->versions[vis[i]].hits++;
+  }
+  return TRI_OK;
 }
 
 }  // extern "C"

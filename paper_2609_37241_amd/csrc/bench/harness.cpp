@@ -65,6 +65,28 @@ int trib_issue(tri_cache *c, int mode, const tri_chain_args *args, void *stream,
   return 0;
 }
 
+// Several chains per step: mode 0 issues ONE tri_decode_chain_layers call
+// over layers[0 .. n_layers), mode 1 issues n_layers tri_decode_chain calls;
+// either way one stream synchronisation ends the step. n_warm untimed steps,
+// then n timed ones into e2e_us. Returns 0 or the first failing status.
+int trib_layers(tri_cache *c, int mode, const tri_chain_args *layers, int n_layers, void *stream,
+                int n_warm, int n, double *e2e_us) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  for (int i = 0; i < n_warm + n; ++i) {
+    const Clock::time_point t0 = Clock::now();
+    int st = 0;
+    if (mode == 0) {
+      st = tri_decode_chain_layers(c, layers, uint32_t(n_layers), stream);
+    } else {
+      for (int l = 0; l < n_layers && st == 0; ++l) st = tri_decode_chain(c, layers + l, stream);
+    }
+    if (hipStreamSynchronize(s) != hipSuccess) return TRI_E_RUNTIME;
+    if (st != 0) return st;
+    if (i >= n_warm) e2e_us[i - n_warm] = us_between(t0, Clock::now());
+  }
+  return 0;
+}
+
 // The mixed-shape stream: calls[i] in order, each synchronised. A MISS is
 // handled the way a caller of the library handles it (install the missed key,
 // call again); missed[i] = 1 marks those calls, whose e2e_us then covers

@@ -130,7 +130,7 @@ struct Version {
   uint64_t hits;
 };
 
-constexpr int kOps = 7;   // op ids 1..6
+constexpr int kOps = 8;   // op ids 1..7
 
 }  // namespace tri
 

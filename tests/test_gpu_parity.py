@@ -471,6 +471,55 @@ def test_chain_beyond_decode_sizes(tri, cache, cfg):
     assert rec == expected_record(model_chain_call(d, cfg.eps, cfg.base, ext=cfg.rope_ext), 0)
 
 
+# ---- several chains per entry call ---------------------------------------------------------
+def test_chain_layers_run_in_order(tri, cache):
+    """Six layers where layer l + 1 adds layer l's residual output: the result
+    is only right if the launches run in layer order. One layer is unaligned
+    (three launches) and one is empty."""
+    cfg = wl.GQA_DECODE
+    n = 6
+    host_layers, dev_layers, args = [], [], []
+    prev_ro = None
+    for l in range(n):
+        inp = wl.host_inputs(cfg, seed=100 + l)
+        layout = "unaligned" if l == 3 else "plain"
+        d = {k: place(v, cfg.dtype, layout) if k not in ("w", "pos") else
+             wl.to_torch(v, cfg.dtype, DEV) for k, v in inp.items()}
+        d["y"], d["res_out"], d["out"] = (empty_like_layout(d["x"]), empty_like_layout(d["x"]),
+                                          empty_like_layout(d["gate"]))
+        if prev_ro is not None:
+            d["residual"] = prev_ro                     # consumes the previous layer
+        a, _ = cache.chain_args(d["x"], d["residual"], d["w"], d["q"], d["k"], d["pos"],
+                                d["gate"], d["up"], cfg.eps, cfg.base, y=d["y"],
+                                residual_out=d["res_out"], out=d["out"])
+        if l == 4:
+            a.T = 0                                     # an empty layer is skipped
+        host_layers.append(inp)
+        dev_layers.append(d)
+        args.append(a)
+        prev_ro = d["res_out"]
+    cache.decode_chain_layers(args)
+    torch.cuda.synchronize()
+    rec = cache.last_selection()
+    assert rec.op == 7 and rec.n_launches == 1 + 1 + 1 + 3 + 1
+    res = None
+    for l in range(n):
+        inp = dict(host_layers[l])
+        if res is not None:
+            inp["residual"] = res
+        if l == 4:                                      # skipped: outputs untouched, so
+            res = np.zeros_like(inp["x"])               # layer 5 reads a zero residual
+            continue
+        want = O.decode_chain(inp, cfg.eps, cfg.base, cfg.dtype)
+        d = dev_layers[l]
+        check(f"res_out[{l}]", host(d["res_out"]), want["res_out"], cfg.dtype, exact=True)
+        for nme in ("y", "q", "k", "out"):
+            check(f"{nme}[{l}]", host(d[nme]), want[nme], cfg.dtype)
+        res = want["res_out"]
+    # layer 5 consumed layer 4's residual output, which was never written
+    assert host(dev_layers[4]["res_out"]).view(np.uint16).max() == 0
+
+
 # ---- chain layouts, degenerate calls, miss path ----------------------------------------------
 @pytest.mark.parametrize("layout", ["strided", "unaligned"])
 def test_chain_three_launch_variant(tri, cache, layout):

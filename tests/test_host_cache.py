@@ -359,6 +359,102 @@ def test_status_strings(lib):
     assert lib.tri_status_str(42) == b"TRI_UNKNOWN"
 
 
+# ---- several chains per entry call ------------------------------------------------------
+def c_layers(lib, cache, calls, stream=None):
+    from paper_2609_37241_amd._lib import ChainArgs
+    arr = (ChainArgs * max(1, len(calls)))()
+    keep = []
+    for i, c in enumerate(calls):
+        a = _chain_struct(c, keep)
+        arr[i] = a
+    return lib.tri_decode_chain_layers(cache, arr, len(calls), stream)
+
+
+def _chain_struct(c, keep):
+    from paper_2609_37241_amd._lib import ChainArgs
+    p, s = c.ptr, c.stride
+    a = ChainArgs()
+    a.dtype, a.nq, a.nk, a.hd = c.dtype, c.nq, c.nk, c.hd
+    a.T, a.H, a.I, a.eps, a.base = c.T, c.H, c.I, c.eps, c.base
+    a.x, a.x_rs = p.get("x"), s["x"]
+    a.res, a.res_rs = p.get("res"), s["res"]
+    a.w = p.get("w")
+    a.y, a.y_rs = p.get("y"), s["y"]
+    a.res_out, a.ro_rs = p.get("res_out"), s["res_out"]
+    a.q, a.q_ts = p.get("q"), s["q"]
+    a.k, a.k_ts = p.get("k"), s["k"]
+    a.pos = p.get("pos")
+    a.gate, a.g_rs = p.get("gate"), s["gate"]
+    a.up, a.u_rs = p.get("up"), s["up"]
+    a.out, a.o_rs = p.get("out"), s["out"]
+    a.q_norm_w, a.k_norm_w, a.qk_eps = p.get("q_w"), p.get("k_w"), c.qk_eps
+    if c.ext is not None:
+        x = c_ext(c.ext)
+        keep.append(x)
+        a.rope_ext = C.pointer(x)
+    return a
+
+
+def run_layers_both(lib, cache, m, calls):
+    st_c = c_layers(lib, cache, calls)
+    st_m = m.call_layers(calls)
+    assert st_c == st_m, (st_c, st_m)
+    assert c_record(lib, cache) == m.last.as_tuple()
+    assert c_stats(lib, cache) == m_stats(m)
+    assert lib.trifake_launch_count() == m.launch_count
+    return st_c
+
+
+def _layer_lists():
+    g = lambda T, **kw: chain_call(BF, T, 4096, 14336, 32, 8, 128, base=5e5, **kw)
+    off = elem_offset(BF)
+    return [
+        [g(1)] * 32,                                           # one version, 32 layers
+        [g(1), g(8), g(1, rope_off=off), g(0), g(3)],          # fused + three-launch layers
+        [g(0), g(0)],                                          # all empty
+        [],                                                    # no layers
+        [g(1), g(-1), g(1)],                                   # invalid layer: nothing runs
+        [g(1), chain_call(BF, 1, 4096, 14336, 32, 8, 127)],    # invalid head_dim
+        [g(1, qk_norm=True), g(1, ext=dict(interleaved=1)), g(2, qk_norm=True)],
+        [chain_call(F, 5, 256, 688, 4, 4, 64), g(1), chain_call(F, 5, 256, 688, 4, 4, 64)],
+    ]
+
+
+@pytest.mark.parametrize("auto", [0, 1])
+def test_layers_parity_with_model(lib, fresh, auto):
+    cache = fresh(flags=auto)
+    m = S.SpecCacheModel(flags=auto)
+    for calls in _layer_lists() * 2:
+        st = run_layers_both(lib, cache, m, calls)
+        if st == S.MISS:
+            while st == S.MISS:        # install the recorded miss, retry the whole list
+                ic, rc = c_install(lib, cache)
+                im, rm = m.install_last_miss()
+                assert ic == im == 0 and rc == rm.as_tuple()
+                st = run_layers_both(lib, cache, m, calls)
+
+
+@pytest.mark.parametrize("fail_at", [0, 1, 5, 9])
+def test_layers_launch_failure_stops_and_counts_once(lib, fresh, fail_at):
+    cache = fresh(flags=1)
+    m = S.SpecCacheModel(flags=1)
+    off = elem_offset(BF)
+    calls = [chain_call(BF, 2, 4096, 14336, 32, 8, 128, rope_off=off * (i % 2)) for i in range(6)]
+    run_layers_both(lib, cache, m, calls)          # installs both versions
+    lib.trifake_fail_at(lib.trifake_launch_count() + fail_at)
+    m.launch_fails = {m.launch_count + fail_at}
+    assert run_layers_both(lib, cache, m, calls) == S.E_LAUNCH
+
+
+def test_layers_limit(lib, fresh):
+    cache = fresh(flags=1)
+    m = S.SpecCacheModel(flags=1)
+    c = chain_call(BF, 1, 256, 688, 4, 4, 64)
+    assert run_layers_both(lib, cache, m, [c] * S.MAX_LAYERS) == S.OK
+    assert run_layers_both(lib, cache, m, [c] * (S.MAX_LAYERS + 1)) == S.E_INVALID
+    assert lib.tri_decode_chain_layers(cache, None, 2, None) == S.E_INVALID
+
+
 # ---- argument preparation ----------------------------------------------------------
 # Argument struct sizes the kernels take (RnArgs, RopeArgs, SwArgs, ChainArgs).
 ARG_SIZES = {"rn": 88, "rope": 112, "sw": 80, "chain": 288}
