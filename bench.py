@@ -332,6 +332,23 @@ def main():
     assert st == 0, st
     latency["llama3_scaled_decode_chain_e2e_us"] = summary(list(e2e[:n2]))
 
+    # ---- runtime-compiled specialization (cold miss = compile + load), then hits ----------
+    jc = tri.SpecCache(jit=True)
+    argsj, _outsj = jc.chain_args(d["x"], d["residual"], d["w"], d["q"], d["k"], d["pos"],
+                                  d["gate"], d["up"], cfg.eps, cfg.base)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    jc.decode_chain_args(argsj, stream)              # miss -> compile + install -> hit
+    stream.synchronize()
+    cold_ms = (time.perf_counter() - t0) * 1e3
+    st = bench.trib_latency(jc.handle, 0, C.byref(argsj), sptr, W, n2, e2e, hst)
+    assert st == 0, st
+    latency["jit_specialized_chain"] = {
+        "cold_miss_ms": cold_ms, "compile_and_load_ms": jc.version_info(0).build_ms,
+        "chain_e2e_us": summary(list(e2e[:n2])), "chain_host_us": summary(list(hst[:n2]))}
+    torch.cuda.synchronize()
+    jc.close()
+
     # ---- one decode step of 32 layers: one entry call vs 32 calls ------------------------
     bench.trib_layers.argtypes = [C.c_void_p, C.c_int, C.c_void_p, C.c_int, C.c_void_p, C.c_int,
                                   C.c_int, C.POINTER(C.c_double)]

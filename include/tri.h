@@ -74,7 +74,10 @@ typedef enum tri_op {
 
 enum { TRI_MAX_LAYERS = 1024 };   /* layers per tri_decode_chain_layers call */
 
-enum { TRI_CACHE_AUTO_INSTALL = 1u };   /* on a miss: install, then launch */
+enum {
+  TRI_CACHE_AUTO_INSTALL = 1u,   /* on a miss: install, then launch */
+  TRI_CACHE_JIT = 2u             /* install compiles a key-specialized kernel */
+};
 
 /* One kernel launch of a selection. */
 typedef struct tri_launch_rec {
@@ -114,6 +117,8 @@ typedef struct tri_version_info {
   int32_t variant;
   int32_t roles[3];
   uint64_t hits;
+  int32_t jit;         /* 1: kernels compiled at install for this key        */
+  float build_ms;      /* install time spent compiling (0 when precompiled)  */
 } tri_version_info;
 
 /* RoPE variants. A zeroed struct (or a NULL pointer where one is taken) is
@@ -195,10 +200,20 @@ typedef struct tri_chain_args {
 /* ---- cache ---------------------------------------------------------------- */
 
 /* Create an empty cache on the current device. capacity 0 selects 256
- * (at most 4096); flags: 0 or TRI_CACHE_AUTO_INSTALL. The cache owns every
- * version, its resolved kernel handles and its device constants; release it
- * with tri_spec_cache_destroy. Errors: INVALID (NULL out, capacity or flags
- * out of range), RUNTIME (no usable device), NOMEM. */
+ * (at most 4096); flags: TRI_CACHE_AUTO_INSTALL and / or TRI_CACHE_JIT. The
+ * cache owns every version, its kernel handles (and, with TRI_CACHE_JIT,
+ * its loaded code objects) and its device constants; release it with
+ * tri_spec_cache_destroy. Errors: INVALID (NULL out, capacity or flags out
+ * of range), RUNTIME (no usable device), NOMEM.
+ *
+ * TRI_CACHE_JIT is the paper's growth path (Sec. 3.5: a miss captures,
+ * compiles and installs a new specialization): installing a key compiles,
+ * with hipRTC for gfx950, a kernel for each of the version's launches whose
+ * shape fields (hidden size, intermediate size, head_dim, rotary dim, head
+ * counts, RoPE variant bits) are compile-time constants of that key, around
+ * the same device bodies as the precompiled variants; the install policy,
+ * the launch geometry and the selection records are those of the
+ * precompiled path. A failed compilation fails the install with RUNTIME. */
 tri_status tri_spec_cache_create(tri_cache **out, uint32_t capacity, uint32_t flags);
 void tri_spec_cache_destroy(tri_cache *cache);
 
@@ -330,6 +345,25 @@ tri_status tri_spec_version_info(const tri_cache *cache, uint32_t index,
  * cache) into out[0..cap); *n gets the count. */
 tri_status tri_spec_version_constants(const tri_cache *cache, uint32_t index,
                                       float *out, uint32_t cap, uint32_t *n);
+
+/* The keys of the installed versions in creation order, TRI_KEY_WORDS words
+ * each, into keys[0 .. cap * TRI_KEY_WORDS); *n = the number of versions
+ * (which may exceed cap). For pre-warming another cache with
+ * tri_spec_import_keys. */
+tri_status tri_spec_export_keys(const tri_cache *cache, uint64_t *keys, uint32_t cap,
+                                uint32_t *n);
+
+/* Install versions for n keys (n * TRI_KEY_WORDS words, e.g. an earlier
+ * export), in order, as an install after a miss would (already installed
+ * keys add nothing). Each key is checked first -- known op, dtype, token
+ * bucket <= 22, flags of the op, sizes within the entry points' limits,
+ * consistent RoPE fields (base > 1 and finite unless a cos/sin cache, rotary
+ * dim even and <= head_dim, Llama-3 parameters as tri_rope_ext requires),
+ * unused fields zero; a malformed key stops the import with INVALID. FULL,
+ * NOMEM, RUNTIME as for an install. *done = keys processed before the
+ * stop (all n on OK). */
+tri_status tri_spec_import_keys(tri_cache *cache, const uint64_t *keys, uint32_t n,
+                                uint32_t *done);
 
 /* Launch the empty kernel (1 workgroup of 64 work-items, no arguments)
  * through the same launch path: the yardstick for per-call cost. */

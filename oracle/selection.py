@@ -66,6 +66,7 @@ HEADS_MAX = 4096
 DEFAULT_CAPACITY = 256
 MAX_CAPACITY = 4096
 FLAG_AUTO_INSTALL = 1
+FLAG_JIT = 2               # compiled specializations: same selections, same records
 
 ALIGN, CONTIG = 1, 2       # per-op guard flag bits
 CHAIN_QK_NORM = 0x40       # chain key flag: the RoPE step has the QK RMSNorm
@@ -460,6 +461,53 @@ def unpack_key(key):
                 high_bits=k5 & 0xFFFFFFFF)
 
 
+def _f32_of_bits(b: int) -> float:
+    return float(np.array([b], dtype=np.uint32).view(np.float32)[0])
+
+
+def key_valid(key) -> bool:
+    """A key the entry points could have produced: known op and dtype, bucket
+    <= 22, the op's flags, sizes within the argument limits, consistent RoPE
+    fields, unused fields zero (the check applied to imported keys)."""
+    f = unpack_key(key)
+    k0, k1, k2, k3, k4, k5 = key
+    op = f["op"]
+    if op not in (OP_RMSNORM, OP_RES_RMSNORM, OP_ROPE_QK, OP_SWIGLU, OP_CHAIN, OP_QK_NORM_ROPE):
+        return False
+    if f["dtype"] not in (DT_F32, DT_BF16) or f["bucket"] > 22:
+        return False
+    if f["flags"] > (0x7F if op == OP_CHAIN else 0x3):
+        return False
+    norm = op in (OP_RMSNORM, OP_RES_RMSNORM, OP_CHAIN)
+    sw = op in (OP_SWIGLU, OP_CHAIN)
+    if (not (1 <= f["H"] < H_LIMIT)) if norm else f["H"] != 0:
+        return False
+    if (not (1 <= f["I"] < I_LIMIT)) if sw else f["I"] != 0:
+        return False
+    if op not in ROPE_OPS:
+        return f["base_bits"] == 0 and k2 == 0 and k3 == 0 and k4 == 0 and k5 == 0
+    if k2 >> 48:
+        return False
+    hd, rd = f["hd"], f["rd"]
+    if hd < 2 or hd % 2 or hd > HD_MAX or not (1 <= f["nq"] <= HEADS_MAX) or f["nk"] > HEADS_MAX:
+        return False
+    if rd < 2 or rd % 2 or rd > hd or f["rope_bits"] > 7:
+        return False
+    if f["rope_bits"] & ROPE_CACHE:
+        return (k3 >> 24) == 0 and f["base_bits"] == 0 and k4 == 0 and k5 == 0
+    base = _f32_of_bits(f["base_bits"])
+    if not (_finite(base) and base > 1.0):
+        return False
+    if f["scaling"] == SCALING_NONE:
+        return (k3 >> 24) == 0 and k4 == 0 and k5 == 0
+    if f["scaling"] != SCALING_LLAMA3 or k5 >> 32:
+        return False
+    fa, lo, hi = (_f32_of_bits(f[n]) for n in ("factor_bits", "low_bits", "high_bits"))
+    if not (_finite(fa) and fa > 0 and _finite(lo) and lo > 0 and _finite(hi) and hi > lo):
+        return False
+    return 1 <= f["orig_max"] < 2 ** 31
+
+
 # ---- install policy: key -> variants, and per-call launch geometry ---------------
 def plan(key, T: int):
     """(variant, roles, launches) for a version with `key`, called with T tokens."""
@@ -504,7 +552,7 @@ class SpecCacheModel:
     """Ordered versions, Algorithm 1 lookup, miss / install / error paths."""
 
     def __init__(self, capacity: int = 0, flags: int = 0):
-        if capacity < 0 or capacity > MAX_CAPACITY or flags & ~FLAG_AUTO_INSTALL:
+        if capacity < 0 or capacity > MAX_CAPACITY or flags & ~(FLAG_AUTO_INSTALL | FLAG_JIT):
             raise ValueError("invalid cache parameters")
         self.capacity = capacity or DEFAULT_CAPACITY
         self.flags = flags
@@ -660,6 +708,17 @@ class SpecCacheModel:
         self.version_hits.append(0)
         self.stats.installs += 1
         return OK
+
+    def import_keys(self, keys) -> Tuple[int, int]:
+        """Install `keys` in order (status, keys processed); a malformed key
+        stops with E_INVALID."""
+        for i, k in enumerate(keys):
+            if not key_valid(tuple(k)):
+                return E_INVALID, i
+            st = self._install(tuple(k))
+            if st < 0:
+                return st, i
+        return OK, len(keys)
 
     def install_last_miss(self) -> Tuple[int, Optional[Record]]:
         if self.last_miss is None:

@@ -102,10 +102,12 @@ def _tokens(t: torch.Tensor, name: str) -> int:
 class SpecCache:
     """One native specialization cache (bound to the current device)."""
 
-    def __init__(self, capacity: int = 0, auto_install: bool = False):
+    def __init__(self, capacity: int = 0, auto_install: bool = False, jit: bool = False):
+        """jit: installs compile key-specialized kernels with hipRTC."""
         h = C.c_void_p()
         st = _dll.tri_spec_cache_create(C.byref(h), capacity,
-                                        AUTO_INSTALL if auto_install else 0)
+                                        (AUTO_INSTALL if auto_install else 0)
+                                        | (L.JIT if jit else 0))
         if st != OK:
             raise TriError(st, "tri_spec_cache_create")
         self._h = h
@@ -280,6 +282,27 @@ class SpecCache:
                                   residual_out, out, q_norm_w, k_norm_w, qk_eps, rope)
         self.decode_chain_args(a, stream)
         return outs
+
+    def export_keys(self):
+        """Keys of the installed versions, creation order (tuples of 6 ints)."""
+        n = C.c_uint32()
+        _dll.tri_spec_export_keys(self._h, None, 0, C.byref(n))
+        buf = (C.c_uint64 * (L.KEY_WORDS * max(1, n.value)))()
+        st = _dll.tri_spec_export_keys(self._h, buf, n.value, C.byref(n))
+        if st != OK:
+            raise TriError(st, "tri_spec_export_keys")
+        w = list(buf)
+        return [tuple(w[i * L.KEY_WORDS:(i + 1) * L.KEY_WORDS]) for i in range(n.value)]
+
+    def import_keys(self, keys) -> int:
+        """Install versions for exported keys (pre-warm); returns the count."""
+        flat = [int(x) for k in keys for x in k]
+        buf = (C.c_uint64 * max(1, len(flat)))(*flat)
+        done = C.c_uint32()
+        st = _dll.tri_spec_import_keys(self._h, buf, len(keys), C.byref(done))
+        if st != OK:
+            raise TriError(st, f"tri_spec_import_keys (after {done.value} keys)")
+        return done.value
 
     def launch_empty(self, stream=None) -> None:
         st = _dll.tri_launch_empty(self._h, _stream_ptr(stream))

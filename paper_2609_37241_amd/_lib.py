@@ -20,6 +20,7 @@ OP_RMSNORM, OP_RES_RMSNORM, OP_ROPE_QK, OP_SWIGLU, OP_CHAIN, OP_QK_NORM_ROPE = 1
 OP_CHAIN_LAYERS = 7
 MAX_LAYERS = 1024
 AUTO_INSTALL = 1
+JIT = 2
 KEY_WORDS = 6
 ROPE_SCALING_NONE, ROPE_SCALING_LLAMA3 = 0, 1
 
@@ -52,7 +53,7 @@ class Stats(C.Structure):
 
 class VersionInfo(C.Structure):
     _fields_ = [("key", C.c_uint64 * KEY_WORDS), ("variant", C.c_int32), ("roles", C.c_int32 * 3),
-                ("hits", C.c_uint64)]
+                ("hits", C.c_uint64), ("jit", C.c_int32), ("build_ms", C.c_float)]
 
 
 class RopeExt(C.Structure):
@@ -84,6 +85,7 @@ class ChainArgs(C.Structure):
 
 
 assert C.sizeof(Selection) == 120 and C.sizeof(ChainArgs) == 240 and C.sizeof(RopeExt) == 48
+assert C.sizeof(VersionInfo) == 80
 
 _P, _I64, _I32, _F, _U32 = C.c_void_p, C.c_int64, C.c_int32, C.c_float, C.c_uint32
 
@@ -109,6 +111,8 @@ SIGNATURES = {
     "tri_spec_version_constants": (C.c_int, [_P, _U32, C.POINTER(C.c_float), _U32,
                                              C.POINTER(C.c_uint32)]),
     "tri_launch_empty": (C.c_int, [_P, _P]),
+    "tri_spec_export_keys": (C.c_int, [_P, C.POINTER(C.c_uint64), _U32, C.POINTER(C.c_uint32)]),
+    "tri_spec_import_keys": (C.c_int, [_P, C.POINTER(C.c_uint64), _U32, C.POINTER(C.c_uint32)]),
     "tri_status_str": (C.c_char_p, [C.c_int]),
 }
 

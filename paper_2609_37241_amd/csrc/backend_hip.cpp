@@ -6,6 +6,10 @@
 // the argument block on the caller's stream -- no symbol lookup, no
 // per-argument marshalling, no device query on the hit path.
 #include <hip/hip_runtime.h>
+#include <hip/hiprtc.h>
+
+#include <chrono>
+#include <vector>
 
 #include "internal.h"
 
@@ -68,5 +72,47 @@ int be_upload(const void *host, uint64_t bytes, void **dev) {
 }
 
 void be_free(void *dev) { (void)hipFree(dev); }
+
+// hipRTC for gfx950 with the device flags of the precompiled kernels (no
+// floating-point contraction, packed FP32 instructions off), then load the
+// code object and resolve the kernel.
+int be_jit(const char *src, uint64_t len, void **fn, void **module, float *ms) {
+  (void)len;
+  const auto t0 = std::chrono::steady_clock::now();
+  hiprtcProgram prog;
+  if (hiprtcCreateProgram(&prog, src, "tri_jit.hip", 0, nullptr, nullptr) != HIPRTC_SUCCESS)
+    return TRI_E_RUNTIME;
+  const char *opts[] = {"--offload-arch=gfx950", "-O3", "-std=c++17", "-ffp-contract=off",
+                        "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"};
+  int st = 0;
+  std::vector<char> code;
+  if (hiprtcCompileProgram(prog, int(sizeof opts / sizeof opts[0]), opts) != HIPRTC_SUCCESS) {
+    st = TRI_E_RUNTIME;
+  } else {
+    size_t n = 0;
+    if (hiprtcGetCodeSize(prog, &n) != HIPRTC_SUCCESS || n == 0) {
+      st = TRI_E_RUNTIME;
+    } else {
+      code.resize(n);
+      if (hiprtcGetCode(prog, code.data()) != HIPRTC_SUCCESS) st = TRI_E_RUNTIME;
+    }
+  }
+  (void)hiprtcDestroyProgram(&prog);
+  if (st != 0) return st;
+  hipModule_t mod = nullptr;
+  if (hipModuleLoadData(&mod, code.data()) != hipSuccess) return TRI_E_RUNTIME;
+  hipFunction_t f = nullptr;
+  if (hipModuleGetFunction(&f, mod, "tri_jit_kernel") != hipSuccess) {
+    (void)hipModuleUnload(mod);
+    return TRI_E_RUNTIME;
+  }
+  *fn = reinterpret_cast<void *>(f);
+  *module = reinterpret_cast<void *>(mod);
+  *ms = float(std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0)
+                  .count());
+  return 0;
+}
+
+void be_unload(void *module) { (void)hipModuleUnload(reinterpret_cast<hipModule_t>(module)); }
 
 }  // namespace tri

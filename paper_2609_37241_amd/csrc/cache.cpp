@@ -67,6 +67,14 @@ void rope_inverse_frequencies(const Key &k, float *out) {
   }
 }
 
+void release_modules(Version &v) {
+  for (int i = 0; i < 3; ++i) {
+    if (v.module[i]) be_unload(v.module[i]);
+    v.module[i] = nullptr;
+    v.fn[i] = nullptr;
+  }
+}
+
 }  // namespace
 
 tri_status install_key(tri_cache *c, const Key &k) {
@@ -79,21 +87,46 @@ tri_status install_key(tri_cache *c, const Key &k) {
   v.key = k;
   v.plan = plan_for_key(k);
   const uint32_t dt = key_dtype(k);
-  for (int i = 0; i < v.plan.n_launches; ++i) {
-    const int st = be_resolve(v.plan.kvariant[i], dt, v.plan.ksub[i], &v.fn[i]);
-    if (st != 0) return tri_status(st);
+  if (c->flags & TRI_CACHE_JIT) {
+    // Compile one specialization per launch of the plan (Sec. 3.5 growth).
+    v.jit = 1;
+    for (int i = 0; i < v.plan.n_launches; ++i) {
+      uint64_t len = 0;
+      char *src = jit_source(k, v.plan, i, &len);
+      if (!src) {
+        release_modules(v);
+        return TRI_E_NOMEM;
+      }
+      float ms = 0.0f;
+      const int st = be_jit(src, len, &v.fn[i], &v.module[i], &ms);
+      free(src);
+      v.build_ms += ms;
+      if (st != 0) {
+        release_modules(v);
+        return tri_status(st);
+      }
+    }
+  } else {
+    for (int i = 0; i < v.plan.n_launches; ++i) {
+      const int st = be_resolve(v.plan.kvariant[i], dt, v.plan.ksub[i], &v.fn[i]);
+      if (st != 0) return tri_status(st);
+    }
   }
   const uint32_t op = key_op(k);
   const bool rope = op == TRI_OP_ROPE_QK || op == TRI_OP_QK_NORM_ROPE || op == TRI_OP_CHAIN;
   if (rope && !(key_rope_bits(k) & kRopeCache)) {
     v.n_consts = key_rd(k) / 2;
     v.h_consts = static_cast<float *>(malloc(sizeof(float) * v.n_consts));
-    if (!v.h_consts) return TRI_E_NOMEM;
+    if (!v.h_consts) {
+      release_modules(v);
+      return TRI_E_NOMEM;
+    }
     rope_inverse_frequencies(k, v.h_consts);
     void *dev = nullptr;
     const int st = be_upload(v.h_consts, sizeof(float) * v.n_consts, &dev);
     if (st != 0) {
       free(v.h_consts);
+      release_modules(v);
       return tri_status(st);
     }
     v.d_consts = static_cast<float *>(dev);
@@ -135,7 +168,7 @@ extern "C" {
 tri_status tri_spec_cache_create(tri_cache **out, uint32_t capacity, uint32_t flags) {
   if (!out) return TRI_E_INVALID;
   *out = nullptr;
-  if (capacity > kMaxCapacity || (flags & ~uint32_t(TRI_CACHE_AUTO_INSTALL)))
+  if (capacity > kMaxCapacity || (flags & ~uint32_t(TRI_CACHE_AUTO_INSTALL | TRI_CACHE_JIT)))
     return TRI_E_INVALID;
   if (capacity == 0) capacity = kDefaultCapacity;
   int device = 0;
@@ -169,6 +202,7 @@ void tri_spec_cache_destroy(tri_cache *c) {
   for (uint32_t i = 0; i < c->n_versions; ++i) {
     if (c->versions[i].d_consts) be_free(c->versions[i].d_consts);
     free(c->versions[i].h_consts);
+    release_modules(c->versions[i]);
   }
   free(c->versions);
   free(c);
@@ -207,7 +241,35 @@ tri_status tri_spec_version_info(const tri_cache *c, uint32_t index, tri_version
   out->variant = v.plan.variant;
   for (int i = 0; i < 3; ++i) out->roles[i] = v.plan.roles[i];
   out->hits = v.hits;
+  out->jit = v.jit;
+  out->build_ms = v.build_ms;
   return TRI_OK;
+}
+
+tri_status tri_spec_export_keys(const tri_cache *c, uint64_t *keys, uint32_t cap, uint32_t *n) {
+  if (!c || !n || (cap && !keys)) return TRI_E_INVALID;
+  *n = c->n_versions;
+  for (uint32_t i = 0; i < c->n_versions && i < cap; ++i)
+    key_words(c->versions[i].key, keys + size_t(i) * TRI_KEY_WORDS);
+  return TRI_OK;
+}
+
+tri_status tri_spec_import_keys(tri_cache *c, const uint64_t *keys, uint32_t n, uint32_t *done) {
+  if (!c || (n && !keys)) return TRI_E_INVALID;
+  uint32_t i = 0;
+  tri_status st = TRI_OK;
+  for (; i < n; ++i) {
+    const uint64_t *w = keys + size_t(i) * TRI_KEY_WORDS;
+    const Key k{w[0], w[1], w[2], w[3], w[4], w[5]};
+    if (!key_valid(k)) {
+      st = TRI_E_INVALID;
+      break;
+    }
+    st = install_key(c, k);
+    if (st != TRI_OK) break;
+  }
+  if (done) *done = i;
+  return st;
 }
 
 tri_status tri_spec_version_constants(const tri_cache *c, uint32_t index, float *out,

@@ -118,12 +118,20 @@ int be_launch(void *fn, uint32_t grid, uint32_t block, const void *args, uint32_
               void *stream);
 int be_upload(const void *host, uint64_t bytes, void **dev);      // per-version constants
 void be_free(void *dev);
+// Compile `src` (len bytes, NUL-terminated) for the device and load it: the
+// kernel `tri_jit_kernel` becomes *fn, the loaded code object *module.
+// 0 or tri_status; *ms gets the compile + load time.
+int be_jit(const char *src, uint64_t len, void **fn, void **module, float *ms);
+void be_unload(void *module);
 
 // ---- versions and the cache ------------------------------------------------------------
 struct Version {
   Key key;
   Plan plan;
   void *fn[3];
+  void *module[3];        // runtime-compiled code objects, or null
+  int32_t jit;
+  float build_ms;
   float *d_consts;        // device copy of the RoPE inverse frequencies, or null
   float *h_consts;        // host copy (rotary_dim/2 floats), or null
   uint32_t n_consts;
@@ -154,4 +162,10 @@ namespace tri {
 int32_t find_version(tri_cache *c, uint32_t op, const Key &k);
 tri_status install_key(tri_cache *c, const Key &k);
 void fill_selection(const Version &v, int32_t index, int64_t T, tri_selection *out);
+// Runtime-compiled specializations (jit.cpp).
+bool key_valid(const Key &k);
+// Source of the specialization of launch `i` of a version (key k, plan p):
+// the device prelude and one kernel; returns a malloc'd NUL-terminated text
+// (caller frees) and its length, or null.
+char *jit_source(const Key &k, const Plan &p, int i, uint64_t *len);
 }  // namespace tri

@@ -2,9 +2,10 @@
 // the kernel's only parameter. Host code fills them on the hit path and hands
 // a pointer to the launch; device code reads them from the kernarg segment.
 // Plain fixed-width fields only, so host (x86-64) and device (amdgcn) lay
-// them out identically; the static_asserts below pin the layout on both.
+// them out identically; the static_asserts below pin the layout on both
+// (with the compiler's own offsetof, as the runtime compiler ships no
+// <stddef.h>).
 #pragma once
-#include <stddef.h>
 #include <stdint.h>
 
 namespace tri {
@@ -68,13 +69,14 @@ struct ChainArgs {
   uint32_t rope_blocks;
 };
 
-static_assert(sizeof(RnArgs) == 88 && offsetof(RnArgs, T) == 72 && offsetof(RnArgs, eps) == 84,
+static_assert(sizeof(RnArgs) == 88 && __builtin_offsetof(RnArgs, T) == 72 &&
+                  __builtin_offsetof(RnArgs, eps) == 84,
               "RnArgs layout");
-static_assert(sizeof(RopeArgs) == 112 && offsetof(RopeArgs, nq) == 88 &&
-                  offsetof(RopeArgs, mode) == 108,
+static_assert(sizeof(RopeArgs) == 112 && __builtin_offsetof(RopeArgs, nq) == 88 &&
+                  __builtin_offsetof(RopeArgs, mode) == 108,
               "RopeArgs layout");
-static_assert(sizeof(SwArgs) == 80 && offsetof(SwArgs, n) == 72, "SwArgs layout");
-static_assert(sizeof(ChainArgs) == 288 && offsetof(ChainArgs, rn_blocks) == 280,
+static_assert(sizeof(SwArgs) == 80 && __builtin_offsetof(SwArgs, n) == 72, "SwArgs layout");
+static_assert(sizeof(ChainArgs) == 288 && __builtin_offsetof(ChainArgs, rn_blocks) == 280,
               "ChainArgs layout");
 
 }  // namespace tri

@@ -8,47 +8,13 @@ namespace tri {
 using namespace dev;
 
 // RNV: RN_WAVE_1/2 (one wavefront per row) or RN_BLOCK_1..16 (one
-// workgroup per row); the RoPE role takes one token per workgroup, with the
-// per-head QK RMSNorm first when QKN and GPT-J pairs when INTER; SWV: SW_FLAT
-// (one vector per work-item, cached) or SW_FLAT_U4_NT (four, streaming).
-template <int DT, int RNV>
-__device__ __forceinline__ void chain_norm_role(const ChainArgs &a, uint32_t blk) {
-  if constexpr (RNV <= RN_WAVE_2) {
-    rn_wave_block<DT, 1 << (RNV - RN_WAVE_1), true, false>(a.rn, blk);
-  } else {
-    __shared__ float red[4];
-    rn_row_regs<DT, 1 << (RNV - RN_BLOCK_1), true, 256, false>(a.rn, blk, threadIdx.x, red);
-  }
-}
-
-// Role order by blockIdx. Decode sizes (SW_FLAT): norm rows, RoPE tokens,
-// then SwiGLU -- the norm and RoPE roles take about as long as SwiGLU but
-// have far fewer workgroups, so dispatching them first shortens the critical
-// path (2.75 vs 3.1 µs device time at 1 token). Streaming sizes
-// (SW_FLAT_U4_NT): SwiGLU first, then norm, then RoPE (about 1 % faster at
-// 8192 tokens than norm first).
+// workgroup per row); SWV: SW_FLAT or SW_FLAT_U4_NT; QKN: QK norm before the
+// rotation; INTER: GPT-J pairs.
 template <int DT, int RNV, int SWV, bool QKN, bool INTER>
 __global__ __launch_bounds__(256) void k_chain(ChainArgs a) {
-  __shared__ float lds[2 * 256];
-  const uint32_t b = blockIdx.x;
-  const uint32_t R = a.rn_blocks, P = a.rope_blocks, S = gridDim.x - R - P;
-  if constexpr (SWV == SW_FLAT_U4_NT) {
-    if (b < S) {
-      sw_flat_part<DT, 4, true>(a.sw, b, S);
-    } else if (b < S + R) {
-      chain_norm_role<DT, RNV>(a, b - S);
-    } else {
-      rope_vec_block<DT, 1, false, 4, QKN, INTER>(a.rope, b - S - R, lds);
-    }
-  } else {
-    if (b < R) {
-      chain_norm_role<DT, RNV>(a, b);
-    } else if (b < R + P) {
-      rope_vec_block<DT, 1, false, 4, QKN, INTER>(a.rope, b - R, lds);
-    } else {
-      sw_flat_part<DT, 1, false>(a.sw, b - R - P, S);
-    }
-  }
+  constexpr bool wave = RNV <= RN_WAVE_2;
+  constexpr int n = wave ? 1 << (RNV - RN_WAVE_1) : 1 << (RNV - RN_BLOCK_1);
+  body_chain<DT, wave, n, SWV == SW_FLAT_U4_NT, QKN, INTER>(a);
 }
 
 namespace {

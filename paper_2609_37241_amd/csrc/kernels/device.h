@@ -217,7 +217,7 @@ __device__ __forceinline__ void rn_row_regs(const RnArgs &a, int64_t row, int la
     float f[V];
     E::unpack(xv[k], f);
 #pragma unroll
-    for (int e = 0; e < V; ++e) ss += f[e] * f[e];
+    for (int e = 0; e < V; ++e) ss = __builtin_fmaf(f[e], f[e], ss);
   }
   if constexpr (LANES == 64)
     ss = wave_sum(ss);
@@ -354,6 +354,17 @@ __device__ __forceinline__ void rope_cos_sin(const RopeArgs &a, int64_t t, int i
   }
 }
 
+// The rotation of a pair (x, y) by (c, s): x c - y s and y c + x s, each one
+// fused multiply-add on a rounded product (device code is compiled without
+// contraction, so these are the only fused operations and their rounding
+// does not depend on the surrounding code).
+__device__ __forceinline__ float rot_a(float x, float y, float c, float s) {
+  return __builtin_fmaf(x, c, -(y * s));
+}
+__device__ __forceinline__ float rot_b(float x, float y, float c, float s) {
+  return __builtin_fmaf(y, c, x * s);
+}
+
 __device__ __forceinline__ char *rope_head(const RopeArgs &a, int64_t t, int h, int es) {
   return h < a.nq ? static_cast<char *>(a.q) + (t * a.q_ts + int64_t(h) * a.hd) * es
                   : static_cast<char *>(a.k) + (t * a.k_ts + int64_t(h - a.nq) * a.hd) * es;
@@ -484,10 +495,10 @@ __device__ __forceinline__ void rope_vec_block(const RopeArgs &a, int64_t blk, f
       if constexpr (QKN) {
         float ss = 0.0f;
 #pragma unroll
-        for (int e = 0; e < V; ++e) ss += f1[e] * f1[e];
+        for (int e = 0; e < V; ++e) ss = __builtin_fmaf(f1[e], f1[e], ss);
         if constexpr (!INTER) {
 #pragma unroll
-          for (int e = 0; e < V; ++e) ss += f2[e] * f2[e];
+          for (int e = 0; e < V; ++e) ss = __builtin_fmaf(f2[e], f2[e], ss);
         }
         ss = group_sum(ss, cpb);
         const float inv = rsqrtf(ss / float(a.hd) + a.eps);
@@ -510,8 +521,8 @@ __device__ __forceinline__ void rope_vec_block(const RopeArgs &a, int64_t blk, f
 #pragma unroll
         for (int e = 0; e < V; e += 2) {
           const float c = cs[base + (e >> 1)], s = sn[base + (e >> 1)];
-          o[e] = f1[e] * c - f1[e + 1] * s;
-          o[e + 1] = f1[e + 1] * c + f1[e] * s;
+          o[e] = rot_a(f1[e], f1[e + 1], c, s);
+          o[e + 1] = rot_b(f1[e], f1[e + 1], c, s);
         }
         if (QKN && !ok[j]) continue;
         st16<NT>(reinterpret_cast<u32x4 *>(b) + chunk, E::pack(o));
@@ -521,8 +532,8 @@ __device__ __forceinline__ void rope_vec_block(const RopeArgs &a, int64_t blk, f
 #pragma unroll
         for (int e = 0; e < V; ++e) {
           const float c = cs[base + e], s = sn[base + e];
-          o1[e] = f1[e] * c - f2[e] * s;
-          o2[e] = f2[e] * c + f1[e] * s;
+          o1[e] = rot_a(f1[e], f2[e], c, s);
+          o2[e] = rot_b(f1[e], f2[e], c, s);
         }
         if (QKN && !ok[j]) continue;
         st16<NT>(reinterpret_cast<u32x4 *>(b) + chunk, E::pack(o1));
@@ -565,8 +576,8 @@ __device__ __forceinline__ void rope_scalar_block(const RopeArgs &a, int64_t t, 
       const int i0 = inter ? 2 * i : i, i1 = inter ? 2 * i + 1 : i + P2;
       char *base = rope_head(a, t, h, E::ES);
       const float v1 = E::ld(base, i0), v2 = E::ld(base, i1);
-      E::st(base, i0, v1 * cs[i] - v2 * sn[i]);
-      E::st(base, i1, v2 * cs[i] + v1 * sn[i]);
+      E::st(base, i0, rot_a(v1, v2, cs[i], sn[i]));
+      E::st(base, i1, rot_b(v1, v2, cs[i], sn[i]));
     }
   } else {
     float *rinv = lds + 512;
@@ -580,7 +591,7 @@ __device__ __forceinline__ void rope_scalar_block(const RopeArgs &a, int64_t t, 
         float ss = 0.0f;
         for (int i = lane; i < a.hd; i += 64) {
           const float v = E::ld(base, i);
-          ss += v * v;
+          ss = __builtin_fmaf(v, v, ss);
         }
         ss = wave_sum(ss);
         if (lane == 0) rinv[hl] = rsqrtf(ss / float(a.hd) + a.eps);
@@ -597,8 +608,8 @@ __device__ __forceinline__ void rope_scalar_block(const RopeArgs &a, int64_t t, 
         const float r = rinv[hl];
         const float n1 = (E::ld(base, i0) * r) * E::ld(w, i0);
         const float n2 = (E::ld(base, i1) * r) * E::ld(w, i1);
-        E::st(base, i0, n1 * cs[i] - n2 * sn[i]);
-        E::st(base, i1, n2 * cs[i] + n1 * sn[i]);
+        E::st(base, i0, rot_a(n1, n2, cs[i], sn[i]));
+        E::st(base, i1, rot_b(n1, n2, cs[i], sn[i]));
       }
       const int tp = hn * pass;
       for (int e = threadIdx.x; e < tp; e += kThreads) {
@@ -698,6 +709,108 @@ __device__ __forceinline__ void sw_scalar_part(const SwArgs &a, int64_t blk, int
     const int64_t j = e - row * a.I;
     const float r = silu_mul(E::ld(a.gate, row * a.g_rs + j), E::ld(a.up, row * a.u_rs + j));
     E::st(a.out, row * a.o_rs + j, r);
+  }
+}
+
+// ---- kernel bodies -----------------------------------------------------------------
+// One body per kernel family, called by the precompiled kernels and by the
+// runtime-compiled specializations; a specialization passes arguments whose
+// shape fields are compile-time constants.
+template <int DT, int NV, bool RES>
+__device__ __forceinline__ void body_rn_wave(const RnArgs &a) {
+  rn_wave_block<DT, NV, RES, false>(a, blockIdx.x);
+}
+
+template <int DT, int NB, bool RES>
+__device__ __forceinline__ void body_rn_block(const RnArgs &a) {
+  __shared__ float red[4];
+  rn_row_regs<DT, NB, RES, 256, false>(a, blockIdx.x, threadIdx.x, red);
+}
+
+template <int DT, bool RES>
+__device__ __forceinline__ void body_rn_loop(const RnArgs &a) {
+  __shared__ double red[4];
+  rn_loop_row<DT, RES>(a, blockIdx.x, red);
+}
+
+template <int DT, bool RES>
+__device__ __forceinline__ void body_rn_scalar(const RnArgs &a) {
+  __shared__ double red[4];
+  rn_scalar_row<DT, RES>(a, blockIdx.x, red);
+}
+
+// QKN: per-head RMSNorm of Q and K before the rotation; INTER: GPT-J pairs.
+template <int DT, bool QKN, bool INTER>
+__device__ __forceinline__ void body_rope_vec(const RopeArgs &a) {
+  __shared__ float lds[2 * 256];
+  rope_vec_block<DT, 1, false, 4, QKN, INTER>(a, blockIdx.x, lds);
+}
+
+template <int DT, bool QKN>
+__device__ __forceinline__ void body_rope_scalar(const RopeArgs &a) {
+  __shared__ float lds[(QKN ? 3 : 2) * 256];
+  rope_scalar_block<DT, QKN>(a, blockIdx.x, lds);
+}
+
+template <int DT, int U, bool NT>
+__device__ __forceinline__ void body_sw_flat(const SwArgs &a) {
+  sw_flat_part<DT, U, NT>(a, blockIdx.x, gridDim.x);
+}
+
+template <int DT>
+__device__ __forceinline__ void body_sw_rows(const SwArgs &a) {
+  sw_rows_part<DT>(a, blockIdx.x, gridDim.x);
+}
+
+template <int DT>
+__device__ __forceinline__ void body_sw_scalar(const SwArgs &a) {
+  sw_scalar_part<DT>(a, blockIdx.x, gridDim.x);
+}
+
+// The fused decode chain: workgroups take the residual-RMSNorm, RoPE-QK and
+// SwiGLU roles by blockIdx range. Norm role: one wavefront per row with N
+// vectors per lane (WAVE) or one workgroup per row with N per work-item;
+// RoPE role: one token per workgroup (QK norm first when QKN, GPT-J pairs
+// when INTER); SwiGLU role: one cached vector per work-item, or four
+// streaming ones (U4).
+//
+// Role order by blockIdx. Decode sizes (one vector): norm rows, RoPE tokens,
+// then SwiGLU -- the norm and RoPE roles take about as long as SwiGLU but
+// have far fewer workgroups, so dispatching them first shortens the critical
+// path (2.75 vs 3.1 µs device time at 1 token). Streaming sizes (U4):
+// SwiGLU first, then norm, then RoPE (about 1 % faster at 8192 tokens than
+// norm first).
+template <int DT, bool WAVE, int N>
+__device__ __forceinline__ void chain_norm_role(const ChainArgs &a, uint32_t blk) {
+  if constexpr (WAVE) {
+    rn_wave_block<DT, N, true, false>(a.rn, blk);
+  } else {
+    __shared__ float red[4];
+    rn_row_regs<DT, N, true, 256, false>(a.rn, blk, threadIdx.x, red);
+  }
+}
+
+template <int DT, bool WAVE, int N, bool U4, bool QKN, bool INTER>
+__device__ __forceinline__ void body_chain(const ChainArgs &a) {
+  __shared__ float lds[2 * 256];
+  const uint32_t b = blockIdx.x;
+  const uint32_t R = a.rn_blocks, P = a.rope_blocks, S = gridDim.x - R - P;
+  if constexpr (U4) {
+    if (b < S) {
+      sw_flat_part<DT, 4, true>(a.sw, b, S);
+    } else if (b < S + R) {
+      chain_norm_role<DT, WAVE, N>(a, b - S);
+    } else {
+      rope_vec_block<DT, 1, false, 4, QKN, INTER>(a.rope, b - S - R, lds);
+    }
+  } else {
+    if (b < R) {
+      chain_norm_role<DT, WAVE, N>(a, b);
+    } else if (b < R + P) {
+      rope_vec_block<DT, 1, false, 4, QKN, INTER>(a.rope, b - R, lds);
+    } else {
+      sw_flat_part<DT, 1, false>(a.sw, b - R - P, S);
+    }
   }
 }
 

@@ -8,25 +8,22 @@ using namespace dev;
 
 template <int DT, int NV, bool RES>
 __global__ __launch_bounds__(256) void k_rn_wave(RnArgs a) {
-  rn_wave_block<DT, NV, RES, false>(a, blockIdx.x);
+  body_rn_wave<DT, NV, RES>(a);
 }
 
 template <int DT, int NB, bool RES>
 __global__ __launch_bounds__(256) void k_rn_block(RnArgs a) {
-  __shared__ float red[4];
-  rn_row_regs<DT, NB, RES, 256, false>(a, blockIdx.x, threadIdx.x, red);
+  body_rn_block<DT, NB, RES>(a);
 }
 
 template <int DT, bool RES>
 __global__ __launch_bounds__(256) void k_rn_loop(RnArgs a) {
-  __shared__ double red[4];
-  rn_loop_row<DT, RES>(a, blockIdx.x, red);
+  body_rn_loop<DT, RES>(a);
 }
 
 template <int DT, bool RES>
 __global__ __launch_bounds__(256) void k_rn_scalar(RnArgs a) {
-  __shared__ double red[4];
-  rn_scalar_row<DT, RES>(a, blockIdx.x, red);
+  body_rn_scalar<DT, RES>(a);
 }
 
 namespace {

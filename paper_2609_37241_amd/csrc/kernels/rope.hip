@@ -11,14 +11,12 @@ using namespace dev;
 // QKN: per-head RMSNorm of Q and K before the rotation; INTER: GPT-J pairs.
 template <int DT, bool QKN, bool INTER>
 __global__ __launch_bounds__(256) void k_rope_vec(RopeArgs a) {
-  __shared__ float lds[2 * 256];
-  rope_vec_block<DT, 1, false, 4, QKN, INTER>(a, blockIdx.x, lds);
+  body_rope_vec<DT, QKN, INTER>(a);
 }
 
 template <int DT, bool QKN>
 __global__ __launch_bounds__(256) void k_rope_scalar(RopeArgs a) {
-  __shared__ float lds[(QKN ? 3 : 2) * 256];
-  rope_scalar_block<DT, QKN>(a, blockIdx.x, lds);
+  body_rope_scalar<DT, QKN>(a);
 }
 
 namespace {

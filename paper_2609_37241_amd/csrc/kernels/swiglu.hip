@@ -7,17 +7,17 @@ using namespace dev;
 
 template <int DT, int U, bool NT>
 __global__ __launch_bounds__(256) void k_sw_flat(SwArgs a) {
-  sw_flat_part<DT, U, NT>(a, blockIdx.x, gridDim.x);
+  body_sw_flat<DT, U, NT>(a);
 }
 
 template <int DT>
 __global__ __launch_bounds__(256) void k_sw_rows(SwArgs a) {
-  sw_rows_part<DT>(a, blockIdx.x, gridDim.x);
+  body_sw_rows<DT>(a);
 }
 
 template <int DT>
 __global__ __launch_bounds__(256) void k_sw_scalar(SwArgs a) {
-  sw_scalar_part<DT>(a, blockIdx.x, gridDim.x);
+  body_sw_scalar<DT>(a);
 }
 
 namespace {

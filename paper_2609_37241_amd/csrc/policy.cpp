@@ -6,6 +6,8 @@
 // and installing a version means choosing among them. The choice is a pure
 // function of the key (dtype, sizes, token bucket, alignment and contiguity
 // flags, RoPE variant), so the same key always selects the same kernels.
+#include <string.h>
+
 #include "internal.h"
 
 namespace tri {
@@ -133,6 +135,46 @@ bool rope_vec_role(int32_t v) {
 }
 
 }  // namespace
+
+// A key the entry points could have produced (used to check imported keys):
+// the same limits as argument validation, unused fields zero.
+bool key_valid(const Key &k) {
+  const uint32_t op = key_op(k), dt = key_dtype(k), fl = key_flags(k);
+  if (op < TRI_OP_RMSNORM || op > TRI_OP_QK_NORM_ROPE) return false;
+  if (dt != TRI_F32 && dt != TRI_BF16) return false;
+  if (key_bucket(k) > 22) return false;
+  const bool chain = op == TRI_OP_CHAIN;
+  if (fl > (chain ? 0x7Fu : 0x3u)) return false;
+  const bool norm = op == TRI_OP_RMSNORM || op == TRI_OP_RES_RMSNORM || chain;
+  const bool sw = op == TRI_OP_SWIGLU || chain;
+  const bool rope = op == TRI_OP_ROPE_QK || op == TRI_OP_QK_NORM_ROPE || chain;
+  const uint64_t H = key_H(k), I = key_I(k);
+  if (norm ? (H < 1 || int64_t(H) >= kHLimit) : H != 0) return false;
+  if (sw ? (I < 1 || int64_t(I) >= kILimit) : I != 0) return false;
+  if (!rope) return k.k0 >> 32 == 0 && k.k2 == 0 && k.k3 == 0 && k.k4 == 0 && k.k5 == 0;
+  const uint32_t hd = key_hd(k), nq = key_nq(k), nk = key_nk(k), rd = key_rd(k);
+  if (k.k2 >> 48) return false;
+  if (hd < 2 || (hd & 1) || int32_t(hd) > kHdMax) return false;
+  if (nq < 1 || int32_t(nq) > kHeadsMax || int32_t(nk) > kHeadsMax) return false;
+  if (rd < 2 || (rd & 1) || rd > hd) return false;
+  const uint32_t bits = key_rope_bits(k), scaling = key_scaling(k);
+  if (bits > 7) return false;
+  if (bits & kRopeCache) return (k.k3 >> 24) == 0 && k.k0 >> 32 == 0 && k.k4 == 0 && k.k5 == 0;
+  float base, f, lo, hi;
+  const uint32_t bb = key_base_bits(k), fb = uint32_t(k.k4), lb = uint32_t(k.k4 >> 32),
+                 hb = uint32_t(k.k5);
+  memcpy(&base, &bb, 4);
+  if (!(base > 1.0f && base <= 3.4028235e38f)) return false;   // finite, > 1 (NaN fails)
+  if (scaling == TRI_ROPE_SCALING_NONE) return (k.k3 >> 24) == 0 && k.k4 == 0 && k.k5 == 0;
+  if (scaling != TRI_ROPE_SCALING_LLAMA3 || k.k5 >> 32) return false;
+  memcpy(&f, &fb, 4);
+  memcpy(&lo, &lb, 4);
+  memcpy(&hi, &hb, 4);
+  const float fmax = 3.4028235e38f;
+  if (!(f > 0.0f && f <= fmax) || !(lo > 0.0f && lo <= fmax) || !(hi > lo && hi <= fmax))
+    return false;
+  return int32_t(key_orig_max(k)) >= 1;
+}
 
 Plan plan_for_key(const Key &k) {
   const uint32_t op = key_op(k), dt = key_dtype(k), b = key_bucket(k), fl = key_flags(k);

@@ -7,6 +7,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <string>
 #include <vector>
 
 #include "internal.h"
@@ -25,6 +26,9 @@ std::vector<Rec> g_log;
 int64_t g_fail_at = -1;        // launch ordinal that fails, -1 none
 int g_init_status = 0;
 int64_t g_uploads = 0;
+std::vector<std::string> g_jit;   // sources compiled, in order
+int64_t g_unloads = 0;
+bool g_jit_fail = false;
 
 uintptr_t encode(int32_t v, uint32_t dt, int32_t sub) {
   return (uintptr_t(uint32_t(v)) << 20) | (uintptr_t(dt) << 16) | uintptr_t(uint32_t(sub) & 0xFFFF) |
@@ -51,9 +55,13 @@ int be_launch(void *fn, uint32_t grid, uint32_t block, const void *args, uint32_
   Rec r;
   memset(&r, 0, sizeof r);
   const uintptr_t h = reinterpret_cast<uintptr_t>(fn);
-  r.kvariant = int32_t((h >> 20) & 0xFFFFF);
-  r.dtype = int32_t((h >> 16) & 0xF);
-  r.ksub = int32_t(h & 0xFFFF);
+  if (h & (uintptr_t(1) << 41)) {   // a compiled specialization: -(its source index + 1)
+    r.kvariant = -int32_t(((h >> 20) & 0xFFFFF) + 1);
+  } else {
+    r.kvariant = int32_t((h >> 20) & 0xFFFFF);
+    r.dtype = int32_t((h >> 16) & 0xF);
+    r.ksub = int32_t(h & 0xFFFF);
+  }
   r.grid = grid;
   r.block = block;
   r.stream = stream;
@@ -74,6 +82,23 @@ int be_upload(const void *host, uint64_t bytes, void **dev) {
 
 void be_free(void *dev) { free(dev); }
 
+// Runtime compilation: records the source and hands out a handle that
+// encodes the position of the source in the log (bit 41 marks it).
+int be_jit(const char *src, uint64_t len, void **fn, void **module, float *ms) {
+  if (g_jit_fail) return TRI_E_RUNTIME;
+  g_jit.emplace_back(src, size_t(len));
+  const uintptr_t idx = uintptr_t(g_jit.size() - 1);
+  *fn = reinterpret_cast<void *>((uintptr_t(1) << 41) | (idx << 20));
+  *module = reinterpret_cast<void *>(uintptr_t(0x100000 + idx));
+  *ms = 1.0f;
+  return 0;
+}
+
+void be_unload(void *module) {
+  (void)module;
+  g_unloads++;
+}
+
 }  // namespace tri
 
 extern "C" {
@@ -83,6 +108,20 @@ void trifake_reset() {
   g_fail_at = -1;
   g_init_status = 0;
   g_uploads = 0;
+  g_jit.clear();
+  g_unloads = 0;
+  g_jit_fail = false;
+}
+int64_t trifake_jit_count() { return int64_t(g_jit.size()); }
+int64_t trifake_unload_count() { return g_unloads; }
+void trifake_jit_fail(int on) { g_jit_fail = on != 0; }
+// Source i of the runtime compilations: copies up to cap bytes, returns its
+// length (or -1).
+int64_t trifake_jit_source(int64_t i, char *buf, int64_t cap) {
+  if (i < 0 || i >= int64_t(g_jit.size())) return -1;
+  const std::string &s = g_jit[size_t(i)];
+  if (buf && cap > 0) memcpy(buf, s.data(), size_t(int64_t(s.size()) < cap ? int64_t(s.size()) : cap));
+  return int64_t(s.size());
 }
 int64_t trifake_launch_count() { return int64_t(g_log.size()); }
 int64_t trifake_upload_count() { return g_uploads; }

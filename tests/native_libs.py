@@ -30,8 +30,8 @@ def ensure_libtri() -> str:
 
 def ensure_fake() -> str:
     srcs = [FAKE_SRC] + [os.path.join(PKG, "csrc", n)
-                         for n in ("api.cpp", "cache.cpp", "policy.cpp", "internal.h",
-                                   "kernargs.h")]
+                         for n in ("api.cpp", "cache.cpp", "policy.cpp", "jit.cpp",
+                                   "internal.h", "kernargs.h", "kernels/device.h")]
     stale = (not os.path.exists(FAKE_LIB)
              or any(os.path.getmtime(s) > os.path.getmtime(FAKE_LIB) for s in srcs))
     if stale:
@@ -48,6 +48,11 @@ def load_fake():
     lib.trifake_upload_count.restype = C.c_int64
     lib.trifake_fail_at.argtypes = [C.c_int64]
     lib.trifake_init_status.argtypes = [C.c_int]
+    lib.trifake_jit_count.restype = C.c_int64
+    lib.trifake_unload_count.restype = C.c_int64
+    lib.trifake_jit_fail.argtypes = [C.c_int]
+    lib.trifake_jit_source.restype = C.c_int64
+    lib.trifake_jit_source.argtypes = [C.c_int64, C.c_char_p, C.c_int64]
     lib.trifake_get.argtypes = [C.c_int64, C.POINTER(C.c_int32), C.POINTER(C.c_int32),
                                 C.POINTER(C.c_int32), C.POINTER(C.c_uint32),
                                 C.POINTER(C.c_uint32), C.POINTER(C.c_void_p),

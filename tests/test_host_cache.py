@@ -338,7 +338,9 @@ def test_install_needs_a_miss_and_is_idempotent(lib, fresh):
 def test_create_errors(lib):
     h = C.c_void_p()
     assert lib.tri_spec_cache_create(C.byref(h), 4097, 0) == S.E_INVALID
-    assert lib.tri_spec_cache_create(C.byref(h), 0, 2) == S.E_INVALID
+    assert lib.tri_spec_cache_create(C.byref(h), 0, 4) == S.E_INVALID
+    assert lib.tri_spec_cache_create(C.byref(h), 0, 3) == S.OK      # auto-install + JIT
+    lib.tri_spec_cache_destroy(h)
     assert lib.tri_spec_cache_create(None, 0, 0) == S.E_INVALID
     lib.trifake_init_status(S.E_RUNTIME)
     assert lib.tri_spec_cache_create(C.byref(h), 0, 0) == S.E_RUNTIME
@@ -453,6 +455,179 @@ def test_layers_limit(lib, fresh):
     assert run_layers_both(lib, cache, m, [c] * S.MAX_LAYERS) == S.OK
     assert run_layers_both(lib, cache, m, [c] * (S.MAX_LAYERS + 1)) == S.E_INVALID
     assert lib.tri_decode_chain_layers(cache, None, 2, None) == S.E_INVALID
+
+
+# ---- runtime-compiled specializations and key import / export ------------------------------
+def test_jit_cache_makes_the_same_selections(lib, fresh):
+    cache = fresh(flags=S.FLAG_AUTO_INSTALL | S.FLAG_JIT)
+    m = S.SpecCacheModel(flags=S.FLAG_AUTO_INSTALL | S.FLAG_JIT)
+    for c in call_zoo():
+        run_both(lib, cache, m, c)
+    # one compiled kernel per launch of every installed version
+    n_launch = sum(len(S.plan(k, 1)[2]) for k in m.versions)
+    assert lib.trifake_jit_count() == n_launch
+
+
+def jit_sources(lib):
+    out = []
+    for i in range(lib.trifake_jit_count()):
+        n = lib.trifake_jit_source(i, None, 0)
+        buf = C.create_string_buffer(n + 1)
+        lib.trifake_jit_source(i, buf, n + 1)
+        out.append(buf.raw[:n].decode())
+    return out
+
+
+def _kernel_part(src):
+    return src[src.rindex('extern "C"'):]
+
+
+def test_jit_source_fixes_the_key_shape(lib, fresh):
+    cache = fresh(flags=S.FLAG_AUTO_INSTALL | S.FLAG_JIT)
+    # fused: RN_BLOCK_2 norm role, QK-norm GPT-J RoPE role, cached SwiGLU
+    c = chain_call(BF, 1, 4096, 12288, 32, 8, 128, base=1e6, qk_norm=True,
+                   ext=dict(interleaved=1))
+    assert S.plan(S.make_key(c), 1)[0] == S.CH_FUSED
+    assert c_call(lib, cache, c) == 0
+    (src,) = jit_sources(lib)
+    k = _kernel_part(src)
+    assert "tri_jit_kernel(tri::ChainArgs a)" in k
+    for frag in ("a.rn.H = 4096;", "a.rope.hd = 128;", "a.rope.rd = 128;", "a.rope.nq = 32;",
+                 "a.rope.nk = 8;", "a.rope.mode = 1u;", "a.sw.I = 12288;",
+                 "body_chain<1, false, 2, false, true, true>(a)"):
+        assert frag in k, frag
+    assert src.startswith("// Kernel argument blocks")     # the embedded prelude
+    assert "#include <hip/" not in src and '#include "../kernargs.h"' not in src
+    # three launches (partial rotary with the QK norm takes the scalar role):
+    # one specialization per role kernel, each with its own fields fixed
+    c = chain_call(F, 2, 4096, 12288, 32, 8, 128, base=1e6, qk_norm=True,
+                   ext=dict(rotary_dim=64, pos_int64=1))
+    assert c_call(lib, cache, c) == 0
+    rn, rope, sw = (_kernel_part(x) for x in jit_sources(lib)[1:])
+    assert "tri::RnArgs a" in rn and "a.H = 4096;" in rn and "body_rn_block<0, 4, true>" in rn
+    assert ("a.rd = 64;" in rope and "a.mode = 2u;" in rope
+            and "body_rope_scalar<0, true>" in rope)
+    assert "a.I = 12288;" in sw and "body_sw_flat<0, 1, false>" in sw
+
+
+def test_jit_failure_installs_nothing(lib, fresh):
+    cache = fresh(flags=S.FLAG_AUTO_INSTALL | S.FLAG_JIT)
+    lib.trifake_jit_fail(1)
+    assert c_call(lib, cache, chain_call(BF, 1, 256, 688, 4, 4, 64)) == S.E_RUNTIME
+    assert c_stats(lib, cache)[5:] == (0, 0)
+    lib.trifake_jit_fail(0)
+    assert c_call(lib, cache, chain_call(BF, 1, 256, 688, 4, 4, 64)) == 0
+    assert c_stats(lib, cache)[5:] == (1, 1)
+
+
+def _hiprtc():
+    h = C.CDLL("/opt/rocm/lib/libhiprtc.so")
+    h.hiprtcCreateProgram.argtypes = [C.POINTER(C.c_void_p), C.c_char_p, C.c_char_p, C.c_int,
+                                      C.c_void_p, C.c_void_p]
+    h.hiprtcCompileProgram.argtypes = [C.c_void_p, C.c_int, C.POINTER(C.c_char_p)]
+    h.hiprtcGetProgramLogSize.argtypes = [C.c_void_p, C.POINTER(C.c_size_t)]
+    h.hiprtcGetProgramLog.argtypes = [C.c_void_p, C.c_char_p]
+    h.hiprtcGetCodeSize.argtypes = [C.c_void_p, C.POINTER(C.c_size_t)]
+    h.hiprtcDestroyProgram.argtypes = [C.POINTER(C.c_void_p)]
+    return h
+
+
+def _compile(h, src):
+    prog = C.c_void_p()
+    assert h.hiprtcCreateProgram(C.byref(prog), src.encode(), b"t.hip", 0, None, None) == 0
+    opts = [b"--offload-arch=gfx950", b"-O3", b"-std=c++17", b"-ffp-contract=off", b"-Xclang",
+            b"-target-feature", b"-Xclang", b"-packed-fp32-ops"]
+    arr = (C.c_char_p * len(opts))(*opts)
+    rc = h.hiprtcCompileProgram(prog, len(opts), arr)
+    n = C.c_size_t()
+    h.hiprtcGetProgramLogSize(prog, C.byref(n))
+    log = C.create_string_buffer(n.value + 1)
+    h.hiprtcGetProgramLog(prog, log)
+    size = C.c_size_t()
+    h.hiprtcGetCodeSize(prog, C.byref(size))
+    h.hiprtcDestroyProgram(C.byref(prog))
+    return rc, log.value.decode(errors="replace"), size.value
+
+
+def test_every_kind_of_generated_source_compiles(lib, fresh):
+    """hipRTC (it needs no GPU) compiles one source for every kernel body
+    and template form the zoo's versions produce."""
+    import os
+    import re
+    if not os.path.exists("/opt/rocm/lib/libhiprtc.so"):
+        pytest.skip("hipRTC not installed")
+    cache = fresh(capacity=S.MAX_CAPACITY, flags=S.FLAG_AUTO_INSTALL | S.FLAG_JIT)
+    for c in call_zoo():
+        c_call(lib, cache, c)
+    forms = {}
+    for src in jit_sources(lib):
+        body = re.search(r"tri::dev::(\w+<[^>]*>)", _kernel_part(src)).group(1)
+        forms.setdefault(body, src)
+    assert len(forms) >= 30
+    h = _hiprtc()
+    for body, src in sorted(forms.items()):
+        rc, log, size = _compile(h, src)
+        assert rc == 0 and size > 0, (body, log[-2000:])
+
+
+def test_export_import_prewarms_a_cache(lib, fresh):
+    a = fresh(capacity=S.MAX_CAPACITY, flags=S.FLAG_AUTO_INSTALL)
+    for c in call_zoo():
+        c_call(lib, a, c)
+    n = C.c_uint32()
+    assert lib.tri_spec_export_keys(a, None, 0, C.byref(n)) == 0
+    buf = (C.c_uint64 * (6 * n.value))()
+    assert lib.tri_spec_export_keys(a, buf, n.value, C.byref(n)) == 0
+    keys = [tuple(buf[6 * i: 6 * i + 6]) for i in range(n.value)]
+    assert all(S.key_valid(k) for k in keys)
+    assert 256 < n.value < S.MAX_CAPACITY
+    b = fresh(capacity=S.MAX_CAPACITY)
+    m = S.SpecCacheModel(capacity=S.MAX_CAPACITY)
+    done = C.c_uint32()
+    assert lib.tri_spec_import_keys(b, buf, n.value, C.byref(done)) == 0 and done.value == n.value
+    assert m.import_keys(keys) == (S.OK, len(keys))
+    for c in call_zoo():                     # no misses after the pre-warm
+        assert run_both(lib, b, m, c, install=False) != S.MISS
+    assert m.stats.misses == 0
+
+
+def _mutations(key):
+    k = list(key)
+    out = []
+    for word, shift, width in ((0, 0, 8), (0, 8, 8), (0, 16, 8), (0, 24, 8), (0, 32, 32),
+                               (1, 0, 32), (1, 32, 32), (2, 0, 16), (2, 16, 16), (2, 32, 16),
+                               (2, 48, 16), (3, 0, 16), (3, 16, 8), (3, 24, 8), (3, 32, 32),
+                               (4, 0, 32), (4, 32, 32), (5, 0, 32), (5, 32, 32)):
+        for val in (0, 1, 2, 3, 7, 0x7F, 0xFF, 0x7F800000, 0x3F800000, 0x4F000000, (1 << width) - 1):
+            val &= (1 << width) - 1
+            m = list(k)
+            m[word] = (m[word] & ~(((1 << width) - 1) << shift)) | (val << shift)
+            out.append(tuple(m))
+    return out
+
+
+def test_imported_keys_are_checked_like_the_model(lib, fresh):
+    base_keys = [S.make_key(c) for c in (
+        chain_call(BF, 8, 4096, 14336, 32, 8, 128, base=5e5),
+        chain_call(F, 1, 256, 688, 4, 4, 64, qk_norm=True, ext=dict(interleaved=1, rotary_dim=32)),
+        rope_call(BF, 3, 8, 2, 128, ext=dict(LLAMA3)),
+        rope_call(BF, 3, 8, 2, 128, ext=dict(cos_sin=CACHE_ADDR, cos_sin_len=7)),
+        rn_call(F, 5, 4096), sw_call(BF, 9, 11008), qkn_call(BF, 1, 32, 8, 128))]
+    seen = set()
+    n_bad = 0
+    for key in base_keys:
+        for mk in [key] + _mutations(key):
+            if mk in seen:
+                continue
+            seen.add(mk)
+            cache = fresh()
+            buf = (C.c_uint64 * 6)(*mk)
+            done = C.c_uint32()
+            st = lib.tri_spec_import_keys(cache, buf, 1, C.byref(done))
+            want = S.key_valid(mk)
+            assert (st == 0) == want, (hex(mk[0]), [hex(x) for x in mk], st)
+            n_bad += not want
+    assert n_bad > 100
 
 
 # ---- argument preparation ----------------------------------------------------------
