@@ -25,6 +25,11 @@ are:
   RMS-normalised over its hd elements with a per-dimension weight (one
   weight vector for Q, one for K) and then rotated; the normalised head is
   not rounded in between, so the fused op rounds once, like every op here.
+* Short ops of the paper's suite (`silu`, `add`, `masked_fill`,
+  `embedding`): silu as in SwiGLU without the up operand; add rounds the
+  exact sum once; masked_fill writes the fill value rounded to the dtype
+  where the uint8 mask is nonzero and copies x bit for bit elsewhere;
+  embedding copies table rows by id and writes zeros for ids out of range.
 * Decode chain: the three ops above on disjoint operands, in one call; with
   head-norm weights given, RoPE becomes QK-RMSNorm + RoPE.
 * RoPE variants (`rope_ext`): GPT-J pairs (2i, 2i + 1) instead of
@@ -265,6 +270,40 @@ def swiglu(gate, up, dtype):
     return round_to(out, dtype)
 
 
+# ---- short element-wise and gather ops (the paper's operator suite, Sec. 4.1) ----
+def silu(x, dtype):
+    """silu(x) = x / (1 + exp(-x)), one rounding; very negative x gives a
+    signed zero (the exponential overflows), never NaN."""
+    v = values(x, dtype)
+    with np.errstate(over="ignore"):
+        return round_to(v / (1.0 + np.exp(-v)), dtype)
+
+
+def add(a, b, dtype):
+    """a + b, one rounding of the exact sum."""
+    return round_to(values(a, dtype) + values(b, dtype), dtype)
+
+
+def masked_fill(x, mask, value, dtype):
+    """Where mask (uint8, nonzero = set) the element becomes `value` rounded
+    to the dtype (from the float32 the caller passes); elsewhere x is copied."""
+    v = round_to(np.full(1, float(np.float32(value)), dtype=np.float64), dtype)[0]
+    out = np.array(x, copy=True)
+    out[np.asarray(mask) != 0] = v
+    return out
+
+
+def embedding(table, ids, dtype):
+    """Rows of table [n_rows, H] picked by ids [T] (int32 or int64); an id
+    outside [0, n_rows) gives a row of zeros."""
+    ids = np.asarray(ids).astype(np.int64)
+    n_rows = table.shape[0]
+    ok = (ids >= 0) & (ids < n_rows)
+    out = np.zeros((ids.shape[0],) + table.shape[1:], dtype=table.dtype)
+    out[ok] = table[ids[ok]]
+    return out
+
+
 def decode_chain(inp: Dict[str, np.ndarray], eps: float, base: float,
                  dtype: str) -> Dict[str, np.ndarray]:
     """Residual add + RMSNorm, RoPE on Q/K and SwiGLU on disjoint operands.
@@ -283,6 +322,6 @@ def decode_chain(inp: Dict[str, np.ndarray], eps: float, base: float,
     return dict(y=y, res_out=h, q=qo, k=ko, out=out)
 
 
-__all__ = ["rmsnorm", "residual_add", "residual_rmsnorm", "rope_inv_freq",
+__all__ = ["silu", "add", "masked_fill", "embedding", "rmsnorm", "residual_add", "residual_rmsnorm", "rope_inv_freq",
            "rope_inv_freq_llama3", "llama3_scale", "rope_angles", "rope_apply", "rope_qk",
            "qk_norm_rope", "rope_ext", "swiglu", "decode_chain", "F32", "BF16"]

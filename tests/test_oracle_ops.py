@@ -351,3 +351,60 @@ def test_chain_with_qk_norm_is_norm_then_rope():
     assert np.array_equal(out["q"], q) and np.array_equal(out["k"], k)
     plain = ops.rope_qk(inp["q"], inp["k"], inp["pos"], 1e6, nm.BF16)
     assert not np.array_equal(out["q"], plain[0])
+
+
+# ---- short ops: silu, add, masked_fill, embedding --------------------------------
+@pytest.mark.parametrize("dtype", [nm.F32, nm.BF16])
+def test_silu_against_torch_float64(dtype):
+    r = np.random.Generator(np.random.PCG64(21))
+    x = wl.host_array(r, (7, 300), dtype, outliers=True)
+    got = ops.silu(x, dtype)
+    want = F.silu(torch.from_numpy(nm.values(x, dtype))).numpy()
+    assert np.array_equal(got, nm.round_to(want, dtype))
+    # closed forms: silu(0) = 0, silu(-200) = -0.0 (overflow branch), silu(+inf) = +inf
+    z = nm.round_to(np.array([0.0, -200.0, np.inf, 1.0]), dtype)
+    v = nm.values(ops.silu(z, dtype), dtype)
+    assert v[0] == 0 and v[1] == 0 and np.signbit(v[1]) and np.isinf(v[2])
+    assert v[3] == nm.values(nm.round_to(np.array([1 / (1 + math.exp(-1))]), dtype), dtype)[0]
+
+
+@pytest.mark.parametrize("dtype", [nm.F32, nm.BF16])
+def test_add_rounds_the_exact_sum_like_torch(dtype):
+    r = np.random.Generator(np.random.PCG64(22))
+    a = wl.host_array(r, (5, 257), dtype, outliers=True)
+    b = wl.host_array(r, (5, 257), dtype)
+    got = ops.add(a, b, dtype)
+    ta, tb = wl.to_torch(a, dtype), wl.to_torch(b, dtype)
+    assert np.array_equal(got, wl.from_torch(ta + tb))     # torch: float32 add, one rounding
+    # 1 + 2^-8 in bf16 is a tie: rounds to even (1.0); 1 + 3 * 2^-9 rounds up
+    if dtype == nm.BF16:
+        one = nm.round_to(np.array([1.0, 1.0]), dtype)
+        d = nm.round_to(np.array([2.0 ** -8, 3 * 2.0 ** -9]), dtype)
+        s = nm.values(ops.add(one, d, dtype), dtype)
+        assert s[0] == 1.0 and s[1] == 1.0 + 2.0 ** -7
+
+
+@pytest.mark.parametrize("dtype", [nm.F32, nm.BF16])
+def test_masked_fill_like_torch(dtype):
+    r = np.random.Generator(np.random.PCG64(23))
+    x = wl.host_array(r, (6, 129), dtype)
+    mask = (r.random((6, 129)) < 0.3).astype(np.uint8) * r.integers(1, 256, (6, 129)).astype(np.uint8)
+    for value in (-1e4, 0.1, float("-inf"), 3.0e38):
+        got = ops.masked_fill(x, mask, value, dtype)
+        t = wl.to_torch(x, dtype).masked_fill(torch.from_numpy(mask != 0), value)
+        assert np.array_equal(got, wl.from_torch(t))
+    assert np.array_equal(ops.masked_fill(x, np.zeros_like(mask), 5.0, dtype), x)
+
+
+@pytest.mark.parametrize("dtype", [nm.F32, nm.BF16])
+def test_embedding_like_torch_and_zero_rows(dtype):
+    r = np.random.Generator(np.random.PCG64(24))
+    table = wl.host_array(r, (50, 64), dtype)
+    ids = r.integers(0, 50, size=9).astype(np.int32)
+    got = ops.embedding(table, ids, dtype)
+    want = F.embedding(torch.from_numpy(ids.astype(np.int64)), wl.to_torch(table, dtype))
+    assert np.array_equal(got, wl.from_torch(want))
+    bad = np.array([3, -1, 50, 2 ** 40, 49], dtype=np.int64)
+    got = ops.embedding(table, bad, dtype)
+    assert np.array_equal(got[0], table[3]) and np.array_equal(got[4], table[49])
+    assert not got[1:4].any()
