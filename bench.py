@@ -65,7 +65,11 @@ def algorithmic_bytes(cfg):
     sw = 3 * T * I * es
     qkn = rope + 2 * hd * es                     # + the two head-norm weights
     return {"rmsnorm": rms, "residual_rmsnorm": res, "rope_qk": rope, "swiglu": sw,
-            "chain": res + rope + sw, "qk_norm_rope": qkn, "chain_qk_norm": res + qkn + sw}
+            "chain": res + rope + sw, "qk_norm_rope": qkn, "chain_qk_norm": res + qkn + sw,
+            # short ops over the [T, H] activations
+            "silu": 2 * T * H * es, "add": 3 * T * H * es, "masked_fill": T * H * (2 * es + 1),
+            # T rows of H / 2 gathered from a Llama-3 sized vocabulary (ids int32)
+            "embedding": 2 * T * (H // 2) * es + 4 * T}
 
 
 def torch_eager_chain(d, eps, base, out):
@@ -409,6 +413,11 @@ def main():
         abq, _ = cb.chain_args(db["x"], db["residual"], db["w"], db["q"], db["k"], db["pos"],
                                db["gate"], db["up"], cfgb.eps, cfgb.base, y=y,
                                residual_out=ro, out=out, q_norm_w=qw, k_norm_w=kw)
+        mask = (torch.rand(db["x"].shape, device=dev) < 0.1).to(torch.uint8)
+        vocab = 128256
+        table = torch.randn((vocab, cfgb.H // 2), device=dev).to(db["x"].dtype)
+        ids = torch.randint(0, vocab, (cfgb.T,), device=dev, dtype=torch.int32)
+        emb_out = torch.empty((cfgb.T, cfgb.H // 2), device=dev, dtype=db["x"].dtype)
         copy_src = torch.empty(1 << 29, dtype=torch.bfloat16, device=dev)
         copy_dst = torch.empty_like(copy_src)
         ops = {
@@ -422,6 +431,10 @@ def main():
             "qk_norm_rope": lambda: cb.qk_norm_rope(db["q"], db["k"], db["pos"], qw, kw,
                                                     cfgb.base, cfgb.eps, stream=stream),
             "chain_qk_norm": lambda: cb.decode_chain_args(abq, stream),
+            "silu": lambda: cb.silu(db["x"], out=y, stream=stream),
+            "add": lambda: cb.add(db["x"], db["residual"], out=y, stream=stream),
+            "masked_fill": lambda: cb.masked_fill(db["x"], mask, -1e4, out=y, stream=stream),
+            "embedding": lambda: cb.embedding(table, ids, out=emb_out, stream=stream),
             "copy_1GiB_torch": lambda: copy_dst.copy_(copy_src),
         }
         nbytes["copy_1GiB_torch"] = 2 * copy_src.numel() * 2
@@ -452,7 +465,7 @@ def main():
                     "kernel": "fused decode chain, 8192 tokens (k_chain: block-per-row norm, "
                               "one-token RoPE blocks, streaming 4-vector SwiGLU)",
                     "bytes_per_launch": ch["bytes"], "avg_launch_us": ch["mean_us"]}
-        del db, y, ro, out, flush, copy_src, copy_dst
+        del db, y, ro, out, flush, copy_src, copy_dst, mask, table, ids, emb_out
 
     # ---- CPU oracle baseline (after all GPU work) ----------------------------------------
     cpu = None

@@ -69,7 +69,8 @@ typedef enum tri_status {
 typedef enum tri_op {
   TRI_OP_RMSNORM = 1, TRI_OP_RES_RMSNORM = 2, TRI_OP_ROPE_QK = 3,
   TRI_OP_SWIGLU = 4, TRI_OP_CHAIN = 5, TRI_OP_QK_NORM_ROPE = 6,
-  TRI_OP_CHAIN_LAYERS = 7   /* selection records of tri_decode_chain_layers */
+  TRI_OP_CHAIN_LAYERS = 7,  /* selection records of tri_decode_chain_layers */
+  TRI_OP_SILU = 8, TRI_OP_ADD = 9, TRI_OP_MASKED_FILL = 10, TRI_OP_EMBEDDING = 11
 } tri_op;
 
 enum { TRI_MAX_LAYERS = 1024 };   /* layers per tri_decode_chain_layers call */
@@ -288,6 +289,35 @@ tri_status tri_rope_qk_ext(tri_cache *cache, tri_dtype dtype,
 tri_status tri_swiglu(tri_cache *cache, tri_dtype dtype,
                       const void *gate, int64_t g_rs, const void *up, int64_t u_rs,
                       void *out, int64_t o_rs, int64_t T, int64_t I, void *stream);
+
+/* ---- short ops of the paper's operator suite (Sec. 4.1 lists silu, add,
+ * masked_fill and embedding among its kernels); same cache, same guards
+ * (dtype, row width, token bucket, 16-byte alignment, contiguity). ----- */
+
+/* out = x / (1 + exp(-x)) over [T, W] (a signed zero where exp overflows).
+ * out may alias x exactly. */
+tri_status tri_silu(tri_cache *cache, tri_dtype dtype, const void *x, int64_t x_rs,
+                    void *out, int64_t o_rs, int64_t T, int64_t W, void *stream);
+
+/* out = RN_dtype(a + b) over [T, W]. out may alias a or b exactly. */
+tri_status tri_add(tri_cache *cache, tri_dtype dtype, const void *a, int64_t a_rs,
+                   const void *b, int64_t b_rs, void *out, int64_t o_rs,
+                   int64_t T, int64_t W, void *stream);
+
+/* out = mask ? RN_dtype(value) : x over [T, W]; mask is uint8 [T, W] with
+ * row stride m_rs (nonzero = fill). Unmasked elements are copied bit for
+ * bit. out may alias x exactly. value may be any float (inf included). */
+tri_status tri_masked_fill(tri_cache *cache, tri_dtype dtype, const void *x, int64_t x_rs,
+                           const uint8_t *mask, int64_t m_rs, float value,
+                           void *out, int64_t o_rs, int64_t T, int64_t W, void *stream);
+
+/* out[t, :] = table[ids[t], :] for t < T: table [n_rows, H] with row stride
+ * t_rs, ids int32 [T] (int64 when ids_int64 is 1; 4- / 8-byte aligned).
+ * An id outside [0, n_rows) yields a row of zeros (ids are device data; the
+ * host never reads them). n_rows >= 1; out must not overlap the table. */
+tri_status tri_embedding(tri_cache *cache, tri_dtype dtype, const void *table, int64_t t_rs,
+                         int64_t n_rows, const void *ids, int32_t ids_int64,
+                         void *out, int64_t o_rs, int64_t T, int64_t H, void *stream);
 
 /* The decode chain: residual+RMSNorm, RoPE-QK (or QK-RMSNorm + RoPE when
  * q_norm_w is set; with the variant of rope_ext when set) and SwiGLU of one

@@ -40,6 +40,9 @@ import numpy as np
 OP_RMSNORM, OP_RES_RMSNORM, OP_ROPE_QK, OP_SWIGLU, OP_CHAIN, OP_QK_NORM_ROPE = 1, 2, 3, 4, 5, 6
 ROPE_OPS = (OP_ROPE_QK, OP_QK_NORM_ROPE, OP_CHAIN)
 OP_CHAIN_LAYERS = 7        # records of the several-chains entry point
+OP_SILU, OP_ADD, OP_MASKED_FILL, OP_EMBEDDING = 8, 9, 10, 11
+ELT_OPS = (OP_SILU, OP_ADD, OP_MASKED_FILL)
+SHORT_OPS = ELT_OPS + (OP_EMBEDDING,)
 MAX_LAYERS = 1024
 DT_F32, DT_BF16 = 0, 1
 OK, MISS = 0, 1
@@ -54,6 +57,8 @@ ROPE_SCALAR, ROPE_VEC, ROPE_VEC_I, ROPE_QKN_SCALAR, ROPE_QKN_VEC, ROPE_QKN_VEC_I
 ROPE_VEC_ROLES = (ROPE_VEC, ROPE_VEC_I, ROPE_QKN_VEC, ROPE_QKN_VEC_I)
 SW_SCALAR, SW_FLAT, SW_FLAT_NT, SW_ROWS, SW_FLAT_U4_NT = 40, 41, 42, 43, 44
 CH_FUSED, CH_SEQ = 50, 51
+ELT_SCALAR, ELT_FLAT, ELT_FLAT_U2, ELT_ROWS = 60, 61, 62, 63
+EMB_SCALAR, EMB_VEC = 70, 71
 DECODE_BUCKET_MAX = 6       # buckets up to here are decode sized
 
 BLOCK = 256
@@ -173,6 +178,26 @@ def sw_role(dtype: int, I: int, flags: int, b: int, T: int,
     return SW_SCALAR, min(cdiv(T * I, BLOCK), GRID_CAP)
 
 
+def elt_role(dtype: int, W: int, flags: int, b: int, T: int) -> Tuple[int, int]:
+    """silu / add / masked_fill: flat vectors when aligned and contiguous
+    (beyond decode sizes two per work-item), vector rows when only the rows
+    are aligned, element-wise otherwise."""
+    v = 16 // elem_size(dtype)
+    if (flags & ALIGN) and (flags & CONTIG):
+        if b <= DECODE_BUCKET_MAX:
+            return ELT_FLAT, max(1, min(cdiv((T * W) // v, BLOCK), GRID_CAP))
+        return ELT_FLAT_U2, max(1, min(cdiv((T * W) // v, 2 * BLOCK), GRID_CAP))
+    if (flags & ALIGN) and W % v == 0:
+        return ELT_ROWS, min(T * cdiv(W // v, BLOCK), GRID_CAP)
+    return ELT_SCALAR, min(cdiv(T * W, BLOCK), GRID_CAP)
+
+
+def emb_role(dtype: int, H: int, flags: int, T: int) -> Tuple[int, int]:
+    """One workgroup per output row; vectors when aligned and H % v == 0."""
+    v = 16 // elem_size(dtype)
+    return (EMB_VEC if (flags & ALIGN) and H % v == 0 else EMB_SCALAR), max(1, min(T, GRID_CAP))
+
+
 # ---- calls -------------------------------------------------------------------
 @dataclasses.dataclass
 class Call:
@@ -180,8 +205,11 @@ class Call:
     op: int
     dtype: int
     T: int
-    H: int = 0
+    H: int = 0                # RMSNorm hidden size; row width W of the short ops
     I: int = 0
+    n_rows: int = 0           # embedding table rows
+    ids64: int = 0            # embedding: int64 ids
+    value: float = 0.0        # masked_fill value
     hd: int = 0
     nq: int = 0
     nk: int = 0
@@ -335,6 +363,35 @@ RES_PTRS = ("x", "res", "w", "y", "res_out")
 RES_STRIDES = ("x", "res", "y", "res_out")
 
 
+def _validate_short(c: Call) -> Optional[int]:
+    es = elem_size(c.dtype)
+    p, s = c.ptr, c.stride
+    if c.op == OP_EMBEDDING:
+        if c.H < 1 or c.n_rows < 1 or c.ids64 not in (0, 1):
+            return E_INVALID
+        if c.H >= I_LIMIT:
+            return E_UNSUPPORTED
+        if any(p.get(n) is None for n in ("table", "ids", "out")):
+            return E_INVALID
+        if p["table"] % es or p["out"] % es or p["ids"] % (8 if c.ids64 else 4):
+            return E_INVALID
+        if s["table"] < c.H or s["out"] < c.H:
+            return E_INVALID
+        return None
+    names = ("a", "b", "out")
+    if c.H < 1:
+        return E_INVALID
+    if c.H >= I_LIMIT:
+        return E_UNSUPPORTED
+    if any(p.get(n) is None for n in names):
+        return E_INVALID
+    if p["a"] % es or p["out"] % es or (c.op != OP_MASKED_FILL and p["b"] % es):
+        return E_INVALID
+    if any(s[n] < c.H for n in names):
+        return E_INVALID
+    return None
+
+
 def validate(c: Call) -> Optional[int]:
     """None if the call is valid and non-empty, else its status."""
     st = _validate_common(c)
@@ -351,6 +408,8 @@ def validate(c: Call) -> Optional[int]:
         return st if st is not None else _validate_qkn(c, c.eps)
     if c.op == OP_SWIGLU:
         return _validate_sw(c)
+    if c.op in SHORT_OPS:
+        return _validate_short(c)
     if c.op == OP_CHAIN:
         checks = [lambda: _validate_rn(c, RES_PTRS, RES_STRIDES), lambda: _validate_rope(c)]
         if chain_has_qk_norm(c):
@@ -401,6 +460,21 @@ def sw_flags(c: Call) -> int:
     return f
 
 
+def short_flags(c: Call) -> int:
+    es = elem_size(c.dtype)
+    p, s = c.ptr, c.stride
+    if c.op == OP_EMBEDDING:
+        return ALIGN if _aligned(es, [p["table"], p["out"]], [s["table"], s["out"]]) else 0
+    v = 16 // es
+    if c.op == OP_MASKED_FILL:
+        al = (_aligned(es, [p["a"], p["out"]], [s["a"], s["out"]])
+              and p["b"] % v == 0 and s["b"] % v == 0)
+    else:
+        al = _aligned(es, [p["a"], p["b"], p["out"]], [s["a"], s["b"], s["out"]])
+    contig = all(s[n] == c.H for n in ("a", "b", "out"))
+    return (ALIGN if al else 0) | (CONTIG if contig else 0)
+
+
 def op_flags(c: Call) -> int:
     if c.op == OP_RMSNORM:
         return rn_flags(c, RN_PTRS, RN_STRIDES)
@@ -412,6 +486,8 @@ def op_flags(c: Call) -> int:
         return rope_flags(c, True)
     if c.op == OP_SWIGLU:
         return sw_flags(c)
+    if c.op in SHORT_OPS:
+        return short_flags(c)
     qkn = chain_has_qk_norm(c)
     return (rn_flags(c, RES_PTRS, RES_STRIDES) | (rope_flags(c, qkn) << 2)
             | (sw_flags(c) << 4) | (CHAIN_QK_NORM if qkn else 0))
@@ -427,7 +503,7 @@ def make_key(c: Call) -> Tuple[int, ...]:
     are unused."""
     b = bucket(c.T)
     flags = op_flags(c)
-    H = c.H if c.op in (OP_RMSNORM, OP_RES_RMSNORM, OP_CHAIN) else 0
+    H = c.H if c.op in (OP_RMSNORM, OP_RES_RMSNORM, OP_CHAIN) + SHORT_OPS else 0
     I = c.I if c.op in (OP_SWIGLU, OP_CHAIN) else 0
     hd, nq, nk = (c.hd, c.nq, c.nk) if c.op in ROPE_OPS else (0, 0, 0)
     base_bits, k3, k4, k5 = 0, 0, 0, 0
@@ -444,6 +520,8 @@ def make_key(c: Call) -> Tuple[int, ...]:
                 k3 |= (SCALING_LLAMA3 << 24) | ((x["original_max_pos"] & 0xFFFFFFFF) << 32)
                 k4 = f32_bits(x["factor"]) | (f32_bits(x["low_freq_factor"]) << 32)
                 k5 = f32_bits(x["high_freq_factor"])
+    if c.op == OP_EMBEDDING:
+        k3 = c.ids64 << 16
     k0 = c.op | (c.dtype << 8) | (b << 16) | (flags << 24) | (base_bits << 32)
     k1 = H | (I << 32)
     k2 = hd | (nq << 16) | (nk << 32)
@@ -472,12 +550,20 @@ def key_valid(key) -> bool:
     f = unpack_key(key)
     k0, k1, k2, k3, k4, k5 = key
     op = f["op"]
-    if op not in (OP_RMSNORM, OP_RES_RMSNORM, OP_ROPE_QK, OP_SWIGLU, OP_CHAIN, OP_QK_NORM_ROPE):
+    if op not in (OP_RMSNORM, OP_RES_RMSNORM, OP_ROPE_QK, OP_SWIGLU, OP_CHAIN,
+                  OP_QK_NORM_ROPE) + SHORT_OPS:
         return False
     if f["dtype"] not in (DT_F32, DT_BF16) or f["bucket"] > 22:
         return False
     if f["flags"] > (0x7F if op == OP_CHAIN else 0x3):
         return False
+    if op in SHORT_OPS:
+        if not (1 <= f["H"] < I_LIMIT) or f["I"] != 0:
+            return False
+        if op == OP_EMBEDDING and f["flags"] & CONTIG:
+            return False
+        k3_ok = (1 << 16) if op == OP_EMBEDDING else 0
+        return f["base_bits"] == 0 and k2 == 0 and (k3 & ~k3_ok) == 0 and k4 == 0 and k5 == 0
     norm = op in (OP_RMSNORM, OP_RES_RMSNORM, OP_CHAIN)
     sw = op in (OP_SWIGLU, OP_CHAIN)
     if (not (1 <= f["H"] < H_LIMIT)) if norm else f["H"] != 0:
@@ -522,6 +608,12 @@ def plan(key, T: int):
         return v, (0, 0, 0), [(v, g, BLOCK)]
     if op == OP_SWIGLU:
         v, g = sw_role(dt, f["I"], fl, b, T)
+        return v, (0, 0, 0), [(v, g, BLOCK)]
+    if op in ELT_OPS:
+        v, g = elt_role(dt, f["H"], fl, b, T)
+        return v, (0, 0, 0), [(v, g, BLOCK)]
+    if op == OP_EMBEDDING:
+        v, g = emb_role(dt, f["H"], fl, T)
         return v, (0, 0, 0), [(v, g, BLOCK)]
     rn = rn_role(dt, f["H"], fl & 3, T)
     ro = rope_role(dt, f["hd"], (fl >> 2) & 3, T, bool(fl & CHAIN_QK_NORM), f["rd"], inter)

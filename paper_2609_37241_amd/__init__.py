@@ -224,6 +224,48 @@ class SpecCache:
                    _rows(o, "out"), T, I, _stream_ptr(stream))
         return o
 
+    # ---- short ops ---------------------------------------------------------------
+    def silu(self, x, out=None, stream=None) -> torch.Tensor:
+        """out = x / (1 + exp(-x)) over [T, W]."""
+        o = torch.empty_like(x) if out is None else out
+        T, W = x.shape
+        self._call("tri_silu", _dll.tri_silu, dtype_code(x.dtype), x.data_ptr(), _rows(x, "x"),
+                   o.data_ptr(), _rows(o, "out"), T, W, _stream_ptr(stream))
+        return o
+
+    def add(self, a, b, out=None, stream=None) -> torch.Tensor:
+        """out = a + b over [T, W] (one rounding)."""
+        o = torch.empty_like(a) if out is None else out
+        T, W = a.shape
+        self._call("tri_add", _dll.tri_add, dtype_code(a.dtype), a.data_ptr(), _rows(a, "a"),
+                   b.data_ptr(), _rows(b, "b"), o.data_ptr(), _rows(o, "out"), T, W,
+                   _stream_ptr(stream))
+        return o
+
+    def masked_fill(self, x, mask, value: float, out=None, stream=None) -> torch.Tensor:
+        """out = where(mask, value, x); mask is uint8 (or bool) [T, W]."""
+        if mask.dtype not in (torch.uint8, torch.bool):
+            raise TypeError("mask must be uint8 or bool")
+        o = torch.empty_like(x) if out is None else out
+        T, W = x.shape
+        self._call("tri_masked_fill", _dll.tri_masked_fill, dtype_code(x.dtype), x.data_ptr(),
+                   _rows(x, "x"), mask.data_ptr(), _rows(mask, "mask"), value, o.data_ptr(),
+                   _rows(o, "out"), T, W, _stream_ptr(stream))
+        return o
+
+    def embedding(self, table, ids, out=None, stream=None) -> torch.Tensor:
+        """out[t] = table[ids[t]] (zeros for ids out of range); ids int32 / int64."""
+        if ids.dtype not in (torch.int32, torch.int64) or ids.dim() != 1:
+            raise TypeError("ids must be a 1-D int32 or int64 tensor")
+        n_rows, H = table.shape
+        T = ids.shape[0]
+        o = torch.empty((T, H), dtype=table.dtype, device=table.device) if out is None else out
+        self._call("tri_embedding", _dll.tri_embedding, dtype_code(table.dtype),
+                   table.data_ptr(), _rows(table, "table"), n_rows, ids.data_ptr(),
+                   int(ids.dtype == torch.int64), o.data_ptr(), _rows(o, "out"), T, H,
+                   _stream_ptr(stream))
+        return o
+
     def chain_args(self, x, residual, w, q, k, pos, gate, up, eps=1e-6, base=10000.0,
                    y=None, residual_out=None, out=None, q_norm_w=None, k_norm_w=None,
                    qk_eps=None, rope: Optional[RopeExt] = None) -> Tuple[ChainArgs, tuple]:

@@ -18,6 +18,7 @@ E_INVALID, E_UNSUPPORTED, E_FULL, E_NOMEM, E_LAUNCH, E_RUNTIME = -1, -2, -3, -4,
 F32, BF16 = 0, 1
 OP_RMSNORM, OP_RES_RMSNORM, OP_ROPE_QK, OP_SWIGLU, OP_CHAIN, OP_QK_NORM_ROPE = 1, 2, 3, 4, 5, 6
 OP_CHAIN_LAYERS = 7
+OP_SILU, OP_ADD, OP_MASKED_FILL, OP_EMBEDDING = 8, 9, 10, 11
 MAX_LAYERS = 1024
 AUTO_INSTALL = 1
 JIT = 2
@@ -102,6 +103,12 @@ SIGNATURES = {
     "tri_qk_norm_rope": (C.c_int, [_P, C.c_int, _P, _I64, _P, _I64, _P, _I64, _I32, _I32, _I32,
                                    _F, _P, _P, _F, _P]),
     "tri_swiglu": (C.c_int, [_P, C.c_int, _P, _I64, _P, _I64, _P, _I64, _I64, _I64, _P]),
+    "tri_silu": (C.c_int, [_P, C.c_int, _P, _I64, _P, _I64, _I64, _I64, _P]),
+    "tri_add": (C.c_int, [_P, C.c_int, _P, _I64, _P, _I64, _P, _I64, _I64, _I64, _P]),
+    "tri_masked_fill": (C.c_int, [_P, C.c_int, _P, _I64, _P, _I64, _F, _P, _I64, _I64, _I64,
+                                  _P]),
+    "tri_embedding": (C.c_int, [_P, C.c_int, _P, _I64, _I64, _P, _I32, _P, _I64, _I64, _I64,
+                                _P]),
     "tri_decode_chain": (C.c_int, [_P, C.POINTER(ChainArgs), _P]),
     "tri_decode_chain_layers": (C.c_int, [_P, C.POINTER(ChainArgs), _U32, _P]),
     "tri_spec_install_last_miss": (C.c_int, [_P, C.POINTER(Selection)]),

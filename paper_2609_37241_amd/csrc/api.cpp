@@ -341,6 +341,64 @@ int chain_launch(const Version &v, const tri_chain_args &p, void *stream, tri_la
   return rc;
 }
 
+// Element-wise ops: W range, non-null element-aligned operands (the mask is
+// bytes), strides >= W.
+inline int check_elt(uint64_t es, int64_t W, const void *a, int64_t a_rs, const void *b,
+                     int64_t b_rs, bool b_is_mask, const void *o, int64_t o_rs) {
+  if (W < 1) return TRI_E_INVALID;
+  if (W >= kILimit) return TRI_E_UNSUPPORTED;
+  if (!a || !b || !o) return TRI_E_INVALID;
+  if (addr(a) % es || addr(o) % es || (!b_is_mask && addr(b) % es)) return TRI_E_INVALID;
+  if (a_rs < W || b_rs < W || o_rs < W) return TRI_E_INVALID;
+  return kGo;
+}
+
+// One launch of a single-kernel op: lookup (miss / auto-install), launch
+// with the argument block, record, count.
+tri_status single_launch(tri_cache *c, uint32_t op, const Key &k, int64_t T, int64_t width,
+                         const void *args, uint32_t args_size, void *stream) {
+  int32_t vi;
+  bool auto_inst = false;
+  const int st = lookup(c, op, k, T, &vi, &auto_inst);
+  if (st != TRI_OK) return tri_status(st);
+  Version &v = c->versions[vi];
+  const tri_launch_rec l{v.plan.kvariant[0],
+                         role_grid(v.plan.kvariant[0], key_dtype(k), T, width), kBlock};
+  const int rc = be_launch(v.fn[0], l.grid_x, kBlock, args, args_size, stream);
+  record(c, op, v, vi, k, 1, &l, rc ? TRI_E_LAUNCH : TRI_OK);
+  return finish(c, v, auto_inst, rc);
+}
+
+// silu (b unused: pass a), add, masked_fill (b = mask).
+tri_status elt_entry(tri_cache *c, uint32_t op, int32_t dtype, const void *a, int64_t a_rs,
+                     const void *b, int64_t b_rs, void *out, int64_t o_rs, int64_t T, int64_t W,
+                     float value, void *stream) {
+  if (!c) return TRI_E_INVALID;
+  c->stats.calls++;
+  int st = check_common(dtype, T);
+  if (st != kGo) return finish_early(c, op, st);
+  const uint64_t es = es_of(uint32_t(dtype));
+  const bool mask = op == TRI_OP_MASKED_FILL;
+  st = check_elt(es, W, a, a_rs, b, b_rs, mask, out, o_rs);
+  if (st != kGo) return finish_early(c, op, st);
+  // alignment: data 16 B; the mask 16 / es bytes (one byte per element of a vector)
+  const uint64_t v = 16 / es;
+  uint64_t o16 = addr(a) | addr(out) | uint64_t(a_rs) * es | uint64_t(o_rs) * es;
+  bool aligned;
+  if (mask) {
+    aligned = (o16 & 15u) == 0 && addr(b) % v == 0 && uint64_t(b_rs) % v == 0;
+  } else {
+    o16 |= addr(b) | uint64_t(b_rs) * es;
+    aligned = (o16 & 15u) == 0;
+  }
+  const bool contig = a_rs == W && b_rs == W && o_rs == W;
+  const unsigned fl = (aligned ? kAlign : 0u) | (contig ? kContig : 0u);
+  const Key k = make_key(op, uint32_t(dtype), T, fl, 0, uint64_t(W), 0, 0, 0, 0);
+  const EltArgs args{a, b, out, a_rs, b_rs, o_rs, T, W, (T * W) / vec_elems(uint32_t(dtype)),
+                     T * W, value, 0};
+  return single_launch(c, op, k, T, W, &args, sizeof args, stream);
+}
+
 // RoPE (op 3) or QK-RMSNorm + RoPE (op 6; the head-norm weights are then
 // required) with an optional variant.
 tri_status rope_entry(tri_cache *c, uint32_t op, int32_t dtype, void *q, int64_t q_ts, void *kp,
@@ -492,6 +550,46 @@ tri_status tri_swiglu(tri_cache *c, tri_dtype dtype, const void *gate, int64_t g
   const int rc = be_launch(v.fn[0], l.grid_x, kBlock, &a, sizeof a, stream);
   record(c, op, v, vi, k, 1, &l, rc ? TRI_E_LAUNCH : TRI_OK);
   return finish(c, v, auto_inst, rc);
+}
+
+tri_status tri_silu(tri_cache *c, tri_dtype dtype, const void *x, int64_t x_rs, void *out,
+                    int64_t o_rs, int64_t T, int64_t W, void *stream) {
+  return elt_entry(c, TRI_OP_SILU, dtype, x, x_rs, x, x_rs, out, o_rs, T, W, 0.0f, stream);
+}
+
+tri_status tri_add(tri_cache *c, tri_dtype dtype, const void *a, int64_t a_rs, const void *b,
+                   int64_t b_rs, void *out, int64_t o_rs, int64_t T, int64_t W, void *stream) {
+  return elt_entry(c, TRI_OP_ADD, dtype, a, a_rs, b, b_rs, out, o_rs, T, W, 0.0f, stream);
+}
+
+tri_status tri_masked_fill(tri_cache *c, tri_dtype dtype, const void *x, int64_t x_rs,
+                           const uint8_t *mask, int64_t m_rs, float value, void *out,
+                           int64_t o_rs, int64_t T, int64_t W, void *stream) {
+  return elt_entry(c, TRI_OP_MASKED_FILL, dtype, x, x_rs, mask, m_rs, out, o_rs, T, W, value,
+                   stream);
+}
+
+tri_status tri_embedding(tri_cache *c, tri_dtype dtype, const void *table, int64_t t_rs,
+                         int64_t n_rows, const void *ids, int32_t ids_int64, void *out,
+                         int64_t o_rs, int64_t T, int64_t H, void *stream) {
+  if (!c) return TRI_E_INVALID;
+  const uint32_t op = TRI_OP_EMBEDDING;
+  c->stats.calls++;
+  int st = check_common(dtype, T);
+  if (st != kGo) return finish_early(c, op, st);
+  const uint64_t es = es_of(uint32_t(dtype));
+  if (H < 1 || n_rows < 1 || (ids_int64 | 1) != 1) return finish_early(c, op, TRI_E_INVALID);
+  if (H >= kILimit) return finish_early(c, op, TRI_E_UNSUPPORTED);
+  if (!table || !ids || !out) return finish_early(c, op, TRI_E_INVALID);
+  if (addr(table) % es || addr(out) % es || addr(ids) % (ids_int64 ? 8 : 4))
+    return finish_early(c, op, TRI_E_INVALID);
+  if (t_rs < H || o_rs < H) return finish_early(c, op, TRI_E_INVALID);
+  const bool aligned =
+      ((addr(table) | addr(out) | uint64_t(t_rs) * es | uint64_t(o_rs) * es) & 15u) == 0;
+  Key k = make_key(op, uint32_t(dtype), T, aligned ? kAlign : 0u, 0, uint64_t(H), 0, 0, 0, 0);
+  k.k3 = uint64_t(ids_int64) << 16;
+  const EmbArgs args{table, ids, out, t_rs, o_rs, T, H, n_rows, ids_int64, 0};
+  return single_launch(c, op, k, T, H, &args, sizeof args, stream);
 }
 
 tri_status tri_decode_chain(tri_cache *c, const tri_chain_args *p, void *stream) {

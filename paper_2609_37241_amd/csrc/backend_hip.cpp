@@ -21,6 +21,8 @@ const void *sw_kernel(int32_t variant, uint32_t dtype);
 const void *chain_kernel_f32(int32_t sub);
 const void *chain_kernel_bf16(int32_t sub);
 const void *empty_kernel();
+const void *elt_kernel(int32_t variant, uint32_t dtype, int32_t op);
+const void *emb_kernel(int32_t variant, uint32_t dtype);
 
 int be_init(int *device) {
   int n = 0;
@@ -39,6 +41,10 @@ int be_resolve(int32_t kvariant, uint32_t dtype, int32_t ksub, void **fn) {
     sym = sw_kernel(kvariant, dtype);
   else if (kvariant == CH_FUSED)
     sym = dtype == TRI_F32 ? chain_kernel_f32(ksub) : chain_kernel_bf16(ksub);
+  else if (kvariant >= ELT_SCALAR && kvariant <= ELT_ROWS)
+    sym = elt_kernel(kvariant, dtype, ksub);
+  else if (kvariant == EMB_SCALAR || kvariant == EMB_VEC)
+    sym = emb_kernel(kvariant, dtype);
   else if (kvariant == EMPTY)
     sym = empty_kernel();
   if (!sym) return TRI_E_RUNTIME;

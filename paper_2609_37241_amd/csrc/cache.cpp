@@ -140,7 +140,9 @@ tri_status install_key(tri_cache *c, const Key &k) {
 void fill_selection(const Version &v, int32_t index, int64_t T, tri_selection *out) {
   const Key &k = v.key;
   const uint32_t dt = key_dtype(k);
-  const int64_t I = key_I(k);
+  // role_grid's width: SwiGLU's I, or the row width of a short op (H field)
+  const uint32_t op = key_op(k);
+  const int64_t I = op >= TRI_OP_SILU && op <= TRI_OP_EMBEDDING ? key_H(k) : key_I(k);
   memset(out, 0, sizeof *out);
   out->op = int32_t(key_op(k));
   out->status = TRI_OK;

@@ -20,6 +20,8 @@ enum Variant : int32_t {
   ROPE_QKN_VEC_I = 35,
   SW_SCALAR = 40, SW_FLAT = 41, SW_FLAT_NT = 42, SW_ROWS = 43, SW_FLAT_U4_NT = 44,
   CH_FUSED = 50, CH_SEQ = 51,
+  ELT_SCALAR = 60, ELT_FLAT = 61, ELT_FLAT_U2 = 62, ELT_ROWS = 63,
+  EMB_SCALAR = 70, EMB_VEC = 71,
   EMPTY = 99,
 };
 
@@ -93,6 +95,9 @@ Role rope_role(uint32_t dtype, int32_t hd, int32_t rd, bool interleaved, unsigne
                bool qk_norm);
 Role sw_role(uint32_t dtype, int64_t I, unsigned flags, uint32_t bucket, int64_t T, bool in_chain);
 uint32_t role_grid(int32_t variant, uint32_t dtype, int64_t T, int64_t I);
+// Element-wise ops (silu, add, masked_fill) over [T, W] and embedding rows.
+Role elt_role(uint32_t dtype, int64_t W, unsigned flags, uint32_t bucket, int64_t T);
+Role emb_role(uint32_t dtype, int64_t H, unsigned flags, int64_t T);
 
 // A version's plan: which kernels it launches, fixed at install.
 struct Plan {
@@ -138,7 +143,7 @@ struct Version {
   uint64_t hits;
 };
 
-constexpr int kOps = 8;   // op ids 1..7
+constexpr int kOps = 12;   // op ids 1..11
 
 }  // namespace tri
 

@@ -58,6 +58,31 @@ struct SwArgs {
   int64_t n;              // flat variants: T*I elements
 };
 
+// Element-wise ops over [T, W]: silu(a), a + b, or masked_fill(a, mask b,
+// value). Flat variants use nvec whole 16-byte vectors of the contiguous
+// T*W elements and n = T*W.
+struct EltArgs {
+  const void *a;
+  const void *b;          // second operand, or the uint8 mask
+  void *out;
+  int64_t a_rs, b_rs, o_rs;
+  int64_t T, W;
+  int64_t nvec, n;
+  float value;            // masked_fill: fill value (rounded to the dtype on the device)
+  int32_t pad;
+};
+
+// Embedding: out[t, :] = table[ids[t], :], zeros for ids outside [0, n_rows).
+struct EmbArgs {
+  const void *table;
+  const void *ids;        // int32 or int64 [T]
+  void *out;
+  int64_t t_rs, o_rs;
+  int64_t T, H, n_rows;
+  int32_t ids64;
+  int32_t pad;
+};
+
 // The fused decode chain: rn_blocks workgroups run residual RMSNorm rows,
 // rope_blocks run RoPE tokens, the remaining gridDim.x - rn_blocks -
 // rope_blocks run SwiGLU (the kernel fixes the order of the three ranges).
@@ -76,6 +101,8 @@ static_assert(sizeof(RopeArgs) == 112 && __builtin_offsetof(RopeArgs, nq) == 88 
                   __builtin_offsetof(RopeArgs, mode) == 108,
               "RopeArgs layout");
 static_assert(sizeof(SwArgs) == 80 && __builtin_offsetof(SwArgs, n) == 72, "SwArgs layout");
+static_assert(sizeof(EltArgs) == 88 && __builtin_offsetof(EltArgs, value) == 80, "EltArgs layout");
+static_assert(sizeof(EmbArgs) == 72 && __builtin_offsetof(EmbArgs, ids64) == 64, "EmbArgs layout");
 static_assert(sizeof(ChainArgs) == 288 && __builtin_offsetof(ChainArgs, rn_blocks) == 280,
               "ChainArgs layout");
 

@@ -626,10 +626,18 @@ __device__ __forceinline__ void rope_scalar_block(const RopeArgs &a, int64_t t, 
 }
 
 // ---- SwiGLU ----------------------------------------------------------------------
-// silu(g) * u = g / (1 + exp(-g)) * u; for g << 0 exp overflows to +inf and
-// the quotient is a signed zero.
+// silu(g) = g / (1 + exp(-g)), evaluated as g * rcp(1 + exp(-g)) with the
+// hardware reciprocal (v_rcp_f32, 1 ulp): the correctly rounded float32
+// division costs about ten vector instructions per element, which made the
+// streaming SwiGLU and silu kernels bound by vector ALU throughput rather
+// than by HBM. For g << 0 exp overflows to +inf, rcp gives +0 and the result
+// is a signed zero.
+__device__ __forceinline__ float silu(float g) {
+  return g * __builtin_amdgcn_rcpf(1.0f + expf(-g));
+}
+
 __device__ __forceinline__ float silu_mul(float g, float u) {
-  return g / (1.0f + expf(-g)) * u;
+  return silu(g) * u;
 }
 
 // Flat contiguous [T*I]: workgroup `blk` of `nblk` handles U vectors per
@@ -712,6 +720,192 @@ __device__ __forceinline__ void sw_scalar_part(const SwArgs &a, int64_t blk, int
   }
 }
 
+// ---- element-wise ops (silu, add, masked_fill) and embedding -------------------------
+constexpr int kOpSilu = 8, kOpAdd = 9, kOpMaskedFill = 10;   // the ABI's op ids
+
+// One element of an element-wise op on float values (masked_fill works on
+// bit patterns instead, see below).
+template <int OP>
+__device__ __forceinline__ float elt_value(float a, float b) {
+  if constexpr (OP == kOpAdd)
+    return a + b;
+  else
+    return silu(a);
+}
+
+// masked_fill on one 16-byte vector: element e takes `fill` (the fill
+// value's bit pattern) where mask byte e is nonzero, else keeps its bits.
+template <int DT>
+__device__ __forceinline__ u32x4 mask_select(u32x4 x, uint64_t m, uint32_t fill) {
+  u32x4 o;
+  if constexpr (DT == kF32) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o[e] = ((m >> (8 * e)) & 0xFF) ? fill : x[e];
+  } else {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t lo = ((m >> (16 * j)) & 0xFF) ? fill : (x[j] & 0xFFFFu);
+      const uint32_t hi = ((m >> (16 * j + 8)) & 0xFF) ? fill : (x[j] >> 16);
+      o[j] = lo | (hi << 16);
+    }
+  }
+  return o;
+}
+
+template <int DT>
+__device__ __forceinline__ uint32_t fill_bits(float value) {
+  if constexpr (DT == kF32)
+    return __float_as_uint(value);
+  else
+    return Elt<kBF16>::pack2(value, 0.0f) & 0xFFFFu;   // round to nearest even
+}
+
+// The V mask bytes of vector vi of a row starting at `m` (aligned to V).
+template <int DT>
+__device__ __forceinline__ uint64_t mask_bytes(const uint8_t *m, int64_t vi) {
+  if constexpr (DT == kF32)
+    return reinterpret_cast<const uint32_t *>(m)[vi];
+  else
+    return reinterpret_cast<const uint64_t *>(m)[vi];
+}
+
+template <int DT, int OP>
+__device__ __forceinline__ u32x4 elt_vector(u32x4 x, const void *b, int64_t vi,
+                                            const uint8_t *mrow, uint32_t fill, bool nt) {
+  using E = Elt<DT>;
+  constexpr int V = E::V;
+  if constexpr (OP == kOpMaskedFill) {
+    return mask_select<DT>(x, mask_bytes<DT>(mrow, vi), fill);
+  } else {
+    float fa[V], fb[V];
+    E::unpack(x, fa);
+    if constexpr (OP == kOpAdd) {
+      const u32x4 y = nt ? ld16<true>(static_cast<const u32x4 *>(b) + vi)
+                         : ld16<false>(static_cast<const u32x4 *>(b) + vi);
+      E::unpack(y, fb);
+    }
+#pragma unroll
+    for (int e = 0; e < V; ++e) fa[e] = elt_value<OP>(fa[e], OP == kOpAdd ? fb[e] : 0.0f);
+    return E::pack(fa);
+  }
+}
+
+// Flat contiguous [T*W]: U vectors per work-item per step (all loads
+// issued before any use); workgroup 0 also does the < V element tail.
+template <int DT, int OP, bool NT, int U = 1>
+__device__ __forceinline__ void elt_flat_part(const EltArgs &a, int64_t blk, int64_t nblk) {
+  using E = Elt<DT>;
+  constexpr int V = E::V;
+  const u32x4 *x = static_cast<const u32x4 *>(a.a);
+  u32x4 *o = static_cast<u32x4 *>(a.out);
+  const uint8_t *m = static_cast<const uint8_t *>(a.b);
+  const uint32_t fill = fill_bits<DT>(a.value);
+  const int64_t step = nblk * kThreads * U;
+  for (int64_t base = blk * kThreads * U + threadIdx.x; base < a.nvec; base += step) {
+    u32x4 xv[U];
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      const int64_t i = base + int64_t(k) * kThreads;
+      if (i < a.nvec) xv[k] = ld16<NT>(x + i);
+    }
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      const int64_t i = base + int64_t(k) * kThreads;
+      if (i < a.nvec) st16<NT>(o + i, elt_vector<DT, OP>(xv[k], a.b, i, m, fill, NT));
+    }
+  }
+  if (blk == 0) {
+    const int64_t i = a.nvec * V + threadIdx.x;
+    if (i < a.n) {
+      if constexpr (OP == kOpMaskedFill) {
+        if (m[i]) E::st(a.out, i, a.value);   // st rounds to the dtype
+        else E::st(a.out, i, E::ld(a.a, i));
+      } else {
+        E::st(a.out, i, elt_value<OP>(E::ld(a.a, i), OP == kOpAdd ? E::ld(a.b, i) : 0.0f));
+      }
+    }
+  }
+}
+
+// Aligned rows with padded strides: (row, 256-vector chunk) items.
+template <int DT, int OP>
+__device__ __forceinline__ void elt_rows_part(const EltArgs &a, int64_t blk, int64_t nblk) {
+  using E = Elt<DT>;
+  constexpr int V = E::V;
+  const int64_t nvr = a.W / V;
+  const int64_t cb = (nvr + kThreads - 1) / kThreads;
+  const uint32_t fill = fill_bits<DT>(a.value);
+  for (int64_t it = blk; it < a.T * cb; it += nblk) {
+    const int64_t row = it / cb;
+    const int64_t vi = (it - row * cb) * kThreads + threadIdx.x;
+    if (vi < nvr) {
+      const u32x4 *x = reinterpret_cast<const u32x4 *>(static_cast<const char *>(a.a) +
+                                                       row * a.a_rs * E::ES);
+      const char *brow = static_cast<const char *>(a.b) +
+                         row * a.b_rs * (OP == kOpMaskedFill ? 1 : E::ES);
+      u32x4 *o = reinterpret_cast<u32x4 *>(static_cast<char *>(a.out) + row * a.o_rs * E::ES);
+      o[vi] = elt_vector<DT, OP>(x[vi], brow, vi, reinterpret_cast<const uint8_t *>(brow), fill,
+                                 false);
+    }
+  }
+}
+
+// Any alignment: element-wise over T*W (masked_fill copies bit patterns).
+template <int DT, int OP>
+__device__ __forceinline__ void elt_scalar_part(const EltArgs &a, int64_t blk, int64_t nblk) {
+  using E = Elt<DT>;
+  const int64_t n = a.T * a.W;
+  for (int64_t e = blk * kThreads + threadIdx.x; e < n; e += nblk * kThreads) {
+    const int64_t row = e / a.W;
+    const int64_t j = e - row * a.W;
+    if constexpr (OP == kOpMaskedFill) {
+      const bool set = static_cast<const uint8_t *>(a.b)[row * a.b_rs + j] != 0;
+      if constexpr (DT == kF32) {
+        const uint32_t x = static_cast<const uint32_t *>(a.a)[row * a.a_rs + j];
+        static_cast<uint32_t *>(a.out)[row * a.o_rs + j] = set ? fill_bits<DT>(a.value) : x;
+      } else {
+        const uint16_t x = static_cast<const uint16_t *>(a.a)[row * a.a_rs + j];
+        static_cast<uint16_t *>(a.out)[row * a.o_rs + j] =
+            set ? uint16_t(fill_bits<DT>(a.value)) : x;
+      }
+    } else {
+      const float r = elt_value<OP>(E::ld(a.a, row * a.a_rs + j),
+                                    OP == kOpAdd ? E::ld(a.b, row * a.b_rs + j) : 0.0f);
+      E::st(a.out, row * a.o_rs + j, r);
+    }
+  }
+}
+
+// Embedding: workgroup b copies output rows b, b + gridDim.x, ...; the row
+// is table row ids[t] when it is in [0, n_rows), zeros otherwise.
+template <int DT, bool VEC>
+__device__ __forceinline__ void emb_rows(const EmbArgs &a) {
+  using E = Elt<DT>;
+  constexpr int V = E::V;
+  for (int64_t t = blockIdx.x; t < a.T; t += gridDim.x) {
+    const int64_t id = a.ids64 ? static_cast<const int64_t *>(a.ids)[t]
+                               : int64_t(static_cast<const int32_t *>(a.ids)[t]);
+    const bool ok = id >= 0 && id < a.n_rows;
+    const char *src = static_cast<const char *>(a.table) + (ok ? id : 0) * a.t_rs * E::ES;
+    char *dst = static_cast<char *>(a.out) + t * a.o_rs * E::ES;
+    if constexpr (VEC) {
+      const int64_t nvr = a.H / V;
+      for (int64_t vi = threadIdx.x; vi < nvr; vi += kThreads) {
+        u32x4 v = {0u, 0u, 0u, 0u};
+        if (ok) v = reinterpret_cast<const u32x4 *>(src)[vi];
+        reinterpret_cast<u32x4 *>(dst)[vi] = v;
+      }
+    } else {
+      for (int64_t j = threadIdx.x; j < a.H; j += kThreads) {
+        if constexpr (DT == kF32)
+          reinterpret_cast<uint32_t *>(dst)[j] = ok ? reinterpret_cast<const uint32_t *>(src)[j] : 0u;
+        else
+          reinterpret_cast<uint16_t *>(dst)[j] = ok ? reinterpret_cast<const uint16_t *>(src)[j] : 0;
+      }
+    }
+  }
+}
+
 // ---- kernel bodies -----------------------------------------------------------------
 // One body per kernel family, called by the precompiled kernels and by the
 // runtime-compiled specializations; a specialization passes arguments whose
@@ -765,6 +959,27 @@ __device__ __forceinline__ void body_sw_rows(const SwArgs &a) {
 template <int DT>
 __device__ __forceinline__ void body_sw_scalar(const SwArgs &a) {
   sw_scalar_part<DT>(a, blockIdx.x, gridDim.x);
+}
+
+// U vectors per work-item, cached loads and stores.
+template <int DT, int OP, int U>
+__device__ __forceinline__ void body_elt_flat(const EltArgs &a) {
+  elt_flat_part<DT, OP, false, U>(a, blockIdx.x, gridDim.x);
+}
+
+template <int DT, int OP>
+__device__ __forceinline__ void body_elt_rows(const EltArgs &a) {
+  elt_rows_part<DT, OP>(a, blockIdx.x, gridDim.x);
+}
+
+template <int DT, int OP>
+__device__ __forceinline__ void body_elt_scalar(const EltArgs &a) {
+  elt_scalar_part<DT, OP>(a, blockIdx.x, gridDim.x);
+}
+
+template <int DT, bool VEC>
+__device__ __forceinline__ void body_emb(const EmbArgs &a) {
+  emb_rows<DT, VEC>(a);
 }
 
 // The fused decode chain: workgroups take the residual-RMSNorm, RoPE-QK and

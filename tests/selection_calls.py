@@ -86,3 +86,35 @@ def chain_call(dtype, T, H, I, nq, nk, hd, *, base=10000.0, eps=1e-6,
 def elem_offset(dtype, n=1):
     """Byte offset of n elements (used to build unaligned layouts)."""
     return n * S.elem_size(dtype)
+
+
+def silu_call(dtype, T, W, *, off=0, pad=0, null=()):
+    ptr = {"a": _addr(30) + off, "b": _addr(30) + off, "out": _addr(32) + off}
+    for n in null:
+        ptr[n] = None
+    if "a" in null:
+        ptr["b"] = None
+    return S.Call(S.OP_SILU, dtype, T, H=W, ptr=ptr, stride={n: W + pad for n in ("a", "b", "out")})
+
+
+def add_call(dtype, T, W, *, off=0, b_off=0, pad=0, null=()):
+    ptr = {"a": _addr(30) + off, "b": _addr(31) + off + b_off, "out": _addr(32) + off}
+    for n in null:
+        ptr[n] = None
+    return S.Call(S.OP_ADD, dtype, T, H=W, ptr=ptr, stride={n: W + pad for n in ("a", "b", "out")})
+
+
+def mf_call(dtype, T, W, *, off=0, m_off=0, pad=0, m_pad=0, value=-1e4, null=()):
+    ptr = {"a": _addr(30) + off, "b": _addr(33) + m_off, "out": _addr(32) + off}
+    for n in null:
+        ptr[n] = None
+    return S.Call(S.OP_MASKED_FILL, dtype, T, H=W, value=value, ptr=ptr,
+                  stride={"a": W + pad, "b": W + m_pad, "out": W + pad})
+
+
+def emb_call(dtype, T, H, n_rows, *, ids64=0, off=0, pad=0, ids_off=0, null=()):
+    ptr = {"table": _addr(34) + off, "ids": _addr(35) + ids_off, "out": _addr(36) + off}
+    for n in null:
+        ptr[n] = None
+    return S.Call(S.OP_EMBEDDING, dtype, T, H=H, n_rows=n_rows, ids64=ids64, ptr=ptr,
+                  stride={"table": H + pad, "out": H + pad})

@@ -71,6 +71,9 @@ OP_CASES = [
     ("residual", nm.BF16, 130, 4096, "plain"), ("residual", nm.F32, 6, 256, "strided"),
     ("swiglu", nm.BF16, 8, 14336, "plain"), ("swiglu", nm.F32, 130, 1000, "plain"),
     ("swiglu", nm.BF16, 5, 11008, "strided"), ("swiglu", nm.F32, 5, 1001, "unaligned"),
+    ("silu", nm.BF16, 130, 4096, "plain"), ("add", nm.F32, 7, 1001, "unaligned"),
+    ("masked_fill", nm.BF16, 9, 4096, "strided"), ("embedding", nm.BF16, 9, 4096, "plain"),
+    ("embedding", nm.F32, 9, 1001, "plain"),
 ]
 
 
@@ -93,6 +96,16 @@ def test_jit_ops_equal_precompiled_bitwise(tri, op, dtype, T, W, layout):
                 ro = empty_like_layout(xd)
                 cache.residual_rmsnorm(xd, x2d, wd, 1e-6, out=y, residual_out=ro)
                 outs.append((y, ro))
+            elif op == "silu":
+                outs.append((cache.silu(xd, out=y),))
+            elif op == "add":
+                outs.append((cache.add(xd, x2d, out=y),))
+            elif op == "masked_fill":
+                m = torch.from_numpy((np.arange(T * W) % 3 == 0).astype(np.uint8).reshape(T, W))
+                outs.append((cache.masked_fill(xd, m.to(DEV), -5.5, out=y),))
+            elif op == "embedding":
+                ids = torch.arange(T, dtype=torch.int32, device=DEV) * 3 - 2
+                outs.append((cache.embedding(xd, ids),))
             else:
                 cache.swiglu(xd, x2d, out=y)
                 outs.append((y,))

@@ -386,6 +386,70 @@ def test_rope_variant_cases(tri, cache, dtype, T, nq, nk, hd, ext, qkn, layout):
         check("q tail", host(qd)[..., rd:], q[..., rd:], dtype, exact=True)
 
 
+# ---- short ops: silu, add, masked_fill, embedding -------------------------------------------
+SHORT_CASES = [
+    # op, dtype, T, W, layout
+    ("silu", nm.BF16, 1, 11008, "plain"), ("silu", nm.F32, 130, 1000, "plain"),
+    ("silu", nm.BF16, 5, 11008, "strided"), ("silu", nm.F32, 5, 1001, "unaligned"),
+    ("silu", nm.BF16, 3, 1001, "plain"),
+    ("add", nm.BF16, 1, 4096, "plain"), ("add", nm.F32, 100, 4096, "plain"),
+    ("add", nm.BF16, 7, 4096, "strided"), ("add", nm.BF16, 7, 1003, "unaligned"),
+    ("add", nm.F32, 3, 1001, "plain"),
+    ("masked_fill", nm.BF16, 1, 4096, "plain"), ("masked_fill", nm.F32, 130, 1000, "plain"),
+    ("masked_fill", nm.BF16, 9, 4096, "strided"), ("masked_fill", nm.F32, 9, 999, "unaligned"),
+    ("masked_fill", nm.BF16, 3, 1001, "plain"),
+]
+
+
+@pytest.mark.parametrize("op,dtype,T,W,layout", SHORT_CASES)
+def test_short_op_variants(tri, cache, op, dtype, T, W, layout):
+    r = rng(T * 17 + W + len(op))
+    a = wl.host_array(r, (T, W), dtype, outliers=True)
+    b = wl.host_array(r, (T, W), dtype)
+    ad, bd = place(a, dtype, layout), place(b, dtype, layout)
+    out = empty_like_layout(ad)
+    if op == "silu":
+        cache.silu(ad, out=out)
+        want = O.silu(a, dtype)
+    elif op == "add":
+        cache.add(ad, bd, out=out)
+        want = O.add(a, b, dtype)
+    else:
+        mask = (r.random((T, W)) < 0.3).astype(np.uint8) * np.uint8(7)
+        md = torch.from_numpy(mask).to(DEV)
+        if layout == "strided":           # padded mask rows too
+            buf = torch.zeros((T, W + 64), dtype=torch.uint8, device=DEV)
+            buf[:, :W] = md
+            md = buf[:, :W]
+        cache.masked_fill(ad, md, float("-inf") if dtype == nm.BF16 else -1e4, out=out)
+        want = O.masked_fill(a, mask, float("-inf") if dtype == nm.BF16 else -1e4, dtype)
+    torch.cuda.synchronize()
+    check(op, host(out), want, dtype, exact=op != "silu")
+
+
+EMB_CASES = [
+    # dtype, T, H, n_rows, int64 ids, layout
+    (nm.BF16, 1, 4096, 32000, False, "plain"), (nm.F32, 9, 4096, 1000, True, "plain"),
+    (nm.BF16, 70, 1001, 50, False, "plain"), (nm.F32, 5, 4096, 10, False, "strided"),
+    (nm.BF16, 6, 4096, 20, True, "unaligned"), (nm.BF16, 300, 128, 7, False, "plain"),
+]
+
+
+@pytest.mark.parametrize("dtype,T,H,n_rows,ids64,layout", EMB_CASES)
+def test_embedding_variants(tri, cache, dtype, T, H, n_rows, ids64, layout):
+    r = rng(T + H + n_rows)
+    table = wl.host_array(r, (n_rows, H), dtype)
+    ids = r.integers(-2, n_rows + 2, size=T)           # some out of range on both sides
+    if ids64:
+        ids[0] = 1 << 40
+    ids = ids.astype(np.int64 if ids64 else np.int32)
+    td = place(table, dtype, layout)
+    out = place(np.zeros((T, H), dtype=table.dtype), dtype, layout)
+    cache.embedding(td, torch.from_numpy(ids).to(DEV), out=out)
+    torch.cuda.synchronize()
+    check("embedding", host(out), O.embedding(table, ids, dtype), dtype, exact=True)
+
+
 # ---- SwiGLU: every variant ---------------------------------------------------------------
 SW_CASES = [
     # dtype, T, I, layout

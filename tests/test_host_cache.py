@@ -15,8 +15,9 @@ import pytest
 from oracle import ops as O
 from oracle import selection as S
 from tests.native_libs import load_fake
-from tests.selection_calls import (CACHE_ADDR, chain_call, elem_offset, qkn_call, res_call,
-                                   rn_call, rope_call, sw_call)
+from tests.selection_calls import (CACHE_ADDR, add_call, chain_call, elem_offset, emb_call,
+                                   mf_call, qkn_call, res_call, rn_call, rope_call, silu_call,
+                                   sw_call)
 import workloads as wl
 
 BF, F = S.DT_BF16, S.DT_F32
@@ -64,6 +65,18 @@ def c_call(lib, cache, c: S.Call, stream=None):
         return lib.tri_qk_norm_rope(cache, c.dtype, p.get("q"), s["q"], p.get("k"), s["k"],
                                     p.get("pos"), c.T, c.nq, c.nk, c.hd, c.base, p.get("q_w"),
                                     p.get("k_w"), c.eps, stream)
+    if c.op == S.OP_SILU:
+        return lib.tri_silu(cache, c.dtype, p.get("a"), s["a"], p.get("out"), s["out"], c.T,
+                            c.H, stream)
+    if c.op == S.OP_ADD:
+        return lib.tri_add(cache, c.dtype, p.get("a"), s["a"], p.get("b"), s["b"], p.get("out"),
+                           s["out"], c.T, c.H, stream)
+    if c.op == S.OP_MASKED_FILL:
+        return lib.tri_masked_fill(cache, c.dtype, p.get("a"), s["a"], p.get("b"), s["b"],
+                                   c.value, p.get("out"), s["out"], c.T, c.H, stream)
+    if c.op == S.OP_EMBEDDING:
+        return lib.tri_embedding(cache, c.dtype, p.get("table"), s["table"], c.n_rows,
+                                 p.get("ids"), c.ids64, p.get("out"), s["out"], c.T, c.H, stream)
     if c.op == S.OP_SWIGLU:
         return lib.tri_swiglu(cache, c.dtype, p.get("gate"), s["gate"], p.get("up"), s["up"],
                               p.get("out"), s["out"], c.T, c.I, stream)
@@ -190,6 +203,20 @@ def call_zoo():
             calls.append(sw_call(d, T, 11008, pad=64))
             calls.append(sw_call(d, T, 11003, pad=1))
             calls.append(chain_call(d, T, 4096, 11008, 32, 32, 128))
+            for W in (4096, 11008, 1001, 8, 1):
+                calls.append(silu_call(d, T, W))
+                calls.append(add_call(d, T, W))
+                calls.append(mf_call(d, T, W))
+                calls.append(emb_call(d, T, W, 32000))
+            calls.append(silu_call(d, T, 4096, pad=64))
+            calls.append(add_call(d, T, 4096, b_off=off))
+            calls.append(add_call(d, T, 4096, off=off))
+            calls.append(mf_call(d, T, 4096, m_off=4))
+            calls.append(mf_call(d, T, 4096, m_off=8, m_pad=8))
+            calls.append(mf_call(d, T, 4096, m_pad=3))
+            calls.append(emb_call(d, T, 4096, 128256, ids64=1))
+            calls.append(emb_call(d, T, 4096, 5, pad=64))
+            calls.append(emb_call(d, T, 4096, 5, off=off))
             calls.append(chain_call(d, T, 8192, 28672, 64, 8, 128, base=500000.0))
             calls.append(chain_call(d, T, 256, 688, 4, 4, 64))
             calls.append(chain_call(d, T, 4096, 14336, 32, 8, 128, sw_pad=64))
@@ -252,6 +279,18 @@ def call_zoo():
               qkn_call(BF, 1, 4, 4, 64, null=("k_w",), ext=dict(interleaved=1)),
               chain_call(BF, 1, 4096, 11008, 32, 32, 128, ext=dict(rotary_dim=130)),
               chain_call(BF, 1, 4096, 11008, 32, 32, 128, ext=dict(LLAMA3, factor=-8.0)),
+              silu_call(BF, 1, 0), silu_call(BF, 1, S.I_LIMIT), silu_call(BF, 1, 64, null=("a",)),
+              silu_call(BF, 1, 64, off=1), silu_call(BF, 3, 64, pad=-1),
+              add_call(BF, 1, 64, null=("b",)), add_call(BF, 1, 64, b_off=1),
+              add_call(F, 1, 64, null=("out",)), add_call(F, 2, 64, pad=-1),
+              mf_call(BF, 1, 64, null=("b",)), mf_call(BF, 1, 64, m_off=1),
+              mf_call(BF, 2, 64, m_pad=-1), mf_call(BF, 1, 64, off=1),
+              mf_call(F, 1, 64, value=float("nan")), mf_call(F, 1, 64, value=float("inf")),
+              emb_call(BF, 1, 0, 10), emb_call(BF, 1, 64, 0), emb_call(BF, 1, 64, 10, ids64=2),
+              emb_call(BF, 1, S.I_LIMIT, 10), emb_call(BF, 1, 64, 10, null=("ids",)),
+              emb_call(BF, 1, 64, 10, ids_off=2), emb_call(BF, 1, 64, 10, ids64=1, ids_off=4),
+              emb_call(BF, 1, 64, 10, off=1), emb_call(BF, 2, 64, 10, pad=-1),
+              emb_call(F, 0, 64, 0),
               sw_call(BF, 1, 0), sw_call(BF, 1, S.I_LIMIT), sw_call(BF, 1, 64, null=("up",)),
               sw_call(BF, 1, 64, off=1), sw_call(BF, 3, 64, pad=-1)]
     return calls
