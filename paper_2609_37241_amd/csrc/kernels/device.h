@@ -384,10 +384,10 @@ __device__ __forceinline__ char *rope_head(const RopeArgs &a, int64_t t, int h, 
 // QKN (requires rd == hd): each head is first RMS-normalised over its hd
 // elements with the Q or K head-norm weight. The cpb work-items of a head
 // hold the whole head in registers, so the sum of squares is a reduction
-// over cpb adjacent lanes and the head is read and written once. Every item
-// of a batch is then computed (clamped items on valid data) so that all
-// lanes of a group take part in the reduction; only stores are guarded.
-// cpb <= 64 (the policy guarantees it).
+// over cpb adjacent lanes and the head is read and written once. Whether an
+// item is valid depends only on the work-item's head group, so the lanes of
+// a group skip or process an item together and every lane a reduction reads
+// from is active. cpb <= 64 (the policy guarantees it).
 template <int DT, int TPB, bool NT, int PF = 4, bool QKN = false, bool INTER = false>
 __device__ __forceinline__ void rope_vec_block(const RopeArgs &a, int64_t blk, float *lds) {
   using E = Elt<DT>;
@@ -486,9 +486,7 @@ __device__ __forceinline__ void rope_vec_block(const RopeArgs &a, int64_t blk, f
   for (;;) {
 #pragma unroll
     for (int j = 0; j < PF; ++j) {
-      if constexpr (!QKN) {
-        if (!ok[j]) continue;
-      }
+      if (!ok[j]) continue;   // uniform over the lanes of a head group
       float f1[V], f2[V];
       E::unpack(x1[j], f1);
       if constexpr (!INTER) E::unpack(x2[j], f2);
@@ -524,7 +522,6 @@ __device__ __forceinline__ void rope_vec_block(const RopeArgs &a, int64_t blk, f
           o[e] = rot_a(f1[e], f1[e + 1], c, s);
           o[e + 1] = rot_b(f1[e], f1[e + 1], c, s);
         }
-        if (QKN && !ok[j]) continue;
         st16<NT>(reinterpret_cast<u32x4 *>(b) + chunk, E::pack(o));
       } else {
         const int base = it[j] * P2 + chunk * V;
@@ -535,7 +532,6 @@ __device__ __forceinline__ void rope_vec_block(const RopeArgs &a, int64_t blk, f
           o1[e] = rot_a(f1[e], f2[e], c, s);
           o2[e] = rot_b(f1[e], f2[e], c, s);
         }
-        if (QKN && !ok[j]) continue;
         st16<NT>(reinterpret_cast<u32x4 *>(b) + chunk, E::pack(o1));
         st16<NT>(reinterpret_cast<u32x4 *>(b + off2) + chunk, E::pack(o2));
       }
