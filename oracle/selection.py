@@ -162,6 +162,18 @@ def rope_role(dtype: int, hd: int, flags: int, T: int, qk_norm: bool = False,
     return (ROPE_QKN_VEC if qk_norm else ROPE_VEC), T
 
 
+def rope_slices(dtype: int, rd: int, interleaved: bool, n_heads: int, b: int,
+                variant: int) -> int:
+    """Workgroups per token of a vector RoPE role at decode sizes: the heads'
+    work-item groups (n_heads * cpb lanes) over 256-wide workgroups, at most
+    4; one otherwise."""
+    if variant not in ROPE_VEC_ROLES or b > DECODE_BUCKET_MAX:
+        return 1
+    v = 16 // elem_size(dtype)
+    cpb = (rd if interleaved else rd // 2) // v
+    return max(1, min(4, cdiv(n_heads * cpb, BLOCK)))
+
+
 def sw_role(dtype: int, I: int, flags: int, b: int, T: int,
             in_chain: bool = False) -> Tuple[int, int]:
     v = 16 // elem_size(dtype)
@@ -603,8 +615,10 @@ def plan(key, T: int):
         v, g = rn_role(dt, f["H"], fl, T)
         return v, (0, 0, 0), [(v, g, BLOCK)]
     inter = bool(f["rope_bits"] & ROPE_INTERLEAVED)
+    nh = f["nq"] + f["nk"]
     if op in (OP_ROPE_QK, OP_QK_NORM_ROPE):
         v, g = rope_role(dt, f["hd"], fl, T, op == OP_QK_NORM_ROPE, f["rd"], inter)
+        g *= rope_slices(dt, f["rd"], inter, nh, b, v)
         return v, (0, 0, 0), [(v, g, BLOCK)]
     if op == OP_SWIGLU:
         v, g = sw_role(dt, f["I"], fl, b, T)
@@ -617,6 +631,7 @@ def plan(key, T: int):
         return v, (0, 0, 0), [(v, g, BLOCK)]
     rn = rn_role(dt, f["H"], fl & 3, T)
     ro = rope_role(dt, f["hd"], (fl >> 2) & 3, T, bool(fl & CHAIN_QK_NORM), f["rd"], inter)
+    ro = (ro[0], ro[1] * rope_slices(dt, f["rd"], inter, nh, b, ro[0]))
     sw = sw_role(dt, f["I"], (fl >> 4) & 3, b, T, in_chain=True)
     roles = (rn[0], ro[0], sw[0])
     fused = ((fl & 0x3F) == 0x3F

@@ -151,12 +151,14 @@ void fill_selection(const Version &v, int32_t index, int64_t T, tri_selection *o
   out->n_launches = v.plan.n_launches;
   for (int i = 0; i < 3; ++i) out->roles[i] = v.plan.roles[i];
   if (v.plan.variant == CH_FUSED) {
-    const uint32_t g = role_grid(v.plan.roles[0], dt, T, I) + role_grid(v.plan.roles[1], dt, T, I) +
+    const uint32_t g = role_grid(v.plan.roles[0], dt, T, I) +
+                       role_grid(v.plan.roles[1], dt, T, I, v.plan.rope_slices) +
                        role_grid(v.plan.roles[2], dt, T, I);
     out->launch[0] = {CH_FUSED, g, kBlock};
   } else {
     for (int i = 0; i < v.plan.n_launches; ++i)
-      out->launch[i] = {v.plan.kvariant[i], role_grid(v.plan.kvariant[i], dt, T, I), kBlock};
+      out->launch[i] = {v.plan.kvariant[i],
+                        role_grid(v.plan.kvariant[i], dt, T, I, v.plan.rope_slices), kBlock};
   }
   key_words(k, out->key);
 }

@@ -94,7 +94,17 @@ Role rn_role(uint32_t dtype, int64_t H, unsigned flags, int64_t T);
 Role rope_role(uint32_t dtype, int32_t hd, int32_t rd, bool interleaved, unsigned flags, int64_t T,
                bool qk_norm);
 Role sw_role(uint32_t dtype, int64_t I, unsigned flags, uint32_t bucket, int64_t T, bool in_chain);
-uint32_t role_grid(int32_t variant, uint32_t dtype, int64_t T, int64_t I);
+// Workgroups of a role variant for T tokens; `slices` multiplies the RoPE
+// roles' one workgroup per token.
+uint32_t role_grid(int32_t variant, uint32_t dtype, int64_t T, int64_t I, int32_t slices = 1);
+// RoPE vector roles at decode sizes split a token's heads over this many
+// workgroups (1 otherwise).
+int32_t rope_slices(uint32_t dtype, int32_t hd, int32_t rd, bool interleaved, int32_t n_heads,
+                    uint32_t bucket, int32_t variant);
+// The slice count's bits in RopeArgs::mode (none for one slice).
+inline uint32_t rope_slice_bits(int32_t slices) {
+  return slices > 1 ? uint32_t(slices) << kRopeSliceShift : 0u;
+}
 // Element-wise ops (silu, add, masked_fill) over [T, W] and embedding rows.
 Role elt_role(uint32_t dtype, int64_t W, unsigned flags, uint32_t bucket, int64_t T);
 Role emb_role(uint32_t dtype, int64_t H, unsigned flags, int64_t T);
@@ -105,6 +115,7 @@ struct Plan {
   int32_t roles[3];       // chain only
   int32_t n_launches;
   int32_t kvariant[3];    // kernel variant per launch
+  int32_t rope_slices;    // workgroups per token of the RoPE role (vector forms)
   int32_t ksub[3];        // kernel sub-selector (residual flag / fused template index)
                           // fused: (role norm variant - RN_WAVE_1) * 8
                           //        + (GPT-J pairs) * 4

@@ -11,8 +11,10 @@
 namespace tri {
 
 // RoPE variant bits: RopeArgs::mode, and key word 3 above the 16-bit rotary
-// dim.
+// dim. Bits 8..15 of RopeArgs::mode: workgroups per token of the vector
+// forms (0 or 1: one).
 constexpr uint32_t kRopeInterleaved = 1, kRopePos64 = 2, kRopeCache = 4;
+constexpr uint32_t kRopeSliceShift = 8;
 
 // Residual add + RMSNorm and plain RMSNorm ([T, H] rows, element strides).
 struct RnArgs {
@@ -44,7 +46,7 @@ struct RopeArgs {
   int64_t cs_len;
   int32_t nq, nk, hd, rd;
   float eps;
-  uint32_t mode;          // kRopeInterleaved | kRopePos64 | kRopeCache
+  uint32_t mode;          // kRopeInterleaved | kRopePos64 | kRopeCache | slices << 8
 };
 
 // SwiGLU over [T, I].

@@ -370,8 +370,10 @@ __device__ __forceinline__ char *rope_head(const RopeArgs &a, int64_t t, int h, 
                   : static_cast<char *>(a.k) + (t * a.k_ts + int64_t(h - a.nq) * a.hd) * es;
 }
 
-// TPB tokens per workgroup; P2 = rd/2 angle pairs per token (a power of
-// two). Rotate-half (INTER false): each half of the rotated span is
+// TPB tokens per workgroup (with TPB == 1 a token's heads may also be
+// split round-robin over S = slices workgroups: workgroup blk takes token
+// blk / S and heads s, s + S, s + 2S, ... with s = blk % S); P2 = rd/2 angle
+// pairs per token (a power of two). Rotate-half (INTER false): each half of the rotated span is
 // cpb = P2/V 16-byte vectors and a work-item holds chunk c of both halves;
 // GPT-J pairs (INTER true): the span is cpb = rd/V vectors of V/2 adjacent
 // pairs each and a work-item holds one. Work-item `tid` owns chunk tid % cpb
@@ -397,10 +399,12 @@ __device__ __forceinline__ void rope_vec_block(const RopeArgs &a, int64_t blk, f
   const int cpb = (INTER ? a.rd : P2) / V;
   const int shift = __builtin_ctz(unsigned(cpb));
   const int chunk = threadIdx.x & (cpb - 1);
-  const int hg = threadIdx.x >> shift;
-  const int hstep = kThreads >> shift;
   const int nh = a.nq + a.nk;
-  const int64_t t0 = blk * TPB;
+  const int S = TPB == 1 && (a.mode >> kRopeSliceShift) > 1 ? int(a.mode >> kRopeSliceShift) : 1;
+  const int64_t tok_blk = S > 1 ? blk / S : blk;
+  const int hg = int(blk - tok_blk * S) + S * int(threadIdx.x >> shift);   // first head
+  const int hstep = S * (kThreads >> shift);
+  const int64_t t0 = tok_blk * TPB;
   const int64_t tlast = a.T - 1;
   float *cs = lds;
   float *sn = lds + TPB * 256;
@@ -427,7 +431,8 @@ __device__ __forceinline__ void rope_vec_block(const RopeArgs &a, int64_t blk, f
   // gather.
   const int ia = threadIdx.x & (P2 - 1);
   const int64_t ta = t0 + (threadIdx.x >> lp);
-  const bool plain = a.mode == 0 || a.mode == kRopeInterleaved;
+  const uint32_t vbits = a.mode & 0xFFu;
+  const bool plain = vbits == 0 || vbits == kRopeInterleaved;
   int32_t pa = 0;
   float ina = 0.0f;
   if (plain) {

@@ -75,6 +75,22 @@ Role rope_role(uint32_t dtype, int32_t hd, int32_t rd, bool interleaved, unsigne
   return {qk_norm ? ROPE_QKN_VEC : ROPE_VEC, uint32_t(T)};
 }
 
+// At decode sizes a token's RoPE work is latency-bound: a work-item that
+// holds two head items runs them back to back. Splitting the heads of a
+// token round-robin over S = ceil(heads * cpb / 256) workgroups (at most 4)
+// gives every work-item at most one item. Beyond decode sizes one workgroup
+// per token already fills the machine.
+int32_t rope_slices(uint32_t dtype, int32_t hd, int32_t rd, bool interleaved, int32_t n_heads,
+                    uint32_t bucket, int32_t variant) {
+  (void)hd;
+  const bool vec = variant == ROPE_VEC || variant == ROPE_VEC_I || variant == ROPE_QKN_VEC ||
+                   variant == ROPE_QKN_VEC_I;
+  if (!vec || bucket > kDecodeBucketMax) return 1;
+  const int64_t cpb = (interleaved ? rd : rd / 2) / vec_elems(dtype);
+  const int64_t s = cdiv(int64_t(n_heads) * cpb, kBlock);
+  return s < 1 ? 1 : (s > 4 ? 4 : int32_t(s));
+}
+
 // Flat SwiGLU streams nontemporally beyond decode sizes: one vector per
 // work-item as a standalone kernel, four per work-item as a role of the fused
 // chain (where the norm and RoPE roles share the workgroup budget).
@@ -125,13 +141,14 @@ Role emb_role(uint32_t dtype, int64_t H, unsigned flags, int64_t T) {
 
 // Workgroups of a role variant for T tokens (I is the SwiGLU width, the
 // row width of an element-wise op, or the embedding row width).
-uint32_t role_grid(int32_t variant, uint32_t dtype, int64_t T, int64_t I) {
+uint32_t role_grid(int32_t variant, uint32_t dtype, int64_t T, int64_t I, int32_t slices) {
   if (variant == RN_WAVE_1 || variant == RN_WAVE_2) return uint32_t(cdiv(T, 4));
   switch (variant) {
     case RN_SCALAR: case RN_BLOCK_1: case RN_BLOCK_2: case RN_BLOCK_4: case RN_BLOCK_8:
-    case RN_BLOCK_16: case RN_LOOP: case ROPE_SCALAR: case ROPE_VEC: case ROPE_VEC_I:
-    case ROPE_QKN_SCALAR: case ROPE_QKN_VEC: case ROPE_QKN_VEC_I:
+    case RN_BLOCK_16: case RN_LOOP: case ROPE_SCALAR: case ROPE_QKN_SCALAR:
       return uint32_t(T);
+    case ROPE_VEC: case ROPE_VEC_I: case ROPE_QKN_VEC: case ROPE_QKN_VEC_I:
+      return uint32_t(T * slices);
     case SW_FLAT: case SW_FLAT_NT: case ELT_FLAT:
       return clamp_grid(cdiv((T * I) / vec_elems(dtype), kBlock));
     case ELT_FLAT_U2:
@@ -219,6 +236,7 @@ bool key_valid(const Key &k) {
 Plan plan_for_key(const Key &k) {
   const uint32_t op = key_op(k), dt = key_dtype(k), b = key_bucket(k), fl = key_flags(k);
   Plan p{};
+  p.rope_slices = 1;
   // The grid does not affect the choice of variant; T = 1 stands in here.
   switch (op) {
     case TRI_OP_RMSNORM:
@@ -232,12 +250,14 @@ Plan plan_for_key(const Key &k) {
     }
     case TRI_OP_ROPE_QK:
     case TRI_OP_QK_NORM_ROPE: {
-      const Role r = rope_role(dt, int32_t(key_hd(k)), int32_t(key_rd(k)),
-                               (key_rope_bits(k) & kRopeInterleaved) != 0, fl, 1,
+      const bool inter = (key_rope_bits(k) & kRopeInterleaved) != 0;
+      const Role r = rope_role(dt, int32_t(key_hd(k)), int32_t(key_rd(k)), inter, fl, 1,
                                op == TRI_OP_QK_NORM_ROPE);
       p.variant = r.variant;
       p.n_launches = 1;
       p.kvariant[0] = r.variant;
+      p.rope_slices = rope_slices(dt, int32_t(key_hd(k)), int32_t(key_rd(k)), inter,
+                                  int32_t(key_nq(k) + key_nk(k)), b, r.variant);
       return p;
     }
     case TRI_OP_SILU:
@@ -269,9 +289,11 @@ Plan plan_for_key(const Key &k) {
       break;
   }
   const Role rn = rn_role(dt, key_H(k), fl & 3u, 1);
-  const Role ro = rope_role(dt, int32_t(key_hd(k)), int32_t(key_rd(k)),
-                            (key_rope_bits(k) & kRopeInterleaved) != 0, (fl >> 2) & 3u, 1,
+  const bool inter = (key_rope_bits(k) & kRopeInterleaved) != 0;
+  const Role ro = rope_role(dt, int32_t(key_hd(k)), int32_t(key_rd(k)), inter, (fl >> 2) & 3u, 1,
                             (fl & kChainQkNorm) != 0);
+  p.rope_slices = rope_slices(dt, int32_t(key_hd(k)), int32_t(key_rd(k)), inter,
+                              int32_t(key_nq(k) + key_nk(k)), b, ro.variant);
   const Role sw = sw_role(dt, key_I(k), (fl >> 4) & 3u, b, 1, true);
   p.roles[0] = rn.variant;
   p.roles[1] = ro.variant;

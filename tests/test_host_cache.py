@@ -523,7 +523,8 @@ def _kernel_part(src):
 
 def test_jit_source_fixes_the_key_shape(lib, fresh):
     cache = fresh(flags=S.FLAG_AUTO_INSTALL | S.FLAG_JIT)
-    # fused: RN_BLOCK_2 norm role, QK-norm GPT-J RoPE role, cached SwiGLU
+    # fused: RN_BLOCK_2 norm role, QK-norm GPT-J RoPE role, cached SwiGLU;
+    # mode = GPT-J pairs | 3 workgroups per token (40 heads x 16 lanes / 256) << 8
     c = chain_call(BF, 1, 4096, 12288, 32, 8, 128, base=1e6, qk_norm=True,
                    ext=dict(interleaved=1))
     assert S.plan(S.make_key(c), 1)[0] == S.CH_FUSED
@@ -532,7 +533,7 @@ def test_jit_source_fixes_the_key_shape(lib, fresh):
     k = _kernel_part(src)
     assert "tri_jit_kernel(tri::ChainArgs a)" in k
     for frag in ("a.rn.H = 4096;", "a.rope.hd = 128;", "a.rope.rd = 128;", "a.rope.nq = 32;",
-                 "a.rope.nk = 8;", "a.rope.mode = 1u;", "a.sw.I = 12288;",
+                 "a.rope.nk = 8;", "a.rope.mode = 769u;", "a.sw.I = 12288;",
                  "body_chain<1, false, 2, false, true, true>(a)"):
         assert frag in k, frag
     assert src.startswith("// Kernel argument blocks")     # the embedded prelude
@@ -712,17 +713,18 @@ def test_chain_argument_block(lib, fresh):
     c = chain_call(BF, 8, 4096, 14336, 32, 8, 128, base=500000.0)
     assert c_call(lib, cache, c) == 0
     kv, dt, sub, grid, block, _, raw = _last_launch(lib, size="chain")
-    # fused kernel: RN_BLOCK_2 (norm role index 3), plain RoPE, cached one-vector SwiGLU
-    assert (kv, dt, sub, grid, block) == (50, BF, 3 * 8, 8 + 8 + 56, 256)
+    # fused kernel: RN_BLOCK_2 (norm role index 3), plain RoPE, cached one-vector SwiGLU;
+    # RoPE: 40 heads x 8 lanes = 320 > 256 -> two workgroups per token
+    assert (kv, dt, sub, grid, block) == (50, BF, 3 * 8, 8 + 16 + 56, 256)
     rope = rope_block(raw, 88)
     assert (rope.q, rope.k, rope.pos) == (c.ptr["q"], c.ptr["k"], c.ptr["pos"])
-    assert (rope.qw, rope.kw, rope.cos_sin, rope.eps, rope.mode) == (0, 0, 0, 0.0, 0)
+    assert (rope.qw, rope.kw, rope.cos_sin, rope.eps, rope.mode) == (0, 0, 0, 0.0, 2 << 8)
     assert (rope.q_ts, rope.k_ts, rope.T, rope.cs_len) == (32 * 128, 8 * 128, 8, 0)
     assert (rope.nq, rope.nk, rope.hd, rope.rd) == (32, 8, 128, 128)
     sw = struct.unpack_from("<3Q7q", raw, 200)
     assert sw[:3] == (c.ptr["gate"], c.ptr["up"], c.ptr["out"])
     assert sw[3:] == (14336, 14336, 14336, 8, 14336, 8 * 14336 // 8, 8 * 14336)
-    assert struct.unpack_from("<2I", raw, 280) == (8, 8)
+    assert struct.unpack_from("<2I", raw, 280) == (8, 16)
     # the RoPE table pointer is this version's uploaded constants
     assert rope.inv != 0
 
@@ -733,7 +735,7 @@ def test_qk_norm_chain_argument_block(lib, fresh):
     assert c_call(lib, cache, c) == 0
     kv, dt, sub, grid, block, _, raw = _last_launch(lib, size="chain")
     # RN_BLOCK_2 with the QK-norm RoPE role and cached SwiGLU
-    assert (kv, dt, sub, grid, block) == (50, BF, 3 * 8 + 2, 1 + 1 + 6, 256)
+    assert (kv, dt, sub, grid, block) == (50, BF, 3 * 8 + 2, 1 + 2 + 6, 256)
     rope = rope_block(raw, 88)
     assert (rope.qw, rope.kw) == (c.ptr["q_w"], c.ptr["k_w"])
     assert rope.eps == np.float32(1e-5)
@@ -742,7 +744,7 @@ def test_qk_norm_chain_argument_block(lib, fresh):
     c2 = qkn_call(BF, 1, 32, 8, 128, base=1e6, eps=1e-5)
     assert c_call(lib, cache, c2) == 0
     kv2, _, _, grid2, _, _, raw2 = _last_launch(lib, size="rope")
-    assert (kv2, grid2) == (S.ROPE_QKN_VEC, 1)
+    assert (kv2, grid2) == (S.ROPE_QKN_VEC, 2)
     assert rope_block(raw2)[4:] == rope[4:]   # all but the per-version table
 
 

@@ -36,20 +36,22 @@ def test_unused_key_fields_are_zero():
 # ---- policy worked by hand --------------------------------------------------------
 def test_policy_llama7b_decode_chain():
     # bf16: 8 elements per 16 B. H = 4096 -> 512 vectors -> 2 per work-item ->
-    # RN_BLOCK_2, one workgroup per row. RoPE one token per block; T = 1 ->
-    # bucket 0 -> SwiGLU one vector per thread: 11008 / 8 = 1376 vectors -> 6 blocks.
+    # RN_BLOCK_2, one workgroup per row. RoPE: 64 heads x (64 / 8 = 8 lanes) =
+    # 512 lanes -> two workgroups per token at decode sizes. T = 1 -> bucket 0
+    # -> SwiGLU one vector per thread: 11008 / 8 = 1376 vectors -> 6 blocks.
     v, roles, launches = S.plan(S.make_key(chain_call(BF, 1, 4096, 11008, 32, 32, 128)), 1)
     assert v == S.CH_FUSED
     assert roles == (14, 31, 41)
-    assert launches == [(50, 1 + 1 + 6, 256)]
+    assert launches == [(50, 1 + 2 + 6, 256)]
 
 
 def test_policy_gqa_decode_chain():
-    # T = 8 -> bucket 3: norm and RoPE one block per row / token (8 + 8);
-    # SwiGLU 8 * 14336 / 8 = 14336 vectors -> 56 blocks.
+    # T = 8 -> bucket 3: norm one block per row (8); RoPE 40 heads x 8 lanes
+    # = 320 -> two blocks per token (16); SwiGLU 8 * 14336 / 8 = 14336 vectors
+    # -> 56 blocks.
     v, roles, launches = S.plan(S.make_key(chain_call(BF, 8, 4096, 14336, 32, 8, 128,
                                                       base=500000.0)), 8)
-    assert (v, roles, launches) == (S.CH_FUSED, (14, 31, 41), [(50, 8 + 8 + 56, 256)])
+    assert (v, roles, launches) == (S.CH_FUSED, (14, 31, 41), [(50, 8 + 16 + 56, 256)])
 
 
 def test_policy_prefill_chain():
@@ -69,7 +71,7 @@ def test_policy_qwen3_decode_chain_with_qk_norm():
     c = chain_call(BF, 1, 4096, 12288, 32, 8, 128, base=1e6, qk_norm=True)
     assert S.unpack_key(S.make_key(c))["flags"] == 0x7F
     v, roles, launches = S.plan(S.make_key(c), 1)
-    assert (v, roles, launches) == (S.CH_FUSED, (14, 34, 41), [(50, 1 + 1 + 6, 256)])
+    assert (v, roles, launches) == (S.CH_FUSED, (14, 34, 41), [(50, 1 + 2 + 6, 256)])
 
 
 def test_qk_norm_is_a_guard():
@@ -87,8 +89,8 @@ def test_qk_norm_weight_alignment_selects_scalar_role():
     # chain then runs as three launches with the scalar QK-norm role.
     c = qkn_call(BF, 4, 32, 8, 128, w_off=elem_offset(BF))
     assert S.plan(S.make_key(c), 4)[2] == [(S.ROPE_QKN_SCALAR, 4, 256)]
-    c = qkn_call(BF, 4, 32, 8, 128)
-    assert S.plan(S.make_key(c), 4)[2] == [(S.ROPE_QKN_VEC, 4, 256)]
+    c = qkn_call(BF, 4, 32, 8, 128)          # 40 heads x 8 lanes: two blocks per token
+    assert S.plan(S.make_key(c), 4)[2] == [(S.ROPE_QKN_VEC, 8, 256)]
     ch = chain_call(BF, 4, 4096, 12288, 32, 8, 128, qk_norm=True, w_off=elem_offset(BF))
     v, roles, launches = S.plan(S.make_key(ch), 4)
     assert v == S.CH_SEQ and roles[1] == S.ROPE_QKN_SCALAR and len(launches) == 3
@@ -263,3 +265,19 @@ def test_stats_invariant_over_mixed_stream():
     assert s.calls == s.hits + s.misses + s.errors + s.empty
     assert len(set(m.versions)) == len(m.versions) <= 9 * 2 * 3
     assert s.misses == len(m.versions)
+
+
+def test_rope_head_slices_worked_by_hand():
+    # slices = min(4, ceil(heads * lanes / 256)) for vector RoPE roles at
+    # decode sizes (bucket <= 6), else 1
+    # bf16 hd 128: 8 lanes per head. 64 + 8 heads -> 576 lanes -> 3.
+    assert S.plan(S.make_key(rope_call(BF, 2, 64, 8, 128)), 2)[2] == [(S.ROPE_VEC, 6, 256)]
+    # f32 hd 128: 16 lanes per head. 64 + 8 heads -> 1152 lanes -> capped at 4.
+    assert S.plan(S.make_key(rope_call(F, 2, 64, 8, 128)), 2)[2] == [(S.ROPE_VEC, 8, 256)]
+    # 4 + 4 heads of 64 (bf16: 4 lanes) -> 32 lanes -> 1.
+    assert S.plan(S.make_key(rope_call(BF, 3, 4, 4, 64)), 3)[2] == [(S.ROPE_VEC, 3, 256)]
+    # beyond decode sizes (T = 65 -> bucket 7): one block per token.
+    assert S.plan(S.make_key(rope_call(BF, 65, 64, 8, 128)), 65)[2] == [(S.ROPE_VEC, 65, 256)]
+    # scalar roles never split.
+    c = rope_call(BF, 2, 64, 8, 128, off=elem_offset(BF))
+    assert S.plan(S.make_key(c), 2)[2] == [(S.ROPE_SCALAR, 2, 256)]
