@@ -278,12 +278,15 @@ def main():
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(graph, stream=stream):
         cache.decode_chain_args(args_c, stream=torch.cuda.current_stream())
-    graph.replay()
+    # replay() enqueues on the current stream: make that the timed stream
+    with torch.cuda.stream(stream):
+        graph.replay()
     stream.synchronize()
     replay = []
     for _ in range(min(K, 2000)):
         a = time.perf_counter()
-        graph.replay()
+        with torch.cuda.stream(stream):
+            graph.replay()
         stream.synchronize()
         replay.append((time.perf_counter() - a) * 1e6)
     latency["torch_eager_chain_e2e_us"] = summary(eager)
@@ -375,16 +378,31 @@ def main():
     g32 = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g32, stream=stream):
         cache.decode_chain_layers(layer_list, stream=torch.cuda.current_stream())
-    g32.replay()
+    with torch.cuda.stream(stream):
+        g32.replay()
     stream.synchronize()
     rep = []
     for _ in range(n3):
         a = time.perf_counter()
-        g32.replay()
+        with torch.cuda.stream(stream):
+            g32.replay()
         stream.synchronize()
         rep.append((time.perf_counter() - a) * 1e6)
     steps["hip_graph_replay"] = summary(rep)
+    # the library's own capture of the same step (tri_graph_build_layers)
+    ng = cache.build_graph(layer_list)
+    ng.launch(stream)
+    stream.synchronize()
+    rep = []
+    for _ in range(n3):
+        a = time.perf_counter()
+        ng.launch(stream)
+        stream.synchronize()
+        rep.append((time.perf_counter() - a) * 1e6)
+    steps["tri_graph_launch"] = summary(rep)
+    steps["tri_graph_launches_per_step"] = ng.launch_count
     latency["decode_step_32_layers_e2e_us"] = steps
+    ng.close()
     del lay_bufs, g32
 
     # ---- mixed-shape stream: guard hits, misses, latency per token bucket ---------------

@@ -51,6 +51,7 @@ extern "C" {
 #endif
 
 typedef struct tri_cache tri_cache;
+typedef struct tri_graph tri_graph;
 
 typedef enum tri_dtype { TRI_F32 = 0, TRI_BF16 = 1 } tri_dtype;
 
@@ -348,6 +349,27 @@ tri_status tri_decode_chain(tri_cache *cache, const tri_chain_args *args, void *
  * amortises the single native entry over a whole decode step. */
 tri_status tri_decode_chain_layers(tri_cache *cache, const tri_chain_args *layers,
                                    uint32_t n_layers, void *stream);
+
+/* A decode step as a HIP graph: the launches that tri_decode_chain_layers
+ * would issue for `layers` (validated, looked up and -- under
+ * TRI_CACHE_AUTO_INSTALL -- installed exactly as that call does; MISS and
+ * errors as there, with no graph made) are captured once, in layer order,
+ * into an instantiated graph that tri_graph_launch replays with one
+ * submission. The graph fixes every pointer, size and kernel: a replay
+ * evaluates no guard, so it is only valid while the caller's arguments stay
+ * exactly those of the build (the data behind the pointers may change).
+ * This is the CUDA-Graph trade-off the paper compares against (Sec. 4):
+ * no per-call host work, no per-call checks. The graph uses the cache's
+ * kernels and constants: destroy graphs before their cache. Capture uses a
+ * private stream of default priority. Not counted in the cache's
+ * statistics beyond the one build call. */
+tri_status tri_graph_build_layers(tri_cache *cache, const tri_chain_args *layers,
+                                  uint32_t n_layers, tri_graph **out);
+/* Replay a graph on `stream` (asynchronous). RUNTIME if the launch fails. */
+tri_status tri_graph_launch(tri_graph *graph, void *stream);
+/* Launches the graph holds (the kernels of all its layers). */
+uint32_t tri_graph_launch_count(const tri_graph *graph);
+void tri_graph_destroy(tri_graph *graph);
 
 /* ---- miss handling, introspection -------------------------------------------- */
 

@@ -23,7 +23,7 @@ from ._lib import (AUTO_INSTALL, BF16, E_FULL, E_INVALID, E_LAUNCH, E_NOMEM, E_R
                    E_UNSUPPORTED, F32, MISS, OK, ROPE_SCALING_LLAMA3, ROPE_SCALING_NONE,
                    ChainArgs, RopeExt, Selection, Stats, VersionInfo)
 
-__all__ = ["SpecCache", "TriError", "dtype_code", "rope_ext", "Selection", "Stats",
+__all__ = ["SpecCache", "Graph", "TriError", "dtype_code", "rope_ext", "Selection", "Stats",
            "ChainArgs", "RopeExt", "OK", "MISS", "E_INVALID", "E_UNSUPPORTED", "E_FULL",
            "E_NOMEM", "E_LAUNCH", "E_RUNTIME", "F32", "BF16", "AUTO_INSTALL"]
 
@@ -97,6 +97,34 @@ def _tokens(t: torch.Tensor, name: str) -> int:
     if (hd > 1 and t.stride(2) != 1) or (nh > 1 and t.stride(1) != hd):
         raise ValueError(f"{name}: heads must be packed (stride {hd}) with unit inner stride")
     return t.stride(0) if t.shape[0] > 1 else max(t.stride(0), nh * hd)
+
+
+class Graph:
+    """A captured decode step (tri_graph); destroy before its cache."""
+
+    def __init__(self, handle: C.c_void_p, cache: "SpecCache"):
+        self._g = handle
+        self._cache = cache          # keeps the cache alive while the graph lives
+
+    @property
+    def launch_count(self) -> int:
+        return _dll.tri_graph_launch_count(self._g)
+
+    def launch(self, stream=None) -> None:
+        st = _dll.tri_graph_launch(self._g, _stream_ptr(stream))
+        if st != OK:
+            raise TriError(st, "tri_graph_launch")
+
+    def close(self) -> None:
+        if self._g:
+            _dll.tri_graph_destroy(self._g)
+            self._g = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 class SpecCache:
@@ -314,6 +342,22 @@ class SpecCache:
         arr = (ChainArgs * max(1, len(layers)))(*layers)
         self._call("tri_decode_chain_layers", _dll.tri_decode_chain_layers, arr, len(layers),
                    _stream_ptr(stream), max_misses=len(layers))
+
+    def build_graph(self, layers) -> "Graph":
+        """Capture the launches of decode_chain_layers(layers) into a HIP
+        graph (guards evaluated once, now). Replays fix every pointer and size."""
+        arr = (ChainArgs * max(1, len(layers)))(*layers)
+        g = C.c_void_p()
+        st = _dll.tri_graph_build_layers(self._h, arr, len(layers), C.byref(g))
+        for _ in range(len(layers)):
+            if st != MISS:
+                break
+            self.install_last_miss()
+            self.misses_handled += 1
+            st = _dll.tri_graph_build_layers(self._h, arr, len(layers), C.byref(g))
+        if st != OK:
+            raise TriError(st, "tri_graph_build_layers")
+        return Graph(g, self)
 
     def decode_chain(self, x, residual, w, q, k, pos, gate, up, eps=1e-6, base=10000.0,
                      y=None, residual_out=None, out=None, stream=None, q_norm_w=None,

@@ -111,6 +111,10 @@ SIGNATURES = {
                                 _P]),
     "tri_decode_chain": (C.c_int, [_P, C.POINTER(ChainArgs), _P]),
     "tri_decode_chain_layers": (C.c_int, [_P, C.POINTER(ChainArgs), _U32, _P]),
+    "tri_graph_build_layers": (C.c_int, [_P, C.POINTER(ChainArgs), _U32, C.POINTER(C.c_void_p)]),
+    "tri_graph_launch": (C.c_int, [_P, _P]),
+    "tri_graph_launch_count": (_U32, [_P]),
+    "tri_graph_destroy": (None, [_P]),
     "tri_spec_install_last_miss": (C.c_int, [_P, C.POINTER(Selection)]),
     "tri_spec_last_selection": (C.c_int, [_P, C.POINTER(Selection)]),
     "tri_spec_stats": (C.c_int, [_P, C.POINTER(Stats)]),

@@ -8,6 +8,7 @@
 // nothing launched; an error returns a negative status, tries no other
 // version and installs nothing (Sec. 3.5).
 #include <math.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include "internal.h"
@@ -400,6 +401,104 @@ tri_status elt_entry(tri_cache *c, uint32_t op, int32_t dtype, const void *a, in
   return single_launch(c, op, k, T, W, &args, sizeof args, stream);
 }
 
+// Several chains per call, split in two passes so that a graph capture can
+// record the second one alone.
+struct LayerPlan {
+  int32_t vis[TRI_MAX_LAYERS];   // version per layer, -1 for an empty layer
+  int32_t last;                  // last non-empty layer, -1 if none
+  bool missed;
+};
+
+// Pass 1, in layer order: validate, pack the key, look the version up;
+// then, under auto-install, install the missing versions. Nothing is
+// installed or launched before every layer has passed. Returns kGo, or the
+// call's final status (error, MISS, install error, or OK for an empty call)
+// with the statistics and record already written.
+int layers_prepare(tri_cache *c, const tri_chain_args *layers, uint32_t n_layers, LayerPlan *lp) {
+  const uint32_t op = TRI_OP_CHAIN_LAYERS;
+  c->stats.calls++;
+  if (n_layers > uint32_t(TRI_MAX_LAYERS) || (n_layers > 0 && !layers))
+    return finish_early(c, op, TRI_E_INVALID);
+  int32_t first_miss = -1;
+  lp->last = -1;
+  for (uint32_t i = 0; i < n_layers; ++i) {
+    Key k;
+    const int st = chain_check(&layers[i], &k);
+    if (st == TRI_OK) {            // T == 0: this layer is a no-op
+      lp->vis[i] = -1;
+      continue;
+    }
+    if (st != kGo) return finish_early(c, op, st);
+    lp->vis[i] = find_version(c, TRI_OP_CHAIN, k);
+    if (lp->vis[i] < 0 && first_miss < 0) first_miss = int32_t(i);
+    lp->last = int32_t(i);
+  }
+  if (lp->last < 0) return finish_early(c, op, TRI_OK);
+  // Misses: one per entry call; the first missed layer's key is recorded.
+  // With auto-install every missing version is installed, in layer order.
+  lp->missed = first_miss >= 0;
+  if (lp->missed) {
+    c->stats.misses++;
+    Key k;
+    chain_check(&layers[first_miss], &k);
+    c->has_miss = true;
+    c->miss_key = k;
+    c->miss_T = layers[first_miss].T;
+    tri_selection &r = c->last;
+    memset(&r, 0, sizeof r);
+    r.op = int32_t(op);
+    r.version = -1;
+    key_words(k, r.key);
+    if (!(c->flags & TRI_CACHE_AUTO_INSTALL)) {
+      r.status = TRI_MISS;
+      return TRI_MISS;
+    }
+    for (uint32_t i = uint32_t(first_miss); i <= uint32_t(lp->last); ++i) {
+      if (lp->vis[i] >= 0 || layers[i].T == 0) continue;
+      chain_check(&layers[i], &k);
+      const tri_status ist = install_key(c, k);
+      if (ist != TRI_OK) {
+        r.status = ist;
+        return ist;
+      }
+      lp->vis[i] = find_version(c, TRI_OP_CHAIN, k);
+    }
+  }
+  return kGo;
+}
+
+// Pass 2: the launches, in layer order on `stream`; record and count.
+tri_status layers_launch(tri_cache *c, const tri_chain_args *layers, uint32_t n_layers,
+                         const LayerPlan &lp, void *stream, uint32_t *n_launched) {
+  const uint32_t op = TRI_OP_CHAIN_LAYERS;
+  int total = 0;
+  for (uint32_t i = 0; i < n_layers; ++i) {
+    if (lp.vis[i] < 0) continue;
+    Version &v = c->versions[lp.vis[i]];
+    tri_launch_rec l[3];
+    int n = 0;
+    const int rc = chain_launch(v, layers[i], stream, l, &n);
+    total += n;
+    if (rc != 0 || int32_t(i) == lp.last) {
+      Key k;
+      chain_check(&layers[i], &k);
+      record(c, op, v, lp.vis[i], k, n, l, rc ? TRI_E_LAUNCH : TRI_OK);
+      c->last.n_launches = total;
+    }
+    if (rc != 0) {
+      if (!lp.missed) c->stats.errors++;
+      return TRI_E_LAUNCH;
+    }
+  }
+  if (n_launched) *n_launched = uint32_t(total);
+  if (!lp.missed) {
+    c->stats.hits++;
+    for (uint32_t i = 0; i < n_layers; ++i)
+      if (lp.vis[i] >= 0) c->versions[lp.vis[i]].hits++;
+  }
+  return TRI_OK;
+}
+
 // RoPE (op 3) or QK-RMSNorm + RoPE (op 6; the head-norm weights are then
 // required) with an optional variant.
 tri_status rope_entry(tri_cache *c, uint32_t op, int32_t dtype, void *q, int64_t q_ts, void *kp,
@@ -616,83 +715,55 @@ tri_status tri_decode_chain(tri_cache *c, const tri_chain_args *p, void *stream)
 tri_status tri_decode_chain_layers(tri_cache *c, const tri_chain_args *layers, uint32_t n_layers,
                                    void *stream) {
   if (!c) return TRI_E_INVALID;
-  const uint32_t op = TRI_OP_CHAIN_LAYERS;
-  c->stats.calls++;
-  if (n_layers > uint32_t(TRI_MAX_LAYERS) || (n_layers > 0 && !layers))
-    return finish_early(c, op, TRI_E_INVALID);
-  // Pass 1, in layer order: validate, pack the key, look the version up.
-  // Nothing is installed or launched before every layer has passed.
-  int32_t vis[TRI_MAX_LAYERS];
-  int32_t first_miss = -1, last = -1;
-  for (uint32_t i = 0; i < n_layers; ++i) {
-    Key k;
-    const int st = chain_check(&layers[i], &k);
-    if (st == TRI_OK) {            // T == 0: this layer is a no-op
-      vis[i] = -1;
-      continue;
-    }
-    if (st != kGo) return finish_early(c, op, st);
-    vis[i] = find_version(c, TRI_OP_CHAIN, k);
-    if (vis[i] < 0 && first_miss < 0) first_miss = int32_t(i);
-    last = int32_t(i);
+  LayerPlan lp;
+  const int st = layers_prepare(c, layers, n_layers, &lp);
+  if (st != kGo) return tri_status(st);
+  return layers_launch(c, layers, n_layers, lp, stream, nullptr);
+}
+
+tri_status tri_graph_build_layers(tri_cache *c, const tri_chain_args *layers, uint32_t n_layers,
+                                  tri_graph **out) {
+  if (!c || !out) return TRI_E_INVALID;
+  *out = nullptr;
+  // Validation, lookup and installs happen outside the capture (installs
+  // allocate and may compile); only the launches are recorded.
+  LayerPlan lp;
+  int st = layers_prepare(c, layers, n_layers, &lp);
+  if (st != kGo) return tri_status(st);
+  tri_graph *g = static_cast<tri_graph *>(calloc(1, sizeof(tri_graph)));
+  if (!g) return TRI_E_NOMEM;
+  void *cap = nullptr;
+  st = be_capture_begin(&cap);
+  if (st != 0) {
+    free(g);
+    return tri_status(st);
   }
-  if (last < 0) return finish_early(c, op, TRI_OK);
-  // Misses: one per entry call; the first missed layer's key is recorded.
-  // With auto-install every missing version is installed, in layer order.
-  const bool missed = first_miss >= 0;
-  if (missed) {
-    c->stats.misses++;
-    Key k;
-    chain_check(&layers[first_miss], &k);
-    c->has_miss = true;
-    c->miss_key = k;
-    c->miss_T = layers[first_miss].T;
-    tri_selection &r = c->last;
-    memset(&r, 0, sizeof r);
-    r.op = int32_t(op);
-    r.version = -1;
-    key_words(k, r.key);
-    if (!(c->flags & TRI_CACHE_AUTO_INSTALL)) {
-      r.status = TRI_MISS;
-      return TRI_MISS;
-    }
-    for (uint32_t i = uint32_t(first_miss); i <= uint32_t(last); ++i) {
-      if (vis[i] >= 0 || layers[i].T == 0) continue;
-      chain_check(&layers[i], &k);
-      const tri_status ist = install_key(c, k);
-      if (ist != TRI_OK) {
-        r.status = ist;
-        return ist;
-      }
-      vis[i] = find_version(c, TRI_OP_CHAIN, k);
-    }
+  uint32_t launched = 0;
+  const tri_status ls = layers_launch(c, layers, n_layers, lp, cap, &launched);
+  void *exec = nullptr;
+  const int es = be_capture_end(cap, &exec);
+  if (ls != TRI_OK || es != 0) {
+    if (exec) be_graph_destroy(exec);
+    free(g);
+    return ls != TRI_OK ? ls : tri_status(es);
   }
-  // Pass 2: the launches, in layer order on the caller's stream.
-  int total = 0;
-  for (uint32_t i = 0; i < n_layers; ++i) {
-    if (vis[i] < 0) continue;
-    Version &v = c->versions[vis[i]];
-    tri_launch_rec l[3];
-    int n = 0;
-    const int rc = chain_launch(v, layers[i], stream, l, &n);
-    total += n;
-    if (rc != 0 || int32_t(i) == last) {
-      Key k;
-      chain_check(&layers[i], &k);
-      record(c, op, v, vis[i], k, n, l, rc ? TRI_E_LAUNCH : TRI_OK);
-      c->last.n_launches = total;
-    }
-    if (rc != 0) {
-      if (!missed) c->stats.errors++;
-      return TRI_E_LAUNCH;
-    }
-  }
-  if (!missed) {
-    c->stats.hits++;
-    for (uint32_t i = 0; i < n_layers; ++i)
-      if (vis[i] >= 0) c->versions[vis[i]].hits++;
-  }
+  g->exec = exec;
+  g->n_launches = launched;
+  *out = g;
   return TRI_OK;
+}
+
+tri_status tri_graph_launch(tri_graph *g, void *stream) {
+  if (!g) return TRI_E_INVALID;
+  return be_graph_launch(g->exec, stream) == 0 ? TRI_OK : TRI_E_RUNTIME;
+}
+
+uint32_t tri_graph_launch_count(const tri_graph *g) { return g ? g->n_launches : 0; }
+
+void tri_graph_destroy(tri_graph *g) {
+  if (!g) return;
+  if (g->exec) be_graph_destroy(g->exec);
+  free(g);
 }
 
 }  // extern "C"

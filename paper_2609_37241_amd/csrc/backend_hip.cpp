@@ -121,4 +121,40 @@ int be_jit(const char *src, uint64_t len, void **fn, void **module, float *ms) {
 
 void be_unload(void *module) { (void)hipModuleUnload(reinterpret_cast<hipModule_t>(module)); }
 
+// Capture on a private non-blocking stream of default priority, in
+// thread-local mode: only this thread's work on that stream is recorded.
+int be_capture_begin(void **stream) {
+  hipStream_t s = nullptr;
+  if (hipStreamCreateWithFlags(&s, hipStreamNonBlocking) != hipSuccess) return TRI_E_RUNTIME;
+  if (hipStreamBeginCapture(s, hipStreamCaptureModeThreadLocal) != hipSuccess) {
+    (void)hipStreamDestroy(s);
+    return TRI_E_RUNTIME;
+  }
+  *stream = s;
+  return 0;
+}
+
+int be_capture_end(void *stream, void **exec) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipGraph_t g = nullptr;
+  const hipError_t e = hipStreamEndCapture(s, &g);
+  (void)hipStreamDestroy(s);
+  if (e != hipSuccess || !g) return TRI_E_RUNTIME;
+  hipGraphExec_t x = nullptr;
+  const hipError_t ie = hipGraphInstantiate(&x, g, nullptr, nullptr, 0);
+  (void)hipGraphDestroy(g);
+  if (ie != hipSuccess) return TRI_E_RUNTIME;
+  *exec = x;
+  return 0;
+}
+
+int be_graph_launch(void *exec, void *stream) {
+  return hipGraphLaunch(static_cast<hipGraphExec_t>(exec), static_cast<hipStream_t>(stream)) ==
+                 hipSuccess
+             ? 0
+             : TRI_E_RUNTIME;
+}
+
+void be_graph_destroy(void *exec) { (void)hipGraphExecDestroy(static_cast<hipGraphExec_t>(exec)); }
+
 }  // namespace tri

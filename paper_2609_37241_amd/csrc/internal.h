@@ -139,6 +139,12 @@ void be_free(void *dev);
 // 0 or tri_status; *ms gets the compile + load time.
 int be_jit(const char *src, uint64_t len, void **fn, void **module, float *ms);
 void be_unload(void *module);
+// Graph capture: a private stream in capture mode; ending the capture
+// instantiates the recorded launches. 0 or tri_status.
+int be_capture_begin(void **stream);
+int be_capture_end(void *stream, void **exec);   // also releases the stream
+int be_graph_launch(void *exec, void *stream);
+void be_graph_destroy(void *exec);
 
 // ---- versions and the cache ------------------------------------------------------------
 struct Version {
@@ -171,6 +177,12 @@ struct tri_cache {
   tri_stats stats;
   tri_selection last;
   void *empty_fn;
+};
+
+// A captured decode step (api.cpp).
+struct tri_graph {
+  void *exec;              // the backend's instantiated graph
+  uint32_t n_launches;
 };
 
 namespace tri {

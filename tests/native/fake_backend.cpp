@@ -29,6 +29,8 @@ int64_t g_uploads = 0;
 std::vector<std::string> g_jit;   // sources compiled, in order
 int64_t g_unloads = 0;
 bool g_jit_fail = false;
+int64_t g_captures = 0, g_capture_start = 0, g_graph_launches = 0, g_graph_destroys = 0;
+bool g_capture_fail = false;
 
 uintptr_t encode(int32_t v, uint32_t dt, int32_t sub) {
   return (uintptr_t(uint32_t(v)) << 20) | (uintptr_t(dt) << 16) | uintptr_t(uint32_t(sub) & 0xFFFF) |
@@ -99,6 +101,35 @@ void be_unload(void *module) {
   g_unloads++;
 }
 
+// Graph capture: launches between begin and end are logged with the
+// capture stream's handle; a "graph" remembers how many they were, and a
+// graph launch is counted.
+int be_capture_begin(void **stream) {
+  if (g_capture_fail) return TRI_E_RUNTIME;
+  *stream = reinterpret_cast<void *>(uintptr_t(0xCA000000u) + uintptr_t(g_captures++));
+  g_capture_start = int64_t(g_log.size());
+  return 0;
+}
+
+int be_capture_end(void *stream, void **exec) {
+  (void)stream;
+  *exec = reinterpret_cast<void *>(uintptr_t(0xE0000000u) +
+                                   uintptr_t(int64_t(g_log.size()) - g_capture_start));
+  return 0;
+}
+
+int be_graph_launch(void *exec, void *stream) {
+  (void)exec;
+  (void)stream;
+  g_graph_launches++;
+  return 0;
+}
+
+void be_graph_destroy(void *exec) {
+  (void)exec;
+  g_graph_destroys++;
+}
+
 }  // namespace tri
 
 extern "C" {
@@ -111,7 +142,12 @@ void trifake_reset() {
   g_jit.clear();
   g_unloads = 0;
   g_jit_fail = false;
+  g_captures = g_capture_start = g_graph_launches = g_graph_destroys = 0;
+  g_capture_fail = false;
 }
+int64_t trifake_graph_launches() { return g_graph_launches; }
+int64_t trifake_graph_destroys() { return g_graph_destroys; }
+void trifake_capture_fail(int on) { g_capture_fail = on != 0; }
 int64_t trifake_jit_count() { return int64_t(g_jit.size()); }
 int64_t trifake_unload_count() { return g_unloads; }
 void trifake_jit_fail(int on) { g_jit_fail = on != 0; }

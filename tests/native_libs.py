@@ -48,6 +48,16 @@ def load_fake():
     lib.trifake_upload_count.restype = C.c_int64
     lib.trifake_fail_at.argtypes = [C.c_int64]
     lib.trifake_init_status.argtypes = [C.c_int]
+    lib.trifake_graph_launches.restype = C.c_int64
+    lib.trifake_graph_destroys.restype = C.c_int64
+    lib.trifake_capture_fail.argtypes = [C.c_int]
+    lib.tri_graph_build_layers.argtypes = [C.c_void_p, C.c_void_p, C.c_uint32,
+                                           C.POINTER(C.c_void_p)]
+    lib.tri_graph_launch.argtypes = [C.c_void_p, C.c_void_p]
+    lib.tri_graph_launch_count.argtypes = [C.c_void_p]
+    lib.tri_graph_launch_count.restype = C.c_uint32
+    lib.tri_graph_destroy.argtypes = [C.c_void_p]
+    lib.tri_graph_destroy.restype = None
     lib.trifake_jit_count.restype = C.c_int64
     lib.trifake_unload_count.restype = C.c_int64
     lib.trifake_jit_fail.argtypes = [C.c_int]

@@ -584,6 +584,69 @@ def test_chain_layers_run_in_order(tri, cache):
     assert host(dev_layers[4]["res_out"]).view(np.uint16).max() == 0
 
 
+def test_graph_of_layers_replays_match_direct_calls(tri, cache):
+    """A captured step of four dependent layers (one three-launch layer),
+    replayed three times with new input data between replays (same
+    pointers): every replay equals a direct tri_decode_chain_layers call on
+    the same data, bit for bit, and the oracle within tolerance."""
+    cfg = wl.GQA_DECODE
+    n = 4
+
+    def make(seed_base):
+        layers, args = [], []
+        prev = None
+        for l in range(n):
+            inp = wl.host_inputs(cfg, seed=seed_base + l)
+            layout = "unaligned" if l == 2 else "plain"
+            d = {k: place(v, cfg.dtype, layout) if k not in ("w", "pos") else
+                 wl.to_torch(v, cfg.dtype, DEV) for k, v in inp.items()}
+            d["y"], d["res_out"], d["out"] = (empty_like_layout(d["x"]),
+                                              empty_like_layout(d["x"]),
+                                              empty_like_layout(d["gate"]))
+            if prev is not None:
+                d["residual"] = prev
+            a, _ = cache.chain_args(d["x"], d["residual"], d["w"], d["q"], d["k"], d["pos"],
+                                    d["gate"], d["up"], cfg.eps, cfg.base, y=d["y"],
+                                    residual_out=d["res_out"], out=d["out"])
+            layers.append((inp, d))
+            args.append(a)
+            prev = d["res_out"]
+        return layers, args
+
+    gl, gargs = make(200)            # buffers the graph is built on
+    dl, dargs = make(200)            # twin buffers for direct calls
+    graph = cache.build_graph(gargs)
+    # layer 2 is unaligned, and so is layer 3, whose residual is layer 2's output
+    assert graph.launch_count == 1 + 1 + 3 + 3
+    try:
+        for rep in range(3):
+            # new data, same pointers: refill layer inputs of both twins
+            for l in range(n):
+                fresh = wl.host_inputs(cfg, seed=300 + 10 * rep + l)
+                for k in ("x", "q", "k", "gate", "up") + (("residual",) if l == 0 else ()):
+                    src = wl.to_torch(fresh[k], cfg.dtype, DEV)
+                    gl[l][1][k].copy_(src)
+                    dl[l][1][k].copy_(src)
+            torch.cuda.synchronize()
+            graph.launch()
+            cache.decode_chain_layers(dargs)
+            torch.cuda.synchronize()
+            for l in range(n):
+                for nme in ("y", "res_out", "out", "q", "k"):
+                    check(f"rep{rep} {nme}[{l}]", host(gl[l][1][nme]), host(dl[l][1][nme]),
+                          cfg.dtype, exact=True)
+            want = O.decode_chain({k: host(v) for k, v in gl[0][1].items()
+                                   if k in ("x", "residual", "w", "pos", "gate", "up")}
+                                  | {"q": wl.host_inputs(cfg, seed=300 + 10 * rep)["q"],
+                                     "k": wl.host_inputs(cfg, seed=300 + 10 * rep)["k"]},
+                                  cfg.eps, cfg.base, cfg.dtype)
+            check(f"rep{rep} out[0] vs oracle", host(gl[0][1]["out"]), want["out"], cfg.dtype)
+            check(f"rep{rep} q[0] vs oracle", host(gl[0][1]["q"]), want["q"], cfg.dtype)
+    finally:
+        torch.cuda.synchronize()
+        graph.close()
+
+
 # ---- chain layouts, degenerate calls, miss path ----------------------------------------------
 @pytest.mark.parametrize("layout", ["strided", "unaligned"])
 def test_chain_three_launch_variant(tri, cache, layout):

@@ -496,6 +496,61 @@ def test_layers_limit(lib, fresh):
     assert lib.tri_decode_chain_layers(cache, None, 2, None) == S.E_INVALID
 
 
+def test_graph_build_records_the_layer_launches_once(lib, fresh):
+    cache = fresh(flags=1)
+    m = S.SpecCacheModel(flags=1)
+    off = elem_offset(BF)
+    calls = [chain_call(BF, 1, 4096, 14336, 32, 8, 128, rope_off=off * (i == 2)) for i in range(4)]
+    keep = []
+    from paper_2609_37241_amd._lib import ChainArgs
+    arr = (ChainArgs * 4)(*[_chain_struct(c, keep) for c in calls])
+    g = C.c_void_p()
+    n0 = lib.trifake_launch_count()
+    assert lib.tri_graph_build_layers(cache, arr, 4, C.byref(g)) == 0
+    # the model: the same one entry call
+    assert m.call_layers(calls) == S.OK
+    assert c_record(lib, cache) == m.last.as_tuple()
+    assert c_stats(lib, cache) == m_stats(m)
+    # fused, fused, three launches, fused; all on the capture stream
+    assert lib.tri_graph_launch_count(g) == 6 == lib.trifake_launch_count() - n0
+    streams = {_launch_at(lib, i)[5] for i in range(n0, n0 + 6)}
+    assert len(streams) == 1 and streams.pop() >= 0xCA000000
+    for _ in range(3):
+        assert lib.tri_graph_launch(g, None) == 0
+    assert lib.trifake_graph_launches() == 3
+    assert lib.trifake_launch_count() - n0 == 6          # replays launch nothing new
+    assert c_stats(lib, cache) == m_stats(m)              # nor touch the statistics
+    lib.tri_graph_destroy(g)
+    assert lib.trifake_graph_destroys() == 1
+
+
+def test_graph_build_miss_and_errors_make_no_graph(lib, fresh):
+    cache = fresh()
+    calls = [chain_call(BF, 1, 256, 688, 4, 4, 64)]
+    keep = []
+    from paper_2609_37241_amd._lib import ChainArgs
+    arr = (ChainArgs * 1)(*[_chain_struct(c, keep) for c in calls])
+    g = C.c_void_p(123)
+    assert lib.tri_graph_build_layers(cache, arr, 1, C.byref(g)) == S.MISS and not g.value
+    bad = (ChainArgs * 1)(*[_chain_struct(chain_call(BF, 1, 256, 688, 4, 4, 63), keep)])
+    assert lib.tri_graph_build_layers(cache, bad, 1, C.byref(g)) == S.E_INVALID and not g.value
+    assert lib.tri_graph_build_layers(cache, arr, 1, None) == S.E_INVALID
+    lib.trifake_capture_fail(1)
+    c_install(lib, cache)
+    assert lib.tri_graph_build_layers(cache, arr, 1, C.byref(g)) == S.E_RUNTIME and not g.value
+    assert lib.tri_graph_launch(None, None) == S.E_INVALID
+
+
+def _launch_at(lib, i, nbytes=16):
+    kv, dt, sub = C.c_int32(), C.c_int32(), C.c_int32()
+    grid, block = C.c_uint32(), C.c_uint32()
+    stream = C.c_void_p()
+    buf = C.create_string_buffer(nbytes)
+    lib.trifake_get(i, C.byref(kv), C.byref(dt), C.byref(sub), C.byref(grid), C.byref(block),
+                    C.byref(stream), buf, nbytes)
+    return kv.value, dt.value, sub.value, grid.value, block.value, stream.value or 0
+
+
 # ---- runtime-compiled specializations and key import / export ------------------------------
 def test_jit_cache_makes_the_same_selections(lib, fresh):
     cache = fresh(flags=S.FLAG_AUTO_INSTALL | S.FLAG_JIT)
