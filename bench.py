@@ -355,6 +355,22 @@ def main():
         "chain_e2e_us": summary(list(e2e[:n2])), "chain_host_us": summary(list(hst[:n2]))}
     torch.cuda.synchronize()
     jc.close()
+    # the same install served from a code directory (a second process's view)
+    import tempfile
+    with tempfile.TemporaryDirectory() as code_dir:
+        times = []
+        for _ in range(2):
+            jd = tri.SpecCache(jit=True, code_dir=code_dir)
+            aj, _o = jd.chain_args(d["x"], d["residual"], d["w"], d["q"], d["k"], d["pos"],
+                                   d["gate"], d["up"], cfg.eps, cfg.base)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            jd.decode_chain_args(aj, stream)
+            stream.synchronize()
+            times.append(((time.perf_counter() - t0) * 1e3, jd.version_info(0).jit))
+            jd.close()
+    latency["jit_specialized_chain"]["cold_miss_ms_first_process"] = times[0][0]
+    latency["jit_specialized_chain"]["cold_miss_ms_code_dir_hit"] = times[1][0]
 
     # ---- one decode step of 32 layers: one entry call vs 32 calls ------------------------
     bench.trib_layers.argtypes = [C.c_void_p, C.c_int, C.c_void_p, C.c_int, C.c_void_p, C.c_int,

@@ -119,7 +119,8 @@ typedef struct tri_version_info {
   int32_t variant;
   int32_t roles[3];
   uint64_t hits;
-  int32_t jit;         /* 1: kernels compiled at install for this key        */
+  int32_t jit;         /* 1: kernels compiled at install for this key;
+                          2: loaded from the code directory                  */
   float build_ms;      /* install time spent compiling (0 when precompiled)  */
 } tri_version_info;
 
@@ -397,6 +398,16 @@ tri_status tri_spec_version_info(const tri_cache *cache, uint32_t index,
  * cache) into out[0..cap); *n gets the count. */
 tri_status tri_spec_version_constants(const tri_cache *cache, uint32_t index,
                                       float *out, uint32_t cap, uint32_t *n);
+
+/* With TRI_CACHE_JIT: a directory of compiled code objects shared across
+ * caches and processes (the on-disk half of the paper's Sec. 2.2 compile
+ * cache). An install first looks for the code object of its exact source
+ * (named by a 64-bit hash of the source text, the target and the compiler
+ * flags) and loads it; otherwise it compiles and stores the object there
+ * (written under a temporary name and renamed). Unreadable or corrupt files
+ * are recompiled; write failures are ignored. NULL or "" turns it off; the
+ * directory must exist. INVALID for a path of 1024 bytes or more. */
+tri_status tri_spec_set_code_dir(tri_cache *cache, const char *dir);
 
 /* The keys of the installed versions in creation order, TRI_KEY_WORDS words
  * each, into keys[0 .. cap * TRI_KEY_WORDS); *n = the number of versions

@@ -130,8 +130,10 @@ class Graph:
 class SpecCache:
     """One native specialization cache (bound to the current device)."""
 
-    def __init__(self, capacity: int = 0, auto_install: bool = False, jit: bool = False):
-        """jit: installs compile key-specialized kernels with hipRTC."""
+    def __init__(self, capacity: int = 0, auto_install: bool = False, jit: bool = False,
+                 code_dir: Optional[str] = None):
+        """jit: installs compile key-specialized kernels with hipRTC; code_dir:
+        a directory of compiled code objects shared across processes."""
         h = C.c_void_p()
         st = _dll.tri_spec_cache_create(C.byref(h), capacity,
                                         (AUTO_INSTALL if auto_install else 0)
@@ -140,6 +142,10 @@ class SpecCache:
             raise TriError(st, "tri_spec_cache_create")
         self._h = h
         self.misses_handled = 0
+        if code_dir is not None:
+            st = _dll.tri_spec_set_code_dir(h, code_dir.encode())
+            if st != OK:
+                raise TriError(st, "tri_spec_set_code_dir")
 
     def close(self):
         if self._h:

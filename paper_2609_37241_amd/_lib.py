@@ -122,6 +122,7 @@ SIGNATURES = {
     "tri_spec_version_constants": (C.c_int, [_P, _U32, C.POINTER(C.c_float), _U32,
                                              C.POINTER(C.c_uint32)]),
     "tri_launch_empty": (C.c_int, [_P, _P]),
+    "tri_spec_set_code_dir": (C.c_int, [_P, C.c_char_p]),
     "tri_spec_export_keys": (C.c_int, [_P, C.POINTER(C.c_uint64), _U32, C.POINTER(C.c_uint32)]),
     "tri_spec_import_keys": (C.c_int, [_P, C.POINTER(C.c_uint64), _U32, C.POINTER(C.c_uint32)]),
     "tri_status_str": (C.c_char_p, [C.c_int]),

@@ -8,8 +8,7 @@
 #include <hip/hip_runtime.h>
 #include <hip/hiprtc.h>
 
-#include <chrono>
-#include <vector>
+#include <stdlib.h>
 
 #include "internal.h"
 
@@ -80,33 +79,39 @@ int be_upload(const void *host, uint64_t bytes, void **dev) {
 void be_free(void *dev) { (void)hipFree(dev); }
 
 // hipRTC for gfx950 with the device flags of the precompiled kernels (no
-// floating-point contraction, packed FP32 instructions off), then load the
-// code object and resolve the kernel.
-int be_jit(const char *src, uint64_t len, void **fn, void **module, float *ms) {
+// floating-point contraction, packed FP32 instructions off).
+int be_compile(const char *src, uint64_t len, void **code, uint64_t *code_len) {
   (void)len;
-  const auto t0 = std::chrono::steady_clock::now();
   hiprtcProgram prog;
   if (hiprtcCreateProgram(&prog, src, "tri_jit.hip", 0, nullptr, nullptr) != HIPRTC_SUCCESS)
     return TRI_E_RUNTIME;
   const char *opts[] = {"--offload-arch=gfx950", "-O3", "-std=c++17", "-ffp-contract=off",
                         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"};
   int st = 0;
-  std::vector<char> code;
   if (hiprtcCompileProgram(prog, int(sizeof opts / sizeof opts[0]), opts) != HIPRTC_SUCCESS) {
     st = TRI_E_RUNTIME;
   } else {
     size_t n = 0;
-    if (hiprtcGetCodeSize(prog, &n) != HIPRTC_SUCCESS || n == 0) {
+    void *buf = nullptr;
+    if (hiprtcGetCodeSize(prog, &n) != HIPRTC_SUCCESS || n == 0 || !(buf = malloc(n))) {
+      st = TRI_E_RUNTIME;
+    } else if (hiprtcGetCode(prog, static_cast<char *>(buf)) != HIPRTC_SUCCESS) {
+      free(buf);
       st = TRI_E_RUNTIME;
     } else {
-      code.resize(n);
-      if (hiprtcGetCode(prog, code.data()) != HIPRTC_SUCCESS) st = TRI_E_RUNTIME;
+      *code = buf;
+      *code_len = n;
     }
   }
   (void)hiprtcDestroyProgram(&prog);
-  if (st != 0) return st;
+  return st;
+}
+
+// Load a code object and resolve its kernel.
+int be_load_code(const void *code, uint64_t code_len, void **fn, void **module) {
+  (void)code_len;
   hipModule_t mod = nullptr;
-  if (hipModuleLoadData(&mod, code.data()) != hipSuccess) return TRI_E_RUNTIME;
+  if (hipModuleLoadData(&mod, code) != hipSuccess) return TRI_E_RUNTIME;
   hipFunction_t f = nullptr;
   if (hipModuleGetFunction(&f, mod, "tri_jit_kernel") != hipSuccess) {
     (void)hipModuleUnload(mod);
@@ -114,8 +119,6 @@ int be_jit(const char *src, uint64_t len, void **fn, void **module, float *ms) {
   }
   *fn = reinterpret_cast<void *>(f);
   *module = reinterpret_cast<void *>(mod);
-  *ms = float(std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0)
-                  .count());
   return 0;
 }
 

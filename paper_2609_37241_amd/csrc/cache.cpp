@@ -88,8 +88,9 @@ tri_status install_key(tri_cache *c, const Key &k) {
   v.plan = plan_for_key(k);
   const uint32_t dt = key_dtype(k);
   if (c->flags & TRI_CACHE_JIT) {
-    // Compile one specialization per launch of the plan (Sec. 3.5 growth).
-    v.jit = 1;
+    // Compile one specialization per launch of the plan (Sec. 3.5 growth),
+    // or load it from the code directory.
+    v.jit = 2;
     for (int i = 0; i < v.plan.n_launches; ++i) {
       uint64_t len = 0;
       char *src = jit_source(k, v.plan, i, &len);
@@ -98,9 +99,11 @@ tri_status install_key(tri_cache *c, const Key &k) {
         return TRI_E_NOMEM;
       }
       float ms = 0.0f;
-      const int st = be_jit(src, len, &v.fn[i], &v.module[i], &ms);
+      bool from_dir = false;
+      const int st = jit_build(c, src, len, &v.fn[i], &v.module[i], &ms, &from_dir);
       free(src);
       v.build_ms += ms;
+      if (!from_dir) v.jit = 1;
       if (st != 0) {
         release_modules(v);
         return tri_status(st);
@@ -247,6 +250,18 @@ tri_status tri_spec_version_info(const tri_cache *c, uint32_t index, tri_version
   out->hits = v.hits;
   out->jit = v.jit;
   out->build_ms = v.build_ms;
+  return TRI_OK;
+}
+
+tri_status tri_spec_set_code_dir(tri_cache *c, const char *dir) {
+  if (!c) return TRI_E_INVALID;
+  if (!dir) {
+    c->code_dir[0] = '\0';
+    return TRI_OK;
+  }
+  const size_t n = strlen(dir);
+  if (n >= sizeof c->code_dir) return TRI_E_INVALID;
+  memcpy(c->code_dir, dir, n + 1);
   return TRI_OK;
 }
 

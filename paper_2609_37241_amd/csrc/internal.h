@@ -134,10 +134,11 @@ int be_launch(void *fn, uint32_t grid, uint32_t block, const void *args, uint32_
               void *stream);
 int be_upload(const void *host, uint64_t bytes, void **dev);      // per-version constants
 void be_free(void *dev);
-// Compile `src` (len bytes, NUL-terminated) for the device and load it: the
-// kernel `tri_jit_kernel` becomes *fn, the loaded code object *module.
-// 0 or tri_status; *ms gets the compile + load time.
-int be_jit(const char *src, uint64_t len, void **fn, void **module, float *ms);
+// Compile `src` (len bytes, NUL-terminated) for the device into a code
+// object (*code malloc'd, caller frees) / load a code object: the kernel
+// `tri_jit_kernel` becomes *fn, the loaded object *module. 0 or tri_status.
+int be_compile(const char *src, uint64_t len, void **code, uint64_t *code_len);
+int be_load_code(const void *code, uint64_t code_len, void **fn, void **module);
 void be_unload(void *module);
 // Graph capture: a private stream in capture mode; ending the capture
 // instantiates the recorded launches. 0 or tri_status.
@@ -177,6 +178,7 @@ struct tri_cache {
   tri_stats stats;
   tri_selection last;
   void *empty_fn;
+  char code_dir[1024];           // compiled code objects; empty: none
 };
 
 // A captured decode step (api.cpp).
@@ -196,4 +198,9 @@ bool key_valid(const Key &k);
 // the device prelude and one kernel; returns a malloc'd NUL-terminated text
 // (caller frees) and its length, or null.
 char *jit_source(const Key &k, const Plan &p, int i, uint64_t *len);
+// Kernel of `src` for this cache: loaded from the cache's code directory
+// when a code object of the same source is there, else compiled (and
+// stored there). *from_dir tells which; *ms the time taken.
+int jit_build(const tri_cache *c, const char *src, uint64_t len, void **fn, void **module,
+              float *ms, bool *from_dir);
 }  // namespace tri

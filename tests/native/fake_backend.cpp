@@ -26,7 +26,8 @@ std::vector<Rec> g_log;
 int64_t g_fail_at = -1;        // launch ordinal that fails, -1 none
 int g_init_status = 0;
 int64_t g_uploads = 0;
-std::vector<std::string> g_jit;   // sources compiled, in order
+std::vector<std::string> g_jit;   // sources of the code objects loaded, in order
+int64_t g_compiles = 0;
 int64_t g_unloads = 0;
 bool g_jit_fail = false;
 int64_t g_captures = 0, g_capture_start = 0, g_graph_launches = 0, g_graph_destroys = 0;
@@ -84,15 +85,28 @@ int be_upload(const void *host, uint64_t bytes, void **dev) {
 
 void be_free(void *dev) { free(dev); }
 
-// Runtime compilation: records the source and hands out a handle that
-// encodes the position of the source in the log (bit 41 marks it).
-int be_jit(const char *src, uint64_t len, void **fn, void **module, float *ms) {
+// Runtime compilation: the "code object" is the source behind a 4-byte
+// tag; loading records the source and hands out a handle that encodes the
+// position of the source in the log (bit 41 marks it).
+int be_compile(const char *src, uint64_t len, void **code, uint64_t *code_len) {
   if (g_jit_fail) return TRI_E_RUNTIME;
-  g_jit.emplace_back(src, size_t(len));
+  g_compiles++;
+  char *buf = static_cast<char *>(malloc(size_t(len) + 4));
+  if (!buf) return TRI_E_NOMEM;
+  memcpy(buf, "CO1:", 4);
+  memcpy(buf + 4, src, size_t(len));
+  *code = buf;
+  *code_len = len + 4;
+  return 0;
+}
+
+int be_load_code(const void *code, uint64_t code_len, void **fn, void **module) {
+  const char *b = static_cast<const char *>(code);
+  if (code_len < 4 || memcmp(b, "CO1:", 4) != 0) return TRI_E_RUNTIME;
+  g_jit.emplace_back(b + 4, size_t(code_len - 4));
   const uintptr_t idx = uintptr_t(g_jit.size() - 1);
   *fn = reinterpret_cast<void *>((uintptr_t(1) << 41) | (idx << 20));
   *module = reinterpret_cast<void *>(uintptr_t(0x100000 + idx));
-  *ms = 1.0f;
   return 0;
 }
 
@@ -140,6 +154,7 @@ void trifake_reset() {
   g_init_status = 0;
   g_uploads = 0;
   g_jit.clear();
+  g_compiles = 0;
   g_unloads = 0;
   g_jit_fail = false;
   g_captures = g_capture_start = g_graph_launches = g_graph_destroys = 0;
@@ -149,6 +164,7 @@ int64_t trifake_graph_launches() { return g_graph_launches; }
 int64_t trifake_graph_destroys() { return g_graph_destroys; }
 void trifake_capture_fail(int on) { g_capture_fail = on != 0; }
 int64_t trifake_jit_count() { return int64_t(g_jit.size()); }
+int64_t trifake_compile_count() { return g_compiles; }
 int64_t trifake_unload_count() { return g_unloads; }
 void trifake_jit_fail(int on) { g_jit_fail = on != 0; }
 // Source i of the runtime compilations: copies up to cap bytes, returns its

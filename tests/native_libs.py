@@ -59,6 +59,8 @@ def load_fake():
     lib.tri_graph_destroy.argtypes = [C.c_void_p]
     lib.tri_graph_destroy.restype = None
     lib.trifake_jit_count.restype = C.c_int64
+    lib.trifake_compile_count.restype = C.c_int64
+    lib.tri_spec_set_code_dir.argtypes = [C.c_void_p, C.c_char_p]
     lib.trifake_unload_count.restype = C.c_int64
     lib.trifake_jit_fail.argtypes = [C.c_int]
     lib.trifake_jit_source.restype = C.c_int64

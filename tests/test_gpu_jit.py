@@ -194,3 +194,27 @@ def test_prewarmed_jit_cache_has_no_misses(tri):
         torch.cuda.synchronize()
         src.close()
         dst.close()
+
+
+def test_code_directory_loads_compiled_kernels(tri, tmp_path):
+    """A second JIT cache on the same code directory loads the compiled
+    kernels instead of compiling them, and they compute the same bits."""
+    cfg = wl.GQA_DECODE
+    inp = wl.host_inputs(cfg)
+    outs, infos = [], []
+    for _ in range(2):
+        d = {k: wl.to_torch(v, cfg.dtype, DEV) for k, v in inp.items()}
+        c = tri.SpecCache(jit=True, code_dir=str(tmp_path))
+        try:
+            y, ro, out = _chain(tri, c, cfg, d)
+            torch.cuda.synchronize()
+            outs.append([host(t) for t in (y, ro, out, d["q"], d["k"])])
+            infos.append((c.version_info(0).jit, c.version_info(0).build_ms))
+        finally:
+            torch.cuda.synchronize()
+            c.close()
+    assert infos[0][0] == 1 and infos[1][0] == 2
+    assert infos[1][1] < infos[0][1]
+    assert len(list(tmp_path.iterdir())) == 1
+    for a, b in zip(*outs):
+        check("loaded == compiled", a, b, cfg.dtype, exact=True)

@@ -605,6 +605,44 @@ def test_jit_source_fixes_the_key_shape(lib, fresh):
     assert "a.I = 12288;" in sw and "body_sw_flat<0, 1, false>" in sw
 
 
+def test_code_directory_shares_compiled_objects(lib, fresh, tmp_path):
+    from paper_2609_37241_amd._lib import VersionInfo
+    calls = [chain_call(BF, 1, 4096, 11008, 32, 32, 128),
+             chain_call(BF, 2, 4096, 14336, 32, 8, 128, rope_off=elem_offset(BF)),   # 3 launches
+             rn_call(F, 3, 4096)]
+    a = fresh(flags=S.FLAG_AUTO_INSTALL | S.FLAG_JIT)
+    assert lib.tri_spec_set_code_dir(a, str(tmp_path).encode()) == 0
+    for c in calls:
+        assert c_call(lib, a, c) == 0
+    assert lib.trifake_compile_count() == 5
+    files = sorted(p.name for p in tmp_path.iterdir())
+    assert len(files) == 5 and all(f.startswith("tri-") and f.endswith(".co") for f in files)
+    v = VersionInfo()
+    assert lib.tri_spec_version_info(a, 0, C.byref(v)) == 0 and v.jit == 1
+    srcs_a = jit_sources(lib)
+    # a second cache with the same directory loads every object, compiles none
+    # (creating a cache here also resets the recording backend's counters)
+    b = fresh(flags=S.FLAG_AUTO_INSTALL | S.FLAG_JIT)
+    assert lib.tri_spec_set_code_dir(b, str(tmp_path).encode()) == 0
+    for c in calls:
+        assert c_call(lib, b, c) == 0
+    assert lib.trifake_compile_count() == 0
+    for i in range(3):
+        assert lib.tri_spec_version_info(b, i, C.byref(v)) == 0 and v.jit == 2
+    assert jit_sources(lib) == srcs_a                 # the same kernels, loaded
+    # a corrupt object is recompiled and replaced
+    (tmp_path / files[0]).write_bytes(b"garbage")
+    c2 = fresh(flags=S.FLAG_AUTO_INSTALL | S.FLAG_JIT)
+    lib.tri_spec_set_code_dir(c2, str(tmp_path).encode())
+    for c in calls:
+        assert c_call(lib, c2, c) == 0
+    assert lib.trifake_compile_count() == 1
+    assert (tmp_path / files[0]).read_bytes()[:4] == b"CO1:"
+    # path limits
+    assert lib.tri_spec_set_code_dir(c2, b"x" * 1024) == S.E_INVALID
+    assert lib.tri_spec_set_code_dir(c2, None) == 0
+
+
 def test_jit_failure_installs_nothing(lib, fresh):
     cache = fresh(flags=S.FLAG_AUTO_INSTALL | S.FLAG_JIT)
     lib.trifake_jit_fail(1)
