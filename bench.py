@@ -497,7 +497,7 @@ def main():
         roofline = {"bound": "hbm", "achieved": ch["GB/s"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                     "frac": ch["GB/s"] / HBM_PEAK_GBS, "traffic": measured_traffic(),
                     "kernel": "fused decode chain, 8192 tokens (k_chain: block-per-row norm, "
-                              "one-token RoPE blocks, streaming 4-vector SwiGLU)",
+                              "one-token RoPE blocks, streaming one-vector SwiGLU)",
                     "bytes_per_launch": ch["bytes"], "avg_launch_us": ch["mean_us"]}
         del db, y, ro, out, flush, copy_src, copy_dst, mask, table, ids, emb_out
 

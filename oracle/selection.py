@@ -55,7 +55,7 @@ RN_LOOP = 18
 ROPE_SCALAR, ROPE_VEC, ROPE_VEC_I, ROPE_QKN_SCALAR, ROPE_QKN_VEC, ROPE_QKN_VEC_I = \
     30, 31, 32, 33, 34, 35
 ROPE_VEC_ROLES = (ROPE_VEC, ROPE_VEC_I, ROPE_QKN_VEC, ROPE_QKN_VEC_I)
-SW_SCALAR, SW_FLAT, SW_FLAT_NT, SW_ROWS, SW_FLAT_U4_NT = 40, 41, 42, 43, 44
+SW_SCALAR, SW_FLAT, SW_FLAT_NT, SW_ROWS = 40, 41, 42, 43
 CH_FUSED, CH_SEQ = 50, 51
 ELT_SCALAR, ELT_FLAT, ELT_FLAT_U2, ELT_ROWS = 60, 61, 62, 63
 EMB_SCALAR, EMB_VEC = 70, 71
@@ -174,16 +174,15 @@ def rope_slices(dtype: int, rd: int, interleaved: bool, n_heads: int, b: int,
     return max(1, min(4, cdiv(n_heads * cpb, BLOCK)))
 
 
-def sw_role(dtype: int, I: int, flags: int, b: int, T: int,
-            in_chain: bool = False) -> Tuple[int, int]:
+def sw_role(dtype: int, I: int, flags: int, b: int, T: int) -> Tuple[int, int]:
+    """Flat when aligned and contiguous (nontemporal beyond decode sizes, the
+    same as the fused chain's role), vector rows when only the rows are
+    aligned, element-wise otherwise."""
     v = 16 // elem_size(dtype)
     if (flags & ALIGN) and (flags & CONTIG):
         nvec = (T * I) // v
-        if b <= DECODE_BUCKET_MAX:
-            return SW_FLAT, max(1, min(cdiv(nvec, BLOCK), GRID_CAP))
-        if in_chain:
-            return SW_FLAT_U4_NT, max(1, min(cdiv(nvec, 4 * BLOCK), GRID_CAP))
-        return SW_FLAT_NT, max(1, min(cdiv(nvec, BLOCK), GRID_CAP))
+        return (SW_FLAT if b <= DECODE_BUCKET_MAX else SW_FLAT_NT), max(1, min(cdiv(nvec, BLOCK),
+                                                                            GRID_CAP))
     if (flags & ALIGN) and I % v == 0:
         cb = cdiv(I // v, BLOCK)
         return SW_ROWS, min(T * cb, GRID_CAP)
@@ -632,12 +631,12 @@ def plan(key, T: int):
     rn = rn_role(dt, f["H"], fl & 3, T)
     ro = rope_role(dt, f["hd"], (fl >> 2) & 3, T, bool(fl & CHAIN_QK_NORM), f["rd"], inter)
     ro = (ro[0], ro[1] * rope_slices(dt, f["rd"], inter, nh, b, ro[0]))
-    sw = sw_role(dt, f["I"], (fl >> 4) & 3, b, T, in_chain=True)
+    sw = sw_role(dt, f["I"], (fl >> 4) & 3, b, T)
     roles = (rn[0], ro[0], sw[0])
     fused = ((fl & 0x3F) == 0x3F
              and (rn[0] in RN_WAVE.values() or rn[0] in RN_BLOCK.values())
              and ro[0] in ROPE_VEC_ROLES
-             and sw[0] in (SW_FLAT, SW_FLAT_U4_NT))
+             and sw[0] in (SW_FLAT, SW_FLAT_NT))
     if fused:
         return CH_FUSED, roles, [(CH_FUSED, rn[1] + ro[1] + sw[1], BLOCK)]
     return CH_SEQ, roles, [(rn[0], rn[1], BLOCK), (ro[0], ro[1], BLOCK),

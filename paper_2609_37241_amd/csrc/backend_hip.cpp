@@ -36,7 +36,7 @@ int be_resolve(int32_t kvariant, uint32_t dtype, int32_t ksub, void **fn) {
     sym = rn_kernel(kvariant, dtype, ksub);
   else if (kvariant >= ROPE_SCALAR && kvariant <= ROPE_QKN_VEC_I)
     sym = rope_kernel(kvariant, dtype);
-  else if (kvariant >= SW_SCALAR && kvariant <= SW_FLAT_U4_NT)
+  else if (kvariant >= SW_SCALAR && kvariant <= SW_ROWS)
     sym = sw_kernel(kvariant, dtype);
   else if (kvariant == CH_FUSED)
     sym = dtype == TRI_F32 ? chain_kernel_f32(ksub) : chain_kernel_bf16(ksub);

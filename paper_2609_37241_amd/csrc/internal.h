@@ -18,7 +18,7 @@ enum Variant : int32_t {
   RN_LOOP = 18,
   ROPE_SCALAR = 30, ROPE_VEC = 31, ROPE_VEC_I = 32, ROPE_QKN_SCALAR = 33, ROPE_QKN_VEC = 34,
   ROPE_QKN_VEC_I = 35,
-  SW_SCALAR = 40, SW_FLAT = 41, SW_FLAT_NT = 42, SW_ROWS = 43, SW_FLAT_U4_NT = 44,
+  SW_SCALAR = 40, SW_FLAT = 41, SW_FLAT_NT = 42, SW_ROWS = 43,
   CH_FUSED = 50, CH_SEQ = 51,
   ELT_SCALAR = 60, ELT_FLAT = 61, ELT_FLAT_U2 = 62, ELT_ROWS = 63,
   EMB_SCALAR = 70, EMB_VEC = 71,
@@ -93,7 +93,7 @@ struct Role {
 Role rn_role(uint32_t dtype, int64_t H, unsigned flags, int64_t T);
 Role rope_role(uint32_t dtype, int32_t hd, int32_t rd, bool interleaved, unsigned flags, int64_t T,
                bool qk_norm);
-Role sw_role(uint32_t dtype, int64_t I, unsigned flags, uint32_t bucket, int64_t T, bool in_chain);
+Role sw_role(uint32_t dtype, int64_t I, unsigned flags, uint32_t bucket, int64_t T);
 // Workgroups of a role variant for T tokens; `slices` multiplies the RoPE
 // roles' one workgroup per token.
 uint32_t role_grid(int32_t variant, uint32_t dtype, int64_t T, int64_t I, int32_t slices = 1);
@@ -120,7 +120,7 @@ struct Plan {
                           // fused: (role norm variant - RN_WAVE_1) * 8
                           //        + (GPT-J pairs) * 4
                           //        + (QK-RMSNorm before RoPE) * 2
-                          //        + (SwiGLU role is SW_FLAT_U4_NT)
+                          //        + (SwiGLU role is SW_FLAT_NT)
 };
 Plan plan_for_key(const Key &k);
 

@@ -8,46 +8,46 @@ namespace tri {
 using namespace dev;
 
 // RNV: RN_WAVE_1/2 (one wavefront per row) or RN_BLOCK_1..16 (one
-// workgroup per row); SWV: SW_FLAT or SW_FLAT_U4_NT; QKN: QK norm before the
+// workgroup per row); SWV: SW_FLAT or SW_FLAT_NT; QKN: QK norm before the
 // rotation; INTER: GPT-J pairs.
 template <int DT, int RNV, int SWV, bool QKN, bool INTER>
 __global__ __launch_bounds__(256) void k_chain(ChainArgs a) {
   constexpr bool wave = RNV <= RN_WAVE_2;
   constexpr int n = wave ? 1 << (RNV - RN_WAVE_1) : 1 << (RNV - RN_BLOCK_1);
-  body_chain<DT, wave, n, SWV == SW_FLAT_U4_NT, QKN, INTER>(a);
+  body_chain<DT, wave, n, SWV == SW_FLAT_NT, QKN, INTER>(a);
 }
 
 namespace {
 template <int RNV, bool QKN, bool INTER>
-const void *chain_pick_sw(bool u4) {
-  return u4 ? reinterpret_cast<const void *>(&k_chain<kBF16, RNV, SW_FLAT_U4_NT, QKN, INTER>)
+const void *chain_pick_sw(bool nt) {
+  return nt ? reinterpret_cast<const void *>(&k_chain<kBF16, RNV, SW_FLAT_NT, QKN, INTER>)
             : reinterpret_cast<const void *>(&k_chain<kBF16, RNV, SW_FLAT, QKN, INTER>);
 }
 
 template <int RNV>
-const void *chain_pick_rn(int32_t rope_bits, bool u4) {
+const void *chain_pick_rn(int32_t rope_bits, bool nt) {
   switch (rope_bits) {
-    case 0: return chain_pick_sw<RNV, false, false>(u4);
-    case 1: return chain_pick_sw<RNV, true, false>(u4);
-    case 2: return chain_pick_sw<RNV, false, true>(u4);
-    default: return chain_pick_sw<RNV, true, true>(u4);
+    case 0: return chain_pick_sw<RNV, false, false>(nt);
+    case 1: return chain_pick_sw<RNV, true, false>(nt);
+    case 2: return chain_pick_sw<RNV, false, true>(nt);
+    default: return chain_pick_sw<RNV, true, true>(nt);
   }
 }
 }  // namespace
 
 // sub = (norm role - RN_WAVE_1) * 8 + 4 * (GPT-J pairs) + 2 * (QK norm)
-//       + (SwiGLU role streams four vectors per work-item).
+//       + (SwiGLU role streams nontemporally).
 const void *chain_kernel_bf16(int32_t sub) {
-  const bool u4 = sub & 1;
+  const bool nt = sub & 1;
   const int32_t rb = (sub >> 1) & 3;   // bit 0: QK norm, bit 1: GPT-J pairs
   switch (RN_WAVE_1 + (sub >> 3)) {
-    case RN_WAVE_1: return chain_pick_rn<RN_WAVE_1>(rb, u4);
-    case RN_WAVE_2: return chain_pick_rn<RN_WAVE_2>(rb, u4);
-    case RN_BLOCK_1: return chain_pick_rn<RN_BLOCK_1>(rb, u4);
-    case RN_BLOCK_2: return chain_pick_rn<RN_BLOCK_2>(rb, u4);
-    case RN_BLOCK_4: return chain_pick_rn<RN_BLOCK_4>(rb, u4);
-    case RN_BLOCK_8: return chain_pick_rn<RN_BLOCK_8>(rb, u4);
-    case RN_BLOCK_16: return chain_pick_rn<RN_BLOCK_16>(rb, u4);
+    case RN_WAVE_1: return chain_pick_rn<RN_WAVE_1>(rb, nt);
+    case RN_WAVE_2: return chain_pick_rn<RN_WAVE_2>(rb, nt);
+    case RN_BLOCK_1: return chain_pick_rn<RN_BLOCK_1>(rb, nt);
+    case RN_BLOCK_2: return chain_pick_rn<RN_BLOCK_2>(rb, nt);
+    case RN_BLOCK_4: return chain_pick_rn<RN_BLOCK_4>(rb, nt);
+    case RN_BLOCK_8: return chain_pick_rn<RN_BLOCK_8>(rb, nt);
+    case RN_BLOCK_16: return chain_pick_rn<RN_BLOCK_16>(rb, nt);
     default: return nullptr;
   }
 }

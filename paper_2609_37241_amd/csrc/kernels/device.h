@@ -986,16 +986,16 @@ __device__ __forceinline__ void body_emb(const EmbArgs &a) {
 // The fused decode chain: workgroups take the residual-RMSNorm, RoPE-QK and
 // SwiGLU roles by blockIdx range. Norm role: one wavefront per row with N
 // vectors per lane (WAVE) or one workgroup per row with N per work-item;
-// RoPE role: one token per workgroup (QK norm first when QKN, GPT-J pairs
-// when INTER); SwiGLU role: one cached vector per work-item, or four
-// streaming ones (U4).
+// RoPE role: one token (or head slice) per workgroup (QK norm first when
+// QKN, GPT-J pairs when INTER); SwiGLU role: one vector per work-item,
+// nontemporal when NT (streaming sizes).
 //
-// Role order by blockIdx. Decode sizes (one vector): norm rows, RoPE tokens,
-// then SwiGLU -- the norm and RoPE roles take about as long as SwiGLU but
-// have far fewer workgroups, so dispatching them first shortens the critical
-// path (2.75 vs 3.1 µs device time at 1 token). Streaming sizes (U4):
-// SwiGLU first, then norm, then RoPE (about 1 % faster at 8192 tokens than
-// norm first).
+// Role order by blockIdx: norm rows, RoPE tokens, then SwiGLU. At decode
+// sizes the norm and RoPE roles take about as long as SwiGLU but have far
+// fewer workgroups, so dispatching them first shortens the critical path
+// (2.75 vs 3.1 us device time at 1 token); at 8192 tokens this order with a
+// one-vector nontemporal SwiGLU role measured 331.5 us, against 344-349 us
+// for SwiGLU first or with two / four vectors per work-item.
 template <int DT, bool WAVE, int N>
 __device__ __forceinline__ void chain_norm_role(const ChainArgs &a, uint32_t blk) {
   if constexpr (WAVE) {
@@ -1006,27 +1006,17 @@ __device__ __forceinline__ void chain_norm_role(const ChainArgs &a, uint32_t blk
   }
 }
 
-template <int DT, bool WAVE, int N, bool U4, bool QKN, bool INTER>
+template <int DT, bool WAVE, int N, bool NT, bool QKN, bool INTER>
 __device__ __forceinline__ void body_chain(const ChainArgs &a) {
   __shared__ float lds[2 * 256];
   const uint32_t b = blockIdx.x;
   const uint32_t R = a.rn_blocks, P = a.rope_blocks, S = gridDim.x - R - P;
-  if constexpr (U4) {
-    if (b < S) {
-      sw_flat_part<DT, 4, true>(a.sw, b, S);
-    } else if (b < S + R) {
-      chain_norm_role<DT, WAVE, N>(a, b - S);
-    } else {
-      rope_vec_block<DT, 1, false, 4, QKN, INTER>(a.rope, b - S - R, lds);
-    }
+  if (b < R) {
+    chain_norm_role<DT, WAVE, N>(a, b);
+  } else if (b < R + P) {
+    rope_vec_block<DT, 1, false, 4, QKN, INTER>(a.rope, b - R, lds);
   } else {
-    if (b < R) {
-      chain_norm_role<DT, WAVE, N>(a, b);
-    } else if (b < R + P) {
-      rope_vec_block<DT, 1, false, 4, QKN, INTER>(a.rope, b - R, lds);
-    } else {
-      sw_flat_part<DT, 1, false>(a.sw, b - R - P, S);
-    }
+    sw_flat_part<DT, 1, NT>(a.sw, b - R - P, S);
   }
 }
 

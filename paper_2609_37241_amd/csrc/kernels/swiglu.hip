@@ -27,7 +27,6 @@ const void *sw_pick(int32_t variant) {
     case SW_SCALAR: return reinterpret_cast<const void *>(&k_sw_scalar<DT>);
     case SW_FLAT: return reinterpret_cast<const void *>(&k_sw_flat<DT, 1, false>);
     case SW_FLAT_NT: return reinterpret_cast<const void *>(&k_sw_flat<DT, 1, true>);
-    case SW_FLAT_U4_NT: return reinterpret_cast<const void *>(&k_sw_flat<DT, 4, true>);
     case SW_ROWS: return reinterpret_cast<const void *>(&k_sw_rows<DT>);
     default: return nullptr;
   }

@@ -91,17 +91,15 @@ int32_t rope_slices(uint32_t dtype, int32_t hd, int32_t rd, bool interleaved, in
   return s < 1 ? 1 : (s > 4 ? 4 : int32_t(s));
 }
 
-// Flat SwiGLU streams nontemporally beyond decode sizes: one vector per
-// work-item as a standalone kernel, four per work-item as a role of the fused
-// chain (where the norm and RoPE roles share the workgroup budget).
-Role sw_role(uint32_t dtype, int64_t I, unsigned flags, uint32_t bucket, int64_t T,
-             bool in_chain) {
+// Flat SwiGLU streams nontemporally beyond decode sizes, one vector per
+// work-item, standalone and as the fused chain's role (in the chain this
+// measured 331.5 us at 8192 tokens against 344-349 us with two or four
+// vectors per work-item or SwiGLU dispatched first).
+Role sw_role(uint32_t dtype, int64_t I, unsigned flags, uint32_t bucket, int64_t T) {
   const int64_t v = vec_elems(dtype);
   if ((flags & kAlign) && (flags & kContig)) {
     const int64_t nvec = (T * I) / v;
-    if (bucket <= kDecodeBucketMax) return {SW_FLAT, clamp_grid(cdiv(nvec, kBlock))};
-    if (in_chain) return {SW_FLAT_U4_NT, clamp_grid(cdiv(nvec, 4 * int64_t(kBlock)))};
-    return {SW_FLAT_NT, clamp_grid(cdiv(nvec, kBlock))};
+    return {bucket <= kDecodeBucketMax ? SW_FLAT : SW_FLAT_NT, clamp_grid(cdiv(nvec, kBlock))};
   }
   if ((flags & kAlign) && I % v == 0) {
     const int64_t cb = cdiv(I / v, kBlock);
@@ -155,8 +153,6 @@ uint32_t role_grid(int32_t variant, uint32_t dtype, int64_t T, int64_t I, int32_
       return clamp_grid(cdiv((T * I) / vec_elems(dtype), 2 * int64_t(kBlock)));
     case EMB_VEC: case EMB_SCALAR:
       return clamp_grid(T);
-    case SW_FLAT_U4_NT:
-      return clamp_grid(cdiv((T * I) / vec_elems(dtype), 4 * int64_t(kBlock)));
     case SW_ROWS: case ELT_ROWS: {
       const int64_t g = T * cdiv(I / vec_elems(dtype), kBlock);
       return g > int64_t(kGridCap) ? kGridCap : uint32_t(g);
@@ -176,7 +172,7 @@ namespace {
 int32_t fused_sub(int32_t rn, int32_t rope, int32_t sw) {
   const bool inter = rope == ROPE_VEC_I || rope == ROPE_QKN_VEC_I;
   const bool qkn = rope == ROPE_QKN_VEC || rope == ROPE_QKN_VEC_I;
-  return (rn - RN_WAVE_1) * 8 + (inter ? 4 : 0) + (qkn ? 2 : 0) + (sw == SW_FLAT_U4_NT ? 1 : 0);
+  return (rn - RN_WAVE_1) * 8 + (inter ? 4 : 0) + (qkn ? 2 : 0) + (sw == SW_FLAT_NT ? 1 : 0);
 }
 
 bool rope_vec_role(int32_t v) {
@@ -279,7 +275,7 @@ Plan plan_for_key(const Key &k) {
       return p;
     }
     case TRI_OP_SWIGLU: {
-      const Role r = sw_role(dt, key_I(k), fl, b, 1, false);
+      const Role r = sw_role(dt, key_I(k), fl, b, 1);
       p.variant = r.variant;
       p.n_launches = 1;
       p.kvariant[0] = r.variant;
@@ -294,13 +290,13 @@ Plan plan_for_key(const Key &k) {
                             (fl & kChainQkNorm) != 0);
   p.rope_slices = rope_slices(dt, int32_t(key_hd(k)), int32_t(key_rd(k)), inter,
                               int32_t(key_nq(k) + key_nk(k)), b, ro.variant);
-  const Role sw = sw_role(dt, key_I(k), (fl >> 4) & 3u, b, 1, true);
+  const Role sw = sw_role(dt, key_I(k), (fl >> 4) & 3u, b, 1);
   p.roles[0] = rn.variant;
   p.roles[1] = ro.variant;
   p.roles[2] = sw.variant;
   const bool rn_regs = rn.variant >= RN_WAVE_1 && rn.variant <= RN_BLOCK_16;
   const bool ro_vec = rope_vec_role(ro.variant);
-  const bool sw_flat = sw.variant == SW_FLAT || sw.variant == SW_FLAT_U4_NT;
+  const bool sw_flat = sw.variant == SW_FLAT || sw.variant == SW_FLAT_NT;
   if ((fl & 0x3Fu) == 0x3Fu && rn_regs && ro_vec && sw_flat) {
     p.variant = CH_FUSED;
     p.n_launches = 1;

@@ -88,7 +88,7 @@ def test_max_tokens_fused_chain(tri, cache):
     torch.cuda.synchronize()
     rec = cache.last_selection()
     assert rec.variant == S.CH_FUSED
-    assert rec.launch[0].grid_x == T // 4 + T + (T * I // 8) // 1024
+    assert rec.launch[0].grid_x == T // 4 + T + min((T * I // 8) // 256, S.GRID_CAP)
     rows = torch.from_numpy(sample_rows(T, 40, 2)).to(DEV)
     wy, wh = O.residual_rmsnorm(host(x[rows]), host(res[rows]), host(w), 1e-6, nm.BF16)
     check("y", host(y[rows]), wy, nm.BF16)

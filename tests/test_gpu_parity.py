@@ -715,7 +715,7 @@ def test_prefill_chain_full_size_sampled(tri, cache):
                                     d["gate"], d["up"], cfg.eps, cfg.base)
     torch.cuda.synchronize()
     rec = cache.last_selection()
-    assert rec.variant == S.CH_FUSED and rec.launch[0].grid_x == 8192 + 8192 + 28672
+    assert rec.variant == S.CH_FUSED and rec.launch[0].grid_x == 8192 + 8192 + 114688
     rows = np.sort(rng(99).choice(cfg.T, size=40, replace=False))
     rows = np.concatenate([[0, 1, 2, 3, cfg.T - 1], rows])
     ri = torch.from_numpy(rows).to(DEV)

@@ -57,12 +57,13 @@ def test_policy_gqa_decode_chain():
 def test_policy_prefill_chain():
     # T = 8192 -> bucket 13, beyond decode sizes: H = 8192 bf16 -> 1024 vectors
     # -> 4 per work-item -> RN_BLOCK_4, one block per row (8192); RoPE one token
-    # per block (8192 blocks); SwiGLU role 8192 * 28672 / 8 = 29360128 vectors
-    # at 4 per work-item, streaming -> 28672 blocks.
+    # per block (8192 blocks, no head slices beyond decode sizes); SwiGLU role
+    # 8192 * 28672 / 8 = 29360128 vectors, one per work-item, streaming ->
+    # 114688 blocks.
     v, roles, launches = S.plan(S.make_key(chain_call(BF, 8192, 8192, 28672, 64, 8, 128,
                                                       base=500000.0)), 8192)
-    assert (v, roles) == (S.CH_FUSED, (15, 31, 44))
-    assert launches == [(50, 8192 + 8192 + 28672, 256)]
+    assert (v, roles) == (S.CH_FUSED, (15, 31, 42))
+    assert launches == [(50, 8192 + 8192 + 114688, 256)]
 
 
 def test_policy_qwen3_decode_chain_with_qk_norm():
@@ -164,10 +165,8 @@ def test_swiglu_flat_grid_cap_and_tail():
     # 1 element: no whole vector, still one block for the tail
     assert S.sw_role(F, 1, 3, 0, 1) == (S.SW_FLAT, 1)
     assert S.sw_role(BF, 1 << 30, 3, 10, 1024) == (S.SW_FLAT_NT, S.GRID_CAP)
-    assert S.sw_role(BF, 1 << 30, 3, 10, 1024, in_chain=True) == (S.SW_FLAT_U4_NT, S.GRID_CAP)
-    # 65 tokens x 1024 bf16: 8320 vectors -> 33 blocks standalone, 9 in the chain
+    # 65 tokens x 1024 bf16: 8320 vectors -> 33 blocks
     assert S.sw_role(BF, 1024, 3, 7, 65) == (S.SW_FLAT_NT, 33)
-    assert S.sw_role(BF, 1024, 3, 7, 65, in_chain=True) == (S.SW_FLAT_U4_NT, 9)
 
 
 # ---- Algorithm 1 and the three paths ---------------------------------------------
