@@ -643,6 +643,233 @@ def plan(key, T: int):
                            (sw[0], sw[1], BLOCK)]
 
 
+
+# ---- install-time tuning (the benchmark-and-keep scheme of Sec. 2) ------------------
+# A key has an ordered list of candidate plans: index 0 is the policy's plan
+# above, the others are the other kernel variants whose preconditions the
+# key guarantees. A tuning cache times every candidate on a call of the
+# key's shapes and keeps the fastest; the policy's plan stays unless another
+# candidate is faster than TUNE_MARGIN times its time.
+FLAG_AUTOTUNE = 4
+TUNE_MARGIN = 0.97
+SLICE_CHOICES = (1, 2, 4)
+SLICE_BUCKET_MAX = 13        # head-slice alternatives up to 8192 tokens
+TUNE_SCRATCH_MAX = 4 << 30   # tuning calls with more operand bytes are not timed
+TUNE_NONE, TUNE_MEASURED, TUNE_STORED, TUNE_SKIPPED = 0, 1, 2, 3
+
+
+@dataclasses.dataclass(frozen=True)
+class Cand:
+    """One candidate plan: the version's variant, the chain's roles, the
+    kernel of each launch and the RoPE role's workgroups per token."""
+    variant: int
+    roles: Tuple[int, int, int]
+    kernels: Tuple[int, ...]
+    slices: int
+
+
+def _slice_options(S: int, b: int) -> List[int]:
+    """The policy's slice count first, then 1, 2, 4 (up to bucket 13)."""
+    if b > SLICE_BUCKET_MAX:
+        return [S]
+    return [S] + [s for s in SLICE_CHOICES if s != S]
+
+
+def _rn_options(dt: int, H: int, fl: int, standalone: bool) -> List[int]:
+    """Norm rows: a row held by one wavefront can also be held by one
+    256-lane workgroup (one vector per lane); a row held in registers can
+    also take the two-pass loop kernel (standalone only: the fused chain
+    holds its rows in registers)."""
+    P = rn_role(dt, H, fl, 1)[0]
+    if P in (RN_SCALAR, RN_LOOP):
+        return [P]
+    out = [P]
+    if P in RN_WAVE.values():
+        out.append(RN_BLOCK[1])
+    if standalone:
+        out.append(RN_LOOP)
+    return out
+
+
+def _other(P: int, a: int, b: int) -> List[int]:
+    return [P, b if P == a else a]
+
+
+def candidates(key) -> List[Cand]:
+    """The candidate plans of `key`, in the library's order (index 0 is the
+    policy's plan).
+
+    * RMSNorm rows: the policy's register layout, the workgroup layout when
+      the policy takes a wavefront, the two-pass loop.
+    * RoPE with a vector role: the vector kernel at each slice option, then
+      the scalar kernel.
+    * SwiGLU / silu / add / masked_fill, flat: the policy's flat form, the
+      other flat form (cached / nontemporal, one / two vectors per
+      work-item), vector rows when a row is a whole number of vectors.
+    * The fused chain: every combination of norm role options x slice
+      options x SwiGLU flat forms (nested in that order, each list starting
+      with the policy's choice), then the three-launch sequence of the
+      policy's roles.
+    * Every other plan is the only candidate of its key.
+    """
+    f = unpack_key(key)
+    op, dt, b, fl = f["op"], f["dtype"], f["bucket"], f["flags"]
+    v = 16 // elem_size(dt)
+    z = (0, 0, 0)
+    if op in (OP_RMSNORM, OP_RES_RMSNORM):
+        return [Cand(r, z, (r,), 1) for r in _rn_options(dt, f["H"], fl, True)]
+    inter = bool(f["rope_bits"] & ROPE_INTERLEAVED)
+    nh = f["nq"] + f["nk"]
+    if op in (OP_ROPE_QK, OP_QK_NORM_ROPE):
+        qkn = op == OP_QK_NORM_ROPE
+        P = rope_role(dt, f["hd"], fl, 1, qkn, f["rd"], inter)[0]
+        if P not in ROPE_VEC_ROLES:
+            return [Cand(P, z, (P,), 1)]
+        S = rope_slices(dt, f["rd"], inter, nh, b, P)
+        sc = ROPE_QKN_SCALAR if qkn else ROPE_SCALAR
+        return [Cand(P, z, (P,), s) for s in _slice_options(S, b)] + [Cand(sc, z, (sc,), 1)]
+    if op == OP_SWIGLU:
+        P = sw_role(dt, f["I"], fl, b, 1)[0]
+        opts = [P]
+        if P in (SW_FLAT, SW_FLAT_NT):
+            opts = _other(P, SW_FLAT, SW_FLAT_NT) + ([SW_ROWS] if f["I"] % v == 0 else [])
+        return [Cand(w, z, (w,), 1) for w in opts]
+    if op in ELT_OPS:
+        P = elt_role(dt, f["H"], fl, b, 1)[0]
+        opts = [P]
+        if P in (ELT_FLAT, ELT_FLAT_U2):
+            opts = _other(P, ELT_FLAT, ELT_FLAT_U2) + ([ELT_ROWS] if f["H"] % v == 0 else [])
+        return [Cand(e, z, (e,), 1) for e in opts]
+    if op == OP_EMBEDDING:
+        P = emb_role(dt, f["H"], fl, 1)[0]
+        return [Cand(P, z, (P,), 1)]
+    variant, roles, _ = plan(key, 1)
+    rn, ro, sw = roles
+    S = rope_slices(dt, f["rd"], inter, nh, b, ro)
+    seq = Cand(CH_SEQ, roles, roles, S)
+    if variant != CH_FUSED:
+        return [seq]
+    out = []
+    for r in _rn_options(dt, f["H"], fl & 3, False):
+        for s in _slice_options(S, b):
+            for w in _other(sw, SW_FLAT, SW_FLAT_NT):
+                out.append(Cand(CH_FUSED, (r, ro, w), (CH_FUSED,), s))
+    return out + [seq]
+
+
+def grid_of(variant: int, dt: int, T: int, width: int, slices: int = 1) -> int:
+    """Workgroups a kernel variant launches for T tokens (width: SwiGLU's I,
+    a short op's row width). Wavefront norm rows: 4 rows per workgroup;
+    other norm and RoPE kernels: one workgroup per row or token (vector RoPE:
+    times its slices); flat kernels: one 16-byte vector per work-item (two
+    for ELT_FLAT_U2); row kernels: the row's vectors over 256 work-items,
+    per row; element-wise kernels: one element per work-item. Flat, row and
+    element-wise grids are capped at GRID_CAP (grid-stride beyond)."""
+    v = 16 // elem_size(dt)
+    if variant in RN_WAVE.values():
+        return cdiv(T, 4)
+    if variant in (RN_SCALAR, RN_LOOP, ROPE_SCALAR, ROPE_QKN_SCALAR) or \
+            variant in RN_BLOCK.values():
+        return T
+    if variant in ROPE_VEC_ROLES:
+        return T * slices
+    if variant in (SW_FLAT, SW_FLAT_NT, ELT_FLAT):
+        return max(1, min(cdiv((T * width) // v, BLOCK), GRID_CAP))
+    if variant == ELT_FLAT_U2:
+        return max(1, min(cdiv((T * width) // v, 2 * BLOCK), GRID_CAP))
+    if variant in (EMB_VEC, EMB_SCALAR):
+        return max(1, min(T, GRID_CAP))
+    if variant in (SW_ROWS, ELT_ROWS):
+        return min(T * cdiv(width // v, BLOCK), GRID_CAP)
+    if variant in (SW_SCALAR, ELT_SCALAR):
+        return min(cdiv(T * width, BLOCK), GRID_CAP)
+    raise ValueError(variant)
+
+
+def cand_plan(key, c: Cand, T: int):
+    """(variant, roles, launches) of candidate c for a call with T tokens, in
+    the form plan() returns."""
+    f = unpack_key(key)
+    dt = f["dtype"]
+    width = f["H"] if f["op"] in SHORT_OPS else f["I"]
+    if c.variant == CH_FUSED:
+        g = (grid_of(c.roles[0], dt, T, width) + grid_of(c.roles[1], dt, T, width, c.slices)
+             + grid_of(c.roles[2], dt, T, width))
+        return CH_FUSED, c.roles, [(CH_FUSED, g, BLOCK)]
+    launches = [(kv, grid_of(kv, dt, T, width, c.slices if kv in ROPE_VEC_ROLES else 1), BLOCK)
+                for kv in c.kernels]
+    return c.variant, c.roles, launches
+
+
+def tune_tokens(key) -> int:
+    """Tokens of the tuning call: the top of the key's bucket."""
+    return 1 << unpack_key(key)["bucket"]
+
+
+def _tune_stride(width: int, fl: int, v: int) -> int:
+    """Row stride of a tuning operand: the width when contiguous, else the
+    next multiple of the vector width above it (aligned) or width + 1."""
+    if fl & CONTIG:
+        return width
+    return cdiv(width + 1, v) * v if fl & ALIGN else width + 1
+
+
+def tune_operand_bytes(key) -> int:
+    """Bytes of the operands of the tuning call (T = tune_tokens(key), row
+    strides by _tune_stride, weights and tables once)."""
+    f = unpack_key(key)
+    op, dt, fl = f["op"], f["dtype"], f["flags"]
+    es = elem_size(dt)
+    v = 16 // es
+    T = tune_tokens(key)
+    H, I = f["H"], f["I"]
+
+    def norm(fl2, res):
+        return (4 if res else 2) * T * _tune_stride(H, fl2, v) * es + H * es
+
+    def rope(fl2, qkn):
+        hd, nq, nk = f["hd"], f["nq"], f["nk"]
+        n = T * _tune_stride(nq * hd, fl2, v) * es
+        if nk:
+            n += T * _tune_stride(nk * hd, fl2, v) * es
+        n += T * (8 if f["rope_bits"] & ROPE_POS64 else 4)
+        if qkn:
+            n += hd * es * (2 if nk else 1)
+        if f["rope_bits"] & ROPE_CACHE:
+            n += f["rd"] * 4
+        return n
+
+    def swiglu(fl2):
+        return 3 * T * _tune_stride(I, fl2, v) * es
+
+    if op in (OP_RMSNORM, OP_RES_RMSNORM):
+        return norm(fl, op == OP_RES_RMSNORM)
+    if op in (OP_ROPE_QK, OP_QK_NORM_ROPE):
+        return rope(fl, op == OP_QK_NORM_ROPE)
+    if op == OP_SWIGLU:
+        return swiglu(fl)
+    if op in ELT_OPS:
+        s = _tune_stride(H, fl, v)
+        n = 2 * T * s * es
+        if op == OP_ADD:
+            n += T * s * es
+        elif op == OP_MASKED_FILL:
+            n += T * s
+        return n
+    if op == OP_EMBEDDING:
+        return 0
+    return norm(fl & 3, True) + rope((fl >> 2) & 3, bool(fl & CHAIN_QK_NORM)) + \
+        swiglu((fl >> 4) & 3)
+
+
+def tune_choice(times: List[float]) -> int:
+    """Index of the kept candidate given each candidate's time: the fastest
+    (the first of equals), unless it is not faster than TUNE_MARGIN times
+    candidate 0's time, in which case the policy's plan (0) stays."""
+    best = min(range(len(times)), key=lambda i: (times[i], i))
+    keep = np.float32(times[best]) < np.float32(TUNE_MARGIN) * np.float32(times[0])
+    return best if keep else 0
+
 # ---- the cache -----------------------------------------------------------------
 @dataclasses.dataclass
 class Stats:
@@ -657,12 +884,19 @@ class Stats:
 class SpecCacheModel:
     """Ordered versions, Algorithm 1 lookup, miss / install / error paths."""
 
-    def __init__(self, capacity: int = 0, flags: int = 0):
-        if capacity < 0 or capacity > MAX_CAPACITY or flags & ~(FLAG_AUTO_INSTALL | FLAG_JIT):
+    def __init__(self, capacity: int = 0, flags: int = 0, timer=None):
+        """timer(key, index, cand) -> time of candidate `index` on the tuning
+        call; used by a tuning cache (FLAG_AUTOTUNE) for keys with several
+        candidates."""
+        if capacity < 0 or capacity > MAX_CAPACITY or \
+                flags & ~(FLAG_AUTO_INSTALL | FLAG_JIT | FLAG_AUTOTUNE):
             raise ValueError("invalid cache parameters")
         self.capacity = capacity or DEFAULT_CAPACITY
         self.flags = flags
+        self.timer = timer
         self.versions: List[Tuple[int, ...]] = []
+        self.choice: List[int] = []        # candidate index per version
+        self.tuned: List[int] = []         # TUNE_* per version
         self.version_hits: List[int] = []
         self.last_miss: Optional[Tuple[Tuple[int, ...], int]] = None
         self.stats = Stats()
@@ -717,7 +951,7 @@ class SpecCacheModel:
                 return st
             i = self.lookup(key)
             auto = True
-        variant, roles, launches = plan(key, c.T)
+        variant, roles, launches = self.version_plan(i, c.T)
         rec.version, rec.variant, rec.roles = i, variant, roles
         rec.n_launches = len(launches)
         rec.launch = tuple(launches) + ((0, 0, 0),) * (3 - len(launches))
@@ -785,7 +1019,7 @@ class SpecCacheModel:
         for i, c in enumerate(calls):
             if vis[i] is None:
                 continue
-            variant, roles, launches = plan(keys[i], c.T)
+            variant, roles, launches = self.version_plan(vis[i], c.T)
             st = self._launch(launches)
             total += len(launches)
             if st < 0 or i == last:
@@ -805,15 +1039,40 @@ class SpecCacheModel:
                     self.version_hits[v] += 1
         return OK
 
-    def _install(self, key) -> int:
+    def version_plan(self, i: int, T: int):
+        """(variant, roles, launches) of version i for a call with T tokens."""
+        key = self.versions[i]
+        return cand_plan(key, candidates(key)[self.choice[i]], T)
+
+    def _install(self, key, candidate: int = -1) -> int:
+        """Install `key` with candidate plan `candidate` (-1: tuned on a
+        tuning cache, else the policy's plan)."""
         if self.lookup(key) >= 0:
             return OK
+        cands = candidates(key)
+        if candidate < -1 or candidate >= len(cands):
+            return E_INVALID
         if len(self.versions) >= self.capacity:
             return E_FULL
+        choice, tuned = max(candidate, 0), TUNE_NONE
+        if candidate < 0 and self.flags & FLAG_AUTOTUNE and len(cands) > 1:
+            if tune_operand_bytes(key) > TUNE_SCRATCH_MAX:
+                tuned = TUNE_SKIPPED
+            else:
+                choice = tune_choice([self.timer(key, j, c) for j, c in enumerate(cands)])
+                tuned = TUNE_MEASURED
         self.versions.append(key)
+        self.choice.append(choice)
+        self.tuned.append(tuned)
         self.version_hits.append(0)
         self.stats.installs += 1
         return OK
+
+    def install_key(self, key, candidate: int = -1) -> int:
+        """A key installed directly (tri_spec_install_key)."""
+        if not key_valid(tuple(key)):
+            return E_INVALID
+        return self._install(tuple(key), candidate)
 
     def import_keys(self, keys) -> Tuple[int, int]:
         """Install `keys` in order (status, keys processed); a malformed key
@@ -833,7 +1092,7 @@ class SpecCacheModel:
         st = self._install(key)
         if st < 0:
             return st, None
-        variant, roles, launches = plan(key, T)
+        variant, roles, launches = self.version_plan(self.lookup(key), T)
         rec = Record(op=key[0] & 0xFF, status=OK, version=self.lookup(key),
                      variant=variant, n_launches=len(launches), roles=roles,
                      launch=tuple(launches) + ((0, 0, 0),) * (3 - len(launches)),
