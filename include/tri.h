@@ -78,7 +78,16 @@ enum { TRI_MAX_LAYERS = 1024 };   /* layers per tri_decode_chain_layers call */
 
 enum {
   TRI_CACHE_AUTO_INSTALL = 1u,   /* on a miss: install, then launch */
-  TRI_CACHE_JIT = 2u             /* install compiles a key-specialized kernel */
+  TRI_CACHE_JIT = 2u,            /* install compiles a key-specialized kernel */
+  TRI_CACHE_AUTOTUNE = 4u        /* install times the key's candidate plans */
+};
+
+/* How a version's plan was chosen (tri_version_info.tuned). */
+enum {
+  TRI_TUNE_NONE = 0,       /* the install policy's plan, or a pinned candidate */
+  TRI_TUNE_MEASURED = 1,   /* the fastest candidate of a timed tuning call     */
+  TRI_TUNE_STORED = 2,     /* a tuning result read from the code directory      */
+  TRI_TUNE_SKIPPED = 3     /* tuning call too large or not possible: policy plan */
 };
 
 /* One kernel launch of a selection. */
@@ -122,6 +131,14 @@ typedef struct tri_version_info {
   int32_t jit;         /* 1: kernels compiled at install for this key;
                           2: loaded from the code directory                  */
   float build_ms;      /* install time spent compiling (0 when precompiled)  */
+  int32_t n_launches;  /* launches per call                                  */
+  int32_t kernels[3];  /* kernel variant of each launch (fused chain: 50)    */
+  int32_t rope_slices; /* workgroups per token of the RoPE role (1: none)    */
+  int32_t candidate;   /* index of the plan among the key's candidates       */
+  int32_t n_candidates;
+  int32_t tuned;       /* TRI_TUNE_*                                          */
+  float tune_ms;       /* install time spent tuning                          */
+  uint32_t reserved;
 } tri_version_info;
 
 /* RoPE variants. A zeroed struct (or a NULL pointer where one is taken) is
@@ -203,7 +220,8 @@ typedef struct tri_chain_args {
 /* ---- cache ---------------------------------------------------------------- */
 
 /* Create an empty cache on the current device. capacity 0 selects 256
- * (at most 4096); flags: TRI_CACHE_AUTO_INSTALL and / or TRI_CACHE_JIT. The
+ * (at most 4096); flags: TRI_CACHE_AUTO_INSTALL, TRI_CACHE_JIT and
+ * TRI_CACHE_AUTOTUNE in any combination. The
  * cache owns every version, its kernel handles (and, with TRI_CACHE_JIT,
  * its loaded code objects) and its device constants; release it with
  * tri_spec_cache_destroy. Errors: INVALID (NULL out, capacity or flags out
@@ -217,6 +235,29 @@ typedef struct tri_chain_args {
  * the same device bodies as the precompiled variants; the install policy,
  * the launch geometry and the selection records are those of the
  * precompiled path. A failed compilation fails the install with RUNTIME. */
+/* TRI_CACHE_AUTOTUNE is the benchmark-and-keep scheme of Triton's
+ * autotuner that the paper describes (Sec. 2): every key has an ordered
+ * list of candidate plans -- index 0 the install policy's plan, then the
+ * other kernel variants whose preconditions the key guarantees (another
+ * register layout or the two-pass kernel for norm rows, 1 / 2 / 4
+ * workgroups per token or the scalar kernel for vector RoPE, the other flat
+ * form or the row kernel for SwiGLU and the element-wise ops, every
+ * combination of those for the fused chain and then its three-launch
+ * sequence). Installing a key with more than one candidate makes a tuning
+ * call of the key's shapes (tokens = the top of its bucket, row strides =
+ * the width when contiguous, else the next multiple of 16 bytes above it,
+ * or one element more when unaligned) on zero-filled device memory of its
+ * own, on a private stream, through the same entry points: two warm-up
+ * rounds and five timed rounds over the candidates in turn, each call
+ * timed with HIP events. The fastest median is kept when it beats
+ * candidate 0's by more than 3 %; otherwise candidate 0 stays. Keys whose
+ * tuning call needs more than 4 GiB of operands keep candidate 0
+ * (TRI_TUNE_SKIPPED), as do keys whose memory cannot be allocated. With a
+ * code directory the choice is stored there (named by a hash of the key,
+ * the device's architecture and the candidate list) and later installs
+ * read it instead of timing. With TRI_CACHE_JIT the chosen plan is then
+ * compiled. Installs (and so misses under auto-install) allocate, create a
+ * stream and synchronize: do them before capturing a graph. */
 tri_status tri_spec_cache_create(tri_cache **out, uint32_t capacity, uint32_t flags);
 void tri_spec_cache_destroy(tri_cache *cache);
 
@@ -427,6 +468,16 @@ tri_status tri_spec_export_keys(const tri_cache *cache, uint64_t *keys, uint32_t
  * stop (all n on OK). */
 tri_status tri_spec_import_keys(tri_cache *cache, const uint64_t *keys, uint32_t n,
                                 uint32_t *done);
+
+/* Install one key (TRI_KEY_WORDS words, checked as tri_spec_import_keys
+ * checks them) with a chosen plan: candidate -1 takes the cache's own rule
+ * (tuned with TRI_CACHE_AUTOTUNE, else the install policy's plan);
+ * 0 .. n_candidates - 1 pins that candidate (tri_version_info reports
+ * n_candidates and the chosen index, so a tuned set of versions can be
+ * exported and reinstalled without timing). A key already installed adds
+ * nothing and keeps its plan. Errors: INVALID (NULL, malformed key,
+ * candidate out of range), FULL, NOMEM, RUNTIME. */
+tri_status tri_spec_install_key(tri_cache *cache, const uint64_t *key, int32_t candidate);
 
 /* Launch the empty kernel (1 workgroup of 64 work-items, no arguments)
  * through the same launch path: the yardstick for per-call cost. */

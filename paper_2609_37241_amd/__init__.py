@@ -131,13 +131,16 @@ class SpecCache:
     """One native specialization cache (bound to the current device)."""
 
     def __init__(self, capacity: int = 0, auto_install: bool = False, jit: bool = False,
-                 code_dir: Optional[str] = None):
-        """jit: installs compile key-specialized kernels with hipRTC; code_dir:
-        a directory of compiled code objects shared across processes."""
+                 code_dir: Optional[str] = None, autotune: bool = False):
+        """jit: installs compile key-specialized kernels with hipRTC; autotune:
+        installs time the key's candidate plans and keep the fastest; code_dir:
+        a directory of compiled code objects and tuning results shared across
+        processes."""
         h = C.c_void_p()
         st = _dll.tri_spec_cache_create(C.byref(h), capacity,
                                         (AUTO_INSTALL if auto_install else 0)
-                                        | (L.JIT if jit else 0))
+                                        | (L.JIT if jit else 0)
+                                        | (L.AUTOTUNE if autotune else 0))
         if st != OK:
             raise TriError(st, "tri_spec_cache_create")
         self._h = h
@@ -395,6 +398,14 @@ class SpecCache:
         if st != OK:
             raise TriError(st, f"tri_spec_import_keys (after {done.value} keys)")
         return done.value
+
+    def install_key(self, key, candidate: int = -1) -> None:
+        """Install one key (6 words) with candidate plan `candidate` (-1: the
+        cache's own rule: tuned under autotune, else the policy's plan)."""
+        buf = (C.c_uint64 * L.KEY_WORDS)(*[int(x) for x in key])
+        st = _dll.tri_spec_install_key(self._h, buf, candidate)
+        if st != OK:
+            raise TriError(st, "tri_spec_install_key")
 
     def launch_empty(self, stream=None) -> None:
         st = _dll.tri_launch_empty(self._h, _stream_ptr(stream))

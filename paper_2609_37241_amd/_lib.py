@@ -22,6 +22,8 @@ OP_SILU, OP_ADD, OP_MASKED_FILL, OP_EMBEDDING = 8, 9, 10, 11
 MAX_LAYERS = 1024
 AUTO_INSTALL = 1
 JIT = 2
+AUTOTUNE = 4
+TUNE_NONE, TUNE_MEASURED, TUNE_STORED, TUNE_SKIPPED = 0, 1, 2, 3
 KEY_WORDS = 6
 ROPE_SCALING_NONE, ROPE_SCALING_LLAMA3 = 0, 1
 
@@ -54,7 +56,11 @@ class Stats(C.Structure):
 
 class VersionInfo(C.Structure):
     _fields_ = [("key", C.c_uint64 * KEY_WORDS), ("variant", C.c_int32), ("roles", C.c_int32 * 3),
-                ("hits", C.c_uint64), ("jit", C.c_int32), ("build_ms", C.c_float)]
+                ("hits", C.c_uint64), ("jit", C.c_int32), ("build_ms", C.c_float),
+                ("n_launches", C.c_int32), ("kernels", C.c_int32 * 3),
+                ("rope_slices", C.c_int32), ("candidate", C.c_int32),
+                ("n_candidates", C.c_int32), ("tuned", C.c_int32), ("tune_ms", C.c_float),
+                ("reserved", C.c_uint32)]
 
 
 class RopeExt(C.Structure):
@@ -86,7 +92,7 @@ class ChainArgs(C.Structure):
 
 
 assert C.sizeof(Selection) == 120 and C.sizeof(ChainArgs) == 240 and C.sizeof(RopeExt) == 48
-assert C.sizeof(VersionInfo) == 80
+assert C.sizeof(VersionInfo) == 120
 
 _P, _I64, _I32, _F, _U32 = C.c_void_p, C.c_int64, C.c_int32, C.c_float, C.c_uint32
 
@@ -125,6 +131,7 @@ SIGNATURES = {
     "tri_spec_set_code_dir": (C.c_int, [_P, C.c_char_p]),
     "tri_spec_export_keys": (C.c_int, [_P, C.POINTER(C.c_uint64), _U32, C.POINTER(C.c_uint32)]),
     "tri_spec_import_keys": (C.c_int, [_P, C.POINTER(C.c_uint64), _U32, C.POINTER(C.c_uint32)]),
+    "tri_spec_install_key": (C.c_int, [_P, C.POINTER(C.c_uint64), _I32]),
     "tri_status_str": (C.c_char_p, [C.c_int]),
 }
 

@@ -8,6 +8,7 @@
 #include <hip/hip_runtime.h>
 #include <hip/hiprtc.h>
 
+#include <stdio.h>
 #include <stdlib.h>
 
 #include "internal.h"
@@ -159,5 +160,81 @@ int be_graph_launch(void *exec, void *stream) {
 }
 
 void be_graph_destroy(void *exec) { (void)hipGraphExecDestroy(static_cast<hipGraphExec_t>(exec)); }
+
+// ---- install-time tuning -------------------------------------------------------
+// Zero-filled by a fill on the tuning stream, so the tuning calls that
+// follow on that stream see zeros (positions 0: every RoPE table read is in
+// range).
+int be_scratch(uint64_t bytes, void *stream, void **dev) {
+  void *p = nullptr;
+  if (hipMalloc(&p, bytes) != hipSuccess) return TRI_E_NOMEM;
+  if (hipMemsetAsync(p, 0, bytes, static_cast<hipStream_t>(stream)) != hipSuccess) {
+    (void)hipFree(p);
+    return TRI_E_RUNTIME;
+  }
+  *dev = p;
+  return 0;
+}
+
+void be_scratch_free(void *dev) { (void)hipFree(dev); }
+
+namespace {
+struct Timer {
+  hipStream_t stream;
+  uint32_t n;
+  hipEvent_t ev[1];   // n events
+};
+}  // namespace
+
+// A private non-blocking stream of default priority and n timing events.
+int be_timer_create(uint32_t n_events, void **timer, void **stream) {
+  Timer *t = static_cast<Timer *>(calloc(1, sizeof(Timer) + sizeof(hipEvent_t) * n_events));
+  if (!t) return TRI_E_NOMEM;
+  if (hipStreamCreateWithFlags(&t->stream, hipStreamNonBlocking) != hipSuccess) {
+    free(t);
+    return TRI_E_RUNTIME;
+  }
+  for (uint32_t i = 0; i < n_events; ++i) {
+    if (hipEventCreate(&t->ev[i]) != hipSuccess) {
+      t->n = i;
+      be_timer_destroy(t);
+      return TRI_E_RUNTIME;
+    }
+  }
+  t->n = n_events;
+  *timer = t;
+  *stream = t->stream;
+  return 0;
+}
+
+int be_timer_record(void *timer, uint32_t i) {
+  Timer *t = static_cast<Timer *>(timer);
+  if (i >= t->n) return TRI_E_INVALID;
+  return hipEventRecord(t->ev[i], t->stream) == hipSuccess ? 0 : TRI_E_RUNTIME;
+}
+
+int be_timer_elapsed(void *timer, uint32_t i, uint32_t j, float *ms) {
+  Timer *t = static_cast<Timer *>(timer);
+  if (i >= t->n || j >= t->n) return TRI_E_INVALID;
+  if (hipEventSynchronize(t->ev[j]) != hipSuccess) return TRI_E_RUNTIME;
+  return hipEventElapsedTime(ms, t->ev[i], t->ev[j]) == hipSuccess ? 0 : TRI_E_RUNTIME;
+}
+
+void be_timer_destroy(void *timer) {
+  Timer *t = static_cast<Timer *>(timer);
+  (void)hipStreamSynchronize(t->stream);
+  for (uint32_t i = 0; i < t->n; ++i) (void)hipEventDestroy(t->ev[i]);
+  (void)hipStreamDestroy(t->stream);
+  free(t);
+}
+
+void be_arch(char *out, uint32_t cap) {
+  if (!cap) return;
+  out[0] = '\0';
+  int dev = 0;
+  hipDeviceProp_t p;
+  if (hipGetDevice(&dev) != hipSuccess || hipGetDeviceProperties(&p, dev) != hipSuccess) return;
+  snprintf(out, cap, "%s", p.gcnArchName);
+}
 
 }  // namespace tri

@@ -7,8 +7,11 @@
 // version matches a key; checking the op's last hit before the ordered scan
 // therefore returns exactly the version the scan would.
 #include <math.h>
+#include <stdio.h>
 #include <stdlib.h>
 #include <string.h>
+
+#include <chrono>
 
 #include "internal.h"
 
@@ -77,16 +80,102 @@ void release_modules(Version &v) {
 
 }  // namespace
 
-tri_status install_key(tri_cache *c, const Key &k) {
+namespace {
+
+// Path of the stored tuning result of key k: named by a hash of the key,
+// the device architecture and the candidate list, so a change of any of
+// them names another file.
+bool tune_path(const tri_cache *c, const Key &k, const Plan *cands, int n, char *path,
+               size_t cap) {
+  if (!c->code_dir[0]) return false;
+  char arch[64] = {0};
+  be_arch(arch, sizeof arch);
+  uint64_t w[TRI_KEY_WORDS];
+  key_words(k, w);
+  uint64_t h = fnv1a64("tri-tune-1", 10);
+  h = fnv1a64(arch, strlen(arch), h);
+  h = fnv1a64(w, sizeof w, h);
+  h = fnv1a64(cands, sizeof(Plan) * size_t(n), h);
+  return snprintf(path, cap, "%s/tri-tune-%016llx.txt", c->code_dir, (unsigned long long)h) <
+         int(cap);
+}
+
+// A stored choice: one decimal index below n.
+bool read_choice(const char *path, int n, int32_t *choice) {
+  void *data = nullptr;
+  uint64_t len = 0;
+  if (!read_file(path, &data, &len)) return false;
+  char buf[16] = {0};
+  memcpy(buf, data, len < 15 ? size_t(len) : 15);
+  free(data);
+  char *end = nullptr;
+  const long v = strtol(buf, &end, 10);
+  if (end == buf || (*end != '\n' && *end != '\0') || v < 0 || v >= n) return false;
+  *choice = int32_t(v);
+  return true;
+}
+
+// Releases what a partly built version holds.
+void drop_version(Version &v) {
+  release_modules(v);
+  if (v.d_consts) be_free(v.d_consts);
+  free(v.h_consts);
+  v.d_consts = nullptr;
+  v.h_consts = nullptr;
+}
+
+}  // namespace
+
+tri_status install_key(tri_cache *c, const Key &k, int32_t candidate) {
   for (uint32_t i = 0; i < c->n_versions; ++i)
     if (c->versions[i].key == k) return TRI_OK;          // idempotent
+  Plan cands[kMaxCandidates];
+  const int nc = plan_candidates(k, cands);
+  if (candidate < -1 || candidate >= nc) return TRI_E_INVALID;
   if (c->n_versions >= c->capacity) return TRI_E_FULL;
 
   Version v;
   memset(&v, 0, sizeof v);
   v.key = k;
-  v.plan = plan_for_key(k);
+  v.n_candidates = nc;
+  v.candidate = candidate < 0 ? 0 : candidate;
   const uint32_t dt = key_dtype(k);
+  const uint32_t op = key_op(k);
+  const bool rope = op == TRI_OP_ROPE_QK || op == TRI_OP_QK_NORM_ROPE || op == TRI_OP_CHAIN;
+  if (rope && !(key_rope_bits(k) & kRopeCache)) {
+    v.n_consts = key_rd(k) / 2;
+    v.h_consts = static_cast<float *>(malloc(sizeof(float) * v.n_consts));
+    if (!v.h_consts) return TRI_E_NOMEM;
+    rope_inverse_frequencies(k, v.h_consts);
+    void *dev = nullptr;
+    const int st = be_upload(v.h_consts, sizeof(float) * v.n_consts, &dev);
+    if (st != 0) {
+      drop_version(v);
+      return tri_status(st);
+    }
+    v.d_consts = static_cast<float *>(dev);
+  }
+
+  if (candidate < 0 && (c->flags & TRI_CACHE_AUTOTUNE) && nc > 1) {
+    // Benchmark-and-keep (Sec. 2): a stored choice, else a timed one.
+    const auto t0 = std::chrono::steady_clock::now();
+    char path[1100];
+    const bool dir = tune_path(c, k, cands, nc, path, sizeof path);
+    if (dir && read_choice(path, nc, &v.candidate)) {
+      v.tuned = TRI_TUNE_STORED;
+    } else {
+      tune_key(c, k, cands, nc, v, &v.candidate, &v.tuned);
+      if (dir && v.tuned == TRI_TUNE_MEASURED) {
+        char buf[16];
+        const int m = snprintf(buf, sizeof buf, "%d\n", v.candidate);
+        write_file(path, buf, uint64_t(m));
+      }
+    }
+    v.tune_ms = float(std::chrono::duration<double, std::milli>(
+                          std::chrono::steady_clock::now() - t0).count());
+  }
+  v.plan = cands[v.candidate];
+
   if (c->flags & TRI_CACHE_JIT) {
     // Compile one specialization per launch of the plan (Sec. 3.5 growth),
     // or load it from the code directory.
@@ -95,7 +184,7 @@ tri_status install_key(tri_cache *c, const Key &k) {
       uint64_t len = 0;
       char *src = jit_source(k, v.plan, i, &len);
       if (!src) {
-        release_modules(v);
+        drop_version(v);
         return TRI_E_NOMEM;
       }
       float ms = 0.0f;
@@ -105,34 +194,18 @@ tri_status install_key(tri_cache *c, const Key &k) {
       v.build_ms += ms;
       if (!from_dir) v.jit = 1;
       if (st != 0) {
-        release_modules(v);
+        drop_version(v);
         return tri_status(st);
       }
     }
   } else {
     for (int i = 0; i < v.plan.n_launches; ++i) {
       const int st = be_resolve(v.plan.kvariant[i], dt, v.plan.ksub[i], &v.fn[i]);
-      if (st != 0) return tri_status(st);
+      if (st != 0) {
+        drop_version(v);
+        return tri_status(st);
+      }
     }
-  }
-  const uint32_t op = key_op(k);
-  const bool rope = op == TRI_OP_ROPE_QK || op == TRI_OP_QK_NORM_ROPE || op == TRI_OP_CHAIN;
-  if (rope && !(key_rope_bits(k) & kRopeCache)) {
-    v.n_consts = key_rd(k) / 2;
-    v.h_consts = static_cast<float *>(malloc(sizeof(float) * v.n_consts));
-    if (!v.h_consts) {
-      release_modules(v);
-      return TRI_E_NOMEM;
-    }
-    rope_inverse_frequencies(k, v.h_consts);
-    void *dev = nullptr;
-    const int st = be_upload(v.h_consts, sizeof(float) * v.n_consts, &dev);
-    if (st != 0) {
-      free(v.h_consts);
-      release_modules(v);
-      return tri_status(st);
-    }
-    v.d_consts = static_cast<float *>(dev);
   }
   c->versions[c->n_versions++] = v;
   c->stats.installs++;
@@ -175,7 +248,8 @@ extern "C" {
 tri_status tri_spec_cache_create(tri_cache **out, uint32_t capacity, uint32_t flags) {
   if (!out) return TRI_E_INVALID;
   *out = nullptr;
-  if (capacity > kMaxCapacity || (flags & ~uint32_t(TRI_CACHE_AUTO_INSTALL | TRI_CACHE_JIT)))
+  if (capacity > kMaxCapacity ||
+      (flags & ~uint32_t(TRI_CACHE_AUTO_INSTALL | TRI_CACHE_JIT | TRI_CACHE_AUTOTUNE)))
     return TRI_E_INVALID;
   if (capacity == 0) capacity = kDefaultCapacity;
   int device = 0;
@@ -250,6 +324,14 @@ tri_status tri_spec_version_info(const tri_cache *c, uint32_t index, tri_version
   out->hits = v.hits;
   out->jit = v.jit;
   out->build_ms = v.build_ms;
+  out->n_launches = v.plan.n_launches;
+  for (int i = 0; i < 3; ++i) out->kernels[i] = i < v.plan.n_launches ? v.plan.kvariant[i] : 0;
+  out->rope_slices = v.plan.rope_slices;
+  out->candidate = v.candidate;
+  out->n_candidates = v.n_candidates;
+  out->tuned = v.tuned;
+  out->tune_ms = v.tune_ms;
+  out->reserved = 0;
   return TRI_OK;
 }
 
@@ -289,6 +371,13 @@ tri_status tri_spec_import_keys(tri_cache *c, const uint64_t *keys, uint32_t n, 
   }
   if (done) *done = i;
   return st;
+}
+
+tri_status tri_spec_install_key(tri_cache *c, const uint64_t *key, int32_t candidate) {
+  if (!c || !key) return TRI_E_INVALID;
+  const Key k{key[0], key[1], key[2], key[3], key[4], key[5]};
+  if (!key_valid(k)) return TRI_E_INVALID;
+  return install_key(c, k, candidate);
 }
 
 tri_status tri_spec_version_constants(const tri_cache *c, uint32_t index, float *out,

@@ -124,6 +124,14 @@ struct Plan {
 };
 Plan plan_for_key(const Key &k);
 
+// Install-time tuning: the key's candidate plans, index 0 = plan_for_key.
+constexpr int kMaxCandidates = 24;
+int plan_candidates(const Key &k, Plan *out);   // returns the count (>= 1)
+constexpr uint32_t kSliceBucketMax = 13;        // head-slice alternatives up to 8192 tokens
+constexpr float kTuneMargin = 0.97f;
+constexpr uint64_t kTuneScratchMax = uint64_t(4) << 30;
+constexpr int kTuneWarmup = 2, kTuneRounds = 5;
+
 // ---- backend --------------------------------------------------------------------------
 // The launch backend. The HIP build resolves kernel handles with the runtime
 // and launches with hipModuleLaunchKernel; the CPU test build records calls.
@@ -146,6 +154,15 @@ int be_capture_begin(void **stream);
 int be_capture_end(void *stream, void **exec);   // also releases the stream
 int be_graph_launch(void *exec, void *stream);
 void be_graph_destroy(void *exec);
+// Tuning: zero-filled device memory (released with be_scratch_free), and a
+// timer = a private stream of default priority with n_events event slots.
+int be_scratch(uint64_t bytes, void *stream, void **dev);
+void be_scratch_free(void *dev);
+int be_timer_create(uint32_t n_events, void **timer, void **stream);
+int be_timer_record(void *timer, uint32_t i);                 // event i on the timer's stream
+int be_timer_elapsed(void *timer, uint32_t i, uint32_t j, float *ms);   // waits for event j
+void be_timer_destroy(void *timer);
+void be_arch(char *out, uint32_t cap);                         // device architecture name
 
 // ---- versions and the cache ------------------------------------------------------------
 struct Version {
@@ -155,6 +172,8 @@ struct Version {
   void *module[3];        // runtime-compiled code objects, or null
   int32_t jit;
   float build_ms;
+  int32_t candidate, n_candidates, tuned;
+  float tune_ms;
   float *d_consts;        // device copy of the RoPE inverse frequencies, or null
   float *h_consts;        // host copy (rotary_dim/2 floats), or null
   uint32_t n_consts;
@@ -188,9 +207,9 @@ struct tri_graph {
 };
 
 namespace tri {
-// Cache core (cache.cpp).
+// Cache core (cache.cpp). install_key: candidate -1 = the cache's rule.
 int32_t find_version(tri_cache *c, uint32_t op, const Key &k);
-tri_status install_key(tri_cache *c, const Key &k);
+tri_status install_key(tri_cache *c, const Key &k, int32_t candidate = -1);
 void fill_selection(const Version &v, int32_t index, int64_t T, tri_selection *out);
 // Runtime-compiled specializations (jit.cpp).
 bool key_valid(const Key &k);
@@ -203,4 +222,15 @@ char *jit_source(const Key &k, const Plan &p, int i, uint64_t *len);
 // stored there). *from_dir tells which; *ms the time taken.
 int jit_build(const tri_cache *c, const char *src, uint64_t len, void **fn, void **module,
               float *ms, bool *from_dir);
+// Code-directory files (jit.cpp).
+uint64_t fnv1a64(const void *p, uint64_t n, uint64_t h = 0xcbf29ce484222325ull);
+bool read_file(const char *path, void **data, uint64_t *n);
+void write_file(const char *path, const void *data, uint64_t n);
+// Install-time tuning (tune.cpp): times the n candidates of `k` on a call
+// of the key's shapes and returns the index to keep in *choice and
+// TRI_TUNE_MEASURED or TRI_TUNE_SKIPPED in *how. `v` holds the version under
+// construction (its device constants serve every candidate). Never fails:
+// problems keep candidate 0.
+void tune_key(tri_cache *c, const Key &k, const Plan *cands, int n, const Version &v,
+              int32_t *choice, int32_t *how);
 }  // namespace tri

@@ -8,6 +8,8 @@
 // flags, RoPE variant), so the same key always selects the same kernels.
 #include <string.h>
 
+#include <initializer_list>
+
 #include "internal.h"
 
 namespace tri {
@@ -311,6 +313,129 @@ Plan plan_for_key(const Key &k) {
   p.kvariant[1] = ro.variant;
   p.kvariant[2] = sw.variant;
   return p;
+}
+
+// ---- candidate plans of install-time tuning ---------------------------------------
+// Index 0 is the policy's plan. The others are the kernel variants whose
+// requirements the key also meets: a norm row held by one wavefront can be
+// held by one workgroup (one vector per lane), and a row held in registers
+// can take the two-pass kernel (standalone only); a vector RoPE role can
+// split a token's heads over 1, 2 or 4 workgroups (up to 8192 tokens) or
+// take the scalar kernel; flat SwiGLU and element-wise kernels have a cached
+// and a streaming (SwiGLU: nontemporal; element-wise: two vectors per
+// work-item) form and a row form when a row is whole vectors. The fused
+// chain takes every combination of its roles' options (norm, then slices,
+// then SwiGLU form, each starting with the policy's choice), then the
+// three-launch sequence of the policy's roles.
+namespace {
+
+int rn_options(uint32_t dt, int64_t H, unsigned fl, bool standalone, int32_t *out) {
+  const int32_t P = rn_role(dt, H, fl, 1).variant;
+  int n = 0;
+  out[n++] = P;
+  if (P == RN_SCALAR || P == RN_LOOP) return n;
+  if (P == RN_WAVE_1 || P == RN_WAVE_2) out[n++] = RN_BLOCK_1;
+  if (standalone) out[n++] = RN_LOOP;
+  return n;
+}
+
+int slice_options(int32_t S, uint32_t bucket, int32_t *out) {
+  int n = 0;
+  out[n++] = S;
+  if (bucket > kSliceBucketMax) return n;
+  const int32_t choices[3] = {1, 2, 4};
+  for (int32_t c : choices)
+    if (c != S) out[n++] = c;
+  return n;
+}
+
+Plan single(int32_t variant, int32_t sub, int32_t slices) {
+  Plan p{};
+  p.variant = variant;
+  p.n_launches = 1;
+  p.kvariant[0] = variant;
+  p.ksub[0] = sub;
+  p.rope_slices = slices;
+  return p;
+}
+
+}  // namespace
+
+int plan_candidates(const Key &k, Plan *out) {
+  const Plan P = plan_for_key(k);
+  const uint32_t op = key_op(k), dt = key_dtype(k), b = key_bucket(k), fl = key_flags(k);
+  const int64_t v = vec_elems(dt);
+  int n = 0;
+  out[n++] = P;
+  switch (op) {
+    case TRI_OP_RMSNORM:
+    case TRI_OP_RES_RMSNORM: {
+      int32_t r[3];
+      const int nr = rn_options(dt, key_H(k), fl, true, r);
+      for (int i = 1; i < nr; ++i) out[n++] = single(r[i], P.ksub[0], 1);
+      return n;
+    }
+    case TRI_OP_ROPE_QK:
+    case TRI_OP_QK_NORM_ROPE: {
+      if (!rope_vec_role(P.variant)) return n;
+      int32_t s[4];
+      const int ns = slice_options(P.rope_slices, b, s);
+      for (int i = 1; i < ns; ++i) out[n++] = single(P.variant, 0, s[i]);
+      out[n++] = single(op == TRI_OP_QK_NORM_ROPE ? ROPE_QKN_SCALAR : ROPE_SCALAR, 0, 1);
+      return n;
+    }
+    case TRI_OP_SWIGLU:
+      if (P.variant == SW_FLAT || P.variant == SW_FLAT_NT) {
+        out[n++] = single(P.variant == SW_FLAT ? SW_FLAT_NT : SW_FLAT, 0, 1);
+        if (key_I(k) % v == 0) out[n++] = single(SW_ROWS, 0, 1);
+      }
+      return n;
+    case TRI_OP_SILU:
+    case TRI_OP_ADD:
+    case TRI_OP_MASKED_FILL:
+      if (P.variant == ELT_FLAT || P.variant == ELT_FLAT_U2) {
+        out[n++] = single(P.variant == ELT_FLAT ? ELT_FLAT_U2 : ELT_FLAT, int32_t(op), 1);
+        if (key_H(k) % v == 0) out[n++] = single(ELT_ROWS, int32_t(op), 1);
+      }
+      return n;
+    case TRI_OP_CHAIN:
+      break;
+    default:
+      return n;
+  }
+  if (P.variant != CH_FUSED) return n;
+  int32_t r[3], s[4];
+  const int nr = rn_options(dt, key_H(k), fl & 3u, false, r);
+  const int ns = slice_options(P.rope_slices, b, s);
+  const int32_t sw0 = P.roles[2], sw1 = sw0 == SW_FLAT ? SW_FLAT_NT : SW_FLAT;
+  n = 0;
+  for (int i = 0; i < nr; ++i)
+    for (int j = 0; j < ns; ++j)
+      for (int32_t w : {sw0, sw1}) {
+        Plan c{};
+        c.variant = CH_FUSED;
+        c.roles[0] = r[i];
+        c.roles[1] = P.roles[1];
+        c.roles[2] = w;
+        c.n_launches = 1;
+        c.kvariant[0] = CH_FUSED;
+        c.ksub[0] = fused_sub(r[i], P.roles[1], w);
+        c.rope_slices = s[j];
+        out[n++] = c;
+      }
+  Plan q{};
+  q.variant = CH_SEQ;
+  q.roles[0] = P.roles[0];
+  q.roles[1] = P.roles[1];
+  q.roles[2] = P.roles[2];
+  q.n_launches = 3;
+  q.kvariant[0] = P.roles[0];
+  q.ksub[0] = 1;
+  q.kvariant[1] = P.roles[1];
+  q.kvariant[2] = P.roles[2];
+  q.rope_slices = P.rope_slices;
+  out[n++] = q;
+  return n;
 }
 
 }  // namespace tri

@@ -4,6 +4,7 @@
 // computes nothing: "kernel handles" encode (variant, dtype, sub), launches
 // are appended to a log with their grid, block and a copy of the argument
 // block, and a launch can be made to fail on purpose (fault injection).
+#include <stdio.h>
 #include <stdlib.h>
 #include <string.h>
 
@@ -32,6 +33,20 @@ int64_t g_unloads = 0;
 bool g_jit_fail = false;
 int64_t g_captures = 0, g_capture_start = 0, g_graph_launches = 0, g_graph_destroys = 0;
 bool g_capture_fail = false;
+
+// Scripted launch costs of the tuning timer: the last matching entry wins
+// (ksub -1 / grid 0 match any); unmatched launches cost 1 ms.
+struct Cost {
+  int32_t kvariant, ksub;
+  uint32_t grid;
+  float ms;
+};
+std::vector<Cost> g_costs;
+std::vector<int64_t> g_marks;
+int64_t g_timers = 0, g_timer_destroys = 0, g_scratch_allocs = 0, g_scratch_frees = 0;
+uint64_t g_scratch_bytes = 0;
+bool g_scratch_fail = false;
+std::string g_arch = "fake";
 
 uintptr_t encode(int32_t v, uint32_t dt, int32_t sub) {
   return (uintptr_t(uint32_t(v)) << 20) | (uintptr_t(dt) << 16) | uintptr_t(uint32_t(sub) & 0xFFFF) |
@@ -144,6 +159,64 @@ void be_graph_destroy(void *exec) {
   g_graph_destroys++;
 }
 
+// Tuning: "scratch" is a stand-in address (nothing dereferences it); the
+// timer's events mark positions in the launch log and an elapsed time is
+// the scripted cost of the launches between two marks.
+int be_scratch(uint64_t bytes, void *stream, void **dev) {
+  (void)stream;
+  if (g_scratch_fail) return TRI_E_NOMEM;
+  g_scratch_bytes = bytes;
+  g_scratch_allocs++;
+  *dev = reinterpret_cast<void *>(uintptr_t(0x5C0000000000ull));
+  return 0;
+}
+
+void be_scratch_free(void *dev) {
+  (void)dev;
+  g_scratch_frees++;
+}
+
+int be_timer_create(uint32_t n_events, void **timer, void **stream) {
+  g_marks.assign(n_events, -1);
+  g_timers++;
+  *timer = reinterpret_cast<void *>(uintptr_t(0x71000000u) + uintptr_t(g_timers));
+  *stream = reinterpret_cast<void *>(uintptr_t(0x72000000u) + uintptr_t(g_timers));
+  return 0;
+}
+
+int be_timer_record(void *timer, uint32_t i) {
+  (void)timer;
+  if (i >= g_marks.size()) return TRI_E_INVALID;
+  g_marks[i] = int64_t(g_log.size());
+  return 0;
+}
+
+float launch_cost(const Rec &r) {
+  float c = 1.0f;
+  for (const Cost &k : g_costs)
+    if (k.kvariant == r.kvariant && (k.ksub < 0 || k.ksub == r.ksub) &&
+        (k.grid == 0 || k.grid == r.grid))
+      c = k.ms;
+  return c;
+}
+
+int be_timer_elapsed(void *timer, uint32_t i, uint32_t j, float *ms) {
+  (void)timer;
+  if (i >= g_marks.size() || j >= g_marks.size() || g_marks[i] < 0 || g_marks[j] < 0)
+    return TRI_E_INVALID;
+  float t = 0.0f;
+  for (int64_t n = g_marks[i]; n < g_marks[j]; ++n) t += launch_cost(g_log[size_t(n)]);
+  *ms = t;
+  return 0;
+}
+
+void be_timer_destroy(void *timer) {
+  (void)timer;
+  g_timer_destroys++;
+}
+
+void be_arch(char *out, uint32_t cap) { snprintf(out, cap, "%s", g_arch.c_str()); }
+
 }  // namespace tri
 
 extern "C" {
@@ -159,6 +232,25 @@ void trifake_reset() {
   g_jit_fail = false;
   g_captures = g_capture_start = g_graph_launches = g_graph_destroys = 0;
   g_capture_fail = false;
+  g_costs.clear();
+  g_marks.clear();
+  g_timers = g_timer_destroys = g_scratch_allocs = g_scratch_frees = 0;
+  g_scratch_bytes = 0;
+  g_scratch_fail = false;
+  g_arch = "fake";
+}
+void trifake_set_cost(int32_t kvariant, int32_t ksub, uint32_t grid, float ms) {
+  g_costs.push_back({kvariant, ksub, grid, ms});
+}
+void trifake_scratch_fail(int on) { g_scratch_fail = on != 0; }
+void trifake_set_arch(const char *a) { g_arch = a ? a : ""; }
+// timers created, timers destroyed, scratch allocations, frees, last size
+void trifake_tune_counts(int64_t *out) {
+  out[0] = g_timers;
+  out[1] = g_timer_destroys;
+  out[2] = g_scratch_allocs;
+  out[3] = g_scratch_frees;
+  out[4] = int64_t(g_scratch_bytes);
 }
 int64_t trifake_graph_launches() { return g_graph_launches; }
 int64_t trifake_graph_destroys() { return g_graph_destroys; }

@@ -30,7 +30,7 @@ def ensure_libtri() -> str:
 
 def ensure_fake() -> str:
     srcs = [FAKE_SRC] + [os.path.join(PKG, "csrc", n)
-                         for n in ("api.cpp", "cache.cpp", "policy.cpp", "jit.cpp",
+                         for n in ("api.cpp", "cache.cpp", "policy.cpp", "jit.cpp", "tune.cpp",
                                    "internal.h", "kernargs.h", "kernels/device.h")]
     stale = (not os.path.exists(FAKE_LIB)
              or any(os.path.getmtime(s) > os.path.getmtime(FAKE_LIB) for s in srcs))
@@ -65,6 +65,10 @@ def load_fake():
     lib.trifake_jit_fail.argtypes = [C.c_int]
     lib.trifake_jit_source.restype = C.c_int64
     lib.trifake_jit_source.argtypes = [C.c_int64, C.c_char_p, C.c_int64]
+    lib.trifake_set_cost.argtypes = [C.c_int32, C.c_int32, C.c_uint32, C.c_float]
+    lib.trifake_scratch_fail.argtypes = [C.c_int]
+    lib.trifake_set_arch.argtypes = [C.c_char_p]
+    lib.trifake_tune_counts.argtypes = [C.POINTER(C.c_int64)]
     lib.trifake_get.argtypes = [C.c_int64, C.POINTER(C.c_int32), C.POINTER(C.c_int32),
                                 C.POINTER(C.c_int32), C.POINTER(C.c_uint32),
                                 C.POINTER(C.c_uint32), C.POINTER(C.c_void_p),
