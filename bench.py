@@ -117,9 +117,10 @@ def measured_traffic():
     return float(fields["chain_traffic_bytes"])
 
 
-def run_mixed_stream(tri, wl, bench, dev, stream, torch):
+def run_mixed_stream(tri, wl, bench, dev, stream, torch, autotune=False):
     """The 10,000-call mixed stream: token counts 1..512, 90 % bf16, 5 % unaligned
-    or padded layouts, through a fresh cache; every call synchronised."""
+    or padded layouts, through a fresh cache (installs timed and tuned with
+    `autotune`); every call synchronised."""
     Tmax = max(wl.MIXED_T_CHOICES)
     H, I, nq, nk, hd = wl.MIXED_H, wl.MIXED_I, wl.MIXED_NQ, wl.MIXED_NK, wl.MIXED_HD
     calls = wl.mixed_stream()
@@ -137,7 +138,7 @@ def run_mixed_stream(tri, wl, bench, dev, stream, torch):
         return torch.randn(shape, device=dev).to(td)
 
     arr = (tri.ChainArgs * len(calls))()
-    cache = tri.SpecCache()
+    cache = tri.SpecCache(autotune=autotune)
     for i, (T, dt, layout) in enumerate(calls):
         if (dt, layout) not in bufs:
             td = torch.bfloat16 if dt == wl.BF16 else torch.float32
@@ -166,8 +167,19 @@ def run_mixed_stream(tri, wl, bench, dev, stream, torch):
         if not m:
             per_bucket.setdefault(T, []).append(t)
     miss_t = [t for t, m in zip(e2e, missed) if m]
+    infos = [cache.version_info(i) for i in range(stats["n_versions"])]
+    tuning = None
+    if autotune:
+        tuning = {"versions_tuned": sum(v.tuned == 1 for v in infos),
+                  "kept_another_candidate": sum(v.candidate != 0 for v in infos),
+                  "tune_ms": summary([v.tune_ms for v in infos if v.tuned == 1]),
+                  "kept": {str(T): sorted({(v.candidate, v.n_candidates) for v in infos
+                                           if 1 << ((v.key[0] >> 16) & 0xFF) == T})
+                           for T in wl.MIXED_T_CHOICES}}
+    torch.cuda.synchronize()
+    cache.close()
     return {
-        "calls": n, "misses": sum(missed), "versions": stats["n_versions"],
+        "calls": n, "misses": sum(missed), "versions": stats["n_versions"], "tuning": tuning,
         "user_level_hit_rate": 1.0 - sum(missed) / n,
         "hit_e2e_us_by_tokens": {str(T): {"median": summary(v)["median"],
                                            "p90": summary(v)["p90"], "n": len(v)}
@@ -423,6 +435,23 @@ def main():
 
     # ---- mixed-shape stream: guard hits, misses, latency per token bucket ---------------
     mixed = None if args.no_stream else run_mixed_stream(tri, wl, bench, dev, stream, torch)
+    mixed_tuned = None if args.no_stream else run_mixed_stream(tri, wl, bench, dev, stream,
+                                                               torch, autotune=True)
+
+    # ---- the 1-token chain through a tuning cache --------------------------------------
+    tc = tri.SpecCache(autotune=True)
+    argst, _outst = tc.chain_args(d["x"], d["residual"], d["w"], d["q"], d["k"], d["pos"],
+                                  d["gate"], d["up"], cfg.eps, cfg.base)
+    tc.decode_chain_args(argst, stream)
+    torch.cuda.synchronize()
+    st = bench.trib_latency(tc.handle, 0, C.byref(argst), sptr, W, n2, e2e, hst)
+    assert st == 0, st
+    vt = tc.version_info(0)
+    latency["autotuned_chain"] = {"chain_e2e_us": summary(list(e2e[:n2])),
+                                  "kept_candidate": vt.candidate,
+                                  "n_candidates": vt.n_candidates, "tune_ms": vt.tune_ms}
+    torch.cuda.synchronize()
+    tc.close()
 
     # ---- 8192-token prefill: HBM bandwidth ------------------------------------------
     bandwidth, roofline = None, None
@@ -523,6 +552,7 @@ def main():
                          f"{os.cpu_count()} logical CPUs visible"}
 
     latency["mixed_stream"] = mixed
+    latency["mixed_stream_autotuned"] = mixed_tuned
     line = {
         "metric": METRIC, "value": ce["median"], "unit": "µs", "n_gpus": 1, "steps": K,
         "warmup": W, "ms_per_step": wall * 1e3 / K, "higher_is_better": False,
