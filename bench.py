@@ -209,6 +209,7 @@ def main():
                                  C.POINTER(C.c_double)]
     bench.trib_stream.argtypes = [C.c_void_p, C.c_void_p, C.c_int, C.c_void_p,
                                   C.POINTER(C.c_double), C.POINTER(C.c_int)]
+    bench.trib_copy.argtypes = [C.c_void_p, C.c_void_p, C.c_int64, C.c_int, C.c_void_p]
     stream = torch.cuda.Stream(device=dev)
     sptr = stream.cuda_stream
 
@@ -500,6 +501,12 @@ def main():
             "embedding": lambda: cb.embedding(table, ids, out=emb_out, stream=stream),
             "copy_1GiB_torch": lambda: copy_dst.copy_(copy_src),
         }
+        n16 = copy_src.numel() * 2 // 16
+        for form, name in ((0, "copy_1GiB_ref_1vec"), (1, "copy_1GiB_ref_2vec"),
+                           (2, "copy_1GiB_ref_4vec_nt")):
+            ops[name] = (lambda f=form: bench.trib_copy(copy_src.data_ptr(), copy_dst.data_ptr(),
+                                                        n16, f, sptr))
+            nbytes[name] = 2 * copy_src.numel() * 2
         nbytes["copy_1GiB_torch"] = 2 * copy_src.numel() * 2
         bandwidth = {}
         for name, fn in ops.items():
@@ -523,8 +530,11 @@ def main():
                                "median_us": statistics.median(times), "GB/s": gbs,
                                "frac_of_peak": gbs / HBM_PEAK_GBS}
         ch = bandwidth["chain"]
+        ceiling = max(bandwidth[n]["GB/s"] for n in bandwidth if n.startswith("copy_1GiB_ref"))
+        bandwidth["copy_ceiling_GB/s"] = ceiling
         roofline = {"bound": "hbm", "achieved": ch["GB/s"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                     "frac": ch["GB/s"] / HBM_PEAK_GBS, "traffic": measured_traffic(),
+                    "copy_ceiling_GBs": ceiling, "frac_of_copy_ceiling": ch["GB/s"] / ceiling,
                     "kernel": "fused decode chain, 8192 tokens (k_chain: block-per-row norm, "
                               "one-token RoPE blocks, streaming one-vector SwiGLU)",
                     "bytes_per_launch": ch["bytes"], "avg_launch_us": ch["mean_us"]}
@@ -550,6 +560,22 @@ def main():
                          "1-token Llama-7B shapes, median; host "
                          f"{platform.processor() or platform.machine()}, "
                          f"{os.cpu_count()} logical CPUs visible"}
+        # the other chain configs, for context (same core; the prefill case as a
+        # 512-token slice scaled to 8192 tokens)
+        by_cfg = {}
+        for name, c, T, scale, n_max in (
+                ("tiny_f32", wl.TINY_F32, None, 1, 1000),
+                ("gqa_decode_bf16", wl.GQA_DECODE, None, 1, 1000),
+                ("prefill8k_bf16 (512-token slice x 16)", wl.PREFILL_8K, 512, 16, 3)):
+            inp_c = wl.host_inputs(c, T=T)
+            tc_ = []
+            t_end = time.perf_counter() + 3.0
+            while len(tc_) < n_max and (time.perf_counter() < t_end or len(tc_) < 3):
+                a = time.perf_counter()
+                O.decode_chain(inp_c, c.eps, c.base, c.dtype)
+                tc_.append((time.perf_counter() - a) * 1e6)
+            by_cfg[name] = {"median_us": statistics.median(tc_) * scale, "calls": len(tc_)}
+        cpu["by_config"] = by_cfg
 
     latency["mixed_stream"] = mixed
     latency["mixed_stream_autotuned"] = mixed_tuned
