@@ -174,6 +174,27 @@ def rope_slices(dtype: int, rd: int, interleaved: bool, n_heads: int, b: int,
     return max(1, min(4, cdiv(n_heads * cpb, BLOCK)))
 
 
+def rope_tokens(dtype: int, rd: int, interleaved: bool, n_heads: int, b: int,
+                variant: int) -> int:
+    """Tokens per workgroup of a vector RoPE role beyond decode sizes: when
+    a token's heads fill fewer than 256 lanes (n_heads * cpb), enough
+    tokens to fill them, rounded up to a power of two, at most 4; one at
+    decode sizes and for the scalar roles."""
+    if variant not in ROPE_VEC_ROLES or b <= DECODE_BUCKET_MAX:
+        return 1
+    v = 16 // elem_size(dtype)
+    lanes = n_heads * ((rd if interleaved else rd // 2) // v)
+    if lanes >= BLOCK:
+        return 1
+    return min(4, next_pow2(cdiv(BLOCK, lanes)))
+
+
+def rope_grid(T: int, slices: int, tokens: int) -> int:
+    """Workgroups of a vector RoPE role: T * slices with head slices, else
+    ceil(T / tokens)."""
+    return T * slices if slices > 1 else cdiv(T, tokens)
+
+
 def sw_role(dtype: int, I: int, flags: int, b: int, T: int) -> Tuple[int, int]:
     """Flat when aligned and contiguous (nontemporal beyond decode sizes, the
     same as the fused chain's role), vector rows when only the rows are
@@ -617,7 +638,9 @@ def plan(key, T: int):
     nh = f["nq"] + f["nk"]
     if op in (OP_ROPE_QK, OP_QK_NORM_ROPE):
         v, g = rope_role(dt, f["hd"], fl, T, op == OP_QK_NORM_ROPE, f["rd"], inter)
-        g *= rope_slices(dt, f["rd"], inter, nh, b, v)
+        if v in ROPE_VEC_ROLES:
+            g = rope_grid(T, rope_slices(dt, f["rd"], inter, nh, b, v),
+                          rope_tokens(dt, f["rd"], inter, nh, b, v))
         return v, (0, 0, 0), [(v, g, BLOCK)]
     if op == OP_SWIGLU:
         v, g = sw_role(dt, f["I"], fl, b, T)
@@ -630,7 +653,9 @@ def plan(key, T: int):
         return v, (0, 0, 0), [(v, g, BLOCK)]
     rn = rn_role(dt, f["H"], fl & 3, T)
     ro = rope_role(dt, f["hd"], (fl >> 2) & 3, T, bool(fl & CHAIN_QK_NORM), f["rd"], inter)
-    ro = (ro[0], ro[1] * rope_slices(dt, f["rd"], inter, nh, b, ro[0]))
+    if ro[0] in ROPE_VEC_ROLES:
+        ro = (ro[0], rope_grid(T, rope_slices(dt, f["rd"], inter, nh, b, ro[0]),
+                               rope_tokens(dt, f["rd"], inter, nh, b, ro[0])))
     sw = sw_role(dt, f["I"], (fl >> 4) & 3, b, T)
     roles = (rn[0], ro[0], sw[0])
     fused = ((fl & 0x3F) == 0x3F
@@ -661,18 +686,25 @@ TUNE_NONE, TUNE_MEASURED, TUNE_STORED, TUNE_SKIPPED = 0, 1, 2, 3
 @dataclasses.dataclass(frozen=True)
 class Cand:
     """One candidate plan: the version's variant, the chain's roles, the
-    kernel of each launch and the RoPE role's workgroups per token."""
+    kernel of each launch, the RoPE role's workgroups per token (slices) and
+    tokens per workgroup."""
     variant: int
     roles: Tuple[int, int, int]
     kernels: Tuple[int, ...]
     slices: int
+    tokens: int = 1
 
 
-def _slice_options(S: int, b: int) -> List[int]:
-    """The policy's slice count first, then 1, 2, 4 (up to bucket 13)."""
-    if b > SLICE_BUCKET_MAX:
-        return [S]
-    return [S] + [s for s in SLICE_CHOICES if s != S]
+def _geometry_options(S: int, P: int, b: int) -> List[Tuple[int, int]]:
+    """(slices, tokens per workgroup) of a vector RoPE role, the policy's
+    first. Decode sizes: slice counts 1, 2, 4. Beyond: tokens per workgroup
+    1, 2, 4, then (up to bucket 13) 2 and 4 slices of one token."""
+    if b <= DECODE_BUCKET_MAX:
+        return [(S, 1)] + [(s, 1) for s in SLICE_CHOICES if s != S]
+    out = [(1, P)] + [(1, p) for p in SLICE_CHOICES if p != P]
+    if b <= SLICE_BUCKET_MAX:
+        out += [(2, 1), (4, 1)]
+    return out
 
 
 def _rn_options(dt: int, H: int, fl: int, standalone: bool) -> List[int]:
@@ -701,12 +733,12 @@ def candidates(key) -> List[Cand]:
 
     * RMSNorm rows: the policy's register layout, the workgroup layout when
       the policy takes a wavefront, the two-pass loop.
-    * RoPE with a vector role: the vector kernel at each slice option, then
-      the scalar kernel.
+    * RoPE with a vector role: the vector kernel at each geometry option
+      (_geometry_options), then the scalar kernel.
     * SwiGLU / silu / add / masked_fill, flat: the policy's flat form, the
       other flat form (cached / nontemporal, one / two vectors per
       work-item), vector rows when a row is a whole number of vectors.
-    * The fused chain: every combination of norm role options x slice
+    * The fused chain: every combination of norm role options x geometry
       options x SwiGLU flat forms (nested in that order, each list starting
       with the policy's choice), then the three-launch sequence of the
       policy's roles.
@@ -726,8 +758,10 @@ def candidates(key) -> List[Cand]:
         if P not in ROPE_VEC_ROLES:
             return [Cand(P, z, (P,), 1)]
         S = rope_slices(dt, f["rd"], inter, nh, b, P)
+        Pt = rope_tokens(dt, f["rd"], inter, nh, b, P)
         sc = ROPE_QKN_SCALAR if qkn else ROPE_SCALAR
-        return [Cand(P, z, (P,), s) for s in _slice_options(S, b)] + [Cand(sc, z, (sc,), 1)]
+        return [Cand(P, z, (P,), s, t) for s, t in _geometry_options(S, Pt, b)] + \
+            [Cand(sc, z, (sc,), 1)]
     if op == OP_SWIGLU:
         P = sw_role(dt, f["I"], fl, b, 1)[0]
         opts = [P]
@@ -746,22 +780,23 @@ def candidates(key) -> List[Cand]:
     variant, roles, _ = plan(key, 1)
     rn, ro, sw = roles
     S = rope_slices(dt, f["rd"], inter, nh, b, ro)
-    seq = Cand(CH_SEQ, roles, roles, S)
+    Pt = rope_tokens(dt, f["rd"], inter, nh, b, ro)
+    seq = Cand(CH_SEQ, roles, roles, S, Pt)
     if variant != CH_FUSED:
         return [seq]
     out = []
     for r in _rn_options(dt, f["H"], fl & 3, False):
-        for s in _slice_options(S, b):
+        for s, t in _geometry_options(S, Pt, b):
             for w in _other(sw, SW_FLAT, SW_FLAT_NT):
-                out.append(Cand(CH_FUSED, (r, ro, w), (CH_FUSED,), s))
+                out.append(Cand(CH_FUSED, (r, ro, w), (CH_FUSED,), s, t))
     return out + [seq]
 
 
-def grid_of(variant: int, dt: int, T: int, width: int, slices: int = 1) -> int:
+def grid_of(variant: int, dt: int, T: int, width: int, slices: int = 1, tokens: int = 1) -> int:
     """Workgroups a kernel variant launches for T tokens (width: SwiGLU's I,
     a short op's row width). Wavefront norm rows: 4 rows per workgroup;
     other norm and RoPE kernels: one workgroup per row or token (vector RoPE:
-    times its slices); flat kernels: one 16-byte vector per work-item (two
+    times its slices, or per `tokens` tokens); flat kernels: one 16-byte vector per work-item (two
     for ELT_FLAT_U2); row kernels: the row's vectors over 256 work-items,
     per row; element-wise kernels: one element per work-item. Flat, row and
     element-wise grids are capped at GRID_CAP (grid-stride beyond)."""
@@ -772,7 +807,7 @@ def grid_of(variant: int, dt: int, T: int, width: int, slices: int = 1) -> int:
             variant in RN_BLOCK.values():
         return T
     if variant in ROPE_VEC_ROLES:
-        return T * slices
+        return rope_grid(T, slices, tokens)
     if variant in (SW_FLAT, SW_FLAT_NT, ELT_FLAT):
         return max(1, min(cdiv((T * width) // v, BLOCK), GRID_CAP))
     if variant == ELT_FLAT_U2:
@@ -793,11 +828,12 @@ def cand_plan(key, c: Cand, T: int):
     dt = f["dtype"]
     width = f["H"] if f["op"] in SHORT_OPS else f["I"]
     if c.variant == CH_FUSED:
-        g = (grid_of(c.roles[0], dt, T, width) + grid_of(c.roles[1], dt, T, width, c.slices)
+        g = (grid_of(c.roles[0], dt, T, width)
+             + grid_of(c.roles[1], dt, T, width, c.slices, c.tokens)
              + grid_of(c.roles[2], dt, T, width))
         return CH_FUSED, c.roles, [(CH_FUSED, g, BLOCK)]
-    launches = [(kv, grid_of(kv, dt, T, width, c.slices if kv in ROPE_VEC_ROLES else 1), BLOCK)
-                for kv in c.kernels]
+    launches = [(kv, grid_of(kv, dt, T, width, c.slices, c.tokens) if kv in ROPE_VEC_ROLES
+                 else grid_of(kv, dt, T, width), BLOCK) for kv in c.kernels]
     return c.variant, c.roles, launches
 
 

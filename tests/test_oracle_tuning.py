@@ -54,18 +54,57 @@ def test_tiny_f32_chain_candidates():
 
 
 def test_prefill_chain_candidates():
-    # Bucket 13: policy RN_BLOCK_4 (15), one slice, SwiGLU nontemporal (42);
-    # the slice alternatives still apply at bucket 13.
+    # Bucket 13: policy RN_BLOCK_4 (15), one token per RoPE workgroup (72
+    # heads x 8 lanes fill 576 lanes), SwiGLU nontemporal (42). Geometry
+    # options beyond decode sizes: 1, 2, 4 tokens per workgroup, then 2 and 4
+    # slices (up to bucket 13).
     k = key_of(chain_call(BF, 8192, 8192, 28672, 64, 8, 128, base=500000.0))
-    want = [Cand(50, (15, 31, w), (50,), s) for s in (1, 2, 4) for w in (42, 41)]
-    want.append(Cand(51, (15, 31, 42), (15, 31, 42), 1))
+    geo = [(1, 1), (1, 2), (1, 4), (2, 1), (4, 1)]
+    want = [Cand(50, (15, 31, w), (50,), s, t) for s, t in geo for w in (42, 41)]
+    want.append(Cand(51, (15, 31, 42), (15, 31, 42), 1, 1))
     assert S.candidates(k) == want
+    # RoPE grids at 8192 tokens: 8192, 4096, 2048, 16384, 32768
+    assert [S.cand_plan(k, c, 8192)[2][0][1] - 8192 - 114688 for c in want[:10:2]] == \
+        [8192, 4096, 2048, 16384, 32768]
 
 
 def test_slices_fixed_beyond_bucket_13():
     k = key_of(chain_call(BF, 8193, 8192, 28672, 64, 8, 128, base=500000.0))
-    assert [c.slices for c in S.candidates(k)] == [1, 1, 1]
-    assert [c.roles[2] for c in S.candidates(k)] == [42, 41, 42]
+    assert [c.slices for c in S.candidates(k)] == [1] * 7
+    assert [c.tokens for c in S.candidates(k)] == [1, 1, 2, 2, 4, 4, 1]
+    assert [c.roles[2] for c in S.candidates(k)] == [42, 41, 42, 41, 42, 41, 42]
+
+
+@pytest.mark.parametrize("nq,nk,hd,dtype,b,want", [
+    (8, 1, 128, BF, 13, 4),        # 9 heads x 8 lanes = 72 lanes: 256 / 72 -> 4
+    (8, 8, 128, BF, 13, 2),        # 128 lanes -> 2
+    (9, 9, 128, BF, 7, 2),         # 144 lanes -> ceil(1.8) = 2
+    (16, 16, 128, BF, 7, 1),       # 256 lanes: full
+    (64, 8, 128, BF, 13, 1),       # 576 lanes
+    (4, 4, 64, F, 9, 4),           # f32 hd 64: 8 heads x 8 lanes = 64 -> 4
+    (8, 1, 128, BF, 6, 1),         # decode sizes: one token per workgroup
+    (1, 0, 16, BF, 10, 4),         # one head of one vector
+])
+def test_rope_tokens_worked_by_hand(nq, nk, hd, dtype, b, want):
+    T = 1 << b
+    f = S.unpack_key(key_of(rope_call(dtype, T, nq, nk, hd)))
+    assert f["bucket"] == b
+    assert S.rope_tokens(dtype, hd, False, nq + nk, b, S.ROPE_VEC) == want
+    assert S.rope_tokens(dtype, hd, False, nq + nk, b, S.ROPE_SCALAR) == 1
+    # the RoPE op's grid at T tokens
+    assert S.plan(key_of(rope_call(dtype, T, nq, nk, hd)), T)[2] == \
+        [(S.ROPE_VEC, -(-T // want), 256)]
+
+
+def test_tp8_shard_chain_policy():
+    # One GPU's share of the 8192-token prefill under 8-way tensor
+    # parallelism: norm rows (8192) + RoPE 4 tokens per workgroup (2048) +
+    # SwiGLU 8192 * 3584 / 8 / 256 = 14336 workgroups.
+    k = key_of(chain_call(BF, 8192, 8192, 3584, 8, 1, 128, base=5e5))
+    assert S.plan(k, 8192) == (S.CH_FUSED, (15, 31, 42), [(50, 8192 + 2048 + 14336, 256)])
+    # tiny f32 at 512 tokens: wavefront rows 128 + RoPE 128 + SwiGLU 344
+    k = key_of(chain_call(F, 512, 256, 688, 4, 4, 64))
+    assert S.plan(k, 512) == (S.CH_FUSED, (11, 31, 42), [(50, 128 + 128 + 344, 256)])
 
 
 def test_qwen3_chain_candidates_keep_the_qk_norm_role():
@@ -179,7 +218,10 @@ def test_candidates_meet_kernel_requirements(call):
         assert S.cand_plan(k, cands[0], T) == S.plan(k, T)
     assert len(set(cands)) == len(cands)                       # no duplicates
     for c in cands:
-        assert 1 <= c.slices <= 4
+        assert 1 <= c.slices <= 4 and c.tokens in (1, 2, 4)
+        assert c.slices == 1 or c.tokens == 1
+        if c.tokens > 1:
+            assert f["bucket"] > S.DECODE_BUCKET_MAX
         if c.variant == S.CH_FUSED:
             rn, ro, sw = c.roles
             assert f["flags"] & 0x3F == 0x3F
@@ -211,8 +253,9 @@ def test_candidate_counts_are_bounded():
     worst = 0
     for call in _zoo():
         worst = max(worst, len(S.candidates(key_of(call))))
-    # 2 norm layouts x 4 slice options x 2 SwiGLU forms + the sequence
-    assert worst <= 17
+
+    # beyond decode sizes: 2 norm layouts x 5 geometries x 2 SwiGLU forms + 1
+    assert worst <= 21
 
 
 # ---- the choice rule -------------------------------------------------------------------
