@@ -529,6 +529,37 @@ def main():
             bandwidth[name] = {"bytes": nbytes[name], "mean_us": mean_us,
                                "median_us": statistics.median(times), "GB/s": gbs,
                                "frac_of_peak": gbs / HBM_PEAK_GBS}
+        # one GPU's share under 8-way tensor parallelism (replicated norm, split
+        # heads and SwiGLU columns): the same fused kernel at the shard's shape
+        cfs = wl.PREFILL_8K_TP8
+        del db["gate"], db["up"], db["q"], db["k"]
+        ds = wl.device_inputs(cfs, dev)
+        outs_ = torch.empty_like(ds["gate"])
+        a_s, _ = cb.chain_args(ds["x"], ds["residual"], ds["w"], ds["q"], ds["k"], ds["pos"],
+                               ds["gate"], ds["up"], cfs.eps, cfs.base, y=y, residual_out=ro,
+                               out=outs_)
+        with torch.cuda.stream(stream):
+            cb.decode_chain_args(a_s, stream)
+        torch.cuda.synchronize()
+        times = []
+        for _ in range(args.bw_reps):
+            with torch.cuda.stream(stream):
+                flush.sum()
+                s_ev = torch.cuda.Event(enable_timing=True)
+                e_ev = torch.cuda.Event(enable_timing=True)
+                s_ev.record(stream)
+                cb.decode_chain_args(a_s, stream)
+                e_ev.record(stream)
+            e_ev.synchronize()
+            times.append(s_ev.elapsed_time(e_ev) * 1e3)
+        nb_s = algorithmic_bytes(cfs)["chain"]
+        mean_us = statistics.fmean(times)
+        gbs = nb_s / (mean_us * 1e-6) / 1e9
+        bandwidth["chain_tp8_shard"] = {"bytes": nb_s, "mean_us": mean_us,
+                                        "median_us": statistics.median(times), "GB/s": gbs,
+                                        "frac_of_peak": gbs / HBM_PEAK_GBS,
+                                        "workload": cfs.name}
+        del ds, outs_
         ch = bandwidth["chain"]
         ceiling = max(bandwidth[n]["GB/s"] for n in bandwidth if n.startswith("copy_1GiB_ref"))
         bandwidth["copy_ceiling_GB/s"] = ceiling

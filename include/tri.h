@@ -138,7 +138,7 @@ typedef struct tri_version_info {
   int32_t n_candidates;
   int32_t tuned;       /* TRI_TUNE_*                                          */
   float tune_ms;       /* install time spent tuning                          */
-  uint32_t reserved;
+  int32_t rope_tokens; /* tokens per workgroup of the RoPE role (1: one)     */
 } tri_version_info;
 
 /* RoPE variants. A zeroed struct (or a NULL pointer where one is taken) is

@@ -60,7 +60,7 @@ class VersionInfo(C.Structure):
                 ("n_launches", C.c_int32), ("kernels", C.c_int32 * 3),
                 ("rope_slices", C.c_int32), ("candidate", C.c_int32),
                 ("n_candidates", C.c_int32), ("tuned", C.c_int32), ("tune_ms", C.c_float),
-                ("reserved", C.c_uint32)]
+                ("rope_tokens", C.c_int32)]
 
 
 class RopeExt(C.Structure):

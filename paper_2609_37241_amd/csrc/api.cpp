@@ -198,7 +198,7 @@ inline RopeArgs rope_args(const Version &v, void *q, int64_t q_ts, void *kp, int
                           const tri_rope_ext &x, const void *q_w, const void *k_w, float eps) {
   const uint32_t mode = (x.interleaved ? kRopeInterleaved : 0u) |
                         (x.pos_int64 ? kRopePos64 : 0u) | (x.cos_sin ? kRopeCache : 0u) |
-                        rope_slice_bits(v.plan.rope_slices);
+                        rope_geometry_bits(v.plan.rope_slices, v.plan.rope_tokens);
   return RopeArgs{q, nk > 0 ? kp : nullptr, pos, v.d_consts, q_w, (q_w && nk > 0) ? k_w : nullptr,
                   x.cos_sin, q_ts, k_ts, T, x.cos_sin ? x.cos_sin_len : 0, nq, nk, hd,
                   x.rotary_dim ? x.rotary_dim : hd, q_w ? eps : 0.0f, mode};
@@ -321,7 +321,8 @@ int chain_launch(const Version &v, const tri_chain_args &p, void *stream, tri_la
   const SwArgs sw{p.gate, p.up, p.out, p.g_rs, p.u_rs, p.o_rs, T, I,
                   (T * I) / vec_elems(dtype), T * I};
   const uint32_t g0 = role_grid(v.plan.roles[0], dtype, T, I);
-  const uint32_t g1 = role_grid(v.plan.roles[1], dtype, T, I, v.plan.rope_slices);
+  const uint32_t g1 =
+      role_grid(v.plan.roles[1], dtype, T, I, v.plan.rope_slices, v.plan.rope_tokens);
   const uint32_t g2 = role_grid(v.plan.roles[2], dtype, T, I);
 
   if (v.plan.variant == CH_FUSED) {
@@ -532,7 +533,8 @@ tri_status rope_entry(tri_cache *c, uint32_t op, int32_t dtype, void *q, int64_t
   const RopeArgs a =
       rope_args(v, q, q_ts, kp, k_ts, pos, T, nq, nk, hd, x, qkn ? q_w : nullptr, k_w, eps);
   const tri_launch_rec l{v.plan.kvariant[0],
-                         role_grid(v.plan.kvariant[0], uint32_t(dtype), T, 0, v.plan.rope_slices),
+                         role_grid(v.plan.kvariant[0], uint32_t(dtype), T, 0, v.plan.rope_slices,
+                                   v.plan.rope_tokens),
                          kBlock};
   const int rc = be_launch(v.fn[0], l.grid_x, kBlock, &a, sizeof a, stream);
   record(c, op, v, vi, k, 1, &l, rc ? TRI_E_LAUNCH : TRI_OK);

@@ -228,13 +228,16 @@ void fill_selection(const Version &v, int32_t index, int64_t T, tri_selection *o
   for (int i = 0; i < 3; ++i) out->roles[i] = v.plan.roles[i];
   if (v.plan.variant == CH_FUSED) {
     const uint32_t g = role_grid(v.plan.roles[0], dt, T, I) +
-                       role_grid(v.plan.roles[1], dt, T, I, v.plan.rope_slices) +
+                       role_grid(v.plan.roles[1], dt, T, I, v.plan.rope_slices,
+                                 v.plan.rope_tokens) +
                        role_grid(v.plan.roles[2], dt, T, I);
     out->launch[0] = {CH_FUSED, g, kBlock};
   } else {
     for (int i = 0; i < v.plan.n_launches; ++i)
       out->launch[i] = {v.plan.kvariant[i],
-                        role_grid(v.plan.kvariant[i], dt, T, I, v.plan.rope_slices), kBlock};
+                        role_grid(v.plan.kvariant[i], dt, T, I, v.plan.rope_slices,
+                                  v.plan.rope_tokens),
+                        kBlock};
   }
   key_words(k, out->key);
 }
@@ -331,7 +334,7 @@ tri_status tri_spec_version_info(const tri_cache *c, uint32_t index, tri_version
   out->n_candidates = v.n_candidates;
   out->tuned = v.tuned;
   out->tune_ms = v.tune_ms;
-  out->reserved = 0;
+  out->rope_tokens = v.plan.rope_tokens;
   return TRI_OK;
 }
 

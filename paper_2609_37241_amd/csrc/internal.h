@@ -94,16 +94,23 @@ Role rn_role(uint32_t dtype, int64_t H, unsigned flags, int64_t T);
 Role rope_role(uint32_t dtype, int32_t hd, int32_t rd, bool interleaved, unsigned flags, int64_t T,
                bool qk_norm);
 Role sw_role(uint32_t dtype, int64_t I, unsigned flags, uint32_t bucket, int64_t T);
-// Workgroups of a role variant for T tokens; `slices` multiplies the RoPE
-// roles' one workgroup per token.
-uint32_t role_grid(int32_t variant, uint32_t dtype, int64_t T, int64_t I, int32_t slices = 1);
+// Workgroups of a role variant for T tokens; a vector RoPE role takes T *
+// slices workgroups with head slices, else ceil(T / tokens).
+uint32_t role_grid(int32_t variant, uint32_t dtype, int64_t T, int64_t I, int32_t slices = 1,
+                   int32_t tokens = 1);
 // RoPE vector roles at decode sizes split a token's heads over this many
 // workgroups (1 otherwise).
 int32_t rope_slices(uint32_t dtype, int32_t hd, int32_t rd, bool interleaved, int32_t n_heads,
                     uint32_t bucket, int32_t variant);
-// The slice count's bits in RopeArgs::mode (none for one slice).
-inline uint32_t rope_slice_bits(int32_t slices) {
-  return slices > 1 ? uint32_t(slices) << kRopeSliceShift : 0u;
+// RoPE vector roles beyond decode sizes take this many tokens per workgroup
+// (1 at decode sizes).
+int32_t rope_tokens(uint32_t dtype, int32_t rd, bool interleaved, int32_t n_heads,
+                    uint32_t bucket, int32_t variant);
+// The slice count's and tokens per workgroup's bits in RopeArgs::mode
+// (none for one).
+inline uint32_t rope_geometry_bits(int32_t slices, int32_t tokens) {
+  return (slices > 1 ? uint32_t(slices) << kRopeSliceShift : 0u) |
+         (tokens > 1 ? uint32_t(tokens) << kRopeTokensShift : 0u);
 }
 // Element-wise ops (silu, add, masked_fill) over [T, W] and embedding rows.
 Role elt_role(uint32_t dtype, int64_t W, unsigned flags, uint32_t bucket, int64_t T);
@@ -117,6 +124,7 @@ struct Plan {
   int32_t kvariant[3];    // kernel variant per launch
   int32_t rope_slices;    // workgroups per token of the RoPE role (vector forms)
   int32_t ksub[3];        // kernel sub-selector (residual flag / fused template index)
+  int32_t rope_tokens;    // tokens per workgroup of the RoPE role (vector forms)
                           // fused: (role norm variant - RN_WAVE_1) * 8
                           //        + (GPT-J pairs) * 4
                           //        + (QK-RMSNorm before RoPE) * 2

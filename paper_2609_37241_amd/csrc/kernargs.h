@@ -12,9 +12,11 @@ namespace tri {
 
 // RoPE variant bits: RopeArgs::mode, and key word 3 above the 16-bit rotary
 // dim. Bits 8..15 of RopeArgs::mode: workgroups per token of the vector
-// forms (0 or 1: one).
+// forms; bits 16..23: tokens per workgroup of the vector forms (0 or 1 in
+// either: one; at most one of the two is above one).
 constexpr uint32_t kRopeInterleaved = 1, kRopePos64 = 2, kRopeCache = 4;
-constexpr uint32_t kRopeSliceShift = 8;
+constexpr uint32_t kRopeSliceShift = 8, kRopeTokensShift = 16;
+constexpr int kRopeTokensMax = 4;
 
 // Residual add + RMSNorm and plain RMSNorm ([T, H] rows, element strides).
 struct RnArgs {

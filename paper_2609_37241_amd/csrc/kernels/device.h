@@ -370,9 +370,11 @@ __device__ __forceinline__ char *rope_head(const RopeArgs &a, int64_t t, int h, 
                   : static_cast<char *>(a.k) + (t * a.k_ts + int64_t(h - a.nq) * a.hd) * es;
 }
 
-// TPB tokens per workgroup (with TPB == 1 a token's heads may also be
-// split round-robin over S = slices workgroups: workgroup blk takes token
-// blk / S and heads s, s + S, s + 2S, ... with s = blk % S); P2 = rd/2 angle
+// tpb tokens per workgroup (mode bits 16..23, at most kRopeTokensMax; `lds`
+// holds 2 * 256 * kRopeTokensMax floats); with one token per workgroup a
+// token's heads may instead be split round-robin over S = slices workgroups
+// (mode bits 8..15: workgroup blk takes token blk / S and heads s, s + S,
+// s + 2S, ... with s = blk % S). P2 = rd/2 angle
 // pairs per token (a power of two). Rotate-half (INTER false): each half of the rotated span is
 // cpb = P2/V 16-byte vectors and a work-item holds chunk c of both halves;
 // GPT-J pairs (INTER true): the span is cpb = rd/V vectors of V/2 adjacent
@@ -390,7 +392,7 @@ __device__ __forceinline__ char *rope_head(const RopeArgs &a, int64_t t, int h, 
 // item is valid depends only on the work-item's head group, so the lanes of
 // a group skip or process an item together and every lane a reduction reads
 // from is active. cpb <= 64 (the policy guarantees it).
-template <int DT, int TPB, bool NT, int PF = 4, bool QKN = false, bool INTER = false>
+template <int DT, bool NT, int PF = 4, bool QKN = false, bool INTER = false>
 __device__ __forceinline__ void rope_vec_block(const RopeArgs &a, int64_t blk, float *lds) {
   using E = Elt<DT>;
   constexpr int V = E::V;
@@ -400,15 +402,18 @@ __device__ __forceinline__ void rope_vec_block(const RopeArgs &a, int64_t blk, f
   const int shift = __builtin_ctz(unsigned(cpb));
   const int chunk = threadIdx.x & (cpb - 1);
   const int nh = a.nq + a.nk;
-  const int S = TPB == 1 && (a.mode >> kRopeSliceShift) > 1 ? int(a.mode >> kRopeSliceShift) : 1;
+  const int tb = int((a.mode >> kRopeTokensShift) & 0xFFu);
+  const int tpb = tb < 1 ? 1 : (tb > kRopeTokensMax ? kRopeTokensMax : tb);
+  const int sb = int((a.mode >> kRopeSliceShift) & 0xFFu);
+  const int S = tpb == 1 && sb > 1 ? sb : 1;
   const int64_t tok_blk = S > 1 ? blk / S : blk;
   const int hg = int(blk - tok_blk * S) + S * int(threadIdx.x >> shift);   // first head
   const int hstep = S * (kThreads >> shift);
-  const int64_t t0 = tok_blk * TPB;
+  const int64_t t0 = tok_blk * tpb;
   const int64_t tlast = a.T - 1;
   float *cs = lds;
-  float *sn = lds + TPB * 256;
-  const int na = TPB * P2;
+  float *sn = lds + kRopeTokensMax * 256;
+  const int na = tpb * P2;
   // byte offset of the second vector of an item (rotate-half: the other half)
   const int off2 = P2 * E::ES;
 
@@ -448,7 +453,7 @@ __device__ __forceinline__ void rope_vec_block(const RopeArgs &a, int64_t blk, f
   auto gather = [&]() {
 #pragma unroll
     for (int j = 0; j < PF; ++j) {
-      ok[j] = tt < TPB && t0 + tt <= tlast && h < nh;
+      ok[j] = tt < tpb && t0 + tt <= tlast && h < nh;
       it[j] = ok[j] ? tt : 0;
       ih[j] = ok[j] ? h : hfirst;
       const char *b = rope_head(a, t0 + it[j], ih[j], E::ES);
@@ -541,7 +546,7 @@ __device__ __forceinline__ void rope_vec_block(const RopeArgs &a, int64_t blk, f
         st16<NT>(reinterpret_cast<u32x4 *>(b + off2) + chunk, E::pack(o2));
       }
     }
-    if (!(tt < TPB && t0 + tt <= tlast && hg < nh)) break;
+    if (!(tt < tpb && t0 + tt <= tlast && hg < nh)) break;
     gather();
   }
 }
@@ -937,8 +942,8 @@ __device__ __forceinline__ void body_rn_scalar(const RnArgs &a) {
 // QKN: per-head RMSNorm of Q and K before the rotation; INTER: GPT-J pairs.
 template <int DT, bool QKN, bool INTER>
 __device__ __forceinline__ void body_rope_vec(const RopeArgs &a) {
-  __shared__ float lds[2 * 256];
-  rope_vec_block<DT, 1, false, 4, QKN, INTER>(a, blockIdx.x, lds);
+  __shared__ float lds[2 * 256 * kRopeTokensMax];
+  rope_vec_block<DT, false, 4, QKN, INTER>(a, blockIdx.x, lds);
 }
 
 template <int DT, bool QKN>
@@ -1008,13 +1013,13 @@ __device__ __forceinline__ void chain_norm_role(const ChainArgs &a, uint32_t blk
 
 template <int DT, bool WAVE, int N, bool NT, bool QKN, bool INTER>
 __device__ __forceinline__ void body_chain(const ChainArgs &a) {
-  __shared__ float lds[2 * 256];
+  __shared__ float lds[2 * 256 * kRopeTokensMax];
   const uint32_t b = blockIdx.x;
   const uint32_t R = a.rn_blocks, P = a.rope_blocks, S = gridDim.x - R - P;
   if (b < R) {
     chain_norm_role<DT, WAVE, N>(a, b);
   } else if (b < R + P) {
-    rope_vec_block<DT, 1, false, 4, QKN, INTER>(a.rope, b - R, lds);
+    rope_vec_block<DT, false, 4, QKN, INTER>(a.rope, b - R, lds);
   } else {
     sw_flat_part<DT, 1, NT>(a.sw, b - R - P, S);
   }

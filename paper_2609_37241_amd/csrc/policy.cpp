@@ -37,6 +37,10 @@ int32_t pow2_index(int64_t n) {   // n in {1, 2, 4, 8, 16}
   return i;
 }
 
+bool rope_vec_role(int32_t v) {
+  return v == ROPE_VEC || v == ROPE_VEC_I || v == ROPE_QKN_VEC || v == ROPE_QKN_VEC_I;
+}
+
 }  // namespace
 
 // Rows of up to 128 16-byte vectors (2 KiB) take one wavefront each, four
@@ -93,6 +97,20 @@ int32_t rope_slices(uint32_t dtype, int32_t hd, int32_t rd, bool interleaved, in
   return s < 1 ? 1 : (s > 4 ? 4 : int32_t(s));
 }
 
+// Beyond decode sizes a token whose heads fill fewer than 256 lanes
+// (n_heads * cpb) leaves most of a workgroup idle; a workgroup then takes
+// enough tokens to fill its lanes, rounded up to a power of two, at most 4
+// (8192 tokens, 8 + 1 heads of 128 bf16: the fused chain 113.0 vs 122.6 us
+// with one token per workgroup; with 72 heads one token stays fastest).
+int32_t rope_tokens(uint32_t dtype, int32_t rd, bool interleaved, int32_t n_heads,
+                    uint32_t bucket, int32_t variant) {
+  if (!rope_vec_role(variant) || bucket <= kDecodeBucketMax) return 1;
+  const int64_t lanes = int64_t(n_heads) * ((interleaved ? rd : rd / 2) / vec_elems(dtype));
+  if (lanes >= int64_t(kBlock)) return 1;
+  const int64_t t = next_pow2(cdiv(kBlock, lanes));
+  return t > kRopeTokensMax ? kRopeTokensMax : int32_t(t);
+}
+
 // Flat SwiGLU streams nontemporally beyond decode sizes, one vector per
 // work-item, standalone and as the fused chain's role (in the chain this
 // measured 331.5 us at 8192 tokens against 344-349 us with two or four
@@ -141,14 +159,15 @@ Role emb_role(uint32_t dtype, int64_t H, unsigned flags, int64_t T) {
 
 // Workgroups of a role variant for T tokens (I is the SwiGLU width, the
 // row width of an element-wise op, or the embedding row width).
-uint32_t role_grid(int32_t variant, uint32_t dtype, int64_t T, int64_t I, int32_t slices) {
+uint32_t role_grid(int32_t variant, uint32_t dtype, int64_t T, int64_t I, int32_t slices,
+                   int32_t tokens) {
   if (variant == RN_WAVE_1 || variant == RN_WAVE_2) return uint32_t(cdiv(T, 4));
   switch (variant) {
     case RN_SCALAR: case RN_BLOCK_1: case RN_BLOCK_2: case RN_BLOCK_4: case RN_BLOCK_8:
     case RN_BLOCK_16: case RN_LOOP: case ROPE_SCALAR: case ROPE_QKN_SCALAR:
       return uint32_t(T);
     case ROPE_VEC: case ROPE_VEC_I: case ROPE_QKN_VEC: case ROPE_QKN_VEC_I:
-      return uint32_t(T * slices);
+      return slices > 1 ? uint32_t(T * slices) : uint32_t(cdiv(T, tokens < 1 ? 1 : tokens));
     case SW_FLAT: case SW_FLAT_NT: case ELT_FLAT:
       return clamp_grid(cdiv((T * I) / vec_elems(dtype), kBlock));
     case ELT_FLAT_U2:
@@ -175,10 +194,6 @@ int32_t fused_sub(int32_t rn, int32_t rope, int32_t sw) {
   const bool inter = rope == ROPE_VEC_I || rope == ROPE_QKN_VEC_I;
   const bool qkn = rope == ROPE_QKN_VEC || rope == ROPE_QKN_VEC_I;
   return (rn - RN_WAVE_1) * 8 + (inter ? 4 : 0) + (qkn ? 2 : 0) + (sw == SW_FLAT_NT ? 1 : 0);
-}
-
-bool rope_vec_role(int32_t v) {
-  return v == ROPE_VEC || v == ROPE_VEC_I || v == ROPE_QKN_VEC || v == ROPE_QKN_VEC_I;
 }
 
 }  // namespace
@@ -235,6 +250,7 @@ Plan plan_for_key(const Key &k) {
   const uint32_t op = key_op(k), dt = key_dtype(k), b = key_bucket(k), fl = key_flags(k);
   Plan p{};
   p.rope_slices = 1;
+  p.rope_tokens = 1;
   // The grid does not affect the choice of variant; T = 1 stands in here.
   switch (op) {
     case TRI_OP_RMSNORM:
@@ -256,6 +272,8 @@ Plan plan_for_key(const Key &k) {
       p.kvariant[0] = r.variant;
       p.rope_slices = rope_slices(dt, int32_t(key_hd(k)), int32_t(key_rd(k)), inter,
                                   int32_t(key_nq(k) + key_nk(k)), b, r.variant);
+      p.rope_tokens = rope_tokens(dt, int32_t(key_rd(k)), inter, int32_t(key_nq(k) + key_nk(k)),
+                                  b, r.variant);
       return p;
     }
     case TRI_OP_SILU:
@@ -292,6 +310,8 @@ Plan plan_for_key(const Key &k) {
                             (fl & kChainQkNorm) != 0);
   p.rope_slices = rope_slices(dt, int32_t(key_hd(k)), int32_t(key_rd(k)), inter,
                               int32_t(key_nq(k) + key_nk(k)), b, ro.variant);
+  p.rope_tokens = rope_tokens(dt, int32_t(key_rd(k)), inter, int32_t(key_nq(k) + key_nk(k)), b,
+                              ro.variant);
   const Role sw = sw_role(dt, key_I(k), (fl >> 4) & 3u, b, 1);
   p.roles[0] = rn.variant;
   p.roles[1] = ro.variant;
@@ -320,8 +340,9 @@ Plan plan_for_key(const Key &k) {
 // requirements the key also meets: a norm row held by one wavefront can be
 // held by one workgroup (one vector per lane), and a row held in registers
 // can take the two-pass kernel (standalone only); a vector RoPE role can
-// split a token's heads over 1, 2 or 4 workgroups (up to 8192 tokens) or
-// take the scalar kernel; flat SwiGLU and element-wise kernels have a cached
+// take another geometry (at decode sizes 1, 2 or 4 workgroups per token;
+// beyond them 1, 2 or 4 tokens per workgroup, or up to 8192 tokens 2 or 4
+// workgroups per token) or the scalar kernel; flat SwiGLU and element-wise kernels have a cached
 // and a streaming (SwiGLU: nontemporal; element-wise: two vectors per
 // work-item) form and a row form when a row is whole vectors. The fused
 // chain takes every combination of its roles' options (norm, then slices,
@@ -339,23 +360,40 @@ int rn_options(uint32_t dt, int64_t H, unsigned fl, bool standalone, int32_t *ou
   return n;
 }
 
-int slice_options(int32_t S, uint32_t bucket, int32_t *out) {
-  int n = 0;
-  out[n++] = S;
-  if (bucket > kSliceBucketMax) return n;
+// (slices, tokens per workgroup) of a vector RoPE role, the policy's first:
+// at decode sizes slice counts 1, 2, 4; beyond them 1, 2, 4 tokens per
+// workgroup, then (up to bucket 13) 2 and 4 slices of one token.
+struct Geometry {
+  int32_t slices, tokens;
+};
+
+int geometry_options(int32_t S, int32_t P, uint32_t bucket, Geometry *out) {
   const int32_t choices[3] = {1, 2, 4};
+  int n = 0;
+  if (bucket <= kDecodeBucketMax) {
+    out[n++] = {S, 1};
+    for (int32_t c : choices)
+      if (c != S) out[n++] = {c, 1};
+    return n;
+  }
+  out[n++] = {1, P};
   for (int32_t c : choices)
-    if (c != S) out[n++] = c;
+    if (c != P) out[n++] = {1, c};
+  if (bucket <= kSliceBucketMax) {
+    out[n++] = {2, 1};
+    out[n++] = {4, 1};
+  }
   return n;
 }
 
-Plan single(int32_t variant, int32_t sub, int32_t slices) {
+Plan single(int32_t variant, int32_t sub, Geometry g = {1, 1}) {
   Plan p{};
   p.variant = variant;
   p.n_launches = 1;
   p.kvariant[0] = variant;
   p.ksub[0] = sub;
-  p.rope_slices = slices;
+  p.rope_slices = g.slices;
+  p.rope_tokens = g.tokens;
   return p;
 }
 
@@ -372,30 +410,30 @@ int plan_candidates(const Key &k, Plan *out) {
     case TRI_OP_RES_RMSNORM: {
       int32_t r[3];
       const int nr = rn_options(dt, key_H(k), fl, true, r);
-      for (int i = 1; i < nr; ++i) out[n++] = single(r[i], P.ksub[0], 1);
+      for (int i = 1; i < nr; ++i) out[n++] = single(r[i], P.ksub[0]);
       return n;
     }
     case TRI_OP_ROPE_QK:
     case TRI_OP_QK_NORM_ROPE: {
       if (!rope_vec_role(P.variant)) return n;
-      int32_t s[4];
-      const int ns = slice_options(P.rope_slices, b, s);
-      for (int i = 1; i < ns; ++i) out[n++] = single(P.variant, 0, s[i]);
-      out[n++] = single(op == TRI_OP_QK_NORM_ROPE ? ROPE_QKN_SCALAR : ROPE_SCALAR, 0, 1);
+      Geometry g[5];
+      const int ng = geometry_options(P.rope_slices, P.rope_tokens, b, g);
+      for (int i = 1; i < ng; ++i) out[n++] = single(P.variant, 0, g[i]);
+      out[n++] = single(op == TRI_OP_QK_NORM_ROPE ? ROPE_QKN_SCALAR : ROPE_SCALAR, 0);
       return n;
     }
     case TRI_OP_SWIGLU:
       if (P.variant == SW_FLAT || P.variant == SW_FLAT_NT) {
-        out[n++] = single(P.variant == SW_FLAT ? SW_FLAT_NT : SW_FLAT, 0, 1);
-        if (key_I(k) % v == 0) out[n++] = single(SW_ROWS, 0, 1);
+        out[n++] = single(P.variant == SW_FLAT ? SW_FLAT_NT : SW_FLAT, 0);
+        if (key_I(k) % v == 0) out[n++] = single(SW_ROWS, 0);
       }
       return n;
     case TRI_OP_SILU:
     case TRI_OP_ADD:
     case TRI_OP_MASKED_FILL:
       if (P.variant == ELT_FLAT || P.variant == ELT_FLAT_U2) {
-        out[n++] = single(P.variant == ELT_FLAT ? ELT_FLAT_U2 : ELT_FLAT, int32_t(op), 1);
-        if (key_H(k) % v == 0) out[n++] = single(ELT_ROWS, int32_t(op), 1);
+        out[n++] = single(P.variant == ELT_FLAT ? ELT_FLAT_U2 : ELT_FLAT, int32_t(op));
+        if (key_H(k) % v == 0) out[n++] = single(ELT_ROWS, int32_t(op));
       }
       return n;
     case TRI_OP_CHAIN:
@@ -404,13 +442,14 @@ int plan_candidates(const Key &k, Plan *out) {
       return n;
   }
   if (P.variant != CH_FUSED) return n;
-  int32_t r[3], s[4];
+  int32_t r[3];
+  Geometry g[5];
   const int nr = rn_options(dt, key_H(k), fl & 3u, false, r);
-  const int ns = slice_options(P.rope_slices, b, s);
+  const int ng = geometry_options(P.rope_slices, P.rope_tokens, b, g);
   const int32_t sw0 = P.roles[2], sw1 = sw0 == SW_FLAT ? SW_FLAT_NT : SW_FLAT;
   n = 0;
   for (int i = 0; i < nr; ++i)
-    for (int j = 0; j < ns; ++j)
+    for (int j = 0; j < ng; ++j)
       for (int32_t w : {sw0, sw1}) {
         Plan c{};
         c.variant = CH_FUSED;
@@ -420,7 +459,8 @@ int plan_candidates(const Key &k, Plan *out) {
         c.n_launches = 1;
         c.kvariant[0] = CH_FUSED;
         c.ksub[0] = fused_sub(r[i], P.roles[1], w);
-        c.rope_slices = s[j];
+        c.rope_slices = g[j].slices;
+        c.rope_tokens = g[j].tokens;
         out[n++] = c;
       }
   Plan q{};
@@ -434,6 +474,7 @@ int plan_candidates(const Key &k, Plan *out) {
   q.kvariant[1] = P.roles[1];
   q.kvariant[2] = P.roles[2];
   q.rope_slices = P.rope_slices;
+  q.rope_tokens = P.rope_tokens;
   out[n++] = q;
   return n;
 }

@@ -71,7 +71,8 @@ def test_max_tokens_residual_rmsnorm(tri, cache, H):
 
 def test_max_tokens_fused_chain(tri, cache):
     """2^22 tokens through the fused chain: 2^20 norm workgroups (a wavefront
-    per row), 2^22 RoPE workgroups and the SwiGLU role at its grid cap."""
+    per row), 2^20 RoPE workgroups (three heads of one vector fill 3 lanes:
+    four tokens per workgroup) and the SwiGLU role at its grid cap."""
     T, H, I, hd = S.T_MAX, 256, 256, 16
     g = gen(6)
     bf = torch.bfloat16
@@ -88,7 +89,7 @@ def test_max_tokens_fused_chain(tri, cache):
     torch.cuda.synchronize()
     rec = cache.last_selection()
     assert rec.variant == S.CH_FUSED
-    assert rec.launch[0].grid_x == T // 4 + T + min((T * I // 8) // 256, S.GRID_CAP)
+    assert rec.launch[0].grid_x == T // 4 + T // 4 + min((T * I // 8) // 256, S.GRID_CAP)
     rows = torch.from_numpy(sample_rows(T, 40, 2)).to(DEV)
     wy, wh = O.residual_rmsnorm(host(x[rows]), host(res[rows]), host(w), 1e-6, nm.BF16)
     check("y", host(y[rows]), wy, nm.BF16)

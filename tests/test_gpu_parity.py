@@ -514,7 +514,12 @@ MEDIUM = [wl.ChainConfig("medium_bf16", wl.BF16, T=100, H=4096, nq=32, nk=8, hd=
                          rope=(("rotary_dim", 64), ("interleaved", 1))),
           wl.ChainConfig("medium_llama31_qkn_bf16", wl.BF16, T=90, H=4096, nq=32, nk=8, hd=128,
                          I=14336, base=5e5, pos_mode="uniform", pos_max=131071, qk_norm=True,
-                         rope=wl.LLAMA3_SCALING + (("interleaved", 1),))]
+                         rope=wl.LLAMA3_SCALING + (("interleaved", 1),)),
+          # few heads per token: four tokens per RoPE workgroup, ragged last block
+          wl.ChainConfig("tp8_shard_bf16", wl.BF16, T=301, H=8192, nq=8, nk=1, hd=128, I=3584,
+                         base=5e5, pos_mode="uniform", pos_max=8191, outliers=True),
+          wl.ChainConfig("tp8_shard_qkn_f32", wl.F32, T=130, H=1024, nq=4, nk=1, hd=128, I=704,
+                         base=1e6, pos_mode="uniform", pos_max=8191, qk_norm=True)]
 
 
 @pytest.mark.parametrize("cfg", MEDIUM, ids=lambda c: c.name)
@@ -707,15 +712,17 @@ def test_invalid_arguments_raise_and_launch_nothing(tri, cache):
 
 
 # ---- full-size prefill chain, sampled ------------------------------------------------------
-def test_prefill_chain_full_size_sampled(tri, cache):
-    cfg = wl.PREFILL_8K
+@pytest.mark.parametrize("cfg,grid", [(wl.PREFILL_8K, 8192 + 8192 + 114688),
+                                      (wl.PREFILL_8K_TP8, 8192 + 2048 + 14336)],
+                         ids=lambda c: c.name if hasattr(c, "name") else str(c))
+def test_prefill_chain_full_size_sampled(tri, cache, cfg, grid):
     d = wl.device_inputs(cfg, DEV)
     src = {k: v.clone() for k, v in d.items() if k in ("q", "k")}
     y, ro, out = cache.decode_chain(d["x"], d["residual"], d["w"], d["q"], d["k"], d["pos"],
                                     d["gate"], d["up"], cfg.eps, cfg.base)
     torch.cuda.synchronize()
     rec = cache.last_selection()
-    assert rec.variant == S.CH_FUSED and rec.launch[0].grid_x == 8192 + 8192 + 114688
+    assert rec.variant == S.CH_FUSED and rec.launch[0].grid_x == grid
     rows = np.sort(rng(99).choice(cfg.T, size=40, replace=False))
     rows = np.concatenate([[0, 1, 2, 3, cfg.T - 1], rows])
     ri = torch.from_numpy(rows).to(DEV)

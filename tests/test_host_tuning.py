@@ -127,7 +127,7 @@ def test_candidates_and_pinned_selections_match_the_model(lib, fresh):
             assert (v.variant, tuple(v.roles), v.n_launches) == \
                 (want.variant, want.roles, len(want.kernels)), (k, i)
             assert tuple(v.kernels)[:v.n_launches] == want.kernels
-            assert v.rope_slices == want.slices
+            assert (v.rope_slices, v.rope_tokens) == (want.slices, want.tokens)
             assert (v.candidate, v.n_candidates, v.tuned) == (i, len(cands), S.TUNE_NONE)
             assert c_call(lib, cache, c) == S.OK and m.call(c) == S.OK
             assert c_record(lib, cache) == m.last.as_tuple(), (k, i)

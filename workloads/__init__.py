@@ -85,8 +85,14 @@ GPTJ_DECODE = ChainConfig("gptj_decode_bf16", BF16, T=4, H=4096, nq=16, nk=16, h
                           pos_mode="uniform", pos_max=2047,
                           rope=(("rotary_dim", 64), ("interleaved", 1)))
 
+# One GPU's share of the 8192-token prefill under 8-way tensor parallelism:
+# the residual stream and its norm replicated (hidden 8192), the heads and
+# the SwiGLU columns split eight ways (8 Q + 1 K heads, intermediate 3584).
+PREFILL_8K_TP8 = ChainConfig("prefill8k_tp8_shard_bf16", BF16, T=8192, H=8192, nq=8, nk=1, hd=128,
+                             I=3584, base=500000.0, pos_mode="arange", outliers=True)
+
 CONFIGS = {c.name: c for c in (TINY_F32, LLAMA7B_DECODE, GQA_DECODE, PREFILL_8K,
-                               QWEN3_8B_DECODE, LLAMA31_8B_DECODE, GPTJ_DECODE)}
+                               QWEN3_8B_DECODE, LLAMA31_8B_DECODE, GPTJ_DECODE, PREFILL_8K_TP8)}
 
 # Mixed-shape stream: token counts, dtype mix and layout anomalies.
 MIXED_T_CHOICES = (1, 2, 4, 8, 16, 32, 64, 128, 512)
