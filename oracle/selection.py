@@ -25,8 +25,9 @@ The install policy (which kernel variant a key selects and how many
 workgroups a call launches) is restated here from its specification,
 independently of the C++ library; the two must agree bit for bit on every
 selection record. Norm rows of up to 128 16-byte vectors take one wavefront
-each, longer rows one workgroup each; decode-sized calls (token bucket <= 6)
-use cached SwiGLU loads, larger calls stream SwiGLU nontemporally.
+each, longer rows one workgroup each; calls that move at most 320 MiB at the
+top of their token bucket use cached SwiGLU loads, larger calls stream SwiGLU
+nontemporally.
 """
 from __future__ import annotations
 
@@ -195,15 +196,31 @@ def rope_grid(T: int, slices: int, tokens: int) -> int:
     return T * slices if slices > 1 else cdiv(T, tokens)
 
 
-def sw_role(dtype: int, I: int, flags: int, b: int, T: int) -> Tuple[int, int]:
-    """Flat when aligned and contiguous (nontemporal beyond decode sizes, the
-    same as the fused chain's role), vector rows when only the rows are
-    aligned, element-wise otherwise."""
+STREAM_BYTES = 320 << 20     # calls moving more stream SwiGLU nontemporally
+
+
+def call_bytes(key) -> int:
+    """Bytes a call at the top of the key's token bucket moves, each
+    activation read once and each output written once (weights, positions
+    and tables left out): SwiGLU 3 T I elements; the chain 4 T H (norm) +
+    2 T (nq + nk) hd (RoPE, whole heads) + 3 T I (SwiGLU); 0 for other ops."""
+    f = unpack_key(key)
+    T, es = 1 << f["bucket"], elem_size(f["dtype"])
+    if f["op"] == OP_SWIGLU:
+        return 3 * T * f["I"] * es
+    if f["op"] == OP_CHAIN:
+        return T * es * (4 * f["H"] + 2 * (f["nq"] + f["nk"]) * f["hd"] + 3 * f["I"])
+    return 0
+
+
+def sw_role(dtype: int, I: int, flags: int, stream: bool, T: int) -> Tuple[int, int]:
+    """Flat when aligned and contiguous (nontemporal when the call streams,
+    call_bytes > STREAM_BYTES, the same as the fused chain's role), vector
+    rows when only the rows are aligned, element-wise otherwise."""
     v = 16 // elem_size(dtype)
     if (flags & ALIGN) and (flags & CONTIG):
         nvec = (T * I) // v
-        return (SW_FLAT if b <= DECODE_BUCKET_MAX else SW_FLAT_NT), max(1, min(cdiv(nvec, BLOCK),
-                                                                            GRID_CAP))
+        return (SW_FLAT_NT if stream else SW_FLAT), max(1, min(cdiv(nvec, BLOCK), GRID_CAP))
     if (flags & ALIGN) and I % v == 0:
         cb = cdiv(I // v, BLOCK)
         return SW_ROWS, min(T * cb, GRID_CAP)
@@ -643,7 +660,7 @@ def plan(key, T: int):
                           rope_tokens(dt, f["rd"], inter, nh, b, v))
         return v, (0, 0, 0), [(v, g, BLOCK)]
     if op == OP_SWIGLU:
-        v, g = sw_role(dt, f["I"], fl, b, T)
+        v, g = sw_role(dt, f["I"], fl, call_bytes(key) > STREAM_BYTES, T)
         return v, (0, 0, 0), [(v, g, BLOCK)]
     if op in ELT_OPS:
         v, g = elt_role(dt, f["H"], fl, b, T)
@@ -656,7 +673,7 @@ def plan(key, T: int):
     if ro[0] in ROPE_VEC_ROLES:
         ro = (ro[0], rope_grid(T, rope_slices(dt, f["rd"], inter, nh, b, ro[0]),
                                rope_tokens(dt, f["rd"], inter, nh, b, ro[0])))
-    sw = sw_role(dt, f["I"], (fl >> 4) & 3, b, T)
+    sw = sw_role(dt, f["I"], (fl >> 4) & 3, call_bytes(key) > STREAM_BYTES, T)
     roles = (rn[0], ro[0], sw[0])
     fused = ((fl & 0x3F) == 0x3F
              and (rn[0] in RN_WAVE.values() or rn[0] in RN_BLOCK.values())
@@ -763,7 +780,7 @@ def candidates(key) -> List[Cand]:
         return [Cand(P, z, (P,), s, t) for s, t in _geometry_options(S, Pt, b)] + \
             [Cand(sc, z, (sc,), 1)]
     if op == OP_SWIGLU:
-        P = sw_role(dt, f["I"], fl, b, 1)[0]
+        P = sw_role(dt, f["I"], fl, call_bytes(key) > STREAM_BYTES, 1)[0]
         opts = [P]
         if P in (SW_FLAT, SW_FLAT_NT):
             opts = _other(P, SW_FLAT, SW_FLAT_NT) + ([SW_ROWS] if f["I"] % v == 0 else [])

@@ -161,12 +161,32 @@ def test_chain_key_keeps_per_role_flags():
 
 def test_swiglu_flat_grid_cap_and_tail():
     # 3 * 5 = 15 f32 elements: 3 whole vectors + a 3-element tail -> 1 block
-    assert S.sw_role(F, 5, 3, 2, 3) == (S.SW_FLAT, 1)
+    assert S.sw_role(F, 5, 3, False, 3) == (S.SW_FLAT, 1)
     # 1 element: no whole vector, still one block for the tail
-    assert S.sw_role(F, 1, 3, 0, 1) == (S.SW_FLAT, 1)
-    assert S.sw_role(BF, 1 << 30, 3, 10, 1024) == (S.SW_FLAT_NT, S.GRID_CAP)
+    assert S.sw_role(F, 1, 3, False, 1) == (S.SW_FLAT, 1)
+    assert S.sw_role(BF, 1 << 30, 3, True, 1024) == (S.SW_FLAT_NT, S.GRID_CAP)
     # 65 tokens x 1024 bf16: 8320 vectors -> 33 blocks
-    assert S.sw_role(BF, 1024, 3, 7, 65) == (S.SW_FLAT_NT, 33)
+    assert S.sw_role(BF, 1024, 3, True, 65) == (S.SW_FLAT_NT, 33)
+
+
+def test_swiglu_streams_beyond_320_mib():
+    # bytes at the top of the bucket: 3 * T * I * 2 for bf16 SwiGLU
+    MiB = 1 << 20
+    k = S.make_key(sw_call(BF, 2048, 28672))             # 3 * 2048 * 28672 * 2 = 336 MiB
+    assert S.call_bytes(k) == 336 * MiB and S.plan(k, 2048)[0] == S.SW_FLAT_NT
+    k = S.make_key(sw_call(BF, 1500, 28672))             # same bucket (11): 2048 at the top
+    assert S.plan(k, 1500)[0] == S.SW_FLAT_NT
+    k = S.make_key(sw_call(BF, 1024, 28672))             # 168 MiB
+    assert S.call_bytes(k) == 168 * MiB and S.plan(k, 1024)[0] == S.SW_FLAT
+    k = S.make_key(sw_call(BF, 1, 1 << 30))              # one token, 6 GiB: streams
+    assert S.plan(k, 1)[0] == S.SW_FLAT_NT
+    # the chain counts norm rows, whole Q/K heads and SwiGLU: Llama-7B shapes
+    # at 2048 tokens: 2048 * 2 * (4 * 4096 + 2 * 64 * 128 + 3 * 11008) = 263 MiB
+    k = S.make_key(chain_call(BF, 2048, 4096, 11008, 32, 32, 128))
+    assert S.call_bytes(k) == 2048 * 2 * (4 * 4096 + 2 * 64 * 128 + 3 * 11008)
+    assert S.plan(k, 2048)[1][2] == S.SW_FLAT
+    k = S.make_key(chain_call(BF, 4096, 4096, 11008, 32, 32, 128))   # 526 MiB
+    assert S.plan(k, 4096)[1][2] == S.SW_FLAT_NT
 
 
 # ---- Algorithm 1 and the three paths ---------------------------------------------

@@ -102,9 +102,10 @@ def test_tp8_shard_chain_policy():
     # SwiGLU 8192 * 3584 / 8 / 256 = 14336 workgroups.
     k = key_of(chain_call(BF, 8192, 8192, 3584, 8, 1, 128, base=5e5))
     assert S.plan(k, 8192) == (S.CH_FUSED, (15, 31, 42), [(50, 8192 + 2048 + 14336, 256)])
-    # tiny f32 at 512 tokens: wavefront rows 128 + RoPE 128 + SwiGLU 344
+    # tiny f32 at 512 tokens: wavefront rows 128 + RoPE 128 + cached SwiGLU 344
+    # (512 * 4 * (4 * 256 + 2 * 8 * 64 + 3 * 688) bytes: far below 320 MiB)
     k = key_of(chain_call(F, 512, 256, 688, 4, 4, 64))
-    assert S.plan(k, 512) == (S.CH_FUSED, (11, 31, 42), [(50, 128 + 128 + 344, 256)])
+    assert S.plan(k, 512) == (S.CH_FUSED, (11, 31, 41), [(50, 128 + 128 + 344, 256)])
 
 
 def test_qwen3_chain_candidates_keep_the_qk_norm_role():
@@ -158,7 +159,9 @@ def test_rope_candidates():
 
 def test_swiglu_candidates():
     assert [c.variant for c in S.candidates(key_of(sw_call(BF, 1, 11008)))] == [41, 42, 43]
-    assert [c.variant for c in S.candidates(key_of(sw_call(BF, 128, 11008)))] == [42, 41, 43]
+    assert [c.variant for c in S.candidates(key_of(sw_call(BF, 128, 11008)))] == [41, 42, 43]
+    # 4096 tokens x 28672: 672 MiB at the top of the bucket, streaming first
+    assert [c.variant for c in S.candidates(key_of(sw_call(BF, 4096, 28672)))] == [42, 41, 43]
     # f32 rows of 688 = 172 vectors
     assert [c.variant for c in S.candidates(key_of(sw_call(F, 3, 688)))] == [41, 42, 43]
     # rows of 690 f32 are not 16-byte multiples: element-wise only
