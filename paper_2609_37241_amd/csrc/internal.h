@@ -25,8 +25,8 @@ enum Variant : int32_t {
   EMPTY = 99,
 };
 
-// Token buckets up to this one are "decode sized" (cached loads); larger
-// buckets stream SwiGLU nontemporally.
+// Token buckets up to this one are "decode sized": RoPE head slices, one
+// token per RoPE workgroup, one vector per element-wise work-item.
 constexpr uint32_t kDecodeBucketMax = 6;
 
 constexpr uint32_t kBlock = 256;
@@ -93,7 +93,11 @@ struct Role {
 Role rn_role(uint32_t dtype, int64_t H, unsigned flags, int64_t T);
 Role rope_role(uint32_t dtype, int32_t hd, int32_t rd, bool interleaved, unsigned flags, int64_t T,
                bool qk_norm);
-Role sw_role(uint32_t dtype, int64_t I, unsigned flags, uint32_t bucket, int64_t T);
+Role sw_role(uint32_t dtype, int64_t I, unsigned flags, bool stream, int64_t T);
+// Bytes a call at the top of the key's token bucket moves (SwiGLU and the
+// chain; 0 for other ops); SwiGLU streams nontemporally above kStreamBytes.
+uint64_t call_bytes(const Key &k);
+constexpr uint64_t kStreamBytes = uint64_t(320) << 20;
 // Workgroups of a role variant for T tokens; a vector RoPE role takes T *
 // slices workgroups with head slices, else ceil(T / tokens).
 uint32_t role_grid(int32_t variant, uint32_t dtype, int64_t T, int64_t I, int32_t slices = 1,

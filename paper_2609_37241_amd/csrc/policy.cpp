@@ -111,15 +111,32 @@ int32_t rope_tokens(uint32_t dtype, int32_t rd, bool interleaved, int32_t n_head
   return t > kRopeTokensMax ? kRopeTokensMax : int32_t(t);
 }
 
-// Flat SwiGLU streams nontemporally beyond decode sizes, one vector per
-// work-item, standalone and as the fused chain's role (in the chain this
-// measured 331.5 us at 8192 tokens against 344-349 us with two or four
-// vectors per work-item or SwiGLU dispatched first).
-Role sw_role(uint32_t dtype, int64_t I, unsigned flags, uint32_t bucket, int64_t T) {
+// Bytes a call at the top of the key's token bucket moves (activations read
+// once, outputs written once; weights, positions and tables left out):
+// SwiGLU 3 T I elements, the chain 4 T H + 2 T (nq + nk) hd + 3 T I; else 0.
+uint64_t call_bytes(const Key &k) {
+  const uint64_t T = uint64_t(1) << key_bucket(k), es = key_dtype(k) == TRI_F32 ? 4 : 2;
+  const uint32_t op = key_op(k);
+  if (op == TRI_OP_SWIGLU) return 3 * T * key_I(k) * es;
+  if (op == TRI_OP_CHAIN)
+    return T * es *
+           (4 * uint64_t(key_H(k)) + 2 * uint64_t(key_nq(k) + key_nk(k)) * key_hd(k) +
+            3 * uint64_t(key_I(k)));
+  return 0;
+}
+
+// Flat SwiGLU, one vector per work-item, standalone and as the fused
+// chain's role, streams nontemporally when the call moves more than
+// kStreamBytes: below that the operands stay in the 256 MiB last-level
+// cache across back-to-back calls and cached loads win (1-7 % at 128-2048
+// tokens of Llama-shaped chains, 263-277 MB), above it streaming wins (4-7 %
+// at 336-554 MB; in the 8192-token chain 331.5 us against 344-349 us with
+// two or four vectors per work-item or SwiGLU dispatched first).
+Role sw_role(uint32_t dtype, int64_t I, unsigned flags, bool stream, int64_t T) {
   const int64_t v = vec_elems(dtype);
   if ((flags & kAlign) && (flags & kContig)) {
     const int64_t nvec = (T * I) / v;
-    return {bucket <= kDecodeBucketMax ? SW_FLAT : SW_FLAT_NT, clamp_grid(cdiv(nvec, kBlock))};
+    return {stream ? SW_FLAT_NT : SW_FLAT, clamp_grid(cdiv(nvec, kBlock))};
   }
   if ((flags & kAlign) && I % v == 0) {
     const int64_t cb = cdiv(I / v, kBlock);
@@ -295,7 +312,7 @@ Plan plan_for_key(const Key &k) {
       return p;
     }
     case TRI_OP_SWIGLU: {
-      const Role r = sw_role(dt, key_I(k), fl, b, 1);
+      const Role r = sw_role(dt, key_I(k), fl, call_bytes(k) > kStreamBytes, 1);
       p.variant = r.variant;
       p.n_launches = 1;
       p.kvariant[0] = r.variant;
@@ -312,7 +329,7 @@ Plan plan_for_key(const Key &k) {
                               int32_t(key_nq(k) + key_nk(k)), b, ro.variant);
   p.rope_tokens = rope_tokens(dt, int32_t(key_rd(k)), inter, int32_t(key_nq(k) + key_nk(k)), b,
                               ro.variant);
-  const Role sw = sw_role(dt, key_I(k), (fl >> 4) & 3u, b, 1);
+  const Role sw = sw_role(dt, key_I(k), (fl >> 4) & 3u, call_bytes(k) > kStreamBytes, 1);
   p.roles[0] = rn.variant;
   p.roles[1] = ro.variant;
   p.roles[2] = sw.variant;

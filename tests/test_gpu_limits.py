@@ -138,12 +138,14 @@ def test_max_heads_rope(tri, cache, dtype, hd, qkn, unaligned):
     assert cache.last_selection().variant == want
 
 
-@pytest.mark.parametrize("I,variant", [(S.I_LIMIT - 8, S.SW_FLAT), (S.I_LIMIT - 3, S.SW_SCALAR)])
+@pytest.mark.parametrize("I,variant", [(S.I_LIMIT - 8, S.SW_FLAT_NT),
+                                       (S.I_LIMIT - 3, S.SW_SCALAR)])
 def test_widest_swiglu_rows_sampled(tri, cache, I, variant):
     """Two rows of nearly 2^31 elements (2^31 - 3 is the widest accepted):
     element indices past 2^31 and grid-stride passes at the grid cap -- the
-    flat vector form (rows a whole number of vectors), or the element-wise
-    form (odd rows are not 16-byte aligned)."""
+    flat vector form, streaming (rows a whole number of vectors; the call
+    moves 24 GiB), or the element-wise form (odd rows are not 16-byte
+    aligned)."""
     T = 2
     g = gen(7)
     gate = torch.randn((T, I), generator=g, device=DEV, dtype=torch.bfloat16)
