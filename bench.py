@@ -606,6 +606,19 @@ def main():
                 O.decode_chain(inp_c, c.eps, c.base, c.dtype)
                 tc_.append((time.perf_counter() - a) * 1e6)
             by_cfg[name] = {"median_us": statistics.median(tc_) * scale, "calls": len(tc_)}
+        # the first 100 calls of the mixed-shape stream (token counts 1..512, bf16 / f32)
+        mc = []
+        for (T, dt, _layout) in wl.mixed_stream()[:100]:
+            c = wl.ChainConfig("mixed", dt, T=T, H=wl.MIXED_H, nq=wl.MIXED_NQ, nk=wl.MIXED_NK,
+                               hd=wl.MIXED_HD, I=wl.MIXED_I, base=wl.MIXED_BASE,
+                               pos_mode="uniform", pos_max=wl.MIXED_POS_MAX)
+            inp_c = wl.host_inputs(c)
+            a = time.perf_counter()
+            O.decode_chain(inp_c, c.eps, c.base, c.dtype)
+            mc.append((time.perf_counter() - a) * 1e6)
+        by_cfg["mixed_stream (first 100 calls)"] = {"median_us": statistics.median(mc),
+                                                     "mean_us": statistics.fmean(mc),
+                                                     "calls": len(mc)}
         cpu["by_config"] = by_cfg
 
     latency["mixed_stream"] = mixed
