@@ -13,6 +13,13 @@ PKG = os.path.join(ROOT, "paper_2609_37241_amd")
 LIBTRI = os.path.join(PKG, "libtri.so")
 FAKE_SRC = os.path.join(ROOT, "tests", "native", "fake_backend.cpp")
 FAKE_LIB = os.path.join(ROOT, "tests", "native", "libtri_fake.so")
+# With TRI_FAKE_SANITIZE=1 the tests load a build of the same sources with
+# AddressSanitizer and UndefinedBehaviorSanitizer (host code only; the
+# process must preload the sanitizer runtimes, see test_host_sanitized.py).
+SANITIZE = os.environ.get("TRI_FAKE_SANITIZE") == "1"
+FAKE_ASAN_LIB = os.path.join(ROOT, "tests", "native", "libtri_fake_asan.so")
+SANITIZE_FLAGS = ["-g", "-O1", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+                  "-fno-sanitize-recover=undefined"]
 
 
 def _build_module():
@@ -32,11 +39,12 @@ def ensure_fake() -> str:
     srcs = [FAKE_SRC] + [os.path.join(PKG, "csrc", n)
                          for n in ("api.cpp", "cache.cpp", "policy.cpp", "jit.cpp", "tune.cpp",
                                    "internal.h", "kernargs.h", "kernels/device.h")]
-    stale = (not os.path.exists(FAKE_LIB)
-             or any(os.path.getmtime(s) > os.path.getmtime(FAKE_LIB) for s in srcs))
+    out = FAKE_ASAN_LIB if SANITIZE else FAKE_LIB
+    stale = (not os.path.exists(out)
+             or any(os.path.getmtime(s) > os.path.getmtime(out) for s in srcs))
     if stale:
-        _build_module().build_host_core(FAKE_SRC, FAKE_LIB)
-    return FAKE_LIB
+        _build_module().build_host_core(FAKE_SRC, out, SANITIZE_FLAGS if SANITIZE else None)
+    return out
 
 
 def load_fake():
