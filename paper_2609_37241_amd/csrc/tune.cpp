@@ -213,27 +213,18 @@ tri_status issue(tri_cache *c, const TuneCall &tc, void *stream) {
   }
 }
 
-}  // namespace
-
-void tune_key(tri_cache *c, const Key &k, const Plan *cands, int n, const Version &v,
-              int32_t *choice, int32_t *how) {
-  *choice = 0;
-  *how = TRI_TUNE_SKIPPED;
-  TuneCall tc;
-  uint64_t operands = 0;
-  const uint64_t bytes = build_call(k, 256, &tc, &operands);
-  if (n < 2 || n > kMaxCandidates || operands > kTuneScratchMax) return;
-
-  // One private cache per candidate, each holding that candidate's version.
-  Version vs[kMaxCandidates];
-  tri_cache pc[kMaxCandidates];
+// Times candidate j's calls through private one-version caches (one per
+// candidate, so each call hits its own version); returns false on any
+// failure (resolve, timer, memory, a call that does not hit, a timing).
+bool time_candidates(tri_cache *c, const Key &k, const Plan *cands, int n, const Version &v,
+                     TuneCall &tc, uint64_t bytes, Version *vs, tri_cache *pc, float *med) {
   for (int j = 0; j < n; ++j) {
     vs[j] = v;
     vs[j].plan = cands[j];
     for (int i = 0; i < 3; ++i) vs[j].fn[i] = vs[j].module[i] = nullptr;
     for (int i = 0; i < cands[j].n_launches; ++i)
       if (be_resolve(cands[j].kvariant[i], key_dtype(k), cands[j].ksub[i], &vs[j].fn[i]) != 0)
-        return;
+        return false;
     memset(&pc[j], 0, sizeof pc[j]);
     pc[j].capacity = 1;
     pc[j].n_versions = 1;
@@ -245,7 +236,8 @@ void tune_key(tri_cache *c, const Key &k, const Plan *cands, int n, const Versio
 
   const uint32_t n_ev = uint32_t(2 * n * kTuneRounds);
   void *timer = nullptr, *stream = nullptr, *mem = nullptr;
-  if (be_timer_create(n_ev, &timer, &stream) != 0) return;
+  if (be_timer_create(n_ev, &timer, &stream) != 0) return false;
+  uint64_t operands = 0;
   bool ok = be_scratch(bytes, stream, &mem) == 0;
   if (ok) build_call(k, reinterpret_cast<uintptr_t>(mem), &tc, &operands);
   for (int r = 0; ok && r < kTuneWarmup + kTuneRounds; ++r) {
@@ -258,7 +250,6 @@ void tune_key(tri_cache *c, const Key &k, const Plan *cands, int n, const Versio
       if (timed) ok = ok && be_timer_record(timer, e + 1) == 0;
     }
   }
-  float med[kMaxCandidates];
   for (int j = 0; ok && j < n; ++j) {
     float t[kTuneRounds];
     for (int r = 0; ok && r < kTuneRounds; ++r) {
@@ -270,12 +261,36 @@ void tune_key(tri_cache *c, const Key &k, const Plan *cands, int n, const Versio
   }
   be_timer_destroy(timer);   // waits for the stream's work first
   if (mem) be_scratch_free(mem);
-  if (!ok) return;
-  int best = 0;
-  for (int j = 1; j < n; ++j)
-    if (med[j] < med[best]) best = j;
-  *choice = med[best] < kTuneMargin * med[0] ? best : 0;
-  *how = TRI_TUNE_MEASURED;
+  return ok;
+}
+
+}  // namespace
+
+void tune_key(tri_cache *c, const Key &k, const Plan *cands, int n, const Version &v,
+              int32_t *choice, int32_t *how) {
+  *choice = 0;
+  *how = TRI_TUNE_SKIPPED;
+  TuneCall tc;
+  uint64_t operands = 0;
+  const uint64_t bytes = build_call(k, 256, &tc, &operands);
+  if (n < 2 || n > kMaxCandidates || operands > kTuneScratchMax) return;
+  // The private caches are large; they live on the heap, not the stack of
+  // whatever thread installs.
+  struct Private {
+    Version vs[kMaxCandidates];
+    tri_cache pc[kMaxCandidates];
+    float med[kMaxCandidates];
+  };
+  Private *p = static_cast<Private *>(calloc(1, sizeof(Private)));
+  if (!p) return;
+  if (time_candidates(c, k, cands, n, v, tc, bytes, p->vs, p->pc, p->med)) {
+    int best = 0;
+    for (int j = 1; j < n; ++j)
+      if (p->med[j] < p->med[best]) best = j;
+    *choice = p->med[best] < kTuneMargin * p->med[0] ? best : 0;
+    *how = TRI_TUNE_MEASURED;
+  }
+  free(p);
 }
 
 }  // namespace tri
