@@ -41,6 +41,8 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-bandwidth", action="store_true")
     p.add_argument("--no-stream", action="store_true", help="skip the mixed-shape stream")
+    p.add_argument("--latency-only", action="store_true",
+                   help="only the 1-token chain, empty-kernel and issue-rate loops (for traces)")
     return p.parse_args()
 
 
@@ -271,6 +273,9 @@ def main():
                       "grid": sel.launch[0].grid_x, "roles": list(sel.roles)},
         "cache_stats": stats,
     }
+    if args.latency_only:
+        emit(args, ce, wall, latency, None, None, None)
+        return
 
     # ---- context: the same chain as PyTorch eager ops, and HIP-graph replay ---------------
     import torch.nn.functional as F  # noqa: F401
@@ -623,6 +628,12 @@ def main():
 
     latency["mixed_stream"] = mixed
     latency["mixed_stream_autotuned"] = mixed_tuned
+    emit(args, ce, wall, latency, bandwidth, roofline, cpu)
+
+
+def emit(args, ce, wall, latency, bandwidth, roofline, cpu):
+    """Print the one JSON result line."""
+    K, W = args.steps, args.warmup
     line = {
         "metric": METRIC, "value": ce["median"], "unit": "µs", "n_gpus": 1, "steps": K,
         "warmup": W, "ms_per_step": wall * 1e3 / K, "higher_is_better": False,
