@@ -399,6 +399,16 @@ class SpecCache:
             raise TriError(st, f"tri_spec_import_keys (after {done.value} keys)")
         return done.value
 
+    def export_plans(self):
+        """(key, candidate index) of every installed version, creation order:
+        a tuned set of versions that import_plans reinstalls without timing."""
+        return [(k, self.version_info(i).candidate) for i, k in enumerate(self.export_keys())]
+
+    def import_plans(self, plans) -> None:
+        """Install (key, candidate) pairs as exported by export_plans."""
+        for key, cand in plans:
+            self.install_key(key, cand)
+
     def install_key(self, key, candidate: int = -1) -> None:
         """Install one key (6 words) with candidate plan `candidate` (-1: the
         cache's own rule: tuned under autotune, else the policy's plan)."""

@@ -281,3 +281,34 @@ def test_compiled_tuned_plan_equals_the_pinned_precompiled_candidate(tri, cfg):
         torch.cuda.synchronize()
         j.close()
         p.close()
+
+
+def test_tuned_plans_export_and_reinstall_without_timing(tri):
+    """A tuned set of versions (keys + kept candidates) reinstalls in a cache
+    without the tuning flag: same plans, nothing timed, same results."""
+    say("export / import of tuned plans")
+    cases = [CASES[0], CASES[1], CASES[7]] + [c for c in CASES if isinstance(c, EltCase)][:3]
+    a = tri.SpecCache(auto_install=True, autotune=True)
+    b = tri.SpecCache()
+    try:
+        inps = [c.host() for c in cases]
+        outs_a = []
+        for c, inp in zip(cases, inps):
+            outs_a.append(c.run(tri, a, inp))
+        torch.cuda.synchronize()
+        plans = a.export_plans()
+        assert len(plans) == len(cases)
+        b.import_plans(plans)
+        for i, (key, cand) in enumerate(plans):
+            v = b.version_info(i)
+            assert (tuple(v.key), v.candidate, v.tuned) == (tuple(key), cand, S.TUNE_NONE)
+        for c, inp, oa in zip(cases, inps, outs_a):
+            ob = c.run(tri, b, inp)
+            torch.cuda.synchronize()
+            for n in oa:
+                check(n, host(ob[n]), host(oa[n]), c.dtype, exact=True)
+        assert b.stats()["misses"] == 0
+    finally:
+        torch.cuda.synchronize()
+        a.close()
+        b.close()
