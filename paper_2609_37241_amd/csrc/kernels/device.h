@@ -991,9 +991,10 @@ __device__ __forceinline__ void body_emb(const EmbArgs &a) {
 // The fused decode chain: workgroups take the residual-RMSNorm, RoPE-QK and
 // SwiGLU roles by blockIdx range. Norm role: one wavefront per row with N
 // vectors per lane (WAVE) or one workgroup per row with N per work-item;
-// RoPE role: one token (or head slice) per workgroup (QK norm first when
-// QKN, GPT-J pairs when INTER); SwiGLU role: one vector per work-item,
-// nontemporal when NT (streaming sizes).
+// RoPE role: one token, one head slice of a token, or up to four tokens per
+// workgroup, as the argument block's mode says (QK norm first when QKN,
+// GPT-J pairs when INTER); SwiGLU role: one vector per work-item,
+// nontemporal when NT (calls that stream more than the last-level cache).
 //
 // Role order by blockIdx: norm rows, RoPE tokens, then SwiGLU. At decode
 // sizes the norm and RoPE roles take about as long as SwiGLU but have far
