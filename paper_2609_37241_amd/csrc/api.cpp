@@ -356,8 +356,10 @@ inline int check_elt(uint64_t es, int64_t W, const void *a, int64_t a_rs, const 
   return kGo;
 }
 
-// One launch of a single-kernel op: lookup (miss / auto-install), launch
-// with the argument block, record, count.
+// One launch of a single-kernel op (norms, SwiGLU, the short ops): lookup
+// (miss / auto-install), launch with the argument block, record, count.
+// `width` is what role_grid takes as I (SwiGLU's I, a short op's row width;
+// unused by the norm grids).
 tri_status single_launch(tri_cache *c, uint32_t op, const Key &k, int64_t T, int64_t width,
                          const void *args, uint32_t args_size, void *stream) {
   int32_t vi;
@@ -561,17 +563,8 @@ tri_status tri_rmsnorm(tri_cache *c, tri_dtype dtype, const void *x, int64_t x_r
 
   const Key k = make_key(op, dtype, T, rn_flags(es, x, x_rs, w, y, y_rs, H), 0, uint64_t(H), 0,
                          0, 0, 0);
-  int32_t vi;
-  bool auto_inst = false;
-  st = lookup(c, op, k, T, &vi, &auto_inst);
-  if (st != TRI_OK) return tri_status(st);
-  Version &v = c->versions[vi];
-
-  RnArgs a{x, nullptr, w, y, nullptr, x_rs, 0, y_rs, 0, T, int32_t(H), eps};
-  const tri_launch_rec l{v.plan.kvariant[0], role_grid(v.plan.kvariant[0], dtype, T, 0), kBlock};
-  const int rc = be_launch(v.fn[0], l.grid_x, kBlock, &a, sizeof a, stream);
-  record(c, op, v, vi, k, 1, &l, rc ? TRI_E_LAUNCH : TRI_OK);
-  return finish(c, v, auto_inst, rc);
+  const RnArgs a{x, nullptr, w, y, nullptr, x_rs, 0, y_rs, 0, T, int32_t(H), eps};
+  return single_launch(c, op, k, T, 0, &a, sizeof a, stream);
 }
 
 tri_status tri_residual_rmsnorm(tri_cache *c, tri_dtype dtype, const void *x, int64_t x_rs,
@@ -592,17 +585,8 @@ tri_status tri_residual_rmsnorm(tri_cache *c, tri_dtype dtype, const void *x, in
   const Key k = make_key(op, dtype, T,
                          res_flags(es, x, x_rs, res, res_rs, w, y, y_rs, res_out, ro_rs, H), 0,
                          uint64_t(H), 0, 0, 0, 0);
-  int32_t vi;
-  bool auto_inst = false;
-  st = lookup(c, op, k, T, &vi, &auto_inst);
-  if (st != TRI_OK) return tri_status(st);
-  Version &v = c->versions[vi];
-
-  RnArgs a{x, res, w, y, res_out, x_rs, res_rs, y_rs, ro_rs, T, int32_t(H), eps};
-  const tri_launch_rec l{v.plan.kvariant[0], role_grid(v.plan.kvariant[0], dtype, T, 0), kBlock};
-  const int rc = be_launch(v.fn[0], l.grid_x, kBlock, &a, sizeof a, stream);
-  record(c, op, v, vi, k, 1, &l, rc ? TRI_E_LAUNCH : TRI_OK);
-  return finish(c, v, auto_inst, rc);
+  const RnArgs a{x, res, w, y, res_out, x_rs, res_rs, y_rs, ro_rs, T, int32_t(H), eps};
+  return single_launch(c, op, k, T, 0, &a, sizeof a, stream);
 }
 
 tri_status tri_rope_qk_ext(tri_cache *c, tri_dtype dtype, void *q, int64_t q_ts, void *kp,
@@ -642,17 +626,8 @@ tri_status tri_swiglu(tri_cache *c, tri_dtype dtype, const void *gate, int64_t g
 
   const Key k = make_key(op, dtype, T, sw_flags(es, gate, g_rs, up, u_rs, out, o_rs, I), 0, 0,
                          uint64_t(I), 0, 0, 0);
-  int32_t vi;
-  bool auto_inst = false;
-  st = lookup(c, op, k, T, &vi, &auto_inst);
-  if (st != TRI_OK) return tri_status(st);
-  Version &v = c->versions[vi];
-
-  SwArgs a{gate, up, out, g_rs, u_rs, o_rs, T, I, (T * I) / vec_elems(dtype), T * I};
-  const tri_launch_rec l{v.plan.kvariant[0], role_grid(v.plan.kvariant[0], dtype, T, I), kBlock};
-  const int rc = be_launch(v.fn[0], l.grid_x, kBlock, &a, sizeof a, stream);
-  record(c, op, v, vi, k, 1, &l, rc ? TRI_E_LAUNCH : TRI_OK);
-  return finish(c, v, auto_inst, rc);
+  const SwArgs a{gate, up, out, g_rs, u_rs, o_rs, T, I, (T * I) / vec_elems(dtype), T * I};
+  return single_launch(c, op, k, T, I, &a, sizeof a, stream);
 }
 
 tri_status tri_silu(tri_cache *c, tri_dtype dtype, const void *x, int64_t x_rs, void *out,
