@@ -546,6 +546,29 @@ def main():
             bandwidth[name] = {"bytes": nbytes[name], "mean_us": mean_us,
                                "median_us": statistics.median(times), "GB/s": gbs,
                                "frac_of_peak": gbs / HBM_PEAK_GBS}
+        # The same yardstick at each op's own size: the reference copy moving
+        # the op's algorithmic bytes (half read, half written). Shorter runs
+        # pay a larger share of ramp-up and tail, so a 0.27 GB op is held to
+        # what a 0.27 GB copy reaches, not the 2 GiB copy's rate.
+        for name in list(bandwidth):
+            half16 = nbytes[name] // 32
+            if name.startswith("copy_") or half16 > n16:
+                continue
+            times = []
+            for _ in range(args.bw_reps):
+                with torch.cuda.stream(stream):
+                    flush.sum()
+                    s_ev = torch.cuda.Event(enable_timing=True)
+                    e_ev = torch.cuda.Event(enable_timing=True)
+                    s_ev.record(stream)
+                    assert bench.trib_copy(copy_src.data_ptr(), copy_dst.data_ptr(), half16, 0,
+                                           sptr) == 0
+                    e_ev.record(stream)
+                e_ev.synchronize()
+                times.append(s_ev.elapsed_time(e_ev) * 1e3)
+            cgbs = 32 * half16 / (statistics.fmean(times) * 1e-6) / 1e9
+            bandwidth[name]["copy_same_bytes_GB/s"] = cgbs
+            bandwidth[name]["frac_of_copy_same_bytes"] = bandwidth[name]["GB/s"] / cgbs
         # one GPU's share under 8-way tensor parallelism (replicated norm, split
         # heads and SwiGLU columns): the same fused kernel at the shard's shape
         cfs = wl.PREFILL_8K_TP8

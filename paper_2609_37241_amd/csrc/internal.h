@@ -128,11 +128,11 @@ struct Plan {
   int32_t kvariant[3];    // kernel variant per launch
   int32_t rope_slices;    // workgroups per token of the RoPE role (vector forms)
   int32_t ksub[3];        // kernel sub-selector (residual flag / fused template index)
-  int32_t rope_tokens;    // tokens per workgroup of the RoPE role (vector forms)
                           // fused: (role norm variant - RN_WAVE_1) * 8
                           //        + (GPT-J pairs) * 4
                           //        + (QK-RMSNorm before RoPE) * 2
                           //        + (SwiGLU role is SW_FLAT_NT)
+  int32_t rope_tokens;    // tokens per workgroup of the RoPE role (vector forms)
 };
 Plan plan_for_key(const Key &k);
 
