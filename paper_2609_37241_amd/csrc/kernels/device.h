@@ -636,10 +636,19 @@ __device__ __forceinline__ void rope_scalar_block(const RopeArgs &a, int64_t t, 
 // hardware reciprocal (v_rcp_f32, 1 ulp): the correctly rounded float32
 // division costs about ten vector instructions per element, which made the
 // streaming SwiGLU and silu kernels bound by vector ALU throughput rather
-// than by HBM. For g << 0 exp overflows to +inf, rcp gives +0 and the result
-// is a signed zero.
+// than by HBM. Below g = -80, 1 + exp(g) is 1 in float32 and silu(g) is
+// g * exp(g); that form keeps the tail where exp(-g) overflows (from
+// g = -88.7 on) and would flush the product to zero although the value is
+// still a normal float32 down to about g = -91.5. The tail is recomputed
+// only where a lane is in it: a select of both forms costs three more
+// vector instructions per element, which the streaming silu kernel
+// measured as 7 % (it sits close to its vector ALU limit), while the
+// branch is skipped whenever no lane of the wavefront is that negative.
+// At g = -inf the tail gives -inf * 0 = NaN, as -inf / (1 + inf) does.
 __device__ __forceinline__ float silu(float g) {
-  return g * __builtin_amdgcn_rcpf(1.0f + expf(-g));
+  float r = g * __builtin_amdgcn_rcpf(1.0f + expf(-g));
+  if (__builtin_expect(g < -80.0f, 0)) r = g * expf(g);
+  return r;
 }
 
 __device__ __forceinline__ float silu_mul(float g, float u) {

@@ -36,6 +36,34 @@ def check(name, got, want, dtype, exact=False):
                              f"first at {tuple(i)}: got {g[tuple(i)]!r} want {o[tuple(i)]!r}")
 
 
+def f32_ulp_distance(a, b) -> np.ndarray:
+    """Number of representable float32 values between two float32 arrays
+    (sign-magnitude patterns mapped onto a monotone integer line)."""
+    def line(x):
+        i = np.asarray(x, dtype=np.float32).view(np.uint32).astype(np.int64)
+        mag = i & 0x7FFFFFFF
+        return np.where(i & 0x80000000, -mag, mag)
+    return np.abs(line(a) - line(b))
+
+
+def error_stats(got, want, dtype):
+    """Largest |g - o|, largest |g - o| / |o| (over o != 0), largest ulp
+    distance from the oracle's correctly rounded value, and the fraction of
+    elements equal to it bit for bit. Finite oracle values only."""
+    got, want = np.asarray(got), np.asarray(want)
+    g, o = nm.values(got, dtype), nm.values(want, dtype)
+    fin = np.isfinite(o)
+    g, o, got, want = g[fin], o[fin], got[fin], want[fin]
+    err = np.abs(g - o)
+    nz = o != 0
+    ulps = nm.bf16_ulp_distance(got, want) if dtype == nm.BF16 else f32_ulp_distance(got, want)
+    bits = np.uint16 if dtype == nm.BF16 else np.uint32
+    return {"n": int(o.size), "max_abs": float(err.max(initial=0.0)),
+            "max_rel": float((err[nz] / np.abs(o[nz])).max(initial=0.0)),
+            "max_ulp": int(ulps.max(initial=0)),
+            "exact": float(np.mean(got.view(bits) == want.view(bits))) if o.size else 1.0}
+
+
 def dt_code(dtype):
     return S.DT_F32 if dtype == nm.F32 else S.DT_BF16
 

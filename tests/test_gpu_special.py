@@ -192,3 +192,27 @@ def test_embedding_copies_special_rows_bit_for_bit(cache):
     torch.cuda.synchronize()
     got, want = host(out), O.embedding(tb, ids, nm.BF16)
     assert np.array_equal(got.view(np.uint16), np.asarray(want).view(np.uint16))
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_silu_negative_tail_keeps_its_value(cache, dtype):
+    """Gates from -60 to -104 (past the float32 overflow of exp(-g) at
+    -88.7): SwiGLU and silu stay within one bf16 ulp of the oracle, and
+    within float32's relative tolerance wherever the oracle's value is a
+    normal float32 (an absolute 1e-42 covers the subnormal range)."""
+    print(f"special: silu tail {dtype}", flush=True)
+    g = -np.linspace(60.0, 104.0, 4096)[None, :]
+    u = rng(6).uniform(0.5, 2.0, g.shape)
+    gb, ub = bits(g, dtype), bits(u, dtype)
+    gd, ud = dev(gb, dtype), dev(ub, dtype)
+    for name, got, want in (("swiglu", cache.swiglu(gd, ud), O.swiglu(gb, ub, dtype)),
+                            ("silu", cache.silu(gd), O.silu(gb, dtype))):
+        torch.cuda.synchronize()
+        got = host(got)
+        if dtype == nm.BF16:
+            assert nm.bf16_ulp_distance(got, want).max() <= 1, name
+        else:
+            gv, ov = nm.values(got, dtype), nm.values(want, dtype)
+            assert (np.abs(gv - ov) <= 1e-5 * np.abs(ov) + 1e-42).all(), name
+        gv, ov = nm.values(got, dtype), nm.values(want, dtype)
+        assert (gv[np.abs(ov) >= 2.0**-126] != 0).all(), name     # no flush to zero

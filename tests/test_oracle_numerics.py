@@ -96,3 +96,21 @@ def test_round_trip_values(dtype):
     x = rng.standard_normal(1000)
     r = nm.round_to(x, dtype)
     assert np.array_equal(nm.round_to(nm.values(r, dtype), dtype), r)
+
+
+def test_f32_ulp_distance_and_error_stats():
+    from tests.parity import error_stats, f32_ulp_distance
+    one = np.float32(1.0)
+    a = np.array([one, 0.0, -0.0, np.nextafter(np.float32(0), one), one], np.float32)
+    b = np.array([np.nextafter(one, np.float32(2)), -0.0, np.nextafter(np.float32(0), one),
+                  -np.nextafter(np.float32(0), one), -one], np.float32)
+    assert list(f32_ulp_distance(a, b)) == [1, 0, 1, 2, 2 * 0x3F800000]
+    got = np.array([1.0, 2.0, 0.0], np.float32)
+    want = np.array([np.nextafter(one, np.float32(2)), 2.0, 0.0], np.float32)
+    s = error_stats(got, want, nm.F32)
+    assert s["n"] == 3 and s["max_ulp"] == 1 and s["exact"] == pytest.approx(2 / 3)
+    assert s["max_abs"] == pytest.approx(2.0**-23)
+    assert s["max_rel"] == pytest.approx(2.0**-23 / (1 + 2.0**-23))
+    sb = error_stats(np.array([0x3F80, 0x4000], np.uint16), np.array([0x3F81, 0x4000], np.uint16),
+                     nm.BF16)
+    assert sb["max_ulp"] == 1 and sb["exact"] == 0.5 and sb["max_abs"] == 2.0**-7
