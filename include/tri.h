@@ -29,7 +29,12 @@
  *   the caller; no entry point allocates on the hit path.
  * - Strides are in ELEMENTS. `*_rs` is a row stride, `*_ts` a token stride;
  *   the innermost stride is always 1. A stride must be at least the logical
- *   width of its row.
+ *   width of its row, and the rows of one operand must span at most 2^47
+ *   bytes: ((rows - 1) * stride + width) * element size, with rows = T (the
+ *   embedding table: n_rows; a cos/sin cache: cos_sin_len rows of rd
+ *   floats). No device memory is that large, and the bound keeps every
+ *   offset the kernels form far from int64 overflow; beyond it the call is
+ *   INVALID.
  * - `stream` is a hipStream_t passed as void* (NULL = the null stream). Work
  *   is enqueued asynchronously; the call returns before it completes.
  * - dtype: weights share the activations' dtype. Arithmetic is float32 with

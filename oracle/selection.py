@@ -67,6 +67,7 @@ GRID_CAP = 1 << 20
 T_MAX = 1 << 22
 H_LIMIT = 1 << 24          # H must be below this
 I_LIMIT = 1 << 31          # I must be below this
+SPAN_MAX = 2 ** 47         # bytes the rows of one operand may span (a bound on strides)
 HD_MAX = 512
 HEADS_MAX = 4096
 DEFAULT_CAPACITY = 256
@@ -299,6 +300,15 @@ def _validate_common(c: Call) -> Optional[int]:
     return None
 
 
+def _extent_ok(rows: int, stride: int, width: int, es: int) -> bool:
+    """`rows` rows of `width` elements, `stride` elements apart, span
+    ((rows - 1) * stride + width) * es bytes; a call is valid only when every
+    operand's span is at most SPAN_MAX (a safety rule of this library, not of
+    the paper: no buffer is that large, and it keeps the kernels' offsets
+    far from int64 overflow)."""
+    return ((rows - 1) * stride + width) * es <= SPAN_MAX
+
+
 def _validate_rn(c: Call, names, strides) -> Optional[int]:
     if c.H < 1:
         return E_INVALID
@@ -309,7 +319,7 @@ def _validate_rn(c: Call, names, strides) -> Optional[int]:
     es = elem_size(c.dtype)
     if any(c.ptr[n] % es for n in names):
         return E_INVALID
-    if any(c.stride[s] < c.H for s in strides):
+    if any(c.stride[s] < c.H or not _extent_ok(c.T, c.stride[s], c.H, es) for s in strides):
         return E_INVALID
     eps = _f32(c.eps)
     if not _finite(eps) or eps < 0:
@@ -352,12 +362,16 @@ def _validate_rope(c: Call) -> Optional[int]:
     es = elem_size(c.dtype)
     if c.ptr["q"] % es or (c.nk > 0 and c.ptr["k"] % es):
         return E_INVALID
-    if c.stride["q"] < c.nq * c.hd:
+    if c.stride["q"] < c.nq * c.hd or not _extent_ok(c.T, c.stride["q"], c.nq * c.hd, es):
         return E_INVALID
-    if c.nk > 0 and c.stride["k"] < c.nk * c.hd:
+    if c.nk > 0 and (c.stride["k"] < c.nk * c.hd
+                     or not _extent_ok(c.T, c.stride["k"], c.nk * c.hd, es)):
         return E_INVALID
     if x["cos_sin"] is not None:
-        if x["cos_sin"] % 4 or x["cos_sin_len"] < 1 or x["scaling"] != SCALING_NONE:
+        rdc = rd if rd else c.hd
+        if (x["cos_sin"] % 4 or x["cos_sin_len"] < 1
+                or not _extent_ok(x["cos_sin_len"], rdc, rdc, 4)
+                or x["scaling"] != SCALING_NONE):
             return E_INVALID
         return None
     base = _f32(c.base)
@@ -403,6 +417,8 @@ def _validate_sw(c: Call) -> Optional[int]:
         return E_INVALID
     if any(c.stride[s] < c.I for s in ("gate", "up", "out")):
         return E_INVALID
+    if not all(_extent_ok(c.T, c.stride[s], c.I, es) for s in ("gate", "up", "out")):
+        return E_INVALID
     return None
 
 
@@ -426,6 +442,8 @@ def _validate_short(c: Call) -> Optional[int]:
             return E_INVALID
         if s["table"] < c.H or s["out"] < c.H:
             return E_INVALID
+        if not _extent_ok(c.n_rows, s["table"], c.H, es) or not _extent_ok(c.T, s["out"], c.H, es):
+            return E_INVALID
         return None
     names = ("a", "b", "out")
     if c.H < 1:
@@ -437,6 +455,10 @@ def _validate_short(c: Call) -> Optional[int]:
     if p["a"] % es or p["out"] % es or (c.op != OP_MASKED_FILL and p["b"] % es):
         return E_INVALID
     if any(s[n] < c.H for n in names):
+        return E_INVALID
+    b_es = 1 if c.op == OP_MASKED_FILL else es
+    if (not _extent_ok(c.T, s["a"], c.H, es) or not _extent_ok(c.T, s["b"], c.H, b_es)
+            or not _extent_ok(c.T, s["out"], c.H, es)):
         return E_INVALID
     return None
 

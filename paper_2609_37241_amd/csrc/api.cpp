@@ -45,9 +45,19 @@ inline int check_common(int32_t dtype, int64_t T) {
   return kGo;
 }
 
-// Norm rows: H range, non-null and element-aligned pointers, strides >= H,
-// finite non-negative eps.
-inline int check_norm(uint64_t es, int64_t H, const void *const *ptrs, int np,
+// `rows` rows of `width` elements, `stride` elements apart (stride >= width
+// >= 1, rows >= 1): their span ((rows - 1) * stride + width) * es must not
+// exceed kSpanMax bytes. No memory that large exists, and within it every
+// offset a kernel forms stays far from int64 overflow.
+inline bool extent_ok(int64_t rows, int64_t stride, int64_t width, uint64_t es) {
+  const uint64_t lim = kSpanMax / es;
+  if (uint64_t(width) > lim) return false;
+  return rows <= 1 || uint64_t(stride) <= (lim - uint64_t(width)) / uint64_t(rows - 1);
+}
+
+// Norm rows: H range, non-null and element-aligned pointers, strides >= H
+// and within the extent limit over T rows, finite non-negative eps.
+inline int check_norm(uint64_t es, int64_t T, int64_t H, const void *const *ptrs, int np,
                       const int64_t *strides, int ns, float eps) {
   if (H < 1) return TRI_E_INVALID;
   if (H >= kHLimit) return TRI_E_UNSUPPORTED;
@@ -56,7 +66,7 @@ inline int check_norm(uint64_t es, int64_t H, const void *const *ptrs, int np,
   for (int i = 0; i < np; ++i)
     if (addr(ptrs[i]) % es) return TRI_E_INVALID;
   for (int i = 0; i < ns; ++i)
-    if (strides[i] < H) return TRI_E_INVALID;
+    if (strides[i] < H || !extent_ok(T, strides[i], H, es)) return TRI_E_INVALID;
   if (!isfinite(eps) || eps < 0.0f) return TRI_E_INVALID;
   return kGo;
 }
@@ -67,9 +77,9 @@ const tri_rope_ext kRopePlain = {0, 0, 0, TRI_ROPE_SCALING_NONE, 0.0f, 0.0f, 0.0
 
 // RoPE arguments in the documented order: head_dim and head counts; the
 // variant fields; pointers and their alignment; strides; the angle source.
-inline int check_rope(uint64_t es, const void *q, int64_t q_ts, const void *k, int64_t k_ts,
-                      const void *pos, int32_t nq, int32_t nk, int32_t hd, float base,
-                      const tri_rope_ext &x) {
+inline int check_rope(uint64_t es, int64_t T, const void *q, int64_t q_ts, const void *k,
+                      int64_t k_ts, const void *pos, int32_t nq, int32_t nk, int32_t hd,
+                      float base, const tri_rope_ext &x) {
   if (hd < 2 || (hd & 1)) return TRI_E_INVALID;
   if (hd > kHdMax) return TRI_E_UNSUPPORTED;
   if (nq < 1 || nk < 0) return TRI_E_INVALID;
@@ -82,10 +92,14 @@ inline int check_rope(uint64_t es, const void *q, int64_t q_ts, const void *k, i
   if (!q || !pos || (nk > 0 && !k)) return TRI_E_INVALID;
   if (addr(pos) % (x.pos_int64 ? 8 : 4)) return TRI_E_INVALID;
   if (addr(q) % es || (nk > 0 && addr(k) % es)) return TRI_E_INVALID;
-  if (q_ts < int64_t(nq) * hd) return TRI_E_INVALID;
-  if (nk > 0 && k_ts < int64_t(nk) * hd) return TRI_E_INVALID;
+  if (q_ts < int64_t(nq) * hd || !extent_ok(T, q_ts, int64_t(nq) * hd, es))
+    return TRI_E_INVALID;
+  if (nk > 0 && (k_ts < int64_t(nk) * hd || !extent_ok(T, k_ts, int64_t(nk) * hd, es)))
+    return TRI_E_INVALID;
   if (x.cos_sin) {
-    if (addr(x.cos_sin) % 4 || x.cos_sin_len < 1 || x.scaling != TRI_ROPE_SCALING_NONE)
+    const int64_t rd = x.rotary_dim ? x.rotary_dim : hd;
+    if (addr(x.cos_sin) % 4 || x.cos_sin_len < 1 || !extent_ok(x.cos_sin_len, rd, rd, 4) ||
+        x.scaling != TRI_ROPE_SCALING_NONE)
       return TRI_E_INVALID;
     return kGo;
   }
@@ -109,13 +123,15 @@ inline int check_qkn(uint64_t es, const void *q_w, const void *k_w, int32_t nk, 
   return kGo;
 }
 
-inline int check_sw(uint64_t es, int64_t I, const void *g, int64_t g_rs, const void *u,
-                    int64_t u_rs, const void *o, int64_t o_rs) {
+inline int check_sw(uint64_t es, int64_t T, int64_t I, const void *g, int64_t g_rs,
+                    const void *u, int64_t u_rs, const void *o, int64_t o_rs) {
   if (I < 1) return TRI_E_INVALID;
   if (I >= kILimit) return TRI_E_UNSUPPORTED;
   if (!g || !u || !o) return TRI_E_INVALID;
   if ((addr(g) | addr(u) | addr(o)) % es) return TRI_E_INVALID;
   if (g_rs < I || u_rs < I || o_rs < I) return TRI_E_INVALID;
+  if (!extent_ok(T, g_rs, I, es) || !extent_ok(T, u_rs, I, es) || !extent_ok(T, o_rs, I, es))
+    return TRI_E_INVALID;
   return kGo;
 }
 
@@ -278,18 +294,18 @@ int chain_check(const tri_chain_args *p, Key *out) {
   {
     const void *ptrs[5] = {p->x, p->res, p->w, p->y, p->res_out};
     const int64_t strides[4] = {p->x_rs, p->res_rs, p->y_rs, p->ro_rs};
-    st = check_norm(es, H, ptrs, 5, strides, 4, p->eps);
+    st = check_norm(es, T, H, ptrs, 5, strides, 4, p->eps);
     if (st != kGo) return st;
   }
   const tri_rope_ext &x = p->rope_ext ? *p->rope_ext : kRopePlain;
-  st = check_rope(es, p->q, p->q_ts, p->k, p->k_ts, p->pos, p->nq, p->nk, p->hd, p->base, x);
+  st = check_rope(es, T, p->q, p->q_ts, p->k, p->k_ts, p->pos, p->nq, p->nk, p->hd, p->base, x);
   if (st != kGo) return st;
   const bool qkn = p->q_norm_w != nullptr;
   if (qkn) {
     st = check_qkn(es, p->q_norm_w, p->k_norm_w, p->nk, p->qk_eps);
     if (st != kGo) return st;
   }
-  st = check_sw(es, I, p->gate, p->g_rs, p->up, p->u_rs, p->out, p->o_rs);
+  st = check_sw(es, T, I, p->gate, p->g_rs, p->up, p->u_rs, p->out, p->o_rs);
   if (st != kGo) return st;
 
   const unsigned fl =
@@ -345,14 +361,17 @@ int chain_launch(const Version &v, const tri_chain_args &p, void *stream, tri_la
 }
 
 // Element-wise ops: W range, non-null element-aligned operands (the mask is
-// bytes), strides >= W.
-inline int check_elt(uint64_t es, int64_t W, const void *a, int64_t a_rs, const void *b,
-                     int64_t b_rs, bool b_is_mask, const void *o, int64_t o_rs) {
+// bytes), strides >= W and within the extent limit over T rows.
+inline int check_elt(uint64_t es, int64_t T, int64_t W, const void *a, int64_t a_rs,
+                     const void *b, int64_t b_rs, bool b_is_mask, const void *o, int64_t o_rs) {
   if (W < 1) return TRI_E_INVALID;
   if (W >= kILimit) return TRI_E_UNSUPPORTED;
   if (!a || !b || !o) return TRI_E_INVALID;
   if (addr(a) % es || addr(o) % es || (!b_is_mask && addr(b) % es)) return TRI_E_INVALID;
   if (a_rs < W || b_rs < W || o_rs < W) return TRI_E_INVALID;
+  if (!extent_ok(T, a_rs, W, es) || !extent_ok(T, b_rs, W, b_is_mask ? 1 : es) ||
+      !extent_ok(T, o_rs, W, es))
+    return TRI_E_INVALID;
   return kGo;
 }
 
@@ -384,7 +403,7 @@ tri_status elt_entry(tri_cache *c, uint32_t op, int32_t dtype, const void *a, in
   if (st != kGo) return finish_early(c, op, st);
   const uint64_t es = es_of(uint32_t(dtype));
   const bool mask = op == TRI_OP_MASKED_FILL;
-  st = check_elt(es, W, a, a_rs, b, b_rs, mask, out, o_rs);
+  st = check_elt(es, T, W, a, a_rs, b, b_rs, mask, out, o_rs);
   if (st != kGo) return finish_early(c, op, st);
   // alignment: data 16 B; the mask 16 / es bytes (one byte per element of a vector)
   const uint64_t v = 16 / es;
@@ -514,7 +533,7 @@ tri_status rope_entry(tri_cache *c, uint32_t op, int32_t dtype, void *q, int64_t
   if (st != kGo) return finish_early(c, op, st);
   const uint64_t es = es_of(uint32_t(dtype));
   const tri_rope_ext &x = ext ? *ext : kRopePlain;
-  st = check_rope(es, q, q_ts, kp, k_ts, pos, nq, nk, hd, base, x);
+  st = check_rope(es, T, q, q_ts, kp, k_ts, pos, nq, nk, hd, base, x);
   if (st != kGo) return finish_early(c, op, st);
   const bool qkn = op == TRI_OP_QK_NORM_ROPE;
   if (qkn) {
@@ -558,7 +577,7 @@ tri_status tri_rmsnorm(tri_cache *c, tri_dtype dtype, const void *x, int64_t x_r
   const uint64_t es = es_of(dtype);
   const void *ptrs[3] = {x, w, y};
   const int64_t strides[2] = {x_rs, y_rs};
-  st = check_norm(es, H, ptrs, 3, strides, 2, eps);
+  st = check_norm(es, T, H, ptrs, 3, strides, 2, eps);
   if (st != kGo) return finish_early(c, op, st);
 
   const Key k = make_key(op, dtype, T, rn_flags(es, x, x_rs, w, y, y_rs, H), 0, uint64_t(H), 0,
@@ -579,7 +598,7 @@ tri_status tri_residual_rmsnorm(tri_cache *c, tri_dtype dtype, const void *x, in
   const uint64_t es = es_of(dtype);
   const void *ptrs[5] = {x, res, w, y, res_out};
   const int64_t strides[4] = {x_rs, res_rs, y_rs, ro_rs};
-  st = check_norm(es, H, ptrs, 5, strides, 4, eps);
+  st = check_norm(es, T, H, ptrs, 5, strides, 4, eps);
   if (st != kGo) return finish_early(c, op, st);
 
   const Key k = make_key(op, dtype, T,
@@ -621,7 +640,7 @@ tri_status tri_swiglu(tri_cache *c, tri_dtype dtype, const void *gate, int64_t g
   int st = check_common(dtype, T);
   if (st != kGo) return finish_early(c, op, st);
   const uint64_t es = es_of(dtype);
-  st = check_sw(es, I, gate, g_rs, up, u_rs, out, o_rs);
+  st = check_sw(es, T, I, gate, g_rs, up, u_rs, out, o_rs);
   if (st != kGo) return finish_early(c, op, st);
 
   const Key k = make_key(op, dtype, T, sw_flags(es, gate, g_rs, up, u_rs, out, o_rs, I), 0, 0,
@@ -661,7 +680,8 @@ tri_status tri_embedding(tri_cache *c, tri_dtype dtype, const void *table, int64
   if (!table || !ids || !out) return finish_early(c, op, TRI_E_INVALID);
   if (addr(table) % es || addr(out) % es || addr(ids) % (ids_int64 ? 8 : 4))
     return finish_early(c, op, TRI_E_INVALID);
-  if (t_rs < H || o_rs < H) return finish_early(c, op, TRI_E_INVALID);
+  if (t_rs < H || o_rs < H || !extent_ok(n_rows, t_rs, H, es) || !extent_ok(T, o_rs, H, es))
+    return finish_early(c, op, TRI_E_INVALID);
   const bool aligned =
       ((addr(table) | addr(out) | uint64_t(t_rs) * es | uint64_t(o_rs) * es) & 15u) == 0;
   Key k = make_key(op, uint32_t(dtype), T, aligned ? kAlign : 0u, 0, uint64_t(H), 0, 0, 0, 0);

@@ -34,6 +34,7 @@ constexpr uint32_t kGridCap = 1u << 20;
 constexpr int64_t kTMax = int64_t(1) << 22;
 constexpr int64_t kHLimit = int64_t(1) << 24;
 constexpr int64_t kILimit = int64_t(1) << 31;
+constexpr uint64_t kSpanMax = uint64_t(1) << 47;   // bytes an operand's rows may span
 constexpr int32_t kHdMax = 512;
 constexpr int32_t kHeadsMax = 4096;
 constexpr uint32_t kDefaultCapacity = 256;

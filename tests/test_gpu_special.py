@@ -163,7 +163,7 @@ def test_rope_special_values_and_positions(tri, cache, dtype, qkn):
     q[0, 0, 3] = INF                      # an infinite element at position 0 (cos 1, sin 0)
     q[1, 1, 70] = NAN
     k[2, 0, :] = 0.0                      # a zero head (QK norm: zeros with eps > 0)
-    k[3, 1, 5] = 1e18                     # large, square still finite in float32 (R6)
+    k[3, 1, 5] = 1e18                     # large, square still finite in float32
     # positions: 0, the largest exactly representable in float32, huge, and ordinary ones
     pos = np.array([0, (1 << 24) - 1, 2_000_000_000, 5, 4095, 1], dtype=np.int32)
     qb, kb = bits(q, dtype), bits(k, dtype)

@@ -293,6 +293,31 @@ def call_zoo():
               emb_call(F, 0, 64, 0),
               sw_call(BF, 1, 0), sw_call(BF, 1, S.I_LIMIT), sw_call(BF, 1, 64, null=("up",)),
               sw_call(BF, 1, 64, off=1), sw_call(BF, 3, 64, pad=-1)]
+    # operand extents: rows spanning exactly 2^47 bytes pass, one element
+    # more (or any stride that would wrap the kernels' offsets) is INVALID;
+    # with one row the stride is never used
+    span = 2 ** 46                                  # bf16 elements in 2^47 bytes
+    calls += [rn_call(BF, 2, 4096, pad=span - 8192), rn_call(BF, 2, 4096, pad=span - 8191),
+              rn_call(F, 3, 64, pad=2 ** 60), rn_call(BF, 1, 4096, pad=2 ** 62),
+              res_call(BF, 2, 4096, pad=2 ** 50), res_call(BF, 9, 1024, pad=2 ** 43),
+              rope_call(BF, 2, 4, 4, 64, pad=2 ** 50), rope_call(BF, 1, 4, 4, 64, pad=2 ** 62),
+              rope_call(BF, 2, 4, 4, 64, pad=span - 512), rope_call(BF, 2, 4, 4, 64,
+                                                                    pad=span - 511),
+              qkn_call(BF, 3, 4, 4, 64, pad=2 ** 61),
+              rope_call(BF, 1, 4, 4, 64, ext=dict(cos_sin=CACHE_ADDR, cos_sin_len=2 ** 39)),
+              rope_call(BF, 1, 4, 4, 64, ext=dict(cos_sin=CACHE_ADDR, cos_sin_len=2 ** 39 + 1)),
+              rope_call(BF, 1, 4, 4, 64, ext=dict(cos_sin=CACHE_ADDR, cos_sin_len=2 ** 62)),
+              rope_call(BF, 1, 4, 4, 64, ext=dict(rotary_dim=32, cos_sin=CACHE_ADDR,
+                                                  cos_sin_len=2 ** 40)),
+              sw_call(BF, 2, 64, pad=2 ** 50), sw_call(F, 2, 64, pad=2 ** 45 - 128),
+              sw_call(F, 2, 64, pad=2 ** 45 - 127),
+              silu_call(BF, 2, 64, pad=2 ** 50), add_call(BF, 2, 64, pad=2 ** 50),
+              mf_call(BF, 2, 64, m_pad=2 ** 47 - 128), mf_call(BF, 2, 64, m_pad=2 ** 47 - 127),
+              emb_call(BF, 1, 64, 2 ** 40), emb_call(BF, 1, 64, 2 ** 40 + 1),
+              emb_call(BF, 2, 64, 10, pad=2 ** 50),
+              chain_call(BF, 2, 4096, 11008, 32, 32, 128, sw_pad=2 ** 50),
+              chain_call(BF, 2, 4096, 11008, 32, 32, 128, res_pad=2 ** 50),
+              chain_call(BF, 2, 4096, 11008, 32, 32, 128, rope_pad=2 ** 50)]
     return calls
 
 

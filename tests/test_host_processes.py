@@ -1,5 +1,5 @@
 """Several processes compile and tune into one code directory at once (CPU,
-recording backend; R21, R33, R34).
+recording backend).
 
 Six processes each make a cache with auto-install, compiled specializations
 and install-time tuning on one shared code directory, meet at a barrier and
