@@ -19,8 +19,8 @@ are:
   forms it; cos and sin of that float32 angle are taken in float64 and not
   rounded before use. Every head of a token (Q and K) uses the same angles.
 * SwiGLU: out = g / (1 + exp(-g)) * u with the gate as the first operand;
-  for very negative g the exponential overflows and the result is a signed
-  zero, never NaN.
+  where the exponential overflows (in float64, below g = -709) the result is
+  a signed zero, never NaN; g = -inf gives NaN (-inf / inf).
 * QK-RMSNorm before RoPE (Qwen3-style heads): every Q and K head vector is
   RMS-normalised over its hd elements with a per-dimension weight (one
   weight vector for Q, one for K) and then rotated; the normalised head is
@@ -272,8 +272,8 @@ def swiglu(gate, up, dtype):
 
 # ---- short element-wise and gather ops (the paper's operator suite, Sec. 4.1) ----
 def silu(x, dtype):
-    """silu(x) = x / (1 + exp(-x)), one rounding; very negative x gives a
-    signed zero (the exponential overflows), never NaN."""
+    """silu(x) = x / (1 + exp(-x)), one rounding; below x = -709 the float64
+    exponential overflows and the result is a signed zero, never NaN."""
     v = values(x, dtype)
     with np.errstate(over="ignore"):
         return round_to(v / (1.0 + np.exp(-v)), dtype)
