@@ -99,7 +99,7 @@ enum {
 typedef struct tri_launch_rec {
   int32_t variant;     /* kernel variant id (the install policy table)       */
   uint32_t grid_x;     /* workgroups                                          */
-  uint32_t block_x;    /* work-items per workgroup                            */
+  uint32_t block_x;    /* work-items per workgroup (256; 1024 for variant 19) */
 } tri_launch_rec;
 
 /* Words of the packed guard key. */

@@ -53,6 +53,9 @@ RN_SCALAR = 10
 RN_WAVE = {1: 11, 2: 12}
 RN_BLOCK = {1: 13, 2: 14, 4: 15, 8: 16, 16: 17}
 RN_LOOP = 18
+RN_WIDE = 19               # a 1024-work-item workgroup per row, 8 vectors per lane
+WIDE_LANES = 1024
+WIDE_ROW_VECS = 8 * WIDE_LANES   # the longest row it holds (16-byte vectors)
 ROPE_SCALAR, ROPE_VEC, ROPE_VEC_I, ROPE_QKN_SCALAR, ROPE_QKN_VEC, ROPE_QKN_VEC_I = \
     30, 31, 32, 33, 34, 35
 ROPE_VEC_ROLES = (ROPE_VEC, ROPE_VEC_I, ROPE_QKN_VEC, ROPE_QKN_VEC_I)
@@ -101,6 +104,11 @@ def cdiv(a: int, b: int) -> int:
     return -(-a // b)
 
 
+def block_of(variant: int) -> int:
+    """Work-items per workgroup: 1024 for the wide norm rows, 256 otherwise."""
+    return WIDE_LANES if variant == RN_WIDE else BLOCK
+
+
 def next_pow2(n: int) -> int:
     p = 1
     while p < n:
@@ -142,7 +150,9 @@ def rn_role(dtype: int, H: int, flags: int, T: int) -> Tuple[int, int]:
     nb = next_pow2(cdiv(nvec, 256))       # a workgroup per row
     if nb <= 16:
         return RN_BLOCK[nb], T
-    return RN_LOOP, T
+    if nvec <= WIDE_ROW_VECS:             # a 1024-lane workgroup per row
+        return RN_WIDE, T
+    return RN_LOOP, T                     # two passes over memory
 
 
 def rope_role(dtype: int, hd: int, flags: int, T: int, qk_norm: bool = False,
@@ -672,7 +682,7 @@ def plan(key, T: int):
     op, dt, b, fl = f["op"], f["dtype"], f["bucket"], f["flags"]
     if op in (OP_RMSNORM, OP_RES_RMSNORM):
         v, g = rn_role(dt, f["H"], fl, T)
-        return v, (0, 0, 0), [(v, g, BLOCK)]
+        return v, (0, 0, 0), [(v, g, block_of(v))]
     inter = bool(f["rope_bits"] & ROPE_INTERLEAVED)
     nh = f["nq"] + f["nk"]
     if op in (OP_ROPE_QK, OP_QK_NORM_ROPE):
@@ -703,7 +713,7 @@ def plan(key, T: int):
              and sw[0] in (SW_FLAT, SW_FLAT_NT))
     if fused:
         return CH_FUSED, roles, [(CH_FUSED, rn[1] + ro[1] + sw[1], BLOCK)]
-    return CH_SEQ, roles, [(rn[0], rn[1], BLOCK), (ro[0], ro[1], BLOCK),
+    return CH_SEQ, roles, [(rn[0], rn[1], block_of(rn[0])), (ro[0], ro[1], BLOCK),
                            (sw[0], sw[1], BLOCK)]
 
 
@@ -748,9 +758,10 @@ def _geometry_options(S: int, P: int, b: int) -> List[Tuple[int, int]]:
 
 def _rn_options(dt: int, H: int, fl: int, standalone: bool) -> List[int]:
     """Norm rows: a row held by one wavefront can also be held by one
-    256-lane workgroup (one vector per lane); a row held in registers can
-    also take the two-pass loop kernel (standalone only: the fused chain
-    holds its rows in registers)."""
+    256-lane workgroup (one vector per lane); standalone (the fused chain
+    takes only the 256-lane register forms), a row of more than 1024
+    vectors held by a 256-lane workgroup can also be held by a 1024-lane
+    one, and any row held in registers can take the two-pass loop kernel."""
     P = rn_role(dt, H, fl, 1)[0]
     if P in (RN_SCALAR, RN_LOOP):
         return [P]
@@ -758,6 +769,8 @@ def _rn_options(dt: int, H: int, fl: int, standalone: bool) -> List[int]:
     if P in RN_WAVE.values():
         out.append(RN_BLOCK[1])
     if standalone:
+        if P in (RN_BLOCK[8], RN_BLOCK[16]):
+            out.append(RN_WIDE)
         out.append(RN_LOOP)
     return out
 
@@ -842,7 +855,7 @@ def grid_of(variant: int, dt: int, T: int, width: int, slices: int = 1, tokens: 
     v = 16 // elem_size(dt)
     if variant in RN_WAVE.values():
         return cdiv(T, 4)
-    if variant in (RN_SCALAR, RN_LOOP, ROPE_SCALAR, ROPE_QKN_SCALAR) or \
+    if variant in (RN_SCALAR, RN_LOOP, RN_WIDE, ROPE_SCALAR, ROPE_QKN_SCALAR) or \
             variant in RN_BLOCK.values():
         return T
     if variant in ROPE_VEC_ROLES:
@@ -872,7 +885,7 @@ def cand_plan(key, c: Cand, T: int):
              + grid_of(c.roles[2], dt, T, width))
         return CH_FUSED, c.roles, [(CH_FUSED, g, BLOCK)]
     launches = [(kv, grid_of(kv, dt, T, width, c.slices, c.tokens) if kv in ROPE_VEC_ROLES
-                 else grid_of(kv, dt, T, width), BLOCK) for kv in c.kernels]
+                 else grid_of(kv, dt, T, width), block_of(kv)) for kv in c.kernels]
     return c.variant, c.roles, launches
 
 

@@ -354,8 +354,8 @@ int chain_launch(const Version &v, const tri_chain_args &p, void *stream, tri_la
   *n = 3;
   int rc = 0;
   for (int i = 0; i < 3; ++i) {
-    l[i] = {v.plan.kvariant[i], grids[i], kBlock};
-    if (rc == 0) rc = be_launch(v.fn[i], grids[i], kBlock, args[i], sizes[i], stream);
+    l[i] = {v.plan.kvariant[i], grids[i], role_block(v.plan.kvariant[i])};
+    if (rc == 0) rc = be_launch(v.fn[i], grids[i], l[i].block_x, args[i], sizes[i], stream);
   }
   return rc;
 }
@@ -387,8 +387,9 @@ tri_status single_launch(tri_cache *c, uint32_t op, const Key &k, int64_t T, int
   if (st != TRI_OK) return tri_status(st);
   Version &v = c->versions[vi];
   const tri_launch_rec l{v.plan.kvariant[0],
-                         role_grid(v.plan.kvariant[0], key_dtype(k), T, width), kBlock};
-  const int rc = be_launch(v.fn[0], l.grid_x, kBlock, args, args_size, stream);
+                         role_grid(v.plan.kvariant[0], key_dtype(k), T, width),
+                         role_block(v.plan.kvariant[0])};
+  const int rc = be_launch(v.fn[0], l.grid_x, l.block_x, args, args_size, stream);
   record(c, op, v, vi, k, 1, &l, rc ? TRI_E_LAUNCH : TRI_OK);
   return finish(c, v, auto_inst, rc);
 }

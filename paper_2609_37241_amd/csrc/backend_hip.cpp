@@ -33,7 +33,7 @@ int be_init(int *device) {
 
 int be_resolve(int32_t kvariant, uint32_t dtype, int32_t ksub, void **fn) {
   const void *sym = nullptr;
-  if (kvariant >= RN_SCALAR && kvariant <= RN_LOOP)
+  if (kvariant >= RN_SCALAR && kvariant <= RN_WIDE)
     sym = rn_kernel(kvariant, dtype, ksub);
   else if (kvariant >= ROPE_SCALAR && kvariant <= ROPE_QKN_VEC_I)
     sym = rope_kernel(kvariant, dtype);

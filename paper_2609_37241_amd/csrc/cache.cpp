@@ -237,7 +237,7 @@ void fill_selection(const Version &v, int32_t index, int64_t T, tri_selection *o
       out->launch[i] = {v.plan.kvariant[i],
                         role_grid(v.plan.kvariant[i], dt, T, I, v.plan.rope_slices,
                                   v.plan.rope_tokens),
-                        kBlock};
+                        role_block(v.plan.kvariant[i])};
   }
   key_words(k, out->key);
 }

@@ -15,7 +15,7 @@ enum Variant : int32_t {
   RN_SCALAR = 10,
   RN_WAVE_1 = 11, RN_WAVE_2 = 12,
   RN_BLOCK_1 = 13, RN_BLOCK_2 = 14, RN_BLOCK_4 = 15, RN_BLOCK_8 = 16, RN_BLOCK_16 = 17,
-  RN_LOOP = 18,
+  RN_LOOP = 18, RN_WIDE = 19,
   ROPE_SCALAR = 30, ROPE_VEC = 31, ROPE_VEC_I = 32, ROPE_QKN_SCALAR = 33, ROPE_QKN_VEC = 34,
   ROPE_QKN_VEC_I = 35,
   SW_SCALAR = 40, SW_FLAT = 41, SW_FLAT_NT = 42, SW_ROWS = 43,
@@ -35,6 +35,7 @@ constexpr int64_t kTMax = int64_t(1) << 22;
 constexpr int64_t kHLimit = int64_t(1) << 24;
 constexpr int64_t kILimit = int64_t(1) << 31;
 constexpr uint64_t kSpanMax = uint64_t(1) << 47;   // bytes an operand's rows may span
+constexpr int64_t kWideRowVecs = 8 * int64_t(kWideLanes);   // longest RN_WIDE row (vectors)
 constexpr int32_t kHdMax = 512;
 constexpr int32_t kHeadsMax = 4096;
 constexpr uint32_t kDefaultCapacity = 256;
@@ -103,6 +104,10 @@ constexpr uint64_t kStreamBytes = uint64_t(320) << 20;
 // slices workgroups with head slices, else ceil(T / tokens).
 uint32_t role_grid(int32_t variant, uint32_t dtype, int64_t T, int64_t I, int32_t slices = 1,
                    int32_t tokens = 1);
+// Work-items per workgroup of a launch of `variant`.
+inline uint32_t role_block(int32_t variant) {
+  return variant == RN_WIDE ? uint32_t(kWideLanes) : kBlock;
+}
 // RoPE vector roles at decode sizes split a token's heads over this many
 // workgroups (1 otherwise).
 int32_t rope_slices(uint32_t dtype, int32_t hd, int32_t rd, bool interleaved, int32_t n_heads,

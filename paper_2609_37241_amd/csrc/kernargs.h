@@ -18,6 +18,10 @@ constexpr uint32_t kRopeInterleaved = 1, kRopePos64 = 2, kRopeCache = 4;
 constexpr uint32_t kRopeSliceShift = 8, kRopeTokensShift = 16;
 constexpr int kRopeTokensMax = 4;
 
+// Work-items of the wide norm workgroup (RN_WIDE): one row of up to
+// 8 * kWideLanes 16-byte vectors per workgroup; every other kernel uses 256.
+constexpr int kWideLanes = 1024;
+
 // Residual add + RMSNorm and plain RMSNorm ([T, H] rows, element strides).
 struct RnArgs {
   const void *x;

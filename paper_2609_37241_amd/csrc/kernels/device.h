@@ -146,14 +146,22 @@ __device__ inline float group_sum(float v, int n) {
   return v;
 }
 
-// Sum over the 256 work-items of a workgroup; `red` is 4 words of LDS.
-template <typename T>
+// Sum over the NW wavefronts of a workgroup (256 work-items by default);
+// `red` is NW words of LDS. The wavefront sums are added in a fixed order.
+template <int NW = 4, typename T>
 __device__ inline T block_sum(T v, T *red) {
   v = wave_sum(v);
   const int wid = threadIdx.x >> 6;
   if ((threadIdx.x & 63) == 0) red[wid] = v;
   __syncthreads();
-  const T s = (red[0] + red[1]) + (red[2] + red[3]);
+  T s;
+  if constexpr (NW == 4) {
+    s = (red[0] + red[1]) + (red[2] + red[3]);
+  } else {
+    s = red[0];
+#pragma unroll
+    for (int i = 1; i < NW; ++i) s += red[i];
+  }
   __syncthreads();
   return s;
 }
@@ -161,7 +169,8 @@ __device__ inline T block_sum(T v, T *red) {
 // ---- RMSNorm / residual RMSNorm --------------------------------------------------
 // One row held in registers: lane `lane` of LANES owns vectors lane + LANES*k,
 // k < NV. With RES, h = RN(x + r) is written to res_out and normalised.
-// LANES = 64: one wavefront per row, no barrier. LANES = 256: one workgroup.
+// LANES = 64: one wavefront per row, no barrier. LANES = 256 or kWideLanes:
+// one workgroup of that many work-items.
 // Without NT (decode sizes) the weight vectors are requested together with the
 // row, so the row costs one memory round trip; with NT (streaming sizes) they
 // are loaded after the reduction to keep fewer registers live.
@@ -222,7 +231,7 @@ __device__ __forceinline__ void rn_row_regs(const RnArgs &a, int64_t row, int la
   if constexpr (LANES == 64)
     ss = wave_sum(ss);
   else
-    ss = block_sum(ss, red);
+    ss = block_sum<LANES / 64>(ss, red);
   const float inv = rsqrtf(ss / float(a.H) + a.eps);
   u32x4 *yr = reinterpret_cast<u32x4 *>(static_cast<char *>(a.y) + row * a.y_rs * E::ES);
 #pragma unroll
@@ -250,13 +259,20 @@ __device__ __forceinline__ void rn_wave_block(const RnArgs &a, int64_t blk) {
   rn_row_regs<DT, NV, RES, 64, NT>(a, row, threadIdx.x & 63, nullptr);
 }
 
+// Vectors a work-item keeps in flight in the long-row kernels' streaming
+// passes (one 16-byte load each, all issued before any is used).
+constexpr int kRnBatch = 8;
+
 // Long rows: two passes over global memory with float64 accumulation (each
 // thread sums up to H/256 elements, so a float32 running sum would lose
-// accuracy at the largest H). Vector form (16-byte aligned rows).
+// accuracy at the largest H). Vector form (16-byte aligned rows). Both passes
+// keep kRnBatch vectors per work-item in flight; pass 2 re-reads x (or h from
+// res_out: the thread's own writes).
 template <int DT, bool RES>
 __device__ __forceinline__ void rn_loop_row(const RnArgs &a, int64_t row, double *red) {
   using E = Elt<DT>;
   constexpr int V = E::V;
+  constexpr int B = kRnBatch;
   const int nvec = a.H / V;
   const u32x4 *xr = reinterpret_cast<const u32x4 *>(static_cast<const char *>(a.x) +
                                                      row * a.x_rs * E::ES);
@@ -266,38 +282,80 @@ __device__ __forceinline__ void rn_loop_row(const RnArgs &a, int64_t row, double
     const u32x4 *rr = reinterpret_cast<const u32x4 *>(static_cast<const char *>(a.res) +
                                                        row * a.res_rs * E::ES);
     u32x4 *orow = reinterpret_cast<u32x4 *>(static_cast<char *>(a.res_out) + row * a.ro_rs * E::ES);
-    for (int vi = threadIdx.x; vi < nvec; vi += kThreads) {
-      float f[V], g[V];
-      E::unpack(xr[vi], f);
-      E::unpack(rr[vi], g);
+    for (int base = threadIdx.x; base < nvec; base += kThreads * B) {
+      u32x4 xv[B], rv[B];
 #pragma unroll
-      for (int e = 0; e < V; ++e) f[e] += g[e];
-      const u32x4 h = E::pack(f);
-      orow[vi] = h;
-      E::unpack(h, f);
+      for (int k = 0; k < B; ++k) {
+        const int vi = base + k * kThreads;
+        if (vi < nvec) {
+          xv[k] = xr[vi];
+          rv[k] = rr[vi];
+        }
+      }
 #pragma unroll
-      for (int e = 0; e < V; ++e) ss += double(f[e]) * double(f[e]);
+      for (int k = 0; k < B; ++k) {
+        const int vi = base + k * kThreads;
+        if (vi < nvec) {
+          float f[V], g[V];
+          E::unpack(xv[k], f);
+          E::unpack(rv[k], g);
+#pragma unroll
+          for (int e = 0; e < V; ++e) f[e] += g[e];
+          const u32x4 h = E::pack(f);
+          orow[vi] = h;
+          E::unpack(h, f);
+#pragma unroll
+          for (int e = 0; e < V; ++e) ss += double(f[e]) * double(f[e]);
+        }
+      }
     }
-    src = orow;   // pass 2 re-reads h (this thread's own writes)
+    src = orow;
   } else {
-    for (int vi = threadIdx.x; vi < nvec; vi += kThreads) {
-      float f[V];
-      E::unpack(xr[vi], f);
+    for (int base = threadIdx.x; base < nvec; base += kThreads * B) {
+      u32x4 xv[B];
 #pragma unroll
-      for (int e = 0; e < V; ++e) ss += double(f[e]) * double(f[e]);
+      for (int k = 0; k < B; ++k) {
+        const int vi = base + k * kThreads;
+        if (vi < nvec) xv[k] = xr[vi];
+      }
+#pragma unroll
+      for (int k = 0; k < B; ++k) {
+        const int vi = base + k * kThreads;
+        if (vi < nvec) {
+          float f[V];
+          E::unpack(xv[k], f);
+#pragma unroll
+          for (int e = 0; e < V; ++e) ss += double(f[e]) * double(f[e]);
+        }
+      }
     }
   }
   ss = block_sum(ss, red);
   const float inv = float(1.0 / sqrt(ss / double(a.H) + double(a.eps)));
   const u32x4 *wr = static_cast<const u32x4 *>(a.w);
   u32x4 *yr = reinterpret_cast<u32x4 *>(static_cast<char *>(a.y) + row * a.y_rs * E::ES);
-  for (int vi = threadIdx.x; vi < nvec; vi += kThreads) {
-    float f[V], w[V];
-    E::unpack(src[vi], f);
-    E::unpack(wr[vi], w);
+  for (int base = threadIdx.x; base < nvec; base += kThreads * B) {
+    u32x4 hv[B], wv[B];
 #pragma unroll
-    for (int e = 0; e < V; ++e) f[e] = (f[e] * inv) * w[e];
-    yr[vi] = E::pack(f);
+    for (int k = 0; k < B; ++k) {
+      const int vi = base + k * kThreads;
+      if (vi < nvec) {
+        hv[k] = src[vi];
+        wv[k] = wr[vi];
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < B; ++k) {
+      const int vi = base + k * kThreads;
+      if (vi < nvec) {
+        float f[V], w[V];
+        E::unpack(hv[k], f);
+        E::unpack(wv[k], w);
+#pragma unroll
+        for (int e = 0; e < V; ++e) f[e] = (f[e] * inv) * w[e];
+        yr[vi] = E::pack(f);
+      }
+    }
   }
 }
 
@@ -940,6 +998,14 @@ template <int DT, bool RES>
 __device__ __forceinline__ void body_rn_loop(const RnArgs &a) {
   __shared__ double red[4];
   rn_loop_row<DT, RES>(a, blockIdx.x, red);
+}
+
+// Rows of 4097..8192 vectors: one 1024-work-item workgroup per row, up to
+// 8 vectors per lane held in registers (all loads issued up front).
+template <int DT, bool RES>
+__device__ __forceinline__ void body_rn_wide(const RnArgs &a) {
+  __shared__ float red[kWideLanes / 64];
+  rn_row_regs<DT, 8, RES, kWideLanes, false>(a, blockIdx.x, threadIdx.x, red);
 }
 
 template <int DT, bool RES>

@@ -48,7 +48,11 @@ bool rope_vec_role(int32_t v) {
 // workgroup per row, up to 16 vectors per work-item: the four wavefronts
 // issue the row's loads and stores in parallel (measured 1.8 µs vs 3.4 µs
 // device time for a single 4096-element bf16 row held by one wavefront) and
-// hold fewer registers per lane when streaming. Longer rows still make two
+// hold fewer registers per lane when streaming. Rows of up to kWideRowVecs
+// vectors take a 1024-work-item workgroup (up to 8 vectors per lane in
+// registers); it streamed bf16 rows of 65,536 elements at 5.4 TB/s against
+// 4.2-4.4 TB/s for the row staged in LDS (one 128 KiB row per CU leaves too
+// few bytes in flight) and 3.9 TB/s for two passes. Longer rows make two
 // passes over global memory. Unaligned or ragged rows take the scalar kernel.
 Role rn_role(uint32_t dtype, int64_t H, unsigned flags, int64_t T) {
   const int64_t v = vec_elems(dtype);
@@ -57,6 +61,7 @@ Role rn_role(uint32_t dtype, int64_t H, unsigned flags, int64_t T) {
   if (nvec <= 128) return {nvec <= 64 ? RN_WAVE_1 : RN_WAVE_2, uint32_t(cdiv(T, 4))};
   const int64_t nb = next_pow2(cdiv(nvec, 256));
   if (nb <= 16) return {RN_BLOCK_1 + pow2_index(nb), uint32_t(T)};
+  if (nvec <= kWideRowVecs) return {RN_WIDE, uint32_t(T)};
   return {RN_LOOP, uint32_t(T)};
 }
 
@@ -181,7 +186,7 @@ uint32_t role_grid(int32_t variant, uint32_t dtype, int64_t T, int64_t I, int32_
   if (variant == RN_WAVE_1 || variant == RN_WAVE_2) return uint32_t(cdiv(T, 4));
   switch (variant) {
     case RN_SCALAR: case RN_BLOCK_1: case RN_BLOCK_2: case RN_BLOCK_4: case RN_BLOCK_8:
-    case RN_BLOCK_16: case RN_LOOP: case ROPE_SCALAR: case ROPE_QKN_SCALAR:
+    case RN_BLOCK_16: case RN_LOOP: case RN_WIDE: case ROPE_SCALAR: case ROPE_QKN_SCALAR:
       return uint32_t(T);
     case ROPE_VEC: case ROPE_VEC_I: case ROPE_QKN_VEC: case ROPE_QKN_VEC_I:
       return slices > 1 ? uint32_t(T * slices) : uint32_t(cdiv(T, tokens < 1 ? 1 : tokens));
@@ -355,8 +360,9 @@ Plan plan_for_key(const Key &k) {
 // ---- candidate plans of install-time tuning ---------------------------------------
 // Index 0 is the policy's plan. The others are the kernel variants whose
 // requirements the key also meets: a norm row held by one wavefront can be
-// held by one workgroup (one vector per lane), and a row held in registers
-// can take the two-pass kernel (standalone only); a vector RoPE role can
+// held by one workgroup (one vector per lane), a row of more than 1024
+// vectors held by a 256-lane workgroup can be held by a 1024-lane one, and a
+// row held in registers can take the two-pass kernel (standalone only); a vector RoPE role can
 // take another geometry (at decode sizes 1, 2 or 4 workgroups per token;
 // beyond them 1, 2 or 4 tokens per workgroup, or up to 8192 tokens 2 or 4
 // workgroups per token) or the scalar kernel; flat SwiGLU and element-wise kernels have a cached
@@ -373,7 +379,9 @@ int rn_options(uint32_t dt, int64_t H, unsigned fl, bool standalone, int32_t *ou
   out[n++] = P;
   if (P == RN_SCALAR || P == RN_LOOP) return n;
   if (P == RN_WAVE_1 || P == RN_WAVE_2) out[n++] = RN_BLOCK_1;
-  if (standalone) out[n++] = RN_LOOP;
+  if (!standalone) return n;
+  if (P == RN_BLOCK_8 || P == RN_BLOCK_16) out[n++] = RN_WIDE;
+  out[n++] = RN_LOOP;
   return n;
 }
 

@@ -159,6 +159,10 @@ RN_CASES = [
     (nm.BF16, 130, 4096, "plain"), (nm.F32, 100, 256, "plain"), (nm.BF16, 70, 8192, "plain"),
     (nm.F32, 65, 4096, "unaligned"), (nm.BF16, 66, 4096, "strided"), (nm.F32, 67, 16384, "plain"),
     (nm.BF16, 13, 1024, "plain"), (nm.BF16, 13, 1032, "plain"), (nm.F32, 7, 512, "plain"),
+    # rows beyond the register forms: staged in LDS up to 128 KiB, two passes beyond
+    (nm.BF16, 5, 40960, "plain"), (nm.BF16, 3, 65536, "strided"), (nm.BF16, 67, 49152, "plain"),
+    (nm.BF16, 2, 65544, "plain"), (nm.F32, 4, 20480, "plain"), (nm.F32, 3, 32768, "plain"),
+    (nm.F32, 2, 32772, "plain"), (nm.F32, 2, 131072, "plain"), (nm.BF16, 5, 40960, "unaligned"),
 ]
 
 

@@ -813,6 +813,26 @@ def _last_launch(lib, nbytes=512, size=None):
     return kv.value, dt.value, sub.value, grid.value, block.value, stream.value, buf.raw
 
 
+def test_wide_rows_launch_1024_work_item_workgroups(lib, fresh):
+    """Rows of 4097..8192 vectors take RN_WIDE: one 1024-work-item workgroup
+    per row (standalone, residual, and as the norm launch of a three-launch
+    chain); every other launch has 256 work-items. Launches and records
+    match the model's plan."""
+    cache = fresh(flags=S.FLAG_AUTO_INSTALL)
+    cases = [(rn_call(BF, 3, 65536), [S.RN_WIDE]), (res_call(F, 2, 20480), [S.RN_WIDE]),
+             (rn_call(BF, 3, 65544), [S.RN_LOOP]), (rn_call(BF, 3, 32768), [S.RN_BLOCK[16]]),
+             (chain_call(BF, 2, 40960, 11008, 32, 32, 128), [S.RN_WIDE, S.ROPE_VEC, S.SW_FLAT])]
+    for c, kinds in cases:
+        n0 = lib.trifake_launch_count()
+        assert c_call(lib, cache, c) == 0
+        got = [(l[0], l[3], l[4]) for l in (_launch_at(lib, i)
+                                             for i in range(n0, lib.trifake_launch_count()))]
+        want = [tuple(l) for l in S.plan(S.make_key(c), c.T)[2]]
+        assert got == want and [g[0] for g in got] == kinds, (c.op, c.H, got)
+        assert [g[2] for g in got] == [1024 if k == S.RN_WIDE else 256 for k in kinds]
+        assert [tuple(l) for l in c_record(lib, cache)[6][:len(want)]] == want
+
+
 def test_rmsnorm_argument_block_and_stream(lib, fresh):
     cache = fresh(flags=1)
     c = res_call(BF, 5, 4096, pad=64)

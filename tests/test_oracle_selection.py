@@ -122,10 +122,17 @@ def test_policy_tiny_f32_chain():
 @pytest.mark.parametrize("H,dtype,want", [
     (64, F, (11, 2)), (256, BF, (11, 2)), (520, BF, (12, 2)), (1024, BF, (12, 2)),
     (1032, BF, (13, 5)), (4096, F, (15, 5)), (8192, F, (16, 5)), (16384, F, (17, 5)),
-    (32768, BF, (17, 5)), (65536, BF, (18, 5)), (100, BF, (10, 5)), (4097, F, (10, 5))])
+    (32768, BF, (17, 5)), (100, BF, (10, 5)), (4097, F, (10, 5)),
+    # beyond 16 vectors per work-item (4096 vectors): a 1024-lane workgroup
+    # up to 8192 vectors (128 KiB) per row, two passes beyond
+    (32776, BF, (19, 5)), (65536, BF, (19, 5)), (65544, BF, (18, 5)),
+    (16388, F, (19, 5)), (32768, F, (19, 5)), (32772, F, (18, 5))])
 def test_rmsnorm_policy_by_row_size(H, dtype, want):
     # 5 rows: rows of <= 128 vectors take a wavefront each, 4 per block
-    # (2 blocks); longer rows one block per row (5 blocks).
+    # (2 blocks); longer rows one block per row (5 blocks). bf16 32776 =
+    # 4097 vectors: 17 per 256-lane work-item -> 1024 lanes; bf16 65536 =
+    # f32 32768 = exactly 8192 vectors -> 1024 lanes; 65544 bf16 / 32772
+    # f32 = 8193 vectors -> two passes.
     v, g = S.rn_role(dtype, H, S.ALIGN | S.CONTIG, 5)
     assert (v, g) == want
 

@@ -125,8 +125,11 @@ def test_unfused_chain_has_one_candidate():
     (512, BF, [11, 13, 18]),       # 64 vectors: wavefront, workgroup, loop
     (1024, BF, [12, 13, 18]),      # 128 vectors: two per lane of a wavefront
     (4096, BF, [14, 18]),          # 512 vectors: workgroup x 2, loop
-    (32768, BF, [17, 18]),         # 4096 vectors: workgroup x 16, loop
-    (65536, BF, [18]),             # 8192 vectors, beyond registers: loop only
+    (8200, BF, [16, 19, 18]),      # 1025 vectors: workgroup x 8, 1024-lane workgroup, loop
+    (32768, BF, [17, 19, 18]),     # 4096 vectors: workgroup x 16, 1024-lane workgroup, loop
+    (65536, BF, [19, 18]),         # 8192 vectors: 1024-lane workgroup x 8, loop
+    (65544, BF, [18]),             # 8193 vectors: loop only
+    (32768, F, [19, 18]),          # 8192 f32 vectors: 1024-lane workgroup x 8, loop
     (100, BF, [10]),               # ragged: scalar only
 ])
 def test_rmsnorm_candidates(H, dtype, want):
