@@ -37,12 +37,14 @@ class TriError(RuntimeError):
         super().__init__(f"{what}: {name} ({status})" if what else f"{name} ({status})")
 
 
+_DT = {torch.float32: F32, torch.bfloat16: BF16}
+
+
 def dtype_code(dt: torch.dtype) -> int:
-    if dt == torch.float32:
-        return F32
-    if dt == torch.bfloat16:
-        return BF16
-    raise TypeError(f"unsupported dtype {dt} (float32 or bfloat16)")
+    try:
+        return _DT[dt]
+    except KeyError:
+        raise TypeError(f"unsupported dtype {dt} (float32 or bfloat16)") from None
 
 
 def rope_ext(rotary_dim: int = 0, interleaved: bool = False, pos_int64: bool = False,
@@ -68,35 +70,67 @@ def rope_ext(rotary_dim: int = 0, interleaved: bool = False, pos_int64: bool = F
     return x
 
 
-def _pos_check(pos: torch.Tensor, ext: Optional[RopeExt]) -> None:
-    want = torch.int64 if ext is not None and ext.pos_int64 else torch.int32
-    if pos.dtype != want:
-        raise TypeError(f"pos must be {want}")
+# The raw handle of a device's current stream, without building a Stream
+# object (torch.cuda.current_stream() costs microseconds per call).
+_raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
 
 
-def _stream_ptr(stream) -> Optional[int]:
-    if stream is None:
-        stream = torch.cuda.current_stream()
-    return stream.cuda_stream or None
+def _stream_ptr(stream, device: int = -1) -> Optional[int]:
+    """hipStream_t of `stream`, or of the current stream of `device` (the
+    current device when -1); None for the null stream."""
+    if stream is not None:
+        return stream.cuda_stream or None
+    if device < 0:
+        device = torch.cuda.current_device()
+    if _raw_stream is not None:
+        return _raw_stream(device) or None
+    return torch.cuda.current_stream(device).cuda_stream or None
 
 
-def _rows(t: torch.Tensor, name: str) -> int:
-    """Row stride (elements) of a [T, W] tensor with unit inner stride."""
-    if t.dim() != 2:
-        raise ValueError(f"{name}: expected 2 dims, got {tuple(t.shape)}")
-    if t.shape[1] > 1 and t.stride(1) != 1:
+def _rows(t: torch.Tensor, name: str, W: int) -> int:
+    """Row stride (elements) of a [T, W] tensor with unit inner stride (the
+    caller has checked the shape); a single row reports at least W."""
+    st = t.stride()
+    if st[0] == W and st[1] == 1:
+        return W
+    sh = t.shape
+    if sh[1] > 1 and st[1] != 1:
         raise ValueError(f"{name}: inner stride must be 1")
-    return t.stride(0) if t.shape[0] > 1 else max(t.stride(0), t.shape[1])
+    return st[0] if sh[0] > 1 else max(st[0], sh[1])
 
 
-def _tokens(t: torch.Tensor, name: str) -> int:
-    """Token stride (elements) of a [T, heads, hd] tensor with heads packed."""
-    if t.dim() != 3:
-        raise ValueError(f"{name}: expected 3 dims, got {tuple(t.shape)}")
-    _, nh, hd = t.shape
-    if (hd > 1 and t.stride(2) != 1) or (nh > 1 and t.stride(1) != hd):
+def _tokens(t: torch.Tensor, name: str, nh: int, hd: int) -> int:
+    """Token stride (elements) of a [T, nh, hd] tensor with heads packed (the
+    caller has checked the shape); a single token reports at least nh * hd."""
+    st = t.stride()
+    if st[0] == nh * hd and st[1] == hd and st[2] == 1:
+        return nh * hd
+    sh = t.shape
+    if (hd > 1 and st[2] != 1) or (nh > 1 and st[1] != hd):
         raise ValueError(f"{name}: heads must be packed (stride {hd}) with unit inner stride")
-    return t.stride(0) if t.shape[0] > 1 else max(t.stride(0), nh * hd)
+    return st[0] if sh[0] > 1 else max(st[0], nh * hd)
+
+
+def _dims(t: torch.Tensor, name: str, n: int) -> tuple:
+    """The shape of `t`, which must have n dimensions."""
+    sh = t.shape
+    if len(sh) != n:
+        raise ValueError(f"{name}: expected {n} dims, got {tuple(sh)}")
+    return sh
+
+
+def _like(t: torch.Tensor, name: str, shape, dtype) -> None:
+    """`t` must have exactly `shape` and `dtype`: the kernels touch T rows of
+    the given width through it, and only the tensor knows its extent."""
+    if t.shape != shape or t.dtype != dtype:
+        raise ValueError(f"{name}: expected {tuple(shape)} {dtype}, got {tuple(t.shape)} {t.dtype}")
+
+
+def _vector(t: torch.Tensor, name: str, n: int, dtype) -> None:
+    """A weight: n contiguous elements of `dtype`."""
+    if t.shape != (n,) or t.dtype != dtype or (n > 1 and t.stride(0) != 1):
+        raise ValueError(f"{name}: expected a contiguous ({n},) {dtype} tensor, "
+                         f"got {tuple(t.shape)} {t.dtype}")
 
 
 class Graph:
@@ -111,7 +145,7 @@ class Graph:
         return _dll.tri_graph_launch_count(self._g)
 
     def launch(self, stream=None) -> None:
-        st = _dll.tri_graph_launch(self._g, _stream_ptr(stream))
+        st = _dll.tri_graph_launch(self._g, _stream_ptr(stream, self._cache._dev))
         if st != OK:
             raise TriError(st, "tri_graph_launch")
 
@@ -144,6 +178,7 @@ class SpecCache:
         if st != OK:
             raise TriError(st, "tri_spec_cache_create")
         self._h = h
+        self._dev = torch.cuda.current_device()   # the device the cache is bound to
         self.misses_handled = 0
         if code_dir is not None:
             st = _dll.tri_spec_set_code_dir(h, code_dir.encode())
@@ -189,51 +224,67 @@ class SpecCache:
     # ---- ops ---------------------------------------------------------------
     def rmsnorm(self, x: torch.Tensor, w: torch.Tensor, eps: float = 1e-6,
                 out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+        T, H = _dims(x, "x", 2)
         y = torch.empty_like(x) if out is None else out
-        T, H = x.shape
+        _like(y, "out", x.shape, x.dtype)
+        _vector(w, "w", H, x.dtype)
         self._call("tri_rmsnorm", _dll.tri_rmsnorm, dtype_code(x.dtype), x.data_ptr(),
-                   _rows(x, "x"), w.data_ptr(), y.data_ptr(), _rows(y, "y"), T, H, eps,
-                   _stream_ptr(stream))
+                   _rows(x, "x", H), w.data_ptr(), y.data_ptr(), _rows(y, "out", H), T, H, eps,
+                   _stream_ptr(stream, self._dev))
         return y
 
     def residual_rmsnorm(self, x, residual, w, eps: float = 1e-6, out=None, residual_out=None,
                          stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+        T, H = _dims(x, "x", 2)
+        _like(residual, "residual", x.shape, x.dtype)
         y = torch.empty_like(x) if out is None else out
         ro = torch.empty_like(residual) if residual_out is None else residual_out
-        T, H = x.shape
+        _like(y, "out", x.shape, x.dtype)
+        _like(ro, "residual_out", x.shape, x.dtype)
+        _vector(w, "w", H, x.dtype)
         self._call("tri_residual_rmsnorm", _dll.tri_residual_rmsnorm, dtype_code(x.dtype),
-                   x.data_ptr(), _rows(x, "x"), residual.data_ptr(), _rows(residual, "residual"),
-                   w.data_ptr(), y.data_ptr(), _rows(y, "out"), ro.data_ptr(),
-                   _rows(ro, "residual_out"), T, H, eps, _stream_ptr(stream))
+                   x.data_ptr(), _rows(x, "x", H), residual.data_ptr(),
+                   _rows(residual, "residual", H), w.data_ptr(), y.data_ptr(),
+                   _rows(y, "out", H), ro.data_ptr(), _rows(ro, "residual_out", H), T, H, eps,
+                   _stream_ptr(stream, self._dev))
         return y, ro
+
+    def _qk(self, q, k, pos, pos_dtype):
+        """Shapes of q [T, nq, hd], k [T, nk, hd] (or None) and pos [T]: returns
+        (T, nq, nk, hd, k pointer, k token stride)."""
+        T, nq, hd = _dims(q, "q", 3)
+        nk, kp, kts = 0, 0, 0
+        if k is not None:
+            _, nk, khd = _dims(k, "k", 3)
+            if k.shape[0] != T or khd != hd or k.dtype != q.dtype:
+                raise ValueError(f"k: expected ({T}, nk, {hd}) {q.dtype}, "
+                                 f"got {tuple(k.shape)} {k.dtype}")
+            if nk:
+                kp, kts = k.data_ptr(), _tokens(k, "k", nk, hd)
+        if pos.shape != (T,) or pos.dtype != pos_dtype or (T > 1 and pos.stride(0) != 1):
+            raise TypeError(f"pos must be a contiguous ({T},) {pos_dtype} tensor")
+        return T, nq, nk, hd, kp, kts
 
     def rope_qk(self, q, k, pos, base: float = 10000.0, stream=None):
         """In-place RoPE of q [T, nq, hd] and k [T, nk, hd] (k may be None)."""
-        T, nq, hd = q.shape
-        nk = 0 if k is None else k.shape[1]
-        kp = 0 if k is None or nk == 0 else k.data_ptr()
-        kts = 0 if k is None or nk == 0 else _tokens(k, "k")
-        if pos.dtype != torch.int32:
-            raise TypeError("pos must be int32")
+        T, nq, nk, hd, kp, kts = self._qk(q, k, pos, torch.int32)
         self._call("tri_rope_qk", _dll.tri_rope_qk, dtype_code(q.dtype), q.data_ptr(),
-                   _tokens(q, "q"), kp, kts, pos.data_ptr(), T, nq, nk, hd, base,
-                   _stream_ptr(stream))
+                   _tokens(q, "q", nq, hd), kp, kts, pos.data_ptr(), T, nq, nk, hd, base,
+                   _stream_ptr(stream, self._dev))
         return q, k
 
     def qk_norm_rope(self, q, k, pos, q_w, k_w=None, base: float = 10000.0, eps: float = 1e-6,
                      stream=None):
         """In-place per-head RMSNorm (weights q_w / k_w [hd]) then RoPE of
         q [T, nq, hd] and k [T, nk, hd] (k may be None)."""
-        T, nq, hd = q.shape
-        nk = 0 if k is None else k.shape[1]
-        kp = 0 if k is None or nk == 0 else k.data_ptr()
-        kts = 0 if k is None or nk == 0 else _tokens(k, "k")
-        if pos.dtype != torch.int32:
-            raise TypeError("pos must be int32")
+        T, nq, nk, hd, kp, kts = self._qk(q, k, pos, torch.int32)
+        _vector(q_w, "q_w", hd, q.dtype)
+        if k_w is not None:
+            _vector(k_w, "k_w", hd, q.dtype)
         kw = 0 if k_w is None else k_w.data_ptr()
         self._call("tri_qk_norm_rope", _dll.tri_qk_norm_rope, dtype_code(q.dtype), q.data_ptr(),
-                   _tokens(q, "q"), kp, kts, pos.data_ptr(), T, nq, nk, hd, base,
-                   q_w.data_ptr(), kw, eps, _stream_ptr(stream))
+                   _tokens(q, "q", nq, hd), kp, kts, pos.data_ptr(), T, nq, nk, hd, base,
+                   q_w.data_ptr(), kw, eps, _stream_ptr(stream, self._dev))
         return q, k
 
     def rope(self, q, k, pos, base: float = 10000.0, ext: Optional[RopeExt] = None, q_w=None,
@@ -241,66 +292,79 @@ class SpecCache:
         """In-place RoPE of q [T, nq, hd] and k [T, nk, hd] (k may be None)
         with an optional variant (`rope_ext(...)`) and, with q_w, the per-head
         QK RMSNorm first (tri_rope_qk_ext)."""
-        T, nq, hd = q.shape
-        nk = 0 if k is None else k.shape[1]
-        kp = 0 if k is None or nk == 0 else k.data_ptr()
-        kts = 0 if k is None or nk == 0 else _tokens(k, "k")
-        _pos_check(pos, ext)
+        pos_dt = torch.int64 if ext is not None and ext.pos_int64 else torch.int32
+        T, nq, nk, hd, kp, kts = self._qk(q, k, pos, pos_dt)
+        if q_w is not None:
+            _vector(q_w, "q_w", hd, q.dtype)
+        if k_w is not None:
+            _vector(k_w, "k_w", hd, q.dtype)
         self._call("tri_rope_qk_ext", _dll.tri_rope_qk_ext, dtype_code(q.dtype), q.data_ptr(),
-                   _tokens(q, "q"), kp, kts, pos.data_ptr(), T, nq, nk, hd, base,
+                   _tokens(q, "q", nq, hd), kp, kts, pos.data_ptr(), T, nq, nk, hd, base,
                    C.byref(ext) if ext is not None else None,
                    0 if q_w is None else q_w.data_ptr(), 0 if k_w is None else k_w.data_ptr(),
-                   eps, _stream_ptr(stream))
+                   eps, _stream_ptr(stream, self._dev))
         return q, k
 
     def swiglu(self, gate, up, out=None, stream=None) -> torch.Tensor:
+        T, I = _dims(gate, "gate", 2)
+        _like(up, "up", gate.shape, gate.dtype)
         o = torch.empty_like(gate) if out is None else out
-        T, I = gate.shape
+        _like(o, "out", gate.shape, gate.dtype)
         self._call("tri_swiglu", _dll.tri_swiglu, dtype_code(gate.dtype), gate.data_ptr(),
-                   _rows(gate, "gate"), up.data_ptr(), _rows(up, "up"), o.data_ptr(),
-                   _rows(o, "out"), T, I, _stream_ptr(stream))
+                   _rows(gate, "gate", I), up.data_ptr(), _rows(up, "up", I), o.data_ptr(),
+                   _rows(o, "out", I), T, I, _stream_ptr(stream, self._dev))
         return o
 
     # ---- short ops ---------------------------------------------------------------
     def silu(self, x, out=None, stream=None) -> torch.Tensor:
         """out = x / (1 + exp(-x)) over [T, W]."""
+        T, W = _dims(x, "x", 2)
         o = torch.empty_like(x) if out is None else out
-        T, W = x.shape
-        self._call("tri_silu", _dll.tri_silu, dtype_code(x.dtype), x.data_ptr(), _rows(x, "x"),
-                   o.data_ptr(), _rows(o, "out"), T, W, _stream_ptr(stream))
+        _like(o, "out", x.shape, x.dtype)
+        self._call("tri_silu", _dll.tri_silu, dtype_code(x.dtype), x.data_ptr(),
+                   _rows(x, "x", W), o.data_ptr(), _rows(o, "out", W), T, W,
+                   _stream_ptr(stream, self._dev))
         return o
 
     def add(self, a, b, out=None, stream=None) -> torch.Tensor:
         """out = a + b over [T, W] (one rounding)."""
+        T, W = _dims(a, "a", 2)
+        _like(b, "b", a.shape, a.dtype)
         o = torch.empty_like(a) if out is None else out
-        T, W = a.shape
-        self._call("tri_add", _dll.tri_add, dtype_code(a.dtype), a.data_ptr(), _rows(a, "a"),
-                   b.data_ptr(), _rows(b, "b"), o.data_ptr(), _rows(o, "out"), T, W,
-                   _stream_ptr(stream))
+        _like(o, "out", a.shape, a.dtype)
+        self._call("tri_add", _dll.tri_add, dtype_code(a.dtype), a.data_ptr(),
+                   _rows(a, "a", W), b.data_ptr(), _rows(b, "b", W), o.data_ptr(),
+                   _rows(o, "out", W), T, W, _stream_ptr(stream, self._dev))
         return o
 
     def masked_fill(self, x, mask, value: float, out=None, stream=None) -> torch.Tensor:
         """out = where(mask, value, x); mask is uint8 (or bool) [T, W]."""
         if mask.dtype not in (torch.uint8, torch.bool):
             raise TypeError("mask must be uint8 or bool")
+        T, W = _dims(x, "x", 2)
+        if mask.shape != x.shape:
+            raise ValueError(f"mask: expected {tuple(x.shape)}, got {tuple(mask.shape)}")
         o = torch.empty_like(x) if out is None else out
-        T, W = x.shape
+        _like(o, "out", x.shape, x.dtype)
         self._call("tri_masked_fill", _dll.tri_masked_fill, dtype_code(x.dtype), x.data_ptr(),
-                   _rows(x, "x"), mask.data_ptr(), _rows(mask, "mask"), value, o.data_ptr(),
-                   _rows(o, "out"), T, W, _stream_ptr(stream))
+                   _rows(x, "x", W), mask.data_ptr(), _rows(mask, "mask", W), value,
+                   o.data_ptr(), _rows(o, "out", W), T, W, _stream_ptr(stream, self._dev))
         return o
 
     def embedding(self, table, ids, out=None, stream=None) -> torch.Tensor:
         """out[t] = table[ids[t]] (zeros for ids out of range); ids int32 / int64."""
         if ids.dtype not in (torch.int32, torch.int64) or ids.dim() != 1:
             raise TypeError("ids must be a 1-D int32 or int64 tensor")
-        n_rows, H = table.shape
+        n_rows, H = _dims(table, "table", 2)
         T = ids.shape[0]
+        if T > 1 and ids.stride(0) != 1:
+            raise ValueError("ids must be contiguous")
         o = torch.empty((T, H), dtype=table.dtype, device=table.device) if out is None else out
+        _like(o, "out", (T, H), table.dtype)
         self._call("tri_embedding", _dll.tri_embedding, dtype_code(table.dtype),
-                   table.data_ptr(), _rows(table, "table"), n_rows, ids.data_ptr(),
-                   int(ids.dtype == torch.int64), o.data_ptr(), _rows(o, "out"), T, H,
-                   _stream_ptr(stream))
+                   table.data_ptr(), _rows(table, "table", H), n_rows, ids.data_ptr(),
+                   int(ids.dtype == torch.int64), o.data_ptr(), _rows(o, "out", H), T, H,
+                   _stream_ptr(stream, self._dev))
         return o
 
     def chain_args(self, x, residual, w, q, k, pos, gate, up, eps=1e-6, base=10000.0,
@@ -309,30 +373,42 @@ class SpecCache:
         """Build the tri_chain_args struct once (outputs allocated if absent).
         With q_norm_w (and k_norm_w) the RoPE step is QK-RMSNorm + RoPE with
         epsilon qk_eps (default: eps); `rope` selects a RoPE variant."""
-        _pos_check(pos, rope)
+        T, H = _dims(x, "x", 2)
+        dt = x.dtype
+        _like(residual, "residual", x.shape, dt)
+        _vector(w, "w", H, dt)
         y = torch.empty_like(x) if y is None else y
         ro = torch.empty_like(residual) if residual_out is None else residual_out
+        _like(y, "y", x.shape, dt)
+        _like(ro, "residual_out", x.shape, dt)
+        pos_dt = torch.int64 if rope is not None and rope.pos_int64 else torch.int32
+        Tq, nq, nk, hd, kp, kts = self._qk(q, k, pos, pos_dt)
+        if Tq != T or q.dtype != dt:
+            raise ValueError(f"q: expected ({T}, nq, hd) {dt}, got {tuple(q.shape)} {q.dtype}")
+        _, I = _dims(gate, "gate", 2)
+        _like(gate, "gate", (T, I), dt)
+        _like(up, "up", (T, I), dt)
         o = torch.empty_like(gate) if out is None else out
-        T, H = x.shape
+        _like(o, "out", (T, I), dt)
         a = ChainArgs()
-        a.dtype = dtype_code(x.dtype)
-        a.nq, a.hd = q.shape[1], q.shape[2]
-        a.nk = 0 if k is None else k.shape[1]
-        a.T, a.H, a.I = T, H, gate.shape[1]
+        a.dtype = dtype_code(dt)
+        a.T, a.H, a.I, a.nq, a.nk, a.hd = T, H, I, nq, nk, hd
         a.eps, a.base = eps, base
-        a.x, a.x_rs = x.data_ptr(), _rows(x, "x")
-        a.res, a.res_rs = residual.data_ptr(), _rows(residual, "residual")
+        a.x, a.x_rs = x.data_ptr(), _rows(x, "x", H)
+        a.res, a.res_rs = residual.data_ptr(), _rows(residual, "residual", H)
         a.w = w.data_ptr()
-        a.y, a.y_rs = y.data_ptr(), _rows(y, "y")
-        a.res_out, a.ro_rs = ro.data_ptr(), _rows(ro, "residual_out")
-        a.q, a.q_ts = q.data_ptr(), _tokens(q, "q")
-        if a.nk:
-            a.k, a.k_ts = k.data_ptr(), _tokens(k, "k")
+        a.y, a.y_rs = y.data_ptr(), _rows(y, "y", H)
+        a.res_out, a.ro_rs = ro.data_ptr(), _rows(ro, "residual_out", H)
+        a.q, a.q_ts = q.data_ptr(), _tokens(q, "q", nq, hd)
+        a.k, a.k_ts = kp, kts
         a.pos = pos.data_ptr()
-        a.gate, a.g_rs = gate.data_ptr(), _rows(gate, "gate")
-        a.up, a.u_rs = up.data_ptr(), _rows(up, "up")
-        a.out, a.o_rs = o.data_ptr(), _rows(o, "out")
+        a.gate, a.g_rs = gate.data_ptr(), _rows(gate, "gate", I)
+        a.up, a.u_rs = up.data_ptr(), _rows(up, "up", I)
+        a.out, a.o_rs = o.data_ptr(), _rows(o, "out", I)
         if q_norm_w is not None:
+            _vector(q_norm_w, "q_norm_w", hd, dt)
+            if k_norm_w is not None:
+                _vector(k_norm_w, "k_norm_w", hd, dt)
             a.q_norm_w = q_norm_w.data_ptr()
             a.k_norm_w = 0 if k_norm_w is None else k_norm_w.data_ptr()
             a.qk_eps = eps if qk_eps is None else qk_eps
@@ -343,14 +419,14 @@ class SpecCache:
 
     def decode_chain_args(self, args: ChainArgs, stream=None) -> None:
         self._call("tri_decode_chain", _dll.tri_decode_chain, C.byref(args),
-                   _stream_ptr(stream))
+                   _stream_ptr(stream, self._dev))
 
     def decode_chain_layers(self, layers, stream=None) -> None:
         """Several chains (a list of ChainArgs from chain_args) in one entry
         call, launched in list order (tri_decode_chain_layers)."""
         arr = (ChainArgs * max(1, len(layers)))(*layers)
         self._call("tri_decode_chain_layers", _dll.tri_decode_chain_layers, arr, len(layers),
-                   _stream_ptr(stream), max_misses=len(layers))
+                   _stream_ptr(stream, self._dev), max_misses=len(layers))
 
     def build_graph(self, layers) -> "Graph":
         """Capture the launches of decode_chain_layers(layers) into a HIP
@@ -418,7 +494,7 @@ class SpecCache:
             raise TriError(st, "tri_spec_install_key")
 
     def launch_empty(self, stream=None) -> None:
-        st = _dll.tri_launch_empty(self._h, _stream_ptr(stream))
+        st = _dll.tri_launch_empty(self._h, _stream_ptr(stream, self._dev))
         if st != OK:
             raise TriError(st, "tri_launch_empty")
 

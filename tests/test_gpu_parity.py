@@ -715,6 +715,47 @@ def test_invalid_arguments_raise_and_launch_nothing(tri, cache):
     assert cache.stats()["n_versions"] == 0
 
 
+def test_binding_rejects_mismatched_shapes_before_any_call(tri, cache):
+    """The C entry points see pointers and strides only; the binding checks
+    that every tensor has the shape and dtype the call implies (outputs with
+    too few rows, short or strided weights, mismatched operands) and raises
+    before calling the library."""
+    f32, bf16, i32 = torch.float32, torch.bfloat16, torch.int32
+    x = torch.zeros((4, 64), dtype=f32, device=DEV)
+    w = torch.ones(64, dtype=f32, device=DEV)
+    q = torch.zeros((4, 2, 64), dtype=f32, device=DEV)
+    k = torch.zeros((4, 1, 64), dtype=f32, device=DEV)
+    pos = torch.zeros(4, dtype=i32, device=DEV)
+    bad = [
+        lambda: cache.rmsnorm(x, w, out=torch.empty((3, 64), dtype=f32, device=DEV)),
+        lambda: cache.rmsnorm(x, torch.ones(32, dtype=f32, device=DEV)),
+        lambda: cache.rmsnorm(x, torch.ones(128, dtype=f32, device=DEV)[::2]),
+        lambda: cache.rmsnorm(x, w.to(bf16)),
+        lambda: cache.rmsnorm(x[0], w),
+        lambda: cache.residual_rmsnorm(x, x[:3], w),
+        lambda: cache.residual_rmsnorm(x, x, w, residual_out=torch.empty((4, 32), dtype=f32,
+                                                                          device=DEV)),
+        lambda: cache.swiglu(x, torch.zeros((4, 32), dtype=f32, device=DEV)),
+        lambda: cache.swiglu(x, x, out=torch.empty((2, 64), dtype=f32, device=DEV)),
+        lambda: cache.add(x, x, out=torch.empty((4, 64), dtype=bf16, device=DEV)),
+        lambda: cache.silu(x, out=torch.empty((5, 64), dtype=f32, device=DEV)),
+        lambda: cache.masked_fill(x, torch.zeros((4, 32), dtype=torch.uint8, device=DEV), 0.0),
+        lambda: cache.embedding(x, pos, out=torch.empty((3, 64), dtype=f32, device=DEV)),
+        lambda: cache.rope_qk(q, k, pos[:3]),
+        lambda: cache.rope_qk(q, k[:2], pos),
+        lambda: cache.rope_qk(q, torch.zeros((4, 1, 32), dtype=f32, device=DEV), pos),
+        lambda: cache.rope_qk(q, k, pos.to(torch.int64)),
+        lambda: cache.qk_norm_rope(q, k, pos, torch.ones(32, dtype=f32, device=DEV)),
+        lambda: cache.decode_chain(x, x, w, q, k, pos, x, x[:2]),
+        lambda: cache.decode_chain(x, x, w, q[:2], k[:2], pos[:2], x, x),
+    ]
+    for i, fn in enumerate(bad):
+        with pytest.raises((ValueError, TypeError)):
+            fn()
+    st = cache.stats()
+    assert st["calls"] == 0 and st["n_versions"] == 0
+
+
 # ---- full-size prefill chain, sampled ------------------------------------------------------
 @pytest.mark.parametrize("cfg,grid", [(wl.PREFILL_8K, 8192 + 8192 + 114688),
                                       (wl.PREFILL_8K_TP8, 8192 + 2048 + 14336)],
