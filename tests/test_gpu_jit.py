@@ -64,9 +64,12 @@ def test_jit_chain_equals_precompiled_bitwise(tri, cfg):
         jit.close()
 
 
-# Standalone ops through a JIT cache: the scalar, loop and vector forms.
+# Standalone ops through a JIT cache: the scalar, loop, wide (1024-lane) and
+# vector forms.
 OP_CASES = [
     ("rmsnorm", nm.BF16, 5, 4096, "plain"), ("rmsnorm", nm.F32, 3, 65536, "plain"),
+    ("rmsnorm", nm.BF16, 3, 65536, "plain"), ("residual", nm.F32, 4, 20480, "plain"),
+    ("residual", nm.BF16, 2, 40960, "strided"),
     ("rmsnorm", nm.BF16, 7, 4097, "plain"), ("rmsnorm", nm.F32, 9, 520, "unaligned"),
     ("residual", nm.BF16, 130, 4096, "plain"), ("residual", nm.F32, 6, 256, "strided"),
     ("swiglu", nm.BF16, 8, 14336, "plain"), ("swiglu", nm.F32, 130, 1000, "plain"),
