@@ -544,6 +544,12 @@ def main():
         emb_out = torch.empty((cfgb.T, cfgb.H // 2), device=dev, dtype=db["x"].dtype)
         copy_src = torch.empty(1 << 29, dtype=torch.bfloat16, device=dev)
         copy_dst = torch.empty_like(copy_src)
+        # long rows: bf16 [2048, 65536] (a 1024-work-item workgroup per row)
+        lx = torch.randn((2048, 65536), device=dev).to(db["x"].dtype)
+        lr, ly, lro = torch.randn_like(lx), torch.empty_like(lx), torch.empty_like(lx)
+        lw = (torch.rand(65536, device=dev) + 0.5).to(lx.dtype)
+        nbytes["rmsnorm_rows65536"] = 2 * lx.numel() * 2 + 65536 * 2
+        nbytes["residual_rmsnorm_rows65536"] = 4 * lx.numel() * 2 + 65536 * 2
         ops = {
             "chain": lambda: cb.decode_chain_args(ab, stream),
             "residual_rmsnorm": lambda: cb.residual_rmsnorm(db["x"], db["residual"], db["w"],
@@ -559,6 +565,9 @@ def main():
             "add": lambda: cb.add(db["x"], db["residual"], out=y, stream=stream),
             "masked_fill": lambda: cb.masked_fill(db["x"], mask, -1e4, out=y, stream=stream),
             "embedding": lambda: cb.embedding(table, ids, out=emb_out, stream=stream),
+            "rmsnorm_rows65536": lambda: cb.rmsnorm(lx, lw, cfgb.eps, out=ly, stream=stream),
+            "residual_rmsnorm_rows65536": lambda: cb.residual_rmsnorm(
+                lx, lr, lw, cfgb.eps, out=ly, residual_out=lro, stream=stream),
             "copy_1GiB_torch": lambda: copy_dst.copy_(copy_src),
         }
         n16 = copy_src.numel() * 2 // 16
@@ -653,6 +662,7 @@ def main():
                               "one-token RoPE blocks, streaming one-vector SwiGLU)",
                     "bytes_per_launch": ch["bytes"], "avg_launch_us": ch["mean_us"]}
         del db, y, ro, out, flush, copy_src, copy_dst, mask, table, ids, emb_out
+        del lx, lr, ly, lro, lw
 
     # ---- CPU oracle baseline (after all GPU work) ----------------------------------------
     cpu = None
