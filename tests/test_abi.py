@@ -59,3 +59,14 @@ def test_struct_layouts_match_the_header(tmp_path):
     want = [C.sizeof(L.Selection), C.sizeof(L.ChainArgs), C.sizeof(L.Stats),
             C.sizeof(L.VersionInfo), L.ChainArgs.pos.offset, L.Selection.key.offset]
     assert got == want
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """bench.py measures one GPU; --gpus N > 1 exits with status 2 and says
+    so, before touching torch or a device."""
+    import subprocess
+    import sys
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr and not r.stdout.strip()
