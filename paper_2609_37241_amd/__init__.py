@@ -67,7 +67,29 @@ def rope_ext(rotary_dim: int = 0, interleaved: bool = False, pos_int64: bool = F
             raise ValueError("cos_sin: contiguous float32 [n, rotary_dim] expected")
         x.cos_sin = cos_sin.data_ptr()
         x.cos_sin_len = cos_sin.shape[0]
+        # The struct holds only the table's address: keep the tensor alive as
+        # long as the struct, and remember its width and device for the
+        # checks of each call that uses it (_check_cos_sin).
+        x._cos_sin = cos_sin
     return x
+
+
+def _check_cos_sin(ext: Optional[RopeExt], hd: int, dev: int) -> None:
+    """A cos/sin table must be on the cache's device and exactly rd floats
+    wide (rd = rotary_dim, or hd when 0): the kernels read rd floats of a
+    row through the bare address, so a narrower table would be read past
+    its end."""
+    if ext is None or not ext.cos_sin:
+        return
+    t = getattr(ext, "_cos_sin", None)
+    if t is None:
+        raise ValueError("cos_sin: build the variant with rope_ext(cos_sin=...) so the "
+                         "table's width and device can be checked")
+    rd = ext.rotary_dim or hd
+    _on(t, "cos_sin", dev)
+    if t.shape[1] != rd:
+        raise ValueError(f"cos_sin: expected rows of {rd} floats (rotary_dim), "
+                         f"got {tuple(t.shape)}")
 
 
 # The raw handle of a device's current stream, without building a Stream
@@ -111,26 +133,39 @@ def _tokens(t: torch.Tensor, name: str, nh: int, hd: int) -> int:
     return st[0] if sh[0] > 1 else max(st[0], nh * hd)
 
 
-def _dims(t: torch.Tensor, name: str, n: int) -> tuple:
-    """The shape of `t`, which must have n dimensions."""
+def _on(t: torch.Tensor, name: str, dev: int) -> None:
+    """`t` must live on GPU `dev`, the device the cache is bound to: the C
+    entry points take bare device addresses, and a kernel handed a host
+    address or another GPU's memory would fault instead of failing a check."""
+    if t.get_device() != dev:
+        where = "the CPU" if t.device.type == "cpu" else str(t.device)
+        raise ValueError(f"{name}: tensor on {where}, expected cuda:{dev} (the cache's device)")
+
+
+def _dims(t: torch.Tensor, name: str, n: int, dev: int) -> tuple:
+    """The shape of `t`, which must have n dimensions and live on GPU `dev`."""
     sh = t.shape
     if len(sh) != n:
         raise ValueError(f"{name}: expected {n} dims, got {tuple(sh)}")
+    _on(t, name, dev)
     return sh
 
 
-def _like(t: torch.Tensor, name: str, shape, dtype) -> None:
-    """`t` must have exactly `shape` and `dtype`: the kernels touch T rows of
-    the given width through it, and only the tensor knows its extent."""
+def _like(t: torch.Tensor, name: str, shape, dtype, dev: int) -> None:
+    """`t` must have exactly `shape` and `dtype` and live on GPU `dev`: the
+    kernels touch T rows of the given width through it, and only the tensor
+    knows its extent."""
     if t.shape != shape or t.dtype != dtype:
         raise ValueError(f"{name}: expected {tuple(shape)} {dtype}, got {tuple(t.shape)} {t.dtype}")
+    _on(t, name, dev)
 
 
-def _vector(t: torch.Tensor, name: str, n: int, dtype) -> None:
-    """A weight: n contiguous elements of `dtype`."""
+def _vector(t: torch.Tensor, name: str, n: int, dtype, dev: int) -> None:
+    """A weight: n contiguous elements of `dtype` on GPU `dev`."""
     if t.shape != (n,) or t.dtype != dtype or (n > 1 and t.stride(0) != 1):
         raise ValueError(f"{name}: expected a contiguous ({n},) {dtype} tensor, "
                          f"got {tuple(t.shape)} {t.dtype}")
+    _on(t, name, dev)
 
 
 class Graph:
@@ -224,10 +259,10 @@ class SpecCache:
     # ---- ops ---------------------------------------------------------------
     def rmsnorm(self, x: torch.Tensor, w: torch.Tensor, eps: float = 1e-6,
                 out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
-        T, H = _dims(x, "x", 2)
+        T, H = _dims(x, "x", 2, self._dev)
         y = torch.empty_like(x) if out is None else out
-        _like(y, "out", x.shape, x.dtype)
-        _vector(w, "w", H, x.dtype)
+        _like(y, "out", x.shape, x.dtype, self._dev)
+        _vector(w, "w", H, x.dtype, self._dev)
         self._call("tri_rmsnorm", _dll.tri_rmsnorm, dtype_code(x.dtype), x.data_ptr(),
                    _rows(x, "x", H), w.data_ptr(), y.data_ptr(), _rows(y, "out", H), T, H, eps,
                    _stream_ptr(stream, self._dev))
@@ -235,13 +270,13 @@ class SpecCache:
 
     def residual_rmsnorm(self, x, residual, w, eps: float = 1e-6, out=None, residual_out=None,
                          stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
-        T, H = _dims(x, "x", 2)
-        _like(residual, "residual", x.shape, x.dtype)
+        T, H = _dims(x, "x", 2, self._dev)
+        _like(residual, "residual", x.shape, x.dtype, self._dev)
         y = torch.empty_like(x) if out is None else out
         ro = torch.empty_like(residual) if residual_out is None else residual_out
-        _like(y, "out", x.shape, x.dtype)
-        _like(ro, "residual_out", x.shape, x.dtype)
-        _vector(w, "w", H, x.dtype)
+        _like(y, "out", x.shape, x.dtype, self._dev)
+        _like(ro, "residual_out", x.shape, x.dtype, self._dev)
+        _vector(w, "w", H, x.dtype, self._dev)
         self._call("tri_residual_rmsnorm", _dll.tri_residual_rmsnorm, dtype_code(x.dtype),
                    x.data_ptr(), _rows(x, "x", H), residual.data_ptr(),
                    _rows(residual, "residual", H), w.data_ptr(), y.data_ptr(),
@@ -252,10 +287,10 @@ class SpecCache:
     def _qk(self, q, k, pos, pos_dtype):
         """Shapes of q [T, nq, hd], k [T, nk, hd] (or None) and pos [T]: returns
         (T, nq, nk, hd, k pointer, k token stride)."""
-        T, nq, hd = _dims(q, "q", 3)
+        T, nq, hd = _dims(q, "q", 3, self._dev)
         nk, kp, kts = 0, 0, 0
         if k is not None:
-            _, nk, khd = _dims(k, "k", 3)
+            _, nk, khd = _dims(k, "k", 3, self._dev)
             if k.shape[0] != T or khd != hd or k.dtype != q.dtype:
                 raise ValueError(f"k: expected ({T}, nk, {hd}) {q.dtype}, "
                                  f"got {tuple(k.shape)} {k.dtype}")
@@ -263,6 +298,7 @@ class SpecCache:
                 kp, kts = k.data_ptr(), _tokens(k, "k", nk, hd)
         if pos.shape != (T,) or pos.dtype != pos_dtype or (T > 1 and pos.stride(0) != 1):
             raise TypeError(f"pos must be a contiguous ({T},) {pos_dtype} tensor")
+        _on(pos, "pos", self._dev)
         return T, nq, nk, hd, kp, kts
 
     def rope_qk(self, q, k, pos, base: float = 10000.0, stream=None):
@@ -278,9 +314,9 @@ class SpecCache:
         """In-place per-head RMSNorm (weights q_w / k_w [hd]) then RoPE of
         q [T, nq, hd] and k [T, nk, hd] (k may be None)."""
         T, nq, nk, hd, kp, kts = self._qk(q, k, pos, torch.int32)
-        _vector(q_w, "q_w", hd, q.dtype)
+        _vector(q_w, "q_w", hd, q.dtype, self._dev)
         if k_w is not None:
-            _vector(k_w, "k_w", hd, q.dtype)
+            _vector(k_w, "k_w", hd, q.dtype, self._dev)
         kw = 0 if k_w is None else k_w.data_ptr()
         self._call("tri_qk_norm_rope", _dll.tri_qk_norm_rope, dtype_code(q.dtype), q.data_ptr(),
                    _tokens(q, "q", nq, hd), kp, kts, pos.data_ptr(), T, nq, nk, hd, base,
@@ -294,10 +330,11 @@ class SpecCache:
         QK RMSNorm first (tri_rope_qk_ext)."""
         pos_dt = torch.int64 if ext is not None and ext.pos_int64 else torch.int32
         T, nq, nk, hd, kp, kts = self._qk(q, k, pos, pos_dt)
+        _check_cos_sin(ext, hd, self._dev)
         if q_w is not None:
-            _vector(q_w, "q_w", hd, q.dtype)
+            _vector(q_w, "q_w", hd, q.dtype, self._dev)
         if k_w is not None:
-            _vector(k_w, "k_w", hd, q.dtype)
+            _vector(k_w, "k_w", hd, q.dtype, self._dev)
         self._call("tri_rope_qk_ext", _dll.tri_rope_qk_ext, dtype_code(q.dtype), q.data_ptr(),
                    _tokens(q, "q", nq, hd), kp, kts, pos.data_ptr(), T, nq, nk, hd, base,
                    C.byref(ext) if ext is not None else None,
@@ -306,10 +343,10 @@ class SpecCache:
         return q, k
 
     def swiglu(self, gate, up, out=None, stream=None) -> torch.Tensor:
-        T, I = _dims(gate, "gate", 2)
-        _like(up, "up", gate.shape, gate.dtype)
+        T, I = _dims(gate, "gate", 2, self._dev)
+        _like(up, "up", gate.shape, gate.dtype, self._dev)
         o = torch.empty_like(gate) if out is None else out
-        _like(o, "out", gate.shape, gate.dtype)
+        _like(o, "out", gate.shape, gate.dtype, self._dev)
         self._call("tri_swiglu", _dll.tri_swiglu, dtype_code(gate.dtype), gate.data_ptr(),
                    _rows(gate, "gate", I), up.data_ptr(), _rows(up, "up", I), o.data_ptr(),
                    _rows(o, "out", I), T, I, _stream_ptr(stream, self._dev))
@@ -318,9 +355,9 @@ class SpecCache:
     # ---- short ops ---------------------------------------------------------------
     def silu(self, x, out=None, stream=None) -> torch.Tensor:
         """out = x / (1 + exp(-x)) over [T, W]."""
-        T, W = _dims(x, "x", 2)
+        T, W = _dims(x, "x", 2, self._dev)
         o = torch.empty_like(x) if out is None else out
-        _like(o, "out", x.shape, x.dtype)
+        _like(o, "out", x.shape, x.dtype, self._dev)
         self._call("tri_silu", _dll.tri_silu, dtype_code(x.dtype), x.data_ptr(),
                    _rows(x, "x", W), o.data_ptr(), _rows(o, "out", W), T, W,
                    _stream_ptr(stream, self._dev))
@@ -328,10 +365,10 @@ class SpecCache:
 
     def add(self, a, b, out=None, stream=None) -> torch.Tensor:
         """out = a + b over [T, W] (one rounding)."""
-        T, W = _dims(a, "a", 2)
-        _like(b, "b", a.shape, a.dtype)
+        T, W = _dims(a, "a", 2, self._dev)
+        _like(b, "b", a.shape, a.dtype, self._dev)
         o = torch.empty_like(a) if out is None else out
-        _like(o, "out", a.shape, a.dtype)
+        _like(o, "out", a.shape, a.dtype, self._dev)
         self._call("tri_add", _dll.tri_add, dtype_code(a.dtype), a.data_ptr(),
                    _rows(a, "a", W), b.data_ptr(), _rows(b, "b", W), o.data_ptr(),
                    _rows(o, "out", W), T, W, _stream_ptr(stream, self._dev))
@@ -341,11 +378,12 @@ class SpecCache:
         """out = where(mask, value, x); mask is uint8 (or bool) [T, W]."""
         if mask.dtype not in (torch.uint8, torch.bool):
             raise TypeError("mask must be uint8 or bool")
-        T, W = _dims(x, "x", 2)
+        T, W = _dims(x, "x", 2, self._dev)
         if mask.shape != x.shape:
             raise ValueError(f"mask: expected {tuple(x.shape)}, got {tuple(mask.shape)}")
+        _on(mask, "mask", self._dev)
         o = torch.empty_like(x) if out is None else out
-        _like(o, "out", x.shape, x.dtype)
+        _like(o, "out", x.shape, x.dtype, self._dev)
         self._call("tri_masked_fill", _dll.tri_masked_fill, dtype_code(x.dtype), x.data_ptr(),
                    _rows(x, "x", W), mask.data_ptr(), _rows(mask, "mask", W), value,
                    o.data_ptr(), _rows(o, "out", W), T, W, _stream_ptr(stream, self._dev))
@@ -355,12 +393,13 @@ class SpecCache:
         """out[t] = table[ids[t]] (zeros for ids out of range); ids int32 / int64."""
         if ids.dtype not in (torch.int32, torch.int64) or ids.dim() != 1:
             raise TypeError("ids must be a 1-D int32 or int64 tensor")
-        n_rows, H = _dims(table, "table", 2)
+        n_rows, H = _dims(table, "table", 2, self._dev)
         T = ids.shape[0]
         if T > 1 and ids.stride(0) != 1:
             raise ValueError("ids must be contiguous")
+        _on(ids, "ids", self._dev)
         o = torch.empty((T, H), dtype=table.dtype, device=table.device) if out is None else out
-        _like(o, "out", (T, H), table.dtype)
+        _like(o, "out", (T, H), table.dtype, self._dev)
         self._call("tri_embedding", _dll.tri_embedding, dtype_code(table.dtype),
                    table.data_ptr(), _rows(table, "table", H), n_rows, ids.data_ptr(),
                    int(ids.dtype == torch.int64), o.data_ptr(), _rows(o, "out", H), T, H,
@@ -372,24 +411,31 @@ class SpecCache:
                    qk_eps=None, rope: Optional[RopeExt] = None) -> Tuple[ChainArgs, tuple]:
         """Build the tri_chain_args struct once (outputs allocated if absent).
         With q_norm_w (and k_norm_w) the RoPE step is QK-RMSNorm + RoPE with
-        epsilon qk_eps (default: eps); `rope` selects a RoPE variant."""
-        T, H = _dims(x, "x", 2)
+        epsilon qk_eps (default: eps); `rope` selects a RoPE variant.
+
+        The struct holds bare device addresses. It keeps a reference to every
+        tensor whose address it holds (inputs, weights, positions and the
+        outputs, including ones allocated here) and to the variant, so reusing
+        it (decode_chain_args, decode_chain_layers, build_graph) never reaches
+        freed memory; the tensors live at least as long as the struct."""
+        T, H = _dims(x, "x", 2, self._dev)
         dt = x.dtype
-        _like(residual, "residual", x.shape, dt)
-        _vector(w, "w", H, dt)
+        _like(residual, "residual", x.shape, dt, self._dev)
+        _vector(w, "w", H, dt, self._dev)
         y = torch.empty_like(x) if y is None else y
         ro = torch.empty_like(residual) if residual_out is None else residual_out
-        _like(y, "y", x.shape, dt)
-        _like(ro, "residual_out", x.shape, dt)
+        _like(y, "y", x.shape, dt, self._dev)
+        _like(ro, "residual_out", x.shape, dt, self._dev)
         pos_dt = torch.int64 if rope is not None and rope.pos_int64 else torch.int32
         Tq, nq, nk, hd, kp, kts = self._qk(q, k, pos, pos_dt)
         if Tq != T or q.dtype != dt:
             raise ValueError(f"q: expected ({T}, nq, hd) {dt}, got {tuple(q.shape)} {q.dtype}")
-        _, I = _dims(gate, "gate", 2)
-        _like(gate, "gate", (T, I), dt)
-        _like(up, "up", (T, I), dt)
+        _check_cos_sin(rope, hd, self._dev)
+        _, I = _dims(gate, "gate", 2, self._dev)
+        _like(gate, "gate", (T, I), dt, self._dev)
+        _like(up, "up", (T, I), dt, self._dev)
         o = torch.empty_like(gate) if out is None else out
-        _like(o, "out", (T, I), dt)
+        _like(o, "out", (T, I), dt, self._dev)
         a = ChainArgs()
         a.dtype = dtype_code(dt)
         a.T, a.H, a.I, a.nq, a.nk, a.hd = T, H, I, nq, nk, hd
@@ -406,15 +452,15 @@ class SpecCache:
         a.up, a.u_rs = up.data_ptr(), _rows(up, "up", I)
         a.out, a.o_rs = o.data_ptr(), _rows(o, "out", I)
         if q_norm_w is not None:
-            _vector(q_norm_w, "q_norm_w", hd, dt)
+            _vector(q_norm_w, "q_norm_w", hd, dt, self._dev)
             if k_norm_w is not None:
-                _vector(k_norm_w, "k_norm_w", hd, dt)
+                _vector(k_norm_w, "k_norm_w", hd, dt, self._dev)
             a.q_norm_w = q_norm_w.data_ptr()
             a.k_norm_w = 0 if k_norm_w is None else k_norm_w.data_ptr()
             a.qk_eps = eps if qk_eps is None else qk_eps
         if rope is not None:
             a.rope_ext = C.pointer(rope)
-            a._rope = rope          # keeps the variant alive as long as the args
+        a._keep = (x, residual, w, y, ro, q, k, pos, gate, up, o, q_norm_w, k_norm_w, rope)
         return a, (y, ro, o)
 
     def decode_chain_args(self, args: ChainArgs, stream=None) -> None:

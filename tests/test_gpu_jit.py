@@ -3,9 +3,11 @@ precompiled kernels and the CPU oracle.
 
 A specialization runs the same device body with the key's shape fields
 fixed at compile time, so on identical inputs it must produce the
-precompiled kernel's output bit for bit; the oracle comparison is repeated
-at the usual tolerance. Every case prints its name (pytest -v) before
-touching the GPU.
+precompiled kernel's output bit for bit. Every output of every case is also
+compared with the CPU oracle on its own (at the usual tolerance, bit for bit
+where the op is exact), so a specialization is never checked only against
+another HIP path. Every case prints its name (pytest -v) before touching
+the GPU.
 """
 import numpy as np
 import pytest
@@ -56,8 +58,9 @@ def test_jit_chain_equals_precompiled_bitwise(tri, cfg):
             check(n, host(g), host(h), cfg.dtype, exact=True)
         want = O.decode_chain(dict(inp, rope_ext=oracle_rope_kw(cfg.rope_ext))
                               if cfg.rope_ext else inp, cfg.eps, cfg.base, cfg.dtype)
-        check("out vs oracle", host(outs_j[2]), want["out"], cfg.dtype)
-        check("q vs oracle", host(b["q"]), want["q"], cfg.dtype)
+        for n, g in (("y", outs_j[0]), ("res_out", outs_j[1]), ("out", outs_j[2]),
+                     ("q", b["q"]), ("k", b["k"])):
+            check(f"{n} vs oracle", host(g), want[n], cfg.dtype, exact=n == "res_out")
     finally:
         torch.cuda.synchronize()
         pre.close()
@@ -86,6 +89,8 @@ def test_jit_ops_equal_precompiled_bitwise(tri, op, dtype, T, W, layout):
     x = wl.host_array(r, (T, W), dtype)
     x2 = wl.host_array(r, (T, W), dtype)
     w = wl.host_weight(r, W, dtype)
+    mask = (np.arange(T * W) % 3 == 0).astype(np.uint8).reshape(T, W)
+    ids = (np.arange(T) * 3 - 2).astype(np.int32)        # id -2 and ids past T: zero rows
     pre, jit = tri.SpecCache(), tri.SpecCache(jit=True)
     try:
         outs = []
@@ -104,11 +109,10 @@ def test_jit_ops_equal_precompiled_bitwise(tri, op, dtype, T, W, layout):
             elif op == "add":
                 outs.append((cache.add(xd, x2d, out=y),))
             elif op == "masked_fill":
-                m = torch.from_numpy((np.arange(T * W) % 3 == 0).astype(np.uint8).reshape(T, W))
-                outs.append((cache.masked_fill(xd, m.to(DEV), -5.5, out=y),))
+                outs.append((cache.masked_fill(xd, torch.from_numpy(mask).to(DEV), -5.5,
+                                               out=y),))
             elif op == "embedding":
-                ids = torch.arange(T, dtype=torch.int32, device=DEV) * 3 - 2
-                outs.append((cache.embedding(xd, ids),))
+                outs.append((cache.embedding(xd, torch.from_numpy(ids).to(DEV)),))
             else:
                 cache.swiglu(xd, x2d, out=y)
                 outs.append((y,))
@@ -116,10 +120,24 @@ def test_jit_ops_equal_precompiled_bitwise(tri, op, dtype, T, W, layout):
         assert jit.version_info(0).jit == 1
         for g, h in zip(outs[1], outs[0]):
             check(op, host(g), host(h), dtype, exact=True)
-        if op == "swiglu":
-            check("vs oracle", host(outs[1][0]), O.swiglu(x, x2, dtype), dtype)
-        elif op == "rmsnorm":
-            check("vs oracle", host(outs[1][0]), O.rmsnorm(x, w, 1e-6, dtype), dtype)
+        if op == "rmsnorm":
+            want = (O.rmsnorm(x, w, 1e-6, dtype),)
+        elif op == "residual":
+            want = O.residual_rmsnorm(x, x2, w, 1e-6, dtype)
+        elif op == "silu":
+            want = (O.silu(x, dtype),)
+        elif op == "add":
+            want = (O.add(x, x2, dtype),)
+        elif op == "masked_fill":
+            want = (O.masked_fill(x, mask, -5.5, dtype),)
+        elif op == "embedding":
+            want = (O.embedding(x, ids, dtype),)
+        else:
+            want = (O.swiglu(x, x2, dtype),)
+        exact = {"residual": (False, True), "add": (True,), "masked_fill": (True,),
+                 "embedding": (True,)}.get(op, (False,))
+        for i, (g, e) in enumerate(zip(want, exact)):
+            check(f"{op}[{i}] vs oracle", host(outs[1][i]), g, dtype, exact=e)
     finally:
         torch.cuda.synchronize()
         pre.close()
@@ -167,6 +185,10 @@ def test_jit_rope_equals_precompiled_bitwise(tri, dtype, T, nq, nk, hd, ext, qkn
         assert jit.version_info(0).jit == 1
         check("q", host(res[1][0]), host(res[0][0]), dtype, exact=True)
         check("k", host(res[1][1]), host(res[0][1]), dtype, exact=True)
+        wq, wk = O.rope_ext(q, k, host(pos), 5e5, dtype, q_w=qw if qkn else None,
+                            k_w=kw if qkn else None, eps=1e-6, **oracle_rope_kw(ext, table))
+        check("q vs oracle", host(res[1][0]), wq, dtype)
+        check("k vs oracle", host(res[1][1]), wk, dtype)
     finally:
         torch.cuda.synchronize()
         pre.close()

@@ -756,11 +756,79 @@ def test_binding_rejects_mismatched_shapes_before_any_call(tri, cache):
     assert st["calls"] == 0 and st["n_versions"] == 0
 
 
-# ---- full-size prefill chain, sampled ------------------------------------------------------
+def test_binding_rejects_host_tensors_and_narrow_cos_sin_tables(tri, cache):
+    """Every tensor must live on the cache's device (a kernel handed a host
+    address would fault), and a cos/sin table must be exactly rotary_dim
+    floats wide (a narrower one would be read past its end): the binding
+    raises before any native call."""
+    f32, i32 = torch.float32, torch.int32
+    x = torch.zeros((4, 64), dtype=f32, device=DEV)
+    w = torch.ones(64, dtype=f32, device=DEV)
+    q = torch.zeros((4, 2, 64), dtype=f32, device=DEV)
+    k = torch.zeros((4, 1, 64), dtype=f32, device=DEV)
+    pos = torch.zeros(4, dtype=i32, device=DEV)
+    m = torch.zeros((4, 64), dtype=torch.uint8, device=DEV)
+    cpu = lambda t: t.cpu()                                          # noqa: E731
+    narrow = tri.rope_ext(cos_sin=torch.zeros((16, 32), dtype=f32, device=DEV))
+    host_tab = tri.rope_ext(cos_sin=torch.zeros((16, 64), dtype=f32))
+    bad = [
+        lambda: cache.rmsnorm(cpu(x), w),
+        lambda: cache.rmsnorm(x, cpu(w)),
+        lambda: cache.rmsnorm(x, w, out=cpu(x)),
+        lambda: cache.residual_rmsnorm(x, cpu(x), w),
+        lambda: cache.swiglu(x, cpu(x)),
+        lambda: cache.silu(cpu(x)),
+        lambda: cache.add(x, cpu(x)),
+        lambda: cache.masked_fill(x, cpu(m), 1.0),
+        lambda: cache.embedding(x, cpu(pos)),
+        lambda: cache.rope_qk(q, k, cpu(pos)),
+        lambda: cache.rope_qk(q, cpu(k), pos),
+        lambda: cache.qk_norm_rope(q, k, pos, cpu(w)),
+        lambda: cache.rope(q, k, pos, ext=narrow),
+        lambda: cache.rope(q, k, pos, ext=host_tab),
+        lambda: cache.decode_chain(x, x, w, q, k, cpu(pos), x, x),
+        lambda: cache.decode_chain(x, x, w, q, k, pos, x, x, rope=narrow),
+    ]
+    for i, fn in enumerate(bad):
+        with pytest.raises(ValueError):
+            fn()
+    st = cache.stats()
+    assert st["calls"] == 0 and st["n_versions"] == 0
+
+
+def test_chain_args_keep_their_tensors_alive(tri, cache):
+    """A prebuilt argument struct holds bare addresses; it keeps every tensor
+    behind them alive (the outputs it allocated included), so a later call
+    through it never writes into memory the allocator has handed out again."""
+    import gc
+    import weakref
+    cfg = wl.TINY_F32
+    d = {k: wl.to_torch(v, cfg.dtype, DEV) for k, v in wl.host_inputs(cfg).items()}
+    args, outs = cache.chain_args(d["x"], d["residual"], d["w"], d["q"], d["k"], d["pos"],
+                                  d["gate"], d["up"], cfg.eps, cfg.base)
+    refs = [weakref.ref(t) for t in list(d.values()) + list(outs)]
+    del d, outs
+    gc.collect()
+    assert all(r() is not None for r in refs)
+    cache.decode_chain_args(args)
+    torch.cuda.synchronize()
+    y, ro, out = (r() for r in refs[-3:])
+    inp = {k: wl.from_torch(r()) for k, r in zip(("x", "residual", "w"), refs[:3])}
+    wy, wh = O.residual_rmsnorm(inp["x"], inp["residual"], inp["w"], cfg.eps, cfg.dtype)
+    check("y", host(y), wy, cfg.dtype)
+    check("res_out", host(ro), wh, cfg.dtype, exact=True)
+    del args, y, ro, out
+    gc.collect()
+    assert all(r() is None for r in refs)
+
+
+# ---- full-size prefill chain, every row --------------------------------------------------
 @pytest.mark.parametrize("cfg,grid", [(wl.PREFILL_8K, 8192 + 8192 + 114688),
                                       (wl.PREFILL_8K_TP8, 8192 + 2048 + 14336)],
                          ids=lambda c: c.name if hasattr(c, "name") else str(c))
-def test_prefill_chain_full_size_sampled(tri, cache, cfg, grid):
+def test_prefill_chain_full_size_all_rows(tri, cache, cfg, grid):
+    """The 8192-token chains in the benchmark's launch configuration; every
+    row of every output against the oracle, 512 rows at a time."""
     d = wl.device_inputs(cfg, DEV)
     src = {k: v.clone() for k, v in d.items() if k in ("q", "k")}
     y, ro, out = cache.decode_chain(d["x"], d["residual"], d["w"], d["q"], d["k"], d["pos"],
@@ -768,30 +836,35 @@ def test_prefill_chain_full_size_sampled(tri, cache, cfg, grid):
     torch.cuda.synchronize()
     rec = cache.last_selection()
     assert rec.variant == S.CH_FUSED and rec.launch[0].grid_x == grid
-    rows = np.sort(rng(99).choice(cfg.T, size=40, replace=False))
-    rows = np.concatenate([[0, 1, 2, 3, cfg.T - 1], rows])
-    ri = torch.from_numpy(rows).to(DEV)
-    x, r, w = host(d["x"][ri]), host(d["residual"][ri]), host(d["w"])
-    wy, wh = O.residual_rmsnorm(x, r, w, cfg.eps, cfg.dtype)
-    check("y", host(y[ri]), wy, cfg.dtype)
-    check("res_out", host(ro[ri]), wh, cfg.dtype, exact=True)
-    pos = host(d["pos"][ri])
-    wq, wk = O.rope_qk(host(src["q"][ri]), host(src["k"][ri]), pos, cfg.base, cfg.dtype)
-    check("q", host(d["q"][ri]), wq, cfg.dtype)
-    check("k", host(d["k"][ri]), wk, cfg.dtype)
-    check("out", host(out[ri]), O.swiglu(host(d["gate"][ri]), host(d["up"][ri]), cfg.dtype),
-          cfg.dtype)
+    w = host(d["w"])
+    for r0 in range(0, cfg.T, 512):
+        sl = slice(r0, min(cfg.T, r0 + 512))
+        wy, wh = O.residual_rmsnorm(host(d["x"][sl]), host(d["residual"][sl]), w, cfg.eps,
+                                    cfg.dtype)
+        check(f"y {sl}", host(y[sl]), wy, cfg.dtype)
+        check(f"res_out {sl}", host(ro[sl]), wh, cfg.dtype, exact=True)
+        wq, wk = O.rope_qk(host(src["q"][sl]), host(src["k"][sl]), host(d["pos"][sl]),
+                           cfg.base, cfg.dtype)
+        check(f"q {sl}", host(d["q"][sl]), wq, cfg.dtype)
+        check(f"k {sl}", host(d["k"][sl]), wk, cfg.dtype)
+        check(f"out {sl}", host(out[sl]),
+              O.swiglu(host(d["gate"][sl]), host(d["up"][sl]), cfg.dtype), cfg.dtype)
 
 
 # ---- mixed-shape stream -----------------------------------------------------------------------
 def test_mixed_stream_selection_and_outputs(tri, cache):
-    """The first 400 calls of the mixed stream on real buffers: every selection
-    record against the oracle's model, outputs against the oracle every 20th."""
+    """All 10,000 calls of the mixed stream on real buffers: every selection
+    record against the oracle's model, outputs against the oracle every 50th
+    call (and on every miss)."""
     Tmax = max(wl.MIXED_T_CHOICES)
     H, I, nq, nk, hd = wl.MIXED_H, wl.MIXED_I, wl.MIXED_NQ, wl.MIXED_NK, wl.MIXED_HD
     bufs = {}
     model = S.SpecCacheModel()
-    for n, (T, dt, layout) in enumerate(wl.mixed_stream(n=400)):
+    stream = wl.mixed_stream()
+    assert len(stream) == wl.MIXED_CALLS
+    for n, (T, dt, layout) in enumerate(stream):
+        if n % 1000 == 0:
+            print(f"mixed stream: call {n}", flush=True)
         key = (dt, layout)
         if key not in bufs:
             r = rng(len(bufs) + 1)
@@ -808,14 +881,15 @@ def test_mixed_stream_selection_and_outputs(tri, cache):
         h, dd = bufs[key]
         d = {k: v[:T] for k, v in dd.items() if k != "w"}
         d["w"] = dd["w"]
-        check_out = n % 20 == 0
+        call = model_chain_call(d, 1e-6, wl.MIXED_BASE)
+        missed = model.call(call) == S.MISS
+        check_out = missed or n % 50 == 0
         if check_out:
             q0, k0 = host(d["q"]), host(d["k"])
         cache.decode_chain(d["x"], d["residual"], d["w"], d["q"], d["k"], d["pos"], d["gate"],
                            d["up"], 1e-6, wl.MIXED_BASE, y=d["y"], residual_out=d["res_out"],
                            out=d["out"])
-        call = model_chain_call(d, 1e-6, wl.MIXED_BASE)
-        if model.call(call) == S.MISS:
+        if missed:
             model.install_last_miss()
             model.call(call)
         assert cache.last_selection().as_tuple() == model.last.as_tuple(), (n, T, dt, layout)
