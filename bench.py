@@ -346,6 +346,10 @@ def main():
     bench.trib_stream.argtypes = [C.c_void_p, C.c_void_p, C.c_int, C.c_void_p,
                                   C.POINTER(C.c_double), C.POINTER(C.c_int)]
     bench.trib_copy.argtypes = [C.c_void_p, C.c_void_p, C.c_int64, C.c_int, C.c_void_p]
+    bench.trib_mix.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int64,
+                                  C.c_int, C.c_int, C.c_void_p]
+    bench.trib_chain_mix.argtypes = [C.c_void_p] * 9 + [C.c_int64] * 5 + [C.c_int,
+                                                                              C.c_void_p]
     stream = torch.cuda.Stream(device=dev)
     sptr = stream.cuda_stream
 
@@ -662,11 +666,11 @@ def main():
                                                         n16, f, sptr))
             nbytes[name] = 2 * copy_src.numel() * 2
         nbytes["copy_1GiB_torch"] = 2 * copy_src.numel() * 2
-        bandwidth = {}
-        for name, fn in ops.items():
-            with torch.cuda.stream(stream):
-                fn()                                 # install / warm
-            torch.cuda.synchronize()
+        def flushed_times(fn, n_launch=1):
+            """µs per launch of fn, each repetition after the read flush; with
+            n_launch > 1, that many back-to-back launches per repetition (the
+            steady state, where each launch also pays for the write-back of
+            the previous one's dirty lines)."""
             times = []
             for _ in range(args.bw_reps):
                 with torch.cuda.stream(stream):
@@ -674,10 +678,19 @@ def main():
                     s_ev = torch.cuda.Event(enable_timing=True)
                     e_ev = torch.cuda.Event(enable_timing=True)
                     s_ev.record(stream)
-                    fn()
+                    for _ in range(n_launch):
+                        fn()
                     e_ev.record(stream)
                 e_ev.synchronize()
-                times.append(s_ev.elapsed_time(e_ev) * 1e3)   # µs
+                times.append(s_ev.elapsed_time(e_ev) * 1e3 / n_launch)   # µs
+            return times
+
+        bandwidth = {}
+        for name, fn in ops.items():
+            with torch.cuda.stream(stream):
+                fn()                                 # install / warm
+            torch.cuda.synchronize()
+            times = flushed_times(fn)
             mean_us = statistics.fmean(times)
             gbs = nbytes[name] / (mean_us * 1e-6) / 1e9
             bandwidth[name] = {"bytes": nbytes[name], "mean_us": mean_us,
@@ -706,6 +719,72 @@ def main():
             cgbs = 32 * half16 / (statistics.fmean(times) * 1e-6) / 1e9
             bandwidth[name]["copy_same_bytes_GB/s"] = cgbs
             bandwidth[name]["frac_of_copy_same_bytes"] = bandwidth[name]["GB/s"] / cgbs
+        # Matched ceilings: reference streams with each op's own read:write
+        # mix over its own byte count (its own buffers where the mix allows),
+        # best of cached and nontemporal; for the chain, its whole traffic
+        # pattern (role layout included) with the arithmetic removed. Run
+        # after the op timings: the references overwrite q and k.
+        E = 2                                         # bf16
+        TH16 = cfgb.T * cfgb.H * E // 16
+        TI16 = cfgb.T * cfgb.I * E // 16
+        QK16 = cfgb.T * (cfgb.nq + cfgb.nk) * cfgb.hd * E // 16
+        L16 = lx.numel() * E // 16
+        P = lambda t: t.data_ptr()                   # noqa: E731
+        matched = {
+            "residual_rmsnorm": ("2 reads : 2 writes", 3, P(db["x"]), P(db["residual"]), P(y),
+                                 P(ro), TH16),
+            "rmsnorm": ("1 read : 1 write", 0, P(db["x"]), None, P(y), None, TH16),
+            "rope_qk": ("in place", 1, P(copy_src), None, None, None, QK16),
+            "qk_norm_rope": ("in place", 1, P(copy_src), None, None, None, QK16),
+            "swiglu": ("2 reads : 1 write", 2, P(db["gate"]), P(db["up"]), P(out), None, TI16),
+            "silu": ("1 read : 1 write", 0, P(db["x"]), None, P(y), None, TH16),
+            "add": ("2 reads : 1 write", 2, P(db["x"]), P(db["residual"]), P(y), None, TH16),
+            "masked_fill": ("1 read : 1 write (mask bytes not streamed)", 0, P(db["x"]), None,
+                            P(y), None, TH16),
+            "embedding": ("1 read : 1 write (contiguous)", 0, P(copy_src), None, P(copy_dst),
+                          None, emb_out.numel() * E // 16),
+            "rmsnorm_rows65536": ("1 read : 1 write", 0, P(lx), None, P(ly), None, L16),
+            "residual_rmsnorm_rows65536": ("2 reads : 2 writes", 3, P(lx), P(lr), P(ly), P(lro),
+                                           L16),
+        }
+        nio = {0: 2, 1: 2, 2: 3, 3: 4}
+        for name, (mix, kind, i0, i1, o0, o1, n) in matched.items():
+            best = 0.0
+            for nt in (0, 1):
+                f = (lambda k=kind, a=i0, b=i1, c=o0, d=o1, m=n, t=nt:
+                     bench.trib_mix(a, b, c, d, m, k, t, sptr))
+                assert f() == 0
+                gbs_ = nio[kind] * 16 * n / (statistics.fmean(flushed_times(f)) * 1e-6) / 1e9
+                best = max(best, gbs_)
+            bandwidth[name]["matched_ceiling"] = mix
+            bandwidth[name]["matched_ceiling_GB/s"] = best
+            bandwidth[name]["frac_of_matched_ceiling"] = bandwidth[name]["GB/s"] / best
+
+        def chain_stream(c, d_, yy, rr, oo):
+            return lambda: bench.trib_chain_mix(
+                P(d_["x"]), P(d_["residual"]), P(yy), P(rr), P(d_["q"]), P(d_["k"]),
+                P(d_["gate"]), P(d_["up"]), P(oo), c.T, c.H, c.nq * c.hd, c.nk * c.hd, c.I, E,
+                sptr)
+
+        # the chain against its parts: three launches in one timed region,
+        # and the steady state (10 back-to-back launches per repetition)
+        parts = (ops["residual_rmsnorm"], ops["rope_qk"], ops["swiglu"])
+        seq = lambda: [f() for f in parts]          # noqa: E731
+        ch = bandwidth["chain"]
+        ch["three_launches_one_region_us"] = statistics.fmean(flushed_times(seq))
+        ch["sum_of_parts_us"] = sum(bandwidth[n]["mean_us"] for n in ("residual_rmsnorm",
+                                                                     "rope_qk", "swiglu"))
+        ch["steady_us"] = statistics.fmean(flushed_times(ops["chain"], 10))
+        ch["steady_GB/s"] = ch["bytes"] / (ch["steady_us"] * 1e-6) / 1e9
+        ch["three_launches_steady_us"] = statistics.fmean(flushed_times(seq, 10))
+        ch["swiglu_steady_us"] = statistics.fmean(flushed_times(ops["swiglu"], 10))
+        for name in ("chain", "chain_qk_norm"):
+            f = chain_stream(cfgb, db, y, ro, out)
+            assert f() == 0
+            cg = bandwidth[name]["bytes"] / (statistics.fmean(flushed_times(f)) * 1e-6) / 1e9
+            bandwidth[name]["matched_ceiling"] = "the chain's traffic and role layout, no arithmetic"
+            bandwidth[name]["matched_ceiling_GB/s"] = cg
+            bandwidth[name]["frac_of_matched_ceiling"] = bandwidth[name]["GB/s"] / cg
         # one GPU's share under 8-way tensor parallelism (replicated norm, split
         # heads and SwiGLU columns): the same fused kernel at the shard's shape
         cfs = wl.PREFILL_8K_TP8
@@ -718,23 +797,18 @@ def main():
         with torch.cuda.stream(stream):
             cb.decode_chain_args(a_s, stream)
         torch.cuda.synchronize()
-        times = []
-        for _ in range(args.bw_reps):
-            with torch.cuda.stream(stream):
-                flush.sum()
-                s_ev = torch.cuda.Event(enable_timing=True)
-                e_ev = torch.cuda.Event(enable_timing=True)
-                s_ev.record(stream)
-                cb.decode_chain_args(a_s, stream)
-                e_ev.record(stream)
-            e_ev.synchronize()
-            times.append(s_ev.elapsed_time(e_ev) * 1e3)
+        times = flushed_times(lambda: cb.decode_chain_args(a_s, stream))
         nb_s = algorithmic_bytes(cfs)["chain"]
         mean_us = statistics.fmean(times)
         gbs = nb_s / (mean_us * 1e-6) / 1e9
+        f = chain_stream(cfs, ds, y, ro, outs_)
+        assert f() == 0
+        cg = nb_s / (statistics.fmean(flushed_times(f)) * 1e-6) / 1e9
         bandwidth["chain_tp8_shard"] = {"bytes": nb_s, "mean_us": mean_us,
                                         "median_us": statistics.median(times), "GB/s": gbs,
                                         "frac_of_peak": gbs / HBM_PEAK_GBS,
+                                        "matched_ceiling_GB/s": cg,
+                                        "frac_of_matched_ceiling": gbs / cg,
                                         "workload": cfs.name}
         del ds, outs_
         ch = bandwidth["chain"]
@@ -743,8 +817,11 @@ def main():
         roofline = {"bound": "hbm", "achieved": ch["GB/s"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                     "frac": ch["GB/s"] / HBM_PEAK_GBS, "traffic": measured_traffic(),
                     "copy_ceiling_GBs": ceiling, "frac_of_copy_ceiling": ch["GB/s"] / ceiling,
+                    "matched_ceiling_GBs": ch["matched_ceiling_GB/s"],
+                    "frac_of_matched_ceiling": ch["frac_of_matched_ceiling"],
+                    "steady_state_GBs": ch["steady_GB/s"],
                     "kernel": "fused decode chain, 8192 tokens (k_chain: block-per-row norm, "
-                              "one-token RoPE blocks, streaming one-vector SwiGLU)",
+                              "one-token streaming RoPE blocks, streaming one-vector SwiGLU)",
                     "bytes_per_launch": ch["bytes"], "avg_launch_us": ch["mean_us"]}
         del db, y, ro, out, flush, copy_src, copy_dst, mask, table, ids, emb_out
         del lx, lr, ly, lro, lw

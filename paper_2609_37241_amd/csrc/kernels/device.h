@@ -1077,6 +1077,14 @@ __device__ __forceinline__ void body_emb(const EmbArgs &a) {
 // (2.75 vs 3.1 us device time at 1 token); at 8192 tokens this order with a
 // one-vector nontemporal SwiGLU role measured 331.5 us, against 344-349 us
 // for SwiGLU first or with two / four vectors per work-item.
+//
+// In the streaming form (NT: calls that move more than the last-level
+// cache) the RoPE role also streams nontemporally and keeps one head item
+// per work-item in flight instead of four: its 77 registers per lane
+// (four items) capped the whole fused kernel at 6 wavefronts per SIMD where
+// SwiGLU alone runs 8, and in alternating launches at 8192 tokens the
+// lighter role took the chain from 357 to 346.5 us (the decode form keeps
+// four items in flight, which its latency needs).
 template <int DT, bool WAVE, int N>
 __device__ __forceinline__ void chain_norm_role(const ChainArgs &a, uint32_t blk) {
   if constexpr (WAVE) {
@@ -1095,7 +1103,7 @@ __device__ __forceinline__ void body_chain(const ChainArgs &a) {
   if (b < R) {
     chain_norm_role<DT, WAVE, N>(a, b);
   } else if (b < R + P) {
-    rope_vec_block<DT, false, 4, QKN, INTER>(a.rope, b - R, lds);
+    rope_vec_block<DT, NT, NT ? 1 : 4, QKN, INTER>(a.rope, b - R, lds);
   } else {
     sw_flat_part<DT, 1, NT>(a.sw, b - R - P, S);
   }
