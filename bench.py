@@ -633,12 +633,17 @@ def main():
         emb_out = torch.empty((cfgb.T, cfgb.H // 2), device=dev, dtype=db["x"].dtype)
         copy_src = torch.empty(1 << 29, dtype=torch.bfloat16, device=dev)
         copy_dst = torch.empty_like(copy_src)
-        # long rows: bf16 [2048, 65536] (a 1024-work-item workgroup per row)
+        # long rows: bf16 [2048, 65536] and the same memory as [1024, 131072]
+        # (each row split over 4 / 8 workgroups that exchange partial sums)
         lx = torch.randn((2048, 65536), device=dev).to(db["x"].dtype)
         lr, ly, lro = torch.randn_like(lx), torch.empty_like(lx), torch.empty_like(lx)
         lw = (torch.rand(65536, device=dev) + 0.5).to(lx.dtype)
         nbytes["rmsnorm_rows65536"] = 2 * lx.numel() * 2 + 65536 * 2
         nbytes["residual_rmsnorm_rows65536"] = 4 * lx.numel() * 2 + 65536 * 2
+        lw2 = (torch.rand(131072, device=dev) + 0.5).to(lx.dtype)
+        v2 = lambda t: t.view(1024, 131072)          # noqa: E731
+        nbytes["rmsnorm_rows131072"] = 2 * lx.numel() * 2 + 131072 * 2
+        nbytes["residual_rmsnorm_rows131072"] = 4 * lx.numel() * 2 + 131072 * 2
         ops = {
             "chain": lambda: cb.decode_chain_args(ab, stream),
             "residual_rmsnorm": lambda: cb.residual_rmsnorm(db["x"], db["residual"], db["w"],
@@ -657,6 +662,10 @@ def main():
             "rmsnorm_rows65536": lambda: cb.rmsnorm(lx, lw, cfgb.eps, out=ly, stream=stream),
             "residual_rmsnorm_rows65536": lambda: cb.residual_rmsnorm(
                 lx, lr, lw, cfgb.eps, out=ly, residual_out=lro, stream=stream),
+            "rmsnorm_rows131072": lambda: cb.rmsnorm(v2(lx), lw2, cfgb.eps, out=v2(ly),
+                                                     stream=stream),
+            "residual_rmsnorm_rows131072": lambda: cb.residual_rmsnorm(
+                v2(lx), v2(lr), lw2, cfgb.eps, out=v2(ly), residual_out=v2(lro), stream=stream),
             "copy_1GiB_torch": lambda: copy_dst.copy_(copy_src),
         }
         n16 = copy_src.numel() * 2 // 16
@@ -746,6 +755,9 @@ def main():
             "rmsnorm_rows65536": ("1 read : 1 write", 0, P(lx), None, P(ly), None, L16),
             "residual_rmsnorm_rows65536": ("2 reads : 2 writes", 3, P(lx), P(lr), P(ly), P(lro),
                                            L16),
+            "rmsnorm_rows131072": ("1 read : 1 write", 0, P(lx), None, P(ly), None, L16),
+            "residual_rmsnorm_rows131072": ("2 reads : 2 writes", 3, P(lx), P(lr), P(ly),
+                                            P(lro), L16),
         }
         nio = {0: 2, 1: 2, 2: 3, 3: 4}
         for name, (mix, kind, i0, i1, o0, o1, n) in matched.items():
@@ -824,7 +836,7 @@ def main():
                               "one-token streaming RoPE blocks, streaming one-vector SwiGLU)",
                     "bytes_per_launch": ch["bytes"], "avg_launch_us": ch["mean_us"]}
         del db, y, ro, out, flush, copy_src, copy_dst, mask, table, ids, emb_out
-        del lx, lr, ly, lro, lw
+        del lx, lr, ly, lro, lw, lw2
 
     # ---- CPU oracle baseline (after all GPU work) ----------------------------------------
     # A child process: the BLAS / OpenMP thread variables only take effect if

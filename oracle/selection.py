@@ -56,6 +56,12 @@ RN_LOOP = 18
 RN_WIDE = 19               # a 1024-work-item workgroup per row, 8 vectors per lane
 WIDE_LANES = 1024
 WIDE_ROW_VECS = 8 * WIDE_LANES   # the longest row it holds (16-byte vectors)
+RN_SPLIT = 20              # a row over S workgroups of 256, 8 vectors per work-item
+SPLIT_SPAN = 8 * 256       # vectors one split workgroup holds
+SPLIT_MAX_SLICES = 64      # workgroups per row, at most
+SPLIT_HEADER_WORDS = 8     # scratch: header, then T*S slots and T counters (64-bit words)
+SPLIT_SCRATCH_WORDS = 1 << 22   # a version's scratch for the top of its bucket, at most
+NORM_VARIANTS = (RN_SCALAR, *RN_WAVE.values(), *RN_BLOCK.values(), RN_LOOP, RN_WIDE, RN_SPLIT)
 ROPE_SCALAR, ROPE_VEC, ROPE_VEC_I, ROPE_QKN_SCALAR, ROPE_QKN_VEC, ROPE_QKN_VEC_I = \
     30, 31, 32, 33, 34, 35
 ROPE_VEC_ROLES = (ROPE_VEC, ROPE_VEC_I, ROPE_QKN_VEC, ROPE_QKN_VEC_I)
@@ -139,8 +145,29 @@ def _aligned(es: int, ptrs, strides) -> bool:
 
 
 # ---- role policies -----------------------------------------------------------
-def rn_role(dtype: int, H: int, flags: int, T: int) -> Tuple[int, int]:
-    """(variant, grid) for RMSNorm / residual RMSNorm rows."""
+def split_slices(dtype: int, H: int) -> int:
+    """Workgroups per row of the split form: the row's 16-byte vectors in
+    spans of SPLIT_SPAN."""
+    return cdiv(H // (16 // elem_size(dtype)), SPLIT_SPAN)
+
+
+def split_words(T: int, S: int) -> int:
+    """Scratch words a split call of T rows uses: the header, one slot per
+    workgroup, one counter per row."""
+    return SPLIT_HEADER_WORDS + T * (S + 1)
+
+
+def split_fits(dtype: int, H: int, b: int) -> bool:
+    """The split form serves rows of at most SPLIT_MAX_SLICES workgroups whose
+    version scratch, sized for the top of bucket b, stays within
+    SPLIT_SCRATCH_WORDS."""
+    S = split_slices(dtype, H)
+    return S <= SPLIT_MAX_SLICES and split_words(1 << b, S) <= SPLIT_SCRATCH_WORDS
+
+
+def rn_role(dtype: int, H: int, flags: int, T: int, b: int) -> Tuple[int, int]:
+    """(variant, grid) for RMSNorm / residual RMSNorm rows (b: the token
+    bucket of the key)."""
     v = 16 // elem_size(dtype)
     if not (flags & ALIGN) or H % v:
         return RN_SCALAR, T
@@ -150,6 +177,8 @@ def rn_role(dtype: int, H: int, flags: int, T: int) -> Tuple[int, int]:
     nb = next_pow2(cdiv(nvec, 256))       # a workgroup per row
     if nb <= 16:
         return RN_BLOCK[nb], T
+    if split_fits(dtype, H, b):           # several workgroups per row
+        return RN_SPLIT, T * split_slices(dtype, H)
     if nvec <= WIDE_ROW_VECS:             # a 1024-lane workgroup per row
         return RN_WIDE, T
     return RN_LOOP, T                     # two passes over memory
@@ -681,7 +710,7 @@ def plan(key, T: int):
     f = unpack_key(key)
     op, dt, b, fl = f["op"], f["dtype"], f["bucket"], f["flags"]
     if op in (OP_RMSNORM, OP_RES_RMSNORM):
-        v, g = rn_role(dt, f["H"], fl, T)
+        v, g = rn_role(dt, f["H"], fl, T, b)
         return v, (0, 0, 0), [(v, g, block_of(v))]
     inter = bool(f["rope_bits"] & ROPE_INTERLEAVED)
     nh = f["nq"] + f["nk"]
@@ -700,7 +729,7 @@ def plan(key, T: int):
     if op == OP_EMBEDDING:
         v, g = emb_role(dt, f["H"], fl, T)
         return v, (0, 0, 0), [(v, g, BLOCK)]
-    rn = rn_role(dt, f["H"], fl & 3, T)
+    rn = rn_role(dt, f["H"], fl & 3, T, b)
     ro = rope_role(dt, f["hd"], (fl >> 2) & 3, T, bool(fl & CHAIN_QK_NORM), f["rd"], inter)
     if ro[0] in ROPE_VEC_ROLES:
         ro = (ro[0], rope_grid(T, rope_slices(dt, f["rd"], inter, nh, b, ro[0]),
@@ -756,13 +785,16 @@ def _geometry_options(S: int, P: int, b: int) -> List[Tuple[int, int]]:
     return out
 
 
-def _rn_options(dt: int, H: int, fl: int, standalone: bool) -> List[int]:
+def _rn_options(dt: int, H: int, fl: int, b: int, standalone: bool) -> List[int]:
     """Norm rows: a row held by one wavefront can also be held by one
     256-lane workgroup (one vector per lane); standalone (the fused chain
     takes only the 256-lane register forms), a row of more than 1024
     vectors held by a 256-lane workgroup can also be held by a 1024-lane
-    one, and any row held in registers can take the two-pass loop kernel."""
-    P = rn_role(dt, H, fl, 1)[0]
+    one, a row of more than 2048 vectors (RN_BLOCK[16]) can also be split
+    over two workgroups when its scratch fits, a split row of at most
+    WIDE_ROW_VECS vectors can be held by a 1024-lane workgroup, and any
+    row held in registers can take the two-pass loop kernel."""
+    P = rn_role(dt, H, fl, 1, b)[0]
     if P in (RN_SCALAR, RN_LOOP):
         return [P]
     out = [P]
@@ -770,6 +802,11 @@ def _rn_options(dt: int, H: int, fl: int, standalone: bool) -> List[int]:
         out.append(RN_BLOCK[1])
     if standalone:
         if P in (RN_BLOCK[8], RN_BLOCK[16]):
+            out.append(RN_WIDE)
+            if P == RN_BLOCK[16] and split_words(1 << b, split_slices(dt, H)) <= \
+                    SPLIT_SCRATCH_WORDS:
+                out.append(RN_SPLIT)
+        if P == RN_SPLIT and H // (16 // elem_size(dt)) <= WIDE_ROW_VECS:
             out.append(RN_WIDE)
         out.append(RN_LOOP)
     return out
@@ -801,7 +838,7 @@ def candidates(key) -> List[Cand]:
     v = 16 // elem_size(dt)
     z = (0, 0, 0)
     if op in (OP_RMSNORM, OP_RES_RMSNORM):
-        return [Cand(r, z, (r,), 1) for r in _rn_options(dt, f["H"], fl, True)]
+        return [Cand(r, z, (r,), 1) for r in _rn_options(dt, f["H"], fl, b, True)]
     inter = bool(f["rope_bits"] & ROPE_INTERLEAVED)
     nh = f["nq"] + f["nk"]
     if op in (OP_ROPE_QK, OP_QK_NORM_ROPE):
@@ -837,7 +874,7 @@ def candidates(key) -> List[Cand]:
     if variant != CH_FUSED:
         return [seq]
     out = []
-    for r in _rn_options(dt, f["H"], fl & 3, False):
+    for r in _rn_options(dt, f["H"], fl & 3, b, False):
         for s, t in _geometry_options(S, Pt, b):
             for w in _other(sw, SW_FLAT, SW_FLAT_NT):
                 out.append(Cand(CH_FUSED, (r, ro, w), (CH_FUSED,), s, t))
@@ -855,6 +892,8 @@ def grid_of(variant: int, dt: int, T: int, width: int, slices: int = 1, tokens: 
     v = 16 // elem_size(dt)
     if variant in RN_WAVE.values():
         return cdiv(T, 4)
+    if variant == RN_SPLIT:               # width: the row width H
+        return T * split_slices(dt, width)
     if variant in (RN_SCALAR, RN_LOOP, RN_WIDE, ROPE_SCALAR, ROPE_QKN_SCALAR) or \
             variant in RN_BLOCK.values():
         return T
@@ -878,14 +917,16 @@ def cand_plan(key, c: Cand, T: int):
     the form plan() returns."""
     f = unpack_key(key)
     dt = f["dtype"]
-    width = f["H"] if f["op"] in SHORT_OPS else f["I"]
+
+    def width(kv):        # the norm rows' H, a short op's W, else SwiGLU's I
+        return f["H"] if f["op"] in SHORT_OPS or kv in NORM_VARIANTS else f["I"]
     if c.variant == CH_FUSED:
-        g = (grid_of(c.roles[0], dt, T, width)
-             + grid_of(c.roles[1], dt, T, width, c.slices, c.tokens)
-             + grid_of(c.roles[2], dt, T, width))
+        g = (grid_of(c.roles[0], dt, T, f["H"])
+             + grid_of(c.roles[1], dt, T, f["I"], c.slices, c.tokens)
+             + grid_of(c.roles[2], dt, T, f["I"]))
         return CH_FUSED, c.roles, [(CH_FUSED, g, BLOCK)]
-    launches = [(kv, grid_of(kv, dt, T, width, c.slices, c.tokens) if kv in ROPE_VEC_ROLES
-                 else grid_of(kv, dt, T, width), block_of(kv)) for kv in c.kernels]
+    launches = [(kv, grid_of(kv, dt, T, width(kv), c.slices, c.tokens) if kv in ROPE_VEC_ROLES
+                 else grid_of(kv, dt, T, width(kv)), block_of(kv)) for kv in c.kernels]
     return c.variant, c.roles, launches
 
 

@@ -336,7 +336,7 @@ int chain_launch(const Version &v, const tri_chain_args &p, void *stream, tri_la
                                 qkn ? p.q_norm_w : nullptr, p.k_norm_w, p.qk_eps);
   const SwArgs sw{p.gate, p.up, p.out, p.g_rs, p.u_rs, p.o_rs, T, I,
                   (T * I) / vec_elems(dtype), T * I};
-  const uint32_t g0 = role_grid(v.plan.roles[0], dtype, T, I);
+  const uint32_t g0 = role_grid(v.plan.roles[0], dtype, T, p.H);
   const uint32_t g1 =
       role_grid(v.plan.roles[1], dtype, T, I, v.plan.rope_slices, v.plan.rope_tokens);
   const uint32_t g2 = role_grid(v.plan.roles[2], dtype, T, I);
@@ -347,9 +347,13 @@ int chain_launch(const Version &v, const tri_chain_args &p, void *stream, tri_la
     *n = 1;
     return be_launch(v.fn[0], l[0].grid_x, kBlock, &a, sizeof a, stream);
   }
-  // Three launches: the residual norm, RoPE and SwiGLU role kernels.
-  const void *args[3] = {&rn, &ro, &sw};
-  const uint32_t sizes[3] = {sizeof rn, sizeof ro, sizeof sw};
+  // Three launches: the residual norm, RoPE and SwiGLU role kernels (a
+  // split norm role takes the version's scratch with its rows).
+  const RnSplitArgs rs{rn, v.d_scratch};
+  const bool split = v.plan.kvariant[0] == RN_SPLIT;
+  const void *args[3] = {split ? static_cast<const void *>(&rs) : &rn, &ro, &sw};
+  const uint32_t sizes[3] = {split ? uint32_t(sizeof rs) : uint32_t(sizeof rn), sizeof ro,
+                             sizeof sw};
   const uint32_t grids[3] = {g0, g1, g2};
   *n = 3;
   int rc = 0;
@@ -375,10 +379,9 @@ inline int check_elt(uint64_t es, int64_t T, int64_t W, const void *a, int64_t a
   return kGo;
 }
 
-// One launch of a single-kernel op (norms, SwiGLU, the short ops): lookup
-// (miss / auto-install), launch with the argument block, record, count.
-// `width` is what role_grid takes as I (SwiGLU's I, a short op's row width;
-// unused by the norm grids).
+// One launch of a single-kernel op (SwiGLU, the short ops): lookup (miss /
+// auto-install), launch with the argument block, record, count. `width` is
+// what role_grid takes as the row width (SwiGLU's I, a short op's W).
 tri_status single_launch(tri_cache *c, uint32_t op, const Key &k, int64_t T, int64_t width,
                          const void *args, uint32_t args_size, void *stream) {
   int32_t vi;
@@ -390,6 +393,27 @@ tri_status single_launch(tri_cache *c, uint32_t op, const Key &k, int64_t T, int
                          role_grid(v.plan.kvariant[0], key_dtype(k), T, width),
                          role_block(v.plan.kvariant[0])};
   const int rc = be_launch(v.fn[0], l.grid_x, l.block_x, args, args_size, stream);
+  record(c, op, v, vi, k, 1, &l, rc ? TRI_E_LAUNCH : TRI_OK);
+  return finish(c, v, auto_inst, rc);
+}
+
+// One launch of a norm version: RnArgs, or with a split plan the rows and
+// the version's scratch.
+tri_status norm_launch(tri_cache *c, uint32_t op, const Key &k, const RnArgs &a, void *stream) {
+  int32_t vi;
+  bool auto_inst = false;
+  const int st = lookup(c, op, k, a.T, &vi, &auto_inst);
+  if (st != TRI_OK) return tri_status(st);
+  Version &v = c->versions[vi];
+  const int32_t kv = v.plan.kvariant[0];
+  const tri_launch_rec l{kv, role_grid(kv, key_dtype(k), a.T, a.H), role_block(kv)};
+  int rc;
+  if (kv == RN_SPLIT) {
+    const RnSplitArgs sa{a, v.d_scratch};
+    rc = be_launch(v.fn[0], l.grid_x, l.block_x, &sa, sizeof sa, stream);
+  } else {
+    rc = be_launch(v.fn[0], l.grid_x, l.block_x, &a, sizeof a, stream);
+  }
   record(c, op, v, vi, k, 1, &l, rc ? TRI_E_LAUNCH : TRI_OK);
   return finish(c, v, auto_inst, rc);
 }
@@ -584,7 +608,7 @@ tri_status tri_rmsnorm(tri_cache *c, tri_dtype dtype, const void *x, int64_t x_r
   const Key k = make_key(op, dtype, T, rn_flags(es, x, x_rs, w, y, y_rs, H), 0, uint64_t(H), 0,
                          0, 0, 0);
   const RnArgs a{x, nullptr, w, y, nullptr, x_rs, 0, y_rs, 0, T, int32_t(H), eps};
-  return single_launch(c, op, k, T, 0, &a, sizeof a, stream);
+  return norm_launch(c, op, k, a, stream);
 }
 
 tri_status tri_residual_rmsnorm(tri_cache *c, tri_dtype dtype, const void *x, int64_t x_rs,
@@ -606,7 +630,7 @@ tri_status tri_residual_rmsnorm(tri_cache *c, tri_dtype dtype, const void *x, in
                          res_flags(es, x, x_rs, res, res_rs, w, y, y_rs, res_out, ro_rs, H), 0,
                          uint64_t(H), 0, 0, 0, 0);
   const RnArgs a{x, res, w, y, res_out, x_rs, res_rs, y_rs, ro_rs, T, int32_t(H), eps};
-  return single_launch(c, op, k, T, 0, &a, sizeof a, stream);
+  return norm_launch(c, op, k, a, stream);
 }
 
 tri_status tri_rope_qk_ext(tri_cache *c, tri_dtype dtype, void *q, int64_t q_ts, void *kp,

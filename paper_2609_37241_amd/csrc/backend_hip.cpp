@@ -33,7 +33,7 @@ int be_init(int *device) {
 
 int be_resolve(int32_t kvariant, uint32_t dtype, int32_t ksub, void **fn) {
   const void *sym = nullptr;
-  if (kvariant >= RN_SCALAR && kvariant <= RN_WIDE)
+  if (kvariant >= RN_SCALAR && kvariant <= RN_SPLIT)
     sym = rn_kernel(kvariant, dtype, ksub);
   else if (kvariant >= ROPE_SCALAR && kvariant <= ROPE_QKN_VEC_I)
     sym = rope_kernel(kvariant, dtype);
@@ -70,6 +70,20 @@ int be_upload(const void *host, uint64_t bytes, void **dev) {
   void *p = nullptr;
   if (hipMalloc(&p, bytes) != hipSuccess) return TRI_E_NOMEM;
   if (hipMemcpy(p, host, bytes, hipMemcpyHostToDevice) != hipSuccess) {
+    (void)hipFree(p);
+    return TRI_E_RUNTIME;
+  }
+  *dev = p;
+  return 0;
+}
+
+// Zero-filled device memory, ready when this returns (a synchronous fill).
+int be_alloc_zeroed(uint64_t bytes, void **dev) {
+  void *p = nullptr;
+  if (hipMalloc(&p, bytes) != hipSuccess) return TRI_E_NOMEM;
+  // the fill runs on the null stream: wait for it, so that no launch on
+  // another stream can reach the memory first
+  if (hipMemset(p, 0, bytes) != hipSuccess || hipStreamSynchronize(nullptr) != hipSuccess) {
     (void)hipFree(p);
     return TRI_E_RUNTIME;
   }

@@ -119,9 +119,17 @@ bool read_choice(const char *path, int n, int32_t *choice) {
 void drop_version(Version &v) {
   release_modules(v);
   if (v.d_consts) be_free(v.d_consts);
+  if (v.d_scratch) be_free(v.d_scratch);
   free(v.h_consts);
   v.d_consts = nullptr;
   v.h_consts = nullptr;
+  v.d_scratch = nullptr;
+}
+
+bool plan_splits(const Plan &p) {
+  for (int i = 0; i < p.n_launches; ++i)
+    if (p.kvariant[i] == RN_SPLIT) return true;
+  return false;
 }
 
 }  // namespace
@@ -156,7 +164,26 @@ tri_status install_key(tri_cache *c, const Key &k, int32_t candidate) {
     v.d_consts = static_cast<float *>(dev);
   }
 
-  if (candidate < 0 && (c->flags & TRI_CACHE_AUTOTUNE) && nc > 1) {
+  // Split norm rows exchange partial sums through a scratch of the version,
+  // zeroed here and left zero by every call, sized for the top of the token
+  // bucket: allocated when the plan splits, or before tuning when any
+  // candidate does (the tuning calls share it, one after another on one
+  // stream), and kept only if the chosen plan splits.
+  const bool tuning = candidate < 0 && (c->flags & TRI_CACHE_AUTOTUNE) && nc > 1;
+  bool need_scratch = plan_splits(cands[v.candidate]);
+  for (int i = 0; tuning && i < nc; ++i) need_scratch = need_scratch || plan_splits(cands[i]);
+  if (need_scratch) {
+    v.scratch_words = split_words(int64_t(1) << key_bucket(k), split_slices(dt, key_H(k)));
+    void *dev = nullptr;
+    const int st = be_alloc_zeroed(v.scratch_words * 8, &dev);
+    if (st != 0) {
+      drop_version(v);
+      return tri_status(st);
+    }
+    v.d_scratch = static_cast<uint64_t *>(dev);
+  }
+
+  if (tuning) {
     // Benchmark-and-keep (Sec. 2): a stored choice, else a timed one.
     const auto t0 = std::chrono::steady_clock::now();
     char path[1100];
@@ -175,6 +202,11 @@ tri_status install_key(tri_cache *c, const Key &k, int32_t candidate) {
                           std::chrono::steady_clock::now() - t0).count());
   }
   v.plan = cands[v.candidate];
+  if (v.d_scratch && !plan_splits(v.plan)) {
+    be_free(v.d_scratch);
+    v.d_scratch = nullptr;
+    v.scratch_words = 0;
+  }
 
   if (c->flags & TRI_CACHE_JIT) {
     // Compile one specialization per launch of the plan (Sec. 3.5 growth),
@@ -216,9 +248,6 @@ tri_status install_key(tri_cache *c, const Key &k, int32_t candidate) {
 void fill_selection(const Version &v, int32_t index, int64_t T, tri_selection *out) {
   const Key &k = v.key;
   const uint32_t dt = key_dtype(k);
-  // role_grid's width: SwiGLU's I, or the row width of a short op (H field)
-  const uint32_t op = key_op(k);
-  const int64_t I = op >= TRI_OP_SILU && op <= TRI_OP_EMBEDDING ? key_H(k) : key_I(k);
   memset(out, 0, sizeof *out);
   out->op = int32_t(key_op(k));
   out->status = TRI_OK;
@@ -227,17 +256,19 @@ void fill_selection(const Version &v, int32_t index, int64_t T, tri_selection *o
   out->n_launches = v.plan.n_launches;
   for (int i = 0; i < 3; ++i) out->roles[i] = v.plan.roles[i];
   if (v.plan.variant == CH_FUSED) {
-    const uint32_t g = role_grid(v.plan.roles[0], dt, T, I) +
-                       role_grid(v.plan.roles[1], dt, T, I, v.plan.rope_slices,
+    const uint32_t g = role_grid(v.plan.roles[0], dt, T, key_H(k)) +
+                       role_grid(v.plan.roles[1], dt, T, key_I(k), v.plan.rope_slices,
                                  v.plan.rope_tokens) +
-                       role_grid(v.plan.roles[2], dt, T, I);
+                       role_grid(v.plan.roles[2], dt, T, key_I(k));
     out->launch[0] = {CH_FUSED, g, kBlock};
   } else {
-    for (int i = 0; i < v.plan.n_launches; ++i)
-      out->launch[i] = {v.plan.kvariant[i],
-                        role_grid(v.plan.kvariant[i], dt, T, I, v.plan.rope_slices,
+    for (int i = 0; i < v.plan.n_launches; ++i) {
+      const int32_t kv = v.plan.kvariant[i];
+      out->launch[i] = {kv,
+                        role_grid(kv, dt, T, launch_width(k, kv), v.plan.rope_slices,
                                   v.plan.rope_tokens),
-                        role_block(v.plan.kvariant[i])};
+                        role_block(kv)};
+    }
   }
   key_words(k, out->key);
 }
@@ -285,6 +316,7 @@ void tri_spec_cache_destroy(tri_cache *c) {
   if (!c) return;
   for (uint32_t i = 0; i < c->n_versions; ++i) {
     if (c->versions[i].d_consts) be_free(c->versions[i].d_consts);
+    if (c->versions[i].d_scratch) be_free(c->versions[i].d_scratch);
     free(c->versions[i].h_consts);
     release_modules(c->versions[i]);
   }

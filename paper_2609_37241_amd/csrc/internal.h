@@ -15,7 +15,7 @@ enum Variant : int32_t {
   RN_SCALAR = 10,
   RN_WAVE_1 = 11, RN_WAVE_2 = 12,
   RN_BLOCK_1 = 13, RN_BLOCK_2 = 14, RN_BLOCK_4 = 15, RN_BLOCK_8 = 16, RN_BLOCK_16 = 17,
-  RN_LOOP = 18, RN_WIDE = 19,
+  RN_LOOP = 18, RN_WIDE = 19, RN_SPLIT = 20,
   ROPE_SCALAR = 30, ROPE_VEC = 31, ROPE_VEC_I = 32, ROPE_QKN_SCALAR = 33, ROPE_QKN_VEC = 34,
   ROPE_QKN_VEC_I = 35,
   SW_SCALAR = 40, SW_FLAT = 41, SW_FLAT_NT = 42, SW_ROWS = 43,
@@ -36,6 +36,11 @@ constexpr int64_t kHLimit = int64_t(1) << 24;
 constexpr int64_t kILimit = int64_t(1) << 31;
 constexpr uint64_t kSpanMax = uint64_t(1) << 47;   // bytes an operand's rows may span
 constexpr int64_t kWideRowVecs = 8 * int64_t(kWideLanes);   // longest RN_WIDE row (vectors)
+// RN_SPLIT: rows beyond 16 * 256 vectors, at most kSplitMaxSlices workgroups
+// per row; a version's scratch (kSplitHeaderWords + 2^bucket * (S + 1)
+// words) may take at most kSplitScratchWords (32 MiB), else the longer
+// forms serve the key.
+constexpr uint64_t kSplitScratchWords = uint64_t(1) << 22;
 constexpr int32_t kHdMax = 512;
 constexpr int32_t kHeadsMax = 4096;
 constexpr uint32_t kDefaultCapacity = 256;
@@ -92,7 +97,13 @@ struct Role {
   int32_t variant;
   uint32_t grid;
 };
-Role rn_role(uint32_t dtype, int64_t H, unsigned flags, int64_t T);
+Role rn_role(uint32_t dtype, int64_t H, unsigned flags, int64_t T, uint32_t bucket);
+// Workgroups per row of RN_SPLIT, and the scratch words a call of T rows
+// of that split needs.
+int32_t split_slices(uint32_t dtype, int64_t H);
+inline uint64_t split_words(int64_t T, int32_t S) {
+  return uint64_t(kSplitHeaderWords) + uint64_t(T) * uint64_t(S + 1);
+}
 Role rope_role(uint32_t dtype, int32_t hd, int32_t rd, bool interleaved, unsigned flags, int64_t T,
                bool qk_norm);
 Role sw_role(uint32_t dtype, int64_t I, unsigned flags, bool stream, int64_t T);
@@ -100,10 +111,15 @@ Role sw_role(uint32_t dtype, int64_t I, unsigned flags, bool stream, int64_t T);
 // chain; 0 for other ops); SwiGLU streams nontemporally above kStreamBytes.
 uint64_t call_bytes(const Key &k);
 constexpr uint64_t kStreamBytes = uint64_t(320) << 20;
-// Workgroups of a role variant for T tokens; a vector RoPE role takes T *
-// slices workgroups with head slices, else ceil(T / tokens).
-uint32_t role_grid(int32_t variant, uint32_t dtype, int64_t T, int64_t I, int32_t slices = 1,
-                   int32_t tokens = 1);
+// Workgroups of a role variant for T tokens; `width` is the row width of
+// the launch's op (H for the norms, I for SwiGLU, W for the short ops); a
+// vector RoPE role takes T * slices workgroups with head slices, else
+// ceil(T / tokens).
+uint32_t role_grid(int32_t variant, uint32_t dtype, int64_t T, int64_t width,
+                   int32_t slices = 1, int32_t tokens = 1);
+// The row width role_grid takes for launch variant `kv` of a version with key k.
+int64_t launch_width(const Key &k, int32_t kv);
+inline bool is_norm_variant(int32_t v) { return v >= RN_SCALAR && v <= RN_SPLIT; }
 // Work-items per workgroup of a launch of `variant`.
 inline uint32_t role_block(int32_t variant) {
   return variant == RN_WIDE ? uint32_t(kWideLanes) : kBlock;
@@ -159,6 +175,7 @@ int be_resolve(int32_t kvariant, uint32_t dtype, int32_t ksub, void **fn);
 int be_launch(void *fn, uint32_t grid, uint32_t block, const void *args, uint32_t args_size,
               void *stream);
 int be_upload(const void *host, uint64_t bytes, void **dev);      // per-version constants
+int be_alloc_zeroed(uint64_t bytes, void **dev);                  // per-version scratch
 void be_free(void *dev);
 // Compile `src` (len bytes, NUL-terminated) for the device into a code
 // object (*code malloc'd, caller frees) / load a code object: the kernel
@@ -195,6 +212,8 @@ struct Version {
   float *d_consts;        // device copy of the RoPE inverse frequencies, or null
   float *h_consts;        // host copy (rotary_dim/2 floats), or null
   uint32_t n_consts;
+  uint64_t *d_scratch;    // split norm rows: the exchange scratch, or null
+  uint64_t scratch_words;
   uint64_t hits;
 };
 

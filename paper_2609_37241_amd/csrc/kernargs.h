@@ -22,6 +22,16 @@ constexpr int kRopeTokensMax = 4;
 // 8 * kWideLanes 16-byte vectors per workgroup; every other kernel uses 256.
 constexpr int kWideLanes = 1024;
 
+// Split norm rows (RN_SPLIT): a row of more than 16 * 256 vectors is held
+// by S = ceil(vectors / kSplitSpan) workgroups of 256 work-items, kSplitVecs
+// vectors per work-item, which exchange their partial sums of squares
+// through a scratch buffer: 8 header words (word 0: a sticky failure flag),
+// then T * S slots (row-major, one per workgroup), then T per-row counters.
+constexpr int kSplitVecs = 8;
+constexpr int kSplitSpan = 256 * kSplitVecs;   // vectors per workgroup
+constexpr int kSplitMaxSlices = 64;            // workgroups per row, at most
+constexpr int kSplitHeaderWords = 8;
+
 // Residual add + RMSNorm and plain RMSNorm ([T, H] rows, element strides).
 struct RnArgs {
   const void *x;
@@ -33,6 +43,14 @@ struct RnArgs {
   int64_t T;
   int32_t H;
   float eps;
+};
+
+// A split norm launch: the row arguments and the scratch of the call
+// (kSplitHeaderWords + T * (S + 1) 64-bit words, all zero when the call
+// starts; the kernel leaves them zero).
+struct RnSplitArgs {
+  RnArgs rn;
+  uint64_t *scratch;
 };
 
 // RoPE on Q [T, nq, hd] and K [T, nk, hd], in place, over the first rd
@@ -105,6 +123,8 @@ struct ChainArgs {
 static_assert(sizeof(RnArgs) == 88 && __builtin_offsetof(RnArgs, T) == 72 &&
                   __builtin_offsetof(RnArgs, eps) == 84,
               "RnArgs layout");
+static_assert(sizeof(RnSplitArgs) == 96 && __builtin_offsetof(RnSplitArgs, scratch) == 88,
+              "RnSplitArgs layout");
 static_assert(sizeof(RopeArgs) == 112 && __builtin_offsetof(RopeArgs, nq) == 88 &&
                   __builtin_offsetof(RopeArgs, mode) == 108,
               "RopeArgs layout");

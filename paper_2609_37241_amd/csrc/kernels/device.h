@@ -259,6 +259,155 @@ __device__ __forceinline__ void rn_wave_block(const RnArgs &a, int64_t blk) {
   rn_row_regs<DT, NV, RES, 64, NT>(a, row, threadIdx.x & 63, nullptr);
 }
 
+// ---- split rows -------------------------------------------------------------------
+// A row of nvec vectors is split over S = ceil(nvec / kSplitSpan)
+// consecutive workgroups (workgroup b: row b / S, slice b % S of
+// kSplitVecs vectors per work-item). Each holds its slice in registers,
+// reduces its partial sum of squares, publishes it in the row's slot of the
+// scratch buffer and waits until all S slots of the row are full; every
+// workgroup of the row then adds the S partials in the same order (one
+// wavefront, lanes 0..S-1), so all of them normalise with the same total.
+// The row is read once and written once: nothing is re-read.
+//
+// Slots carry their own "full" bit, so the exchange needs no memory fence:
+// a slot is one relaxed device-scope 64-bit atomic, and nothing else is
+// communicated. The row's last reader (a per-row counter reaching S)
+// clears the row's slots and counter, so the scratch is all zero again when
+// the kernel ends, ready for the next call on the stream. No counter is
+// shared between rows: atomics on one address serialise, and a ticket or
+// completion counter for the whole grid measured 5-20x slower.
+//
+// The wait relies on the S workgroups of a row being resident together:
+// they are consecutive in dispatch order, so once the earlier ones run the
+// later ones are next in line (S <= 64, far below the workgroups the GPU
+// holds). As a guard against anything else occupying the GPU indefinitely,
+// the wait is bounded (kSplitSpinMax polls, several hundred milliseconds):
+// a row whose partials do not all arrive is written as NaN and sets the
+// sticky failure flag in header word 0, after which every call on that
+// scratch writes NaN rows instead of trusting the exchange. A failure is
+// therefore loud and never silent.
+constexpr int kSplitSpinMax = 1 << 18;
+constexpr uint64_t kSlotFull = uint64_t(1) << 63;
+
+template <int DT, bool RES>
+__device__ __forceinline__ void rn_split_row(const RnArgs &a, uint64_t *scratch) {
+  using E = Elt<DT>;
+  constexpr int V = E::V;
+  constexpr int NB = kSplitVecs;
+  __shared__ float red[4];
+  __shared__ float total;
+  const int nvec = a.H / V;
+  const int S = (nvec + kSplitSpan - 1) / kSplitSpan;
+  const int64_t row = int64_t(blockIdx.x) / S;
+  const int s = int(int64_t(blockIdx.x) - row * S);
+  uint64_t *slots = scratch + kSplitHeaderWords + row * S;
+  uint64_t *count = scratch + kSplitHeaderWords + a.T * S + row;
+  const int v0 = s * kSplitSpan + int(threadIdx.x);
+  const u32x4 *xr = reinterpret_cast<const u32x4 *>(static_cast<const char *>(a.x) +
+                                                     row * a.x_rs * E::ES);
+  const u32x4 *wr = static_cast<const u32x4 *>(a.w);
+  u32x4 xv[NB], wv[NB];
+#pragma unroll
+  for (int k = 0; k < NB; ++k) {
+    const int vi = v0 + 256 * k;
+    xv[k] = vi < nvec ? xr[vi] : u32x4{0, 0, 0, 0};
+  }
+  if constexpr (RES) {
+    const u32x4 *rr = reinterpret_cast<const u32x4 *>(static_cast<const char *>(a.res) +
+                                                       row * a.res_rs * E::ES);
+    u32x4 *orow = reinterpret_cast<u32x4 *>(static_cast<char *>(a.res_out) + row * a.ro_rs * E::ES);
+    u32x4 rv[NB];
+#pragma unroll
+    for (int k = 0; k < NB; ++k) {
+      const int vi = v0 + 256 * k;
+      rv[k] = vi < nvec ? rr[vi] : u32x4{0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int k = 0; k < NB; ++k) {
+      float f[V], g[V];
+      E::unpack(xv[k], f);
+      E::unpack(rv[k], g);
+#pragma unroll
+      for (int e = 0; e < V; ++e) f[e] += g[e];
+      xv[k] = E::pack(f);
+      const int vi = v0 + 256 * k;
+      if (vi < nvec) orow[vi] = xv[k];
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < NB; ++k) {
+    const int vi = v0 + 256 * k;
+    wv[k] = vi < nvec ? wr[vi] : u32x4{0, 0, 0, 0};
+  }
+  float ss = 0.0f;
+#pragma unroll
+  for (int k = 0; k < NB; ++k) {
+    float f[V];
+    E::unpack(xv[k], f);
+#pragma unroll
+    for (int e = 0; e < V; ++e) ss = __builtin_fmaf(f[e], f[e], ss);
+  }
+  ss = block_sum(ss, red);
+  if (threadIdx.x < 64) {   // one whole wavefront: the exchange
+    const int lane = int(threadIdx.x);
+    float sum = __builtin_nanf("");
+    if (scratch[0] == 0) {
+      if (lane == 0)
+        __hip_atomic_store(&slots[s], kSlotFull | __float_as_uint(ss), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+      bool have = lane >= S;
+      float part = 0.0f;
+      bool late = false;
+      for (int it = 0;; ++it) {
+        if (!have) {
+          const uint64_t w = __hip_atomic_load(&slots[lane], __ATOMIC_RELAXED,
+                                               __HIP_MEMORY_SCOPE_AGENT);
+          if (w & kSlotFull) {
+            have = true;
+            part = __uint_as_float(uint32_t(w));
+          }
+        }
+        if (__all(have)) break;
+        if (it >= kSplitSpinMax) {
+          late = true;
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+      }
+      sum = wave_sum(part);
+      if (lane == 0) {
+        if (late) {
+          sum = __builtin_nanf("");
+          __hip_atomic_store(&scratch[0], uint64_t(1), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        const uint64_t c = __hip_atomic_fetch_add(count, uint64_t(1), __ATOMIC_RELAXED,
+                                                  __HIP_MEMORY_SCOPE_AGENT);
+        if (c == uint64_t(S) - 1) {   // the row's last reader: clear for the next call
+          for (int j = 0; j < S; ++j)
+            __hip_atomic_store(&slots[j], uint64_t(0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          __hip_atomic_store(count, uint64_t(0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+      }
+    }
+    if (lane == 0) total = sum;
+  }
+  __syncthreads();
+  const float inv = rsqrtf(total / float(a.H) + a.eps);
+  u32x4 *yr = reinterpret_cast<u32x4 *>(static_cast<char *>(a.y) + row * a.y_rs * E::ES);
+#pragma unroll
+  for (int k = 0; k < NB; ++k) {
+    const int vi = v0 + 256 * k;
+    if (vi < nvec) {
+      float f[V], w[V];
+      E::unpack(xv[k], f);
+      E::unpack(wv[k], w);
+#pragma unroll
+      for (int e = 0; e < V; ++e) f[e] = (f[e] * inv) * w[e];
+      yr[vi] = E::pack(f);
+    }
+  }
+}
+
 // Vectors a work-item keeps in flight in the long-row kernels' streaming
 // passes (one 16-byte load each, all issued before any is used).
 constexpr int kRnBatch = 8;
@@ -1006,6 +1155,12 @@ template <int DT, bool RES>
 __device__ __forceinline__ void body_rn_wide(const RnArgs &a) {
   __shared__ float red[kWideLanes / 64];
   rn_row_regs<DT, 8, RES, kWideLanes, false>(a, blockIdx.x, threadIdx.x, red);
+}
+
+// Rows of more than 4096 vectors over several workgroups (rn_split_row).
+template <int DT, bool RES>
+__device__ __forceinline__ void body_rn_split(const RnSplitArgs &a) {
+  rn_split_row<DT, RES>(a.rn, a.scratch);
 }
 
 template <int DT, bool RES>

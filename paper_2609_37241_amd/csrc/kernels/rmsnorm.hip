@@ -27,6 +27,11 @@ __global__ __launch_bounds__(kWideLanes) void k_rn_wide(RnArgs a) {
 }
 
 template <int DT, bool RES>
+__global__ __launch_bounds__(256) void k_rn_split(RnSplitArgs a) {
+  body_rn_split<DT, RES>(a);
+}
+
+template <int DT, bool RES>
 __global__ __launch_bounds__(256) void k_rn_scalar(RnArgs a) {
   body_rn_scalar<DT, RES>(a);
 }
@@ -45,6 +50,7 @@ const void *rn_pick(int32_t variant) {
     case RN_BLOCK_16: return reinterpret_cast<const void *>(&k_rn_block<DT, 16, RES>);
     case RN_LOOP: return reinterpret_cast<const void *>(&k_rn_loop<DT, RES>);
     case RN_WIDE: return reinterpret_cast<const void *>(&k_rn_wide<DT, RES>);
+    case RN_SPLIT: return reinterpret_cast<const void *>(&k_rn_split<DT, RES>);
     default: return nullptr;
   }
 }

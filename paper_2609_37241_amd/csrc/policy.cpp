@@ -43,24 +43,38 @@ bool rope_vec_role(int32_t v) {
 
 }  // namespace
 
+int32_t split_slices(uint32_t dtype, int64_t H) {
+  return int32_t(cdiv(H / vec_elems(dtype), kSplitSpan));
+}
+
 // Rows of up to 128 16-byte vectors (2 KiB) take one wavefront each, four
 // rows per workgroup, with no barrier. Longer rows take one 256-work-item
 // workgroup per row, up to 16 vectors per work-item: the four wavefronts
 // issue the row's loads and stores in parallel (measured 1.8 µs vs 3.4 µs
 // device time for a single 4096-element bf16 row held by one wavefront) and
-// hold fewer registers per lane when streaming. Rows of up to kWideRowVecs
-// vectors take a 1024-work-item workgroup (up to 8 vectors per lane in
-// registers); it streamed bf16 rows of 65,536 elements at 5.4 TB/s against
-// 4.2-4.4 TB/s for the row staged in LDS (one 128 KiB row per CU leaves too
-// few bytes in flight) and 3.9 TB/s for two passes. Longer rows make two
-// passes over global memory. Unaligned or ragged rows take the scalar kernel.
-Role rn_role(uint32_t dtype, int64_t H, unsigned flags, int64_t T) {
+// hold fewer registers per lane when streaming. Rows beyond 4096 vectors
+// are split over S = ceil(vectors / 2048) workgroups of 256 work-items, 8
+// vectors per work-item, which exchange partial sums through the version's
+// scratch (up to 64 workgroups per row, and a scratch of at most
+// kSplitScratchWords for the top of the token bucket). Against the forms
+// it replaces, at 256-512 MiB per operand (probe, 1 GiB read flush): bf16
+// rows of 49,152 / 65,536 elements 94.9 / 94.5 us vs 97.2 / 101.1 us for a
+// 1024-work-item workgroup per row (residual 176.1 / 177.9 vs 182.2 /
+// 181.8), f32 rows of 32,768 a tie (93.0 / 176.0 us both); bf16 rows of
+// 131,072 / 262,144 and f32 rows of 65,536 1.25-1.37x faster than two
+// passes over memory. Beyond the split's limits a row of up to
+// kWideRowVecs vectors takes the 1024-work-item workgroup and longer rows
+// make two passes. Unaligned or ragged rows take the scalar kernel.
+Role rn_role(uint32_t dtype, int64_t H, unsigned flags, int64_t T, uint32_t bucket) {
   const int64_t v = vec_elems(dtype);
   if (!(flags & kAlign) || H % v) return {RN_SCALAR, uint32_t(T)};
   const int64_t nvec = H / v;
   if (nvec <= 128) return {nvec <= 64 ? RN_WAVE_1 : RN_WAVE_2, uint32_t(cdiv(T, 4))};
   const int64_t nb = next_pow2(cdiv(nvec, 256));
   if (nb <= 16) return {RN_BLOCK_1 + pow2_index(nb), uint32_t(T)};
+  const int32_t S = split_slices(dtype, H);
+  if (S <= kSplitMaxSlices && split_words(int64_t(1) << bucket, S) <= kSplitScratchWords)
+    return {RN_SPLIT, uint32_t(T * S)};
   if (nvec <= kWideRowVecs) return {RN_WIDE, uint32_t(T)};
   return {RN_LOOP, uint32_t(T)};
 }
@@ -179,11 +193,13 @@ Role emb_role(uint32_t dtype, int64_t H, unsigned flags, int64_t T) {
   return {(flags & kAlign) && H % v == 0 ? EMB_VEC : EMB_SCALAR, clamp_grid(T)};
 }
 
-// Workgroups of a role variant for T tokens (I is the SwiGLU width, the
-// row width of an element-wise op, or the embedding row width).
+// Workgroups of a role variant for T tokens (I is the row width: the norm
+// row H, the SwiGLU width, the row width of an element-wise op, or the
+// embedding row width).
 uint32_t role_grid(int32_t variant, uint32_t dtype, int64_t T, int64_t I, int32_t slices,
                    int32_t tokens) {
   if (variant == RN_WAVE_1 || variant == RN_WAVE_2) return uint32_t(cdiv(T, 4));
+  if (variant == RN_SPLIT) return uint32_t(T * split_slices(dtype, I));
   switch (variant) {
     case RN_SCALAR: case RN_BLOCK_1: case RN_BLOCK_2: case RN_BLOCK_4: case RN_BLOCK_8:
     case RN_BLOCK_16: case RN_LOOP: case RN_WIDE: case ROPE_SCALAR: case ROPE_QKN_SCALAR:
@@ -207,6 +223,12 @@ uint32_t role_grid(int32_t variant, uint32_t dtype, int64_t T, int64_t I, int32_
     default:
       return 0;
   }
+}
+
+int64_t launch_width(const Key &k, int32_t kv) {
+  const uint32_t op = key_op(k);
+  if (is_norm_variant(kv) || (op >= TRI_OP_SILU && op <= TRI_OP_EMBEDDING)) return key_H(k);
+  return key_I(k);
 }
 
 namespace {
@@ -277,7 +299,7 @@ Plan plan_for_key(const Key &k) {
   switch (op) {
     case TRI_OP_RMSNORM:
     case TRI_OP_RES_RMSNORM: {
-      const Role r = rn_role(dt, key_H(k), fl, 1);
+      const Role r = rn_role(dt, key_H(k), fl, 1, b);
       p.variant = r.variant;
       p.n_launches = 1;
       p.kvariant[0] = r.variant;
@@ -326,7 +348,7 @@ Plan plan_for_key(const Key &k) {
     default:
       break;
   }
-  const Role rn = rn_role(dt, key_H(k), fl & 3u, 1);
+  const Role rn = rn_role(dt, key_H(k), fl & 3u, 1, b);
   const bool inter = (key_rope_bits(k) & kRopeInterleaved) != 0;
   const Role ro = rope_role(dt, int32_t(key_hd(k)), int32_t(key_rd(k)), inter, (fl >> 2) & 3u, 1,
                             (fl & kChainQkNorm) != 0);
@@ -361,8 +383,10 @@ Plan plan_for_key(const Key &k) {
 // Index 0 is the policy's plan. The others are the kernel variants whose
 // requirements the key also meets: a norm row held by one wavefront can be
 // held by one workgroup (one vector per lane), a row of more than 1024
-// vectors held by a 256-lane workgroup can be held by a 1024-lane one, and a
-// row held in registers can take the two-pass kernel (standalone only); a vector RoPE role can
+// vectors held by a 256-lane workgroup can be held by a 1024-lane one (and,
+// beyond 2048 vectors, split over workgroups), a split row of at most 8192
+// vectors by a 1024-lane workgroup, and a row held in registers can take
+// the two-pass kernel (standalone only); a vector RoPE role can
 // take another geometry (at decode sizes 1, 2 or 4 workgroups per token;
 // beyond them 1, 2 or 4 tokens per workgroup, or up to 8192 tokens 2 or 4
 // workgroups per token) or the scalar kernel; flat SwiGLU and element-wise kernels have a cached
@@ -373,14 +397,22 @@ Plan plan_for_key(const Key &k) {
 // three-launch sequence of the policy's roles.
 namespace {
 
-int rn_options(uint32_t dt, int64_t H, unsigned fl, bool standalone, int32_t *out) {
-  const int32_t P = rn_role(dt, H, fl, 1).variant;
+int rn_options(uint32_t dt, int64_t H, unsigned fl, uint32_t b, bool standalone,
+               int32_t *out) {
+  const int32_t P = rn_role(dt, H, fl, 1, b).variant;
   int n = 0;
   out[n++] = P;
   if (P == RN_SCALAR || P == RN_LOOP) return n;
   if (P == RN_WAVE_1 || P == RN_WAVE_2) out[n++] = RN_BLOCK_1;
   if (!standalone) return n;
-  if (P == RN_BLOCK_8 || P == RN_BLOCK_16) out[n++] = RN_WIDE;
+  if (P == RN_BLOCK_8 || P == RN_BLOCK_16) {
+    out[n++] = RN_WIDE;
+    // a split row is at least two workgroups: rows beyond 2048 vectors
+    if (P == RN_BLOCK_16 &&
+        split_words(int64_t(1) << b, split_slices(dt, H)) <= kSplitScratchWords)
+      out[n++] = RN_SPLIT;
+  }
+  if (P == RN_SPLIT && H / vec_elems(dt) <= kWideRowVecs) out[n++] = RN_WIDE;
   out[n++] = RN_LOOP;
   return n;
 }
@@ -433,8 +465,8 @@ int plan_candidates(const Key &k, Plan *out) {
   switch (op) {
     case TRI_OP_RMSNORM:
     case TRI_OP_RES_RMSNORM: {
-      int32_t r[3];
-      const int nr = rn_options(dt, key_H(k), fl, true, r);
+      int32_t r[4];
+      const int nr = rn_options(dt, key_H(k), fl, b, true, r);
       for (int i = 1; i < nr; ++i) out[n++] = single(r[i], P.ksub[0]);
       return n;
     }
@@ -467,9 +499,9 @@ int plan_candidates(const Key &k, Plan *out) {
       return n;
   }
   if (P.variant != CH_FUSED) return n;
-  int32_t r[3];
+  int32_t r[4];
   Geometry g[5];
-  const int nr = rn_options(dt, key_H(k), fl & 3u, false, r);
+  const int nr = rn_options(dt, key_H(k), fl & 3u, b, false, r);
   const int ng = geometry_options(P.rope_slices, P.rope_tokens, b, g);
   const int32_t sw0 = P.roles[2], sw1 = sw0 == SW_FLAT ? SW_FLAT_NT : SW_FLAT;
   n = 0;

@@ -45,6 +45,8 @@ std::vector<Cost> g_costs;
 std::vector<int64_t> g_marks;
 int64_t g_timers = 0, g_timer_destroys = 0, g_scratch_allocs = 0, g_scratch_frees = 0;
 uint64_t g_scratch_bytes = 0;
+int64_t g_zero_allocs = 0;
+uint64_t g_zero_bytes = 0;
 bool g_scratch_fail = false;
 std::string g_arch = "fake";
 
@@ -95,6 +97,16 @@ int be_upload(const void *host, uint64_t bytes, void **dev) {
   memcpy(p, host, bytes);
   *dev = p;
   g_uploads++;
+  return 0;
+}
+
+// Per-version scratch of split norm rows: zeroed host memory (counted).
+int be_alloc_zeroed(uint64_t bytes, void **dev) {
+  void *p = calloc(1, bytes);
+  if (!p) return TRI_E_NOMEM;
+  *dev = p;
+  g_zero_allocs++;
+  g_zero_bytes += bytes;
   return 0;
 }
 
@@ -237,7 +249,14 @@ void trifake_reset() {
   g_timers = g_timer_destroys = g_scratch_allocs = g_scratch_frees = 0;
   g_scratch_bytes = 0;
   g_scratch_fail = false;
+  g_zero_allocs = 0;
+  g_zero_bytes = 0;
   g_arch = "fake";
+}
+// zeroed scratch allocations of split norm versions and their total bytes
+void trifake_zero_allocs(int64_t *out) {
+  out[0] = g_zero_allocs;
+  out[1] = int64_t(g_zero_bytes);
 }
 void trifake_set_cost(int32_t kvariant, int32_t ksub, uint32_t grid, float ms) {
   g_costs.push_back({kvariant, ksub, grid, ms});

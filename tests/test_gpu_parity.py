@@ -159,10 +159,13 @@ RN_CASES = [
     (nm.BF16, 130, 4096, "plain"), (nm.F32, 100, 256, "plain"), (nm.BF16, 70, 8192, "plain"),
     (nm.F32, 65, 4096, "unaligned"), (nm.BF16, 66, 4096, "strided"), (nm.F32, 67, 16384, "plain"),
     (nm.BF16, 13, 1024, "plain"), (nm.BF16, 13, 1032, "plain"), (nm.F32, 7, 512, "plain"),
-    # rows beyond the register forms: staged in LDS up to 128 KiB, two passes beyond
+    # rows beyond 4096 vectors: split over ceil(vectors / 2048) workgroups
+    # (3..16 here, a ragged last slice at 8193 vectors), two passes beyond 64
     (nm.BF16, 5, 40960, "plain"), (nm.BF16, 3, 65536, "strided"), (nm.BF16, 67, 49152, "plain"),
     (nm.BF16, 2, 65544, "plain"), (nm.F32, 4, 20480, "plain"), (nm.F32, 3, 32768, "plain"),
     (nm.F32, 2, 32772, "plain"), (nm.F32, 2, 131072, "plain"), (nm.BF16, 5, 40960, "unaligned"),
+    (nm.BF16, 300, 65536, "plain"), (nm.BF16, 3, 1048576, "plain"), (nm.F32, 2, 524288, "plain"),
+    (nm.BF16, 2, 1048584, "plain"), (nm.F32, 2, 524292, "plain"),
 ]
 
 
@@ -191,7 +194,36 @@ def test_rmsnorm_variants(tri, cache, dtype, T, H, layout, res):
     sel = cache.last_selection()
     es = 4 if dtype == nm.F32 else 2
     flags = S.ALIGN if (xd.data_ptr() % 16 == 0 and (xd.stride(0) * es) % 16 == 0) else 0
-    assert sel.variant == S.rn_role(S.DT_F32 if dtype == nm.F32 else S.DT_BF16, H, flags, T)[0]
+    assert sel.variant == S.rn_role(S.DT_F32 if dtype == nm.F32 else S.DT_BF16, H, flags, T,
+                                    S.bucket(T))[0]
+
+
+def test_split_rows_reuse_their_scratch(tri, cache):
+    """A split version's scratch is cleared by each call's last readers, so
+    back-to-back calls of one version (different data, fewer rows within the
+    bucket, the plain and the residual form, and calls of other versions in
+    between) each match the oracle; every row is checked."""
+    r = rng(17)
+    H = 65536                                   # bf16: 8192 vectors, 4 workgroups per row
+    w = wl.host_weight(r, H, nm.BF16)
+    wd = wl.to_torch(w, nm.BF16, DEV)
+    for step, T in enumerate((7, 8, 5, 8, 1)):  # bucket 3 for all but the last
+        x = wl.host_array(r, (T, H), nm.BF16)
+        res = wl.host_array(r, (T, H), nm.BF16)
+        xd, rd = wl.to_torch(x, nm.BF16, DEV), wl.to_torch(res, nm.BF16, DEV)
+        y = cache.rmsnorm(xd, wd, 1e-6)
+        y2, ro = cache.residual_rmsnorm(xd, rd, wd, 1e-6)
+        z = cache.rmsnorm(xd[:, :4096].contiguous(), wd[:4096].contiguous(), 1e-6)
+        torch.cuda.synchronize()
+        assert cache.last_selection().variant != S.RN_SPLIT
+        check(f"{step} y", host(y), O.rmsnorm(x, w, 1e-6, nm.BF16), nm.BF16)
+        wy, wh = O.residual_rmsnorm(x, res, w, 1e-6, nm.BF16)
+        check(f"{step} residual y", host(y2), wy, nm.BF16)
+        check(f"{step} res_out", host(ro), wh, nm.BF16, exact=True)
+        check(f"{step} short rows", host(z), O.rmsnorm(x[:, :4096], w[:4096], 1e-6, nm.BF16),
+              nm.BF16)
+    kinds = {cache.version_info(i).variant for i in range(cache.stats()["n_versions"])}
+    assert S.RN_SPLIT in kinds
 
 
 def test_rmsnorm_in_place(tri, cache):

@@ -813,15 +813,19 @@ def _last_launch(lib, nbytes=512, size=None):
     return kv.value, dt.value, sub.value, grid.value, block.value, stream.value, buf.raw
 
 
-def test_wide_rows_launch_1024_work_item_workgroups(lib, fresh):
-    """Rows of 4097..8192 vectors take RN_WIDE: one 1024-work-item workgroup
-    per row (standalone, residual, and as the norm launch of a three-launch
-    chain); every other launch has 256 work-items. Launches and records
-    match the model's plan."""
+def test_long_rows_launch_split_wide_and_loop_forms(lib, fresh):
+    """Rows beyond 4096 vectors are split over S = ceil(vectors / 2048)
+    workgroups of 256 (standalone, residual, and as the norm launch of a
+    three-launch chain); where the split's scratch for the key's bucket would
+    be too large a row of up to 8192 vectors takes one 1024-work-item
+    workgroup, and longer rows two passes. Launches and records match the
+    model's plan."""
     cache = fresh(flags=S.FLAG_AUTO_INSTALL)
-    cases = [(rn_call(BF, 3, 65536), [S.RN_WIDE]), (res_call(F, 2, 20480), [S.RN_WIDE]),
-             (rn_call(BF, 3, 65544), [S.RN_LOOP]), (rn_call(BF, 3, 32768), [S.RN_BLOCK[16]]),
-             (chain_call(BF, 2, 40960, 11008, 32, 32, 128), [S.RN_WIDE, S.ROPE_VEC, S.SW_FLAT])]
+    cases = [(rn_call(BF, 3, 65536), [S.RN_SPLIT]), (res_call(F, 2, 20480), [S.RN_SPLIT]),
+             (rn_call(BF, 3, 65544), [S.RN_SPLIT]), (rn_call(BF, 3, 32768), [S.RN_BLOCK[16]]),
+             (rn_call(BF, 3, 1048584), [S.RN_LOOP]),
+             (rn_call(BF, (1 << 19) + 1, 32776), [S.RN_WIDE]),
+             (chain_call(BF, 2, 40960, 11008, 32, 32, 128), [S.RN_SPLIT, S.ROPE_VEC, S.SW_FLAT])]
     for c, kinds in cases:
         n0 = lib.trifake_launch_count()
         assert c_call(lib, cache, c) == 0
@@ -831,6 +835,33 @@ def test_wide_rows_launch_1024_work_item_workgroups(lib, fresh):
         assert got == want and [g[0] for g in got] == kinds, (c.op, c.H, got)
         assert [g[2] for g in got] == [1024 if k == S.RN_WIDE else 256 for k in kinds]
         assert [tuple(l) for l in c_record(lib, cache)[6][:len(want)]] == want
+
+
+def test_split_rows_carry_the_version_scratch(lib, fresh):
+    """A split version owns a zeroed scratch sized for the top of its token
+    bucket (8 header words, S slots and one counter per row, 8 bytes each),
+    allocated at install; every launch of the version passes its address
+    after the row arguments (a 96-byte argument block); versions of other
+    forms allocate none; the cache frees it."""
+    import ctypes as C
+    lib.trifake_zero_allocs.argtypes = [C.POINTER(C.c_int64)]
+    counts = (C.c_int64 * 2)()
+    cache = fresh(flags=S.FLAG_AUTO_INSTALL)
+    lib.trifake_zero_allocs(counts)
+    base = list(counts)
+    c = res_call(BF, 3, 65536)                  # bucket 2 -> 4 rows, S = 4
+    ptrs = []
+    for _ in range(2):
+        assert c_call(lib, cache, c) == 0
+        kv, dt, sub, grid, block, stream, raw = _last_launch(lib)
+        assert (kv, grid, block, sub) == (S.RN_SPLIT, 12, 256, 1)
+        ptrs.append(int.from_bytes(raw[88:96], "little"))
+    assert ptrs[0] == ptrs[1] != 0
+    lib.trifake_zero_allocs(counts)
+    assert (counts[0] - base[0], counts[1] - base[1]) == (1, 8 * (8 + 4 * 5))
+    assert c_call(lib, cache, rn_call(BF, 3, 32768)) == 0      # RN_BLOCK[16]: none
+    lib.trifake_zero_allocs(counts)
+    assert counts[0] - base[0] == 1
 
 
 def test_rmsnorm_argument_block_and_stream(lib, fresh):

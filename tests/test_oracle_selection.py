@@ -123,24 +123,49 @@ def test_policy_tiny_f32_chain():
     (64, F, (11, 2)), (256, BF, (11, 2)), (520, BF, (12, 2)), (1024, BF, (12, 2)),
     (1032, BF, (13, 5)), (4096, F, (15, 5)), (8192, F, (16, 5)), (16384, F, (17, 5)),
     (32768, BF, (17, 5)), (100, BF, (10, 5)), (4097, F, (10, 5)),
-    # beyond 16 vectors per work-item (4096 vectors): a 1024-lane workgroup
-    # up to 8192 vectors (128 KiB) per row, two passes beyond
-    (32776, BF, (19, 5)), (65536, BF, (19, 5)), (65544, BF, (18, 5)),
-    (16388, F, (19, 5)), (32768, F, (19, 5)), (32772, F, (18, 5))])
+    # beyond 16 vectors per work-item (4096 vectors): split over
+    # S = ceil(vectors / 2048) workgroups, T * S of them, up to S = 64
+    (32776, BF, (20, 15)), (65536, BF, (20, 20)), (65544, BF, (20, 25)),
+    (16388, F, (20, 15)), (32768, F, (20, 20)), (32772, F, (20, 25)),
+    (1048576, BF, (20, 320)), (524288, F, (20, 320)),
+    # S = 65: beyond the split and beyond 8192 vectors -> two passes
+    (1048584, BF, (18, 5)), (524292, F, (18, 5))])
 def test_rmsnorm_policy_by_row_size(H, dtype, want):
-    # 5 rows: rows of <= 128 vectors take a wavefront each, 4 per block
-    # (2 blocks); longer rows one block per row (5 blocks). bf16 32776 =
-    # 4097 vectors: 17 per 256-lane work-item -> 1024 lanes; bf16 65536 =
-    # f32 32768 = exactly 8192 vectors -> 1024 lanes; 65544 bf16 / 32772
-    # f32 = 8193 vectors -> two passes.
-    v, g = S.rn_role(dtype, H, S.ALIGN | S.CONTIG, 5)
+    # 5 rows (bucket 3): rows of <= 128 vectors take a wavefront each, 4 per
+    # block (2 blocks); longer rows one block per row (5 blocks). bf16 32776
+    # = f32 16388 = 4097 vectors -> 3 split workgroups per row; bf16 65536 =
+    # f32 32768 = 8192 vectors -> 4; 8193 vectors -> 5; bf16 2^20 = f32 2^19
+    # = 131072 vectors -> 64 (the most); one more vector -> 65: two passes.
+    v, g = S.rn_role(dtype, H, S.ALIGN | S.CONTIG, 5, 3)
     assert (v, g) == want
+
+
+@pytest.mark.parametrize("dtype,H,b,want", [
+    # S = 64: scratch words 8 + 2^b * 65 <= 2^22 holds up to b = 15
+    (BF, 1048576, 15, S.RN_SPLIT), (BF, 1048576, 16, S.RN_LOOP),
+    # S = 3 (4097 vectors): 8 + 2^b * 4 <= 2^22 up to b = 19; beyond, the
+    # row still fits a 1024-lane workgroup
+    (BF, 32776, 19, S.RN_SPLIT), (BF, 32776, 20, S.RN_WIDE), (F, 16388, 22, S.RN_WIDE),
+    # S = 4 (8192 vectors): 8 + 2^b * 5 <= 2^22 up to b = 19
+    (F, 32768, 19, S.RN_SPLIT), (F, 32768, 20, S.RN_WIDE)])
+def test_split_rows_need_their_scratch_to_fit(dtype, H, b, want):
+    assert S.rn_role(dtype, H, S.ALIGN | S.CONTIG, 1, b)[0] == want
+
+
+def test_split_scratch_layout_by_hand():
+    # 3 rows of bf16 65536 (8192 vectors, 4 workgroups each): 8 header words,
+    # 12 slots, 3 counters
+    assert S.split_slices(BF, 65536) == 4 and S.split_words(3, 4) == 8 + 12 + 3
+    assert S.grid_of(S.RN_SPLIT, BF, 3, 65536) == 12
+    # f32 16388 = 4097 vectors: 3 workgroups, the last holds one vector
+    assert S.split_slices(F, 16388) == 3
 
 
 @pytest.mark.parametrize("T", [1, 8, 64, 65, 8192])
 def test_rmsnorm_policy_does_not_depend_on_tokens(T):
-    assert S.rn_role(BF, 4096, S.ALIGN | S.CONTIG, T) == (S.RN_BLOCK[2], T)
-    assert S.rn_role(F, 256, S.ALIGN | S.CONTIG, T) == (S.RN_WAVE[1], -(-T // 4))
+    b = S.bucket(T)
+    assert S.rn_role(BF, 4096, S.ALIGN | S.CONTIG, T, b) == (S.RN_BLOCK[2], T)
+    assert S.rn_role(F, 256, S.ALIGN | S.CONTIG, T, b) == (S.RN_WAVE[1], -(-T // 4))
 
 
 def test_unaligned_and_strided_layouts():

@@ -126,10 +126,11 @@ def test_unfused_chain_has_one_candidate():
     (1024, BF, [12, 13, 18]),      # 128 vectors: two per lane of a wavefront
     (4096, BF, [14, 18]),          # 512 vectors: workgroup x 2, loop
     (8200, BF, [16, 19, 18]),      # 1025 vectors: workgroup x 8, 1024-lane workgroup, loop
-    (32768, BF, [17, 19, 18]),     # 4096 vectors: workgroup x 16, 1024-lane workgroup, loop
-    (65536, BF, [19, 18]),         # 8192 vectors: 1024-lane workgroup x 8, loop
-    (65544, BF, [18]),             # 8193 vectors: loop only
-    (32768, F, [19, 18]),          # 8192 f32 vectors: 1024-lane workgroup x 8, loop
+    (32768, BF, [17, 19, 20, 18]),  # 4096 vectors: workgroup x 16, 1024 lanes, 2-way split, loop
+    (65536, BF, [20, 19, 18]),     # 8192 vectors: 4-way split, 1024-lane workgroup x 8, loop
+    (65544, BF, [20, 18]),         # 8193 vectors: 5-way split, loop (too long for 1024 lanes)
+    (32768, F, [20, 19, 18]),      # 8192 f32 vectors: 4-way split, 1024 lanes, loop
+    (1048584, BF, [18]),           # 131073 vectors: 65 workgroups is too many -> loop only
     (100, BF, [10]),               # ragged: scalar only
 ])
 def test_rmsnorm_candidates(H, dtype, want):
