@@ -367,6 +367,35 @@ tri_status tri_embedding(tri_cache *cache, tri_dtype dtype, const void *table, i
                          int64_t n_rows, const void *ids, int32_t ids_int64,
                          void *out, int64_t o_rs, int64_t T, int64_t H, void *stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation):
+ * tri_residual_rmsnorm that allocates nothing on any path. Same arguments,
+ * validation, guards, version lookup, kernels and selection records as
+ * tri_residual_rmsnorm, with two differences:
+ *  - it never installs: a miss returns TRI_MISS (key recorded for
+ *    tri_spec_install_last_miss) even under TRI_CACHE_AUTO_INSTALL, since
+ *    an install may allocate; install the version beforehand (an ordinary
+ *    call, tri_spec_install_key or tri_spec_import_keys);
+ *  - a version that splits its rows over several workgroups (rows of more
+ *    than 4096 16-byte vectors) exchanges its partial sums through the
+ *    library's fixed per-GPU array of TRI_NOALLOC_SCRATCH_BYTES (held from
+ *    the first cache created on that GPU until the process ends) instead of
+ *    the version's own scratch. A call needs 8 * (8 + T * (S + 1)) bytes of
+ *    it, S = ceil(H / (8 * 2048)) for bf16 (H / (4 * 2048) for f32); a
+ *    larger call returns TRI_E_UNSUPPORTED with nothing launched. Every
+ *    call on a GPU shares that GPU's array and leaves it zeroed for the
+ *    next: calls whose kernels overlap on one GPU (other streams, other
+ *    caches) race.
+ * TRI_E_RUNTIME if the array could not be located on the cache's device. */
+enum { TRI_NOALLOC_SCRATCH_BYTES = 1 << 20 };
+tri_status tri_residual_rmsnorm_noalloc(tri_cache *cache, tri_dtype dtype,
+                                        const void *x, int64_t x_rs,
+                                        const void *res, int64_t res_rs,
+                                        const void *w,
+                                        void *y, int64_t y_rs,
+                                        void *res_out, int64_t ro_rs,
+                                        int64_t T, int64_t H, float eps, void *stream);
+
 /* The decode chain: residual+RMSNorm, RoPE-QK (or QK-RMSNorm + RoPE when
  * q_norm_w is set; with the variant of rope_ext when set) and SwiGLU of one
  * decode step, on disjoint operands

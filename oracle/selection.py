@@ -61,6 +61,7 @@ SPLIT_SPAN = 8 * 256       # vectors one split workgroup holds
 SPLIT_MAX_SLICES = 64      # workgroups per row, at most
 SPLIT_HEADER_WORDS = 8     # scratch: header, then T*S slots and T counters (64-bit words)
 SPLIT_SCRATCH_WORDS = 1 << 22   # a version's scratch for the top of its bucket, at most
+NOALLOC_SCRATCH_BYTES = 1 << 20  # the allocation-free entry point's fixed scratch per GPU
 NORM_VARIANTS = (RN_SCALAR, *RN_WAVE.values(), *RN_BLOCK.values(), RN_LOOP, RN_WIDE, RN_SPLIT)
 ROPE_SCALAR, ROPE_VEC, ROPE_VEC_I, ROPE_QKN_SCALAR, ROPE_QKN_VEC, ROPE_QKN_VEC_I = \
     30, 31, 32, 33, 34, 35

@@ -284,6 +284,29 @@ class SpecCache:
                    _stream_ptr(stream, self._dev))
         return y, ro
 
+    def residual_rmsnorm_noalloc(self, x, residual, w, eps: float = 1e-6, out=None,
+                                 residual_out=None, stream=None):
+        """residual_rmsnorm through the allocation-free entry point
+        (tri_residual_rmsnorm_noalloc): the outputs must be given, nothing is
+        installed (a miss raises TriError with status MISS: install the
+        version first, e.g. with an ordinary call), and a split version uses
+        the GPU's fixed scratch."""
+        if out is None or residual_out is None:
+            raise ValueError("out and residual_out are required (nothing is allocated)")
+        T, H = _dims(x, "x", 2, self._dev)
+        _like(residual, "residual", x.shape, x.dtype, self._dev)
+        _like(out, "out", x.shape, x.dtype, self._dev)
+        _like(residual_out, "residual_out", x.shape, x.dtype, self._dev)
+        _vector(w, "w", H, x.dtype, self._dev)
+        st = _dll.tri_residual_rmsnorm_noalloc(
+            self._h, dtype_code(x.dtype), x.data_ptr(), _rows(x, "x", H), residual.data_ptr(),
+            _rows(residual, "residual", H), w.data_ptr(), out.data_ptr(), _rows(out, "out", H),
+            residual_out.data_ptr(), _rows(residual_out, "residual_out", H), T, H, eps,
+            _stream_ptr(stream, self._dev))
+        if st != OK:
+            raise TriError(st, "tri_residual_rmsnorm_noalloc")
+        return out, residual_out
+
     def _qk(self, q, k, pos, pos_dtype):
         """Shapes of q [T, nq, hd], k [T, nk, hd] (or None) and pos [T]: returns
         (T, nq, nk, hd, k pointer, k token stride)."""

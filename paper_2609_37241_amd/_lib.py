@@ -25,6 +25,7 @@ JIT = 2
 AUTOTUNE = 4
 TUNE_NONE, TUNE_MEASURED, TUNE_STORED, TUNE_SKIPPED = 0, 1, 2, 3
 KEY_WORDS = 6
+NOALLOC_SCRATCH_BYTES = 1 << 20
 ROPE_SCALING_NONE, ROPE_SCALING_LLAMA3 = 0, 1
 
 
@@ -102,6 +103,8 @@ SIGNATURES = {
     "tri_rmsnorm": (C.c_int, [_P, C.c_int, _P, _I64, _P, _P, _I64, _I64, _I64, _F, _P]),
     "tri_residual_rmsnorm": (C.c_int, [_P, C.c_int, _P, _I64, _P, _I64, _P, _P, _I64, _P, _I64,
                                        _I64, _I64, _F, _P]),
+    "tri_residual_rmsnorm_noalloc": (C.c_int, [_P, C.c_int, _P, _I64, _P, _I64, _P, _P, _I64,
+                                               _P, _I64, _I64, _I64, _F, _P]),
     "tri_rope_qk": (C.c_int, [_P, C.c_int, _P, _I64, _P, _I64, _P, _I64, _I32, _I32, _I32, _F,
                               _P]),
     "tri_rope_qk_ext": (C.c_int, [_P, C.c_int, _P, _I64, _P, _I64, _P, _I64, _I32, _I32, _I32,

@@ -223,13 +223,8 @@ inline RopeArgs rope_args(const Version &v, void *q, int64_t q_ts, void *kp, int
 // ---- lookup and launch bookkeeping -----------------------------------------------------
 // Finds the version for `k`. On a miss records it and, with auto-install,
 // installs and returns the new version (*auto_inst = true).
-inline int lookup(tri_cache *c, uint32_t op, const Key &k, int64_t T, int32_t *vi,
-                  bool *auto_inst) {
-  int32_t i = find_version(c, op, k);
-  if (i >= 0) {
-    *vi = i;
-    return TRI_OK;
-  }
+// The bookkeeping of a miss: counter, recorded key, selection record.
+inline tri_selection &note_miss(tri_cache *c, uint32_t op, const Key &k, int64_t T) {
   c->stats.misses++;
   c->has_miss = true;
   c->miss_key = k;
@@ -239,10 +234,19 @@ inline int lookup(tri_cache *c, uint32_t op, const Key &k, int64_t T, int32_t *v
   r.op = int32_t(op);
   r.version = -1;
   key_words(k, r.key);
-  if (!(c->flags & TRI_CACHE_AUTO_INSTALL)) {
-    r.status = TRI_MISS;
-    return TRI_MISS;
+  r.status = TRI_MISS;
+  return r;
+}
+
+inline int lookup(tri_cache *c, uint32_t op, const Key &k, int64_t T, int32_t *vi,
+                  bool *auto_inst) {
+  int32_t i = find_version(c, op, k);
+  if (i >= 0) {
+    *vi = i;
+    return TRI_OK;
   }
+  tri_selection &r = note_miss(c, op, k, T);
+  if (!(c->flags & TRI_CACHE_AUTO_INSTALL)) return TRI_MISS;
   const tri_status st = install_key(c, k);
   if (st != TRI_OK) {
     r.status = st;
@@ -631,6 +635,50 @@ tri_status tri_residual_rmsnorm(tri_cache *c, tri_dtype dtype, const void *x, in
                          uint64_t(H), 0, 0, 0, 0);
   const RnArgs a{x, res, w, y, res_out, x_rs, res_rs, y_rs, ro_rs, T, int32_t(H), eps};
   return norm_launch(c, op, k, a, stream);
+}
+
+tri_status tri_residual_rmsnorm_noalloc(tri_cache *c, tri_dtype dtype, const void *x,
+                                        int64_t x_rs, const void *res, int64_t res_rs,
+                                        const void *w, void *y, int64_t y_rs, void *res_out,
+                                        int64_t ro_rs, int64_t T, int64_t H, float eps,
+                                        void *stream) {
+  if (!c) return TRI_E_INVALID;
+  const uint32_t op = TRI_OP_RES_RMSNORM;
+  c->stats.calls++;
+  int st = check_common(dtype, T);
+  if (st != kGo) return finish_early(c, op, st);
+  const uint64_t es = es_of(dtype);
+  const void *ptrs[5] = {x, res, w, y, res_out};
+  const int64_t strides[4] = {x_rs, res_rs, y_rs, ro_rs};
+  st = check_norm(es, T, H, ptrs, 5, strides, 4, eps);
+  if (st != kGo) return finish_early(c, op, st);
+
+  const Key k = make_key(op, dtype, T,
+                         res_flags(es, x, x_rs, res, res_rs, w, y, y_rs, res_out, ro_rs, H), 0,
+                         uint64_t(H), 0, 0, 0, 0);
+  // Lookup only: an install may allocate, so a miss is returned as is.
+  const int32_t vi = find_version(c, op, k);
+  if (vi < 0) {
+    note_miss(c, op, k, T);
+    return TRI_MISS;
+  }
+  Version &v = c->versions[vi];
+  const int32_t kv = v.plan.kvariant[0];
+  const RnArgs a{x, res, w, y, res_out, x_rs, res_rs, y_rs, ro_rs, T, int32_t(H), eps};
+  const tri_launch_rec l{kv, role_grid(kv, uint32_t(dtype), T, H), role_block(kv)};
+  int rc;
+  if (kv == RN_SPLIT) {
+    // the GPU's fixed scratch in place of the version's own
+    if (!c->noalloc_scratch) return finish_early(c, op, TRI_E_RUNTIME);
+    if (split_words(T, split_slices(uint32_t(dtype), H)) > kNoAllocScratchWords)
+      return finish_early(c, op, TRI_E_UNSUPPORTED);
+    const RnSplitArgs sa{a, static_cast<uint64_t *>(c->noalloc_scratch)};
+    rc = be_launch(v.fn[0], l.grid_x, l.block_x, &sa, sizeof sa, stream);
+  } else {
+    rc = be_launch(v.fn[0], l.grid_x, l.block_x, &a, sizeof a, stream);
+  }
+  record(c, op, v, vi, k, 1, &l, rc ? TRI_E_LAUNCH : TRI_OK);
+  return finish(c, v, false, rc);
 }
 
 tri_status tri_rope_qk_ext(tri_cache *c, tri_dtype dtype, void *q, int64_t q_ts, void *kp,

@@ -302,6 +302,9 @@ tri_status tri_spec_cache_create(tri_cache **out, uint32_t capacity, uint32_t fl
     free(c);
     return tri_status(st);
   }
+  // the allocation-free entry point's fixed scratch on this device (a
+  // failed lookup only disables the split rows of that entry point)
+  if (be_noalloc_scratch(device, &c->noalloc_scratch) != 0) c->noalloc_scratch = nullptr;
   c->capacity = capacity;
   c->flags = flags;
   c->device = device;

@@ -198,6 +198,11 @@ int be_timer_record(void *timer, uint32_t i);                 // event i on the 
 int be_timer_elapsed(void *timer, uint32_t i, uint32_t j, float *ms);   // waits for event j
 void be_timer_destroy(void *timer);
 void be_arch(char *out, uint32_t cap);                         // device architecture name
+// The fixed scratch of the allocation-free entry point: the device address
+// of this device's copy of the library's static array (looked up once per
+// device, with that device current). 0 or tri_status.
+constexpr uint64_t kNoAllocScratchWords = uint64_t(TRI_NOALLOC_SCRATCH_BYTES) / 8;
+int be_noalloc_scratch(int device, void **ptr);
 
 // ---- versions and the cache ------------------------------------------------------------
 struct Version {
@@ -234,6 +239,7 @@ struct tri_cache {
   tri_stats stats;
   tri_selection last;
   void *empty_fn;
+  void *noalloc_scratch;         // this device's static scratch, or null
   char code_dir[1024];           // compiled code objects; empty: none
 };
 

@@ -1,10 +1,41 @@
 // RMSNorm and residual-add + RMSNorm kernels, one per install-policy variant
 // and dtype. Row bodies live in device.h (shared with the fused chain).
+#include <mutex>
+
 #include "../internal.h"
 #include "device.h"
 
 namespace tri {
 using namespace dev;
+
+// The fixed exchange scratch of tri_residual_rmsnorm_noalloc: one copy per
+// GPU, zero at load, left zero by every split call. In host code the name
+// stands for a host-side shadow, not for device memory: kernels receive the
+// device address looked up below, never the name.
+static __device__ __align__(256) uint64_t scratch[kNoAllocScratchWords];
+
+namespace {
+std::mutex g_scratch_mu;
+constexpr int kMaxDevices = 64;
+void *g_scratch_ptr[kMaxDevices];
+int g_scratch_status[kMaxDevices];   // 0: not looked up; 1: found; -1: failed
+}  // namespace
+
+// Device address of `device`'s copy of `scratch`, looked up once per device
+// with that device current (the caller's contract: cache creation).
+int be_noalloc_scratch(int device, void **ptr) {
+  *ptr = nullptr;
+  if (device < 0 || device >= kMaxDevices) return TRI_E_RUNTIME;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_status[device] == 0) {
+    void *p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    g_scratch_status[device] = e == hipSuccess && p ? 1 : -1;
+    g_scratch_ptr[device] = g_scratch_status[device] == 1 ? p : nullptr;
+  }
+  *ptr = g_scratch_ptr[device];
+  return g_scratch_status[device] == 1 ? 0 : TRI_E_RUNTIME;
+}
 
 template <int DT, int NV, bool RES>
 __global__ __launch_bounds__(256) void k_rn_wave(RnArgs a) {

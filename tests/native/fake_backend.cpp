@@ -112,6 +112,17 @@ int be_alloc_zeroed(uint64_t bytes, void **dev) {
 
 void be_free(void *dev) { free(dev); }
 
+// The allocation-free entry point's fixed scratch: one host array standing
+// in for every device's copy (looked up once, counted).
+uint64_t g_noalloc[kNoAllocScratchWords];
+int64_t g_noalloc_lookups = 0;
+int be_noalloc_scratch(int device, void **ptr) {
+  (void)device;
+  g_noalloc_lookups++;
+  *ptr = g_noalloc;
+  return 0;
+}
+
 // Runtime compilation: the "code object" is the source behind a 4-byte
 // tag; loading records the source and hands out a handle that encodes the
 // position of the source in the log (bit 41 marks it).
@@ -251,7 +262,14 @@ void trifake_reset() {
   g_scratch_fail = false;
   g_zero_allocs = 0;
   g_zero_bytes = 0;
+  tri::g_noalloc_lookups = 0;
   g_arch = "fake";
+}
+// address of the fixed scratch of the allocation-free entry point, and the
+// lookups made
+void *trifake_noalloc_scratch(int64_t *lookups) {
+  if (lookups) *lookups = tri::g_noalloc_lookups;
+  return tri::g_noalloc;
 }
 // zeroed scratch allocations of split norm versions and their total bytes
 void trifake_zero_allocs(int64_t *out) {
