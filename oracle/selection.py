@@ -71,6 +71,7 @@ CH_FUSED, CH_SEQ = 50, 51
 ELT_SCALAR, ELT_FLAT, ELT_FLAT_U2, ELT_ROWS = 60, 61, 62, 63
 EMB_SCALAR, EMB_VEC = 70, 71
 DECODE_BUCKET_MAX = 6       # buckets up to here are decode sized
+BUCKET_MAX = 22             # ceil(log2 T) of the largest T
 
 BLOCK = 256
 GRID_CAP = 1 << 20
@@ -84,6 +85,7 @@ DEFAULT_CAPACITY = 256
 MAX_CAPACITY = 4096
 FLAG_AUTO_INSTALL = 1
 FLAG_JIT = 2               # compiled specializations: same selections, same records
+FLAG_GENERIC = 8           # a miss installs a generic (range-guarded) version
 
 ALIGN, CONTIG = 1, 2       # per-op guard flag bits
 CHAIN_QK_NORM = 0x40       # chain key flag: the RoPE step has the QK RMSNorm
@@ -1000,6 +1002,100 @@ def tune_choice(times: List[float]) -> int:
     keep = np.float32(times[best]) < np.float32(TUNE_MARGIN) * np.float32(times[0])
     return best if keep else 0
 
+# ---- guards: exact and generic versions ------------------------------------------
+# The paper's guards can hold across many concrete inputs (a rank check and a
+# shape bound, Sec. 3.2, Fig. 4), so versions may overlap and Algorithm 1's
+# first match in creation order decides. An exact version matches its key
+# only. A generic version matches every key equal to its own except that
+#  * the token bucket may lie anywhere in [b_lo, b_hi], the widest run of
+#    buckets around its own over which the install policy's plan (kernels,
+#    roles, RoPE geometry) does not change;
+#  * for norm rows held by one wavefront or one workgroup (or the scalar
+#    kernel) H may lie anywhere in [h_lo, h_hi] within its divisibility
+#    class: the row lengths the same kernel serves, for every bucket.
+# Plans that split norm rows (their scratch is sized by H and the bucket) get
+# exact versions only. Plan equality is candidate-0 equality.
+H_ANY, H_MULTIPLE, H_RAGGED = 0, 1, 2        # divisibility classes of a generic H range
+
+
+@dataclasses.dataclass(frozen=True)
+class Guard:
+    """What a version matches: `key` exactly (b_lo < 0), or generic ranges."""
+    key: Tuple[int, ...]
+    b_lo: int = -1
+    b_hi: int = -1
+    h_lo: int = 0          # 0: H must equal the key's
+    h_hi: int = 0
+    h_mod: int = H_ANY
+
+    def holds(self, key) -> bool:
+        key = tuple(key)
+        if self.b_lo < 0:
+            return key == self.key
+        bucket_bits = 0xFF << 16
+        if key[0] & ~bucket_bits != self.key[0] & ~bucket_bits:
+            return False
+        if not self.b_lo <= (key[0] >> 16) & 0xFF <= self.b_hi:
+            return False
+        if self.h_lo:                      # word 1: H in the low half, I in the high half
+            if key[1] >> 32 != self.key[1] >> 32:
+                return False
+            H = key[1] & 0xFFFFFFFF
+            v = 16 // elem_size((self.key[0] >> 8) & 0xFF)
+            if not self.h_lo <= H <= self.h_hi:
+                return False
+            if (self.h_mod == H_MULTIPLE and H % v) or (self.h_mod == H_RAGGED and H % v == 0):
+                return False
+        elif key[1] != self.key[1]:
+            return False
+        return key[2:] == self.key[2:]
+
+
+def _with_bucket(key, b: int):
+    k = list(key)
+    k[0] = (k[0] & ~(0xFF << 16)) | (b << 16)
+    return tuple(k)
+
+
+def _norm_h_range(dt: int, H: int, fl: int):
+    """(h_lo, h_hi, h_mod) of the rows the norm kernel chosen for H serves at
+    every bucket, or None when the choice depends on the bucket (rows beyond
+    4096 vectors)."""
+    v = 16 // elem_size(dt)
+    if not fl & ALIGN:
+        return 1, H_LIMIT - 1, H_ANY
+    if H % v:
+        return 1, H_LIMIT - 1, H_RAGGED
+    n = H // v
+    for lo, hi in ((1, 64), (65, 128), (129, 256), (257, 512), (513, 1024), (1025, 2048),
+                   (2049, 4096)):
+        if lo <= n <= hi:
+            return lo * v, hi * v, H_MULTIPLE
+    return None
+
+
+def generic_guard(key) -> Guard:
+    """The guard of the generic version a miss on `key` installs (exact when
+    the plan splits norm rows)."""
+    P = candidates(key)[0]
+    if RN_SPLIT in P.kernels or RN_SPLIT in P.roles:
+        return Guard(tuple(key))
+    f = unpack_key(key)
+    b = f["bucket"]
+    lo = b
+    while lo > 0 and candidates(_with_bucket(key, lo - 1))[0] == P:
+        lo -= 1
+    hi = b
+    while hi < BUCKET_MAX and candidates(_with_bucket(key, hi + 1))[0] == P:
+        hi += 1
+    h = None
+    if f["op"] in (OP_RMSNORM, OP_RES_RMSNORM):
+        h = _norm_h_range(f["dtype"], f["H"], f["flags"])
+    if h is None:
+        return Guard(tuple(key), lo, hi)
+    return Guard(tuple(key), lo, hi, *h)
+
+
 # ---- the cache -----------------------------------------------------------------
 @dataclasses.dataclass
 class Stats:
@@ -1019,12 +1115,13 @@ class SpecCacheModel:
         call; used by a tuning cache (FLAG_AUTOTUNE) for keys with several
         candidates."""
         if capacity < 0 or capacity > MAX_CAPACITY or \
-                flags & ~(FLAG_AUTO_INSTALL | FLAG_JIT | FLAG_AUTOTUNE):
+                flags & ~(FLAG_AUTO_INSTALL | FLAG_JIT | FLAG_AUTOTUNE | FLAG_GENERIC):
             raise ValueError("invalid cache parameters")
         self.capacity = capacity or DEFAULT_CAPACITY
         self.flags = flags
         self.timer = timer
-        self.versions: List[Tuple[int, ...]] = []
+        self.versions: List[Tuple[int, ...]] = []   # the key each version was made for
+        self.guards: List[Guard] = []
         self.choice: List[int] = []        # candidate index per version
         self.tuned: List[int] = []         # TUNE_* per version
         self.version_hits: List[int] = []
@@ -1038,8 +1135,8 @@ class SpecCacheModel:
 
     def lookup(self, key) -> int:
         """Algorithm 1's scan: index of the first version whose guards hold."""
-        for i, vkey in enumerate(self.versions):
-            if vkey == key:
+        for i, g in enumerate(self.guards):
+            if g.holds(key):
                 return i
         return -1
 
@@ -1074,7 +1171,7 @@ class SpecCacheModel:
                 rec.status = MISS
                 self.last = rec
                 return MISS
-            st = self._install(key)
+            st = self._install(key, generic=bool(self.flags & FLAG_GENERIC))
             if st < 0:
                 rec.status = st
                 self.last = rec
@@ -1141,7 +1238,8 @@ class SpecCacheModel:
                 return done(MISS)
             for i in range(first_miss, last + 1):
                 if vis[i] is not None and vis[i] < 0:
-                    st = self._install(keys[i])
+                    # an earlier layer's generic install may already cover it
+                    st = self._install(keys[i], generic=bool(self.flags & FLAG_GENERIC))
                     if st < 0:
                         return done(st)
                     vis[i] = self.lookup(keys[i])
@@ -1174,9 +1272,11 @@ class SpecCacheModel:
         key = self.versions[i]
         return cand_plan(key, candidates(key)[self.choice[i]], T)
 
-    def _install(self, key, candidate: int = -1) -> int:
+    def _install(self, key, candidate: int = -1, generic: bool = False) -> int:
         """Install `key` with candidate plan `candidate` (-1: tuned on a
-        tuning cache, else the policy's plan)."""
+        tuning cache, else the policy's plan), as a generic version when
+        `generic`. A key some version already matches adds nothing: a version
+        appended behind it could never be selected."""
         if self.lookup(key) >= 0:
             return OK
         cands = candidates(key)
@@ -1192,6 +1292,7 @@ class SpecCacheModel:
                 choice = tune_choice([self.timer(key, j, c) for j, c in enumerate(cands)])
                 tuned = TUNE_MEASURED
         self.versions.append(key)
+        self.guards.append(generic_guard(key) if generic else Guard(tuple(key)))
         self.choice.append(choice)
         self.tuned.append(tuned)
         self.version_hits.append(0)
@@ -1219,7 +1320,7 @@ class SpecCacheModel:
         if self.last_miss is None:
             return E_INVALID, None
         key, T = self.last_miss
-        st = self._install(key)
+        st = self._install(key, generic=bool(self.flags & FLAG_GENERIC))
         if st < 0:
             return st, None
         variant, roles, launches = self.version_plan(self.lookup(key), T)
