@@ -131,10 +131,10 @@ def measured_traffic():
     return float(fields["chain_traffic_bytes"])
 
 
-def run_mixed_stream(tri, wl, bench, dev, stream, torch, autotune=False):
+def run_mixed_stream(tri, wl, bench, dev, stream, torch, autotune=False, generic=False):
     """The 10,000-call mixed stream: token counts 1..512, 90 % bf16, 5 % unaligned
     or padded layouts, through a fresh cache (installs timed and tuned with
-    `autotune`); every call synchronised."""
+    `autotune`; generic versions with `generic`); every call synchronised."""
     Tmax = max(wl.MIXED_T_CHOICES)
     H, I, nq, nk, hd = wl.MIXED_H, wl.MIXED_I, wl.MIXED_NQ, wl.MIXED_NK, wl.MIXED_HD
     calls = wl.mixed_stream()
@@ -152,7 +152,7 @@ def run_mixed_stream(tri, wl, bench, dev, stream, torch, autotune=False):
         return torch.randn(shape, device=dev).to(td)
 
     arr = (tri.ChainArgs * len(calls))()
-    cache = tri.SpecCache(autotune=autotune)
+    cache = tri.SpecCache(autotune=autotune, generic=generic)
     for i, (T, dt, layout) in enumerate(calls):
         if (dt, layout) not in bufs:
             td = torch.bfloat16 if dt == wl.BF16 else torch.float32
@@ -587,6 +587,8 @@ def main():
     mixed = None if args.no_stream else run_mixed_stream(tri, wl, bench, dev, stream, torch)
     mixed_tuned = None if args.no_stream else run_mixed_stream(tri, wl, bench, dev, stream,
                                                                torch, autotune=True)
+    mixed_generic = None if args.no_stream else run_mixed_stream(tri, wl, bench, dev, stream,
+                                                                 torch, generic=True)
 
     # ---- the 1-token chain through a tuning cache --------------------------------------
     tc = tri.SpecCache(autotune=True)
@@ -847,6 +849,7 @@ def main():
 
     latency["mixed_stream"] = mixed
     latency["mixed_stream_autotuned"] = mixed_tuned
+    latency["mixed_stream_generic"] = mixed_generic
     emit(args, ce, wall, latency, bandwidth, roofline, cpu)
 
 

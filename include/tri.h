@@ -84,8 +84,13 @@ enum { TRI_MAX_LAYERS = 1024 };   /* layers per tri_decode_chain_layers call */
 enum {
   TRI_CACHE_AUTO_INSTALL = 1u,   /* on a miss: install, then launch */
   TRI_CACHE_JIT = 2u,            /* install compiles a key-specialized kernel */
-  TRI_CACHE_AUTOTUNE = 4u        /* install times the key's candidate plans */
+  TRI_CACHE_AUTOTUNE = 4u,       /* install times the key's candidate plans */
+  TRI_CACHE_GENERIC = 8u         /* a miss installs a generic (range) version */
 };
+
+/* Divisibility class of a generic version's hidden-size range
+ * (tri_version_info.h_mod). */
+enum { TRI_H_ANY = 0, TRI_H_MULTIPLE = 1, TRI_H_RAGGED = 2 };
 
 /* How a version's plan was chosen (tri_version_info.tuned). */
 enum {
@@ -144,6 +149,14 @@ typedef struct tri_version_info {
   int32_t tuned;       /* TRI_TUNE_*                                          */
   float tune_ms;       /* install time spent tuning                          */
   int32_t rope_tokens; /* tokens per workgroup of the RoPE role (1: one)     */
+  /* Guards (Sec. 3.2): an exact version (b_lo < 0) matches its key only; a
+   * generic one matches every key equal to its own except that the token
+   * bucket may lie in [b_lo, b_hi] and, when h_lo > 0, the hidden size H in
+   * [h_lo, h_hi] within class h_mod (TRI_H_*: any; a whole number of 16-byte
+   * vectors; not one). */
+  int32_t b_lo, b_hi;
+  uint32_t h_lo, h_hi;
+  int32_t h_mod;
 } tri_version_info;
 
 /* RoPE variants. A zeroed struct (or a NULL pointer where one is taken) is
@@ -225,8 +238,8 @@ typedef struct tri_chain_args {
 /* ---- cache ---------------------------------------------------------------- */
 
 /* Create an empty cache on the current device. capacity 0 selects 256
- * (at most 4096); flags: TRI_CACHE_AUTO_INSTALL, TRI_CACHE_JIT and
- * TRI_CACHE_AUTOTUNE in any combination. The
+ * (at most 4096); flags: TRI_CACHE_AUTO_INSTALL, TRI_CACHE_JIT,
+ * TRI_CACHE_AUTOTUNE and TRI_CACHE_GENERIC in any combination. The
  * cache owns every version, its kernel handles (and, with TRI_CACHE_JIT,
  * its loaded code objects) and its device constants; release it with
  * tri_spec_cache_destroy. Errors: INVALID (NULL out, capacity or flags out
@@ -263,6 +276,24 @@ typedef struct tri_chain_args {
  * read it instead of timing. With TRI_CACHE_JIT the chosen plan is then
  * compiled. Installs (and so misses under auto-install) allocate, create a
  * stream and synchronize: do them before capturing a graph. */
+/* TRI_CACHE_GENERIC: the paper's guards can hold across many concrete
+ * inputs (Sec. 3.2: a rank check and a shape bound such as
+ * weight.numel() <= 4096), so versions may overlap and the first one in
+ * creation order whose guards hold runs (Algorithm 1). With this flag an
+ * install made for a miss (auto-install, tri_spec_install_last_miss)
+ * creates a generic version: it matches the missed key with any token
+ * bucket in the widest run of buckets around the key's over which the
+ * install policy picks the same plan, and -- for RMSNorm and residual
+ * RMSNorm rows held by one wavefront or one workgroup, or by the scalar
+ * kernel -- any hidden size that kernel serves (rows of 1-64, 65-128,
+ * 129-256, ..., 2049-4096 16-byte vectors, every length of the scalar
+ * kernel's class). Plans that split norm rows over workgroups get exact
+ * versions. tri_spec_install_key and tri_spec_import_keys always create
+ * exact versions, so exact versions installed first take precedence over
+ * later generic ones that overlap them, and a key that an installed
+ * version already matches installs nothing (a version behind it could
+ * never run). With TRI_CACHE_JIT, a version with a hidden-size range runs
+ * the precompiled kernels (a compiled specialization fixes H). */
 tri_status tri_spec_cache_create(tri_cache **out, uint32_t capacity, uint32_t flags);
 void tri_spec_cache_destroy(tri_cache *cache);
 
@@ -452,10 +483,11 @@ void tri_graph_destroy(tri_graph *graph);
 /* Install a version for the key of the most recent MISS (Sec. 3.5: growth on
  * a miss): the install policy picks the kernel variant(s) from the key, the
  * kernel handles are resolved once, per-version constants (the RoPE inverse
- * frequencies) are uploaded, and the version is appended. Idempotent: a key
- * already installed adds nothing. `out` (nullable) receives the selection a
- * call with the missed arguments will make. Errors: INVALID (no miss yet),
- * FULL, NOMEM, RUNTIME. */
+ * frequencies) are uploaded, and the version is appended (generic under
+ * TRI_CACHE_GENERIC). Idempotent: a key that an installed version already
+ * matches adds nothing. `out` (nullable) receives the selection a call with
+ * the missed arguments will make. Errors: INVALID (no miss yet), FULL,
+ * NOMEM, RUNTIME. */
 tri_status tri_spec_install_last_miss(tri_cache *cache, tri_selection *out);
 
 /* Copy the selection record of the last entry call. */

@@ -200,16 +200,19 @@ class SpecCache:
     """One native specialization cache (bound to the current device)."""
 
     def __init__(self, capacity: int = 0, auto_install: bool = False, jit: bool = False,
-                 code_dir: Optional[str] = None, autotune: bool = False):
+                 code_dir: Optional[str] = None, autotune: bool = False,
+                 generic: bool = False):
         """jit: installs compile key-specialized kernels with hipRTC; autotune:
         installs time the key's candidate plans and keep the fastest; code_dir:
         a directory of compiled code objects and tuning results shared across
-        processes."""
+        processes; generic: a miss installs a generic version that also
+        serves the token buckets (and norm row lengths) with the same plan."""
         h = C.c_void_p()
         st = _dll.tri_spec_cache_create(C.byref(h), capacity,
                                         (AUTO_INSTALL if auto_install else 0)
                                         | (L.JIT if jit else 0)
-                                        | (L.AUTOTUNE if autotune else 0))
+                                        | (L.AUTOTUNE if autotune else 0)
+                                        | (L.GENERIC if generic else 0))
         if st != OK:
             raise TriError(st, "tri_spec_cache_create")
         self._h = h

@@ -23,6 +23,7 @@ MAX_LAYERS = 1024
 AUTO_INSTALL = 1
 JIT = 2
 AUTOTUNE = 4
+GENERIC = 8
 TUNE_NONE, TUNE_MEASURED, TUNE_STORED, TUNE_SKIPPED = 0, 1, 2, 3
 KEY_WORDS = 6
 NOALLOC_SCRATCH_BYTES = 1 << 20
@@ -61,7 +62,8 @@ class VersionInfo(C.Structure):
                 ("n_launches", C.c_int32), ("kernels", C.c_int32 * 3),
                 ("rope_slices", C.c_int32), ("candidate", C.c_int32),
                 ("n_candidates", C.c_int32), ("tuned", C.c_int32), ("tune_ms", C.c_float),
-                ("rope_tokens", C.c_int32)]
+                ("rope_tokens", C.c_int32), ("b_lo", C.c_int32), ("b_hi", C.c_int32),
+                ("h_lo", C.c_uint32), ("h_hi", C.c_uint32), ("h_mod", C.c_int32)]
 
 
 class RopeExt(C.Structure):
@@ -93,7 +95,7 @@ class ChainArgs(C.Structure):
 
 
 assert C.sizeof(Selection) == 120 and C.sizeof(ChainArgs) == 240 and C.sizeof(RopeExt) == 48
-assert C.sizeof(VersionInfo) == 120
+assert C.sizeof(VersionInfo) == 144
 
 _P, _I64, _I32, _F, _U32 = C.c_void_p, C.c_int64, C.c_int32, C.c_float, C.c_uint32
 

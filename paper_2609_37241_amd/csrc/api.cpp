@@ -247,7 +247,7 @@ inline int lookup(tri_cache *c, uint32_t op, const Key &k, int64_t T, int32_t *v
   }
   tri_selection &r = note_miss(c, op, k, T);
   if (!(c->flags & TRI_CACHE_AUTO_INSTALL)) return TRI_MISS;
-  const tri_status st = install_key(c, k);
+  const tri_status st = install_key(c, k, -1, (c->flags & TRI_CACHE_GENERIC) != 0);
   if (st != TRI_OK) {
     r.status = st;
     return st;
@@ -507,7 +507,8 @@ int layers_prepare(tri_cache *c, const tri_chain_args *layers, uint32_t n_layers
     for (uint32_t i = uint32_t(first_miss); i <= uint32_t(lp->last); ++i) {
       if (lp->vis[i] >= 0 || layers[i].T == 0) continue;
       chain_check(&layers[i], &k);
-      const tri_status ist = install_key(c, k);
+      // an earlier layer's generic install may already cover this key
+      const tri_status ist = install_key(c, k, -1, (c->flags & TRI_CACHE_GENERIC) != 0);
       if (ist != TRI_OK) {
         r.status = ist;
         return ist;

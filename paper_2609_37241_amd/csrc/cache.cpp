@@ -2,32 +2,59 @@
 // counters and introspection.
 //
 // Versions are kept in creation order and looked up with the first-match
-// rule of the paper's ordered dispatch (Algorithm 1, Sec. 3.2). Guards are
-// equality tests on a packed key and install is idempotent, so at most one
-// version matches a key; checking the op's last hit before the ordered scan
-// therefore returns exactly the version the scan would.
+// rule of the paper's ordered dispatch (Algorithm 1, Sec. 3.2): the first
+// version whose guard holds. Exact guards are equality on the packed key;
+// generic guards accept ranges of token buckets (and of norm row lengths),
+// so versions may overlap. Every guard is a function of the key alone and
+// versions are only ever appended, so the first match of a key never
+// changes once found: the op's last lookup key and a direct-mapped memo of
+// keys return exactly the version the scan would, without scanning.
 #include <math.h>
 #include <stdio.h>
 #include <stdlib.h>
 #include <string.h>
 
 #include <chrono>
+#include <initializer_list>
 
 #include "internal.h"
 
 namespace tri {
 
+int32_t scan_versions(const tri_cache *c, const Key &k) {
+  const uint32_t n = c->n_versions;
+  for (uint32_t i = 0; i < n; ++i)
+    if (guard_holds(c->versions[i].key, c->versions[i].guard, k)) return int32_t(i);
+  return -1;
+}
+
+namespace {
+inline uint32_t memo_slot(const Key &k) {
+  uint64_t h = k.k0 * 0x9E3779B97F4A7C15ull;
+  for (uint64_t w : {k.k1, k.k2, k.k3, k.k4, k.k5})
+    h = (h ^ (w + 0x632BE59BD9B4E019ull + (h << 6) + (h >> 2))) * 0xBF58476D1CE4E5B9ull;
+  return uint32_t(h ^ (h >> 29)) & (kMemoSlots - 1);
+}
+}  // namespace
+
 int32_t find_version(tri_cache *c, uint32_t op, const Key &k) {
   const int32_t h = c->last_hit[op];
-  if (h >= 0 && c->versions[h].key == k) return h;
-  const uint32_t n = c->n_versions;
-  for (uint32_t i = 0; i < n; ++i) {
-    if (c->versions[i].key == k) {
-      c->last_hit[op] = int32_t(i);
-      return int32_t(i);
+  if (h >= 0 && c->last_key[op] == k) return h;
+  MemoSlot *m = c->memo ? &c->memo[memo_slot(k)] : nullptr;
+  int32_t i;
+  if (m && m->version >= 0 && m->key == k) {
+    i = m->version;
+  } else {
+    i = scan_versions(c, k);
+    if (i < 0) return -1;   // a miss is not remembered: an install may follow
+    if (m) {
+      m->key = k;
+      m->version = i;
     }
   }
-  return -1;
+  c->last_hit[op] = i;
+  c->last_key[op] = k;
+  return i;
 }
 
 namespace {
@@ -134,9 +161,10 @@ bool plan_splits(const Plan &p) {
 
 }  // namespace
 
-tri_status install_key(tri_cache *c, const Key &k, int32_t candidate) {
-  for (uint32_t i = 0; i < c->n_versions; ++i)
-    if (c->versions[i].key == k) return TRI_OK;          // idempotent
+tri_status install_key(tri_cache *c, const Key &k, int32_t candidate, bool generic) {
+  // A key that a version already matches adds nothing: a version appended
+  // behind that one could never be selected.
+  if (scan_versions(c, k) >= 0) return TRI_OK;
   Plan cands[kMaxCandidates];
   const int nc = plan_candidates(k, cands);
   if (candidate < -1 || candidate >= nc) return TRI_E_INVALID;
@@ -145,6 +173,7 @@ tri_status install_key(tri_cache *c, const Key &k, int32_t candidate) {
   Version v;
   memset(&v, 0, sizeof v);
   v.key = k;
+  v.guard = generic ? generic_guard(k) : kExact;
   v.n_candidates = nc;
   v.candidate = candidate < 0 ? 0 : candidate;
   const uint32_t dt = key_dtype(k);
@@ -208,7 +237,9 @@ tri_status install_key(tri_cache *c, const Key &k, int32_t candidate) {
     v.scratch_words = 0;
   }
 
-  if (c->flags & TRI_CACHE_JIT) {
+  // A compiled specialization fixes the key's shape fields, so a version
+  // with a range of row lengths runs the precompiled kernels.
+  if ((c->flags & TRI_CACHE_JIT) && v.guard.h_lo == 0) {
     // Compile one specialization per launch of the plan (Sec. 3.5 growth),
     // or load it from the code directory.
     v.jit = 2;
@@ -245,7 +276,8 @@ tri_status install_key(tri_cache *c, const Key &k, int32_t candidate) {
   return TRI_OK;
 }
 
-void fill_selection(const Version &v, int32_t index, int64_t T, tri_selection *out) {
+void fill_selection(const Version &v, int32_t index, int64_t T, tri_selection *out,
+                    const Key *call_key) {
   const Key &k = v.key;
   const uint32_t dt = key_dtype(k);
   memset(out, 0, sizeof *out);
@@ -270,7 +302,7 @@ void fill_selection(const Version &v, int32_t index, int64_t T, tri_selection *o
                         role_block(kv)};
     }
   }
-  key_words(k, out->key);
+  key_words(call_key ? *call_key : k, out->key);
 }
 
 }  // namespace tri
@@ -283,7 +315,8 @@ tri_status tri_spec_cache_create(tri_cache **out, uint32_t capacity, uint32_t fl
   if (!out) return TRI_E_INVALID;
   *out = nullptr;
   if (capacity > kMaxCapacity ||
-      (flags & ~uint32_t(TRI_CACHE_AUTO_INSTALL | TRI_CACHE_JIT | TRI_CACHE_AUTOTUNE)))
+      (flags & ~uint32_t(TRI_CACHE_AUTO_INSTALL | TRI_CACHE_JIT | TRI_CACHE_AUTOTUNE |
+                         TRI_CACHE_GENERIC)))
     return TRI_E_INVALID;
   if (capacity == 0) capacity = kDefaultCapacity;
   int device = 0;
@@ -292,13 +325,18 @@ tri_status tri_spec_cache_create(tri_cache **out, uint32_t capacity, uint32_t fl
   tri_cache *c = static_cast<tri_cache *>(calloc(1, sizeof(tri_cache)));
   if (!c) return TRI_E_NOMEM;
   c->versions = static_cast<Version *>(calloc(capacity, sizeof(Version)));
-  if (!c->versions) {
+  c->memo = static_cast<MemoSlot *>(calloc(kMemoSlots, sizeof(MemoSlot)));
+  if (!c->versions || !c->memo) {
+    free(c->versions);
+    free(c->memo);
     free(c);
     return TRI_E_NOMEM;
   }
+  for (uint32_t i = 0; i < kMemoSlots; ++i) c->memo[i].version = -1;
   st = be_resolve(EMPTY, 0, 0, &c->empty_fn);
   if (st != 0) {
     free(c->versions);
+    free(c->memo);
     free(c);
     return tri_status(st);
   }
@@ -324,19 +362,17 @@ void tri_spec_cache_destroy(tri_cache *c) {
     release_modules(c->versions[i]);
   }
   free(c->versions);
+  free(c->memo);
   free(c);
 }
 
 tri_status tri_spec_install_last_miss(tri_cache *c, tri_selection *out) {
   if (!c || !c->has_miss) return TRI_E_INVALID;
-  const tri_status st = install_key(c, c->miss_key);
+  const tri_status st = install_key(c, c->miss_key, -1, (c->flags & TRI_CACHE_GENERIC) != 0);
   if (st != TRI_OK) return st;
   if (out) {
-    for (uint32_t i = 0; i < c->n_versions; ++i)
-      if (c->versions[i].key == c->miss_key) {
-        fill_selection(c->versions[i], int32_t(i), c->miss_T, out);
-        break;
-      }
+    const int32_t i = scan_versions(c, c->miss_key);
+    if (i >= 0) fill_selection(c->versions[i], i, c->miss_T, out, &c->miss_key);
   }
   return TRI_OK;
 }
@@ -370,6 +406,11 @@ tri_status tri_spec_version_info(const tri_cache *c, uint32_t index, tri_version
   out->tuned = v.tuned;
   out->tune_ms = v.tune_ms;
   out->rope_tokens = v.plan.rope_tokens;
+  out->b_lo = v.guard.b_lo;
+  out->b_hi = v.guard.b_hi;
+  out->h_lo = v.guard.h_lo;
+  out->h_hi = v.guard.h_hi;
+  out->h_mod = v.guard.h_mod;
   return TRI_OK;
 }
 

@@ -158,6 +158,36 @@ struct Plan {
 };
 Plan plan_for_key(const Key &k);
 
+inline bool operator==(const Plan &a, const Plan &b) {
+  if (a.variant != b.variant || a.n_launches != b.n_launches ||
+      a.rope_slices != b.rope_slices || a.rope_tokens != b.rope_tokens)
+    return false;
+  for (int i = 0; i < 3; ++i)
+    if (a.roles[i] != b.roles[i] || a.kvariant[i] != b.kvariant[i] || a.ksub[i] != b.ksub[i])
+      return false;
+  return true;
+}
+
+// ---- guards ----------------------------------------------------------------------------
+// What a version matches (Algorithm 1 scans versions in creation order and
+// takes the first whose guard holds). Exact (b_lo < 0): its key. Generic:
+// every key equal to its own except that the token bucket may lie in
+// [b_lo, b_hi] and, with h_lo > 0, H in [h_lo, h_hi] of divisibility class
+// h_mod (TRI_H_*).
+struct Guard {
+  int32_t b_lo, b_hi;
+  uint32_t h_lo, h_hi;
+  int32_t h_mod;
+};
+constexpr Guard kExact = {-1, -1, 0, 0, TRI_H_ANY};
+constexpr uint32_t kBucketMax = 22;
+// The guard of the generic version a miss on k installs: the widest run of
+// buckets around k's with plan_for_key's plan, and for norm rows served by
+// one bucket-independent kernel the row lengths it serves; exact when the
+// plan splits norm rows.
+Guard generic_guard(const Key &k);
+bool guard_holds(const Key &vk, const Guard &g, const Key &k);
+
 // Install-time tuning: the key's candidate plans, index 0 = plan_for_key.
 constexpr int kMaxCandidates = 24;
 int plan_candidates(const Key &k, Plan *out);   // returns the count (>= 1)
@@ -206,7 +236,8 @@ int be_noalloc_scratch(int device, void **ptr);
 
 // ---- versions and the cache ------------------------------------------------------------
 struct Version {
-  Key key;
+  Key key;                // the key the version was made for
+  Guard guard;
   Plan plan;
   void *fn[3];
   void *module[3];        // runtime-compiled code objects, or null
@@ -224,6 +255,15 @@ struct Version {
 
 constexpr int kOps = 12;   // op ids 1..11
 
+// Memo of first matches: a direct-mapped table of keys and the version
+// Algorithm 1's scan selected for them. First match depends only on the key
+// and versions are only ever appended, so an entry stays right for good.
+constexpr uint32_t kMemoSlots = 1024;
+struct MemoSlot {
+  Key key;
+  int32_t version;   // -1: empty
+};
+
 }  // namespace tri
 
 struct tri_cache {
@@ -232,7 +272,9 @@ struct tri_cache {
   int device;
   uint32_t n_versions;
   tri::Version *versions;
-  int32_t last_hit[tri::kOps];   // per op: version index of the last hit, -1 none
+  int32_t last_hit[tri::kOps];   // per op: version of the op's last lookup key, -1 none
+  tri::Key last_key[tri::kOps];  // per op: that key
+  tri::MemoSlot *memo;           // kMemoSlots entries, or null (no memo)
   bool has_miss;
   tri::Key miss_key;
   int64_t miss_T;
@@ -252,8 +294,15 @@ struct tri_graph {
 namespace tri {
 // Cache core (cache.cpp). install_key: candidate -1 = the cache's rule.
 int32_t find_version(tri_cache *c, uint32_t op, const Key &k);
-tri_status install_key(tri_cache *c, const Key &k, int32_t candidate = -1);
-void fill_selection(const Version &v, int32_t index, int64_t T, tri_selection *out);
+// Algorithm 1 without the memos: the first version whose guard holds.
+int32_t scan_versions(const tri_cache *c, const Key &k);
+// candidate -1 = the cache's rule; generic: a generic version (miss installs
+// under TRI_CACHE_GENERIC), else exact.
+tri_status install_key(tri_cache *c, const Key &k, int32_t candidate = -1, bool generic = false);
+// The selection record a call with T tokens and key *call_key (null: the
+// version's own key) makes on version v.
+void fill_selection(const Version &v, int32_t index, int64_t T, tri_selection *out,
+                    const Key *call_key = nullptr);
 // Runtime-compiled specializations (jit.cpp).
 bool key_valid(const Key &k);
 // Source of the specialization of launch `i` of a version (key k, plan p):

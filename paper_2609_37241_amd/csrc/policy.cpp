@@ -379,6 +379,91 @@ Plan plan_for_key(const Key &k) {
   return p;
 }
 
+// ---- generic guards ------------------------------------------------------------------
+namespace {
+
+Key with_bucket(const Key &k, uint32_t b) {
+  Key x = k;
+  x.k0 = (x.k0 & ~(uint64_t(0xFF) << 16)) | (uint64_t(b) << 16);
+  return x;
+}
+
+bool splits_rows(const Plan &p) {
+  for (int i = 0; i < p.n_launches; ++i)
+    if (p.kvariant[i] == RN_SPLIT) return true;
+  return p.roles[0] == RN_SPLIT;
+}
+
+// The row lengths served by the norm kernel rn_role picks for H at every
+// bucket: unaligned rows take the scalar kernel at any length, aligned
+// ragged ones at every length that is not a whole number of vectors; rows
+// of whole vectors one wavefront (1-64, 65-128 vectors) or one workgroup
+// (129-256, 257-512, ..., 2049-4096 vectors). Longer rows: none (their
+// kernel depends on the bucket through the split's scratch).
+bool norm_h_range(uint32_t dt, uint32_t H, unsigned fl, Guard *g) {
+  const int64_t v = vec_elems(dt);
+  if (!(fl & kAlign) || H % v) {
+    g->h_lo = 1;
+    g->h_hi = uint32_t(kHLimit - 1);
+    g->h_mod = (fl & kAlign) ? TRI_H_RAGGED : TRI_H_ANY;
+    return true;
+  }
+  const int64_t n = int64_t(H) / v;
+  int64_t lo, hi;
+  if (n <= 64) {
+    lo = 1, hi = 64;
+  } else if (n <= 128) {
+    lo = 65, hi = 128;
+  } else {
+    const int64_t nb = next_pow2(cdiv(n, 256));
+    if (nb > 16) return false;
+    lo = nb == 1 ? 129 : 128 * nb + 1;
+    hi = 256 * nb;
+  }
+  g->h_lo = uint32_t(lo * v);
+  g->h_hi = uint32_t(hi * v);
+  g->h_mod = TRI_H_MULTIPLE;
+  return true;
+}
+
+}  // namespace
+
+Guard generic_guard(const Key &k) {
+  const Plan P = plan_for_key(k);
+  if (splits_rows(P)) return kExact;
+  uint32_t lo = key_bucket(k), hi = lo;
+  while (lo > 0 && plan_for_key(with_bucket(k, lo - 1)) == P) --lo;
+  while (hi < kBucketMax && plan_for_key(with_bucket(k, hi + 1)) == P) ++hi;
+  Guard g = kExact;
+  g.b_lo = int32_t(lo);
+  g.b_hi = int32_t(hi);
+  const uint32_t op = key_op(k);
+  if (op == TRI_OP_RMSNORM || op == TRI_OP_RES_RMSNORM) {
+    Guard h = g;
+    if (norm_h_range(key_dtype(k), key_H(k), key_flags(k), &h)) g = h;
+  }
+  return g;
+}
+
+bool guard_holds(const Key &vk, const Guard &g, const Key &k) {
+  if (g.b_lo < 0) return vk == k;
+  const uint64_t bucket_bits = uint64_t(0xFF) << 16;
+  if ((vk.k0 & ~bucket_bits) != (k.k0 & ~bucket_bits)) return false;
+  const int32_t b = int32_t(key_bucket(k));
+  if (b < g.b_lo || b > g.b_hi) return false;
+  if (g.h_lo) {   // word 1: H in the low half, I in the high half
+    if ((vk.k1 >> 32) != (k.k1 >> 32)) return false;
+    const uint32_t H = key_H(k);
+    if (H < g.h_lo || H > g.h_hi) return false;
+    const uint32_t v = key_dtype(vk) == TRI_F32 ? 4u : 8u;
+    if ((g.h_mod == TRI_H_MULTIPLE && H % v) || (g.h_mod == TRI_H_RAGGED && H % v == 0))
+      return false;
+  } else if (vk.k1 != k.k1) {
+    return false;
+  }
+  return vk.k2 == k.k2 && vk.k3 == k.k3 && vk.k4 == k.k4 && vk.k5 == k.k5;
+}
+
 // ---- candidate plans of install-time tuning ---------------------------------------
 // Index 0 is the policy's plan. The others are the kernel variants whose
 // requirements the key also meets: a norm row held by one wavefront can be

@@ -884,19 +884,26 @@ def test_prefill_chain_full_size_all_rows(tri, cache, cfg, grid):
 
 
 # ---- mixed-shape stream -----------------------------------------------------------------------
-def test_mixed_stream_selection_and_outputs(tri, cache):
-    """All 10,000 calls of the mixed stream on real buffers: every selection
-    record against the oracle's model, outputs against the oracle every 50th
-    call (and on every miss)."""
+def _mixed_stream_on_gpu(tri, cache, model, exact_before=(), exact_at=None, check_every=50):
+    """The 10,000-call mixed stream on real buffers: every selection record
+    against the model's, outputs against the oracle every `check_every`-th
+    call and on every miss. `exact_before` keys are installed exactly before
+    the stream, `exact_at` = (call index, keys) installs more midway."""
     Tmax = max(wl.MIXED_T_CHOICES)
     H, I, nq, nk, hd = wl.MIXED_H, wl.MIXED_I, wl.MIXED_NQ, wl.MIXED_NK, wl.MIXED_HD
     bufs = {}
-    model = S.SpecCacheModel()
+    for k in exact_before:
+        cache.install_key(k)
+        assert model.install_key(k) == S.OK
     stream = wl.mixed_stream()
     assert len(stream) == wl.MIXED_CALLS
     for n, (T, dt, layout) in enumerate(stream):
         if n % 1000 == 0:
             print(f"mixed stream: call {n}", flush=True)
+        if exact_at is not None and n == exact_at[0]:
+            for k in exact_at[1]:
+                cache.install_key(k)
+                assert model.install_key(k) == S.OK
         key = (dt, layout)
         if key not in bufs:
             r = rng(len(bufs) + 1)
@@ -915,7 +922,7 @@ def test_mixed_stream_selection_and_outputs(tri, cache):
         d["w"] = dd["w"]
         call = model_chain_call(d, 1e-6, wl.MIXED_BASE)
         missed = model.call(call) == S.MISS
-        check_out = missed or n % 50 == 0
+        check_out = missed or n % check_every == 0
         if check_out:
             q0, k0 = host(d["q"]), host(d["k"])
         cache.decode_chain(d["x"], d["residual"], d["w"], d["q"], d["k"], d["pos"], d["gate"],
@@ -936,6 +943,50 @@ def test_mixed_stream_selection_and_outputs(tri, cache):
     torch.cuda.synchronize()
     s = cache.stats()
     assert s["misses"] == model.stats.misses and s["n_versions"] == len(model.versions)
+
+
+def test_mixed_stream_selection_and_outputs(tri, cache):
+    """All 10,000 calls of the mixed stream on real buffers: every selection
+    record against the oracle's model, outputs against the oracle every 50th
+    call (and on every miss)."""
+    _mixed_stream_on_gpu(tri, cache, S.SpecCacheModel())
+
+
+def test_mixed_stream_with_overlapping_generic_versions(tri):
+    """The same stream on a cache that installs generic versions on a miss,
+    with exact versions installed first for every third distinct key of the
+    first 200 calls and, after 5,000 calls, for every other distinct key of
+    the stream: versions overlap and the first in creation order runs.
+    Records bit for bit against the model on every call; outputs against the
+    oracle every 50th call and on every miss."""
+    def mk(T, dt, layout):
+        d = S.DT_BF16 if dt == wl.BF16 else S.DT_F32
+        es = 2 if d == S.DT_BF16 else 4
+        off = es if layout == wl.LAYOUT_UNALIGNED else 0
+        pad = wl.MIXED_PAD if layout == wl.LAYOUT_STRIDED else 0
+        from tests.selection_calls import chain_call
+        return S.make_key(chain_call(d, T, wl.MIXED_H, wl.MIXED_I, wl.MIXED_NQ, wl.MIXED_NK,
+                                     wl.MIXED_HD, res_off=off, rope_off=off, sw_off=off,
+                                     res_pad=pad, rope_pad=pad, sw_pad=pad))
+    stream = wl.mixed_stream()
+    first, every = [], []
+    for i, (T, dt, layout) in enumerate(stream):
+        k = mk(T, dt, layout)
+        if i < 200 and k not in first:
+            first.append(k)
+        if k not in every:
+            every.append(k)
+    flags = S.FLAG_GENERIC
+    cache = tri.SpecCache(generic=True)
+    try:
+        _mixed_stream_on_gpu(tri, cache, S.SpecCacheModel(flags=flags), exact_before=first[::3],
+                             exact_at=(5000, every[::2]))
+        guards = [(cache.version_info(i).b_lo, cache.version_info(i).b_hi)
+                  for i in range(cache.stats()["n_versions"])]
+        assert any(b >= 0 for b, _ in guards) and any(b < 0 for b, _ in guards)
+    finally:
+        torch.cuda.synchronize()
+        cache.close()
 
 
 # ---- HIP graph capture of the hit path ------------------------------------------------------

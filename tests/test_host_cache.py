@@ -402,7 +402,7 @@ def test_install_needs_a_miss_and_is_idempotent(lib, fresh):
 def test_create_errors(lib):
     h = C.c_void_p()
     assert lib.tri_spec_cache_create(C.byref(h), 4097, 0) == S.E_INVALID
-    assert lib.tri_spec_cache_create(C.byref(h), 0, 8) == S.E_INVALID
+    assert lib.tri_spec_cache_create(C.byref(h), 0, 16) == S.E_INVALID
     assert lib.tri_spec_cache_create(C.byref(h), 0, 3) == S.OK      # auto-install + JIT
     lib.tri_spec_cache_destroy(h)
     assert lib.tri_spec_cache_create(None, 0, 0) == S.E_INVALID

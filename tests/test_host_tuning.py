@@ -399,7 +399,8 @@ def test_jit_compiles_only_the_kept_plan(lib, fresh):
 
 
 def test_create_accepts_the_tuning_flag(lib):
-    for flags, ok in ((4, True), (7, True), (8, False), (12, False)):
+    # 8 is the generic-version flag; 16 and above are not flags
+    for flags, ok in ((4, True), (7, True), (15, True), (16, False), (20, False)):
         h = C.c_void_p()
         st = lib.tri_spec_cache_create(C.byref(h), 0, flags)
         assert (st == 0) == ok, flags
