@@ -244,6 +244,26 @@ CPU_THREAD_VARS = ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS",
                    "BLIS_NUM_THREADS", "NUMEXPR_NUM_THREADS", "VECLIB_MAXIMUM_THREADS")
 
 
+def host_cost():
+    """The library's own host work per decode-chain hit, step by step (the
+    native microbenchmark over a launch backend that does nothing), and
+    Algorithm 1's scan to the last of n versions without the memos."""
+    lib = C.CDLL(os.path.join(ROOT, "paper_2609_37241_amd", "libtri_hostcost.so"))
+    lib.trib_hostcost.argtypes = [C.POINTER(C.c_int32), C.c_int32, C.POINTER(C.c_double)]
+    ns = (1, 52, 256, 4096)
+    arr = (C.c_int32 * len(ns))(*ns)
+    out = (C.c_double * (6 + len(ns)))()
+    if lib.trib_hostcost(arr, len(ns), out) != 0:
+        return None
+    names = ("validation", "key_packing", "lookup_last_key", "lookup_key_memo",
+             "argument_fill_and_launch_call", "whole_entry")
+    res = {n: out[i] for i, n in enumerate(names)}
+    res["scan_to_last_of_n_versions"] = {str(n): out[6 + i] for i, n in enumerate(ns)}
+    res["note"] = ("1-token Llama-7B chain; the launch call returns at once, so whole_entry "
+                   "is the library's part of chain_host_us, the rest is the HIP launch")
+    return res
+
+
 def cpu_model() -> str:
     """The host CPU's model name from /proc/cpuinfo (platform.processor() is
     empty on Linux)."""
@@ -411,6 +431,7 @@ def main():
                       "grid": sel.launch[0].grid_x, "roles": list(sel.roles)},
         "cache_stats": stats,
     }
+    latency["host_cost_ns"] = host_cost()
     if args.latency_only:
         emit(args, ce, wall, latency, None, None, None)
         return

@@ -70,3 +70,21 @@ def test_bench_refuses_more_than_one_gpu():
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2
     assert "one GPU" in r.stderr and not r.stdout.strip()
+
+
+def test_host_cost_microbenchmark_runs():
+    """The host-cost microbenchmark (library over a launch that does nothing)
+    returns positive figures, and Algorithm 1's scan to the last of 4096
+    versions costs clearly more than a scan of one version and than a
+    lookup through the key memo."""
+    import ctypes as C
+    path = os.path.join(ROOT, "paper_2609_37241_amd", "libtri_hostcost.so")
+    if not os.path.exists(path):
+        import __graft_entry__
+        __graft_entry__.build()
+    lib = C.CDLL(path)
+    ns = (C.c_int32 * 2)(1, 4096)
+    out = (C.c_double * 8)()
+    assert lib.trib_hostcost(ns, 2, out) == 0
+    assert all(out[i] > 0 for i in (1, 2, 3, 4, 5, 6, 7))     # out[0] is a difference
+    assert out[7] > 10 * out[6] and out[7] > 10 * out[3]
