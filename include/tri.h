@@ -295,6 +295,10 @@ typedef struct tri_chain_args {
  * never run). With TRI_CACHE_JIT, a version with a hidden-size range runs
  * the precompiled kernels (a compiled specialization fixes H). */
 tri_status tri_spec_cache_create(tri_cache **out, uint32_t capacity, uint32_t flags);
+/* Release a cache and everything it owns (versions, kernel handles, loaded
+ * code objects, device constants and scratch). Not in the paper (its module
+ * lives as long as the Python callable); NULL is ignored. Graphs built from
+ * the cache must be destroyed first. */
 void tri_spec_cache_destroy(tri_cache *cache);
 
 /* ---- ops (the hit path) ------------------------------------------------------ */
@@ -430,7 +434,11 @@ tri_status tri_residual_rmsnorm_noalloc(tri_cache *cache, tri_dtype dtype,
 /* The decode chain: residual+RMSNorm, RoPE-QK (or QK-RMSNorm + RoPE when
  * q_norm_w is set; with the variant of rope_ext when set) and SwiGLU of one
  * decode step, on disjoint operands
- * (overlap between the three ops is undefined). When
+ * (overlap between the three ops is undefined). Not an operation of the
+ * paper, which keeps one launch per kernel (its Sec. 5 contrasts the SCM
+ * with mega-kernels); it is this path's one native entry (Sec. 3.1) for the
+ * three short ops of a decode step, with the guards of all three in one key
+ * (validation order: norm, RoPE, QK norm, SwiGLU). When
  * every tensor is 16-byte aligned and contiguous this is ONE launch of a
  * fused kernel whose workgroups take the three roles by blockIdx range;
  * otherwise three launches. If a later launch of the three fails, earlier
@@ -490,19 +498,27 @@ void tri_graph_destroy(tri_graph *graph);
  * NOMEM, RUNTIME. */
 tri_status tri_spec_install_last_miss(tri_cache *cache, tri_selection *out);
 
-/* Copy the selection record of the last entry call. */
+/* Copy the selection record of the last entry call (which version of
+ * Algorithm 1's ordered list ran, its kernels and launch geometry, the
+ * packed key). Not in the paper: introspection for parity with the
+ * selection model and for reporting. INVALID for NULL arguments. */
 tri_status tri_spec_last_selection(const tri_cache *cache, tri_selection *out);
 
-/* Copy the counters. */
+/* Copy the counters (calls, hits, misses, errors, T == 0 no-ops, installs):
+ * the hit rate of Sec. 3.5's three paths. Not in the paper as an interface.
+ * INVALID for NULL arguments. */
 tri_status tri_spec_stats(const tri_cache *cache, tri_stats *out);
 
-/* Describe version `index` (creation order). INVALID if out of range. */
+/* Describe version `index` (creation order; the versions of Algorithm 1).
+ * Not in the paper: introspection. INVALID if out of range. */
 tri_status tri_spec_version_info(const tri_cache *cache, uint32_t index,
                                  tri_version_info *out);
 
 /* Copy version `index`'s host copy of its constants (RoPE inverse
  * frequencies, rotary_dim/2 floats; none for other ops or with a cos/sin
- * cache) into out[0..cap); *n gets the count. */
+ * cache) into out[0..cap); *n gets the count. The paper's captured
+ * constants (Sec. 3.3) made visible for parity tests; not an interface of
+ * the paper. INVALID if out of range or out is NULL while *n > 0. */
 tri_status tri_spec_version_constants(const tri_cache *cache, uint32_t index,
                                       float *out, uint32_t cap, uint32_t *n);
 
@@ -546,10 +562,13 @@ tri_status tri_spec_import_keys(tri_cache *cache, const uint64_t *keys, uint32_t
 tri_status tri_spec_install_key(tri_cache *cache, const uint64_t *key, int32_t candidate);
 
 /* Launch the empty kernel (1 workgroup of 64 work-items, no arguments)
- * through the same launch path: the yardstick for per-call cost. */
+ * through the same launch path: the yardstick for per-call cost. Not in the
+ * paper (its measurements compare against eager and torch.compile, Sec. 4);
+ * the target of this path is a per-call cost close to this launch's. */
 tri_status tri_launch_empty(tri_cache *cache, void *stream);
 
-/* Static name of a status value. */
+/* Static name of a status value ("TRI_UNKNOWN" for other values). Not in
+ * the paper. */
 const char *tri_status_str(int status);
 
 #ifdef __cplusplus
