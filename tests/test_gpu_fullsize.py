@@ -168,3 +168,44 @@ def test_embedding_8192(tri, data):
     for sl in chunks():
         want = O.embedding(table, host(data["ids"][sl]), nm.BF16)
         check(f"embedding {sl}", host(out[sl]), want, nm.BF16, exact=True)
+
+
+# ---- long rows: the benchmark's bf16 [2048, 65536] and the same memory as
+# [1024, 131072], each row split over 4 / 8 workgroups ------------------------------------------
+@pytest.fixture(scope="module")
+def long_rows():
+    g = torch.Generator(device=DEV)
+    g.manual_seed(12)
+    d = dict(x=torch.randn((2048, 65536), generator=g, device=DEV).to(torch.bfloat16),
+             r=torch.randn((2048, 65536), generator=g, device=DEV).to(torch.bfloat16),
+             w=(torch.rand(65536, generator=g, device=DEV) + 0.5).to(torch.bfloat16),
+             w2=(torch.rand(131072, generator=g, device=DEV) + 0.5).to(torch.bfloat16))
+    yield d
+    del d
+    torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("H,res", [(65536, False), (65536, True), (131072, False),
+                                   (131072, True)],
+                         ids=["rmsnorm65536", "residual65536", "rmsnorm131072",
+                              "residual131072"])
+def test_long_rows_all_rows(tri, long_rows, H, res):
+    T = 2048 * 65536 // H
+    S_ = H // 8 // 2048                                  # slices of 2048 vectors
+    print(f"full size: long rows T={T} H={H} residual={res}", flush=True)
+    x, r = long_rows["x"].view(T, H), long_rows["r"].view(T, H)
+    w = long_rows["w"] if H == 65536 else long_rows["w2"]
+    if res:
+        (y, ro), sel = run(tri, lambda c: c.residual_rmsnorm(x, r, w, CFG.eps))
+    else:
+        y, sel = run(tri, lambda c: c.rmsnorm(x, w, CFG.eps))
+    assert sel.variant == S.RN_SPLIT and sel.launch[0].grid_x == T * S_
+    wh = host(w)
+    for a in range(0, T, 256):                           # 256 rows: 16-32 M elements
+        b = slice(a, min(T, a + 256))
+        if res:
+            wy, wr = O.residual_rmsnorm(host(x[b]), host(r[b]), wh, CFG.eps, nm.BF16)
+            check(f"res_out {b}", host(ro[b]), wr, nm.BF16, exact=True)
+        else:
+            wy = O.rmsnorm(host(x[b]), wh, CFG.eps, nm.BF16)
+        check(f"y {b}", host(y[b]), wy, nm.BF16)
