@@ -45,6 +45,15 @@
  *   status and leaves the cache unchanged except its counters.
  * - One thread per cache. A cache is bound to the device current when it is
  *   created.
+ * - RMSNorm rows of more than 4096 16-byte vectors may be split over several
+ *   workgroups of one launch that exchange partial sums through scratch the
+ *   version owns (allocated zeroed at install, left zeroed by every launch).
+ *   Launches of one such version must not overlap in time: issue its calls
+ *   on one stream (or order the streams), or use one cache per stream.
+ *   The exchange waits a bounded time; a row whose partial sums do not all
+ *   arrive is written as NaN and marks the scratch failed, after which
+ *   every launch on it writes NaN rows (destroy the cache to recover). A
+ *   failure is loud, never a silently wrong value.
  */
 #ifndef TRI_H
 #define TRI_H
