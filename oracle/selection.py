@@ -1074,12 +1074,16 @@ def _norm_h_range(dt: int, H: int, fl: int):
     return None
 
 
-def generic_guard(key) -> Guard:
-    """The guard of the generic version a miss on `key` installs (exact when
-    the plan splits norm rows)."""
+def generic_guard(key, plan=None) -> Guard:
+    """The guard of the generic version a miss on `key` installs, running
+    `plan` (default: the policy's plan): the widest run of token buckets
+    around the key's over which the policy keeps its plan and, for norm rows
+    held by one wavefront or workgroup, the row lengths that kernel serves.
+    A version whose plan splits norm rows keeps only the buckets whose
+    scratch fits: its scratch is sized for the top of the run, at most
+    SPLIT_SCRATCH_WORDS (when the policy itself splits, the run already ends
+    there; a tuned split choice clamps it)."""
     P = candidates(key)[0]
-    if RN_SPLIT in P.kernels or RN_SPLIT in P.roles:
-        return Guard(tuple(key))
     f = unpack_key(key)
     b = f["bucket"]
     lo = b
@@ -1088,6 +1092,10 @@ def generic_guard(key) -> Guard:
     hi = b
     while hi < BUCKET_MAX and candidates(_with_bucket(key, hi + 1))[0] == P:
         hi += 1
+    run = plan if plan is not None else P
+    if RN_SPLIT in run.kernels or RN_SPLIT in run.roles:
+        while hi > b and not split_fits(f["dtype"], f["H"], hi):
+            hi -= 1
     h = None
     if f["op"] in (OP_RMSNORM, OP_RES_RMSNORM):
         h = _norm_h_range(f["dtype"], f["H"], f["flags"])
@@ -1292,7 +1300,7 @@ class SpecCacheModel:
                 choice = tune_choice([self.timer(key, j, c) for j, c in enumerate(cands)])
                 tuned = TUNE_MEASURED
         self.versions.append(key)
-        self.guards.append(generic_guard(key) if generic else Guard(tuple(key)))
+        self.guards.append(generic_guard(key, cands[choice]) if generic else Guard(tuple(key)))
         self.choice.append(choice)
         self.tuned.append(tuned)
         self.version_hits.append(0)
