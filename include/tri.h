@@ -19,8 +19,11 @@
  * Q and K head counts, token-count bucket ceil(log2 T), 16-byte alignment of
  * every activation / weight pointer and row stride, contiguity of every row
  * stride, the RoPE base and the RoPE variant (rotary dim, pairing, position
- * width, angle source, frequency scaling and its parameters). They are
- * equality tests on a packed key, so at most one version matches.
+ * width, angle source, frequency scaling and its parameters), packed into
+ * one key. An exact version tests equality on the key, so at most one exact
+ * version matches; a generic version (TRI_CACHE_GENERIC) holds over a range
+ * of token buckets (and of row lengths), so versions may overlap and the
+ * first in creation order runs.
  *
  * Conventions (all entry points)
  * ------------------------------
@@ -296,8 +299,10 @@ typedef struct tri_chain_args {
  * RMSNorm rows held by one wavefront or one workgroup, or by the scalar
  * kernel -- any hidden size that kernel serves (rows of 1-64, 65-128,
  * 129-256, ..., 2049-4096 16-byte vectors, every length of the scalar
- * kernel's class). Plans that split norm rows over workgroups get exact
- * versions. tri_spec_install_key and tri_spec_import_keys always create
+ * kernel's class). A version whose plan (the policy's or a tuned one)
+ * splits norm rows over workgroups keeps only the buckets of that run whose
+ * split scratch fits (at most 32 MiB, allocated for the top bucket at
+ * install), and matches its exact hidden size. tri_spec_install_key and tri_spec_import_keys always create
  * exact versions, so exact versions installed first take precedence over
  * later generic ones that overlap them, and a key that an installed
  * version already matches installs nothing (a version behind it could

@@ -153,11 +153,6 @@ void drop_version(Version &v) {
   v.d_scratch = nullptr;
 }
 
-bool plan_splits(const Plan &p) {
-  for (int i = 0; i < p.n_launches; ++i)
-    if (p.kvariant[i] == RN_SPLIT) return true;
-  return false;
-}
 
 }  // namespace
 
@@ -173,7 +168,7 @@ tri_status install_key(tri_cache *c, const Key &k, int32_t candidate, bool gener
   Version v;
   memset(&v, 0, sizeof v);
   v.key = k;
-  v.guard = generic ? generic_guard(k) : kExact;
+  v.guard = kExact;   // the generic guard follows the plan's choice below
   v.n_candidates = nc;
   v.candidate = candidate < 0 ? 0 : candidate;
   const uint32_t dt = key_dtype(k);
@@ -194,15 +189,20 @@ tri_status install_key(tri_cache *c, const Key &k, int32_t candidate, bool gener
   }
 
   // Split norm rows exchange partial sums through a scratch of the version,
-  // zeroed here and left zero by every call, sized for the top of the token
-  // bucket: allocated when the plan splits, or before tuning when any
-  // candidate does (the tuning calls share it, one after another on one
-  // stream), and kept only if the chosen plan splits.
+  // zeroed here and left zero by every call, sized for the top token bucket
+  // the version serves (the key's; for a generic version the top of its run
+  // as a split version, whose guard keeps only buckets where this fits):
+  // allocated when the plan splits, or before tuning when any candidate does
+  // (the tuning calls share it, one after another on one stream), and kept
+  // only if the chosen plan splits.
   const bool tuning = candidate < 0 && (c->flags & TRI_CACHE_AUTOTUNE) && nc > 1;
-  bool need_scratch = plan_splits(cands[v.candidate]);
-  for (int i = 0; tuning && i < nc; ++i) need_scratch = need_scratch || plan_splits(cands[i]);
-  if (need_scratch) {
-    v.scratch_words = split_words(int64_t(1) << key_bucket(k), split_slices(dt, key_H(k)));
+  int split_cand = splits_rows(cands[v.candidate]) ? v.candidate : -1;
+  for (int i = 0; tuning && split_cand < 0 && i < nc; ++i)
+    if (splits_rows(cands[i])) split_cand = i;
+  if (split_cand >= 0) {
+    const uint32_t top =
+        generic ? uint32_t(generic_guard(k, cands[split_cand]).b_hi) : key_bucket(k);
+    v.scratch_words = split_words(int64_t(1) << top, split_slices(dt, key_H(k)));
     void *dev = nullptr;
     const int st = be_alloc_zeroed(v.scratch_words * 8, &dev);
     if (st != 0) {
@@ -231,7 +231,8 @@ tri_status install_key(tri_cache *c, const Key &k, int32_t candidate, bool gener
                           std::chrono::steady_clock::now() - t0).count());
   }
   v.plan = cands[v.candidate];
-  if (v.d_scratch && !plan_splits(v.plan)) {
+  v.guard = generic ? generic_guard(k, v.plan) : kExact;
+  if (v.d_scratch && !splits_rows(v.plan)) {
     be_free(v.d_scratch);
     v.d_scratch = nullptr;
     v.scratch_words = 0;

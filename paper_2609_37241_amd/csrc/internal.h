@@ -101,6 +101,9 @@ Role rn_role(uint32_t dtype, int64_t H, unsigned flags, int64_t T, uint32_t buck
 // Workgroups per row of RN_SPLIT, and the scratch words a call of T rows
 // of that split needs.
 int32_t split_slices(uint32_t dtype, int64_t H);
+// Whether rows of H split at most kSplitMaxSlices ways with a scratch for
+// the top of `bucket` of at most kSplitScratchWords.
+bool split_fits(uint32_t dtype, int64_t H, uint32_t bucket);
 inline uint64_t split_words(int64_t T, int32_t S) {
   return uint64_t(kSplitHeaderWords) + uint64_t(T) * uint64_t(S + 1);
 }
@@ -181,11 +184,13 @@ struct Guard {
 };
 constexpr Guard kExact = {-1, -1, 0, 0, TRI_H_ANY};
 constexpr uint32_t kBucketMax = 22;
-// The guard of the generic version a miss on k installs: the widest run of
-// buckets around k's with plan_for_key's plan, and for norm rows served by
-// one bucket-independent kernel the row lengths it serves; exact when the
-// plan splits norm rows.
-Guard generic_guard(const Key &k);
+// The guard of the generic version a miss on k installs, running `chosen`:
+// the widest run of buckets around k's with plan_for_key's plan, and for
+// norm rows served by one bucket-independent kernel the row lengths it
+// serves. When `chosen` splits norm rows the run keeps only the buckets
+// whose split scratch fits (the version's scratch is sized for its top).
+Guard generic_guard(const Key &k, const Plan &chosen);
+bool splits_rows(const Plan &p);
 bool guard_holds(const Key &vk, const Guard &g, const Key &k);
 
 // Install-time tuning: the key's candidate plans, index 0 = plan_for_key.

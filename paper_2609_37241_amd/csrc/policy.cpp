@@ -47,6 +47,11 @@ int32_t split_slices(uint32_t dtype, int64_t H) {
   return int32_t(cdiv(H / vec_elems(dtype), kSplitSpan));
 }
 
+bool split_fits(uint32_t dtype, int64_t H, uint32_t bucket) {
+  const int32_t S = split_slices(dtype, H);
+  return S <= kSplitMaxSlices && split_words(int64_t(1) << bucket, S) <= kSplitScratchWords;
+}
+
 // Rows of up to 128 16-byte vectors (2 KiB) take one wavefront each, four
 // rows per workgroup, with no barrier. Longer rows take one 256-work-item
 // workgroup per row, up to 16 vectors per work-item: the four wavefronts
@@ -72,9 +77,7 @@ Role rn_role(uint32_t dtype, int64_t H, unsigned flags, int64_t T, uint32_t buck
   if (nvec <= 128) return {nvec <= 64 ? RN_WAVE_1 : RN_WAVE_2, uint32_t(cdiv(T, 4))};
   const int64_t nb = next_pow2(cdiv(nvec, 256));
   if (nb <= 16) return {RN_BLOCK_1 + pow2_index(nb), uint32_t(T)};
-  const int32_t S = split_slices(dtype, H);
-  if (S <= kSplitMaxSlices && split_words(int64_t(1) << bucket, S) <= kSplitScratchWords)
-    return {RN_SPLIT, uint32_t(T * S)};
+  if (split_fits(dtype, H, bucket)) return {RN_SPLIT, uint32_t(T * split_slices(dtype, H))};
   if (nvec <= kWideRowVecs) return {RN_WIDE, uint32_t(T)};
   return {RN_LOOP, uint32_t(T)};
 }
@@ -388,12 +391,6 @@ Key with_bucket(const Key &k, uint32_t b) {
   return x;
 }
 
-bool splits_rows(const Plan &p) {
-  for (int i = 0; i < p.n_launches; ++i)
-    if (p.kvariant[i] == RN_SPLIT) return true;
-  return p.roles[0] == RN_SPLIT;
-}
-
 // The row lengths served by the norm kernel rn_role picks for H at every
 // bucket: unaligned rows take the scalar kernel at any length, aligned
 // ragged ones at every length that is not a whole number of vectors; rows
@@ -428,12 +425,23 @@ bool norm_h_range(uint32_t dt, uint32_t H, unsigned fl, Guard *g) {
 
 }  // namespace
 
-Guard generic_guard(const Key &k) {
+bool splits_rows(const Plan &p) {
+  for (int i = 0; i < p.n_launches; ++i)
+    if (p.kvariant[i] == RN_SPLIT) return true;
+  return p.roles[0] == RN_SPLIT;
+}
+
+Guard generic_guard(const Key &k, const Plan &chosen) {
   const Plan P = plan_for_key(k);
-  if (splits_rows(P)) return kExact;
-  uint32_t lo = key_bucket(k), hi = lo;
+  const uint32_t b = key_bucket(k);
+  uint32_t lo = b, hi = b;
   while (lo > 0 && plan_for_key(with_bucket(k, lo - 1)) == P) --lo;
   while (hi < kBucketMax && plan_for_key(with_bucket(k, hi + 1)) == P) ++hi;
+  // A split version's scratch is sized for the top of its run: keep only
+  // the buckets whose scratch fits (the policy's own split stops there
+  // already; a tuned split choice is clamped here).
+  if (splits_rows(chosen))
+    while (hi > b && !split_fits(key_dtype(k), key_H(k), hi)) --hi;
   Guard g = kExact;
   g.b_lo = int32_t(lo);
   g.b_hi = int32_t(hi);

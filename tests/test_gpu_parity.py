@@ -226,6 +226,41 @@ def test_split_rows_reuse_their_scratch(tri, cache):
     assert S.RN_SPLIT in kinds
 
 
+def test_generic_split_version_across_buckets(tri):
+    """One generic split version (bf16 rows of 65536, 4 workgroups per row)
+    serves calls of 1 to 700 rows, buckets 0 to 10, through one scratch
+    sized for the top of its run; every row of every call against the
+    oracle, the plain and the residual form."""
+    r = rng(19)
+    H = 65536
+    w = wl.host_weight(r, H, nm.BF16)
+    wd = wl.to_torch(w, nm.BF16, DEV)
+    c = tri.SpecCache(auto_install=True, generic=True)
+    try:
+        for step, T in enumerate((3, 700, 1, 64, 129, 2)):
+            print(f"generic split: call {step}, {T} rows", flush=True)
+            x = wl.host_array(r, (T, H), nm.BF16)
+            res = wl.host_array(r, (T, H), nm.BF16)
+            xd, rd = wl.to_torch(x, nm.BF16, DEV), wl.to_torch(res, nm.BF16, DEV)
+            y = c.rmsnorm(xd, wd, 1e-6)
+            sel = c.last_selection()
+            y2, ro = c.residual_rmsnorm(xd, rd, wd, 1e-6)
+            torch.cuda.synchronize()
+            assert sel.variant == S.RN_SPLIT and sel.launch[0].grid_x == 4 * T
+            check(f"{step} y", host(y), O.rmsnorm(x, w, 1e-6, nm.BF16), nm.BF16)
+            wy, wh = O.residual_rmsnorm(x, res, w, 1e-6, nm.BF16)
+            check(f"{step} residual y", host(y2), wy, nm.BF16)
+            check(f"{step} res_out", host(ro), wh, nm.BF16, exact=True)
+        st = c.stats()
+        assert st["n_versions"] == 2 and st["misses"] == 2      # the plain and the residual op
+        for i in range(2):
+            v = c.version_info(i)
+            assert (v.b_lo, v.b_hi, v.h_lo) == (0, 19, 0)
+    finally:
+        torch.cuda.synchronize()
+        c.close()
+
+
 def test_rmsnorm_in_place(tri, cache):
     r = rng(3)
     x = wl.host_array(r, (6, 4096), nm.BF16)
