@@ -27,6 +27,18 @@ def lib():
     return load_fake()
 
 
+def _guards(lib, h):
+    from paper_2609_37241_amd._lib import Stats, VersionInfo
+    st_ = Stats()
+    lib.tri_spec_stats(h, C.byref(st_))
+    out = []
+    for i in range(st_.n_versions):
+        v = VersionInfo()
+        assert lib.tri_spec_version_info(h, i, C.byref(v)) == 0
+        out.append((v.b_lo, v.b_hi, v.h_lo, v.h_hi, v.h_mod))
+    return out
+
+
 def _check(lib, calls, flags=0):
     lib.trifake_reset()
     h = C.c_void_p()
@@ -35,6 +47,7 @@ def _check(lib, calls, flags=0):
         m = S.SpecCacheModel(capacity=S.MAX_CAPACITY, flags=flags)
         for c in calls:
             run_both(lib, h, m, c)
+        assert _guards(lib, h) == [(g.b_lo, g.b_hi, g.h_lo, g.h_hi, g.h_mod) for g in m.guards]
     finally:
         lib.tri_spec_cache_destroy(h)
 
@@ -146,3 +159,26 @@ def test_random_short_op_calls(lib, calls):
 @given(st.lists(chain_calls(), min_size=1, max_size=4), st.sampled_from([0, 1]))
 def test_random_chain_calls(lib, calls, auto):
     _check(lib, calls, flags=S.FLAG_AUTO_INSTALL if auto else 0)
+
+
+# Generic (range-guarded) versions: longer call lists, so that later calls
+# land in the runs and row-length ranges of earlier versions.
+GENERIC = S.FLAG_GENERIC | S.FLAG_AUTO_INSTALL
+
+
+@SETTINGS
+@given(st.lists(norm_calls(), min_size=2, max_size=12))
+def test_random_norm_calls_generic(lib, calls):
+    _check(lib, calls, flags=GENERIC)
+
+
+@SETTINGS
+@given(st.lists(chain_calls(), min_size=2, max_size=8))
+def test_random_chain_calls_generic(lib, calls):
+    _check(lib, calls, flags=GENERIC)
+
+
+@SETTINGS
+@given(st.lists(st.one_of(rope_calls(), short_calls()), min_size=2, max_size=10))
+def test_random_rope_and_short_calls_generic(lib, calls):
+    _check(lib, calls, flags=GENERIC)
