@@ -243,3 +243,51 @@ def test_code_directory_loads_compiled_kernels(tri, tmp_path):
     assert len(list(tmp_path.iterdir())) == 1
     for a, b in zip(*outs):
         check("loaded == compiled", a, b, cfg.dtype, exact=True)
+
+
+def test_jit_generic_versions(tri):
+    """A compiling cache that installs generic versions: one compiled chain
+    specialization serves the Llama-7B chain at 1-64 tokens (its run of
+    buckets: the key's shape fields are compiled in, the tokens stay a
+    run-time argument), and a norm version with a row-length range runs
+    the precompiled kernel (a compiled one would fix H); every output
+    against the oracle."""
+    r = rng(23)
+    dt, H, I, nq, nk, hd, base, eps = nm.BF16, 4096, 11008, 32, 32, 128, 1e4, 1e-6
+    w = wl.host_weight(r, H, dt)
+    wd = wl.to_torch(w, dt, DEV)
+    c = tri.SpecCache(auto_install=True, jit=True, generic=True)
+    try:
+        for T in (3, 1, 50, 64):
+            print(f"jit generic chain: T={T}", flush=True)
+            h = dict(x=wl.host_array(r, (T, H), dt), residual=wl.host_array(r, (T, H), dt),
+                     q=wl.host_array(r, (T, nq, hd), dt), k=wl.host_array(r, (T, nk, hd), dt),
+                     gate=wl.host_array(r, (T, I), dt), up=wl.host_array(r, (T, I), dt))
+            pos = r.integers(0, 4096, T).astype(np.int32)
+            d = {k: wl.to_torch(v, dt, DEV) for k, v in h.items()}
+            y, ro, out = c.decode_chain(d["x"], d["residual"], wd, d["q"], d["k"],
+                                        torch.from_numpy(pos).to(DEV), d["gate"], d["up"],
+                                        eps, base)
+            torch.cuda.synchronize()
+            want = O.decode_chain(dict(h, w=w, pos=pos), eps, base, dt)
+            for n, g in (("y", y), ("out", out), ("q", d["q"]), ("k", d["k"])):
+                check(f"T={T} {n}", host(g), want[n], dt)
+            check(f"T={T} res_out", host(ro), want["res_out"], dt, exact=True)
+        st = c.stats()
+        assert st["n_versions"] == 1 and st["misses"] == 1
+        v = c.version_info(0)
+        assert v.jit == 1 and (v.b_lo, v.b_hi) == (0, 6)
+        for T, Hn in ((5, 4000), (9, 3000)):             # 257..512 vectors: one kernel class
+            print(f"jit generic rmsnorm: T={T} H={Hn}", flush=True)
+            x = wl.host_array(r, (T, Hn), dt)
+            wn = wl.host_weight(r, Hn, dt)
+            y = c.rmsnorm(wl.to_torch(x, dt, DEV), wl.to_torch(wn, dt, DEV), eps)
+            torch.cuda.synchronize()
+            check(f"rmsnorm T={T} H={Hn}", host(y), O.rmsnorm(x, wn, eps, dt), dt)
+        st = c.stats()
+        assert st["n_versions"] == 2 and st["misses"] == 2
+        v = c.version_info(1)
+        assert v.jit == 0 and (v.h_lo, v.h_hi) == (2056, 4096)
+    finally:
+        torch.cuda.synchronize()
+        c.close()
