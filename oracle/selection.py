@@ -168,9 +168,10 @@ def split_fits(dtype: int, H: int, b: int) -> bool:
     return S <= SPLIT_MAX_SLICES and split_words(1 << b, S) <= SPLIT_SCRATCH_WORDS
 
 
-def rn_role(dtype: int, H: int, flags: int, T: int, b: int) -> Tuple[int, int]:
-    """(variant, grid) for RMSNorm / residual RMSNorm rows (b: the token
-    bucket of the key)."""
+def rn_role(dtype: int, H: int, flags: int, T: int, b: int,
+            res: bool = True) -> Tuple[int, int]:
+    """(variant, grid) for residual RMSNorm rows (res) or plain RMSNorm rows
+    (b: the token bucket of the key)."""
     v = 16 // elem_size(dtype)
     if not (flags & ALIGN) or H % v:
         return RN_SCALAR, T
@@ -180,6 +181,8 @@ def rn_role(dtype: int, H: int, flags: int, T: int, b: int) -> Tuple[int, int]:
     nb = next_pow2(cdiv(nvec, 256))       # a workgroup per row
     if nb <= 16:
         return RN_BLOCK[nb], T
+    if not res and nvec <= WIDE_ROW_VECS:  # plain rows: a 1024-lane workgroup
+        return RN_WIDE, T
     if split_fits(dtype, H, b):           # several workgroups per row
         return RN_SPLIT, T * split_slices(dtype, H)
     if nvec <= WIDE_ROW_VECS:             # a 1024-lane workgroup per row
@@ -713,7 +716,7 @@ def plan(key, T: int):
     f = unpack_key(key)
     op, dt, b, fl = f["op"], f["dtype"], f["bucket"], f["flags"]
     if op in (OP_RMSNORM, OP_RES_RMSNORM):
-        v, g = rn_role(dt, f["H"], fl, T, b)
+        v, g = rn_role(dt, f["H"], fl, T, b, op == OP_RES_RMSNORM)
         return v, (0, 0, 0), [(v, g, block_of(v))]
     inter = bool(f["rope_bits"] & ROPE_INTERLEAVED)
     nh = f["nq"] + f["nk"]
@@ -788,16 +791,18 @@ def _geometry_options(S: int, P: int, b: int) -> List[Tuple[int, int]]:
     return out
 
 
-def _rn_options(dt: int, H: int, fl: int, b: int, standalone: bool) -> List[int]:
+def _rn_options(dt: int, H: int, fl: int, b: int, standalone: bool,
+                res: bool = True) -> List[int]:
     """Norm rows: a row held by one wavefront can also be held by one
     256-lane workgroup (one vector per lane); standalone (the fused chain
     takes only the 256-lane register forms), a row of more than 1024
     vectors held by a 256-lane workgroup can also be held by a 1024-lane
     one, a row of more than 2048 vectors (RN_BLOCK[16]) can also be split
     over two workgroups when its scratch fits, a split row of at most
-    WIDE_ROW_VECS vectors can be held by a 1024-lane workgroup, and any
-    row held in registers can take the two-pass loop kernel."""
-    P = rn_role(dt, H, fl, 1, b)[0]
+    WIDE_ROW_VECS vectors can be held by a 1024-lane workgroup and a row
+    held by a 1024-lane workgroup can be split when its scratch fits, and
+    any row held in registers can take the two-pass loop kernel."""
+    P = rn_role(dt, H, fl, 1, b, res)[0]
     if P in (RN_SCALAR, RN_LOOP):
         return [P]
     out = [P]
@@ -811,6 +816,8 @@ def _rn_options(dt: int, H: int, fl: int, b: int, standalone: bool) -> List[int]
                 out.append(RN_SPLIT)
         if P == RN_SPLIT and H // (16 // elem_size(dt)) <= WIDE_ROW_VECS:
             out.append(RN_WIDE)
+        if P == RN_WIDE and split_fits(dt, H, b):
+            out.append(RN_SPLIT)
         out.append(RN_LOOP)
     return out
 
@@ -841,7 +848,8 @@ def candidates(key) -> List[Cand]:
     v = 16 // elem_size(dt)
     z = (0, 0, 0)
     if op in (OP_RMSNORM, OP_RES_RMSNORM):
-        return [Cand(r, z, (r,), 1) for r in _rn_options(dt, f["H"], fl, b, True)]
+        return [Cand(r, z, (r,), 1)
+                for r in _rn_options(dt, f["H"], fl, b, True, op == OP_RES_RMSNORM)]
     inter = bool(f["rope_bits"] & ROPE_INTERLEAVED)
     nh = f["nq"] + f["nk"]
     if op in (OP_ROPE_QK, OP_QK_NORM_ROPE):
@@ -1057,10 +1065,10 @@ def _with_bucket(key, b: int):
     return tuple(k)
 
 
-def _norm_h_range(dt: int, H: int, fl: int):
+def _norm_h_range(dt: int, H: int, fl: int, res: bool = True):
     """(h_lo, h_hi, h_mod) of the rows the norm kernel chosen for H serves at
-    every bucket, or None when the choice depends on the bucket (rows beyond
-    4096 vectors)."""
+    every bucket, or None when the choice depends on the bucket (residual
+    rows beyond 4096 vectors, plain rows beyond 8192)."""
     v = 16 // elem_size(dt)
     if not fl & ALIGN:
         return 1, H_LIMIT - 1, H_ANY
@@ -1068,7 +1076,7 @@ def _norm_h_range(dt: int, H: int, fl: int):
         return 1, H_LIMIT - 1, H_RAGGED
     n = H // v
     for lo, hi in ((1, 64), (65, 128), (129, 256), (257, 512), (513, 1024), (1025, 2048),
-                   (2049, 4096)):
+                   (2049, 4096)) + (() if res else ((4097, WIDE_ROW_VECS),)):
         if lo <= n <= hi:
             return lo * v, hi * v, H_MULTIPLE
     return None
@@ -1082,7 +1090,8 @@ def generic_guard(key, plan=None) -> Guard:
     A version whose plan splits norm rows keeps only the buckets whose
     scratch fits: its scratch is sized for the top of the run, at most
     SPLIT_SCRATCH_WORDS (when the policy itself splits, the run already ends
-    there; a tuned split choice clamps it)."""
+    there; a tuned split choice clamps it); and it matches only its own
+    row length (the scratch is sized by the row's slice count)."""
     P = candidates(key)[0]
     f = unpack_key(key)
     b = f["bucket"]
@@ -1093,12 +1102,13 @@ def generic_guard(key, plan=None) -> Guard:
     while hi < BUCKET_MAX and candidates(_with_bucket(key, hi + 1))[0] == P:
         hi += 1
     run = plan if plan is not None else P
-    if RN_SPLIT in run.kernels or RN_SPLIT in run.roles:
+    splits = RN_SPLIT in run.kernels or RN_SPLIT in run.roles
+    if splits:
         while hi > b and not split_fits(f["dtype"], f["H"], hi):
             hi -= 1
     h = None
-    if f["op"] in (OP_RMSNORM, OP_RES_RMSNORM):
-        h = _norm_h_range(f["dtype"], f["H"], f["flags"])
+    if f["op"] in (OP_RMSNORM, OP_RES_RMSNORM) and not splits:
+        h = _norm_h_range(f["dtype"], f["H"], f["flags"], f["op"] == OP_RES_RMSNORM)
     if h is None:
         return Guard(tuple(key), lo, hi)
     return Guard(tuple(key), lo, hi, *h)

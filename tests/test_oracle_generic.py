@@ -57,17 +57,18 @@ def test_generic_ranges_by_hand(call, b_lo, b_hi, h):
 
 
 @pytest.mark.parametrize("call,b_hi", [
-    # f32 rows of 20000 = 5000 vectors: S = ceil(5000 / 2048) = 3 workgroups
-    # per row; a call of 2^b rows needs 8 + 2^b * (3 + 1) scratch words,
-    # at most 2^22 = 4,194,304: 2^19 -> 2,097,160 fits, 2^20 -> 4,194,312
-    # does not, and from bucket 20 on the row goes to the 1024-lane
-    # workgroup (5000 <= 8192 vectors)
-    (rn_call(F, 3, 20000), 19),
+    # residual f32 rows of 20000 = 5000 vectors: S = ceil(5000 / 2048) = 3
+    # workgroups per row; a call of 2^b rows needs 8 + 2^b * (3 + 1) scratch
+    # words, at most 2^22 = 4,194,304: 2^19 -> 2,097,160 fits, 2^20 ->
+    # 4,194,312 does not, and from bucket 20 on the row goes to the
+    # 1024-lane workgroup (5000 <= 8192 vectors)
+    (res_call(F, 3, 20000), 19),
     # bf16 rows of 65536 = 8192 vectors, S = 4: 8 + 5 * 2^19 = 2,621,448
     # fits, 8 + 5 * 2^20 = 5,242,888 does not
     (res_call(BF, 3, 65536), 19),
-    # bf16 rows of 2^20 = 131072 vectors, S = 64: 8 + 65 * 2^15 = 2,129,928
-    # fits, 8 + 65 * 2^16 = 4,259,848 does not; beyond, the two-pass loop
+    # plain bf16 rows of 2^20 = 131072 vectors (beyond the 1024-lane
+    # workgroup), S = 64: 8 + 65 * 2^15 = 2,129,928 fits, 8 + 65 * 2^16 =
+    # 4,259,848 does not; beyond, the two-pass loop
     (rn_call(BF, 2, 1 << 20), 15),
 ])
 def test_split_rows_get_the_buckets_their_scratch_holds(call, b_hi):
@@ -81,8 +82,21 @@ def test_split_rows_get_the_buckets_their_scratch_holds(call, b_hi):
     assert S.split_fits(f["dtype"], f["H"], b_hi) and not S.split_fits(f["dtype"], f["H"], b_hi + 1)
     assert g.holds(S.make_key(call)) and g.holds(S._with_bucket(key, 0))
     assert not g.holds(S._with_bucket(key, b_hi + 1))
-    other = dict(F=rn_call(F, 3, 20008), BF=res_call(BF, 3, 65544))
+    other = dict(F=res_call(F, 3, 20008), BF=res_call(BF, 3, 65544))
     assert not g.holds(S.make_key(other["F" if call.dtype == F else "BF"]))
+
+
+@pytest.mark.parametrize("call,h", [
+    # plain rows of 4097..8192 vectors take the 1024-lane workgroup at every
+    # bucket: f32 4097 * 4 = 16388 .. 8192 * 4 = 32768, bf16 32776 .. 65536
+    (rn_call(F, 3, 20000), (16388, 32768)),
+    (rn_call(BF, 7, 65536), (32776, 65536)),
+    (rn_call(BF, 1, 32776), (32776, 65536)),
+])
+def test_plain_wide_rows_get_every_bucket_and_their_class(call, h):
+    g = S.generic_guard(S.make_key(call))
+    assert (g.b_lo, g.b_hi, g.h_lo, g.h_hi, g.h_mod) == (0, 22) + h + (S.H_MULTIPLE,)
+    assert S.candidates(S.make_key(call))[0].kernels == (S.RN_WIDE,)
 
 
 def test_a_tuned_split_choice_clamps_the_run():
@@ -91,22 +105,25 @@ def test_a_tuned_split_choice_clamps_the_run():
     2049..4096 vectors); the tuning candidates are [that, the 1024-lane
     workgroup, the split over S = 2, the two-pass loop]. A version running
     the split keeps buckets whose scratch 8 + 3 * 2^b words fits: b <= 20
-    (3,145,736), not 21 (6,291,464). The row-length range stays: every row
-    of 2049..4096 vectors splits in two."""
+    (3,145,736), not 21 (6,291,464), and only its own row length."""
     key = S.make_key(rn_call(BF, 3, 32768))
     cands = S.candidates(key)
     assert [c.kernels[0] for c in cands] == [S.RN_BLOCK[16], S.RN_WIDE, S.RN_SPLIT, S.RN_LOOP]
     g = S.generic_guard(key, cands[2])
-    assert (g.b_lo, g.b_hi, g.h_lo, g.h_hi, g.h_mod) == (0, 20, 16392, 32768, S.H_MULTIPLE)
+    assert (g.b_lo, g.b_hi, g.h_lo) == (0, 20, 0)
     for c in (cands[0], cands[1], cands[3]):
-        assert (S.generic_guard(key, c).b_lo, S.generic_guard(key, c).b_hi) == (0, 22)
+        gc = S.generic_guard(key, c)
+        assert (gc.b_lo, gc.b_hi, gc.h_lo, gc.h_hi) == (0, 22, 16392, 32768)
     # through the model: a timer that favours the split
     m = S.SpecCacheModel(flags=G | S.FLAG_AUTOTUNE,
                          timer=lambda k, i, c: 0.5 if S.RN_SPLIT in c.kernels else 1.0)
     assert m.call(rn_call(BF, 3, 32768)) == S.OK and m.choice == [2]
     assert (m.guards[0].b_lo, m.guards[0].b_hi) == (0, 20)
-    assert m.call(rn_call(BF, 1 << 20, 16392)) == S.OK and m.last.version == 0   # bucket 20
+    assert m.call(rn_call(BF, 1 << 20, 32768)) == S.OK and m.last.version == 0   # bucket 20
     assert m.call(rn_call(BF, (1 << 20) + 1, 32768)) == S.OK                    # bucket 21
+    # the bucket-21 miss made a version of the policy's plan over every bucket
+    # and the whole row class: another row length of the class lands there
+    assert m.call(rn_call(BF, 3, 16392)) == S.OK and m.last.version == 1
     assert m.stats.misses == 2 and len(m.versions) == 2
 
 

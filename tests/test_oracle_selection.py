@@ -152,6 +152,23 @@ def test_split_rows_need_their_scratch_to_fit(dtype, H, b, want):
     assert S.rn_role(dtype, H, S.ALIGN | S.CONTIG, 1, b)[0] == want
 
 
+@pytest.mark.parametrize("dtype,H,b,want", [
+    # plain rows of 4097..8192 vectors: the 1024-lane workgroup at any bucket
+    (BF, 32776, 0, S.RN_WIDE), (BF, 65536, 3, S.RN_WIDE), (F, 32768, 22, S.RN_WIDE),
+    (F, 16388, 19, S.RN_WIDE),
+    # 8193 vectors and more: split while the scratch fits (S = 5: 8 + 6 * 2^b
+    # <= 2^22 up to b = 19), then two passes
+    (BF, 65544, 19, S.RN_SPLIT), (BF, 65544, 20, S.RN_LOOP),
+    # up to 4096 vectors the same as the residual rows
+    (BF, 32768, 3, S.RN_BLOCK[16]), (F, 256, 3, S.RN_WAVE[1])])
+def test_plain_rows_policy(dtype, H, b, want):
+    assert S.rn_role(dtype, H, S.ALIGN | S.CONTIG, 1, b, res=False)[0] == want
+    cands = [c.kernels[0] for c in S.candidates(S.make_key(rn_call(dtype, 1 << b, H)))]
+    assert cands[0] == want
+    if want == S.RN_WIDE:                       # tuning may still split, or loop
+        assert cands[1:] == ([S.RN_SPLIT] if S.split_fits(dtype, H, b) else []) + [S.RN_LOOP]
+
+
 def test_split_scratch_layout_by_hand():
     # 3 rows of bf16 65536 (8192 vectors, 4 workgroups each): 8 header words,
     # 12 slots, 3 counters

@@ -121,22 +121,24 @@ def test_unfused_chain_has_one_candidate():
     assert S.candidates(k) == [Cand(51, (10, 31, 41), (10, 31, 41), 2)]
 
 
-@pytest.mark.parametrize("H,dtype,want", [
-    (512, BF, [11, 13, 18]),       # 64 vectors: wavefront, workgroup, loop
-    (1024, BF, [12, 13, 18]),      # 128 vectors: two per lane of a wavefront
-    (4096, BF, [14, 18]),          # 512 vectors: workgroup x 2, loop
-    (8200, BF, [16, 19, 18]),      # 1025 vectors: workgroup x 8, 1024-lane workgroup, loop
-    (32768, BF, [17, 19, 20, 18]),  # 4096 vectors: workgroup x 16, 1024 lanes, 2-way split, loop
-    (65536, BF, [20, 19, 18]),     # 8192 vectors: 4-way split, 1024-lane workgroup x 8, loop
-    (65544, BF, [20, 18]),         # 8193 vectors: 5-way split, loop (too long for 1024 lanes)
-    (32768, F, [20, 19, 18]),      # 8192 f32 vectors: 4-way split, 1024 lanes, loop
-    (1048584, BF, [18]),           # 131073 vectors: 65 workgroups is too many -> loop only
-    (100, BF, [10]),               # ragged: scalar only
+@pytest.mark.parametrize("H,dtype,want,plain", [
+    (512, BF, [11, 13, 18], None),       # 64 vectors: wavefront, workgroup, loop
+    (1024, BF, [12, 13, 18], None),      # 128 vectors: two per lane of a wavefront
+    (4096, BF, [14, 18], None),          # 512 vectors: workgroup x 2, loop
+    (8200, BF, [16, 19, 18], None),      # 1025 vectors: workgroup x 8, 1024-lane workgroup, loop
+    (32768, BF, [17, 19, 20, 18], None),  # 4096 vectors: x 16, 1024 lanes, 2-way split, loop
+    # 8192 vectors: residual rows 4-way split, 1024-lane workgroup x 8, loop;
+    # plain rows the 1024-lane workgroup first, then the split, then the loop
+    (65536, BF, [20, 19, 18], [19, 20, 18]),
+    (65544, BF, [20, 18], None),         # 8193 vectors: 5-way split, loop (too long for 1024 lanes)
+    (32768, F, [20, 19, 18], [19, 20, 18]),  # 8192 f32 vectors
+    (1048584, BF, [18], None),           # 131073 vectors: 65 workgroups is too many -> loop only
+    (100, BF, [10], None),               # ragged: scalar only
 ])
-def test_rmsnorm_candidates(H, dtype, want):
-    for mk in (rn_call, res_call):
+def test_rmsnorm_candidates(H, dtype, want, plain):
+    for mk, w in ((rn_call, plain or want), (res_call, want)):
         cands = S.candidates(key_of(mk(dtype, 3, H)))
-        assert [c.variant for c in cands] == want
+        assert [c.variant for c in cands] == w
         assert all(c.kernels == (c.variant,) and c.slices == 1 for c in cands)
 
 
