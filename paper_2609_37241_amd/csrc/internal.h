@@ -97,7 +97,9 @@ struct Role {
   int32_t variant;
   uint32_t grid;
 };
-Role rn_role(uint32_t dtype, int64_t H, unsigned flags, int64_t T, uint32_t bucket);
+// res: residual RMSNorm rows (and the chain's norm role); plain RMSNorm rows
+// of 4097..kWideRowVecs vectors take the 1024-lane workgroup at any bucket.
+Role rn_role(uint32_t dtype, int64_t H, unsigned flags, int64_t T, uint32_t bucket, bool res);
 // Workgroups per row of RN_SPLIT, and the scratch words a call of T rows
 // of that split needs.
 int32_t split_slices(uint32_t dtype, int64_t H);

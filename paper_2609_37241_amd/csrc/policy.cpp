@@ -64,19 +64,26 @@ bool split_fits(uint32_t dtype, int64_t H, uint32_t bucket) {
 // kSplitScratchWords for the top of the token bucket). Against the forms
 // it replaces, at 256-512 MiB per operand (probe, 1 GiB read flush): bf16
 // rows of 49,152 / 65,536 elements 94.9 / 94.5 us vs 97.2 / 101.1 us for a
-// 1024-work-item workgroup per row (residual 176.1 / 177.9 vs 182.2 /
-// 181.8), f32 rows of 32,768 a tie (93.0 / 176.0 us both); bf16 rows of
+// 1024-work-item workgroup per row holding the weights with the row
+// (residual 176.1 / 177.9 vs 182.2 / 181.8), f32 rows of 32,768 a tie (93.0 / 176.0 us both); bf16 rows of
 // 131,072 / 262,144 and f32 rows of 65,536 1.25-1.37x faster than two
 // passes over memory. Beyond the split's limits a row of up to
 // kWideRowVecs vectors takes the 1024-work-item workgroup and longer rows
-// make two passes. Unaligned or ragged rows take the scalar kernel.
-Role rn_role(uint32_t dtype, int64_t H, unsigned flags, int64_t T, uint32_t bucket) {
+// make two passes. Plain RMSNorm rows of 4097..kWideRowVecs vectors take
+// the 1024-work-item workgroup at every bucket: its plain form keeps two
+// workgroups per CU and has no exchange to wait for, which the residual
+// form's early residual_out stores hide in the split (in the library,
+// 1 GiB read flush: bf16 rows of 65,536 90.6 vs 93.2 us split, of 40,960
+// 59.1 vs 64.9 us, f32 rows of 32,768 91.9 vs 92.5 us). Unaligned or
+// ragged rows take the scalar kernel.
+Role rn_role(uint32_t dtype, int64_t H, unsigned flags, int64_t T, uint32_t bucket, bool res) {
   const int64_t v = vec_elems(dtype);
   if (!(flags & kAlign) || H % v) return {RN_SCALAR, uint32_t(T)};
   const int64_t nvec = H / v;
   if (nvec <= 128) return {nvec <= 64 ? RN_WAVE_1 : RN_WAVE_2, uint32_t(cdiv(T, 4))};
   const int64_t nb = next_pow2(cdiv(nvec, 256));
   if (nb <= 16) return {RN_BLOCK_1 + pow2_index(nb), uint32_t(T)};
+  if (!res && nvec <= kWideRowVecs) return {RN_WIDE, uint32_t(T)};
   if (split_fits(dtype, H, bucket)) return {RN_SPLIT, uint32_t(T * split_slices(dtype, H))};
   if (nvec <= kWideRowVecs) return {RN_WIDE, uint32_t(T)};
   return {RN_LOOP, uint32_t(T)};
@@ -302,7 +309,7 @@ Plan plan_for_key(const Key &k) {
   switch (op) {
     case TRI_OP_RMSNORM:
     case TRI_OP_RES_RMSNORM: {
-      const Role r = rn_role(dt, key_H(k), fl, 1, b);
+      const Role r = rn_role(dt, key_H(k), fl, 1, b, op == TRI_OP_RES_RMSNORM);
       p.variant = r.variant;
       p.n_launches = 1;
       p.kvariant[0] = r.variant;
@@ -351,7 +358,7 @@ Plan plan_for_key(const Key &k) {
     default:
       break;
   }
-  const Role rn = rn_role(dt, key_H(k), fl & 3u, 1, b);
+  const Role rn = rn_role(dt, key_H(k), fl & 3u, 1, b, true);
   const bool inter = (key_rope_bits(k) & kRopeInterleaved) != 0;
   const Role ro = rope_role(dt, int32_t(key_hd(k)), int32_t(key_rd(k)), inter, (fl >> 2) & 3u, 1,
                             (fl & kChainQkNorm) != 0);
@@ -395,9 +402,10 @@ Key with_bucket(const Key &k, uint32_t b) {
 // bucket: unaligned rows take the scalar kernel at any length, aligned
 // ragged ones at every length that is not a whole number of vectors; rows
 // of whole vectors one wavefront (1-64, 65-128 vectors) or one workgroup
-// (129-256, 257-512, ..., 2049-4096 vectors). Longer rows: none (their
-// kernel depends on the bucket through the split's scratch).
-bool norm_h_range(uint32_t dt, uint32_t H, unsigned fl, Guard *g) {
+// (129-256, 257-512, ..., 2049-4096 vectors; plain rows also 4097-8192 in
+// the 1024-lane workgroup). Longer rows: none (their kernel depends on the
+// bucket through the split's scratch).
+bool norm_h_range(uint32_t dt, uint32_t H, unsigned fl, bool res, Guard *g) {
   const int64_t v = vec_elems(dt);
   if (!(fl & kAlign) || H % v) {
     g->h_lo = 1;
@@ -411,11 +419,14 @@ bool norm_h_range(uint32_t dt, uint32_t H, unsigned fl, Guard *g) {
     lo = 1, hi = 64;
   } else if (n <= 128) {
     lo = 65, hi = 128;
-  } else {
+  } else if (n <= 4096) {
     const int64_t nb = next_pow2(cdiv(n, 256));
-    if (nb > 16) return false;
     lo = nb == 1 ? 129 : 128 * nb + 1;
     hi = 256 * nb;
+  } else if (!res && n <= kWideRowVecs) {
+    lo = 4097, hi = kWideRowVecs;
+  } else {
+    return false;
   }
   g->h_lo = uint32_t(lo * v);
   g->h_hi = uint32_t(hi * v);
@@ -440,15 +451,18 @@ Guard generic_guard(const Key &k, const Plan &chosen) {
   // A split version's scratch is sized for the top of its run: keep only
   // the buckets whose scratch fits (the policy's own split stops there
   // already; a tuned split choice is clamped here).
-  if (splits_rows(chosen))
+  // It also matches only its own row length: the scratch is sized by the
+  // row's slice count.
+  const bool splits = splits_rows(chosen);
+  if (splits)
     while (hi > b && !split_fits(key_dtype(k), key_H(k), hi)) --hi;
   Guard g = kExact;
   g.b_lo = int32_t(lo);
   g.b_hi = int32_t(hi);
   const uint32_t op = key_op(k);
-  if (op == TRI_OP_RMSNORM || op == TRI_OP_RES_RMSNORM) {
+  if ((op == TRI_OP_RMSNORM || op == TRI_OP_RES_RMSNORM) && !splits) {
     Guard h = g;
-    if (norm_h_range(key_dtype(k), key_H(k), key_flags(k), &h)) g = h;
+    if (norm_h_range(key_dtype(k), key_H(k), key_flags(k), op == TRI_OP_RES_RMSNORM, &h)) g = h;
   }
   return g;
 }
@@ -490,9 +504,9 @@ bool guard_holds(const Key &vk, const Guard &g, const Key &k) {
 // three-launch sequence of the policy's roles.
 namespace {
 
-int rn_options(uint32_t dt, int64_t H, unsigned fl, uint32_t b, bool standalone,
+int rn_options(uint32_t dt, int64_t H, unsigned fl, uint32_t b, bool standalone, bool res,
                int32_t *out) {
-  const int32_t P = rn_role(dt, H, fl, 1, b).variant;
+  const int32_t P = rn_role(dt, H, fl, 1, b, res).variant;
   int n = 0;
   out[n++] = P;
   if (P == RN_SCALAR || P == RN_LOOP) return n;
@@ -506,6 +520,7 @@ int rn_options(uint32_t dt, int64_t H, unsigned fl, uint32_t b, bool standalone,
       out[n++] = RN_SPLIT;
   }
   if (P == RN_SPLIT && H / vec_elems(dt) <= kWideRowVecs) out[n++] = RN_WIDE;
+  if (P == RN_WIDE && split_fits(dt, H, b)) out[n++] = RN_SPLIT;
   out[n++] = RN_LOOP;
   return n;
 }
@@ -559,7 +574,7 @@ int plan_candidates(const Key &k, Plan *out) {
     case TRI_OP_RMSNORM:
     case TRI_OP_RES_RMSNORM: {
       int32_t r[4];
-      const int nr = rn_options(dt, key_H(k), fl, b, true, r);
+      const int nr = rn_options(dt, key_H(k), fl, b, true, op == TRI_OP_RES_RMSNORM, r);
       for (int i = 1; i < nr; ++i) out[n++] = single(r[i], P.ksub[0]);
       return n;
     }
@@ -594,7 +609,7 @@ int plan_candidates(const Key &k, Plan *out) {
   if (P.variant != CH_FUSED) return n;
   int32_t r[4];
   Geometry g[5];
-  const int nr = rn_options(dt, key_H(k), fl & 3u, b, false, r);
+  const int nr = rn_options(dt, key_H(k), fl & 3u, b, false, true, r);
   const int ng = geometry_options(P.rope_slices, P.rope_tokens, b, g);
   const int32_t sw0 = P.roles[2], sw1 = sw0 == SW_FLAT ? SW_FLAT_NT : SW_FLAT;
   n = 0;

@@ -814,17 +814,19 @@ def _last_launch(lib, nbytes=512, size=None):
 
 
 def test_long_rows_launch_split_wide_and_loop_forms(lib, fresh):
-    """Rows beyond 4096 vectors are split over S = ceil(vectors / 2048)
-    workgroups of 256 (standalone, residual, and as the norm launch of a
-    three-launch chain); where the split's scratch for the key's bucket would
-    be too large a row of up to 8192 vectors takes one 1024-work-item
-    workgroup, and longer rows two passes. Launches and records match the
-    model's plan."""
+    """Residual rows beyond 4096 vectors are split over S = ceil(vectors /
+    2048) workgroups of 256 (standalone, and as the norm launch of a
+    three-launch chain), plain rows beyond 8192 vectors too; plain rows of
+    4097..8192 vectors take one 1024-work-item workgroup, and so do residual
+    ones where the split's scratch for the key's bucket would be too large;
+    longer rows make two passes. Launches and records match the model's
+    plan."""
     cache = fresh(flags=S.FLAG_AUTO_INSTALL)
-    cases = [(rn_call(BF, 3, 65536), [S.RN_SPLIT]), (res_call(F, 2, 20480), [S.RN_SPLIT]),
+    cases = [(rn_call(BF, 3, 65536), [S.RN_WIDE]), (res_call(BF, 3, 65536), [S.RN_SPLIT]),
+             (res_call(F, 2, 20480), [S.RN_SPLIT]), (rn_call(F, 2, 20480), [S.RN_WIDE]),
              (rn_call(BF, 3, 65544), [S.RN_SPLIT]), (rn_call(BF, 3, 32768), [S.RN_BLOCK[16]]),
              (rn_call(BF, 3, 1048584), [S.RN_LOOP]),
-             (rn_call(BF, (1 << 19) + 1, 32776), [S.RN_WIDE]),
+             (res_call(BF, (1 << 19) + 1, 32776), [S.RN_WIDE]),
              (chain_call(BF, 2, 40960, 11008, 32, 32, 128), [S.RN_SPLIT, S.ROPE_VEC, S.SW_FLAT])]
     for c, kinds in cases:
         n0 = lib.trifake_launch_count()

@@ -9,7 +9,7 @@ import ctypes as C
 import pytest
 
 from oracle import selection as S
-from tests.selection_calls import chain_call, elem_offset, rn_call
+from tests.selection_calls import chain_call, elem_offset, res_call, rn_call
 from tests.test_host_cache import (c_call, c_install, c_record, c_stats, call_zoo, lib,  # noqa
                                    m_stats, run_both)
 import workloads as wl
@@ -166,22 +166,22 @@ def _zero_allocs(lib):
 
 
 def test_generic_split_version_serves_its_run_with_a_scratch_for_the_top(lib, fresh):
-    """bf16 rows of 65536 (S = 4): one generic version serves buckets 0..19,
-    with a zeroed scratch of 8 + 5 * 2^19 words allocated at install; a call
-    in bucket 20 is a miss on both sides (the policy then takes the
-    1024-lane workgroup, whose version needs no scratch)."""
+    """Residual bf16 rows of 65536 (S = 4): one generic version serves
+    buckets 0..19, with a zeroed scratch of 8 + 5 * 2^19 words allocated at
+    install; a call in bucket 20 is a miss on both sides (the policy then
+    takes the 1024-lane workgroup, whose version needs no scratch)."""
     flags = G | S.FLAG_AUTO_INSTALL
     cache = fresh(flags=flags)
     m = S.SpecCacheModel(flags=flags)
     n0, b0 = _zero_allocs(lib)
     for T in (3, 1, 64, 5000):
-        run_both(lib, cache, m, rn_call(BF, T, 65536), install=False)
+        run_both(lib, cache, m, res_call(BF, T, 65536), install=False)
     assert c_guards(lib, cache) == m_guards(m) == [(0, 19, 0, 0, 0)]
     n1, b1 = _zero_allocs(lib)
     assert (n1 - n0, b1 - b0) == (1, 8 * (8 + 5 * (1 << 19)))
     assert c_stats(lib, cache) == m_stats(m) and m.stats.misses == 1
     # a bucket-20 key: a miss that installs the next version
-    key20 = S._with_bucket(S.make_key(rn_call(BF, 3, 65536)), 20)
+    key20 = S._with_bucket(S.make_key(res_call(BF, 3, 65536)), 20)
     assert c_install_key(lib, cache, key20) == m.install_key(key20) == S.OK
     assert len(c_guards(lib, cache)) == len(m.versions) == 2
     assert _zero_allocs(lib)[0] == n1                        # RN_WIDE: no scratch
@@ -191,7 +191,9 @@ def test_tuned_split_choice_is_clamped_to_the_buckets_its_scratch_holds(lib, fre
     """bf16 rows of 32768: the policy's 256-lane workgroup holds at every
     bucket, but a tuned split (S = 2) only where 8 + 3 * 2^b words fit, so
     the generic version's run is 0..20 (scratch sized for 2^20 rows), not
-    0..22; the same run comes out of the model."""
+    0..22, and only its own row length; the same guard comes out of the
+    model. A bucket-21 miss then makes a version of the policy's plan over
+    every bucket and the row class, where another length lands."""
     from tests.test_host_tuning import scripted_timer, set_costs
     costs = [(S.RN_SPLIT, -1, 0, 0.5)]
     flags = G | S.FLAG_AUTO_INSTALL | S.FLAG_AUTOTUNE
@@ -202,15 +204,16 @@ def test_tuned_split_choice_is_clamped_to_the_buckets_its_scratch_holds(lib, fre
     c = rn_call(BF, 3, 32768)
     assert c_call(lib, cache, c) == m.call(c) == S.OK
     assert m.choice == [2] and c_record(lib, cache) == m.last.as_tuple()
-    assert c_guards(lib, cache) == m_guards(m) == [(0, 20, 16392, 32768, S.H_MULTIPLE)]
+    assert c_guards(lib, cache) == m_guards(m) == [(0, 20, 0, 0, 0)]
     n1, b1 = _zero_allocs(lib)
     assert (n1 - n0, b1 - b0) == (1, 8 * (8 + 3 * (1 << 20)))
-    # inside the run, other lengths of the class split with the same scratch
-    for T, H in ((1, 16392), (700, 24576), (1 << 20, 32768)):
-        cc = rn_call(BF, T, H)
+    for T in (1, 700, 1 << 20):
+        cc = rn_call(BF, T, 32768)
         assert c_call(lib, cache, cc) == m.call(cc) == S.OK
         assert c_record(lib, cache) == m.last.as_tuple() and m.last.version == 0
-    # bucket 21: beyond the run, a miss on both sides
-    cc = rn_call(BF, (1 << 20) + 1, 32768)
-    assert c_call(lib, cache, cc) == m.call(cc) == S.OK
+    for T, H, v in (((1 << 20) + 1, 32768, 1), (700, 24576, 1)):
+        cc = rn_call(BF, T, H)
+        assert c_call(lib, cache, cc) == m.call(cc) == S.OK
+        assert c_record(lib, cache) == m.last.as_tuple() and m.last.version == v
+    assert c_guards(lib, cache) == m_guards(m)
     assert c_stats(lib, cache) == m_stats(m) and m.stats.misses == 2
