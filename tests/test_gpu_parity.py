@@ -159,8 +159,12 @@ RN_CASES = [
     (nm.BF16, 130, 4096, "plain"), (nm.F32, 100, 256, "plain"), (nm.BF16, 70, 8192, "plain"),
     (nm.F32, 65, 4096, "unaligned"), (nm.BF16, 66, 4096, "strided"), (nm.F32, 67, 16384, "plain"),
     (nm.BF16, 13, 1024, "plain"), (nm.BF16, 13, 1032, "plain"), (nm.F32, 7, 512, "plain"),
-    # rows beyond 4096 vectors: split over ceil(vectors / 2048) workgroups
-    # (3..16 here, a ragged last slice at 8193 vectors), two passes beyond 64
+    # rows beyond 4096 vectors: residual rows (and plain rows beyond 8192
+    # vectors) split over ceil(vectors / 2048) workgroups (3..16 here, a
+    # ragged last slice at 8193 vectors), plain rows of up to 8192 vectors
+    # in one 1024-lane workgroup (4097 vectors: one lane group holds the
+    # last vector), two passes beyond 64 slices
+    (nm.BF16, 3, 32776, "plain"), (nm.F32, 4, 16388, "strided"), (nm.BF16, 9, 32776, "unaligned"),
     (nm.BF16, 5, 40960, "plain"), (nm.BF16, 3, 65536, "strided"), (nm.BF16, 67, 49152, "plain"),
     (nm.BF16, 2, 65544, "plain"), (nm.F32, 4, 20480, "plain"), (nm.F32, 3, 32768, "plain"),
     (nm.F32, 2, 32772, "plain"), (nm.F32, 2, 131072, "plain"), (nm.BF16, 5, 40960, "unaligned"),
