@@ -48,7 +48,8 @@
  *   status and leaves the cache unchanged except its counters.
  * - One thread per cache. A cache is bound to the device current when it is
  *   created.
- * - RMSNorm rows of more than 4096 16-byte vectors may be split over several
+ * - Residual RMSNorm rows of more than 4096 16-byte vectors, and plain
+ *   RMSNorm rows of more than 8192, may be split over several
  *   workgroups of one launch that exchange partial sums through scratch the
  *   version owns (allocated zeroed at install, left zeroed by every launch).
  *   Launches of one such version must not overlap in time: issue its calls
@@ -298,11 +299,12 @@ typedef struct tri_chain_args {
  * install policy picks the same plan, and -- for RMSNorm and residual
  * RMSNorm rows held by one wavefront or one workgroup, or by the scalar
  * kernel -- any hidden size that kernel serves (rows of 1-64, 65-128,
- * 129-256, ..., 2049-4096 16-byte vectors, every length of the scalar
- * kernel's class). A version whose plan (the policy's or a tuned one)
- * splits norm rows over workgroups keeps only the buckets of that run whose
- * split scratch fits (at most 32 MiB, allocated for the top bucket at
- * install), and matches its exact hidden size. tri_spec_install_key and tri_spec_import_keys always create
+ * 129-256, ..., 2049-4096 16-byte vectors, plain RMSNorm rows also
+ * 4097-8192, every length of the scalar kernel's class). A version whose
+ * plan (the policy's or a tuned one) splits norm rows over workgroups keeps
+ * only the buckets of that run whose split scratch fits (at most 32 MiB,
+ * allocated for the top bucket at install), and matches its exact hidden
+ * size. tri_spec_install_key and tri_spec_import_keys always create
  * exact versions, so exact versions installed first take precedence over
  * later generic ones that overlap them, and a key that an installed
  * version already matches installs nothing (a version behind it could
