@@ -1070,3 +1070,48 @@ def test_chain_call_replays_from_a_hip_graph(tri, cache):
         torch.cuda.synchronize()
         for n in ("y", "res_out", "q", "k", "out"):
             check(f"replay {step}: {n}", host(A[n]), host(B[n]), cfg.dtype, exact=True)
+
+
+@pytest.mark.parametrize("entry", ["ordinary", "noalloc"])
+def test_split_norm_replays_from_a_hip_graph(tri, cache, entry):
+    """A split residual norm (bf16 rows of 65536, 4 workgroups per row)
+    captured in a graph after its version is installed: the captured launch
+    exchanges partial sums through its scratch, which every launch leaves
+    zeroed, so the graph needs no clearing node. Four replays, with the
+    program's own eager work between them, each equal a direct call on twin
+    buffers bit for bit and the oracle within tolerance."""
+    print(f"graph replay of a split norm ({entry})", flush=True)
+    T, H = 5, 65536
+    r = rng(29)
+    w = wl.host_weight(r, H, nm.BF16)
+    x0, r0 = wl.host_array(r, (T, H), nm.BF16), wl.host_array(r, (T, H), nm.BF16)
+    wd = wl.to_torch(w, nm.BF16, DEV)
+    A = dict(x=wl.to_torch(x0, nm.BF16, DEV), r=wl.to_torch(r0, nm.BF16, DEV))
+    B = {k: v.clone() for k, v in A.items()}
+    for d in (A, B):
+        d["y"], d["ro"] = torch.empty_like(d["x"]), torch.empty_like(d["x"])
+    call = cache.residual_rmsnorm_noalloc if entry == "noalloc" else cache.residual_rmsnorm
+    cache.residual_rmsnorm(B["x"], B["r"], wd, 1e-6, out=B["y"], residual_out=B["ro"])
+    torch.cuda.synchronize()
+    assert cache.last_selection().variant == S.RN_SPLIT
+    s = torch.cuda.Stream()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        call(A["x"], A["r"], wd, 1e-6, out=A["y"], residual_out=A["ro"],
+             stream=torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    for step in range(4):
+        for d in (A, B):                       # the program's own eager work in between
+            d["x"].mul_(0.5).add_(0.25)
+            d["r"].mul_(-1.0)
+        torch.cuda.synchronize()
+        g.replay()
+        cache.residual_rmsnorm(B["x"], B["r"], wd, 1e-6, out=B["y"], residual_out=B["ro"])
+        torch.cuda.synchronize()
+        for n in ("y", "ro"):
+            check(f"replay {step}: {n}", host(A[n]), host(B[n]), nm.BF16, exact=True)
+        wy, wh = O.residual_rmsnorm(host(A["x"]), host(A["r"]), w, 1e-6, nm.BF16)
+        check(f"replay {step}: y vs oracle", host(A["y"]), wy, nm.BF16)
+        check(f"replay {step}: res_out vs oracle", host(A["ro"]), wh, nm.BF16, exact=True)
+    del g
+    torch.cuda.synchronize()
