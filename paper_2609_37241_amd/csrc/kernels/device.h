@@ -852,8 +852,29 @@ __device__ __forceinline__ void rope_scalar_block(const RopeArgs &a, int64_t t, 
 // measured as 7 % (it sits close to its vector ALU limit), while the
 // branch is skipped whenever no lane of the wavefront is that negative.
 // At g = -inf the tail gives -inf * 0 = NaN, as -inf / (1 + inf) does.
+//
+// exp(-g) itself is 2^th * 2^tl with th = RN(-g * hi), tl = the rest of
+// -g * log2(e) (an fma recovers the product's rounding error, lo carries
+// log2(e) - hi), and 2^tl = 1 + tl ln 2 to first order (|tl| < 2^-17): the
+// hardware exp2 (v_exp_f32, 1 ulp) and four more instructions instead of
+// the library expf's range reduction. The relative error of silu stays
+// below 2.4e-7 for |g| <= 80 (checked against the float64 value over
+// 3 million arguments, as expf's form gives 1.9e-7). At one token the
+// SwiGLU role is the chain's critical path and runs its instructions back
+// to back on one wavefront per SIMD: the shorter sequence measured 2.37
+// against 2.56 us of device time for the standalone 1-token SwiGLU
+// (rocprofv3, 3000 launches each). g is capped at 100 for the exponent
+// (exp(-100) is far below float32's resolution next to 1), which keeps
+// th and tl finite at g = +inf, where silu is +inf.
 __device__ __forceinline__ float silu(float g) {
-  float r = g * __builtin_amdgcn_rcpf(1.0f + expf(-g));
+  constexpr float kLog2eHi = 1.44269502162933349609375f;   // RN_f32(log2 e)
+  constexpr float kLog2eLo = 1.925963e-08f;                // log2 e - kLog2eHi
+  constexpr float kLn2 = 0.693147180559945309f;
+  const float ng = -__builtin_fminf(g, 100.0f);
+  const float th = ng * kLog2eHi;
+  const float tl = __builtin_fmaf(ng, kLog2eHi, -th) + ng * kLog2eLo;
+  const float e = __builtin_amdgcn_exp2f(th);
+  float r = g * __builtin_amdgcn_rcpf(1.0f + __builtin_fmaf(e * tl, kLn2, e));
   if (__builtin_expect(g < -80.0f, 0)) r = g * expf(g);
   return r;
 }
