@@ -486,7 +486,8 @@ def _layer_lists():
     ]
 
 
-@pytest.mark.parametrize("auto", [0, 1])
+@pytest.mark.parametrize("auto", [0, 1, S.FLAG_GENERIC, S.FLAG_GENERIC | 1],
+                         ids=["exact", "exact-auto", "generic", "generic-auto"])
 def test_layers_parity_with_model(lib, fresh, auto):
     cache = fresh(flags=auto)
     m = S.SpecCacheModel(flags=auto)
@@ -498,6 +499,15 @@ def test_layers_parity_with_model(lib, fresh, auto):
                 im, rm = m.install_last_miss()
                 assert ic == im == 0 and rc == rm.as_tuple()
                 st = run_layers_both(lib, cache, m, calls)
+    from paper_2609_37241_amd._lib import VersionInfo
+    got = []
+    for i in range(len(m.versions)):
+        v = VersionInfo()
+        assert lib.tri_spec_version_info(cache, i, C.byref(v)) == 0
+        got.append((v.b_lo, v.b_hi, v.h_lo, v.h_hi, v.h_mod))
+    assert got == [(g.b_lo, g.b_hi, g.h_lo, g.h_hi, g.h_mod) for g in m.guards]
+    if auto & S.FLAG_GENERIC:
+        assert any(g.b_lo >= 0 for g in m.guards)
 
 
 @pytest.mark.parametrize("fail_at", [0, 1, 5, 9])
