@@ -56,6 +56,7 @@ RN_LOOP = 18
 RN_WIDE = 19               # a 1024-work-item workgroup per row, 8 vectors per lane
 WIDE_LANES = 1024
 WIDE_ROW_VECS = 8 * WIDE_LANES   # the longest row it holds (16-byte vectors)
+WIDE_PLAIN_VECS = 7 * WIDE_LANES  # plain rows up to here take it by policy
 RN_SPLIT = 20              # a row over S workgroups of 256, 8 vectors per work-item
 SPLIT_SPAN = 8 * 256       # vectors one split workgroup holds
 SPLIT_MAX_SLICES = 64      # workgroups per row, at most
@@ -181,7 +182,7 @@ def rn_role(dtype: int, H: int, flags: int, T: int, b: int,
     nb = next_pow2(cdiv(nvec, 256))       # a workgroup per row
     if nb <= 16:
         return RN_BLOCK[nb], T
-    if not res and nvec <= WIDE_ROW_VECS:  # plain rows: a 1024-lane workgroup
+    if not res and nvec <= WIDE_PLAIN_VECS:  # plain rows: a 1024-lane workgroup
         return RN_WIDE, T
     if split_fits(dtype, H, b):           # several workgroups per row
         return RN_SPLIT, T * split_slices(dtype, H)
@@ -1076,7 +1077,7 @@ def _norm_h_range(dt: int, H: int, fl: int, res: bool = True):
         return 1, H_LIMIT - 1, H_RAGGED
     n = H // v
     for lo, hi in ((1, 64), (65, 128), (129, 256), (257, 512), (513, 1024), (1025, 2048),
-                   (2049, 4096)) + (() if res else ((4097, WIDE_ROW_VECS),)):
+                   (2049, 4096)) + (() if res else ((4097, WIDE_PLAIN_VECS),)):
         if lo <= n <= hi:
             return lo * v, hi * v, H_MULTIPLE
     return None

@@ -87,16 +87,24 @@ def test_split_rows_get_the_buckets_their_scratch_holds(call, b_hi):
 
 
 @pytest.mark.parametrize("call,h", [
-    # plain rows of 4097..8192 vectors take the 1024-lane workgroup at every
-    # bucket: f32 4097 * 4 = 16388 .. 8192 * 4 = 32768, bf16 32776 .. 65536
-    (rn_call(F, 3, 20000), (16388, 32768)),
-    (rn_call(BF, 7, 65536), (32776, 65536)),
-    (rn_call(BF, 1, 32776), (32776, 65536)),
+    # plain rows of 4097..7168 vectors take the 1024-lane workgroup at every
+    # bucket: f32 4097 * 4 = 16388 .. 7168 * 4 = 28672, bf16 32776 .. 57344
+    (rn_call(F, 3, 20000), (16388, 28672)),
+    (rn_call(BF, 7, 57344), (32776, 57344)),
+    (rn_call(BF, 1, 32776), (32776, 57344)),
 ])
 def test_plain_wide_rows_get_every_bucket_and_their_class(call, h):
     g = S.generic_guard(S.make_key(call))
     assert (g.b_lo, g.b_hi, g.h_lo, g.h_hi, g.h_mod) == (0, 22) + h + (S.H_MULTIPLE,)
     assert S.candidates(S.make_key(call))[0].kernels == (S.RN_WIDE,)
+
+
+def test_plain_rows_of_7169_to_8192_vectors_split_like_residual_rows():
+    # bf16 65536 = 8192 vectors: S = 4, the run ends at bucket 19 (as for
+    # residual rows), and the row length is exact
+    g = S.generic_guard(S.make_key(rn_call(BF, 3, 65536)))
+    assert (g.b_lo, g.b_hi, g.h_lo) == (0, 19, 0)
+    assert S.candidates(S.make_key(rn_call(BF, 3, 65536)))[0].kernels == (S.RN_SPLIT,)
 
 
 def test_a_tuned_split_choice_clamps_the_run():

@@ -153,9 +153,13 @@ def test_split_rows_need_their_scratch_to_fit(dtype, H, b, want):
 
 
 @pytest.mark.parametrize("dtype,H,b,want", [
-    # plain rows of 4097..8192 vectors: the 1024-lane workgroup at any bucket
-    (BF, 32776, 0, S.RN_WIDE), (BF, 65536, 3, S.RN_WIDE), (F, 32768, 22, S.RN_WIDE),
+    # plain rows of 4097..7168 vectors: the 1024-lane workgroup at any bucket
+    (BF, 32776, 0, S.RN_WIDE), (BF, 57344, 3, S.RN_WIDE), (F, 28672, 22, S.RN_WIDE),
     (F, 16388, 19, S.RN_WIDE),
+    # 7169..8192 vectors: split like residual rows (S = 4), the 1024-lane
+    # workgroup where the scratch does not fit
+    (BF, 57352, 3, S.RN_SPLIT), (BF, 65536, 19, S.RN_SPLIT), (BF, 65536, 20, S.RN_WIDE),
+    (F, 32768, 3, S.RN_SPLIT),
     # 8193 vectors and more: split while the scratch fits (S = 5: 8 + 6 * 2^b
     # <= 2^22 up to b = 19), then two passes
     (BF, 65544, 19, S.RN_SPLIT), (BF, 65544, 20, S.RN_LOOP),

@@ -127,11 +127,14 @@ def test_unfused_chain_has_one_candidate():
     (4096, BF, [14, 18], None),          # 512 vectors: workgroup x 2, loop
     (8200, BF, [16, 19, 18], None),      # 1025 vectors: workgroup x 8, 1024-lane workgroup, loop
     (32768, BF, [17, 19, 20, 18], None),  # 4096 vectors: x 16, 1024 lanes, 2-way split, loop
-    # 8192 vectors: residual rows 4-way split, 1024-lane workgroup x 8, loop;
+    # 8192 vectors: 4-way split, 1024-lane workgroup x 8, loop
+    (65536, BF, [20, 19, 18], None),
+    # 7168 vectors: residual rows 4-way split, 1024-lane workgroup x 7, loop;
     # plain rows the 1024-lane workgroup first, then the split, then the loop
-    (65536, BF, [20, 19, 18], [19, 20, 18]),
+    (57344, BF, [20, 19, 18], [19, 20, 18]),
     (65544, BF, [20, 18], None),         # 8193 vectors: 5-way split, loop (too long for 1024 lanes)
-    (32768, F, [20, 19, 18], [19, 20, 18]),  # 8192 f32 vectors
+    (32768, F, [20, 19, 18], None),          # 8192 f32 vectors
+    (28672, F, [20, 19, 18], [19, 20, 18]),  # 7168 f32 vectors
     (1048584, BF, [18], None),           # 131073 vectors: 65 workgroups is too many -> loop only
     (100, BF, [10], None),               # ragged: scalar only
 ])
