@@ -662,7 +662,9 @@ def main():
         copy_src = torch.empty(1 << 29, dtype=torch.bfloat16, device=dev)
         copy_dst = torch.empty_like(copy_src)
         # long rows: bf16 [2048, 65536] and the same memory as [1024, 131072]
-        # (each row split over 4 / 8 workgroups that exchange partial sums)
+        # (each row split over 4 / 8 workgroups that exchange partial sums),
+        # and plain rows of [2048, 57344] in the front of that memory (one
+        # 1024-lane workgroup per row)
         lx = torch.randn((2048, 65536), device=dev).to(db["x"].dtype)
         lr, ly, lro = torch.randn_like(lx), torch.empty_like(lx), torch.empty_like(lx)
         lw = (torch.rand(65536, device=dev) + 0.5).to(lx.dtype)
@@ -672,6 +674,9 @@ def main():
         v2 = lambda t: t.view(1024, 131072)          # noqa: E731
         nbytes["rmsnorm_rows131072"] = 2 * lx.numel() * 2 + 131072 * 2
         nbytes["residual_rmsnorm_rows131072"] = 4 * lx.numel() * 2 + 131072 * 2
+        v57 = lambda t: t.view(-1)[:2048 * 57344].view(2048, 57344)   # noqa: E731
+        lw57 = (torch.rand(57344, device=dev) + 0.5).to(lx.dtype)
+        nbytes["rmsnorm_rows57344"] = 2 * 2048 * 57344 * 2 + 57344 * 2
         ops = {
             "chain": lambda: cb.decode_chain_args(ab, stream),
             "residual_rmsnorm": lambda: cb.residual_rmsnorm(db["x"], db["residual"], db["w"],
@@ -694,6 +699,8 @@ def main():
                                                      stream=stream),
             "residual_rmsnorm_rows131072": lambda: cb.residual_rmsnorm(
                 v2(lx), v2(lr), lw2, cfgb.eps, out=v2(ly), residual_out=v2(lro), stream=stream),
+            "rmsnorm_rows57344": lambda: cb.rmsnorm(v57(lx), lw57, cfgb.eps, out=v57(ly),
+                                                    stream=stream),
             "copy_1GiB_torch": lambda: copy_dst.copy_(copy_src),
         }
         n16 = copy_src.numel() * 2 // 16
@@ -786,6 +793,8 @@ def main():
             "rmsnorm_rows131072": ("1 read : 1 write", 0, P(lx), None, P(ly), None, L16),
             "residual_rmsnorm_rows131072": ("2 reads : 2 writes", 3, P(lx), P(lr), P(ly),
                                             P(lro), L16),
+            "rmsnorm_rows57344": ("1 read : 1 write", 0, P(lx), None, P(ly), None,
+                                  2048 * 57344 * 2 // 16),
         }
         nio = {0: 2, 1: 2, 2: 3, 3: 4}
         for name, (mix, kind, i0, i1, o0, o1, n) in matched.items():

@@ -49,7 +49,7 @@
  * - One thread per cache. A cache is bound to the device current when it is
  *   created.
  * - Residual RMSNorm rows of more than 4096 16-byte vectors, and plain
- *   RMSNorm rows of more than 8192, may be split over several
+ *   RMSNorm rows of more than 7168, may be split over several
  *   workgroups of one launch that exchange partial sums through scratch the
  *   version owns (allocated zeroed at install, left zeroed by every launch).
  *   Launches of one such version must not overlap in time: issue its calls
@@ -300,7 +300,7 @@ typedef struct tri_chain_args {
  * RMSNorm rows held by one wavefront or one workgroup, or by the scalar
  * kernel -- any hidden size that kernel serves (rows of 1-64, 65-128,
  * 129-256, ..., 2049-4096 16-byte vectors, plain RMSNorm rows also
- * 4097-8192, every length of the scalar kernel's class). A version whose
+ * 4097-7168, every length of the scalar kernel's class). A version whose
  * plan (the policy's or a tuned one) splits norm rows over workgroups keeps
  * only the buckets of that run whose split scratch fits (at most 32 MiB,
  * allocated for the top bucket at install), and matches its exact hidden

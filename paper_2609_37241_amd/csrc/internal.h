@@ -36,6 +36,7 @@ constexpr int64_t kHLimit = int64_t(1) << 24;
 constexpr int64_t kILimit = int64_t(1) << 31;
 constexpr uint64_t kSpanMax = uint64_t(1) << 47;   // bytes an operand's rows may span
 constexpr int64_t kWideRowVecs = 8 * int64_t(kWideLanes);   // longest RN_WIDE row (vectors)
+constexpr int64_t kWidePlainVecs = 7 * int64_t(kWideLanes);  // plain rows up to here: RN_WIDE
 // RN_SPLIT: rows beyond 16 * 256 vectors, at most kSplitMaxSlices workgroups
 // per row; a version's scratch (kSplitHeaderWords + 2^bucket * (S + 1)
 // words) may take at most kSplitScratchWords (32 MiB), else the longer
@@ -98,7 +99,7 @@ struct Role {
   uint32_t grid;
 };
 // res: residual RMSNorm rows (and the chain's norm role); plain RMSNorm rows
-// of 4097..kWideRowVecs vectors take the 1024-lane workgroup at any bucket.
+// of 4097..kWidePlainVecs vectors take the 1024-lane workgroup at any bucket.
 Role rn_role(uint32_t dtype, int64_t H, unsigned flags, int64_t T, uint32_t bucket, bool res);
 // Workgroups per row of RN_SPLIT, and the scratch words a call of T rows
 // of that split needs.

@@ -69,13 +69,18 @@ bool split_fits(uint32_t dtype, int64_t H, uint32_t bucket) {
 // 131,072 / 262,144 and f32 rows of 65,536 1.25-1.37x faster than two
 // passes over memory. Beyond the split's limits a row of up to
 // kWideRowVecs vectors takes the 1024-work-item workgroup and longer rows
-// make two passes. Plain RMSNorm rows of 4097..kWideRowVecs vectors take
+// make two passes. Plain RMSNorm rows of 4097..kWidePlainVecs vectors take
 // the 1024-work-item workgroup at every bucket: its plain form keeps two
 // workgroups per CU and has no exchange to wait for, which the residual
-// form's early residual_out stores hide in the split (in the library,
-// 1 GiB read flush: bf16 rows of 65,536 90.6 vs 93.2 us split, of 40,960
-// 59.1 vs 64.9 us, f32 rows of 32,768 91.9 vs 92.5 us). Unaligned or
-// ragged rows take the scalar kernel.
+// form's early residual_out stores hide in the split. A sweep of both forms
+// (bf16 and f32 rows of 4097, 5120, 6144, 7168 and 8192 vectors, 1-4096
+// rows, back to back and after a 1 GiB read flush) put the split ahead
+// only for rows of 8192 vectors (by up to 15 % at 1-64 rows, where four
+// workgroups per row pull it from HBM in parallel); with the threshold at
+// 7168 vectors the policy's form is within 10.3 % of the faster one at
+// every point (0.8 % on average), against 15 % with the 1024-lane form up to 8192
+// vectors and 25 % with the split for all of them. Unaligned or ragged rows
+// take the scalar kernel.
 Role rn_role(uint32_t dtype, int64_t H, unsigned flags, int64_t T, uint32_t bucket, bool res) {
   const int64_t v = vec_elems(dtype);
   if (!(flags & kAlign) || H % v) return {RN_SCALAR, uint32_t(T)};
@@ -83,7 +88,7 @@ Role rn_role(uint32_t dtype, int64_t H, unsigned flags, int64_t T, uint32_t buck
   if (nvec <= 128) return {nvec <= 64 ? RN_WAVE_1 : RN_WAVE_2, uint32_t(cdiv(T, 4))};
   const int64_t nb = next_pow2(cdiv(nvec, 256));
   if (nb <= 16) return {RN_BLOCK_1 + pow2_index(nb), uint32_t(T)};
-  if (!res && nvec <= kWideRowVecs) return {RN_WIDE, uint32_t(T)};
+  if (!res && nvec <= kWidePlainVecs) return {RN_WIDE, uint32_t(T)};
   if (split_fits(dtype, H, bucket)) return {RN_SPLIT, uint32_t(T * split_slices(dtype, H))};
   if (nvec <= kWideRowVecs) return {RN_WIDE, uint32_t(T)};
   return {RN_LOOP, uint32_t(T)};
@@ -423,8 +428,8 @@ bool norm_h_range(uint32_t dt, uint32_t H, unsigned fl, bool res, Guard *g) {
     const int64_t nb = next_pow2(cdiv(n, 256));
     lo = nb == 1 ? 129 : 128 * nb + 1;
     hi = 256 * nb;
-  } else if (!res && n <= kWideRowVecs) {
-    lo = 4097, hi = kWideRowVecs;
+  } else if (!res && n <= kWidePlainVecs) {
+    lo = 4097, hi = kWidePlainVecs;
   } else {
     return false;
   }

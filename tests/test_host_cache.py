@@ -826,13 +826,14 @@ def _last_launch(lib, nbytes=512, size=None):
 def test_long_rows_launch_split_wide_and_loop_forms(lib, fresh):
     """Residual rows beyond 4096 vectors are split over S = ceil(vectors /
     2048) workgroups of 256 (standalone, and as the norm launch of a
-    three-launch chain), plain rows beyond 8192 vectors too; plain rows of
-    4097..8192 vectors take one 1024-work-item workgroup, and so do residual
-    ones where the split's scratch for the key's bucket would be too large;
-    longer rows make two passes. Launches and records match the model's
-    plan."""
+    three-launch chain), plain rows beyond 7168 vectors too; plain rows of
+    4097..7168 vectors take one 1024-work-item workgroup, and so do rows of
+    up to 8192 vectors where the split's scratch for the key's bucket would
+    be too large; longer rows make two passes. Launches and records match
+    the model's plan."""
     cache = fresh(flags=S.FLAG_AUTO_INSTALL)
-    cases = [(rn_call(BF, 3, 65536), [S.RN_WIDE]), (res_call(BF, 3, 65536), [S.RN_SPLIT]),
+    cases = [(rn_call(BF, 3, 65536), [S.RN_SPLIT]), (rn_call(BF, 3, 57344), [S.RN_WIDE]),
+             (res_call(BF, 3, 65536), [S.RN_SPLIT]),
              (res_call(F, 2, 20480), [S.RN_SPLIT]), (rn_call(F, 2, 20480), [S.RN_WIDE]),
              (rn_call(BF, 3, 65544), [S.RN_SPLIT]), (rn_call(BF, 3, 32768), [S.RN_BLOCK[16]]),
              (rn_call(BF, 3, 1048584), [S.RN_LOOP]),
