@@ -98,8 +98,13 @@ enum {
   TRI_CACHE_AUTO_INSTALL = 1u,   /* on a miss: install, then launch */
   TRI_CACHE_JIT = 2u,            /* install compiles a key-specialized kernel */
   TRI_CACHE_AUTOTUNE = 4u,       /* install times the key's candidate plans */
-  TRI_CACHE_GENERIC = 8u         /* a miss installs a generic (range) version */
+  TRI_CACHE_GENERIC = 8u,        /* a miss installs a generic (range) version */
+  TRI_CACHE_RESIDENT_ARGS = 16u  /* fused-chain argument blocks held on the device */
 };
+
+/* Resident argument blocks (TRI_CACHE_RESIDENT_ARGS): blocks per device and
+ * dtype, and the largest fused-chain launch (workgroups) that uses one. */
+enum { TRI_RESIDENT_SLOTS = 40, TRI_RESIDENT_MAX_GRID = 512 };
 
 /* Divisibility class of a generic version's hidden-size range
  * (tri_version_info.h_mod). */
@@ -252,7 +257,8 @@ typedef struct tri_chain_args {
 
 /* Create an empty cache on the current device. capacity 0 selects 256
  * (at most 4096); flags: TRI_CACHE_AUTO_INSTALL, TRI_CACHE_JIT,
- * TRI_CACHE_AUTOTUNE and TRI_CACHE_GENERIC in any combination. The
+ * TRI_CACHE_AUTOTUNE, TRI_CACHE_GENERIC and TRI_CACHE_RESIDENT_ARGS in any
+ * combination. The
  * cache owns every version, its kernel handles (and, with TRI_CACHE_JIT,
  * its loaded code objects) and its device constants; release it with
  * tri_spec_cache_destroy. Errors: INVALID (NULL out, capacity or flags out
@@ -310,6 +316,34 @@ typedef struct tri_chain_args {
  * version already matches installs nothing (a version behind it could
  * never run). With TRI_CACHE_JIT, a version with a hidden-size range runs
  * the precompiled kernels (a compiled specialization fixes H). */
+/* TRI_CACHE_RESIDENT_ARGS (not in the paper; it removes part of the
+ * per-call launch cost the paper measures in Sec. 2.3): the runtime places
+ * a launch's kernel arguments in device memory on every launch, which costs
+ * about as much host and end-to-end time as the 1-token chain's whole
+ * kernel. With this flag a fused-chain launch of at most
+ * TRI_RESIDENT_MAX_GRID workgroups by a precompiled version takes its
+ * argument block from a table in device memory instead: the first call with
+ * a given block (every pointer, stride, size, eps and the launch geometry
+ * equal) copies it into a free slot of the device's table for the dtype
+ * (TRI_RESIDENT_SLOTS per device and dtype, shared by the process's
+ * caches), synchronously on a private stream; every later call with an
+ * equal block launches a form of the same kernel that takes no kernel
+ * arguments and finds its slot through its own LDS allocation (the call
+ * requests slot x 1280 bytes of dynamic LDS, which the kernel reads back
+ * from a hardware register). Pointers are held, not the data behind them:
+ * positions, activations and weights are read on every call. Outputs equal
+ * the ordinary launch's bit for bit, and the selection records are the
+ * same. A held block is never rewritten while the cache lives; slots return
+ * to the device's pool when the cache is destroyed (after the device has
+ * finished its work). Calls launch as without the flag (kernel arguments)
+ * when the cache holds TRI_RESIDENT_SLOTS blocks of the dtype or the pool
+ * has none free, when the block is new while the caller's stream is being
+ * captured, for compiled specializations (TRI_CACHE_JIT), three-launch
+ * plans and larger grids, and on a device that fails the check made at
+ * creation (launches at several LDS sizes whose slot the kernel must read
+ * back exactly). tri_spec_resident_info tells how many launches used a held
+ * block. A first call with a new block synchronizes a private stream:
+ * make it before another thread starts a global-mode stream capture. */
 tri_status tri_spec_cache_create(tri_cache **out, uint32_t capacity, uint32_t flags);
 /* Release a cache and everything it owns (versions, kernel handles, loaded
  * code objects, device constants and scratch). Not in the paper (its module
@@ -524,6 +558,18 @@ tri_status tri_spec_last_selection(const tri_cache *cache, tri_selection *out);
  * the hit rate of Sec. 3.5's three paths. Not in the paper as an interface.
  * INVALID for NULL arguments. */
 tri_status tri_spec_stats(const tri_cache *cache, tri_stats *out);
+
+/* Resident argument blocks of a cache (TRI_CACHE_RESIDENT_ARGS). */
+typedef struct tri_resident_info {
+  int32_t enabled;      /* 1: the flag is set and the device passed the check */
+  uint32_t held;        /* blocks the cache holds (both dtypes)              */
+  uint64_t launches;    /* launches that took a held block                   */
+} tri_resident_info;
+
+/* Copy the cache's resident-block state. Not in the paper: introspection
+ * of TRI_CACHE_RESIDENT_ARGS (all zero without the flag). INVALID for NULL
+ * arguments. */
+tri_status tri_spec_resident_info(const tri_cache *cache, tri_resident_info *out);
 
 /* Describe version `index` (creation order; the versions of Algorithm 1).
  * Not in the paper: introspection. INVALID if out of range. */

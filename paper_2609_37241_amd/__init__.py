@@ -201,18 +201,22 @@ class SpecCache:
 
     def __init__(self, capacity: int = 0, auto_install: bool = False, jit: bool = False,
                  code_dir: Optional[str] = None, autotune: bool = False,
-                 generic: bool = False):
+                 generic: bool = False, resident_args: bool = False):
         """jit: installs compile key-specialized kernels with hipRTC; autotune:
         installs time the key's candidate plans and keep the fastest; code_dir:
         a directory of compiled code objects and tuning results shared across
         processes; generic: a miss installs a generic version that also
-        serves the token buckets (and norm row lengths) with the same plan."""
+        serves the token buckets (and norm row lengths) with the same plan;
+        resident_args: fused-chain launches at decode sizes take their
+        argument block from a table in device memory (written on the first
+        call with that block) instead of kernel arguments."""
         h = C.c_void_p()
         st = _dll.tri_spec_cache_create(C.byref(h), capacity,
                                         (AUTO_INSTALL if auto_install else 0)
                                         | (L.JIT if jit else 0)
                                         | (L.AUTOTUNE if autotune else 0)
-                                        | (L.GENERIC if generic else 0))
+                                        | (L.GENERIC if generic else 0)
+                                        | (L.RESIDENT_ARGS if resident_args else 0))
         if st != OK:
             raise TriError(st, "tri_spec_cache_create")
         self._h = h
@@ -580,6 +584,13 @@ class SpecCache:
         s = Stats()
         _dll.tri_spec_stats(self._h, C.byref(s))
         return s.as_dict()
+
+    def resident_info(self) -> dict:
+        r = L.ResidentInfo()
+        st = _dll.tri_spec_resident_info(self._h, C.byref(r))
+        if st != OK:
+            raise TriError(st, "tri_spec_resident_info")
+        return {"enabled": r.enabled, "held": r.held, "launches": r.launches}
 
     def version_info(self, i: int) -> VersionInfo:
         v = VersionInfo()

@@ -24,6 +24,8 @@ AUTO_INSTALL = 1
 JIT = 2
 AUTOTUNE = 4
 GENERIC = 8
+RESIDENT_ARGS = 16
+RESIDENT_SLOTS, RESIDENT_MAX_GRID = 40, 512
 TUNE_NONE, TUNE_MEASURED, TUNE_STORED, TUNE_SKIPPED = 0, 1, 2, 3
 KEY_WORDS = 6
 NOALLOC_SCRATCH_BYTES = 1 << 20
@@ -54,6 +56,10 @@ class Stats(C.Structure):
 
     def as_dict(self):
         return {n: getattr(self, n) for n, _ in self._fields_}
+
+
+class ResidentInfo(C.Structure):
+    _fields_ = [("enabled", C.c_int32), ("held", C.c_uint32), ("launches", C.c_uint64)]
 
 
 class VersionInfo(C.Structure):
@@ -95,7 +101,7 @@ class ChainArgs(C.Structure):
 
 
 assert C.sizeof(Selection) == 120 and C.sizeof(ChainArgs) == 240 and C.sizeof(RopeExt) == 48
-assert C.sizeof(VersionInfo) == 144
+assert C.sizeof(VersionInfo) == 144 and C.sizeof(ResidentInfo) == 16
 
 _P, _I64, _I32, _F, _U32 = C.c_void_p, C.c_int64, C.c_int32, C.c_float, C.c_uint32
 
@@ -129,6 +135,7 @@ SIGNATURES = {
     "tri_spec_install_last_miss": (C.c_int, [_P, C.POINTER(Selection)]),
     "tri_spec_last_selection": (C.c_int, [_P, C.POINTER(Selection)]),
     "tri_spec_stats": (C.c_int, [_P, C.POINTER(Stats)]),
+    "tri_spec_resident_info": (C.c_int, [_P, C.POINTER(ResidentInfo)]),
     "tri_spec_version_info": (C.c_int, [_P, _U32, C.POINTER(VersionInfo)]),
     "tri_spec_version_constants": (C.c_int, [_P, _U32, C.POINTER(C.c_float), _U32,
                                              C.POINTER(C.c_uint32)]),

@@ -325,11 +325,13 @@ int chain_check(const tri_chain_args *p, Key *out) {
   return kGo;
 }
 
-// The launches of one chain call on version v: one fused launch, or the
-// three role kernels in order (stopping at the first failure). l receives
-// the launch records, *n their count. Returns 0 or the failing launch's code.
-int chain_launch(const Version &v, const tri_chain_args &p, void *stream, tri_launch_rec *l,
-                 int *n) {
+// The launches of one chain call on version v of cache c: one fused launch
+// (from a resident argument block when the version has the argument-free
+// form and the cache holds or can hold the block), or the three role
+// kernels in order (stopping at the first failure). l receives the launch
+// records, *n their count. Returns 0 or the failing launch's code.
+int chain_launch(tri_cache *c, const Version &v, const tri_chain_args &p, void *stream,
+                 tri_launch_rec *l, int *n) {
   const uint32_t dtype = uint32_t(p.dtype);
   const int64_t T = p.T, I = p.I;
   const tri_rope_ext &x = p.rope_ext ? *p.rope_ext : kRopePlain;
@@ -347,9 +349,18 @@ int chain_launch(const Version &v, const tri_chain_args &p, void *stream, tri_la
 
   if (v.plan.variant == CH_FUSED) {
     const ChainArgs a{rn, ro, sw, g0, g1};
-    l[0] = {CH_FUSED, g0 + g1 + g2, kBlock};
+    const uint32_t grid = g0 + g1 + g2;
+    l[0] = {CH_FUSED, grid, kBlock};
     *n = 1;
-    return be_launch(v.fn[0], l[0].grid_x, kBlock, &a, sizeof a, stream);
+    if (v.fn_res && grid <= kResidentMaxGrid) {
+      const int32_t slot = resident_slot(c, dtype, a, grid, stream);
+      if (slot >= 0) {
+        const int rc = be_launch_resident(v.fn_res, grid, kBlock, uint32_t(slot), stream);
+        if (rc == 0) c->resident_launches++;
+        return rc;
+      }
+    }
+    return be_launch(v.fn[0], grid, kBlock, &a, sizeof a, stream);
   }
   // Three launches: the residual norm, RoPE and SwiGLU role kernels (a
   // split norm role takes the version's scratch with its rows).
@@ -529,7 +540,7 @@ tri_status layers_launch(tri_cache *c, const tri_chain_args *layers, uint32_t n_
     Version &v = c->versions[lp.vis[i]];
     tri_launch_rec l[3];
     int n = 0;
-    const int rc = chain_launch(v, layers[i], stream, l, &n);
+    const int rc = chain_launch(c, v, layers[i], stream, l, &n);
     total += n;
     if (rc != 0 || int32_t(i) == lp.last) {
       Key k;
@@ -778,7 +789,7 @@ tri_status tri_decode_chain(tri_cache *c, const tri_chain_args *p, void *stream)
   Version &v = c->versions[vi];
   tri_launch_rec l[3];
   int n = 0;
-  const int rc = chain_launch(v, *p, stream, l, &n);
+  const int rc = chain_launch(c, v, *p, stream, l, &n);
   record(c, op, v, vi, k, n, l, rc ? TRI_E_LAUNCH : TRI_OK);
   return finish(c, v, auto_inst, rc);
 }

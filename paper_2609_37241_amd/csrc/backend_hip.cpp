@@ -11,6 +11,8 @@
 #include <stdio.h>
 #include <stdlib.h>
 
+#include <mutex>
+
 #include "internal.h"
 
 namespace tri {
@@ -23,6 +25,11 @@ const void *chain_kernel_bf16(int32_t sub);
 const void *empty_kernel();
 const void *elt_kernel(int32_t variant, uint32_t dtype, int32_t op);
 const void *emb_kernel(int32_t variant, uint32_t dtype);
+const void *chain_kernel_resident_f32(int32_t sub);
+const void *chain_kernel_resident_bf16(int32_t sub);
+int chain_resident_table_f32(int device, void **ptr);
+int chain_resident_table_bf16(int device, void **ptr);
+int resident_check();
 
 int be_init(int *device) {
   int n = 0;
@@ -64,6 +71,87 @@ int be_launch(void *fn, uint32_t grid, uint32_t block, const void *args, uint32_
       hipModuleLaunchKernel(reinterpret_cast<hipFunction_t>(fn), grid, 1, 1, block, 1, 1, 0,
                             reinterpret_cast<hipStream_t>(stream), args ? params : nullptr, nullptr);
   return e == hipSuccess ? 0 : -1;
+}
+
+// ---- resident argument blocks ----------------------------------------------------------
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_res_mu;
+int g_res_check[kMaxDevices];             // 0: not checked; 1: passed; -1: failed
+hipStream_t g_res_stream[kMaxDevices];    // private copy stream per device
+}  // namespace
+
+// The device's table for dtype, once the device has passed the check of the
+// LDS channel (made once per device, with it current).
+int be_resident_table(int device, uint32_t dtype, void **table) {
+  *table = nullptr;
+  if (device < 0 || device >= kMaxDevices) return TRI_E_RUNTIME;
+  {
+    std::lock_guard<std::mutex> lock(g_res_mu);
+    if (g_res_check[device] == 0) g_res_check[device] = resident_check() == 0 ? 1 : -1;
+    if (g_res_check[device] != 1) return TRI_E_RUNTIME;
+  }
+  if (dtype == TRI_F32) return chain_resident_table_f32(device, table);
+  if (dtype == TRI_BF16) return chain_resident_table_bf16(device, table);
+  return TRI_E_RUNTIME;
+}
+
+int be_resolve_resident(uint32_t dtype, int32_t ksub, void **fn) {
+  const void *sym = dtype == TRI_F32    ? chain_kernel_resident_f32(ksub)
+                    : dtype == TRI_BF16 ? chain_kernel_resident_bf16(ksub)
+                                        : nullptr;
+  if (!sym) return TRI_E_RUNTIME;
+  hipFunction_t f = nullptr;
+  if (hipGetFuncBySymbol(&f, sym) != hipSuccess || !f) return TRI_E_RUNTIME;
+  *fn = reinterpret_cast<void *>(f);
+  return 0;
+}
+
+// A copy into `device`'s table on that device's private stream, complete
+// when this returns (the caller's streams are not touched).
+int be_resident_write(int device, void *dst, const void *src, uint32_t bytes) {
+  if (device < 0 || device >= kMaxDevices) return TRI_E_RUNTIME;
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess) return TRI_E_RUNTIME;
+  if (cur != device && hipSetDevice(device) != hipSuccess) return TRI_E_RUNTIME;
+  int st = 0;
+  {
+    std::lock_guard<std::mutex> lock(g_res_mu);
+    hipStream_t &s = g_res_stream[device];
+    if (!s && hipStreamCreateWithFlags(&s, hipStreamNonBlocking) != hipSuccess) {
+      s = nullptr;
+      st = TRI_E_RUNTIME;
+    }
+    if (st == 0 && (hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, s) != hipSuccess ||
+                    hipStreamSynchronize(s) != hipSuccess))
+      st = TRI_E_RUNTIME;
+  }
+  if (cur != device) (void)hipSetDevice(cur);
+  return st;
+}
+
+// No kernel arguments: the slot travels as the dynamic LDS size.
+int be_launch_resident(void *fn, uint32_t grid, uint32_t block, uint32_t slot, void *stream) {
+  if (slot >= kResidentSlots) return -1;
+  const hipError_t e = hipModuleLaunchKernel(reinterpret_cast<hipFunction_t>(fn), grid, 1, 1,
+                                             block, 1, 1, slot * kLdsGranule,
+                                             reinterpret_cast<hipStream_t>(stream), nullptr,
+                                             nullptr);
+  return e == hipSuccess ? 0 : -1;
+}
+
+int be_stream_capturing(void *stream) {
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(reinterpret_cast<hipStream_t>(stream), &cs) != hipSuccess) return 1;
+  return cs == hipStreamCaptureStatusNone ? 0 : 1;
+}
+
+void be_device_sync(int device) {
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess) return;
+  if (cur != device && hipSetDevice(device) != hipSuccess) return;
+  (void)hipDeviceSynchronize();
+  if (cur != device) (void)hipSetDevice(cur);
 }
 
 int be_upload(const void *host, uint64_t bytes, void **dev) {

@@ -118,7 +118,7 @@ int trib_hostcost(const int32_t *ns, int32_t nn, double *out) {
   const double launch_ns = ns_per([&](int) {
     tri_launch_rec l[3];
     int n = 0;
-    g_sink += uint64_t(chain_launch(c->versions[vi], *g_pa, nullptr, l, &n)) + l[0].grid_x;
+    g_sink += uint64_t(chain_launch(c, c->versions[vi], *g_pa, nullptr, l, &n)) + l[0].grid_x;
   }, N);
   const double entry_ns = ns_per([&](int) { g_sink += uint64_t(tri_decode_chain(c, g_pa, nullptr)); }, N);
   out[0] = check_ns - key_ns;

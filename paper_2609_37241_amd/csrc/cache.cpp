@@ -270,6 +270,11 @@ tri_status install_key(tri_cache *c, const Key &k, int32_t candidate, bool gener
         return tri_status(st);
       }
     }
+    // the argument-free form of a fused chain, for resident argument blocks
+    // (without it the version launches with kernel arguments)
+    if (dt <= 1 && c->rtable[dt] && v.plan.variant == CH_FUSED &&
+        be_resolve_resident(dt, v.plan.ksub[0], &v.fn_res) != 0)
+      v.fn_res = nullptr;
   }
   c->versions[c->n_versions++] = v;
   c->stats.installs++;
@@ -317,7 +322,7 @@ tri_status tri_spec_cache_create(tri_cache **out, uint32_t capacity, uint32_t fl
   *out = nullptr;
   if (capacity > kMaxCapacity ||
       (flags & ~uint32_t(TRI_CACHE_AUTO_INSTALL | TRI_CACHE_JIT | TRI_CACHE_AUTOTUNE |
-                         TRI_CACHE_GENERIC)))
+                         TRI_CACHE_GENERIC | TRI_CACHE_RESIDENT_ARGS)))
     return TRI_E_INVALID;
   if (capacity == 0) capacity = kDefaultCapacity;
   int device = 0;
@@ -344,6 +349,19 @@ tri_status tri_spec_cache_create(tri_cache **out, uint32_t capacity, uint32_t fl
   // the allocation-free entry point's fixed scratch on this device (a
   // failed lookup only disables the split rows of that entry point)
   if (be_noalloc_scratch(device, &c->noalloc_scratch) != 0) c->noalloc_scratch = nullptr;
+  // resident argument blocks: the device's tables (a failed lookup or
+  // check leaves the flag without effect)
+  if (flags & TRI_CACHE_RESIDENT_ARGS) {
+    c->held = static_cast<ResidentChain *>(calloc(2 * kResidentSlots, sizeof(ResidentChain)));
+    if (!c->held) {
+      free(c->versions);
+      free(c->memo);
+      free(c);
+      return TRI_E_NOMEM;
+    }
+    for (uint32_t dt : {uint32_t(TRI_F32), uint32_t(TRI_BF16)})
+      if (be_resident_table(device, dt, &c->rtable[dt]) != 0) c->rtable[dt] = nullptr;
+  }
   c->capacity = capacity;
   c->flags = flags;
   c->device = device;
@@ -356,6 +374,8 @@ tri_status tri_spec_cache_create(tri_cache **out, uint32_t capacity, uint32_t fl
 
 void tri_spec_cache_destroy(tri_cache *c) {
   if (!c) return;
+  resident_release_all(c);
+  free(c->held);
   for (uint32_t i = 0; i < c->n_versions; ++i) {
     if (c->versions[i].d_consts) be_free(c->versions[i].d_consts);
     if (c->versions[i].d_scratch) be_free(c->versions[i].d_scratch);
@@ -387,6 +407,15 @@ tri_status tri_spec_last_selection(const tri_cache *c, tri_selection *out) {
 tri_status tri_spec_stats(const tri_cache *c, tri_stats *out) {
   if (!c || !out) return TRI_E_INVALID;
   *out = c->stats;
+  return TRI_OK;
+}
+
+tri_status tri_spec_resident_info(const tri_cache *c, tri_resident_info *out) {
+  if (!c || !out) return TRI_E_INVALID;
+  memset(out, 0, sizeof *out);
+  out->enabled = (c->rtable[0] || c->rtable[1]) ? 1 : 0;
+  out->held = c->n_held[0] + c->n_held[1];
+  out->launches = c->resident_launches;
   return TRI_OK;
 }
 

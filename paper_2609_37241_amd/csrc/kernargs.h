@@ -120,6 +120,21 @@ struct ChainArgs {
   uint32_t rope_blocks;
 };
 
+// A fused-chain argument block held in device memory for launches without
+// kernel arguments: the block, the launch's workgroup count and a tag that
+// marks the slot as written (kResidentTag + slot; zero until then). Slot k
+// of a device's table is found by a launch that requests k * kLdsGranule
+// bytes of dynamic LDS (the kernel reads its own LDS allocation back).
+constexpr uint32_t kResidentSlots = 40;        // per device and dtype
+constexpr uint32_t kResidentTag = 0x52455300u;
+constexpr uint32_t kLdsGranule = 1280;         // LDS allocation granule, bytes
+struct ResidentChain {
+  ChainArgs a;
+  uint32_t grid;
+  uint32_t tag;
+  uint64_t pad[3];
+};
+
 static_assert(sizeof(RnArgs) == 88 && __builtin_offsetof(RnArgs, T) == 72 &&
                   __builtin_offsetof(RnArgs, eps) == 84,
               "RnArgs layout");
@@ -133,5 +148,7 @@ static_assert(sizeof(EltArgs) == 88 && __builtin_offsetof(EltArgs, value) == 80,
 static_assert(sizeof(EmbArgs) == 72 && __builtin_offsetof(EmbArgs, ids64) == 64, "EmbArgs layout");
 static_assert(sizeof(ChainArgs) == 288 && __builtin_offsetof(ChainArgs, rn_blocks) == 280,
               "ChainArgs layout");
+static_assert(sizeof(ResidentChain) == 320 && __builtin_offsetof(ResidentChain, tag) == 292,
+              "ResidentChain layout");
 
 }  // namespace tri

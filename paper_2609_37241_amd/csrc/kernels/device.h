@@ -1359,11 +1359,15 @@ __device__ __forceinline__ void chain_norm_role(const ChainArgs &a, uint32_t blk
   }
 }
 
+//
+// `nblk` is the launch's workgroup count (gridDim.x, or the resident block's
+// count in a launch without kernel arguments, which must not read gridDim:
+// that would give the kernel implicit arguments again).
 template <int DT, bool WAVE, int N, bool NT, bool QKN, bool INTER>
-__device__ __forceinline__ void body_chain(const ChainArgs &a) {
+__device__ __forceinline__ void body_chain(const ChainArgs &a, uint32_t nblk) {
   __shared__ float lds[2 * 256 * kRopeTokensMax];
   const uint32_t b = blockIdx.x;
-  const uint32_t R = a.rn_blocks, P = a.rope_blocks, S = gridDim.x - R - P;
+  const uint32_t R = a.rn_blocks, P = a.rope_blocks, S = nblk - R - P;
   if (b < R) {
     chain_norm_role<DT, WAVE, N>(a, b);
   } else if (b < R + P) {
@@ -1371,6 +1375,65 @@ __device__ __forceinline__ void body_chain(const ChainArgs &a) {
   } else {
     sw_flat_part<DT, 1, NT>(a.sw, b - R - P, S);
   }
+}
+
+// The slot of a launch without kernel arguments. The workgroup's LDS
+// allocation is readable in the LDS_ALLOC hardware register (bits 12..20,
+// in 256-byte units; the hardware allocates whole kLdsGranule-byte
+// granules): less the granules of the kernel's static LDS, it is the slot
+// the host encoded as slot * kLdsGranule bytes of dynamic LDS. Reading a
+// register costs no memory access, unlike the dispatch packet.
+__device__ __forceinline__ uint32_t resident_slot() {
+  const uint32_t units = __builtin_amdgcn_s_getreg((8 << 11) | (12 << 6) | 6);
+  return units / (kLdsGranule / 256) -
+         (__builtin_amdgcn_groupstaticsize() + kLdsGranule - 1) / kLdsGranule;
+}
+
+template <typename P>
+__device__ __forceinline__ P *in_global(P *p) {
+  typedef __attribute__((address_space(1))) P *gptr;
+  gptr g;
+  // an empty move the compiler cannot look through: the result is a
+  // global-address-space pointer, so no cast pair folds back to flat
+  asm("" : "=s"(g) : "0"((gptr)p));
+  return (P *)g;
+}
+
+// The fused chain without kernel arguments: its block comes from slot
+// resident_slot() of `table` (a device's table in constant memory: the host
+// writes a slot only while no launch can read it). An unwritten slot or an
+// index beyond the table runs nothing.
+template <int DT, bool WAVE, int N, bool NT, bool QKN, bool INTER>
+__device__ __forceinline__ void body_chain_resident(const ResidentChain *table) {
+  const uint32_t s = resident_slot();
+  if (s >= kResidentSlots) return;
+  typedef __attribute__((address_space(4))) const uint32_t cu32;
+  cu32 *w = (cu32 *)(table + s);
+  if (w[__builtin_offsetof(ResidentChain, tag) / 4] != kResidentTag + s) return;
+  uint32_t words[sizeof(ChainArgs) / 4];
+#pragma unroll
+  for (uint32_t i = 0; i < sizeof(ChainArgs) / 4; ++i) words[i] = w[i];
+  ChainArgs a;
+  __builtin_memcpy(&a, words, sizeof a);
+  // pointers read from memory could point anywhere; these are global
+  // memory, as kernel-argument pointers are taken to be (global, not flat,
+  // loads and stores)
+  a.rn.x = in_global(a.rn.x);
+  a.rn.res = in_global(a.rn.res);
+  a.rn.w = in_global(a.rn.w);
+  a.rn.y = in_global(a.rn.y);
+  a.rn.res_out = in_global(a.rn.res_out);
+  a.rope.q = in_global(a.rope.q);
+  a.rope.k = in_global(a.rope.k);
+  a.rope.pos = in_global(a.rope.pos);
+  a.rope.inv_freq = in_global(a.rope.inv_freq);
+  a.rope.qw = in_global(a.rope.qw);
+  a.rope.kw = in_global(a.rope.kw);
+  a.rope.cos_sin = in_global(a.rope.cos_sin);
+  a.sw.gate = in_global(a.sw.gate);
+  a.sw.up = in_global(a.sw.up);
+  a.sw.out = in_global(a.sw.out);
+  body_chain<DT, WAVE, N, NT, QKN, INTER>(a, w[__builtin_offsetof(ResidentChain, grid) / 4]);
 }
 
 }  // namespace dev

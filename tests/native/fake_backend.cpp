@@ -21,6 +21,7 @@ struct Rec {
   unsigned char args[512];
   uint32_t nargs;
   void *stream;
+  int32_t slot;   // resident launch: the slot (its block is in args); -1 otherwise
 };
 
 std::vector<Rec> g_log;
@@ -33,6 +34,13 @@ int64_t g_unloads = 0;
 bool g_jit_fail = false;
 int64_t g_captures = 0, g_capture_start = 0, g_graph_launches = 0, g_graph_destroys = 0;
 bool g_capture_fail = false;
+void *g_capturing = nullptr;   // the capture stream between begin and end
+
+// Resident argument blocks: one host table per dtype stands in for the
+// device's (shared by every cache, as the device's is).
+tri::ResidentChain g_res_table[2][tri::kResidentSlots];
+bool g_res_check_fail = false, g_res_write_fail = false, g_force_capturing = false;
+int64_t g_res_writes = 0, g_res_syncs = 0;
 
 // Scripted launch costs of the tuning timer: the last matching entry wins
 // (ksub -1 / grid 0 match any); unmatched launches cost 1 ms.
@@ -87,8 +95,62 @@ int be_launch(void *fn, uint32_t grid, uint32_t block, const void *args, uint32_
   r.stream = stream;
   r.nargs = args && args_size <= sizeof r.args ? args_size : 0;
   if (r.nargs) memcpy(r.args, args, r.nargs);
+  r.slot = -1;
   g_log.push_back(r);
   return n == g_fail_at ? -1 : 0;
+}
+
+int be_resident_table(int device, uint32_t dtype, void **table) {
+  (void)device;
+  *table = nullptr;
+  if (g_res_check_fail || dtype > 1) return TRI_E_RUNTIME;
+  *table = g_res_table[dtype];
+  return 0;
+}
+
+int be_resolve_resident(uint32_t dtype, int32_t ksub, void **fn) {
+  *fn = reinterpret_cast<void *>(encode(CH_FUSED, dtype, ksub) | (uintptr_t(1) << 42));
+  return 0;
+}
+
+int be_resident_write(int device, void *dst, const void *src, uint32_t bytes) {
+  (void)device;
+  if (g_res_write_fail) return TRI_E_RUNTIME;
+  memcpy(dst, src, bytes);
+  g_res_writes++;
+  return 0;
+}
+
+// Logged like a launch with arguments, with the block the kernel would find
+// in its slot (none when the slot is out of range or its tag unset).
+int be_launch_resident(void *fn, uint32_t grid, uint32_t block, uint32_t slot, void *stream) {
+  const int64_t n = int64_t(g_log.size());
+  Rec r;
+  memset(&r, 0, sizeof r);
+  const uintptr_t h = reinterpret_cast<uintptr_t>(fn);
+  r.kvariant = int32_t((h >> 20) & 0xFFFFF);
+  r.dtype = int32_t((h >> 16) & 0xF);
+  r.ksub = int32_t(h & 0xFFFF);
+  r.grid = grid;
+  r.block = block;
+  r.stream = stream;
+  r.slot = int32_t(slot);
+  if (r.dtype <= 1 && slot < kResidentSlots &&
+      g_res_table[r.dtype][slot].tag == kResidentTag + slot) {
+    r.nargs = sizeof(ChainArgs);
+    memcpy(r.args, &g_res_table[r.dtype][slot].a, sizeof(ChainArgs));
+  }
+  g_log.push_back(r);
+  return n == g_fail_at ? -1 : 0;
+}
+
+int be_stream_capturing(void *stream) {
+  return g_force_capturing || (g_capturing && stream == g_capturing) ? 1 : 0;
+}
+
+void be_device_sync(int device) {
+  (void)device;
+  g_res_syncs++;
 }
 
 int be_upload(const void *host, uint64_t bytes, void **dev) {
@@ -160,11 +222,13 @@ int be_capture_begin(void **stream) {
   if (g_capture_fail) return TRI_E_RUNTIME;
   *stream = reinterpret_cast<void *>(uintptr_t(0xCA000000u) + uintptr_t(g_captures++));
   g_capture_start = int64_t(g_log.size());
+  g_capturing = *stream;
   return 0;
 }
 
 int be_capture_end(void *stream, void **exec) {
   (void)stream;
+  g_capturing = nullptr;
   *exec = reinterpret_cast<void *>(uintptr_t(0xE0000000u) +
                                    uintptr_t(int64_t(g_log.size()) - g_capture_start));
   return 0;
@@ -264,6 +328,29 @@ void trifake_reset() {
   g_zero_bytes = 0;
   tri::g_noalloc_lookups = 0;
   g_arch = "fake";
+  g_capturing = nullptr;
+  g_res_check_fail = g_res_write_fail = g_force_capturing = false;
+  g_res_writes = g_res_syncs = 0;
+}
+// resident blocks: make the device check fail / the block copy fail /
+// every stream report a capture; counts of block copies and device syncs
+void trifake_resident_check_fail(int on) { g_res_check_fail = on != 0; }
+void trifake_resident_write_fail(int on) { g_res_write_fail = on != 0; }
+void trifake_force_capturing(int on) { g_force_capturing = on != 0; }
+void trifake_resident_counts(int64_t *out) {
+  out[0] = g_res_writes;
+  out[1] = g_res_syncs;
+}
+// the stand-in table's slot s of dtype: its tag and grid (-1 out of range)
+int64_t trifake_resident_tag(int32_t dtype, int32_t s, uint32_t *grid) {
+  if (dtype < 0 || dtype > 1 || s < 0 || s >= int32_t(tri::kResidentSlots)) return -1;
+  if (grid) *grid = g_res_table[dtype][s].grid;
+  return int64_t(g_res_table[dtype][s].tag);
+}
+// slot of launch i (-1: a launch with arguments), or -2 if there is no launch i
+int32_t trifake_slot(int64_t i) {
+  if (i < 0 || i >= int64_t(g_log.size())) return -2;
+  return g_log[size_t(i)].slot;
 }
 // address of the fixed scratch of the allocation-free entry point, and the
 // lookups made

@@ -38,7 +38,8 @@ def ensure_libtri() -> str:
 def ensure_fake() -> str:
     srcs = [FAKE_SRC] + [os.path.join(PKG, "csrc", n)
                          for n in ("api.cpp", "cache.cpp", "policy.cpp", "jit.cpp", "tune.cpp",
-                                   "internal.h", "kernargs.h", "kernels/device.h")]
+                                   "resident.cpp", "internal.h", "kernargs.h",
+                                   "kernels/device.h")]
     out = FAKE_ASAN_LIB if SANITIZE else FAKE_LIB
     stale = (not os.path.exists(out)
              or any(os.path.getmtime(s) > os.path.getmtime(out) for s in srcs))
@@ -81,4 +82,12 @@ def load_fake():
                                 C.POINTER(C.c_int32), C.POINTER(C.c_uint32),
                                 C.POINTER(C.c_uint32), C.POINTER(C.c_void_p),
                                 C.c_char_p, C.c_int]
+    lib.trifake_resident_check_fail.argtypes = [C.c_int]
+    lib.trifake_resident_write_fail.argtypes = [C.c_int]
+    lib.trifake_force_capturing.argtypes = [C.c_int]
+    lib.trifake_resident_counts.argtypes = [C.POINTER(C.c_int64)]
+    lib.trifake_resident_tag.argtypes = [C.c_int32, C.c_int32, C.POINTER(C.c_uint32)]
+    lib.trifake_resident_tag.restype = C.c_int64
+    lib.trifake_slot.argtypes = [C.c_int64]
+    lib.trifake_slot.restype = C.c_int32
     return lib

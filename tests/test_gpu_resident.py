@@ -1,0 +1,232 @@
+"""GPU: fused-chain launches from resident argument blocks
+(TRI_CACHE_RESIDENT_ARGS) against the ordinary launches and the CPU oracle.
+
+A resident launch takes no kernel arguments and finds its block in the
+device's table through its LDS allocation; its outputs must equal an
+ordinary launch's bit for bit, follow the data behind the held pointers on
+every call, and stay right when a slot is rewritten for another cache or a
+hit is replayed from a graph.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import ops as O
+from tests.parity import binding_rope_ext, check
+from tests.test_gpu_parity import CHAIN_CFGS, DEV, chain_oracle, host
+import workloads as wl
+
+pytestmark = pytest.mark.gpu
+SLOTS = 40
+
+
+@pytest.fixture(scope="module")
+def tri():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2609_37241_amd as tri
+    return tri
+
+
+def make_cache(tri, **kw):
+    return tri.SpecCache(auto_install=True, **kw)
+
+
+def device_inputs(cfg, seed=None):
+    inp = wl.host_inputs(cfg) if seed is None else wl.host_inputs(cfg, seed=seed)
+    d = {k: wl.to_torch(v, cfg.dtype, DEV) for k, v in inp.items()}
+    d["y"], d["res_out"] = torch.empty_like(d["x"]), torch.empty_like(d["x"])
+    d["out"] = torch.empty_like(d["gate"])
+    return inp, d
+
+
+def args_of(tri, cache, cfg, d):
+    rope = binding_rope_ext(tri, cfg.rope_ext) if cfg.rope_ext else None
+    a, _ = cache.chain_args(d["x"], d["residual"], d["w"], d["q"], d["k"], d["pos"], d["gate"],
+                            d["up"], cfg.eps, cfg.base, y=d["y"], residual_out=d["res_out"],
+                            out=d["out"], q_norm_w=d.get("q_norm_w"),
+                            k_norm_w=d.get("k_norm_w"), rope=rope)
+    return a
+
+
+def same_outputs(tag, a, b, dtype):
+    for n in ("y", "res_out", "q", "k", "out"):
+        check(f"{tag} {n}", host(a[n]), host(b[n]), dtype, exact=True)
+
+
+def test_the_device_passes_the_lds_channel_check(tri):
+    c = make_cache(tri, resident_args=True)
+    try:
+        assert c.resident_info() == {"enabled": 1, "held": 0, "launches": 0}
+    finally:
+        c.close()
+
+
+@pytest.mark.parametrize("cfg", CHAIN_CFGS, ids=lambda c: c.name)
+def test_resident_chain_equals_ordinary_and_oracle(tri, cfg):
+    inp, a = device_inputs(cfg)
+    b = {k: v.clone() for k, v in a.items()}
+    q0, k0 = a["q"].clone(), a["k"].clone()
+    plain, res = make_cache(tri), make_cache(tri, resident_args=True)
+    try:
+        aa, ab = args_of(tri, plain, cfg, a), args_of(tri, res, cfg, b)
+        for call in range(3):
+            if call:
+                for d in (a, b):                      # undo the in-place rotation
+                    d["q"].copy_(q0)
+                    d["k"].copy_(k0)
+            plain.decode_chain_args(aa)
+            res.decode_chain_args(ab)
+            torch.cuda.synchronize()
+            same_outputs(f"call {call}", b, a, cfg.dtype)
+            assert res.last_selection().as_tuple() == plain.last_selection().as_tuple()
+        assert res.resident_info() == {"enabled": 1, "held": 1, "launches": 3}
+        assert plain.resident_info()["launches"] == 0
+        want = chain_oracle(inp, cfg)
+        for n in ("y", "q", "k", "out"):
+            check(n, host(b[n]), want[n], cfg.dtype)
+        check("res_out", host(b["res_out"]), want["res_out"], cfg.dtype, exact=True)
+    finally:
+        torch.cuda.synchronize()
+        plain.close()
+        res.close()
+
+
+def test_resident_blocks_read_new_data_on_every_call(tri):
+    """Only pointers are held: new positions, activations and weights written
+    into the same tensors give the oracle's result for the new data."""
+    cfg = wl.LLAMA7B_DECODE
+    _, d = device_inputs(cfg)
+    c = make_cache(tri, resident_args=True)
+    try:
+        a = args_of(tri, c, cfg, d)
+        for step in range(5):
+            inp = wl.host_inputs(cfg, seed=500 + step)
+            for k in ("x", "residual", "w", "q", "k", "pos", "gate", "up"):
+                d[k].copy_(wl.to_torch(inp[k], cfg.dtype, DEV))
+            torch.cuda.synchronize()
+            c.decode_chain_args(a)
+            torch.cuda.synchronize()
+            want = O.decode_chain(inp, cfg.eps, cfg.base, cfg.dtype)
+            for n in ("y", "q", "k", "out"):
+                check(f"step {step} {n}", host(d[n]), want[n], cfg.dtype)
+            check(f"step {step} res_out", host(d["res_out"]), want["res_out"], cfg.dtype,
+                  exact=True)
+        assert c.resident_info() == {"enabled": 1, "held": 1, "launches": 5}
+    finally:
+        torch.cuda.synchronize()
+        c.close()
+
+
+def _layer_stack(tri, cache, cfg, n, seed):
+    """n dependent layers (layer l + 1 reads layer l's residual output)."""
+    layers, args = [], []
+    prev = None
+    for l in range(n):
+        _, d = device_inputs(cfg, seed=seed + l)
+        if prev is not None:
+            d["residual"] = prev
+        args.append(args_of(tri, cache, cfg, d))
+        layers.append(d)
+        prev = d["res_out"]
+    return layers, args
+
+
+def test_more_layers_than_slots_match_ordinary_layers(tri):
+    """45 layers: the first 40 blocks are held, the last 5 launch with kernel
+    arguments; two steps, every output equal to an ordinary cache's."""
+    cfg = wl.GQA_DECODE
+    n = SLOTS + 5
+    plain, res = make_cache(tri), make_cache(tri, resident_args=True)
+    try:
+        la, aa = _layer_stack(tri, plain, cfg, n, 700)
+        lb, ab = _layer_stack(tri, res, cfg, n, 700)
+        for step in range(2):
+            if step:
+                for l in range(n):
+                    fresh = wl.host_inputs(cfg, seed=900 + l)
+                    for k in ("x", "q", "k", "gate", "up"):
+                        src = wl.to_torch(fresh[k], cfg.dtype, DEV)
+                        la[l][k].copy_(src)
+                        lb[l][k].copy_(src)
+                torch.cuda.synchronize()
+            plain.decode_chain_layers(aa)
+            res.decode_chain_layers(ab)
+            torch.cuda.synchronize()
+            for l in range(n):
+                same_outputs(f"step {step} layer {l}", lb[l], la[l], cfg.dtype)
+        info = res.resident_info()
+        assert info["held"] == SLOTS and info["launches"] == 2 * SLOTS
+    finally:
+        torch.cuda.synchronize()
+        plain.close()
+        res.close()
+
+
+def test_a_freed_slot_serves_another_cache(tri):
+    """Cache A holds slot blocks for its buffers and is destroyed; cache B's
+    block is then written into a freed slot: B's outputs are B's data's."""
+    cfg = wl.LLAMA7B_DECODE
+    inp_a, da = device_inputs(cfg, seed=41)
+    inp_b, db = device_inputs(cfg, seed=42)
+    a_cache = make_cache(tri, resident_args=True)
+    a_cache.decode_chain_args(args_of(tri, a_cache, cfg, da))
+    torch.cuda.synchronize()
+    assert a_cache.resident_info()["launches"] == 1
+    a_cache.close()
+    b_cache = make_cache(tri, resident_args=True)
+    try:
+        b_cache.decode_chain_args(args_of(tri, b_cache, cfg, db))
+        torch.cuda.synchronize()
+        assert b_cache.resident_info() == {"enabled": 1, "held": 1, "launches": 1}
+        want = O.decode_chain(inp_b, cfg.eps, cfg.base, cfg.dtype)
+        for n in ("y", "q", "k", "out"):
+            check(n, host(db[n]), want[n], cfg.dtype)
+        want_a = O.decode_chain(inp_a, cfg.eps, cfg.base, cfg.dtype)
+        for n in ("y", "out"):
+            check(f"A {n}", host(da[n]), want_a[n], cfg.dtype)
+    finally:
+        torch.cuda.synchronize()
+        b_cache.close()
+
+
+def test_resident_hit_replays_from_a_hip_graph(tri):
+    """A hit on a held block captured in a graph: replays, with eager work
+    and synchronisations in between, equal direct ordinary calls on twin
+    buffers bit for bit. A block first seen under capture is not written
+    (the captured launch carries its arguments)."""
+    cfg = wl.LLAMA7B_DECODE
+    _, A = device_inputs(cfg)
+    B = {k: v.clone() for k, v in A.items()}
+    _, C2 = device_inputs(cfg, seed=77)
+    res, plain = make_cache(tri, resident_args=True), make_cache(tri)
+    try:
+        args_a, args_b = args_of(tri, res, cfg, A), args_of(tri, plain, cfg, B)
+        args_c = args_of(tri, res, cfg, C2)
+        q0, k0 = A["q"].clone(), A["k"].clone()
+        res.decode_chain_args(args_a)              # holds A's block
+        plain.decode_chain_args(args_b)            # installs the ordinary version
+        torch.cuda.synchronize()
+        for d in (A, B):
+            d["q"].copy_(q0)
+            d["k"].copy_(k0)
+        torch.cuda.synchronize()
+        s = torch.cuda.Stream()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            res.decode_chain_args(args_a, stream=torch.cuda.current_stream())
+            res.decode_chain_args(args_c, stream=torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        assert res.resident_info()["held"] == 1    # C2's block was not written
+        check("q before replay", host(A["q"]), host(B["q"]), cfg.dtype, exact=True)
+        for step in range(4):
+            for d in (A, B):
+                d["x"].mul_(0.5).add_(0.25)
+            torch.cuda.synchronize()
+            g.replay()
+            plain.decode_chain_args(args_b)
+            torch.cuda.synchronize()
+            same_outputs(f"replay {step}", A, B, cfg.dtype)
+    finally:
+        torch.cuda.synchronize()
+        res.close()
+        plain.close()

@@ -402,7 +402,7 @@ def test_install_needs_a_miss_and_is_idempotent(lib, fresh):
 def test_create_errors(lib):
     h = C.c_void_p()
     assert lib.tri_spec_cache_create(C.byref(h), 4097, 0) == S.E_INVALID
-    assert lib.tri_spec_cache_create(C.byref(h), 0, 16) == S.E_INVALID
+    assert lib.tri_spec_cache_create(C.byref(h), 0, 32) == S.E_INVALID
     assert lib.tri_spec_cache_create(C.byref(h), 0, 3) == S.OK      # auto-install + JIT
     lib.tri_spec_cache_destroy(h)
     assert lib.tri_spec_cache_create(None, 0, 0) == S.E_INVALID
@@ -624,7 +624,7 @@ def test_jit_source_fixes_the_key_shape(lib, fresh):
     assert "tri_jit_kernel(tri::ChainArgs a)" in k
     for frag in ("a.rn.H = 4096;", "a.rope.hd = 128;", "a.rope.rd = 128;", "a.rope.nq = 32;",
                  "a.rope.nk = 8;", "a.rope.mode = 769u;", "a.sw.I = 12288;",
-                 "body_chain<1, false, 2, false, true, true>(a)"):
+                 "body_chain<1, false, 2, false, true, true>(a, gridDim.x)"):
         assert frag in k, frag
     assert src.startswith("// Kernel argument blocks")     # the embedded prelude
     assert "#include <hip/" not in src and '#include "../kernargs.h"' not in src

@@ -1,0 +1,298 @@
+"""Resident argument blocks (TRI_CACHE_RESIDENT_ARGS) on the CPU, against the
+recording backend: which launches take a held block, what block the kernel
+finds in its slot, the slot pool shared by caches, and the cases that must
+launch with kernel arguments instead (full table or pool, a captured stream,
+a failed device check or copy, large grids, three-launch plans, compiled
+specializations). Selection records and statistics stay those of the
+oracle's selection model.
+"""
+import ctypes as C
+
+import pytest
+
+from oracle import selection as S
+from tests.native_libs import load_fake
+from tests.selection_calls import chain_call, elem_offset
+from tests.test_host_cache import _chain_struct, c_call, c_layers, call_zoo, run_both
+import workloads as wl
+
+BF, F = S.DT_BF16, S.DT_F32
+AUTO, JIT, RES = 1, 2, 16
+SLOTS, MAX_GRID = 40, 512
+TAG = 0x52455300
+CHAIN_BYTES = 288
+INV_FREQ = slice(112, 120)   # RopeArgs.inv_freq inside the chain block: per-version constants
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return load_fake()
+
+
+@pytest.fixture
+def fresh(lib):
+    caches = []
+
+    def make(capacity=0, flags=0):
+        lib.trifake_reset()
+        h = C.c_void_p()
+        assert lib.tri_spec_cache_create(C.byref(h), capacity, flags) == 0
+        caches.append(h)
+        return h
+    yield make
+    for h in caches:
+        lib.tri_spec_cache_destroy(h)
+
+
+def info(lib, cache):
+    from paper_2609_37241_amd._lib import ResidentInfo
+    r = ResidentInfo()
+    assert lib.tri_spec_resident_info(cache, C.byref(r)) == 0
+    return r.enabled, r.held, r.launches
+
+
+def counts(lib):
+    out = (C.c_int64 * 2)()
+    lib.trifake_resident_counts(out)
+    return out[0], out[1]
+
+
+def launches(lib, start=0):
+    """(slot, kernel variant, dtype, sub, grid, block, argument block) of every
+    launch from `start` on (a resident launch's block is the one its slot holds)."""
+    out = []
+    for i in range(start, lib.trifake_launch_count()):
+        kv, dt, sub = C.c_int32(), C.c_int32(), C.c_int32()
+        grid, block = C.c_uint32(), C.c_uint32()
+        stream = C.c_void_p()
+        buf = C.create_string_buffer(CHAIN_BYTES)
+        assert lib.trifake_get(i, C.byref(kv), C.byref(dt), C.byref(sub), C.byref(grid),
+                               C.byref(block), C.byref(stream), buf, CHAIN_BYTES) >= 0
+        out.append((lib.trifake_slot(i), kv.value, dt.value, sub.value, grid.value,
+                    block.value, buf.raw))
+    return out
+
+
+def masked(raw):
+    return raw[:INV_FREQ.start] + raw[INV_FREQ.stop:]
+
+
+def llama(i=0, T=1, dtype=BF):
+    """The 1-token Llama-7B chain; layer i's activations sit i MiB further on."""
+    return chain_call(dtype, T, 4096, 11008, 32, 32, 128, res_off=i << 20, rope_off=i << 20,
+                      sw_off=i << 20)
+
+
+def test_resident_launch_finds_the_ordinary_block(lib, fresh):
+    c = llama()
+    plain = fresh(flags=AUTO)
+    assert c_call(lib, plain, c) == 0
+    (slot0, *ordinary, raw0), = launches(lib)
+    assert slot0 == -1
+    assert info(lib, plain) == (0, 0, 0)
+    cache = fresh(flags=AUTO | RES)
+    for _ in range(5):
+        assert c_call(lib, cache, c) == 0
+    got = launches(lib)
+    assert len(got) == 5
+    slot = got[0][0]
+    assert 0 <= slot < SLOTS
+    for s, *geom, raw in got:
+        # the same kernel variant, geometry and block, from the same slot
+        assert s == slot and geom == ordinary
+        assert masked(raw) == masked(raw0)
+    grid = C.c_uint32()
+    assert lib.trifake_resident_tag(BF, slot, C.byref(grid)) == TAG + slot
+    assert grid.value == ordinary[3]
+    assert counts(lib)[0] == 1                  # one copy, on the first call
+    assert info(lib, cache) == (1, 1, 5)
+
+
+def test_selection_parity_over_call_zoo_with_resident_blocks(lib, fresh):
+    """Records and statistics are the model's; a fused launch of at most 512
+    workgroups takes a held block while the dtype's table has room; blocks
+    are held in first-seen order and repeats find their slot again."""
+    cache = fresh(capacity=4096, flags=RES)
+    m = S.SpecCacheModel(capacity=4096)
+    for _ in range(2):
+        for c in call_zoo():
+            run_both(lib, cache, m, c)
+    held = {BF: {}, F: {}}
+    for slot, kv, dt, sub, grid, block, raw in launches(lib):
+        if kv != S.CH_FUSED or grid > MAX_GRID:
+            assert slot == -1
+            continue
+        key = (raw, grid)
+        table = held[dt]
+        if key in table:
+            assert slot == table[key]
+        elif len(table) < SLOTS:
+            assert slot >= 0 and slot not in table.values()
+            table[key] = slot
+        else:
+            assert slot == -1
+    assert held[BF] and held[F]
+    enabled, n_held, _ = info(lib, cache)
+    assert (enabled, n_held) == (1, len(held[BF]) + len(held[F]))
+    assert counts(lib)[0] == n_held
+
+
+def test_mixed_stream_with_resident_blocks(lib, fresh):
+    cache = fresh(flags=RES)
+    m = S.SpecCacheModel()
+    for T, dt, layout in wl.mixed_stream()[:3000]:
+        d = BF if dt == wl.BF16 else F
+        off = elem_offset(d) if layout == wl.LAYOUT_UNALIGNED else 0
+        pad = wl.MIXED_PAD if layout == wl.LAYOUT_STRIDED else 0
+        c = chain_call(d, T, wl.MIXED_H, wl.MIXED_I, wl.MIXED_NQ, wl.MIXED_NK, wl.MIXED_HD,
+                       res_off=off, rope_off=off, sw_off=off, res_pad=pad, rope_pad=pad,
+                       sw_pad=pad)
+        run_both(lib, cache, m, c)
+    got = launches(lib)
+    res = [g for g in got if g[0] >= 0]
+    # every small fused launch is resident (fewer distinct blocks than slots)
+    assert all(g[0] >= 0 for g in got if g[1] == S.CH_FUSED and g[4] <= MAX_GRID)
+    assert all(g[1] == S.CH_FUSED and g[4] <= MAX_GRID for g in res)
+    assert len(res) > 1500
+    assert counts(lib)[0] == info(lib, cache)[1] <= 2 * SLOTS
+
+
+def test_layers_hold_one_block_per_layer(lib, fresh):
+    cache = fresh(flags=AUTO | RES)
+    calls = [llama(i) for i in range(32)]
+    for step in range(3):
+        n0 = lib.trifake_launch_count()
+        assert c_layers(lib, cache, calls) == 0
+        got = launches(lib, n0)
+        assert [g[0] for g in got] == list(range(32))   # layer i holds slot i
+    assert counts(lib)[0] == 32
+    assert info(lib, cache) == (1, 32, 96)
+    # the single entry point finds the same slots, in any order
+    for i in (7, 3, 31, 0):
+        n0 = lib.trifake_launch_count()
+        assert c_call(lib, cache, calls[i]) == 0
+        assert launches(lib, n0)[0][0] == i
+    assert counts(lib)[0] == 32
+
+
+def test_blocks_beyond_the_table_launch_with_arguments(lib, fresh):
+    cache = fresh(flags=AUTO | RES)
+    calls = [llama(i) for i in range(SLOTS + 5)]
+    assert c_layers(lib, cache, calls) == 0
+    got = launches(lib)
+    assert [g[0] for g in got] == list(range(SLOTS)) + [-1] * 5
+    plain = {masked(g[-1]) for g in got[SLOTS:]}
+    assert len(plain) == 5                                # their own argument blocks
+    assert info(lib, cache)[:2] == (1, SLOTS)
+    # the dtypes have tables of their own
+    n0 = lib.trifake_launch_count()
+    assert c_call(lib, cache, llama(0, dtype=F)) == 0
+    assert launches(lib, n0)[0][0] == 0
+    assert info(lib, cache)[:2] == (1, SLOTS + 1)
+
+
+def test_slots_return_to_the_pool_when_the_cache_is_destroyed(lib):
+    lib.trifake_reset()
+    a, b = C.c_void_p(), C.c_void_p()
+    assert lib.tri_spec_cache_create(C.byref(a), 0, AUTO | RES) == 0
+    assert lib.tri_spec_cache_create(C.byref(b), 0, AUTO | RES) == 0
+    try:
+        assert c_layers(lib, a, [llama(i) for i in range(SLOTS)]) == 0
+        n0 = lib.trifake_launch_count()
+        assert c_call(lib, b, llama(100)) == 0            # the pool is empty
+        assert launches(lib, n0)[0][0] == -1
+        assert info(lib, b)[:2] == (1, 0)
+        syncs = counts(lib)[1]
+        lib.tri_spec_cache_destroy(a)
+        a = None
+        assert counts(lib)[1] == syncs + 1                # the device went idle first
+        n0 = lib.trifake_launch_count()
+        assert c_call(lib, b, llama(100)) == 0
+        assert launches(lib, n0)[0][0] == 0               # a freed slot, rewritten
+        grid = C.c_uint32()
+        assert lib.trifake_resident_tag(BF, 0, C.byref(grid)) == TAG
+    finally:
+        if a:
+            lib.tri_spec_cache_destroy(a)
+        lib.tri_spec_cache_destroy(b)
+    # a cache that held nothing does not wait for the device
+    lib.trifake_reset()
+    h = C.c_void_p()
+    assert lib.tri_spec_cache_create(C.byref(h), 0, RES) == 0
+    lib.tri_spec_cache_destroy(h)
+    assert counts(lib) == (0, 0)
+
+
+def test_new_blocks_are_not_written_while_the_stream_is_captured(lib, fresh):
+    cache = fresh(flags=AUTO | RES)
+    c1, c2, c3 = llama(0), llama(1), llama(2)
+    assert c_call(lib, cache, c1) == 0
+    lib.trifake_force_capturing(1)
+    assert c_call(lib, cache, c2) == 0                  # new: kernel arguments
+    assert c_call(lib, cache, c1) == 0                  # held: still resident
+    lib.trifake_force_capturing(0)
+    assert c_call(lib, cache, c2) == 0
+    assert [g[0] for g in launches(lib)] == [0, -1, 0, 1]
+    assert counts(lib)[0] == 2
+    # a graph build captures on its own stream: held layers resident, new ones not
+    from paper_2609_37241_amd._lib import ChainArgs
+    keep = []
+    arr = (ChainArgs * 3)(*[_chain_struct(c, keep) for c in (c1, c3, c2)])
+    g = C.c_void_p()
+    n0 = lib.trifake_launch_count()
+    assert lib.tri_graph_build_layers(cache, arr, 3, C.byref(g)) == 0
+    assert [x[0] for x in launches(lib, n0)] == [0, -1, 1]
+    assert counts(lib)[0] == 2
+    lib.tri_graph_destroy(g)
+
+
+def test_failed_check_or_copy_launches_with_arguments(lib, fresh):
+    lib.trifake_reset()
+    lib.trifake_resident_check_fail(1)
+    h = C.c_void_p()
+    assert lib.tri_spec_cache_create(C.byref(h), 0, AUTO | RES) == 0
+    try:
+        assert c_call(lib, h, llama()) == 0
+        assert c_call(lib, h, llama()) == 0
+        assert [g[0] for g in launches(lib)] == [-1, -1]
+        assert info(lib, h) == (0, 0, 0)
+    finally:
+        lib.tri_spec_cache_destroy(h)
+        lib.trifake_resident_check_fail(0)
+    cache = fresh(flags=AUTO | RES)
+    lib.trifake_resident_write_fail(1)
+    assert c_call(lib, cache, llama()) == 0
+    lib.trifake_resident_write_fail(0)
+    assert c_call(lib, cache, llama()) == 0
+    # the slot of the failed copy went back to the pool and is taken again
+    assert [g[0] for g in launches(lib)] == [-1, 0]
+    assert info(lib, cache) == (1, 1, 1)
+
+
+def test_only_small_fused_launches_of_precompiled_versions_are_resident(lib, fresh):
+    cache = fresh(flags=AUTO | RES)
+    m = S.SpecCacheModel(flags=S.FLAG_AUTO_INSTALL)
+    for T in (1, 8, 64, 512, 4096):
+        run_both(lib, cache, m, llama(T=T), install=False)
+    # a chain whose norm rows are split runs three launches
+    run_both(lib, cache, m, chain_call(BF, 2, 65536, 11008, 32, 32, 128), install=False)
+    got = launches(lib)
+    assert any(g[4] > MAX_GRID for g in got)
+    for slot, kv, dt, sub, grid, block, raw in got:
+        assert (slot >= 0) == (kv == S.CH_FUSED and grid <= MAX_GRID), (kv, grid)
+    assert sum(g[1] != S.CH_FUSED for g in got) == 3
+    # compiled specializations carry their arguments
+    jc = fresh(flags=AUTO | RES | JIT)
+    assert c_call(lib, jc, llama()) == 0
+    assert c_call(lib, jc, llama()) == 0
+    assert [g[0] for g in launches(lib)] == [-1, -1]
+    assert info(lib, jc) == (1, 0, 0)
+
+
+def test_resident_info_arguments(lib, fresh):
+    from paper_2609_37241_amd._lib import ResidentInfo
+    r = ResidentInfo()
+    assert lib.tri_spec_resident_info(None, C.byref(r)) == S.E_INVALID
+    cache = fresh()
+    assert lib.tri_spec_resident_info(cache, None) == S.E_INVALID
+    assert info(lib, cache) == (0, 0, 0)

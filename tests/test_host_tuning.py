@@ -392,15 +392,17 @@ def test_jit_compiles_only_the_kept_plan(lib, fresh):
     assert c_call(lib, cache, LLAMA_CHAIN) == S.OK
     (src,) = jit_sources(lib)
     # fused template: RN_BLOCK_2 norm, plain RoPE, nontemporal SwiGLU; one slice
-    assert "body_chain<1, false, 2, true, false, false>(a)" in src
+    assert "body_chain<1, false, 2, true, false, false>(a, gridDim.x)" in src
     assert "a.rope.mode = 0u;" in src
     v = info(lib, cache)
     assert (v.candidate, v.tuned, v.jit) == (3, S.TUNE_MEASURED, 1)
 
 
 def test_create_accepts_the_tuning_flag(lib):
-    # 8 is the generic-version flag; 16 and above are not flags
-    for flags, ok in ((4, True), (7, True), (15, True), (16, False), (20, False)):
+    # 8 is the generic-version flag, 16 resident argument blocks; 32 and above
+    # are not flags
+    for flags, ok in ((4, True), (7, True), (15, True), (16, True), (31, True), (32, False),
+                      (36, False)):
         h = C.c_void_p()
         st = lib.tri_spec_cache_create(C.byref(h), 0, flags)
         assert (st == 0) == ok, flags
