@@ -264,6 +264,11 @@ def host_cost():
              "argument_fill_and_launch_call", "whole_entry")
     res = {n: out[i] for i, n in enumerate(names)}
     res["scan_to_last_of_n_versions"] = {str(n): out[6 + i] for i, n in enumerate(ns)}
+    lib.trib_hostcost_resident.argtypes = [C.POINTER(C.c_double)]
+    rout = (C.c_double * 3)()
+    if lib.trib_hostcost_resident(rout) == 0:
+        res["whole_entry_resident"] = {"one_block": rout[0], "40_blocks_in_order": rout[1],
+                                       "40_blocks_first_and_last": rout[2]}
     res["note"] = ("1-token Llama-7B chain; the launch call returns at once, so whole_entry "
                    "is the library's part of chain_host_us, the rest is the HIP launch")
     return res
@@ -382,59 +387,83 @@ def main():
     cfg = wl.LLAMA7B_DECODE
     inp = wl.host_inputs(cfg)
     d = {k: wl.to_torch(v, cfg.dtype, dev) for k, v in inp.items()}
+    # `rcache` holds the call's argument block in device memory
+    # (TRI_CACHE_RESIDENT_ARGS: launches without kernel arguments), `cache`
+    # launches with kernel arguments; both run the same kernel on the same
+    # buffers. The headline is the resident cache's.
     cache = tri.SpecCache()
+    rcache = tri.SpecCache(resident_args=True)
     args_c, _outs = cache.chain_args(d["x"], d["residual"], d["w"], d["q"], d["k"], d["pos"],
                                      d["gate"], d["up"], cfg.eps, cfg.base)
     cache.decode_chain_args(args_c, stream)          # miss -> install -> hit
+    rcache.decode_chain_args(args_c, stream)         # miss -> install -> block held -> hit
     torch.cuda.synchronize()
-    sel = cache.last_selection()
+    sel = rcache.last_selection()
     K, W = args.steps, args.warmup
     e2e = (C.c_double * max(K, 1))()
     hst = (C.c_double * max(K, 1))()
 
-    def run(mode, n_warm, n):
-        st = bench.trib_latency(cache.handle, mode, C.byref(args_c), sptr, n_warm, n, e2e, hst)
+    def run(c, mode, n_warm, n):
+        st = bench.trib_latency(c.handle, mode, C.byref(args_c), sptr, n_warm, n, e2e, hst)
         if st != 0:
             raise RuntimeError(f"latency loop failed: {st}")
 
-    run(1, W, 0)                                     # warm the empty-kernel path
+    run(cache, 1, W, 0)                              # warm the empty-kernel path
     torch.cuda.synchronize()
-    run(1, 0, K)
+    run(cache, 1, 0, K)
     torch.cuda.synchronize()
     empty_e2e, empty_host = list(e2e[:K]), list(hst[:K])
 
-    run(0, W, 0)                                     # W untimed warmup steps
+    run(cache, 0, W, 0)                              # with kernel arguments
+    torch.cuda.synchronize()
+    run(cache, 0, 0, K)
+    torch.cuda.synchronize()
+    args_e2e, args_host = list(e2e[:K]), list(hst[:K])
+
+    run(rcache, 0, W, 0)                             # W untimed warmup steps
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    run(0, 0, K)                                     # exactly K timed steps
+    run(rcache, 0, 0, K)                             # exactly K timed steps
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     chain_e2e, chain_host = list(e2e[:K]), list(hst[:K])
 
     tot = C.c_double()
     n_issue = min(K, 10000)
-    assert bench.trib_issue(cache.handle, 0, C.byref(args_c), sptr, n_issue, C.byref(tot)) == 0
-    issue_us = tot.value / n_issue
+    issue_us = {}
+    for name, c in (("resident", rcache), ("kernel_args", cache)):
+        assert bench.trib_issue(c.handle, 0, C.byref(args_c), sptr, n_issue, C.byref(tot)) == 0
+        issue_us[name] = tot.value / n_issue
 
     n_py = min(K, 2000)
-    py = []
-    for _ in range(n_py):
-        a = time.perf_counter()
-        cache.decode_chain_args(args_c, stream)
-        stream.synchronize()
-        py.append((time.perf_counter() - a) * 1e6)
-    stats = cache.stats()
+    py = {}
+    for name, c in (("resident", rcache), ("kernel_args", cache)):
+        t = []
+        for _ in range(n_py):
+            a = time.perf_counter()
+            c.decode_chain_args(args_c, stream)
+            stream.synchronize()
+            t.append((time.perf_counter() - a) * 1e6)
+        py[name] = summary(t)
+    stats = rcache.stats()
+    resident = rcache.resident_info()
 
     ce, ee = summary(chain_e2e), summary(empty_e2e)
+    ke = summary(args_e2e)
     latency = {
         "chain_e2e_us": ce, "chain_host_us": summary(chain_host),
         "empty_e2e_us": ee, "empty_host_us": summary(empty_host),
         "ratio_to_empty_median": ce["median"] / ee["median"],
-        "python_binding_e2e_us": summary(py),
-        "pipelined_issue_us_per_call": issue_us,
+        "chain_kernel_args_e2e_us": ke, "chain_kernel_args_host_us": summary(args_host),
+        "kernel_args_ratio_to_empty_median": ke["median"] / ee["median"],
+        "python_binding_e2e_us": py["resident"],
+        "python_binding_kernel_args_e2e_us": py["kernel_args"],
+        "pipelined_issue_us_per_call": issue_us["resident"],
+        "pipelined_issue_kernel_args_us_per_call": issue_us["kernel_args"],
         "selection": {"variant": sel.variant, "n_launches": sel.n_launches,
                       "grid": sel.launch[0].grid_x, "roles": list(sel.roles)},
         "cache_stats": stats,
+        "resident_blocks": resident,
     }
     latency["host_cost_ns"] = host_cost()
     if args.latency_only:
@@ -494,6 +523,11 @@ def main():
     assert st == 0, st
     latency["gqa_decode_chain_e2e_us"] = summary(list(e2e[:n2]))
     latency["gqa_decode_chain_host_us"] = summary(list(hst[:n2]))
+    rcache.decode_chain_args(args2, stream)           # installs the GQA version there
+    torch.cuda.synchronize()
+    st = bench.trib_latency(rcache.handle, 0, C.byref(args2), sptr, W, n2, e2e, hst)
+    assert st == 0, st
+    latency["gqa_decode_chain_resident_e2e_us"] = summary(list(e2e[:n2]))
 
     # ---- Qwen3-8B-shaped decode (1 token, per-head QK-RMSNorm before RoPE) -------------
     cfg3 = wl.QWEN3_8B_DECODE
@@ -578,6 +612,12 @@ def main():
         st = bench.trib_layers(cache.handle, mode, lay_args, n_layers, sptr, 20, n3, e2e)
         assert st == 0, st
         steps[name] = summary(list(e2e[:n3]))
+    # the same step from resident argument blocks (one block per layer)
+    for mode, name in ((0, "resident_one_call"), (1, "resident_per_layer_calls")):
+        st = bench.trib_layers(rcache.handle, mode, lay_args, n_layers, sptr, 20, n3, e2e)
+        assert st == 0, st
+        steps[name] = summary(list(e2e[:n3]))
+    steps["resident_blocks"] = rcache.resident_info()
     layer_list = [lay_args[l] for l in range(n_layers)]
     g32 = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g32, stream=stream):
@@ -607,6 +647,8 @@ def main():
     steps["tri_graph_launches_per_step"] = ng.launch_count
     latency["decode_step_32_layers_e2e_us"] = steps
     ng.close()
+    torch.cuda.synchronize()
+    rcache.close()
     del lay_bufs, g32
 
     # ---- mixed-shape stream: guard hits, misses, latency per token bucket ---------------
@@ -906,6 +948,9 @@ def emit(args, ce, wall, latency, bandwidth, roofline, cpu):
                                "SwiGLU) at T=1, hidden 4096, 32+32 heads x 128, "
                                "intermediate 11008, RoPE base 1e4",
                    "accumulate": "f32",
+                   "launch": "argument block resident in device memory "
+                             "(TRI_CACHE_RESIDENT_ARGS); with kernel arguments: "
+                             "latency.chain_kernel_args_e2e_us",
                    "hip_force_dev_kernarg": os.environ.get("HIP_FORCE_DEV_KERNARG",
                                                            "unset (runtime default)"),
                    "bandwidth_workload": "prefill8k_bf16: T=8192, hidden 8192, 64+8 heads x "

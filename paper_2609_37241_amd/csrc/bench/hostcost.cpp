@@ -151,4 +151,36 @@ int trib_hostcost(const int32_t *ns, int32_t nn, double *out) {
   return 0;
 }
 
+// Entry calls on a cache with resident argument blocks (the 1-token chain):
+// out[0] ns per call with one held block; out[1] ns per call stepping
+// through 40 held blocks in order (the next layer's block is the one after
+// the last match); out[2] ns per call alternating between the first and the
+// last of the 40 (the longest search). Returns 0, or -1 on failure.
+int trib_hostcost_resident(double *out) {
+  const int N = 200000;
+  tri_cache *c = nullptr;
+  if (tri_spec_cache_create(&c, kMaxCapacity, TRI_CACHE_AUTO_INSTALL | TRI_CACHE_RESIDENT_ARGS) !=
+      TRI_OK)
+    return -1;
+  std::vector<tri_chain_args> layers(kResidentSlots);
+  for (uint32_t i = 0; i < kResidentSlots; ++i) {
+    layers[i] = chain_args(11008);
+    layers[i].x = static_cast<char *>(const_cast<void *>(layers[i].x)) + 4096 * i;
+    if (tri_decode_chain(c, &layers[i], nullptr) != TRI_OK) return -1;
+  }
+  tri_resident_info info;
+  if (tri_spec_resident_info(c, &info) != TRI_OK || info.held != kResidentSlots) return -1;
+  const tri_chain_args *volatile pl = layers.data();
+  out[0] = ns_per([&](int) { g_sink += uint64_t(tri_decode_chain(c, pl, nullptr)); }, N);
+  out[1] = ns_per([&](int i) {
+    g_sink += uint64_t(tri_decode_chain(c, pl + (i % kResidentSlots), nullptr));
+  }, N);
+  out[2] = ns_per([&](int i) {
+    g_sink += uint64_t(tri_decode_chain(c, pl + ((i & 1) ? kResidentSlots - 1 : 0), nullptr));
+  }, N);
+  if (tri_spec_resident_info(c, &info) != TRI_OK || info.held != kResidentSlots) return -1;
+  tri_spec_cache_destroy(c);
+  return 0;
+}
+
 }  // extern "C"
