@@ -99,11 +99,12 @@ enum {
   TRI_CACHE_JIT = 2u,            /* install compiles a key-specialized kernel */
   TRI_CACHE_AUTOTUNE = 4u,       /* install times the key's candidate plans */
   TRI_CACHE_GENERIC = 8u,        /* a miss installs a generic (range) version */
-  TRI_CACHE_RESIDENT_ARGS = 16u  /* fused-chain argument blocks held on the device */
+  TRI_CACHE_RESIDENT_ARGS = 16u  /* argument blocks held in device memory */
 };
 
-/* Resident argument blocks (TRI_CACHE_RESIDENT_ARGS): blocks per device and
- * dtype, and the largest fused-chain launch (workgroups) that uses one. */
+/* Resident argument blocks (TRI_CACHE_RESIDENT_ARGS): blocks per device,
+ * kernel family and dtype, and the largest launch (workgroups) that uses
+ * one. */
 enum { TRI_RESIDENT_SLOTS = 40, TRI_RESIDENT_MAX_GRID = 512 };
 
 /* Divisibility class of a generic version's hidden-size range
@@ -320,29 +321,31 @@ typedef struct tri_chain_args {
  * per-call launch cost the paper measures in Sec. 2.3): the runtime places
  * a launch's kernel arguments in device memory on every launch, which costs
  * about as much host and end-to-end time as the 1-token chain's whole
- * kernel. With this flag a fused-chain launch of at most
- * TRI_RESIDENT_MAX_GRID workgroups by a precompiled version takes its
- * argument block from a table in device memory instead: the first call with
- * a given block (every pointer, stride, size, eps and the launch geometry
- * equal) copies it into a free slot of the device's table for the dtype
- * (TRI_RESIDENT_SLOTS per device and dtype, shared by the process's
- * caches), synchronously on a private stream; every later call with an
- * equal block launches a form of the same kernel that takes no kernel
- * arguments and finds its slot through its own LDS allocation (the call
- * requests slot x 1280 bytes of dynamic LDS, which the kernel reads back
- * from a hardware register). Pointers are held, not the data behind them:
- * positions, activations and weights are read on every call. Outputs equal
- * the ordinary launch's bit for bit, and the selection records are the
- * same. A held block is never rewritten while the cache lives; slots return
- * to the device's pool when the cache is destroyed (after the device has
- * finished its work). Calls launch as without the flag (kernel arguments)
- * when the cache holds TRI_RESIDENT_SLOTS blocks of the dtype or the pool
+ * kernel. With this flag a launch of at most TRI_RESIDENT_MAX_GRID
+ * workgroups by a precompiled version takes its argument block from a table
+ * in device memory instead -- every op's launches, the fused chain's and the
+ * three of a three-launch chain. The first call with a given block (every
+ * pointer, stride, size, eps and the launch geometry equal) copies it into
+ * a free slot of the device's table for the kernel's family (the chain,
+ * norms, RoPE, SwiGLU, element-wise ops, embedding) and dtype
+ * (TRI_RESIDENT_SLOTS each per device, shared by the process's caches),
+ * synchronously on a private stream; every later call with an equal block
+ * launches a form of the same kernel that takes no kernel arguments and
+ * finds its slot through its own LDS allocation (the call requests slot x
+ * 1280 bytes of dynamic LDS, which the kernel reads back from a hardware
+ * register). Pointers are held, not the data behind them: positions,
+ * activations and weights are read on every call. Outputs equal the
+ * ordinary launch's bit for bit, and the selection records are the same. A
+ * held block is never rewritten while the cache lives; slots return to the
+ * device's pool when the cache is destroyed (after the device has finished
+ * its work). Calls launch as without the flag (kernel arguments) when the
+ * cache holds TRI_RESIDENT_SLOTS blocks of the family and dtype or the pool
  * has none free, when the block is new while the caller's stream is being
- * captured, for compiled specializations (TRI_CACHE_JIT), three-launch
- * plans and larger grids, and on a device that fails the check made at
- * creation (launches at several LDS sizes whose slot the kernel must read
- * back exactly). tri_spec_resident_info tells how many launches used a held
- * block. A first call with a new block synchronizes a private stream:
+ * captured, for compiled specializations (TRI_CACHE_JIT), larger grids and
+ * tri_residual_rmsnorm_noalloc, and on a device that fails the check made
+ * at creation (launches at several LDS sizes whose slot the kernel must
+ * read back exactly). tri_spec_resident_info tells how many launches used a
+ * held block. A first call with a new block synchronizes a private stream:
  * make it before another thread starts a global-mode stream capture. */
 tri_status tri_spec_cache_create(tri_cache **out, uint32_t capacity, uint32_t flags);
 /* Release a cache and everything it owns (versions, kernel handles, loaded

@@ -325,11 +325,28 @@ int chain_check(const tri_chain_args *p, Key *out) {
   return kGo;
 }
 
-// The launches of one chain call on version v of cache c: one fused launch
-// (from a resident argument block when the version has the argument-free
-// form and the cache holds or can hold the block), or the three role
-// kernels in order (stopping at the first failure). l receives the launch
-// records, *n their count. Returns 0 or the failing launch's code.
+// Launch i of version v of cache c with its argument block: from a
+// resident block when the launch has an argument-free form, its grid is at
+// most kResidentMaxGrid and the cache holds (or can hold) the block;
+// otherwise with kernel arguments. 0 or the launch's failure code.
+int launch(tri_cache *c, const Version &v, int i, uint32_t dtype, uint32_t grid, uint32_t block,
+           const void *args, uint32_t size, void *stream) {
+  if (v.fn_res[i] && grid <= kResidentMaxGrid) {
+    const int32_t slot =
+        resident_slot(c, resident_family(v.plan.kvariant[i]), dtype, args, size, grid, stream);
+    if (slot >= 0) {
+      const int rc = be_launch_resident(v.fn_res[i], grid, block, uint32_t(slot), stream);
+      if (rc == 0) c->resident_launches++;
+      return rc;
+    }
+  }
+  return be_launch(v.fn[i], grid, block, args, size, stream);
+}
+
+// The launches of one chain call on version v of cache c: one fused launch,
+// or the three role kernels in order (stopping at the first failure), each
+// through launch(). l receives the launch records, *n their count. Returns
+// 0 or the failing launch's code.
 int chain_launch(tri_cache *c, const Version &v, const tri_chain_args &p, void *stream,
                  tri_launch_rec *l, int *n) {
   const uint32_t dtype = uint32_t(p.dtype);
@@ -352,15 +369,7 @@ int chain_launch(tri_cache *c, const Version &v, const tri_chain_args &p, void *
     const uint32_t grid = g0 + g1 + g2;
     l[0] = {CH_FUSED, grid, kBlock};
     *n = 1;
-    if (v.fn_res && grid <= kResidentMaxGrid) {
-      const int32_t slot = resident_slot(c, dtype, a, grid, stream);
-      if (slot >= 0) {
-        const int rc = be_launch_resident(v.fn_res, grid, kBlock, uint32_t(slot), stream);
-        if (rc == 0) c->resident_launches++;
-        return rc;
-      }
-    }
-    return be_launch(v.fn[0], grid, kBlock, &a, sizeof a, stream);
+    return launch(c, v, 0, dtype, grid, kBlock, &a, sizeof a, stream);
   }
   // Three launches: the residual norm, RoPE and SwiGLU role kernels (a
   // split norm role takes the version's scratch with its rows).
@@ -374,7 +383,7 @@ int chain_launch(tri_cache *c, const Version &v, const tri_chain_args &p, void *
   int rc = 0;
   for (int i = 0; i < 3; ++i) {
     l[i] = {v.plan.kvariant[i], grids[i], role_block(v.plan.kvariant[i])};
-    if (rc == 0) rc = be_launch(v.fn[i], grids[i], l[i].block_x, args[i], sizes[i], stream);
+    if (rc == 0) rc = launch(c, v, i, dtype, grids[i], l[i].block_x, args[i], sizes[i], stream);
   }
   return rc;
 }
@@ -407,7 +416,7 @@ tri_status single_launch(tri_cache *c, uint32_t op, const Key &k, int64_t T, int
   const tri_launch_rec l{v.plan.kvariant[0],
                          role_grid(v.plan.kvariant[0], key_dtype(k), T, width),
                          role_block(v.plan.kvariant[0])};
-  const int rc = be_launch(v.fn[0], l.grid_x, l.block_x, args, args_size, stream);
+  const int rc = launch(c, v, 0, key_dtype(k), l.grid_x, l.block_x, args, args_size, stream);
   record(c, op, v, vi, k, 1, &l, rc ? TRI_E_LAUNCH : TRI_OK);
   return finish(c, v, auto_inst, rc);
 }
@@ -425,9 +434,9 @@ tri_status norm_launch(tri_cache *c, uint32_t op, const Key &k, const RnArgs &a,
   int rc;
   if (kv == RN_SPLIT) {
     const RnSplitArgs sa{a, v.d_scratch};
-    rc = be_launch(v.fn[0], l.grid_x, l.block_x, &sa, sizeof sa, stream);
+    rc = launch(c, v, 0, key_dtype(k), l.grid_x, l.block_x, &sa, sizeof sa, stream);
   } else {
-    rc = be_launch(v.fn[0], l.grid_x, l.block_x, &a, sizeof a, stream);
+    rc = launch(c, v, 0, key_dtype(k), l.grid_x, l.block_x, &a, sizeof a, stream);
   }
   record(c, op, v, vi, k, 1, &l, rc ? TRI_E_LAUNCH : TRI_OK);
   return finish(c, v, auto_inst, rc);
@@ -598,7 +607,7 @@ tri_status rope_entry(tri_cache *c, uint32_t op, int32_t dtype, void *q, int64_t
                          role_grid(v.plan.kvariant[0], uint32_t(dtype), T, 0, v.plan.rope_slices,
                                    v.plan.rope_tokens),
                          kBlock};
-  const int rc = be_launch(v.fn[0], l.grid_x, kBlock, &a, sizeof a, stream);
+  const int rc = launch(c, v, 0, uint32_t(dtype), l.grid_x, kBlock, &a, sizeof a, stream);
   record(c, op, v, vi, k, 1, &l, rc ? TRI_E_LAUNCH : TRI_OK);
   return finish(c, v, auto_inst, rc);
 }
@@ -678,6 +687,8 @@ tri_status tri_residual_rmsnorm_noalloc(tri_cache *c, tri_dtype dtype, const voi
   const int32_t kv = v.plan.kvariant[0];
   const RnArgs a{x, res, w, y, res_out, x_rs, res_rs, y_rs, ro_rs, T, int32_t(H), eps};
   const tri_launch_rec l{kv, role_grid(kv, uint32_t(dtype), T, H), role_block(kv)};
+  // Always with kernel arguments: a resident block's first use copies it
+  // to the device, which this entry point does not do.
   int rc;
   if (kv == RN_SPLIT) {
     // the GPU's fixed scratch in place of the version's own

@@ -25,10 +25,20 @@ const void *chain_kernel_bf16(int32_t sub);
 const void *empty_kernel();
 const void *elt_kernel(int32_t variant, uint32_t dtype, int32_t op);
 const void *emb_kernel(int32_t variant, uint32_t dtype);
+const void *rn_kernel_resident(int32_t variant, uint32_t dtype, int32_t res);
+const void *rope_kernel_resident(int32_t variant, uint32_t dtype);
+const void *sw_kernel_resident(int32_t variant, uint32_t dtype);
 const void *chain_kernel_resident_f32(int32_t sub);
 const void *chain_kernel_resident_bf16(int32_t sub);
-int chain_resident_table_f32(int device, void **ptr);
-int chain_resident_table_bf16(int device, void **ptr);
+const void *elt_kernel_resident(int32_t variant, uint32_t dtype, int32_t op);
+const void *emb_kernel_resident(int32_t variant, uint32_t dtype);
+const void *resident_symbol_chain_f32();
+const void *resident_symbol_chain_bf16();
+const void *resident_symbol_norm();
+const void *resident_symbol_rope();
+const void *resident_symbol_swiglu();
+const void *resident_symbol_elt();
+const void *resident_symbol_emb();
 int resident_check();
 
 int be_init(int *device) {
@@ -79,27 +89,61 @@ constexpr int kMaxDevices = 64;
 std::mutex g_res_mu;
 int g_res_check[kMaxDevices];             // 0: not checked; 1: passed; -1: failed
 hipStream_t g_res_stream[kMaxDevices];    // private copy stream per device
+// device addresses of the tables, per device: [family][dtype]
+void *g_res_table[kMaxDevices][kResFamilies][2];
+
+// The table symbol of a family and dtype and the block offset into it: the
+// chain has a table per dtype (one per kernel file), the other families one
+// dtype-major table.
+const void *table_symbol(uint32_t fam, uint32_t dt, uint32_t *first) {
+  *first = 0;
+  switch (fam) {
+    case kResChain: return dt == TRI_F32 ? resident_symbol_chain_f32() : resident_symbol_chain_bf16();
+    case kResNorm: *first = dt * kResidentSlots; return resident_symbol_norm();
+    case kResRope: *first = dt * kResidentSlots; return resident_symbol_rope();
+    case kResSwiglu: *first = dt * kResidentSlots; return resident_symbol_swiglu();
+    case kResElt: *first = dt * kResidentSlots; return resident_symbol_elt();
+    case kResEmb: *first = dt * kResidentSlots; return resident_symbol_emb();
+    default: return nullptr;
+  }
+}
 }  // namespace
 
-// The device's table for dtype, once the device has passed the check of the
-// LDS channel (made once per device, with it current).
-int be_resident_table(int device, uint32_t dtype, void **table) {
+// The device's table for a family and dtype, once the device has passed the
+// check of the LDS channel (made once per device, with it current).
+int be_resident_table(int device, uint32_t family, uint32_t dtype, void **table) {
   *table = nullptr;
-  if (device < 0 || device >= kMaxDevices) return TRI_E_RUNTIME;
-  {
-    std::lock_guard<std::mutex> lock(g_res_mu);
-    if (g_res_check[device] == 0) g_res_check[device] = resident_check() == 0 ? 1 : -1;
-    if (g_res_check[device] != 1) return TRI_E_RUNTIME;
+  if (device < 0 || device >= kMaxDevices || family >= kResFamilies || dtype > 1)
+    return TRI_E_RUNTIME;
+  std::lock_guard<std::mutex> lock(g_res_mu);
+  if (g_res_check[device] == 0) g_res_check[device] = resident_check() == 0 ? 1 : -1;
+  if (g_res_check[device] != 1) return TRI_E_RUNTIME;
+  void *&t = g_res_table[device][family][dtype];
+  if (!t) {
+    uint32_t first = 0;
+    const void *sym = table_symbol(family, dtype, &first);
+    void *p = nullptr;
+    if (!sym || hipGetSymbolAddress(&p, sym) != hipSuccess || !p) return TRI_E_RUNTIME;
+    t = static_cast<char *>(p) + size_t(first) * sizeof(ResidentBlock);
   }
-  if (dtype == TRI_F32) return chain_resident_table_f32(device, table);
-  if (dtype == TRI_BF16) return chain_resident_table_bf16(device, table);
-  return TRI_E_RUNTIME;
+  *table = t;
+  return 0;
 }
 
-int be_resolve_resident(uint32_t dtype, int32_t ksub, void **fn) {
-  const void *sym = dtype == TRI_F32    ? chain_kernel_resident_f32(ksub)
-                    : dtype == TRI_BF16 ? chain_kernel_resident_bf16(ksub)
-                                        : nullptr;
+int be_resolve_resident(int32_t kvariant, uint32_t dtype, int32_t ksub, void **fn) {
+  const void *sym = nullptr;
+  if (kvariant >= RN_SCALAR && kvariant <= RN_SPLIT)
+    sym = rn_kernel_resident(kvariant, dtype, ksub);
+  else if (kvariant >= ROPE_SCALAR && kvariant <= ROPE_QKN_VEC_I)
+    sym = rope_kernel_resident(kvariant, dtype);
+  else if (kvariant >= SW_SCALAR && kvariant <= SW_ROWS)
+    sym = sw_kernel_resident(kvariant, dtype);
+  else if (kvariant == CH_FUSED)
+    sym = dtype == TRI_F32 ? chain_kernel_resident_f32(ksub) : chain_kernel_resident_bf16(ksub);
+  else if (kvariant >= ELT_SCALAR && kvariant <= ELT_ROWS)
+    sym = elt_kernel_resident(kvariant, dtype, ksub);
+  else if (kvariant == EMB_SCALAR || kvariant == EMB_VEC)
+    sym = emb_kernel_resident(kvariant, dtype);
   if (!sym) return TRI_E_RUNTIME;
   hipFunction_t f = nullptr;
   if (hipGetFuncBySymbol(&f, sym) != hipSuccess || !f) return TRI_E_RUNTIME;

@@ -46,12 +46,13 @@ void be_arch(char *out, uint32_t cap) {
   if (cap) out[0] = '\0';
 }
 // resident argument blocks: host tables stand in for the device's
-int be_resident_table(int, uint32_t dtype, void **table) {
-  static ResidentChain tables[2][kResidentSlots];
-  *table = dtype <= 1 ? tables[dtype] : nullptr;
-  return dtype <= 1 ? 0 : TRI_E_RUNTIME;
+int be_resident_table(int, uint32_t family, uint32_t dtype, void **table) {
+  static ResidentBlock tables[kResFamilies][2][kResidentSlots];
+  const bool ok = family < kResFamilies && dtype <= 1;
+  *table = ok ? tables[family][dtype] : nullptr;
+  return ok ? 0 : TRI_E_RUNTIME;
 }
-int be_resolve_resident(uint32_t, int32_t, void **fn) {
+int be_resolve_resident(int32_t, uint32_t, int32_t, void **fn) {
   *fn = reinterpret_cast<void *>(uintptr_t(0x2000));
   return 0;
 }

@@ -270,11 +270,14 @@ tri_status install_key(tri_cache *c, const Key &k, int32_t candidate, bool gener
         return tri_status(st);
       }
     }
-    // the argument-free form of a fused chain, for resident argument blocks
-    // (without it the version launches with kernel arguments)
-    if (dt <= 1 && c->rtable[dt] && v.plan.variant == CH_FUSED &&
-        be_resolve_resident(dt, v.plan.ksub[0], &v.fn_res) != 0)
-      v.fn_res = nullptr;
+    // the argument-free form of each launch's kernel, for resident argument
+    // blocks (without it that launch carries its kernel arguments)
+    for (int i = 0; dt <= 1 && i < v.plan.n_launches; ++i) {
+      const uint32_t fam = resident_family(v.plan.kvariant[i]);
+      if (fam < kResFamilies && c->rtable[fam][dt] &&
+          be_resolve_resident(v.plan.kvariant[i], dt, v.plan.ksub[i], &v.fn_res[i]) != 0)
+        v.fn_res[i] = nullptr;
+    }
   }
   c->versions[c->n_versions++] = v;
   c->stats.installs++;
@@ -352,15 +355,18 @@ tri_status tri_spec_cache_create(tri_cache **out, uint32_t capacity, uint32_t fl
   // resident argument blocks: the device's tables (a failed lookup or
   // check leaves the flag without effect)
   if (flags & TRI_CACHE_RESIDENT_ARGS) {
-    c->held = static_cast<ResidentChain *>(calloc(2 * kResidentSlots, sizeof(ResidentChain)));
+    c->held = static_cast<ResidentBlock *>(
+        calloc(size_t(kResFamilies) * 2 * kResidentSlots, sizeof(ResidentBlock)));
     if (!c->held) {
       free(c->versions);
       free(c->memo);
       free(c);
       return TRI_E_NOMEM;
     }
-    for (uint32_t dt : {uint32_t(TRI_F32), uint32_t(TRI_BF16)})
-      if (be_resident_table(device, dt, &c->rtable[dt]) != 0) c->rtable[dt] = nullptr;
+    for (uint32_t fam = 0; fam < kResFamilies; ++fam)
+      for (uint32_t dt : {uint32_t(TRI_F32), uint32_t(TRI_BF16)})
+        if (be_resident_table(device, fam, dt, &c->rtable[fam][dt]) != 0)
+          c->rtable[fam][dt] = nullptr;
   }
   c->capacity = capacity;
   c->flags = flags;
@@ -413,8 +419,12 @@ tri_status tri_spec_stats(const tri_cache *c, tri_stats *out) {
 tri_status tri_spec_resident_info(const tri_cache *c, tri_resident_info *out) {
   if (!c || !out) return TRI_E_INVALID;
   memset(out, 0, sizeof *out);
-  out->enabled = (c->rtable[0] || c->rtable[1]) ? 1 : 0;
-  out->held = c->n_held[0] + c->n_held[1];
+  for (uint32_t fam = 0; fam < kResFamilies; ++fam) {
+    for (uint32_t dt = 0; dt < 2; ++dt) {
+      if (c->rtable[fam][dt]) out->enabled = 1;
+      out->held += c->n_held[fam][dt];
+    }
+  }
   out->launches = c->resident_launches;
   return TRI_OK;
 }

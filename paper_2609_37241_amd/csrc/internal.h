@@ -242,23 +242,34 @@ void be_arch(char *out, uint32_t cap);                         // device archite
 constexpr uint64_t kNoAllocScratchWords = uint64_t(TRI_NOALLOC_SCRATCH_BYTES) / 8;
 int be_noalloc_scratch(int device, void **ptr);
 
-// Resident argument blocks of fused-chain launches (TRI_CACHE_RESIDENT_ARGS).
-// be_resident_table: the device address of this device's table for dtype,
+// Resident argument blocks (TRI_CACHE_RESIDENT_ARGS). be_resident_table: the
+// device address of this device's table for a kernel family and dtype,
 // looked up -- and the LDS channel checked -- once per device with it
-// current. be_resolve_resident: the argument-free form of fused-chain
-// kernel ksub. be_resident_write: a synchronous copy into `device`'s table.
+// current. be_resolve_resident: the argument-free form of the kernel
+// be_resolve gives for the same (kvariant, dtype, ksub). be_resident_write:
+// a synchronous copy into `device`'s table.
 // be_launch_resident: launch `fn` on slot `slot` (slot * kLdsGranule bytes
 // of dynamic LDS, no kernel arguments). be_stream_capturing: 1 when the
 // stream is being captured (or the query fails), else 0. be_device_sync:
 // wait until `device` is idle (the current device is kept). 0 or tri_status.
-int be_resident_table(int device, uint32_t dtype, void **table);
-int be_resolve_resident(uint32_t dtype, int32_t ksub, void **fn);
+int be_resident_table(int device, uint32_t family, uint32_t dtype, void **table);
+int be_resolve_resident(int32_t kvariant, uint32_t dtype, int32_t ksub, void **fn);
 int be_resident_write(int device, void *dst, const void *src, uint32_t bytes);
 int be_launch_resident(void *fn, uint32_t grid, uint32_t block, uint32_t slot, void *stream);
 int be_stream_capturing(void *stream);
 void be_device_sync(int device);
 static_assert(kResidentSlots == uint32_t(TRI_RESIDENT_SLOTS), "resident slots");
 constexpr uint32_t kResidentMaxGrid = TRI_RESIDENT_MAX_GRID;
+// The resident family of a kernel variant (kResFamilies: none).
+inline uint32_t resident_family(int32_t kvariant) {
+  if (kvariant == CH_FUSED) return kResChain;
+  if (kvariant >= RN_SCALAR && kvariant <= RN_SPLIT) return kResNorm;
+  if (kvariant >= ROPE_SCALAR && kvariant <= ROPE_QKN_VEC_I) return kResRope;
+  if (kvariant >= SW_SCALAR && kvariant <= SW_ROWS) return kResSwiglu;
+  if (kvariant >= ELT_SCALAR && kvariant <= ELT_ROWS) return kResElt;
+  if (kvariant == EMB_SCALAR || kvariant == EMB_VEC) return kResEmb;
+  return kResFamilies;
+}
 
 // ---- versions and the cache ------------------------------------------------------------
 struct Version {
@@ -273,7 +284,7 @@ struct Version {
   float tune_ms;
   float *d_consts;        // device copy of the RoPE inverse frequencies, or null
   float *h_consts;        // host copy (rotary_dim/2 floats), or null
-  void *fn_res;           // fused chain: the argument-free form of fn[0], or null
+  void *fn_res[3];        // the argument-free form of each launch's kernel, or null
   uint32_t n_consts;
   uint64_t *d_scratch;    // split norm rows: the exchange scratch, or null
   uint64_t scratch_words;
@@ -310,22 +321,24 @@ struct tri_cache {
   void *empty_fn;
   void *noalloc_scratch;         // this device's static scratch, or null
   char code_dir[1024];           // compiled code objects; empty: none
-  // TRI_CACHE_RESIDENT_ARGS: per dtype (TRI_F32, TRI_BF16) the device table
-  // (null: not in use), the blocks held (host copies, tag set) and the slot
-  // of each, and the index of the block the last resident launch matched.
-  void *rtable[2];
-  tri::ResidentChain *held;      // [2][kResidentSlots], or null
-  uint32_t n_held[2];
-  uint32_t last_held[2];
+  // TRI_CACHE_RESIDENT_ARGS: per kernel family and dtype (TRI_F32, TRI_BF16)
+  // the device table (null: not in use), the blocks held (host copies with
+  // tag and size set) and the index of the block the last resident launch
+  // matched.
+  void *rtable[tri::kResFamilies][2];
+  tri::ResidentBlock *held;      // [kResFamilies][2][kResidentSlots], or null
+  uint32_t n_held[tri::kResFamilies][2];
+  uint32_t last_held[tri::kResFamilies][2];
   uint64_t resident_launches;
 };
 
 namespace tri {
-// The slot of a held block equal to (a, grid) for dtype, holding a new one
-// when the cache and the device's pool have room and `stream` is not being
-// captured; -1: launch with kernel arguments (resident.cpp).
-int32_t resident_slot(tri_cache *c, uint32_t dtype, const ChainArgs &a, uint32_t grid,
-                      void *stream);
+// The slot of a held block of the family and dtype equal to the `size`
+// bytes at `args` and `grid`, holding a new one when the cache and the
+// device's pool have room and `stream` is not being captured; -1: launch
+// with kernel arguments (resident.cpp).
+int32_t resident_slot(tri_cache *c, uint32_t family, uint32_t dtype, const void *args,
+                      uint32_t size, uint32_t grid, void *stream);
 // Return the cache's slots to the device's pool (after the device is idle).
 void resident_release_all(tri_cache *c);
 }  // namespace tri

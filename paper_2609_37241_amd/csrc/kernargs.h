@@ -120,19 +120,33 @@ struct ChainArgs {
   uint32_t rope_blocks;
 };
 
-// A fused-chain argument block held in device memory for launches without
-// kernel arguments: the block, the launch's workgroup count and a tag that
-// marks the slot as written (kResidentTag + slot; zero until then). Slot k
-// of a device's table is found by a launch that requests k * kLdsGranule
-// bytes of dynamic LDS (the kernel reads its own LDS allocation back).
-constexpr uint32_t kResidentSlots = 40;        // per device and dtype
+// An argument block held in device memory for launches without kernel
+// arguments: the kernel's argument struct (zero beyond its size), the
+// launch's workgroup count and a tag that marks the slot as written
+// (kResidentTag + slot; zero until then). Each kernel family has a table of
+// kResidentSlots blocks per device and dtype; slot k is found by a launch
+// that requests k * kLdsGranule bytes of dynamic LDS (the kernel reads its
+// own LDS allocation back). `size` is the host's bookkeeping.
+constexpr uint32_t kResidentSlots = 40;        // per device, family and dtype
 constexpr uint32_t kResidentTag = 0x52455300u;
 constexpr uint32_t kLdsGranule = 1280;         // LDS allocation granule, bytes
-struct ResidentChain {
-  ChainArgs a;
+constexpr uint32_t kResidentArgsMax = 288;     // the largest argument struct
+enum ResidentFamily : uint32_t {
+  kResChain = 0,   // the fused decode chain (ChainArgs)
+  kResNorm,        // RMSNorm and residual RMSNorm rows (RnArgs, RnSplitArgs)
+  kResRope,        // RoPE and QK-RMSNorm + RoPE (RopeArgs)
+  kResSwiglu,      // SwiGLU (SwArgs)
+  kResElt,         // silu, add, masked_fill (EltArgs)
+  kResEmb,         // embedding rows (EmbArgs)
+  kResFamilies
+};
+struct ResidentBlock {
+  uint64_t args[kResidentArgsMax / 8];
   uint32_t grid;
   uint32_t tag;
-  uint64_t pad[3];
+  uint32_t size;
+  uint32_t pad0;
+  uint64_t pad[2];
 };
 
 static_assert(sizeof(RnArgs) == 88 && __builtin_offsetof(RnArgs, T) == 72 &&
@@ -148,7 +162,10 @@ static_assert(sizeof(EltArgs) == 88 && __builtin_offsetof(EltArgs, value) == 80,
 static_assert(sizeof(EmbArgs) == 72 && __builtin_offsetof(EmbArgs, ids64) == 64, "EmbArgs layout");
 static_assert(sizeof(ChainArgs) == 288 && __builtin_offsetof(ChainArgs, rn_blocks) == 280,
               "ChainArgs layout");
-static_assert(sizeof(ResidentChain) == 320 && __builtin_offsetof(ResidentChain, tag) == 292,
-              "ResidentChain layout");
+static_assert(sizeof(ResidentBlock) == 320 && __builtin_offsetof(ResidentBlock, grid) == 288 &&
+                  __builtin_offsetof(ResidentBlock, tag) == 292,
+              "ResidentBlock layout");
+static_assert(sizeof(ChainArgs) <= kResidentArgsMax && sizeof(RnSplitArgs) <= kResidentArgsMax,
+              "argument structs fit a resident block");
 
 }  // namespace tri

@@ -3,21 +3,11 @@
 // for every (norm role variant, SwiGLU role) the install policy can pick, in
 // two forms: with the argument block as the kernel argument, and without
 // kernel arguments, reading the block from this device's resident table.
-#include <hip/hip_runtime.h>
-
-#include <mutex>
-
 #include "../internal.h"
 #include "device.h"
 
 namespace tri {
 using namespace dev;
-
-// Resident argument blocks of this dtype's fused chain: one table per GPU,
-// zero at load (every tag unset). In host code the name stands for a
-// host-side shadow, not for device memory: the host writes the table through
-// the device address looked up below, never through the name.
-static __device__ __align__(256) ResidentChain resident_bf16[kResidentSlots];
 
 // RNV: RN_WAVE_1/2 (one wavefront per row) or RN_BLOCK_1..16 (one
 // workgroup per row); SWV: SW_FLAT or SW_FLAT_NT; QKN: QK norm before the
@@ -29,11 +19,20 @@ __global__ __launch_bounds__(256) void k_chain(ChainArgs a) {
   body_chain<DT, wave, n, SWV == SW_FLAT_NT, QKN, INTER>(a, gridDim.x);
 }
 
+// Resident argument blocks of this dtype's fused chain: one table per GPU,
+// zero at load (every tag unset). In host code the name stands for a
+// host-side shadow, not for device memory: the host writes the table through
+// its device address, never through the name.
+static __device__ __align__(256) ResidentBlock resident_chain_bf16[kResidentSlots];
+
 template <int DT, int RNV, int SWV, bool QKN, bool INTER>
 __global__ __launch_bounds__(256) void k_chain_res() {
   constexpr bool wave = RNV <= RN_WAVE_2;
   constexpr int n = wave ? 1 << (RNV - RN_WAVE_1) : 1 << (RNV - RN_BLOCK_1);
-  body_chain_resident<DT, wave, n, SWV == SW_FLAT_NT, QKN, INTER>(resident_bf16);
+  ChainArgs a;
+  uint32_t g;
+  if (resident_args(resident_chain_bf16, a, g))
+    body_chain<DT, wave, n, SWV == SW_FLAT_NT, QKN, INTER>(a, g);
 }
 
 namespace {
@@ -72,11 +71,6 @@ const void *chain_pick(int32_t sub) {
     default: return nullptr;
   }
 }
-
-std::mutex g_table_mu;
-constexpr int kMaxDevices = 64;
-void *g_table_ptr[kMaxDevices];
-int g_table_status[kMaxDevices];   // 0: not looked up; 1: found; -1: failed
 }  // namespace
 
 // sub = (norm role - RN_WAVE_1) * 8 + 4 * (GPT-J pairs) + 2 * (QK norm)
@@ -84,20 +78,9 @@ int g_table_status[kMaxDevices];   // 0: not looked up; 1: found; -1: failed
 const void *chain_kernel_bf16(int32_t sub) { return chain_pick<false>(sub); }
 const void *chain_kernel_resident_bf16(int32_t sub) { return chain_pick<true>(sub); }
 
-// Device address of `device`'s copy of the resident table, looked up once
-// per device with that device current.
-int chain_resident_table_bf16(int device, void **ptr) {
-  *ptr = nullptr;
-  if (device < 0 || device >= kMaxDevices) return TRI_E_RUNTIME;
-  std::lock_guard<std::mutex> lock(g_table_mu);
-  if (g_table_status[device] == 0) {
-    void *p = nullptr;
-    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(resident_bf16));
-    g_table_status[device] = e == hipSuccess && p ? 1 : -1;
-    g_table_ptr[device] = g_table_status[device] == 1 ? p : nullptr;
-  }
-  *ptr = g_table_ptr[device];
-  return g_table_status[device] == 1 ? 0 : TRI_E_RUNTIME;
+// Host shadow of this dtype's resident table.
+const void *resident_symbol_chain_bf16() {
+  return reinterpret_cast<const void *>(&resident_chain_bf16);
 }
 
 }  // namespace tri

@@ -1119,13 +1119,13 @@ __device__ __forceinline__ void elt_scalar_part(const EltArgs &a, int64_t blk, i
   }
 }
 
-// Embedding: workgroup b copies output rows b, b + gridDim.x, ...; the row
-// is table row ids[t] when it is in [0, n_rows), zeros otherwise.
+// Embedding: workgroup b of nblk copies output rows b, b + nblk, ...; the
+// row is table row ids[t] when it is in [0, n_rows), zeros otherwise.
 template <int DT, bool VEC>
-__device__ __forceinline__ void emb_rows(const EmbArgs &a) {
+__device__ __forceinline__ void emb_rows(const EmbArgs &a, uint32_t nblk) {
   using E = Elt<DT>;
   constexpr int V = E::V;
-  for (int64_t t = blockIdx.x; t < a.T; t += gridDim.x) {
+  for (int64_t t = blockIdx.x; t < a.T; t += nblk) {
     const int64_t id = a.ids64 ? static_cast<const int64_t *>(a.ids)[t]
                                : int64_t(static_cast<const int32_t *>(a.ids)[t]);
     const bool ok = id >= 0 && id < a.n_rows;
@@ -1291,40 +1291,44 @@ __device__ __forceinline__ void body_rope_scalar(const RopeArgs &a) {
   rope_scalar_block<DT, QKN>(a, blockIdx.x, lds);
 }
 
+// The bodies that stride over the grid take the launch's workgroup count:
+// gridDim.x, or a resident block's count in a launch without kernel
+// arguments (which must not read gridDim: that would give it implicit
+// kernel arguments again).
 template <int DT, int U, bool NT>
-__device__ __forceinline__ void body_sw_flat(const SwArgs &a) {
-  sw_flat_part<DT, U, NT>(a, blockIdx.x, gridDim.x);
+__device__ __forceinline__ void body_sw_flat(const SwArgs &a, uint32_t nblk = gridDim.x) {
+  sw_flat_part<DT, U, NT>(a, blockIdx.x, nblk);
 }
 
 template <int DT>
-__device__ __forceinline__ void body_sw_rows(const SwArgs &a) {
-  sw_rows_part<DT>(a, blockIdx.x, gridDim.x);
+__device__ __forceinline__ void body_sw_rows(const SwArgs &a, uint32_t nblk = gridDim.x) {
+  sw_rows_part<DT>(a, blockIdx.x, nblk);
 }
 
 template <int DT>
-__device__ __forceinline__ void body_sw_scalar(const SwArgs &a) {
-  sw_scalar_part<DT>(a, blockIdx.x, gridDim.x);
+__device__ __forceinline__ void body_sw_scalar(const SwArgs &a, uint32_t nblk = gridDim.x) {
+  sw_scalar_part<DT>(a, blockIdx.x, nblk);
 }
 
 // U vectors per work-item, cached loads and stores.
 template <int DT, int OP, int U>
-__device__ __forceinline__ void body_elt_flat(const EltArgs &a) {
-  elt_flat_part<DT, OP, false, U>(a, blockIdx.x, gridDim.x);
+__device__ __forceinline__ void body_elt_flat(const EltArgs &a, uint32_t nblk = gridDim.x) {
+  elt_flat_part<DT, OP, false, U>(a, blockIdx.x, nblk);
 }
 
 template <int DT, int OP>
-__device__ __forceinline__ void body_elt_rows(const EltArgs &a) {
-  elt_rows_part<DT, OP>(a, blockIdx.x, gridDim.x);
+__device__ __forceinline__ void body_elt_rows(const EltArgs &a, uint32_t nblk = gridDim.x) {
+  elt_rows_part<DT, OP>(a, blockIdx.x, nblk);
 }
 
 template <int DT, int OP>
-__device__ __forceinline__ void body_elt_scalar(const EltArgs &a) {
-  elt_scalar_part<DT, OP>(a, blockIdx.x, gridDim.x);
+__device__ __forceinline__ void body_elt_scalar(const EltArgs &a, uint32_t nblk = gridDim.x) {
+  elt_scalar_part<DT, OP>(a, blockIdx.x, nblk);
 }
 
 template <int DT, bool VEC>
-__device__ __forceinline__ void body_emb(const EmbArgs &a) {
-  emb_rows<DT, VEC>(a);
+__device__ __forceinline__ void body_emb(const EmbArgs &a, uint32_t nblk = gridDim.x) {
+  emb_rows<DT, VEC>(a, nblk);
 }
 
 // The fused decode chain: workgroups take the residual-RMSNorm, RoPE-QK and
@@ -1399,41 +1403,69 @@ __device__ __forceinline__ P *in_global(P *p) {
   return (P *)g;
 }
 
-// The fused chain without kernel arguments: its block comes from slot
-// resident_slot() of `table` (a device's table in constant memory: the host
-// writes a slot only while no launch can read it). An unwritten slot or an
-// index beyond the table runs nothing.
-template <int DT, bool WAVE, int N, bool NT, bool QKN, bool INTER>
-__device__ __forceinline__ void body_chain_resident(const ResidentChain *table) {
+// Pointers read from memory could point anywhere; these are global memory,
+// as kernel-argument pointers are taken to be (global, not flat, loads and
+// stores).
+__device__ __forceinline__ void to_global(RnArgs &a) {
+  a.x = in_global(a.x);
+  a.res = in_global(a.res);
+  a.w = in_global(a.w);
+  a.y = in_global(a.y);
+  a.res_out = in_global(a.res_out);
+}
+__device__ __forceinline__ void to_global(RnSplitArgs &a) {
+  to_global(a.rn);
+  a.scratch = in_global(a.scratch);
+}
+__device__ __forceinline__ void to_global(RopeArgs &a) {
+  a.q = in_global(a.q);
+  a.k = in_global(a.k);
+  a.pos = in_global(a.pos);
+  a.inv_freq = in_global(a.inv_freq);
+  a.qw = in_global(a.qw);
+  a.kw = in_global(a.kw);
+  a.cos_sin = in_global(a.cos_sin);
+}
+__device__ __forceinline__ void to_global(SwArgs &a) {
+  a.gate = in_global(a.gate);
+  a.up = in_global(a.up);
+  a.out = in_global(a.out);
+}
+__device__ __forceinline__ void to_global(EltArgs &a) {
+  a.a = in_global(a.a);
+  a.b = in_global(a.b);
+  a.out = in_global(a.out);
+}
+__device__ __forceinline__ void to_global(EmbArgs &a) {
+  a.table = in_global(a.table);
+  a.ids = in_global(a.ids);
+  a.out = in_global(a.out);
+}
+__device__ __forceinline__ void to_global(ChainArgs &a) {
+  to_global(a.rn);
+  to_global(a.rope);
+  to_global(a.sw);
+}
+
+// The argument block of a launch without kernel arguments: slot
+// resident_slot() of `table` (this device's table of the kernel's family and
+// dtype, read as constant memory: the host writes a slot only while no
+// launch can read it). False for an index beyond the table or an unwritten
+// slot: the launch then runs nothing.
+template <class A>
+__device__ __forceinline__ bool resident_args(const ResidentBlock *table, A &a, uint32_t &grid) {
   const uint32_t s = resident_slot();
-  if (s >= kResidentSlots) return;
+  if (s >= kResidentSlots) return false;
   typedef __attribute__((address_space(4))) const uint32_t cu32;
   cu32 *w = (cu32 *)(table + s);
-  if (w[__builtin_offsetof(ResidentChain, tag) / 4] != kResidentTag + s) return;
-  uint32_t words[sizeof(ChainArgs) / 4];
+  if (w[__builtin_offsetof(ResidentBlock, tag) / 4] != kResidentTag + s) return false;
+  uint32_t words[sizeof(A) / 4];
 #pragma unroll
-  for (uint32_t i = 0; i < sizeof(ChainArgs) / 4; ++i) words[i] = w[i];
-  ChainArgs a;
+  for (uint32_t i = 0; i < sizeof(A) / 4; ++i) words[i] = w[i];
   __builtin_memcpy(&a, words, sizeof a);
-  // pointers read from memory could point anywhere; these are global
-  // memory, as kernel-argument pointers are taken to be (global, not flat,
-  // loads and stores)
-  a.rn.x = in_global(a.rn.x);
-  a.rn.res = in_global(a.rn.res);
-  a.rn.w = in_global(a.rn.w);
-  a.rn.y = in_global(a.rn.y);
-  a.rn.res_out = in_global(a.rn.res_out);
-  a.rope.q = in_global(a.rope.q);
-  a.rope.k = in_global(a.rope.k);
-  a.rope.pos = in_global(a.rope.pos);
-  a.rope.inv_freq = in_global(a.rope.inv_freq);
-  a.rope.qw = in_global(a.rope.qw);
-  a.rope.kw = in_global(a.rope.kw);
-  a.rope.cos_sin = in_global(a.rope.cos_sin);
-  a.sw.gate = in_global(a.sw.gate);
-  a.sw.up = in_global(a.sw.up);
-  a.sw.out = in_global(a.sw.out);
-  body_chain<DT, WAVE, N, NT, QKN, INTER>(a, w[__builtin_offsetof(ResidentChain, grid) / 4]);
+  to_global(a);
+  grid = w[__builtin_offsetof(ResidentBlock, grid) / 4];
+  return true;
 }
 
 }  // namespace dev

@@ -222,7 +222,7 @@ bool time_candidates(tri_cache *c, const Key &k, const Plan *cands, int n, const
     vs[j] = v;
     vs[j].plan = cands[j];
     for (int i = 0; i < 3; ++i) vs[j].fn[i] = vs[j].module[i] = nullptr;
-    vs[j].fn_res = nullptr;   // tuning launches carry their arguments
+    for (int i = 0; i < 3; ++i) vs[j].fn_res[i] = nullptr;   // tuning launches carry arguments
     for (int i = 0; i < cands[j].n_launches; ++i)
       if (be_resolve(cands[j].kvariant[i], key_dtype(k), cands[j].ksub[i], &vs[j].fn[i]) != 0)
         return false;

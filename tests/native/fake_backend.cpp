@@ -36,9 +36,9 @@ int64_t g_captures = 0, g_capture_start = 0, g_graph_launches = 0, g_graph_destr
 bool g_capture_fail = false;
 void *g_capturing = nullptr;   // the capture stream between begin and end
 
-// Resident argument blocks: one host table per dtype stands in for the
-// device's (shared by every cache, as the device's is).
-tri::ResidentChain g_res_table[2][tri::kResidentSlots];
+// Resident argument blocks: one host table per family and dtype stands in
+// for the device's (shared by every cache, as the device's is).
+tri::ResidentBlock g_res_table[tri::kResFamilies][2][tri::kResidentSlots];
 bool g_res_check_fail = false, g_res_write_fail = false, g_force_capturing = false;
 int64_t g_res_writes = 0, g_res_syncs = 0;
 
@@ -100,16 +100,16 @@ int be_launch(void *fn, uint32_t grid, uint32_t block, const void *args, uint32_
   return n == g_fail_at ? -1 : 0;
 }
 
-int be_resident_table(int device, uint32_t dtype, void **table) {
+int be_resident_table(int device, uint32_t family, uint32_t dtype, void **table) {
   (void)device;
   *table = nullptr;
-  if (g_res_check_fail || dtype > 1) return TRI_E_RUNTIME;
-  *table = g_res_table[dtype];
+  if (g_res_check_fail || family >= kResFamilies || dtype > 1) return TRI_E_RUNTIME;
+  *table = g_res_table[family][dtype];
   return 0;
 }
 
-int be_resolve_resident(uint32_t dtype, int32_t ksub, void **fn) {
-  *fn = reinterpret_cast<void *>(encode(CH_FUSED, dtype, ksub) | (uintptr_t(1) << 42));
+int be_resolve_resident(int32_t kvariant, uint32_t dtype, int32_t ksub, void **fn) {
+  *fn = reinterpret_cast<void *>(encode(kvariant, dtype, ksub) | (uintptr_t(1) << 42));
   return 0;
 }
 
@@ -135,10 +135,12 @@ int be_launch_resident(void *fn, uint32_t grid, uint32_t block, uint32_t slot, v
   r.block = block;
   r.stream = stream;
   r.slot = int32_t(slot);
-  if (r.dtype <= 1 && slot < kResidentSlots &&
-      g_res_table[r.dtype][slot].tag == kResidentTag + slot) {
-    r.nargs = sizeof(ChainArgs);
-    memcpy(r.args, &g_res_table[r.dtype][slot].a, sizeof(ChainArgs));
+  const uint32_t fam = resident_family(r.kvariant);
+  if (fam < kResFamilies && r.dtype <= 1 && slot < kResidentSlots &&
+      g_res_table[fam][r.dtype][slot].tag == kResidentTag + slot) {
+    const ResidentBlock &b = g_res_table[fam][r.dtype][slot];
+    r.nargs = b.size;
+    memcpy(r.args, b.args, b.size);
   }
   g_log.push_back(r);
   return n == g_fail_at ? -1 : 0;
@@ -341,11 +343,17 @@ void trifake_resident_counts(int64_t *out) {
   out[0] = g_res_writes;
   out[1] = g_res_syncs;
 }
-// the stand-in table's slot s of dtype: its tag and grid (-1 out of range)
-int64_t trifake_resident_tag(int32_t dtype, int32_t s, uint32_t *grid) {
-  if (dtype < 0 || dtype > 1 || s < 0 || s >= int32_t(tri::kResidentSlots)) return -1;
-  if (grid) *grid = g_res_table[dtype][s].grid;
-  return int64_t(g_res_table[dtype][s].tag);
+// the stand-in table's slot s of a family and dtype: its tag, grid and
+// argument size (-1 out of range)
+int64_t trifake_resident_tag(int32_t family, int32_t dtype, int32_t s, uint32_t *grid,
+                             uint32_t *size) {
+  if (family < 0 || family >= int32_t(tri::kResFamilies) || dtype < 0 || dtype > 1 || s < 0 ||
+      s >= int32_t(tri::kResidentSlots))
+    return -1;
+  const tri::ResidentBlock &b = g_res_table[family][dtype][s];
+  if (grid) *grid = b.grid;
+  if (size) *size = b.size;
+  return int64_t(b.tag);
 }
 // slot of launch i (-1: a launch with arguments), or -2 if there is no launch i
 int32_t trifake_slot(int64_t i) {

@@ -86,7 +86,8 @@ def load_fake():
     lib.trifake_resident_write_fail.argtypes = [C.c_int]
     lib.trifake_force_capturing.argtypes = [C.c_int]
     lib.trifake_resident_counts.argtypes = [C.POINTER(C.c_int64)]
-    lib.trifake_resident_tag.argtypes = [C.c_int32, C.c_int32, C.POINTER(C.c_uint32)]
+    lib.trifake_resident_tag.argtypes = [C.c_int32, C.c_int32, C.c_int32,
+                                         C.POINTER(C.c_uint32), C.POINTER(C.c_uint32)]
     lib.trifake_resident_tag.restype = C.c_int64
     lib.trifake_slot.argtypes = [C.c_int64]
     lib.trifake_slot.restype = C.c_int32

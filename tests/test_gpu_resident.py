@@ -1,16 +1,18 @@
-"""GPU: fused-chain launches from resident argument blocks
-(TRI_CACHE_RESIDENT_ARGS) against the ordinary launches and the CPU oracle.
+"""GPU: launches from resident argument blocks (TRI_CACHE_RESIDENT_ARGS) --
+the fused chain, the three-launch chain and every standalone op -- against
+the ordinary launches and the CPU oracle.
 
 A resident launch takes no kernel arguments and finds its block in the
-device's table through its LDS allocation; its outputs must equal an
-ordinary launch's bit for bit, follow the data behind the held pointers on
-every call, and stay right when a slot is rewritten for another cache or a
-hit is replayed from a graph.
+device's table of its kernel family through its LDS allocation; its outputs
+must equal an ordinary launch's bit for bit and the oracle's, follow the
+data behind the held pointers on every call, and stay right when a slot is
+rewritten for another cache or a hit is replayed from a graph.
 """
 import numpy as np
 import pytest
 import torch
 
+from oracle import numerics as nm
 from oracle import ops as O
 from tests.parity import binding_rope_ext, check
 from tests.test_gpu_parity import CHAIN_CFGS, DEV, chain_oracle, host
@@ -230,3 +232,165 @@ def test_resident_hit_replays_from_a_hip_graph(tri):
         torch.cuda.synchronize()
         res.close()
         plain.close()
+
+
+# ---- the standalone ops and the three-launch chain -----------------------------------
+def rng(seed):
+    return np.random.Generator(np.random.PCG64(seed))
+
+
+def _out(d, name, like):
+    """Output tensor `name` of d, allocated on first use: calls reuse it, so
+    a cache sees the same argument block every time."""
+    if name not in d:
+        d[name] = torch.empty_like(like)
+    return d[name]
+
+
+def _op_case(name, seed):
+    """(host inputs, oracle outputs, runner) of one standalone op call. The
+    runner takes a cache and device copies of the inputs (outputs kept in the
+    same dict) and returns the device outputs by name (in-place outputs
+    included)."""
+    r = rng(seed)
+    bf, f32 = nm.BF16, nm.F32
+    if name in ("rmsnorm_bf16", "rmsnorm_f32_1024x128", "rmsnorm_wide_bf16"):
+        dt, T, H = {"rmsnorm_bf16": (bf, 1, 4096), "rmsnorm_f32_1024x128": (f32, 1024, 128),
+                    "rmsnorm_wide_bf16": (bf, 2, 57344)}[name]
+        h = {"x": wl.host_array(r, (T, H), dt), "w": wl.host_weight(r, H, dt)}
+        want = {"y": O.rmsnorm(h["x"], h["w"], 1e-6, dt)}
+        return dt, h, want, lambda c, d: {
+            "y": c.rmsnorm(d["x"], d["w"], 1e-6, out=_out(d, "y", d["x"]))}
+    if name in ("residual_bf16", "residual_split_bf16"):
+        T, H = (4, 8192) if name == "residual_bf16" else (2, 65536)
+        h = {"x": wl.host_array(r, (T, H), bf), "r": wl.host_array(r, (T, H), bf),
+             "w": wl.host_weight(r, H, bf)}
+        y, ro = O.residual_rmsnorm(h["x"], h["r"], h["w"], 1e-6, bf)
+
+        def run(c, d):
+            y_, ro_ = c.residual_rmsnorm(d["x"], d["r"], d["w"], 1e-6, out=_out(d, "y", d["x"]),
+                                         residual_out=_out(d, "ro", d["x"]))
+            return {"y": y_, "res_out": ro_}
+        return bf, h, {"y": y, "res_out": ro}, run
+    if name in ("rope_bf16", "qk_norm_rope_bf16"):
+        T, nq, nk, hd = 2, 32, 8, 128
+        pos = r.integers(0, 8192, size=T).astype(np.int32)
+        h = {"q": wl.host_array(r, (T, nq, hd), bf), "k": wl.host_array(r, (T, nk, hd), bf),
+             "pos": pos}
+        if name == "rope_bf16":
+            q, k = O.rope_qk(h["q"], h["k"], pos, 5e5, bf)
+
+            def run(c, d):
+                c.rope_qk(d["q"], d["k"], d["pos"], 5e5)
+                return {"q": d["q"], "k": d["k"]}
+        else:
+            h["qw"], h["kw"] = wl.host_weight(r, hd, bf), wl.host_weight(r, hd, bf)
+            q, k = O.qk_norm_rope(h["q"], h["k"], pos, 1e6, h["qw"], h["kw"], 1e-6, bf)
+
+            def run(c, d):
+                c.qk_norm_rope(d["q"], d["k"], d["pos"], d["qw"], d["kw"], 1e6, 1e-6)
+                return {"q": d["q"], "k": d["k"]}
+        return bf, h, {"q": q, "k": k}, run
+    if name == "swiglu_bf16":
+        h = {"g": wl.host_array(r, (1, 11008), bf), "u": wl.host_array(r, (1, 11008), bf)}
+        return bf, h, {"out": O.swiglu(h["g"], h["u"], bf)}, \
+            lambda c, d: {"out": c.swiglu(d["g"], d["u"], out=_out(d, "o", d["g"]))}
+    if name == "silu_bf16":
+        h = {"a": wl.host_array(r, (1, 4096), bf, outliers=True)}
+        return bf, h, {"out": O.silu(h["a"], bf)}, \
+            lambda c, d: {"out": c.silu(d["a"], out=_out(d, "o", d["a"]))}
+    if name == "add_f32":
+        h = {"a": wl.host_array(r, (2, 4096), f32), "b": wl.host_array(r, (2, 4096), f32)}
+        return f32, h, {"out": O.add(h["a"], h["b"], f32)}, \
+            lambda c, d: {"out": c.add(d["a"], d["b"], out=_out(d, "o", d["a"]))}
+    if name == "masked_fill_bf16":
+        h = {"a": wl.host_array(r, (2, 4096), bf),
+             "m": (r.random((2, 4096)) < 0.3).astype(np.uint8)}
+        return bf, h, {"out": O.masked_fill(h["a"], h["m"], -1e4, bf)}, \
+            lambda c, d: {"out": c.masked_fill(d["a"], d["m"], -1e4, out=_out(d, "o", d["a"]))}
+    if name == "embedding_bf16":
+        h = {"t": wl.host_array(r, (4000, 4096), bf),
+             "ids": r.integers(-2, 4002, size=8).astype(np.int32)}
+        return bf, h, {"out": O.embedding(h["t"], h["ids"], bf)}, \
+            lambda c, d: {"out": c.embedding(
+                d["t"], d["ids"], out=_out(d, "o", torch.empty((8, 4096), dtype=d["t"].dtype,
+                                                                device=DEV)))}
+    raise ValueError(name)
+
+
+OPS = ["rmsnorm_bf16", "rmsnorm_f32_1024x128", "rmsnorm_wide_bf16", "residual_bf16",
+       "residual_split_bf16", "rope_bf16", "qk_norm_rope_bf16", "swiglu_bf16", "silu_bf16",
+       "add_f32", "masked_fill_bf16", "embedding_bf16"]
+EXACT = {"res_out", "out"}   # outputs the oracle fixes bit for bit (silu's aside)
+
+
+def _to_device(h, dt):
+    out = {}
+    for k, v in h.items():
+        if k in ("pos", "ids", "m"):
+            out[k] = torch.from_numpy(v).to(DEV)
+        else:
+            out[k] = wl.to_torch(v, dt, DEV)
+    return out
+
+
+@pytest.mark.parametrize("name", OPS)
+def test_resident_standalone_op_equals_ordinary_and_oracle(tri, name):
+    """Three calls on each cache with the same inputs: the resident cache's
+    outputs equal the ordinary cache's bit for bit and the oracle's."""
+    dt, h, want, run = _op_case(name, seed=len(name) * 31)
+    plain, res = make_cache(tri), make_cache(tri, resident_args=True)
+    try:
+        a, b = _to_device(h, dt), _to_device(h, dt)
+        for call in range(3):
+            for d in (a, b):                  # inputs afresh (RoPE works in place)
+                for k, v in _to_device(h, dt).items():
+                    d[k].copy_(v)
+            ga = run(plain, a)
+            gb = run(res, b)
+            torch.cuda.synchronize()
+            for n in want:
+                check(f"{name} call {call} {n}", host(gb[n]), host(ga[n]), dt, exact=True)
+            assert res.last_selection().as_tuple()[3:] == plain.last_selection().as_tuple()[3:]
+        info = res.resident_info()
+        assert info["held"] == 1 and info["launches"] == 3, info
+        for n, w in want.items():
+            exact = n in EXACT and name != "silu_bf16"
+            check(f"{name} {n} vs oracle", host(gb[n]), w, dt, exact=exact)
+    finally:
+        torch.cuda.synchronize()
+        plain.close()
+        res.close()
+
+
+def test_resident_three_launch_chain(tri):
+    """An unaligned GQA chain runs three launches (norm, RoPE, SwiGLU): each
+    from its family's resident table, outputs equal to the ordinary cache's
+    and the oracle's."""
+    cfg = wl.GQA_DECODE
+    inp = wl.host_inputs(cfg)
+    from tests.test_gpu_parity import empty_like_layout, place
+
+    def dev_inputs():
+        d = {k: place(v, cfg.dtype, "unaligned") if k not in ("w", "pos") else
+             wl.to_torch(v, cfg.dtype, DEV) for k, v in inp.items()}
+        d["y"], d["res_out"], d["out"] = (empty_like_layout(d["x"]), empty_like_layout(d["x"]),
+                                          empty_like_layout(d["gate"]))
+        return d
+    a, b = dev_inputs(), dev_inputs()
+    plain, res = make_cache(tri), make_cache(tri, resident_args=True)
+    try:
+        plain.decode_chain_args(args_of(tri, plain, cfg, a))
+        res.decode_chain_args(args_of(tri, res, cfg, b))
+        torch.cuda.synchronize()
+        assert res.last_selection().n_launches == 3
+        assert res.resident_info() == {"enabled": 1, "held": 3, "launches": 3}
+        same_outputs("three launches", b, a, cfg.dtype)
+        want = O.decode_chain(inp, cfg.eps, cfg.base, cfg.dtype)
+        for n in ("y", "q", "k", "out"):
+            check(n, host(b[n]), want[n], cfg.dtype)
+        check("res_out", host(b["res_out"]), want["res_out"], cfg.dtype, exact=True)
+    finally:
+        torch.cuda.synchronize()
+        plain.close()
+        res.close()

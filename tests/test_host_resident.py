@@ -1,10 +1,10 @@
 """Resident argument blocks (TRI_CACHE_RESIDENT_ARGS) on the CPU, against the
 recording backend: which launches take a held block, what block the kernel
-finds in its slot, the slot pool shared by caches, and the cases that must
-launch with kernel arguments instead (full table or pool, a captured stream,
-a failed device check or copy, large grids, three-launch plans, compiled
-specializations). Selection records and statistics stay those of the
-oracle's selection model.
+finds in its slot, the slot pools shared by caches (one per kernel family
+and dtype), and the cases that must launch with kernel arguments instead
+(full table or pool, a captured stream, a failed device check or copy,
+large grids, compiled specializations, the allocation-free entry point).
+Selection records and statistics stay those of the oracle's selection model.
 """
 import ctypes as C
 
@@ -12,7 +12,8 @@ import pytest
 
 from oracle import selection as S
 from tests.native_libs import load_fake
-from tests.selection_calls import chain_call, elem_offset
+from tests.selection_calls import (add_call, chain_call, elem_offset, emb_call, mf_call,
+                                   qkn_call, res_call, rn_call, rope_call, silu_call, sw_call)
 from tests.test_host_cache import _chain_struct, c_call, c_layers, call_zoo, run_both
 import workloads as wl
 
@@ -22,6 +23,24 @@ SLOTS, MAX_GRID = 40, 512
 TAG = 0x52455300
 CHAIN_BYTES = 288
 INV_FREQ = slice(112, 120)   # RopeArgs.inv_freq inside the chain block: per-version constants
+FAM_CHAIN, FAM_NORM, FAM_ROPE, FAM_SW, FAM_ELT, FAM_EMB = range(6)
+
+
+def family(kv):
+    """The resident table family of a kernel variant (None: no table)."""
+    if kv == S.CH_FUSED:
+        return FAM_CHAIN
+    if kv in S.NORM_VARIANTS:
+        return FAM_NORM
+    if S.ROPE_SCALAR <= kv <= S.ROPE_QKN_VEC_I:
+        return FAM_ROPE
+    if S.SW_SCALAR <= kv <= S.SW_ROWS:
+        return FAM_SW
+    if S.ELT_SCALAR <= kv <= S.ELT_ROWS:
+        return FAM_ELT
+    if kv in (S.EMB_SCALAR, S.EMB_VEC):
+        return FAM_EMB
+    return None
 
 
 @pytest.fixture(scope="module")
@@ -101,29 +120,31 @@ def test_resident_launch_finds_the_ordinary_block(lib, fresh):
         # the same kernel variant, geometry and block, from the same slot
         assert s == slot and geom == ordinary
         assert masked(raw) == masked(raw0)
-    grid = C.c_uint32()
-    assert lib.trifake_resident_tag(BF, slot, C.byref(grid)) == TAG + slot
-    assert grid.value == ordinary[3]
+    grid, size = C.c_uint32(), C.c_uint32()
+    assert lib.trifake_resident_tag(FAM_CHAIN, BF, slot, C.byref(grid), C.byref(size)) == \
+        TAG + slot
+    assert (grid.value, size.value) == (ordinary[3], CHAIN_BYTES)
     assert counts(lib)[0] == 1                  # one copy, on the first call
     assert info(lib, cache) == (1, 1, 5)
 
 
 def test_selection_parity_over_call_zoo_with_resident_blocks(lib, fresh):
-    """Records and statistics are the model's; a fused launch of at most 512
-    workgroups takes a held block while the dtype's table has room; blocks
-    are held in first-seen order and repeats find their slot again."""
+    """Records and statistics are the model's; a launch of at most 512
+    workgroups takes a held block while its family's table for the dtype has
+    room; blocks are held in first-seen order and repeats find their slot
+    again."""
     cache = fresh(capacity=4096, flags=RES)
     m = S.SpecCacheModel(capacity=4096)
     for _ in range(2):
         for c in call_zoo():
             run_both(lib, cache, m, c)
-    held = {BF: {}, F: {}}
+    held = {}
     for slot, kv, dt, sub, grid, block, raw in launches(lib):
-        if kv != S.CH_FUSED or grid > MAX_GRID:
+        if family(kv) is None or grid > MAX_GRID:
             assert slot == -1
             continue
         key = (raw, grid)
-        table = held[dt]
+        table = held.setdefault((family(kv), dt), {})
         if key in table:
             assert slot == table[key]
         elif len(table) < SLOTS:
@@ -131,9 +152,9 @@ def test_selection_parity_over_call_zoo_with_resident_blocks(lib, fresh):
             table[key] = slot
         else:
             assert slot == -1
-    assert held[BF] and held[F]
+    assert {f for f, _ in held} == {FAM_CHAIN, FAM_NORM, FAM_ROPE, FAM_SW, FAM_ELT, FAM_EMB}
     enabled, n_held, _ = info(lib, cache)
-    assert (enabled, n_held) == (1, len(held[BF]) + len(held[F]))
+    assert (enabled, n_held) == (1, sum(len(t) for t in held.values()))
     assert counts(lib)[0] == n_held
 
 
@@ -150,11 +171,13 @@ def test_mixed_stream_with_resident_blocks(lib, fresh):
         run_both(lib, cache, m, c)
     got = launches(lib)
     res = [g for g in got if g[0] >= 0]
-    # every small fused launch is resident (fewer distinct blocks than slots)
-    assert all(g[0] >= 0 for g in got if g[1] == S.CH_FUSED and g[4] <= MAX_GRID)
-    assert all(g[1] == S.CH_FUSED and g[4] <= MAX_GRID for g in res)
+    # every launch of at most 512 workgroups is resident (fewer distinct
+    # blocks than slots), three-launch chains included
+    assert all(g[0] >= 0 for g in got if g[4] <= MAX_GRID)
+    assert all(g[4] <= MAX_GRID for g in res)
+    assert any(g[1] != S.CH_FUSED for g in res)
     assert len(res) > 1500
-    assert counts(lib)[0] == info(lib, cache)[1] <= 2 * SLOTS
+    assert counts(lib)[0] == info(lib, cache)[1]
 
 
 def test_layers_hold_one_block_per_layer(lib, fresh):
@@ -209,8 +232,7 @@ def test_slots_return_to_the_pool_when_the_cache_is_destroyed(lib):
         n0 = lib.trifake_launch_count()
         assert c_call(lib, b, llama(100)) == 0
         assert launches(lib, n0)[0][0] == 0               # a freed slot, rewritten
-        grid = C.c_uint32()
-        assert lib.trifake_resident_tag(BF, 0, C.byref(grid)) == TAG
+        assert lib.trifake_resident_tag(FAM_CHAIN, BF, 0, None, None) == TAG
     finally:
         if a:
             lib.tri_spec_cache_destroy(a)
@@ -269,18 +291,19 @@ def test_failed_check_or_copy_launches_with_arguments(lib, fresh):
     assert info(lib, cache) == (1, 1, 1)
 
 
-def test_only_small_fused_launches_of_precompiled_versions_are_resident(lib, fresh):
+def test_only_small_launches_of_precompiled_versions_are_resident(lib, fresh):
     cache = fresh(flags=AUTO | RES)
     m = S.SpecCacheModel(flags=S.FLAG_AUTO_INSTALL)
     for T in (1, 8, 64, 512, 4096):
         run_both(lib, cache, m, llama(T=T), install=False)
-    # a chain whose norm rows are split runs three launches
+    # a chain whose norm rows are split runs three launches, each resident
     run_both(lib, cache, m, chain_call(BF, 2, 65536, 11008, 32, 32, 128), install=False)
     got = launches(lib)
     assert any(g[4] > MAX_GRID for g in got)
     for slot, kv, dt, sub, grid, block, raw in got:
-        assert (slot >= 0) == (kv == S.CH_FUSED and grid <= MAX_GRID), (kv, grid)
-    assert sum(g[1] != S.CH_FUSED for g in got) == 3
+        assert (slot >= 0) == (grid <= MAX_GRID), (kv, grid)
+    assert [family(g[1]) for g in got[-3:]] == [FAM_NORM, FAM_ROPE, FAM_SW]
+    assert got[-3][1] == S.RN_SPLIT and len(got[-3][-1]) == CHAIN_BYTES
     # compiled specializations carry their arguments
     jc = fresh(flags=AUTO | RES | JIT)
     assert c_call(lib, jc, llama()) == 0
@@ -296,3 +319,55 @@ def test_resident_info_arguments(lib, fresh):
     cache = fresh()
     assert lib.tri_spec_resident_info(cache, None) == S.E_INVALID
     assert info(lib, cache) == (0, 0, 0)
+
+
+STANDALONE = [
+    (FAM_NORM, lambda o: rn_call(BF, 1, 4096, off=o)),
+    (FAM_NORM, lambda o: res_call(F, 4, 4096, off=o)),
+    (FAM_NORM, lambda o: rn_call(F, 1024, 128, off=o)),        # the paper's rms_norm case
+    (FAM_ROPE, lambda o: rope_call(BF, 1, 32, 8, 128, off=o)),
+    (FAM_ROPE, lambda o: qkn_call(BF, 1, 32, 8, 128, off=o)),
+    (FAM_SW, lambda o: sw_call(BF, 1, 11008, off=o)),
+    (FAM_ELT, lambda o: silu_call(BF, 1, 4096, off=o)),
+    (FAM_ELT, lambda o: add_call(F, 2, 4096, off=o)),
+    (FAM_ELT, lambda o: mf_call(BF, 2, 4096, off=o)),
+    (FAM_EMB, lambda o: emb_call(BF, 8, 4096, 32000, off=o)),
+]
+
+
+@pytest.mark.parametrize("fam,make", STANDALONE)
+def test_standalone_ops_take_held_blocks_of_their_family(lib, fresh, fam, make):
+    """Each op's launch finds its own argument block in its family's table:
+    the same kernel variant, geometry and bytes as an ordinary cache's
+    launch; a second block of the same op takes the next slot."""
+    plain = fresh(flags=AUTO)
+    m = S.SpecCacheModel(flags=S.FLAG_AUTO_INSTALL)
+    run_both(lib, plain, m, make(0), install=False)
+    (slot0, *ordinary, raw0), = launches(lib)
+    assert slot0 == -1
+    cache = fresh(flags=AUTO | RES)
+    m = S.SpecCacheModel(flags=S.FLAG_AUTO_INSTALL)
+    for c in (make(0), make(0), make(1 << 20), make(0)):
+        run_both(lib, cache, m, c, install=False)
+    got = launches(lib)
+    assert [g[0] for g in got] == [0, 0, 1, 0]
+    for slot, *geom, raw in (got[0], got[1], got[3]):
+        assert geom == ordinary
+        n = lib.trifake_resident_tag(fam, geom[1], slot, None, None)
+        assert n == TAG + slot
+        if fam == FAM_ROPE:                   # but the version's own frequency table
+            assert raw[:24] + raw[32:] == raw0[:24] + raw0[32:]
+        else:
+            assert raw == raw0
+    assert family(got[0][1]) == fam
+    assert info(lib, cache) == (1, 2, 4)
+
+
+def test_noalloc_entry_always_carries_its_arguments(lib, fresh):
+    cache = fresh(flags=AUTO | RES)
+    c = res_call(BF, 1, 4096)
+    assert c_call(lib, cache, c) == 0                   # installs; resident
+    from tests.test_host_noalloc import noalloc
+    assert noalloc(lib, cache, c) == 0
+    assert [g[0] for g in launches(lib)] == [0, -1]
+    assert counts(lib)[0] == 1
