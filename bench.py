@@ -136,10 +136,12 @@ def measured_traffic():
     return float(fields["chain_traffic_bytes"])
 
 
-def run_mixed_stream(tri, wl, bench, dev, stream, torch, autotune=False, generic=False):
+def run_mixed_stream(tri, wl, bench, dev, stream, torch, autotune=False, generic=False,
+                     resident=False):
     """The 10,000-call mixed stream: token counts 1..512, 90 % bf16, 5 % unaligned
     or padded layouts, through a fresh cache (installs timed and tuned with
-    `autotune`; generic versions with `generic`); every call synchronised."""
+    `autotune`; generic versions with `generic`; resident argument blocks
+    with `resident`); every call synchronised."""
     Tmax = max(wl.MIXED_T_CHOICES)
     H, I, nq, nk, hd = wl.MIXED_H, wl.MIXED_I, wl.MIXED_NQ, wl.MIXED_NK, wl.MIXED_HD
     calls = wl.mixed_stream()
@@ -157,7 +159,7 @@ def run_mixed_stream(tri, wl, bench, dev, stream, torch, autotune=False, generic
         return torch.randn(shape, device=dev).to(td)
 
     arr = (tri.ChainArgs * len(calls))()
-    cache = tri.SpecCache(autotune=autotune, generic=generic)
+    cache = tri.SpecCache(autotune=autotune, generic=generic, resident_args=resident)
     for i, (T, dt, layout) in enumerate(calls):
         if (dt, layout) not in bufs:
             td = torch.bfloat16 if dt == wl.BF16 else torch.float32
@@ -181,6 +183,7 @@ def run_mixed_stream(tri, wl, bench, dev, stream, torch, autotune=False, generic
     st = bench.trib_stream(cache.handle, arr, n, stream.cuda_stream, e2e, missed)
     assert st == 0, st
     stats = cache.stats()
+    res_info = cache.resident_info() if resident else None
     per_bucket = {}
     for (T, _, _), t, m in zip(calls, e2e, missed):
         if not m:
@@ -205,6 +208,7 @@ def run_mixed_stream(tri, wl, bench, dev, stream, torch, autotune=False, generic
                                   for T, v in sorted(per_bucket.items())},
         "miss_handling_e2e_us": summary(miss_t) if miss_t else None,
         "cache_stats": stats,
+        "resident_blocks": res_info,
     }
 
 
@@ -664,6 +668,8 @@ def main():
                                                                torch, autotune=True)
     mixed_generic = None if args.no_stream else run_mixed_stream(tri, wl, bench, dev, stream,
                                                                  torch, generic=True)
+    mixed_resident = None if args.no_stream else run_mixed_stream(tri, wl, bench, dev, stream,
+                                                                  torch, resident=True)
 
     # ---- the 1-token chain through a tuning cache --------------------------------------
     tc = tri.SpecCache(autotune=True)
@@ -936,6 +942,7 @@ def main():
     latency["mixed_stream"] = mixed
     latency["mixed_stream_autotuned"] = mixed_tuned
     latency["mixed_stream_generic"] = mixed_generic
+    latency["mixed_stream_resident"] = mixed_resident
     emit(args, ce, wall, latency, bandwidth, roofline, cpu)
 
 
