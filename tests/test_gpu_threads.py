@@ -43,11 +43,13 @@ def _run_threads(fn, n):
     assert not errors, errors
 
 
-def test_one_cache_per_thread(tri):
+@pytest.mark.parametrize("resident", [False, True], ids=["kernel_args", "resident"])
+def test_one_cache_per_thread(tri, resident):
     """Four threads, each with its own cache, stream and buffers, 200 decode
     chains each (q / k restored before every call); the last results match
-    the oracle."""
-    print("threads: one cache per thread", flush=True)
+    the oracle. With resident argument blocks the caches claim slots of the
+    device's shared pools at the same time and each launch finds its own."""
+    print(f"threads: one cache per thread (resident={resident})", flush=True)
     cfgs = [wl.LLAMA7B_DECODE, wl.GQA_DECODE, wl.QWEN3_8B_DECODE, wl.TINY_F32]
     results = {}
 
@@ -55,7 +57,7 @@ def test_one_cache_per_thread(tri):
         cfg = cfgs[i]
         inp = wl.host_inputs(cfg, seed=100 + i)
         stream = torch.cuda.Stream(device=DEV)
-        cache = tri.SpecCache(auto_install=True)
+        cache = tri.SpecCache(auto_install=True, resident_args=resident)
         try:
             with torch.cuda.stream(stream):
                 d = {k: wl.to_torch(v, cfg.dtype, DEV) for k, v in inp.items()}
@@ -74,6 +76,8 @@ def test_one_cache_per_thread(tri):
             stream.synchronize()
             st = cache.stats()
             assert (st["hits"], st["misses"], st["n_versions"]) == (199, 1, 1)
+            if resident:
+                assert cache.resident_info() == {"enabled": 1, "held": 1, "launches": 200}
             results[i] = (inp, dict(y=host(y), res_out=host(ro), out=host(out),
                                     q=host(d["q"]), k=host(d["k"])))
         finally:
