@@ -371,3 +371,65 @@ def test_noalloc_entry_always_carries_its_arguments(lib, fresh):
     assert noalloc(lib, cache, c) == 0
     assert [g[0] for g in launches(lib)] == [0, -1]
     assert counts(lib)[0] == 1
+
+
+# ---- random calls: a resident cache launches exactly what an ordinary one does -------------
+from hypothesis import given, strategies as st  # noqa: E402
+
+from tests.test_host_fuzz import (SETTINGS, chain_calls, norm_calls, rope_calls,  # noqa: E402
+                                  short_calls)
+
+
+def _version_fields(kv):
+    """Byte ranges of a launch's block that hold the version's own device
+    memory (RoPE frequency table, split-row scratch): equal within a cache,
+    different between two caches."""
+    if kv == S.CH_FUSED:
+        return [INV_FREQ]
+    if S.ROPE_SCALAR <= kv <= S.ROPE_QKN_VEC_I:
+        return [slice(24, 32)]
+    if kv == S.RN_SPLIT:
+        return [slice(88, 96)]
+    return []
+
+
+def _masked_block(kv, raw):
+    b = bytearray(raw)
+    for sl in _version_fields(kv):
+        b[sl] = bytes(sl.stop - sl.start)
+    return bytes(b)
+
+
+def _run_log(lib, calls, flags):
+    lib.trifake_reset()
+    h = C.c_void_p()
+    assert lib.tri_spec_cache_create(C.byref(h), S.MAX_CAPACITY, flags) == 0
+    try:
+        sts = [c_call(lib, h, c) for c in calls]
+        return sts, launches(lib), info(lib, h)
+    finally:
+        lib.tri_spec_cache_destroy(h)
+
+
+@SETTINGS
+@given(st.lists(st.one_of(norm_calls(), rope_calls(), short_calls(), chain_calls()),
+                min_size=1, max_size=8))
+def test_random_calls_launch_the_same_from_resident_blocks(lib, calls):
+    calls = calls + calls                       # every block seen twice
+    st_a, log_a, _ = _run_log(lib, calls, AUTO)
+    st_b, log_b, (enabled, n_held, n_res) = _run_log(lib, calls, AUTO | RES)
+    assert st_a == st_b
+    assert len(log_a) == len(log_b)
+    seen = {}
+    for (sa, *ga, ra), (sb, *gb, rb) in zip(log_a, log_b):
+        assert sa == -1 and ga == gb
+        kv, dt, grid = gb[0], gb[1], gb[3]
+        assert _masked_block(kv, rb) == _masked_block(kv, ra)
+        if family(kv) is None or grid > MAX_GRID:
+            assert sb == -1
+        else:                                   # few blocks: every table has room
+            assert sb >= 0
+            key = (family(kv), dt, rb, grid)
+            assert seen.setdefault(key, sb) == sb
+    assert (enabled, n_held) == (1, len(seen))
+    assert n_res == sum(1 for g in log_b if g[0] >= 0)
