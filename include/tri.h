@@ -103,9 +103,9 @@ enum {
 };
 
 /* Resident argument blocks (TRI_CACHE_RESIDENT_ARGS): blocks per device,
- * kernel family and dtype, and the largest launch (workgroups) that uses
- * one. */
-enum { TRI_RESIDENT_SLOTS = 40, TRI_RESIDENT_MAX_GRID = 512 };
+ * kernel family and dtype; the largest launch (workgroups) that may take
+ * any of them; the first blocks, which launches of any size may take. */
+enum { TRI_RESIDENT_SLOTS = 40, TRI_RESIDENT_MAX_GRID = 512, TRI_RESIDENT_ANY_GRID_SLOTS = 10 };
 
 /* Divisibility class of a generic version's hidden-size range
  * (tri_version_info.h_mod). */
@@ -321,10 +321,9 @@ typedef struct tri_chain_args {
  * per-call launch cost the paper measures in Sec. 2.3): the runtime places
  * a launch's kernel arguments in device memory on every launch, which costs
  * about as much host and end-to-end time as the 1-token chain's whole
- * kernel. With this flag a launch of at most TRI_RESIDENT_MAX_GRID
- * workgroups by a precompiled version takes its argument block from a table
- * in device memory instead -- every op's launches, the fused chain's and the
- * three of a three-launch chain. The first call with a given block (every
+ * kernel. With this flag a launch by a precompiled version takes its
+ * argument block from a table in device memory instead -- every op's
+ * launches, the fused chain's and the three of a three-launch chain. The first call with a given block (every
  * pointer, stride, size, eps and the launch geometry equal) copies it into
  * a free slot of the device's table for the kernel's family (the chain,
  * norms, RoPE, SwiGLU, element-wise ops, embedding) and dtype
@@ -338,12 +337,17 @@ typedef struct tri_chain_args {
  * ordinary launch's bit for bit, and the selection records are the same. A
  * held block is never rewritten while the cache lives; slots return to the
  * device's pool when the cache is destroyed (after the device has finished
- * its work). Calls launch as without the flag (kernel arguments) when the
- * cache holds TRI_RESIDENT_SLOTS blocks of the family and dtype or the pool
- * has none free, when the block is new while the caller's stream is being
- * captured, for compiled specializations (TRI_CACHE_JIT), larger grids and
- * tri_residual_rmsnorm_noalloc, and on a device that fails the check made
- * at creation (launches at several LDS sizes whose slot the kernel must
+ * its work). Slot k costs k x 1280 bytes of LDS per workgroup: a launch of
+ * more than TRI_RESIDENT_MAX_GRID workgroups only takes one of the first
+ * TRI_RESIDENT_ANY_GRID_SLOTS slots, at which the most workgroups a compute
+ * unit runs at once (eight of 256 work-items) still fit its 160 KB of LDS
+ * beside the kernels' own, so a large launch never runs fewer workgroups at
+ * once. Calls launch as without the flag (kernel arguments) when the cache
+ * holds TRI_RESIDENT_SLOTS blocks of the family and dtype or the pool has
+ * no slot free that the launch may take, when the block is new while the
+ * caller's stream is being captured, for compiled specializations
+ * (TRI_CACHE_JIT) and tri_residual_rmsnorm_noalloc, and on a device that
+ * fails the check made at creation (launches at several LDS sizes whose slot the kernel must
  * read back exactly). tri_spec_resident_info tells how many launches used a
  * held block. A first call with a new block synchronizes a private stream:
  * make it before another thread starts a global-mode stream capture. */

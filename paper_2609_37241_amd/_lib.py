@@ -25,7 +25,7 @@ JIT = 2
 AUTOTUNE = 4
 GENERIC = 8
 RESIDENT_ARGS = 16
-RESIDENT_SLOTS, RESIDENT_MAX_GRID = 40, 512
+RESIDENT_SLOTS, RESIDENT_MAX_GRID, RESIDENT_ANY_GRID_SLOTS = 40, 512, 10
 TUNE_NONE, TUNE_MEASURED, TUNE_STORED, TUNE_SKIPPED = 0, 1, 2, 3
 KEY_WORDS = 6
 NOALLOC_SCRATCH_BYTES = 1 << 20

@@ -326,14 +326,16 @@ int chain_check(const tri_chain_args *p, Key *out) {
 }
 
 // Launch i of version v of cache c with its argument block: from a
-// resident block when the launch has an argument-free form, its grid is at
-// most kResidentMaxGrid and the cache holds (or can hold) the block;
+// resident block when the launch has an argument-free form and the cache
+// holds (or can hold) the block in a slot the launch may take (any slot up
+// to kResidentMaxGrid workgroups, else the first kResidentAnyGridSlots);
 // otherwise with kernel arguments. 0 or the launch's failure code.
 int launch(tri_cache *c, const Version &v, int i, uint32_t dtype, uint32_t grid, uint32_t block,
            const void *args, uint32_t size, void *stream) {
-  if (v.fn_res[i] && grid <= kResidentMaxGrid) {
-    const int32_t slot =
-        resident_slot(c, resident_family(v.plan.kvariant[i]), dtype, args, size, grid, stream);
+  if (v.fn_res[i]) {
+    const uint32_t limit = grid <= kResidentMaxGrid ? kResidentSlots : kResidentAnyGridSlots;
+    const int32_t slot = resident_slot(c, resident_family(v.plan.kvariant[i]), dtype, args,
+                                       size, grid, stream, limit);
     if (slot >= 0) {
       const int rc = be_launch_resident(v.fn_res[i], grid, block, uint32_t(slot), stream);
       if (rc == 0) c->resident_launches++;

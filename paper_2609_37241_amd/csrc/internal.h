@@ -259,7 +259,14 @@ int be_launch_resident(void *fn, uint32_t grid, uint32_t block, uint32_t slot, v
 int be_stream_capturing(void *stream);
 void be_device_sync(int device);
 static_assert(kResidentSlots == uint32_t(TRI_RESIDENT_SLOTS), "resident slots");
+// Launches of more than kResidentMaxGrid workgroups take only slots below
+// kResidentAnyGridSlots: slot k adds k * kLdsGranule bytes of LDS per
+// workgroup, and up to slot 9 eight 256-lane workgroups (a compute unit's
+// most) with at most 7 granules of static LDS still fit its 160 KB.
 constexpr uint32_t kResidentMaxGrid = TRI_RESIDENT_MAX_GRID;
+constexpr uint32_t kResidentAnyGridSlots = TRI_RESIDENT_ANY_GRID_SLOTS;
+static_assert(8 * (kResidentAnyGridSlots - 1 + 7) * kLdsGranule <= 160 * 1024,
+              "any-grid slots keep eight workgroups per compute unit");
 // The resident family of a kernel variant (kResFamilies: none).
 inline uint32_t resident_family(int32_t kvariant) {
   if (kvariant == CH_FUSED) return kResChain;
@@ -334,11 +341,11 @@ struct tri_cache {
 
 namespace tri {
 // The slot of a held block of the family and dtype equal to the `size`
-// bytes at `args` and `grid`, holding a new one when the cache and the
-// device's pool have room and `stream` is not being captured; -1: launch
-// with kernel arguments (resident.cpp).
+// bytes at `args` and `grid`, holding a new one in a free slot below
+// `limit` when the cache and the device's pool have room and `stream` is
+// not being captured; -1: launch with kernel arguments (resident.cpp).
 int32_t resident_slot(tri_cache *c, uint32_t family, uint32_t dtype, const void *args,
-                      uint32_t size, uint32_t grid, void *stream);
+                      uint32_t size, uint32_t grid, void *stream, uint32_t limit);
 // Return the cache's slots to the device's pool (after the device is idle).
 void resident_release_all(tri_cache *c);
 }  // namespace tri

@@ -26,11 +26,12 @@ bool pool_index_ok(int device, uint32_t fam, uint32_t dt) {
   return device >= 0 && device < kMaxDevices && fam < kResFamilies && dt <= 1;
 }
 
-int32_t pool_claim(int device, uint32_t fam, uint32_t dt) {
+// The lowest free slot below `limit`, or -1.
+int32_t pool_claim(int device, uint32_t fam, uint32_t dt, uint32_t limit) {
   if (!pool_index_ok(device, fam, dt)) return -1;
   std::lock_guard<std::mutex> lock(g_pool_mu);
   uint64_t &used = g_pool_used[device][fam][dt];
-  for (uint32_t s = 0; s < kResidentSlots; ++s) {
+  for (uint32_t s = 0; s < limit && s < kResidentSlots; ++s) {
     if (!((used >> s) & 1u)) {
       used |= uint64_t(1) << s;
       return int32_t(s);
@@ -56,7 +57,7 @@ inline ResidentBlock *held_of(tri_cache *c, uint32_t fam, uint32_t dt) {
 }  // namespace
 
 int32_t resident_slot(tri_cache *c, uint32_t fam, uint32_t dt, const void *args, uint32_t size,
-                      uint32_t grid, void *stream) {
+                      uint32_t grid, void *stream, uint32_t limit) {
   if (fam >= kResFamilies || dt > 1 || !c->rtable[fam][dt] || !c->held ||
       size > kResidentArgsMax)
     return -1;
@@ -64,6 +65,8 @@ int32_t resident_slot(tri_cache *c, uint32_t fam, uint32_t dt, const void *args,
   const uint32_t n = c->n_held[fam][dt];
   // The last match first, then the blocks after it: the layers of a decode
   // step come round in the order they were first seen.
+  // A held block's grid is part of it, so its slot is below the limit its
+  // launches have.
   for (uint32_t i = 0, j = c->last_held[fam][dt]; i < n; ++i, j = j + 1 == n ? 0 : j + 1) {
     if (same_block(h[j], args, size, grid)) {
       c->last_held[fam][dt] = j;
@@ -74,7 +77,7 @@ int32_t resident_slot(tri_cache *c, uint32_t fam, uint32_t dt, const void *args,
   // it; never while the caller's stream is captured (the copy is no part of
   // the caller's graph).
   if (n >= kResidentSlots || be_stream_capturing(stream) != 0) return -1;
-  const int32_t s = pool_claim(c->device, fam, dt);
+  const int32_t s = pool_claim(c->device, fam, dt, limit);
   if (s < 0) return -1;
   ResidentBlock b;
   memset(&b, 0, sizeof b);

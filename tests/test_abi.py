@@ -47,12 +47,12 @@ def test_struct_layouts_match_the_header(tmp_path):
     from paper_2609_37241_amd import _lib as L
     src = tmp_path / "sz.c"
     src.write_text('#include "tri.h"\n#include <stdio.h>\n#include <stddef.h>\n'
-                   'int main(void){printf("%zu %zu %zu %zu %zu %zu %zu %zu %d %d\\n",'
+                   'int main(void){printf("%zu %zu %zu %zu %zu %zu %zu %zu %d %d %d\\n",'
                    ' sizeof(tri_selection), sizeof(tri_chain_args), sizeof(tri_stats),'
                    ' sizeof(tri_version_info), offsetof(tri_chain_args, pos),'
                    ' offsetof(tri_selection, key), sizeof(tri_resident_info),'
                    ' offsetof(tri_resident_info, launches), TRI_RESIDENT_SLOTS,'
-                   ' TRI_RESIDENT_MAX_GRID);return 0;}\n')
+                   ' TRI_RESIDENT_MAX_GRID, TRI_RESIDENT_ANY_GRID_SLOTS);return 0;}\n')
     exe = tmp_path / "sz"
     import subprocess
     subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)],
@@ -62,7 +62,7 @@ def test_struct_layouts_match_the_header(tmp_path):
     want = [C.sizeof(L.Selection), C.sizeof(L.ChainArgs), C.sizeof(L.Stats),
             C.sizeof(L.VersionInfo), L.ChainArgs.pos.offset, L.Selection.key.offset,
             C.sizeof(L.ResidentInfo), L.ResidentInfo.launches.offset, L.RESIDENT_SLOTS,
-            L.RESIDENT_MAX_GRID]
+            L.RESIDENT_MAX_GRID, L.RESIDENT_ANY_GRID_SLOTS]
     assert got == want
 
 

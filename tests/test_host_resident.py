@@ -19,7 +19,7 @@ import workloads as wl
 
 BF, F = S.DT_BF16, S.DT_F32
 AUTO, JIT, RES = 1, 2, 16
-SLOTS, MAX_GRID = 40, 512
+SLOTS, MAX_GRID, ANY_GRID_SLOTS = 40, 512, 10
 TAG = 0x52455300
 CHAIN_BYTES = 288
 INV_FREQ = slice(112, 120)   # RopeArgs.inv_freq inside the chain block: per-version constants
@@ -41,6 +41,31 @@ def family(kv):
     if kv in (S.EMB_SCALAR, S.EMB_VEC):
         return FAM_EMB
     return None
+
+
+class PoolModel:
+    """The slot each launch of one resident cache takes: a held block keeps
+    its slot; a new block takes the lowest free slot of its family and dtype
+    (below ANY_GRID_SLOTS for launches beyond MAX_GRID workgroups), or none
+    (-1: kernel arguments)."""
+
+    def __init__(self):
+        self.used, self.held = {}, {}
+
+    def expect(self, kv, dt, grid, raw):
+        fam = family(kv)
+        if fam is None:
+            return -1
+        key = (fam, dt, raw, grid)
+        if key not in self.held:
+            used = self.used.setdefault((fam, dt), set())
+            limit = SLOTS if grid <= MAX_GRID else ANY_GRID_SLOTS
+            free = [k for k in range(limit) if k not in used]
+            if not free:
+                return -1
+            used.add(free[0])
+            self.held[key] = free[0]
+        return self.held[key]
 
 
 @pytest.fixture(scope="module")
@@ -138,23 +163,13 @@ def test_selection_parity_over_call_zoo_with_resident_blocks(lib, fresh):
     for _ in range(2):
         for c in call_zoo():
             run_both(lib, cache, m, c)
-    held = {}
-    for slot, kv, dt, sub, grid, block, raw in launches(lib):
-        if family(kv) is None or grid > MAX_GRID:
-            assert slot == -1
-            continue
-        key = (raw, grid)
-        table = held.setdefault((family(kv), dt), {})
-        if key in table:
-            assert slot == table[key]
-        elif len(table) < SLOTS:
-            assert slot >= 0 and slot not in table.values()
-            table[key] = slot
-        else:
-            assert slot == -1
-    assert {f for f, _ in held} == {FAM_CHAIN, FAM_NORM, FAM_ROPE, FAM_SW, FAM_ELT, FAM_EMB}
+    pm = PoolModel()
+    got = launches(lib)
+    for slot, kv, dt, sub, grid, block, raw in got:
+        assert slot == pm.expect(kv, dt, grid, raw), (kv, dt, grid)
+    assert {f for f, _ in pm.used} == {FAM_CHAIN, FAM_NORM, FAM_ROPE, FAM_SW, FAM_ELT, FAM_EMB}
     enabled, n_held, _ = info(lib, cache)
-    assert (enabled, n_held) == (1, sum(len(t) for t in held.values()))
+    assert (enabled, n_held) == (1, len(pm.held))
     assert counts(lib)[0] == n_held
 
 
@@ -170,13 +185,14 @@ def test_mixed_stream_with_resident_blocks(lib, fresh):
                        sw_pad=pad)
         run_both(lib, cache, m, c)
     got = launches(lib)
+    pm = PoolModel()
+    for slot, kv, dt, sub, grid, block, raw in got:
+        assert slot == pm.expect(kv, dt, grid, raw), (kv, dt, grid)
     res = [g for g in got if g[0] >= 0]
-    # every launch of at most 512 workgroups is resident (fewer distinct
-    # blocks than slots), three-launch chains included
-    assert all(g[0] >= 0 for g in got if g[4] <= MAX_GRID)
-    assert all(g[4] <= MAX_GRID for g in res)
-    assert any(g[1] != S.CH_FUSED for g in res)
-    assert len(res) > 1500
+    # few distinct blocks: nearly every launch is resident, three-launch
+    # chains and 512-token calls included
+    assert len(res) > 0.99 * len(got)
+    assert any(g[1] != S.CH_FUSED for g in res) and any(g[4] > MAX_GRID for g in res)
     assert counts(lib)[0] == info(lib, cache)[1]
 
 
@@ -291,7 +307,7 @@ def test_failed_check_or_copy_launches_with_arguments(lib, fresh):
     assert info(lib, cache) == (1, 1, 1)
 
 
-def test_only_small_launches_of_precompiled_versions_are_resident(lib, fresh):
+def test_large_launches_take_only_the_first_slots(lib, fresh):
     cache = fresh(flags=AUTO | RES)
     m = S.SpecCacheModel(flags=S.FLAG_AUTO_INSTALL)
     for T in (1, 8, 64, 512, 4096):
@@ -299,12 +315,28 @@ def test_only_small_launches_of_precompiled_versions_are_resident(lib, fresh):
     # a chain whose norm rows are split runs three launches, each resident
     run_both(lib, cache, m, chain_call(BF, 2, 65536, 11008, 32, 32, 128), install=False)
     got = launches(lib)
-    assert any(g[4] > MAX_GRID for g in got)
-    for slot, kv, dt, sub, grid, block, raw in got:
-        assert (slot >= 0) == (grid <= MAX_GRID), (kv, grid)
+    assert sum(g[4] > MAX_GRID for g in got) >= 2
+    assert [g[0] for g in got[:5]] == [0, 1, 2, 3, 4]    # every size, slots in order
     assert [family(g[1]) for g in got[-3:]] == [FAM_NORM, FAM_ROPE, FAM_SW]
+    assert all(g[0] >= 0 for g in got[-3:])
     assert got[-3][1] == S.RN_SPLIT and len(got[-3][-1]) == CHAIN_BYTES
-    # compiled specializations carry their arguments
+
+
+def test_large_launch_without_a_first_slot_carries_its_arguments(lib, fresh):
+    """Slots 0-9 taken by small launches: a large launch carries its
+    arguments, a small one still takes slot 10 and on."""
+    big = fresh(flags=AUTO | RES)
+    m = S.SpecCacheModel(flags=S.FLAG_AUTO_INSTALL)
+    for i in range(ANY_GRID_SLOTS):
+        run_both(lib, big, m, llama(i), install=False)
+    run_both(lib, big, m, llama(0, T=512), install=False)
+    run_both(lib, big, m, llama(ANY_GRID_SLOTS), install=False)
+    got = launches(lib)
+    assert got[-2][4] > MAX_GRID
+    assert [g[0] for g in got] == list(range(ANY_GRID_SLOTS)) + [-1, ANY_GRID_SLOTS]
+
+
+def test_compiled_specializations_carry_their_arguments(lib, fresh):
     jc = fresh(flags=AUTO | RES | JIT)
     assert c_call(lib, jc, llama()) == 0
     assert c_call(lib, jc, llama()) == 0
@@ -420,16 +452,11 @@ def test_random_calls_launch_the_same_from_resident_blocks(lib, calls):
     st_b, log_b, (enabled, n_held, n_res) = _run_log(lib, calls, AUTO | RES)
     assert st_a == st_b
     assert len(log_a) == len(log_b)
-    seen = {}
+    pm = PoolModel()
     for (sa, *ga, ra), (sb, *gb, rb) in zip(log_a, log_b):
         assert sa == -1 and ga == gb
         kv, dt, grid = gb[0], gb[1], gb[3]
         assert _masked_block(kv, rb) == _masked_block(kv, ra)
-        if family(kv) is None or grid > MAX_GRID:
-            assert sb == -1
-        else:                                   # few blocks: every table has room
-            assert sb >= 0
-            key = (family(kv), dt, rb, grid)
-            assert seen.setdefault(key, sb) == sb
-    assert (enabled, n_held) == (1, len(seen))
+        assert sb == pm.expect(kv, dt, grid, rb)
+    assert (enabled, n_held) == (1, len(pm.held))
     assert n_res == sum(1 for g in log_b if g[0] >= 0)
