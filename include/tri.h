@@ -350,7 +350,10 @@ typedef struct tri_chain_args {
  * fails the check made at creation (launches at several LDS sizes whose slot the kernel must
  * read back exactly). tri_spec_resident_info tells how many launches used a
  * held block. A first call with a new block synchronizes a private stream:
- * make it before another thread starts a global-mode stream capture. */
+ * make it before another thread starts a global-mode stream capture. A
+ * graph that captured resident launches (tri_graph_build_layers, or the
+ * caller's own capture) reads the cache's slots when replayed: destroy it
+ * before the cache. */
 tri_status tri_spec_cache_create(tri_cache **out, uint32_t capacity, uint32_t flags);
 /* Release a cache and everything it owns (versions, kernel handles, loaded
  * code objects, device constants and scratch). Not in the paper (its module

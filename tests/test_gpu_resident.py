@@ -397,3 +397,47 @@ def test_resident_three_launch_chain(tri):
         torch.cuda.synchronize()
         plain.close()
         res.close()
+
+
+def test_captured_step_of_held_blocks_replays_like_direct_calls(tri):
+    """A decode step whose layers' blocks are held, captured with
+    tri_graph_build_layers: every replay (new data, same pointers) equals an
+    ordinary cache's direct call on twin buffers bit for bit, and its first
+    layer the oracle."""
+    cfg = wl.GQA_DECODE
+    n = 4
+    plain, res = make_cache(tri), make_cache(tri, resident_args=True)
+    graph = None
+    try:
+        la, aa = _layer_stack(tri, plain, cfg, n, 1300)
+        lb, ab = _layer_stack(tri, res, cfg, n, 1300)
+        res.decode_chain_layers(ab)                  # holds the four blocks
+        torch.cuda.synchronize()
+        graph = res.build_graph(ab)
+        assert graph.launch_count == n
+        for rep in range(3):
+            fresh = [wl.host_inputs(cfg, seed=1400 + 10 * rep + l) for l in range(n)]
+            for l in range(n):
+                for k in ("x", "q", "k", "gate", "up") + (("residual",) if l == 0 else ()):
+                    src = wl.to_torch(fresh[l][k], cfg.dtype, DEV)
+                    la[l][k].copy_(src)
+                    lb[l][k].copy_(src)
+            torch.cuda.synchronize()
+            graph.launch()
+            plain.decode_chain_layers(aa)
+            torch.cuda.synchronize()
+            for l in range(n):
+                same_outputs(f"replay {rep} layer {l}", lb[l], la[l], cfg.dtype)
+            want = O.decode_chain({k: fresh[0][k] for k in ("x", "residual", "q", "k", "gate",
+                                                             "up")}
+                                  | {"w": host(lb[0]["w"]), "pos": host(lb[0]["pos"])},
+                                  cfg.eps, cfg.base, cfg.dtype)
+            for nme in ("out", "q", "y"):
+                check(f"replay {rep} {nme}[0] vs oracle", host(lb[0][nme]), want[nme], cfg.dtype)
+        assert res.resident_info()["held"] == n
+    finally:
+        torch.cuda.synchronize()
+        if graph is not None:
+            graph.close()
+        plain.close()
+        res.close()
