@@ -196,6 +196,45 @@ class Graph:
             pass
 
 
+class Prepared:
+    """One op call of a cache marshalled once (SpecCache.prepare): calling it
+    issues the same entry call again -- same tensors, sizes and scalars -- on
+    the given stream or the device's current one, without the binding's
+    shape checks and argument conversion. The tensors it was made from stay
+    alive with it: their contents may change between calls, their storage
+    must not. A MISS installs and calls again, as the ordinary method does;
+    an error raises TriError."""
+
+    __slots__ = ("_cache", "_what", "_fn", "_raw", "_args", "_cargs", "_max_misses", "result")
+
+    def __init__(self, cache: "SpecCache", what: str, fn, args, max_misses: int, result):
+        self._cache = cache
+        self._what = what
+        self._fn = fn
+        self._args = args                      # without the trailing stream
+        self._max_misses = max_misses
+        # every argument as its own ctypes object, for a call through a
+        # prototype-free pointer to the same function (no per-call conversion)
+        types = fn.argtypes[1:-1]
+        self._cargs = (C.c_void_p(cache._h.value),) + tuple(
+            t(a) if isinstance(a, (int, float)) else a     # None (NULL), byref(...) as they are
+            for t, a in zip(types, args))
+        self._raw = C.cast(fn, C.CFUNCTYPE(C.c_int))
+        self.result = result
+
+    def __call__(self, stream=None):
+        cache = self._cache
+        if not cache._h:
+            raise TriError(E_INVALID, f"{self._what}: the cache is closed")
+        s = _stream_ptr(stream, cache._dev)
+        st = self._raw(*self._cargs, C.c_void_p(s))
+        if st == MISS:
+            cache._call(self._what, self._fn, *self._args, s, max_misses=self._max_misses)
+        elif st != OK:
+            raise TriError(st, self._what)
+        return self.result
+
+
 class SpecCache:
     """One native specialization cache (bound to the current device)."""
 
@@ -222,6 +261,7 @@ class SpecCache:
         self._h = h
         self._dev = torch.cuda.current_device()   # the device the cache is bound to
         self.misses_handled = 0
+        self._rec = None                           # prepare(): the recorded entry call
         if code_dir is not None:
             st = _dll.tri_spec_set_code_dir(h, code_dir.encode())
             if st != OK:
@@ -245,7 +285,11 @@ class SpecCache:
     # ---- miss path ---------------------------------------------------------
     def _call(self, what: str, fn, *args, max_misses: int = 1) -> None:
         """One entry call; on MISS install the recorded key and call again
-        (a call over several layers can miss once per distinct version)."""
+        (a call over several layers can miss once per distinct version).
+        While prepare() records, the call is noted instead of issued."""
+        if self._rec is not None:
+            self._rec.append((what, fn, args, max_misses))
+            return
         st = fn(self._h, *args)
         for _ in range(max_misses):
             if st != MISS:
@@ -255,6 +299,25 @@ class SpecCache:
             st = fn(self._h, *args)
         if st != OK:
             raise TriError(st, what)
+
+    def prepare(self, op: str, *args, **kwargs) -> Prepared:
+        """Marshal one call of method `op` (e.g. "rmsnorm", "swiglu",
+        "decode_chain") once and return it as a Prepared call: its `result`
+        is what the method returns (output tensors allocated now when not
+        given), and calling it issues the entry call with those arguments.
+        Nothing is launched by prepare() itself."""
+        if op in ("prepare", "close") or op.startswith("_") or not callable(getattr(self, op, None)):
+            raise ValueError(f"prepare: {op!r} is not an op of the cache")
+        rec = []
+        self._rec = rec
+        try:
+            result = getattr(self, op)(*args, **kwargs)
+        finally:
+            self._rec = None
+        if len(rec) != 1:
+            raise ValueError(f"prepare: {op!r} does not make exactly one entry call")
+        what, fn, cargs, max_misses = rec[0]
+        return Prepared(self, what, fn, cargs[:-1], max_misses, result)
 
     def install_last_miss(self) -> Selection:
         sel = Selection()
