@@ -84,3 +84,67 @@ def test_rope_ext_keeps_its_table_alive():
     del ext
     gc.collect()
     assert ref() is None
+
+
+class _NullStream:
+    cuda_stream = 0        # the null stream, named without asking torch for a device
+
+
+_NULL_STREAM = _NullStream()
+
+
+class _Shell(tri.SpecCache):
+    """A cache that was never created: nothing to release."""
+
+    def close(self):
+        self._h = None
+
+
+def _recording_cache():
+    """A SpecCache shell that only records: prepare() runs the op method,
+    whose one entry call is noted, never issued (no library call here)."""
+    import ctypes as C
+    c = object.__new__(_Shell)
+    c._h = C.c_void_p(0x1000)
+    c._dev = -1            # a CPU tensor's device index: the checks pass
+    c._rec = None
+    c.misses_handled = 0
+    return c
+
+
+def test_prepare_converts_every_argument_once():
+    """The prepared call holds the op's arguments (without the stream) as
+    C objects of the entry point's parameter types, and the method's result."""
+    import ctypes as C
+    from paper_2609_37241_amd import _lib as L
+    c = _recording_cache()
+    x = torch.zeros(4, 8, dtype=torch.bfloat16)
+    w = torch.ones(8, dtype=torch.bfloat16)
+    y = torch.empty_like(x)
+    p = c.prepare("rmsnorm", x, w, 1e-6, out=y, stream=_NULL_STREAM)
+    assert p.result is y
+    types = L.SIGNATURES["tri_rmsnorm"][1]
+    assert len(p._cargs) == len(types) - 1                   # the stream comes per call
+    assert isinstance(p._cargs[0], C.c_void_p) and p._cargs[0].value == 0x1000
+    for t, a in zip(types[1:-1], p._cargs[1:]):
+        assert type(a) is t, (t, a)
+    assert p._cargs[1].value == L.BF16 and p._cargs[-1].value == pytest.approx(1e-6)
+    assert (p._cargs[2].value, p._cargs[4].value) == (x.data_ptr() or None, w.data_ptr() or None)
+    assert [a.value for a in p._cargs[6:9]] == [8, 4, 8]      # y row stride, T, H
+
+
+def test_prepare_keeps_the_struct_of_a_prebuilt_chain_call():
+    import ctypes as C
+    c = _recording_cache()
+    args = tri.ChainArgs()
+    p = c.prepare("decode_chain_args", args, _NULL_STREAM)
+    (ref,) = p._cargs[1:]
+    assert type(ref).__name__ == "CArgObject" and ref._obj is args   # passed by reference
+    assert isinstance(p._cargs[0], C.c_void_p)
+
+
+def test_prepare_refuses_what_is_not_an_op_call():
+    c = _recording_cache()
+    for bad in ("close", "prepare", "_call", "no_such_op"):
+        with pytest.raises(ValueError):
+            c.prepare(bad)
