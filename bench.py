@@ -636,6 +636,22 @@ def main():
         assert st == 0, st
         steps[name] = summary(list(e2e[:n3]))
     steps["resident_blocks"] = rcache.resident_info()
+    # the same step as a plain Python loop over prepared calls (one per layer)
+    # on the resident cache: no graph, every guard evaluated on every call
+    prepared_layers = [rcache.prepare("decode_chain_args", lay_args[l], stream)
+                       for l in range(n_layers)]
+    for _ in range(20):
+        for pl in prepared_layers:
+            pl(stream)
+    stream.synchronize()
+    rep = []
+    for _ in range(n3):
+        a = time.perf_counter()
+        for pl in prepared_layers:
+            pl(stream)
+        stream.synchronize()
+        rep.append((time.perf_counter() - a) * 1e6)
+    steps["resident_prepared_python_loop"] = summary(rep)
     layer_list = [lay_args[l] for l in range(n_layers)]
     g32 = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g32, stream=stream):
