@@ -308,6 +308,8 @@ class SpecCache:
         Nothing is launched by prepare() itself."""
         if op in ("prepare", "close") or op.startswith("_") or not callable(getattr(self, op, None)):
             raise ValueError(f"prepare: {op!r} is not an op of the cache")
+        if not self._h:
+            raise TriError(E_INVALID, "prepare: the cache is closed")
         rec = []
         self._rec = rec
         try:

@@ -148,3 +148,6 @@ def test_prepare_refuses_what_is_not_an_op_call():
     for bad in ("close", "prepare", "_call", "no_such_op"):
         with pytest.raises(ValueError):
             c.prepare(bad)
+    c.close()
+    with pytest.raises(tri.TriError):
+        c.prepare("rmsnorm", torch.zeros(1, 8), torch.ones(8), 1e-6, stream=_NULL_STREAM)
