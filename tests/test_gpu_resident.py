@@ -441,3 +441,34 @@ def test_captured_step_of_held_blocks_replays_like_direct_calls(tri):
             graph.close()
         plain.close()
         res.close()
+
+
+def test_one_resident_cache_on_two_streams(tri):
+    """Calls alternate between two streams (two buffer sets, one held block
+    each, the second written while the first stream's launches may still
+    run); every chain matches the oracle."""
+    cfg = wl.LLAMA7B_DECODE
+    streams = [torch.cuda.Stream(device=DEV), torch.cuda.Stream(device=DEV)]
+    c = make_cache(tri, resident_args=True)
+    try:
+        sets = []
+        for i, s in enumerate(streams):
+            inp, d = device_inputs(cfg, seed=1500 + i)
+            sets.append((inp, d, d["q"].clone(), d["k"].clone(), args_of(tri, c, cfg, d), s))
+        torch.cuda.synchronize()
+        for it in range(100):
+            for inp, d, q0, k0, a, s in sets:
+                with torch.cuda.stream(s):
+                    d["q"].copy_(q0)
+                    d["k"].copy_(k0)
+                c.decode_chain_args(a, stream=s)
+        torch.cuda.synchronize()
+        for inp, d, q0, k0, a, s in sets:
+            want = O.decode_chain(inp, cfg.eps, cfg.base, cfg.dtype)
+            for n in ("y", "q", "k", "out"):
+                check(n, host(d[n]), want[n], cfg.dtype)
+            check("res_out", host(d["res_out"]), want["res_out"], cfg.dtype, exact=True)
+        assert c.resident_info() == {"enabled": 1, "held": 2, "launches": 200}
+    finally:
+        torch.cuda.synchronize()
+        c.close()
