@@ -472,3 +472,45 @@ def test_one_resident_cache_on_two_streams(tri):
     finally:
         torch.cuda.synchronize()
         c.close()
+
+
+def test_captured_step_of_new_blocks_carries_arguments(tri):
+    """A step captured before any of its blocks is held: the capture writes
+    no block (its launches carry their arguments), the replays equal direct
+    ordinary calls, and later direct calls then hold the blocks."""
+    cfg = wl.GQA_DECODE
+    n = 3
+    plain, res = make_cache(tri), make_cache(tri, resident_args=True)
+    graph = None
+    try:
+        la, aa = _layer_stack(tri, plain, cfg, n, 1600)
+        lb, ab = _layer_stack(tri, res, cfg, n, 1600)
+        graph = res.build_graph(ab)                  # installs, then captures
+        assert res.resident_info()["held"] == 0
+        for rep in range(2):
+            fresh = [wl.host_inputs(cfg, seed=1700 + 10 * rep + l) for l in range(n)]
+            for l in range(n):
+                for k in ("x", "q", "k", "gate", "up") + (("residual",) if l == 0 else ()):
+                    src = wl.to_torch(fresh[l][k], cfg.dtype, DEV)
+                    la[l][k].copy_(src)
+                    lb[l][k].copy_(src)
+            torch.cuda.synchronize()
+            graph.launch()
+            plain.decode_chain_layers(aa)
+            torch.cuda.synchronize()
+            for l in range(n):
+                same_outputs(f"replay {rep} layer {l}", lb[l], la[l], cfg.dtype)
+        want = O.decode_chain({k: fresh[0][k] for k in ("x", "residual", "q", "k", "gate", "up")}
+                              | {"w": host(lb[0]["w"]), "pos": host(lb[0]["pos"])},
+                              cfg.eps, cfg.base, cfg.dtype)
+        check("out[0] vs oracle", host(lb[0]["out"]), want["out"], cfg.dtype)
+        assert res.resident_info()["held"] == 0
+        res.decode_chain_layers(ab)                  # outside a capture: held now
+        torch.cuda.synchronize()
+        assert res.resident_info()["held"] == n
+    finally:
+        torch.cuda.synchronize()
+        if graph is not None:
+            graph.close()
+        plain.close()
+        res.close()
