@@ -514,3 +514,20 @@ def test_captured_step_of_new_blocks_carries_arguments(tri):
             graph.close()
         plain.close()
         res.close()
+
+
+def test_mixed_stream_from_resident_blocks(tri):
+    """All 10,000 calls of the mixed stream (1-512 tokens, two dtypes, odd
+    layouts) on a resident cache: every selection record against the
+    oracle's model, outputs against the oracle every 50th call and on every
+    miss; nearly every launch takes a held block."""
+    from oracle import selection as S
+    from tests.test_gpu_parity import _mixed_stream_on_gpu
+    c = tri.SpecCache(resident_args=True)
+    try:
+        _mixed_stream_on_gpu(tri, c, S.SpecCacheModel())
+        info = c.resident_info()
+        assert info["enabled"] == 1 and info["launches"] > 9000, info
+    finally:
+        torch.cuda.synchronize()
+        c.close()
