@@ -212,21 +212,8 @@ def run_mixed_stream(tri, wl, bench, dev, stream, torch, autotune=False, generic
     }
 
 
-def python_rmsnorm_vs_eager(tri, torch, dev, n=2000, reps=5):
-    import torch.nn.functional as F
-    g = torch.Generator(device=dev)
-    g.manual_seed(0)
-    x = torch.randn((1024, 128), generator=g, device=dev)
-    w = torch.rand(128, generator=g, device=dev) + 0.5
-    y = torch.empty_like(x)
-    c = tri.SpecCache(auto_install=True)
-    rc = tri.SpecCache(auto_install=True, resident_args=True)
-    # the same call marshalled once (SpecCache.prepare), from the resident cache
-    prepared = rc.prepare("rmsnorm", x, w, 1e-6, out=y)
-    fns = {"tri": lambda: c.rmsnorm(x, w, 1e-6, out=y),
-           "tri_resident": lambda: rc.rmsnorm(x, w, 1e-6, out=y),
-           "tri_resident_prepared": prepared,
-           "torch_eager": lambda: F.rms_norm(x, (128,), w, 1e-6)}
+def _python_vs_eager(torch, fns, n, reps):
+    """E2E (call + sync) and host time per call of each callable, in turn."""
     out = {}
     for name, fn in fns.items():
         for _ in range(200):
@@ -246,16 +233,58 @@ def python_rmsnorm_vs_eager(tri, torch, dev, n=2000, reps=5):
             host.append((time.perf_counter() - a) / n * 1e6)
             torch.cuda.synchronize()
         out[name] = {"e2e_us": summary(e2e), "host_us_per_call": statistics.median(host)}
-    torch.cuda.synchronize()
-    c.close()
-    rc.close()
     for name in ("tri", "tri_resident", "tri_resident_prepared"):
         sfx = name[3:]
         out["eager_over_tri" + sfx + "_e2e"] = (out["torch_eager"]["e2e_us"]["median"]
                                                 / out[name]["e2e_us"]["median"])
         out["eager_over_tri" + sfx + "_host"] = (out["torch_eager"]["host_us_per_call"]
                                                  / out[name]["host_us_per_call"])
+    return out
+
+
+def python_rmsnorm_vs_eager(tri, torch, dev, n=2000, reps=5):
+    import torch.nn.functional as F
+    g = torch.Generator(device=dev)
+    g.manual_seed(0)
+    x = torch.randn((1024, 128), generator=g, device=dev)
+    w = torch.rand(128, generator=g, device=dev) + 0.5
+    y = torch.empty_like(x)
+    c = tri.SpecCache(auto_install=True)
+    rc = tri.SpecCache(auto_install=True, resident_args=True)
+    # the same call marshalled once (SpecCache.prepare), from the resident cache
+    prepared = rc.prepare("rmsnorm", x, w, 1e-6, out=y)
+    out = _python_vs_eager(torch, {
+        "tri": lambda: c.rmsnorm(x, w, 1e-6, out=y),
+        "tri_resident": lambda: rc.rmsnorm(x, w, 1e-6, out=y),
+        "tri_resident_prepared": prepared,
+        "torch_eager": lambda: F.rms_norm(x, (128,), w, 1e-6)}, n, reps)
+    torch.cuda.synchronize()
+    c.close()
+    rc.close()
     out["workload"] = "float32 x (1024, 128), weight (128,), eps 1e-6"
+    return out
+
+
+def python_silu_vs_eager(tri, torch, dev, n=2000, reps=5):
+    """silu, another op of the paper's suite, the same way: bf16 x (1024, 4096)
+    (one decode step's activations of a batch), the binding vs torch eager."""
+    import torch.nn.functional as F
+    g = torch.Generator(device=dev)
+    g.manual_seed(1)
+    x = torch.randn((1024, 4096), generator=g, device=dev).to(torch.bfloat16)
+    y = torch.empty_like(x)
+    c = tri.SpecCache(auto_install=True)
+    rc = tri.SpecCache(auto_install=True, resident_args=True)
+    prepared = rc.prepare("silu", x, out=y)
+    out = _python_vs_eager(torch, {
+        "tri": lambda: c.silu(x, out=y),
+        "tri_resident": lambda: rc.silu(x, out=y),
+        "tri_resident_prepared": prepared,
+        "torch_eager": lambda: F.silu(x)}, n, reps)
+    torch.cuda.synchronize()
+    c.close()
+    rc.close()
+    out["workload"] = "bf16 x (1024, 4096)"
     return out
 
 
@@ -493,6 +522,7 @@ def main():
     # eager rms_norm, on the current stream: end to end (call + sync) and
     # host only (calls issued back to back, one sync after).
     latency["rms_norm_1024x128_from_python"] = python_rmsnorm_vs_eager(tri, torch, dev)
+    latency["silu_1024x4096_bf16_from_python"] = python_silu_vs_eager(tri, torch, dev)
 
     # ---- context: the same chain as PyTorch eager ops, and HIP-graph replay ---------------
     import torch.nn.functional as F  # noqa: F401
