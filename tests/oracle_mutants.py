@@ -198,6 +198,13 @@ def _rn_role_wide_wave(dtype, H, flags, T, b, res=True):
     return _orig_rn_role(dtype, H, flags, T, b, res)
 
 
+def _rn_role_residual_wide(dtype, H, flags, T, b, res=True):
+    v = 16 // S.elem_size(dtype)
+    if res and (flags & S.ALIGN) and H % v == 0 and 4096 < H // v <= S.WIDE_ROW_VECS:
+        return S.RN_WIDE, T
+    return _orig_rn_role(dtype, H, flags, T, b, res)
+
+
 SELECTION_MUTANTS = {
     "bucket_floor_log2": (S, "bucket", _bucket_floor),
     "lookup_last_match": (S.SpecCacheModel, "lookup", _lookup_last),
@@ -208,6 +215,8 @@ SELECTION_MUTANTS = {
     "generic_run_one_bucket_short": (S, "generic_guard", _generic_one_short),
     "generic_row_class_one_vector_short": (S, "_norm_h_range", _h_range_shifted),
     "wavefront_rows_up_to_256_vectors": (S, "rn_role", _rn_role_wide_wave),
+    "plain_wide_rows_up_to_8192_vectors": (S, "WIDE_PLAIN_VECS", 8 * S.WIDE_LANES),
+    "residual_rows_wide_instead_of_split": (S, "rn_role", _rn_role_residual_wide),
 }
 
 _name = os.environ.get("TRI_ORACLE_MUTANT")
