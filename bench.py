@@ -771,8 +771,8 @@ def main():
         copy_dst = torch.empty_like(copy_src)
         # long rows: bf16 [2048, 65536] and the same memory as [1024, 131072]
         # (each row split over 4 / 8 workgroups that exchange partial sums),
-        # and plain rows of [2048, 57344] in the front of that memory (one
-        # 1024-lane workgroup per row)
+        # and plain rows of [2048, 57344] in the front of that memory (256
+        # 1024-lane workgroups, each taking every 256th row)
         lx = torch.randn((2048, 65536), device=dev).to(db["x"].dtype)
         lr, ly, lro = torch.randn_like(lx), torch.empty_like(lx), torch.empty_like(lx)
         lw = (torch.rand(65536, device=dev) + 0.5).to(lx.dtype)

@@ -346,7 +346,9 @@ typedef struct tri_chain_args {
  * holds TRI_RESIDENT_SLOTS blocks of the family and dtype or the pool has
  * no slot free that the launch may take, when the block is new while the
  * caller's stream is being captured, for compiled specializations
- * (TRI_CACHE_JIT) and tri_residual_rmsnorm_noalloc, and on a device that
+ * (TRI_CACHE_JIT), tri_residual_rmsnorm_noalloc and plain RMSNorm rows
+ * of 4097..8192 16-byte vectors (that kernel holds its weights in 128 KiB
+ * of LDS, which leaves too little for the slot), and on a device that
  * fails the check made at creation (launches at several LDS sizes whose slot the kernel must
  * read back exactly). tri_spec_resident_info tells how many launches used a
  * held block. A first call with a new block synchronizes a private stream:

@@ -53,10 +53,12 @@ RN_SCALAR = 10
 RN_WAVE = {1: 11, 2: 12}
 RN_BLOCK = {1: 13, 2: 14, 4: 15, 8: 16, 16: 17}
 RN_LOOP = 18
-RN_WIDE = 19               # a 1024-work-item workgroup per row, 8 vectors per lane
+RN_WIDE = 19               # 1024-work-item workgroups, a row each, 8 vectors per lane
 WIDE_LANES = 1024
 WIDE_ROW_VECS = 8 * WIDE_LANES   # the longest row it holds (16-byte vectors)
 WIDE_PLAIN_VECS = 7 * WIDE_LANES  # plain rows up to here take it by policy
+WIDE_GRID = 256                   # plain rows: at most this many workgroups, each
+                                  # taking rows b, b + 256, ... (residual: one per row)
 RN_SPLIT = 20              # a row over S workgroups of 256, 8 vectors per work-item
 SPLIT_SPAN = 8 * 256       # vectors one split workgroup holds
 SPLIT_MAX_SLICES = 64      # workgroups per row, at most
@@ -182,13 +184,19 @@ def rn_role(dtype: int, H: int, flags: int, T: int, b: int,
     nb = next_pow2(cdiv(nvec, 256))       # a workgroup per row
     if nb <= 16:
         return RN_BLOCK[nb], T
-    if not res and nvec <= WIDE_PLAIN_VECS:  # plain rows: a 1024-lane workgroup
-        return RN_WIDE, T
+    if not res and nvec <= WIDE_PLAIN_VECS:  # plain rows: 1024-lane workgroups
+        return RN_WIDE, wide_grid(T, res)
     if split_fits(dtype, H, b):           # several workgroups per row
         return RN_SPLIT, T * split_slices(dtype, H)
-    if nvec <= WIDE_ROW_VECS:             # a 1024-lane workgroup per row
-        return RN_WIDE, T
+    if nvec <= WIDE_ROW_VECS:             # 1024-lane workgroups
+        return RN_WIDE, wide_grid(T, res)
     return RN_LOOP, T                     # two passes over memory
+
+
+def wide_grid(T: int, res: bool) -> int:
+    """Workgroups of a wide-row norm launch: one per row for residual rows;
+    for plain rows at most WIDE_GRID, each taking every WIDE_GRID-th row."""
+    return T if res else min(T, WIDE_GRID)
 
 
 def rope_role(dtype: int, hd: int, flags: int, T: int, qk_norm: bool = False,
@@ -893,10 +901,12 @@ def candidates(key) -> List[Cand]:
     return out + [seq]
 
 
-def grid_of(variant: int, dt: int, T: int, width: int, slices: int = 1, tokens: int = 1) -> int:
+def grid_of(variant: int, dt: int, T: int, width: int, slices: int = 1, tokens: int = 1,
+            res: bool = True) -> int:
     """Workgroups a kernel variant launches for T tokens (width: SwiGLU's I,
     a short op's row width). Wavefront norm rows: 4 rows per workgroup;
-    other norm and RoPE kernels: one workgroup per row or token (vector RoPE:
+    plain wide norm rows (res False): wide_grid; other norm and RoPE
+    kernels: one workgroup per row or token (vector RoPE:
     times its slices, or per `tokens` tokens); flat kernels: one 16-byte vector per work-item (two
     for ELT_FLAT_U2); row kernels: the row's vectors over 256 work-items,
     per row; element-wise kernels: one element per work-item. Flat, row and
@@ -906,7 +916,9 @@ def grid_of(variant: int, dt: int, T: int, width: int, slices: int = 1, tokens: 
         return cdiv(T, 4)
     if variant == RN_SPLIT:               # width: the row width H
         return T * split_slices(dt, width)
-    if variant in (RN_SCALAR, RN_LOOP, RN_WIDE, ROPE_SCALAR, ROPE_QKN_SCALAR) or \
+    if variant == RN_WIDE:
+        return wide_grid(T, res)
+    if variant in (RN_SCALAR, RN_LOOP, ROPE_SCALAR, ROPE_QKN_SCALAR) or \
             variant in RN_BLOCK.values():
         return T
     if variant in ROPE_VEC_ROLES:
@@ -937,8 +949,9 @@ def cand_plan(key, c: Cand, T: int):
              + grid_of(c.roles[1], dt, T, f["I"], c.slices, c.tokens)
              + grid_of(c.roles[2], dt, T, f["I"]))
         return CH_FUSED, c.roles, [(CH_FUSED, g, BLOCK)]
+    res = f["op"] != OP_RMSNORM           # the chain's norm role is residual
     launches = [(kv, grid_of(kv, dt, T, width(kv), c.slices, c.tokens) if kv in ROPE_VEC_ROLES
-                 else grid_of(kv, dt, T, width(kv)), block_of(kv)) for kv in c.kernels]
+                 else grid_of(kv, dt, T, width(kv), res=res), block_of(kv)) for kv in c.kernels]
     return c.variant, c.roles, launches
 
 

@@ -432,7 +432,8 @@ tri_status norm_launch(tri_cache *c, uint32_t op, const Key &k, const RnArgs &a,
   if (st != TRI_OK) return tri_status(st);
   Version &v = c->versions[vi];
   const int32_t kv = v.plan.kvariant[0];
-  const tri_launch_rec l{kv, role_grid(kv, key_dtype(k), a.T, a.H), role_block(kv)};
+  const tri_launch_rec l{kv, norm_grid(kv, key_dtype(k), a.T, a.H, op == TRI_OP_RES_RMSNORM),
+                         role_block(kv)};
   int rc;
   if (kv == RN_SPLIT) {
     const RnSplitArgs sa{a, v.d_scratch};
@@ -688,7 +689,7 @@ tri_status tri_residual_rmsnorm_noalloc(tri_cache *c, tri_dtype dtype, const voi
   Version &v = c->versions[vi];
   const int32_t kv = v.plan.kvariant[0];
   const RnArgs a{x, res, w, y, res_out, x_rs, res_rs, y_rs, ro_rs, T, int32_t(H), eps};
-  const tri_launch_rec l{kv, role_grid(kv, uint32_t(dtype), T, H), role_block(kv)};
+  const tri_launch_rec l{kv, norm_grid(kv, uint32_t(dtype), T, H, true), role_block(kv)};
   // Always with kernel arguments: a resident block's first use copies it
   // to the device, which this entry point does not do.
   int rc;

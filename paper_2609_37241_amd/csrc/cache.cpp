@@ -306,8 +306,10 @@ void fill_selection(const Version &v, int32_t index, int64_t T, tri_selection *o
     for (int i = 0; i < v.plan.n_launches; ++i) {
       const int32_t kv = v.plan.kvariant[i];
       out->launch[i] = {kv,
-                        role_grid(kv, dt, T, launch_width(k, kv), v.plan.rope_slices,
-                                  v.plan.rope_tokens),
+                        is_norm_variant(kv)
+                            ? norm_grid(kv, dt, T, launch_width(k, kv), key_op(k) != TRI_OP_RMSNORM)
+                            : role_grid(kv, dt, T, launch_width(k, kv), v.plan.rope_slices,
+                                        v.plan.rope_tokens),
                         role_block(kv)};
     }
   }

@@ -123,6 +123,9 @@ constexpr uint64_t kStreamBytes = uint64_t(320) << 20;
 // ceil(T / tokens).
 uint32_t role_grid(int32_t variant, uint32_t dtype, int64_t T, int64_t width,
                    int32_t slices = 1, int32_t tokens = 1);
+// Workgroups of a norm launch: role_grid's, except the plain (not residual)
+// wide-row form, which takes at most kWideGrid workgroups.
+uint32_t norm_grid(int32_t variant, uint32_t dtype, int64_t T, int64_t H, bool res);
 // The row width role_grid takes for launch variant `kv` of a version with key k.
 int64_t launch_width(const Key &k, int32_t kv);
 inline bool is_norm_variant(int32_t v) { return v >= RN_SCALAR && v <= RN_SPLIT; }

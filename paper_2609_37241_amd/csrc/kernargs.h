@@ -21,6 +21,9 @@ constexpr int kRopeTokensMax = 4;
 // Work-items of the wide norm workgroup (RN_WIDE): one row of up to
 // 8 * kWideLanes 16-byte vectors per workgroup; every other kernel uses 256.
 constexpr int kWideLanes = 1024;
+// Most workgroups of a plain wide-row launch (one per compute unit of an
+// MI355X); beyond that many rows each workgroup takes rows b, b + grid, ...
+constexpr int kWideGrid = 256;
 
 // Split norm rows (RN_SPLIT): a row of more than 16 * 256 vectors is held
 // by S = ceil(vectors / kSplitSpan) workgroups of 256 work-items, kSplitVecs

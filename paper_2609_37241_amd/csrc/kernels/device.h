@@ -1253,17 +1253,130 @@ __device__ __forceinline__ void rn_row_wide_plain(const RnArgs &a, int64_t row, 
   }
 }
 
-// Rows of 4097..8192 vectors: one 1024-work-item workgroup per row, up to
-// 8 vectors per lane held in registers (all loads issued up front). The
-// residual form requests the weights with the row (measured 1 % faster for
-// it); the plain form is rn_row_wide_plain.
+// Buffer access to one row: the row's uniform base with its byte length as
+// the range. A load past the range returns zeros and a store past it is
+// dropped, so a row of any length up to 8 * kWideLanes vectors needs no
+// branch, and each access is the descriptor plus one per-lane offset.
+// Descriptor word 3: data format 32 bits (nonzero, as untyped loads need),
+// no swizzle, no index stride.
+constexpr int kRowRsrcWord3 = 0x00020000;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(const void *base, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, bytes, kRowRsrcWord3);
+}
+
+__device__ __forceinline__ void wide_load(__amdgpu_buffer_rsrc_t r, uint32_t off0, u32x4 *xv) {
+#pragma unroll
+  for (int k = 0; k < 8; ++k)
+    xv[k] = __builtin_amdgcn_raw_buffer_load_b128(r, off0 + uint32_t(k) * (kWideLanes * 16u), 0, 0);
+}
+
+// One row of the pipelined plain form, held packed in xv (zeros past the
+// row's end); the lane's weight vectors are in wl. Same arithmetic in the
+// same order as rn_row_wide_plain, so both give the same bits.
+template <int DT>
+__device__ __forceinline__ void wide_norm_store(const RnArgs &a, u32x4 *xv, const u32x4 *wl,
+                                                __amdgpu_buffer_rsrc_t yr, uint32_t off0,
+                                                float *red) {
+  using E = Elt<DT>;
+  constexpr int V = E::V;
+  float ss = 0.0f;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    float f[V];
+    E::unpack(xv[k], f);
+#pragma unroll
+    for (int e = 0; e < V; ++e) ss = __builtin_fmaf(f[e], f[e], ss);
+  }
+  // the output pass unpacks again: the floats are not kept
+#pragma unroll
+  for (int k = 0; k < 8; ++k) asm volatile("" : "+v"(xv[k]));
+  ss = wave_sum(ss);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  ss = wave_sum(red[threadIdx.x & 15]) * 0.25f;
+  const float inv = rsqrtf(ss / float(a.H) + a.eps);
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const u32x4 w = wl[j * kWideLanes + threadIdx.x];
+    u32x4 yv;
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+      if constexpr (DT == kBF16) {
+        const float x0 = __uint_as_float(xv[j][d] << 16), x1 = __uint_as_float(xv[j][d] & 0xFFFF0000u);
+        const float w0 = __uint_as_float(w[d] << 16), w1 = __uint_as_float(w[d] & 0xFFFF0000u);
+        yv[d] = E::pack2((x0 * inv) * w0, (x1 * inv) * w1);
+      } else {
+        yv[d] = __float_as_uint((__uint_as_float(xv[j][d]) * inv) * __uint_as_float(w[d]));
+      }
+    }
+    __builtin_amdgcn_raw_buffer_store_b128(yv, yr, off0 + uint32_t(j) * (kWideLanes * 16u), 0, 0);
+  }
+}
+
+// Plain RMSNorm when a workgroup has several rows: workgroup b takes rows
+// b, b + nblk, ... and requests each next row before the current row's
+// reduction, so one row's loads overlap the previous row's stores on the
+// same CU (one row per workgroup, the loads of every workgroup on the chip
+// start together and then their stores, at bf16 rows of 57,344 measured
+// 0.85 of a copy of the same bytes, against 0.90 with this loop). Two row
+// buffers used in turn, so no register copy makes the next row's loads
+// complete early; the weights wait in LDS (each lane reads back only the
+// vectors it wrote: no barrier), which keeps the lane at 8 + 8 vectors
+// (121 VGPRs; holding the weights in registers spills). The partial sums
+// alternate between two LDS rows, so one barrier per row suffices.
+template <int DT>
+__device__ __forceinline__ void rn_rows_wide_plain(const RnArgs &a, uint32_t nblk, u32x4 *wl,
+                                                   float (*red)[kWideLanes / 64]) {
+  using E = Elt<DT>;
+  const uint32_t off0 = uint32_t(threadIdx.x) * 16u;
+  const int rowb = (a.H / E::V) * 16;
+  const char *xbase = static_cast<const char *>(a.x);
+  char *ybase = static_cast<char *>(a.y);
+  const int64_t xs = a.x_rs * E::ES, ys = a.y_rs * E::ES;
+  int64_t row = blockIdx.x;
+  u32x4 ra[8], rb[8];
+  wide_load(row_rsrc(a.w, rowb), off0, ra);
+#pragma unroll
+  for (int k = 0; k < 8; ++k) wl[k * kWideLanes + threadIdx.x] = ra[k];
+  wide_load(row_rsrc(xbase + row * xs, rowb), off0, ra);
+  for (;;) {
+    if (row + nblk >= a.T) {
+      wide_norm_store<DT>(a, ra, wl, row_rsrc(ybase + row * ys, rowb), off0, red[0]);
+      return;
+    }
+    wide_load(row_rsrc(xbase + (row + nblk) * xs, rowb), off0, rb);
+    wide_norm_store<DT>(a, ra, wl, row_rsrc(ybase + row * ys, rowb), off0, red[0]);
+    row += nblk;
+    if (row + nblk >= a.T) {
+      wide_norm_store<DT>(a, rb, wl, row_rsrc(ybase + row * ys, rowb), off0, red[1]);
+      return;
+    }
+    wide_load(row_rsrc(xbase + (row + nblk) * xs, rowb), off0, ra);
+    wide_norm_store<DT>(a, rb, wl, row_rsrc(ybase + row * ys, rowb), off0, red[1]);
+    row += nblk;
+  }
+}
+
+// Rows of 4097..8192 vectors on 1024-work-item workgroups, up to 8 vectors
+// per lane held in registers (all loads issued up front). The residual form
+// takes one row per workgroup (grid T) and requests the weights with the
+// row (measured 1 % faster for it; a loop over rows measured 4-35 % slower).
+// The plain form is launched on at most kWideGrid workgroups: with one row
+// each, rn_row_wide_plain; with more, rn_rows_wide_plain.
 template <int DT, bool RES>
-__device__ __forceinline__ void body_rn_wide(const RnArgs &a) {
-  __shared__ float red[kWideLanes / 64];
-  if constexpr (RES)
+__device__ __forceinline__ void body_rn_wide(const RnArgs &a, uint32_t nblk = gridDim.x) {
+  if constexpr (RES) {
+    __shared__ float red[kWideLanes / 64];
     rn_row_regs<DT, 8, RES, kWideLanes, false>(a, blockIdx.x, threadIdx.x, red);
-  else
-    rn_row_wide_plain<DT>(a, blockIdx.x, threadIdx.x, red);
+  } else {
+    __shared__ float red[2][kWideLanes / 64];
+    __shared__ u32x4 wl[8 * kWideLanes];
+    if (a.T <= int64_t(nblk)) {
+      if (int64_t(blockIdx.x) < a.T) rn_row_wide_plain<DT>(a, blockIdx.x, threadIdx.x, red[0]);
+    } else {
+      rn_rows_wide_plain<DT>(a, nblk, wl, red);
+    }
+  }
 }
 
 // Rows of more than 4096 vectors over several workgroups (rn_split_row).

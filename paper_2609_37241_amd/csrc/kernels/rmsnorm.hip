@@ -104,7 +104,7 @@ template <int DT, bool RES>
 __global__ __launch_bounds__(kWideLanes) void k_rn_wide_res() {
   RnArgs a;
   uint32_t g;
-  if (resident_args(norm_table<DT>(), a, g)) body_rn_wide<DT, RES>(a);
+  if (resident_args(norm_table<DT>(), a, g)) body_rn_wide<DT, RES>(a, g);
 }
 
 template <int DT, bool RES>
@@ -157,7 +157,11 @@ const void *rn_pick_resident(int32_t variant) {
     case RN_BLOCK_8: return sym(&k_rn_block_res<DT, 8, RES>);
     case RN_BLOCK_16: return sym(&k_rn_block_res<DT, 16, RES>);
     case RN_LOOP: return sym(&k_rn_loop_res<DT, RES>);
-    case RN_WIDE: return sym(&k_rn_wide_res<DT, RES>);
+    // the plain wide form holds its weights in 128 KiB of static LDS,
+    // which leaves too little for the slot channel: kernel arguments only
+    case RN_WIDE:
+      if constexpr (RES) return sym(&k_rn_wide_res<DT, RES>);
+      else return nullptr;
     case RN_SPLIT: return sym(&k_rn_split_res<DT, RES>);
     default: return nullptr;
   }

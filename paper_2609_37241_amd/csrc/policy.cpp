@@ -88,9 +88,9 @@ Role rn_role(uint32_t dtype, int64_t H, unsigned flags, int64_t T, uint32_t buck
   if (nvec <= 128) return {nvec <= 64 ? RN_WAVE_1 : RN_WAVE_2, uint32_t(cdiv(T, 4))};
   const int64_t nb = next_pow2(cdiv(nvec, 256));
   if (nb <= 16) return {RN_BLOCK_1 + pow2_index(nb), uint32_t(T)};
-  if (!res && nvec <= kWidePlainVecs) return {RN_WIDE, uint32_t(T)};
+  if (!res && nvec <= kWidePlainVecs) return {RN_WIDE, norm_grid(RN_WIDE, dtype, T, H, res)};
   if (split_fits(dtype, H, bucket)) return {RN_SPLIT, uint32_t(T * split_slices(dtype, H))};
-  if (nvec <= kWideRowVecs) return {RN_WIDE, uint32_t(T)};
+  if (nvec <= kWideRowVecs) return {RN_WIDE, norm_grid(RN_WIDE, dtype, T, H, res)};
   return {RN_LOOP, uint32_t(T)};
 }
 
@@ -238,6 +238,11 @@ uint32_t role_grid(int32_t variant, uint32_t dtype, int64_t T, int64_t I, int32_
     default:
       return 0;
   }
+}
+
+uint32_t norm_grid(int32_t variant, uint32_t dtype, int64_t T, int64_t H, bool res) {
+  if (variant == RN_WIDE && !res && T > kWideGrid) return uint32_t(kWideGrid);
+  return role_grid(variant, dtype, T, H);
 }
 
 int64_t launch_width(const Key &k, int32_t kv) {

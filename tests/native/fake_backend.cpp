@@ -109,6 +109,11 @@ int be_resident_table(int device, uint32_t family, uint32_t dtype, void **table)
 }
 
 int be_resolve_resident(int32_t kvariant, uint32_t dtype, int32_t ksub, void **fn) {
+  // as the device library: the plain wide-row norm has no argument-free form
+  if (kvariant == RN_WIDE && ksub == 0) {
+    *fn = nullptr;
+    return TRI_E_RUNTIME;
+  }
   *fn = reinterpret_cast<void *>(encode(kvariant, dtype, ksub) | (uintptr_t(1) << 42));
   return 0;
 }

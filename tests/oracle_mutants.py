@@ -217,6 +217,7 @@ SELECTION_MUTANTS = {
     "wavefront_rows_up_to_256_vectors": (S, "rn_role", _rn_role_wide_wave),
     "plain_wide_rows_up_to_8192_vectors": (S, "WIDE_PLAIN_VECS", 8 * S.WIDE_LANES),
     "residual_rows_wide_instead_of_split": (S, "rn_role", _rn_role_residual_wide),
+    "plain_wide_rows_one_workgroup_each": (S, "WIDE_GRID", 1 << 40),
 }
 
 _name = os.environ.get("TRI_ORACLE_MUTANT")

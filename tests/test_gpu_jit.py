@@ -74,6 +74,8 @@ OP_CASES = [
     ("rmsnorm", nm.BF16, 3, 65536, "plain"), ("residual", nm.F32, 4, 20480, "plain"),
     ("residual", nm.BF16, 2, 40960, "strided"),
     ("rmsnorm", nm.BF16, 7, 4097, "plain"), ("rmsnorm", nm.F32, 9, 520, "unaligned"),
+    # plain rows of 5120 vectors on 256 workgroups that take 1-2 rows each
+    ("rmsnorm", nm.BF16, 300, 40960, "plain"),
     ("residual", nm.BF16, 130, 4096, "plain"), ("residual", nm.F32, 6, 256, "strided"),
     ("swiglu", nm.BF16, 8, 14336, "plain"), ("swiglu", nm.F32, 130, 1000, "plain"),
     ("swiglu", nm.BF16, 5, 11008, "strided"), ("swiglu", nm.F32, 5, 1001, "unaligned"),

@@ -170,6 +170,11 @@ RN_CASES = [
     (nm.F32, 2, 32772, "plain"), (nm.F32, 2, 131072, "plain"), (nm.BF16, 5, 40960, "unaligned"),
     (nm.BF16, 300, 65536, "plain"), (nm.BF16, 3, 1048576, "plain"), (nm.F32, 2, 524288, "plain"),
     (nm.BF16, 2, 1048584, "plain"), (nm.F32, 2, 524292, "plain"),
+    # plain rows of 4097..7168 vectors beyond 256 rows: 256 workgroups, each
+    # taking every 256th row (1 to 4 rows; an odd and an even count end the
+    # two-buffer loop on either buffer); a ragged 4097-vector row, strided
+    (nm.BF16, 257, 57344, "plain"), (nm.F32, 600, 20480, "plain"),
+    (nm.BF16, 513, 32776, "strided"), (nm.BF16, 1000, 49152, "plain"),
 ]
 
 
@@ -198,8 +203,8 @@ def test_rmsnorm_variants(tri, cache, dtype, T, H, layout, res):
     sel = cache.last_selection()
     es = 4 if dtype == nm.F32 else 2
     flags = S.ALIGN if (xd.data_ptr() % 16 == 0 and (xd.stride(0) * es) % 16 == 0) else 0
-    assert sel.variant == S.rn_role(S.DT_F32 if dtype == nm.F32 else S.DT_BF16, H, flags, T,
-                                    S.bucket(T), res)[0]
+    assert (sel.variant, sel.launch[0].grid_x) == S.rn_role(
+        S.DT_F32 if dtype == nm.F32 else S.DT_BF16, H, flags, T, S.bucket(T), res)
 
 
 def test_split_rows_reuse_their_scratch(tri, cache):
@@ -257,7 +262,7 @@ def test_generic_split_version_across_buckets(tri):
             torch.cuda.synchronize()
             assert sel.variant == S.RN_SPLIT and sel.launch[0].grid_x == 4 * T
             assert sel2.variant == S.RN_SPLIT and sel2.launch[0].grid_x == 4 * T
-            assert sel3.variant == S.RN_WIDE and sel3.launch[0].grid_x == T
+            assert sel3.variant == S.RN_WIDE and sel3.launch[0].grid_x == min(T, 256)
             check(f"{step} y", host(y), O.rmsnorm(x, w, 1e-6, nm.BF16), nm.BF16)
             check(f"{step} y 57344", host(y3), O.rmsnorm(x[:, :57344], w[:57344], 1e-6, nm.BF16),
                   nm.BF16)

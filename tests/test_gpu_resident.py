@@ -356,7 +356,9 @@ def test_resident_standalone_op_equals_ordinary_and_oracle(tri, name):
                 check(f"{name} call {call} {n}", host(gb[n]), host(ga[n]), dt, exact=True)
             assert res.last_selection().as_tuple()[3:] == plain.last_selection().as_tuple()[3:]
         info = res.resident_info()
-        assert info["held"] == 1 and info["launches"] == 3, info
+        # the plain wide-row norm has no argument-free form: kernel arguments
+        held = 0 if name == "rmsnorm_wide_bf16" else 1
+        assert info["held"] == held and info["launches"] == 3 * held, info
         for n, w in want.items():
             exact = n in EXACT and name != "silu_bf16"
             check(f"{name} {n} vs oracle", host(gb[n]), w, dt, exact=exact)

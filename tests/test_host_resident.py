@@ -26,8 +26,12 @@ INV_FREQ = slice(112, 120)   # RopeArgs.inv_freq inside the chain block: per-ver
 FAM_CHAIN, FAM_NORM, FAM_ROPE, FAM_SW, FAM_ELT, FAM_EMB = range(6)
 
 
-def family(kv):
-    """The resident table family of a kernel variant (None: no table)."""
+def family(kv, sub=1):
+    """The resident table family of a kernel variant (None: no table; `sub`
+    0 with a norm variant: the plain form, whose wide-row kernel has no
+    argument-free twin)."""
+    if kv == S.RN_WIDE and sub == 0:
+        return None
     if kv == S.CH_FUSED:
         return FAM_CHAIN
     if kv in S.NORM_VARIANTS:
@@ -52,8 +56,8 @@ class PoolModel:
     def __init__(self):
         self.used, self.held = {}, {}
 
-    def expect(self, kv, dt, grid, raw):
-        fam = family(kv)
+    def expect(self, kv, dt, grid, raw, sub=1):
+        fam = family(kv, sub)
         if fam is None:
             return -1
         key = (fam, dt, raw, grid)
@@ -166,7 +170,7 @@ def test_selection_parity_over_call_zoo_with_resident_blocks(lib, fresh):
     pm = PoolModel()
     got = launches(lib)
     for slot, kv, dt, sub, grid, block, raw in got:
-        assert slot == pm.expect(kv, dt, grid, raw), (kv, dt, grid)
+        assert slot == pm.expect(kv, dt, grid, raw, sub), (kv, dt, grid)
     assert {f for f, _ in pm.used} == {FAM_CHAIN, FAM_NORM, FAM_ROPE, FAM_SW, FAM_ELT, FAM_EMB}
     enabled, n_held, _ = info(lib, cache)
     assert (enabled, n_held) == (1, len(pm.held))
@@ -187,7 +191,7 @@ def test_mixed_stream_with_resident_blocks(lib, fresh):
     got = launches(lib)
     pm = PoolModel()
     for slot, kv, dt, sub, grid, block, raw in got:
-        assert slot == pm.expect(kv, dt, grid, raw), (kv, dt, grid)
+        assert slot == pm.expect(kv, dt, grid, raw, sub), (kv, dt, grid)
     res = [g for g in got if g[0] >= 0]
     # few distinct blocks: nearly every launch is resident, three-launch
     # chains and 512-token calls included
@@ -455,8 +459,8 @@ def test_random_calls_launch_the_same_from_resident_blocks(lib, calls):
     pm = PoolModel()
     for (sa, *ga, ra), (sb, *gb, rb) in zip(log_a, log_b):
         assert sa == -1 and ga == gb
-        kv, dt, grid = gb[0], gb[1], gb[3]
+        kv, dt, sub, grid = gb[0], gb[1], gb[2], gb[3]
         assert _masked_block(kv, rb) == _masked_block(kv, ra)
-        assert sb == pm.expect(kv, dt, grid, rb)
+        assert sb == pm.expect(kv, dt, grid, rb, sub)
     assert (enabled, n_held) == (1, len(pm.held))
     assert n_res == sum(1 for g in log_b if g[0] >= 0)

@@ -173,6 +173,31 @@ def test_plain_rows_policy(dtype, H, b, want):
         assert cands[1:] == ([S.RN_SPLIT] if S.split_fits(dtype, H, b) else []) + [S.RN_LOOP]
 
 
+@pytest.mark.parametrize("dtype, H, T, want", [
+    # plain rows of 5120 and 7168 vectors: a workgroup per row up to 256
+    # rows, then 256 workgroups, each taking every 256th row
+    (BF, 57344, 1, 1), (BF, 40960, 100, 100), (BF, 57344, 256, 256), (BF, 57344, 257, 256),
+    (BF, 57344, 2048, 256), (F, 28672, 300, 256)])
+def test_plain_wide_rows_grid_by_hand(dtype, H, T, want):
+    assert S.plan(S.make_key(rn_call(dtype, T, H)), T)[2] == [(S.RN_WIDE, want, 1024)]
+
+
+def test_wide_rows_grid_of_candidates_by_hand():
+    # bf16 rows of 65,536 (8192 vectors) at 2048 rows split by policy; the
+    # tuning candidate on the 1024-lane form launches 256 workgroups for
+    # plain rows and one per row for residual rows
+    for call, want in ((rn_call(BF, 2048, 65536), 256), (res_call(BF, 2048, 65536), 2048)):
+        key = S.make_key(call)
+        wide = [c for c in S.candidates(key) if c.kernels == (S.RN_WIDE,)]
+        assert len(wide) == 1
+        assert S.cand_plan(key, wide[0], 2048)[2] == [(S.RN_WIDE, want, 1024)]
+    # residual rows take the wide form when the split's scratch does not fit
+    # (bucket 20), a workgroup per row
+    assert S.rn_role(BF, 65536, S.ALIGN | S.CONTIG, 1 << 20, 20) == (S.RN_WIDE, 1 << 20)
+    assert S.grid_of(S.RN_WIDE, BF, 2048, 57344) == 2048
+    assert S.grid_of(S.RN_WIDE, BF, 2048, 57344, res=False) == 256
+
+
 def test_split_scratch_layout_by_hand():
     # 3 rows of bf16 65536 (8192 vectors, 4 workgroups each): 8 header words,
     # 12 slots, 3 counters
