@@ -207,6 +207,30 @@ def test_rmsnorm_variants(tri, cache, dtype, T, H, layout, res):
         S.DT_F32 if dtype == nm.F32 else S.DT_BF16, H, flags, T, S.bucket(T), res)
 
 
+@pytest.mark.parametrize("dtype,H", [(nm.BF16, 57344), (nm.F32, 20480), (nm.BF16, 32776)])
+def test_plain_wide_rows_same_bits_at_any_row_count(tri, cache, dtype, H):
+    """Plain rows of 4097..7168 vectors: one call of 600 rows (256 workgroups
+    that take 2-3 rows each, the next row requested before the current
+    row's reduction) gives every row the same bits as calls of at most 256
+    rows (one row per workgroup), and the oracle's values."""
+    r = rng(H + 600)
+    T = 600
+    x = wl.host_array(r, (T, H), dtype)
+    w = wl.host_weight(r, H, dtype)
+    xd, wd = wl.to_torch(x, dtype, DEV), wl.to_torch(w, dtype, DEV)
+    whole = cache.rmsnorm(xd, wd, 1e-6)
+    sel = cache.last_selection()
+    assert (sel.variant, sel.launch[0].grid_x) == (S.RN_WIDE, 256)
+    parts = []
+    for lo in range(0, T, 256):
+        parts.append(cache.rmsnorm(xd[lo:lo + 256], wd, 1e-6))
+        sel = cache.last_selection()
+        assert (sel.variant, sel.launch[0].grid_x) == (S.RN_WIDE, min(256, T - lo))
+    torch.cuda.synchronize()
+    check("600 rows vs chunks", host(whole), host(torch.cat(parts)), dtype, exact=True)
+    check("600 rows vs oracle", host(whole), O.rmsnorm(x, w, 1e-6, dtype), dtype)
+
+
 def test_split_rows_reuse_their_scratch(tri, cache):
     """A split version's scratch is cleared by each call's last readers, so
     back-to-back calls of one version (different data, fewer rows within the
