@@ -770,7 +770,8 @@ def main():
         copy_src = torch.empty(1 << 29, dtype=torch.bfloat16, device=dev)
         copy_dst = torch.empty_like(copy_src)
         # long rows: bf16 [2048, 65536] and the same memory as [1024, 131072]
-        # (each row split over 4 / 8 workgroups that exchange partial sums),
+        # (residual rows and plain rows of 131072 split over 4 / 8 workgroups
+        # that exchange partial sums; plain rows of 65536 on 256 workgroups),
         # and plain rows of [2048, 57344] in the front of that memory (256
         # 1024-lane workgroups, each taking every 256th row)
         lx = torch.randn((2048, 65536), device=dev).to(db["x"].dtype)

@@ -57,6 +57,7 @@ RN_WIDE = 19               # 1024-work-item workgroups, a row each, 8 vectors pe
 WIDE_LANES = 1024
 WIDE_ROW_VECS = 8 * WIDE_LANES   # the longest row it holds (16-byte vectors)
 WIDE_PLAIN_VECS = 7 * WIDE_LANES  # plain rows up to here take it by policy
+WIDE_PLAIN_BUCKET = 9             # plain rows up to WIDE_ROW_VECS take it from here
 WIDE_GRID = 256                   # plain rows: at most this many workgroups, each
                                   # taking rows b, b + 256, ... (residual: one per row)
 RN_SPLIT = 20              # a row over S workgroups of 256, 8 vectors per work-item
@@ -185,6 +186,8 @@ def rn_role(dtype: int, H: int, flags: int, T: int, b: int,
     if nb <= 16:
         return RN_BLOCK[nb], T
     if not res and nvec <= WIDE_PLAIN_VECS:  # plain rows: 1024-lane workgroups
+        return RN_WIDE, wide_grid(T, res)
+    if not res and nvec <= WIDE_ROW_VECS and b >= WIDE_PLAIN_BUCKET:  # the same, past 256 rows
         return RN_WIDE, wide_grid(T, res)
     if split_fits(dtype, H, b):           # several workgroups per row
         return RN_SPLIT, T * split_slices(dtype, H)

@@ -37,6 +37,7 @@ constexpr int64_t kILimit = int64_t(1) << 31;
 constexpr uint64_t kSpanMax = uint64_t(1) << 47;   // bytes an operand's rows may span
 constexpr int64_t kWideRowVecs = 8 * int64_t(kWideLanes);   // longest RN_WIDE row (vectors)
 constexpr int64_t kWidePlainVecs = 7 * int64_t(kWideLanes);  // plain rows up to here: RN_WIDE
+constexpr uint32_t kWidePlainBucket = 9;  // longer plain rows (up to kWideRowVecs): RN_WIDE from here
 // RN_SPLIT: rows beyond 16 * 256 vectors, at most kSplitMaxSlices workgroups
 // per row; a version's scratch (kSplitHeaderWords + 2^bucket * (S + 1)
 // words) may take at most kSplitScratchWords (32 MiB), else the longer

@@ -70,17 +70,20 @@ bool split_fits(uint32_t dtype, int64_t H, uint32_t bucket) {
 // passes over memory. Beyond the split's limits a row of up to
 // kWideRowVecs vectors takes the 1024-work-item workgroup and longer rows
 // make two passes. Plain RMSNorm rows of 4097..kWidePlainVecs vectors take
-// the 1024-work-item workgroup at every bucket: its plain form keeps two
-// workgroups per CU and has no exchange to wait for, which the residual
-// form's early residual_out stores hide in the split. A sweep of both forms
+// the 1024-work-item workgroups at every bucket, and longer plain rows of up
+// to kWideRowVecs vectors from bucket kWidePlainBucket on (more than 256
+// rows, where its workgroups each take several rows and overlap one row's
+// loads with the previous row's stores): the plain form has no exchange to
+// wait for, which the residual form's early residual_out stores hide in the
+// split. Against the split at 8192 vectors (bf16 and f32, 256-4096 rows,
+// after a 1 GiB read flush and back to back) it took 0.84-0.98 of the
+// split's time, except bf16 rows at 2048 and 4096 back to back (1.02). An
+// earlier sweep of both forms
 // (bf16 and f32 rows of 4097, 5120, 6144, 7168 and 8192 vectors, 1-4096
 // rows, back to back and after a 1 GiB read flush) put the split ahead
 // only for rows of 8192 vectors (by up to 15 % at 1-64 rows, where four
-// workgroups per row pull it from HBM in parallel); with the threshold at
-// 7168 vectors the policy's form is within 10.3 % of the faster one at
-// every point (0.8 % on average), against 15 % with the 1024-lane form up to 8192
-// vectors and 25 % with the split for all of them. Unaligned or ragged rows
-// take the scalar kernel.
+// workgroups per row pull it from HBM in parallel). Unaligned or ragged
+// rows take the scalar kernel.
 Role rn_role(uint32_t dtype, int64_t H, unsigned flags, int64_t T, uint32_t bucket, bool res) {
   const int64_t v = vec_elems(dtype);
   if (!(flags & kAlign) || H % v) return {RN_SCALAR, uint32_t(T)};
@@ -89,6 +92,8 @@ Role rn_role(uint32_t dtype, int64_t H, unsigned flags, int64_t T, uint32_t buck
   const int64_t nb = next_pow2(cdiv(nvec, 256));
   if (nb <= 16) return {RN_BLOCK_1 + pow2_index(nb), uint32_t(T)};
   if (!res && nvec <= kWidePlainVecs) return {RN_WIDE, norm_grid(RN_WIDE, dtype, T, H, res)};
+  if (!res && nvec <= kWideRowVecs && bucket >= kWidePlainBucket)
+    return {RN_WIDE, norm_grid(RN_WIDE, dtype, T, H, res)};
   if (split_fits(dtype, H, bucket)) return {RN_SPLIT, uint32_t(T * split_slices(dtype, H))};
   if (nvec <= kWideRowVecs) return {RN_WIDE, norm_grid(RN_WIDE, dtype, T, H, res)};
   return {RN_LOOP, uint32_t(T)};

@@ -218,6 +218,7 @@ SELECTION_MUTANTS = {
     "plain_wide_rows_up_to_8192_vectors": (S, "WIDE_PLAIN_VECS", 8 * S.WIDE_LANES),
     "residual_rows_wide_instead_of_split": (S, "rn_role", _rn_role_residual_wide),
     "plain_wide_rows_one_workgroup_each": (S, "WIDE_GRID", 1 << 40),
+    "plain_8192_vector_rows_wide_one_bucket_early": (S, "WIDE_PLAIN_BUCKET", 8),
 }
 
 _name = os.environ.get("TRI_ORACLE_MUTANT")

@@ -171,7 +171,8 @@ def test_embedding_8192(tri, data):
 
 
 # ---- long rows: the benchmark's bf16 [2048, 65536] and the same memory as
-# [1024, 131072], each row split over 4 / 8 workgroups -------------------------------------------
+# [1024, 131072]: rows split over 4 / 8 workgroups, except plain rows of 65536
+# (256 workgroups of 1024, each taking every 256th row) -----------------------------------------
 @pytest.fixture(scope="module")
 def long_rows():
     g = torch.Generator(device=DEV)
@@ -199,7 +200,10 @@ def test_long_rows_all_rows(tri, long_rows, H, res):
         (y, ro), sel = run(tri, lambda c: c.residual_rmsnorm(x, r, w, CFG.eps))
     else:
         y, sel = run(tri, lambda c: c.rmsnorm(x, w, CFG.eps))
-    assert sel.variant == S.RN_SPLIT and sel.launch[0].grid_x == T * S_
+    if res or H > 65536:                                 # split rows
+        assert sel.variant == S.RN_SPLIT and sel.launch[0].grid_x == T * S_
+    else:                                                # 256 workgroups, 8 rows each
+        assert sel.variant == S.RN_WIDE and sel.launch[0].grid_x == 256
     wh = host(w)
     for a in range(0, T, 256):                           # 256 rows: 16-32 M elements
         b = slice(a, min(T, a + 256))

@@ -260,12 +260,14 @@ def test_split_rows_reuse_their_scratch(tri, cache):
 
 
 def test_generic_split_version_across_buckets(tri):
-    """One generic split version per form (plain and residual bf16 rows of
-    65536, 4 workgroups per row) serves calls of 1 to 700 rows, buckets 0
-    to 10, through one scratch sized for the top of its run; plain rows of
-    57344 (7168 vectors) take one generic 1024-lane version over every
-    bucket and their row class; every row of every call against the
-    oracle."""
+    """One generic split version of residual bf16 rows of 65536 (4
+    workgroups per row) serves calls of 1 to 700 rows, buckets 0 to 10,
+    through one scratch sized for the top of its run; plain rows of 65536
+    split up to 256 rows (buckets 0-8, one generic version) and take a
+    second generic version on 256 1024-lane workgroups beyond (the 700-row
+    call); plain rows of 57344 (7168 vectors) take one generic 1024-lane
+    version over every bucket and their row class; every row of every call
+    against the oracle."""
     r = rng(19)
     H = 65536
     w = wl.host_weight(r, H, nm.BF16)
@@ -284,7 +286,8 @@ def test_generic_split_version_across_buckets(tri):
             y3 = c.rmsnorm(xd[:, :57344], wd[:57344], 1e-6)
             sel3 = c.last_selection()
             torch.cuda.synchronize()
-            assert sel.variant == S.RN_SPLIT and sel.launch[0].grid_x == 4 * T
+            assert (sel.variant, sel.launch[0].grid_x) == (
+                (S.RN_SPLIT, 4 * T) if T <= 256 else (S.RN_WIDE, 256))
             assert sel2.variant == S.RN_SPLIT and sel2.launch[0].grid_x == 4 * T
             assert sel3.variant == S.RN_WIDE and sel3.launch[0].grid_x == min(T, 256)
             check(f"{step} y", host(y), O.rmsnorm(x, w, 1e-6, nm.BF16), nm.BF16)
@@ -294,11 +297,12 @@ def test_generic_split_version_across_buckets(tri):
             check(f"{step} residual y", host(y2), wy, nm.BF16)
             check(f"{step} res_out", host(ro), wh, nm.BF16, exact=True)
         st = c.stats()
-        assert st["n_versions"] == 3 and st["misses"] == 3      # plain, residual, plain 57344
+        # plain, residual, plain 57344 (first call); plain 700 rows (second)
+        assert st["n_versions"] == 4 and st["misses"] == 4
         guards = [(c.version_info(i).variant, c.version_info(i).b_lo, c.version_info(i).b_hi,
-                   c.version_info(i).h_lo, c.version_info(i).h_hi) for i in range(3)]
-        assert guards == [(S.RN_SPLIT, 0, 19, 0, 0), (S.RN_SPLIT, 0, 19, 0, 0),
-                          (S.RN_WIDE, 0, 22, 32776, 57344)]
+                   c.version_info(i).h_lo, c.version_info(i).h_hi) for i in range(4)]
+        assert guards == [(S.RN_SPLIT, 0, 8, 0, 0), (S.RN_SPLIT, 0, 19, 0, 0),
+                          (S.RN_WIDE, 0, 22, 32776, 57344), (S.RN_WIDE, 9, 22, 0, 0)]
     finally:
         torch.cuda.synchronize()
         c.close()

@@ -99,12 +99,16 @@ def test_plain_wide_rows_get_every_bucket_and_their_class(call, h):
     assert S.candidates(S.make_key(call))[0].kernels == (S.RN_WIDE,)
 
 
-def test_plain_rows_of_7169_to_8192_vectors_split_like_residual_rows():
-    # bf16 65536 = 8192 vectors: S = 4, the run ends at bucket 19 (as for
-    # residual rows), and the row length is exact
+def test_plain_rows_of_7169_to_8192_vectors_split_up_to_256_rows():
+    # bf16 65536 = 8192 vectors: split (S = 4) up to bucket 8, where the
+    # run ends; from bucket 9 the 1024-lane form to the last bucket; the
+    # row length is exact either way
     g = S.generic_guard(S.make_key(rn_call(BF, 3, 65536)))
-    assert (g.b_lo, g.b_hi, g.h_lo) == (0, 19, 0)
+    assert (g.b_lo, g.b_hi, g.h_lo) == (0, 8, 0)
     assert S.candidates(S.make_key(rn_call(BF, 3, 65536)))[0].kernels == (S.RN_SPLIT,)
+    g = S.generic_guard(S.make_key(rn_call(BF, 700, 65536)))
+    assert (g.b_lo, g.b_hi, g.h_lo) == (9, 22, 0)
+    assert S.candidates(S.make_key(rn_call(BF, 700, 65536)))[0].kernels == (S.RN_WIDE,)
 
 
 def test_a_tuned_split_choice_clamps_the_run():

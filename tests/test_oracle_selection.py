@@ -156,10 +156,12 @@ def test_split_rows_need_their_scratch_to_fit(dtype, H, b, want):
     # plain rows of 4097..7168 vectors: the 1024-lane workgroup at any bucket
     (BF, 32776, 0, S.RN_WIDE), (BF, 57344, 3, S.RN_WIDE), (F, 28672, 22, S.RN_WIDE),
     (F, 16388, 19, S.RN_WIDE),
-    # 7169..8192 vectors: split like residual rows (S = 4), the 1024-lane
-    # workgroup where the scratch does not fit
-    (BF, 57352, 3, S.RN_SPLIT), (BF, 65536, 19, S.RN_SPLIT), (BF, 65536, 20, S.RN_WIDE),
-    (F, 32768, 3, S.RN_SPLIT),
+    # 7169..8192 vectors: split like residual rows (S = 4) up to bucket 8
+    # (256 rows), the 1024-lane workgroups from bucket 9 on
+    (BF, 57352, 3, S.RN_SPLIT), (BF, 65536, 8, S.RN_SPLIT), (BF, 65536, 9, S.RN_WIDE),
+    (BF, 65536, 19, S.RN_WIDE), (BF, 65536, 20, S.RN_WIDE),
+    (F, 32768, 3, S.RN_SPLIT), (F, 32768, 8, S.RN_SPLIT), (F, 32768, 9, S.RN_WIDE),
+    (BF, 57352, 9, S.RN_WIDE),
     # 8193 vectors and more: split while the scratch fits (S = 5: 8 + 6 * 2^b
     # <= 2^22 up to b = 19), then two passes
     (BF, 65544, 19, S.RN_SPLIT), (BF, 65544, 20, S.RN_LOOP),
@@ -183,9 +185,9 @@ def test_plain_wide_rows_grid_by_hand(dtype, H, T, want):
 
 
 def test_wide_rows_grid_of_candidates_by_hand():
-    # bf16 rows of 65,536 (8192 vectors) at 2048 rows split by policy; the
-    # tuning candidate on the 1024-lane form launches 256 workgroups for
-    # plain rows and one per row for residual rows
+    # bf16 rows of 65,536 (8192 vectors) at 2048 rows: plain rows take the
+    # 1024-lane form by policy (256 workgroups); residual rows split by
+    # policy and have it as a tuning candidate, one workgroup per row
     for call, want in ((rn_call(BF, 2048, 65536), 256), (res_call(BF, 2048, 65536), 2048)):
         key = S.make_key(call)
         wide = [c for c in S.candidates(key) if c.kernels == (S.RN_WIDE,)]
