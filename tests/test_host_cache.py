@@ -826,7 +826,7 @@ def _last_launch(lib, nbytes=512, size=None):
 def test_long_rows_launch_split_wide_and_loop_forms(lib, fresh):
     """Residual rows beyond 4096 vectors are split over S = ceil(vectors /
     2048) workgroups of 256 (standalone, and as the norm launch of a
-    three-launch chain), plain rows beyond 7168 vectors too; plain rows of
+    three-launch chain), plain rows beyond 7168 vectors too (up to 256 rows); plain rows of
     4097..7168 vectors take one 1024-work-item workgroup, and so do rows of
     up to 8192 vectors where the split's scratch for the key's bucket would
     be too large; longer rows make two passes. Launches and records match
@@ -848,6 +848,29 @@ def test_long_rows_launch_split_wide_and_loop_forms(lib, fresh):
         assert got == want and [g[0] for g in got] == kinds, (c.op, c.H, got)
         assert [g[2] for g in got] == [1024 if k == S.RN_WIDE else 256 for k in kinds]
         assert [tuple(l) for l in c_record(lib, cache)[6][:len(want)]] == want
+
+
+@pytest.mark.parametrize("dtype,H", [(BF, 57344), (BF, 65536), (F, 32768), (BF, 32776)])
+def test_plain_wide_rows_launch_at_most_256_workgroups(lib, fresh, dtype, H):
+    """Plain rows of 4097..8192 vectors on the 1024-work-item form launch
+    one workgroup per row up to 256 rows and 256 workgroups beyond (each
+    taking every 256th row); rows of 7169..8192 vectors split up to 256
+    rows. Launch and record against the model's plan at the edges."""
+    cache = fresh(flags=S.FLAG_AUTO_INSTALL)
+    for T in (1, 255, 256, 257, 700, 2048, 4096):
+        c = rn_call(dtype, T, H)
+        n0 = lib.trifake_launch_count()
+        assert c_call(lib, cache, c) == 0
+        got = [(l[0], l[3], l[4]) for l in (_launch_at(lib, i)
+                                             for i in range(n0, lib.trifake_launch_count()))]
+        want = [tuple(l) for l in S.plan(S.make_key(c), T)[2]]
+        assert got == want, (H, T, got, want)
+        if T > 256:
+            assert got == [(S.RN_WIDE, 256, 1024)]
+        elif H // (16 // S.elem_size(dtype)) <= S.WIDE_PLAIN_VECS:
+            assert got == [(S.RN_WIDE, T, 1024)]
+        else:
+            assert got[0][0] == S.RN_SPLIT
 
 
 def test_split_rows_carry_the_version_scratch(lib, fresh):
